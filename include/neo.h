@@ -1,0 +1,249 @@
+/*
+ * neo.h -- C-ABI of libneo: blocked-layout (NCHW[x]c) CNN inference on
+ * MI355X (gfx950).
+ *
+ * The operations follow the problem statement of "Optimizing CNN Model
+ * Inference on CPUs" (NeoCPU):
+ *   - the convolution of Section 3.1.1 and its blocked layouts NCHW[x]c for
+ *     feature maps and KCRS[x]c[y]k for filters (Algorithm 1's INPUT/OUTPUT);
+ *   - the LayoutTransform node of Section 3.2;
+ *   - the graph-level plan of Section 3.2, which keeps every convolution in
+ *     NCHW[x]c with one constant x and inserts layout transforms only before
+ *     the first blocked operation and before layout-dependent operations;
+ *   - the memory-bound operations the paper fuses into the convolution (bias,
+ *     batch norm folded into the weights, residual add, ReLU; Sections 2.2
+ *     and 3).
+ *
+ * Conventions for every call:
+ *   - Pointers documented "device" are HIP device pointers owned by the
+ *     caller; the library never frees them.  They must be 16-byte aligned.
+ *   - Pointers documented "host" are read during the call only.
+ *   - Feature maps in NCHW16c are [N][ceil(C/16)][H][W][16] float32 with the
+ *     padded channel lanes (c >= C) holding +0.0.  Plain NCHW is
+ *     [N][C][H][W].  Filters in KCRS[16]c[16]k are
+ *     [ceil(K/16)][ceil(C/16)][R][S][16 (c)][16 (k)], output channel
+ *     innermost, zero padded.
+ *   - Every device call is asynchronous on `stream` (a hipStream_t; NULL is
+ *     the null stream) and never synchronizes.  A kernel fault surfaces at
+ *     the caller's next synchronization.
+ *   - Return value: NEO_OK (0) or a negative NEO_ERR_* code; on error nothing
+ *     was launched and neo_last_error() holds a message.  No exception or
+ *     abort crosses the ABI.
+ *   - Tensors are limited to 2^31 - 1 elements.
+ */
+#ifndef NEO_H
+#define NEO_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum neo_status {
+    NEO_OK = 0,
+    NEO_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad enum */
+    NEO_ERR_SHAPE = -2,       /* sizes inconsistent (e.g. empty output)   */
+    NEO_ERR_ALIGN = -3,       /* device pointer not 16-byte aligned        */
+    NEO_ERR_UNSUPPORTED = -4, /* valid but not implemented (e.g. groups)   */
+    NEO_ERR_HIP = -5,         /* HIP runtime error; message has its text   */
+    NEO_ERR_OOM = -6,         /* device allocation failed                  */
+    NEO_ERR_STATE = -7        /* object destroyed, or wrong kind of plan   */
+};
+
+typedef void* neo_stream_t; /* hipStream_t */
+
+enum neo_act { NEO_ACT_NONE = 0, NEO_ACT_RELU = 1 };
+
+/* Channel block of the blocked layout used by every kernel: 16 fp32 lanes =
+ * 64 bytes per pixel block, so two neighbouring pixels fill one 128-byte line. */
+#define NEO_BLOCK 16
+
+/* Epilogue fused into the convolution (Sections 2.2 and 3: bias, folded batch
+ * norm, element-wise add and activation are fused into the CONV):
+ *   y = act(conv + bias[k] + residual)
+ * `residual`: NULL, or a device NCHW16c tensor with the output's shape
+ * [N][ceil(K/16)][OH][OW][16] (contiguous, no channel view). */
+typedef struct neo_epilogue {
+    int act;               /* enum neo_act */
+    const float* residual; /* device, or NULL */
+} neo_epilogue;
+
+/*
+ * Convolution over NCHW16c (Section 3.1.1, Algorithm 1):
+ *   y[n][k][oh][ow] = act( sum_{c<C, r<R, s<S}
+ *        x[n][c][oh*stride_h - pad_h + r][ow*stride_w - pad_w + s] * w[k][c][r][s]
+ *        + bias[k] + residual[n][k][oh][ow] )
+ * with x taken as zero outside the input (cross-correlation, zero padding),
+ * OH = (H + 2 pad_h - R) / stride_h + 1 and OW likewise (floor).
+ *
+ *   x        device NCHW16c [N][ceil(C/16)][H][W][16]
+ *   w_packed device KCRS[16]c[16]k, as written by neo_pack_filter(.., 16, 16, ..)
+ *   bias     device [ceil(K/16)*16] (zero padded) or NULL
+ *   ep       host, may be NULL (= no activation, no residual)
+ *   y        device NCHW16c with `y_cblk_total` channel blocks; the K output
+ *            channels are written to blocks [y_cblk_offset, y_cblk_offset +
+ *            ceil(K/16)), so a producer can write straight into a slice of a
+ *            channel concatenation.  Pass 0 and ceil(K/16) for a plain output.
+ * Dilation and groups are 1.  Returns NEO_ERR_SHAPE if OH or OW < 1.
+ * The padded output lanes (k >= K) are written as +0.0 (ReLU keeps them 0).
+ */
+int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* w_packed, int K,
+                       int R, int S, const float* bias, int stride_h, int stride_w, int pad_h,
+                       int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
+                       int y_cblk_total, neo_stream_t stream);
+
+/*
+ * LayoutTransform node (Section 3.2): NCHW <-> NCHW[x]c, or NCHW[x]c ->
+ * NCHW[x']c.  A block of 0 means plain NCHW; a block x > 0 means
+ * [N][ceil(C/x)][H][W][x] with zero-filled padding lanes.  Blocks: 0, 1, 2,
+ * 4, 8, 16, 32, 64.  A pure permutation: bit-exact.  src and dst are device
+ * buffers that must not overlap.
+ */
+int neo_layout_transform(const float* src, int src_block, float* dst, int dst_block, int N,
+                         int C, int H, int W, neo_stream_t stream);
+
+/*
+ * Filter pre-transformation KCRS -> KCRS[ic_bn]c[oc_bn]k (Section 3.1.1, done
+ * once at plan time as Section 3.2 describes for model parameters):
+ *   w_packed[k/oc][c/ic][r][s][c%ic][k%oc] = w[k][c][r][s], zero padded.
+ * w_kcrs and w_packed are device buffers; ic_bn, oc_bn in {1,2,4,8,16,32,64}.
+ * Bit-exact.  neo_conv2d_blocked consumes ic_bn = oc_bn = 16.
+ */
+int neo_pack_filter(const float* w_kcrs, int K, int C, int R, int S, int ic_bn, int oc_bn,
+                    float* w_packed, neo_stream_t stream);
+
+/*
+ * Batch-norm folding (inference simplification inherited by the paper,
+ * Section 3): with scale[k] = gamma[k] / sqrt(var[k] + eps),
+ *   w_out[k][c][r][s] = w[k][c][r][s] * scale[k]
+ *   bias_out[k]       = (bias[k] - mean[k]) * scale[k] + beta[k]
+ * computed in double and rounded once to float.  All pointers are host;
+ * `bias` may be NULL (taken as 0).  w_out may equal w.  Synchronous, CPU only.
+ */
+int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,
+                const float* mean, const float* var, float eps, int K, int C, int R, int S,
+                float* w_out, float* bias_out);
+
+/*
+ * Layout-tolerant pooling on NCHW16c (Section 3.2 lists pooling among the
+ * operations that handle the blocked layout):
+ *   max: y = max over in-bounds taps of the R x S window (padding = -inf)
+ *   avg: y = mean over the in-bounds taps (padding excluded from the count)
+ * OH = (H + 2 pad_h - R) / stride_h + 1 (floor); pad must be < window.
+ * x, y device NCHW16c; y has `y_cblk_total` blocks and receives blocks
+ * [y_cblk_offset, y_cblk_offset + ceil(C/16)) (concat slice, as for conv).
+ */
+int neo_maxpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S,
+                          int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                          int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+int neo_avgpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S,
+                          int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                          int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+
+/* Global average pool on NCHW16c: y[n][c] = mean over H*W of x[n][c];
+ * x device NCHW16c, y device NCHW16c with H = W = 1. */
+int neo_global_avgpool_blocked(const float* x, int N, int C, int H, int W, float* y,
+                               neo_stream_t stream);
+
+/*
+ * Dense (fully connected) layer after Flatten, a layout-dependent operation
+ * that consumes the default layout (Section 3.2):
+ *   y[n][o] = act( sum_i w[o][i] * x[n][i] + bias[o] )
+ * x device [N][IN], w device [OUT][IN] (row-major), bias device [OUT] or
+ * NULL, y device [N][OUT].
+ */
+int neo_dense(const float* x, int N, int IN, const float* w, int OUT, const float* bias,
+              int act, float* y, neo_stream_t stream);
+
+/* ------------------------------------------------------------------------------------ */
+/* Graph plan (Section 3.2: layout-transformation elimination)                           */
+/* ------------------------------------------------------------------------------------ */
+enum neo_op {
+    NEO_OP_INPUT = 0,   /* the network input, plain NCHW (N, C, H, W of plan_create) */
+    NEO_OP_CONV = 1,    /* conv [+ bias] [+ batch norm] [+ residual] [+ act]          */
+    NEO_OP_MAXPOOL = 2, /* R x S window, stride, pad                                  */
+    NEO_OP_AVGPOOL = 3, /* in-bounds-count average                                    */
+    NEO_OP_GAP = 4,     /* global average pool                                        */
+    NEO_OP_CONCAT = 5,  /* channel concatenation of inputs[0..n_inputs)               */
+    NEO_OP_FLATTEN = 6, /* (N, C, H, W) -> (N, C*H*W), c-major; layout dependent      */
+    NEO_OP_DENSE = 7,   /* y = act(W x + b), W [K][in]                                */
+    NEO_OP_OUTPUT = 8   /* the network output (one input), returned in plain layout   */
+};
+
+/* One operation of a network description.  All pointers are host and are
+ * only read during neo_plan_create (the plan keeps its own device copies). */
+typedef struct neo_node {
+    int op;              /* enum neo_op */
+    int n_inputs;
+    const int* inputs;   /* ids (indices into the node array) of the inputs */
+    int K, R, S;         /* conv: out channels, window; dense: K = out features; pools: R, S */
+    int stride_h, stride_w, pad_h, pad_w;
+    int act;             /* conv, dense: enum neo_act */
+    int residual;        /* conv: id of a node added before the activation, or -1 */
+    const float* w;      /* conv: KCRS [K][C][R][S]; dense: [K][in] */
+    const float* bias;   /* [K] or NULL */
+    const float* bn_gamma, *bn_beta, *bn_mean, *bn_var; /* [K] each, or all NULL */
+    float bn_eps;
+} neo_node;
+
+typedef struct neo_plan neo_plan;
+
+enum neo_plan_flags {
+    /* Build the plan on the host only: layouts, transforms, folded and packed
+     * parameters and buffer offsets, but no device memory.  Such a plan can be
+     * described and its parameters read back, not run. */
+    NEO_PLAN_HOST_ONLY = 1,
+    /* Transform around every blocked operation instead of keeping the blocked
+     * layout between them (the baseline the paper's elimination improves on).
+     * Results are bit-identical to the default plan. */
+    NEO_PLAN_NAIVE = 2
+};
+
+/*
+ * Build a plan from `n_nodes` nodes (any order that refers to existing ids;
+ * they are sorted topologically) for an input of shape (N, C, H, W):
+ * infer each value's layout from the operation categories of Section 3.2
+ * (convolution and pooling run in NCHW[block]c, concatenation follows its
+ * inputs, flatten/dense/output need the default layout), insert
+ * LayoutTransform steps only where a consumer needs another layout, fold
+ * batch norm, pre-pack the filters, and allocate device buffers (concat
+ * inputs are written in place into channel slices of the concat buffer).
+ * `block` must be 16.  On success *out owns all device memory of the plan.
+ */
+int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
+                    unsigned flags, neo_plan** out);
+
+/* Write a JSON description (values with shape and layout, inserted
+ * transforms, steps, buffer bytes) into buf (NUL-terminated, truncated to
+ * len).  Returns the full length needed (excluding the NUL), or an error. */
+int neo_plan_describe(const neo_plan* plan, char* buf, size_t len);
+
+/* Output shape of the network: dims[0..3] = N, C, H, W (H = W = 1 after a
+ * flatten or dense).  Returns NEO_OK. */
+int neo_plan_output_shape(const neo_plan* plan, int* dims);
+
+/* Copy a conv node's prepared parameters to host memory: the folded, packed
+ * KCRS[16]c[16]k filter (ceil(K/16)*ceil(C/16)*R*S*256 floats) and the folded
+ * bias (ceil(K/16)*16 floats).  Either pointer may be NULL.  Synchronous. */
+int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, float* bias);
+
+/*
+ * Run the plan: x_nchw device plain NCHW input of the plan's input shape,
+ * y_out device plain output of neo_plan_output_shape.  Asynchronous on
+ * `stream`; no host synchronization inside.  Not reentrant for one plan
+ * (intermediate buffers belong to the plan).
+ */
+int neo_run_graph(neo_plan* plan, const float* x_nchw, float* y_out, neo_stream_t stream);
+
+/* Free the plan and its device memory (synchronizes the device first).
+ * NULL is ignored.  Later use of the handle returns NEO_ERR_STATE. */
+void neo_plan_destroy(neo_plan* plan);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* neo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NEO_H */

@@ -1,0 +1,233 @@
+// C-ABI entry points of libneo: argument validation, then the launchers.
+#include <cmath>
+#include <cstdio>
+#include <limits>
+#include <string>
+
+#include "neo_internal.h"
+
+namespace neo {
+
+static thread_local std::string g_err;
+
+void set_error(const std::string& msg) { g_err = msg; }
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    g_err = std::string(what) + ": " + hipGetErrorString(e);
+    return NEO_ERR_HIP;
+}
+
+void fold_bn_host(const float* w, const float* bias, const float* gamma, const float* beta,
+                  const float* mean, const float* var, float eps, int K, int C, int R, int S,
+                  float* w_out, float* bias_out) {
+    const long per_k = (long)C * R * S;
+    for (int k = 0; k < K; ++k) {
+        const double scale = (double)gamma[k] / std::sqrt((double)var[k] + (double)eps);
+        for (long i = 0; i < per_k; ++i)
+            w_out[k * per_k + i] = (float)((double)w[k * per_k + i] * scale);
+        const double b = bias ? (double)bias[k] : 0.0;
+        bias_out[k] = (float)((b - (double)mean[k]) * scale + (double)beta[k]);
+    }
+}
+
+void pack_filter_host(const float* w, int K, int C, int R, int S, int ib, int ob, float* out) {
+    const int KB = cdiv(K, ob), CB = cdiv(C, ib);
+    long t = 0;
+    for (int kb = 0; kb < KB; ++kb)
+        for (int cb = 0; cb < CB; ++cb)
+            for (int r = 0; r < R; ++r)
+                for (int s = 0; s < S; ++s)
+                    for (int ci = 0; ci < ib; ++ci)
+                        for (int ko = 0; ko < ob; ++ko, ++t) {
+                            const int k = kb * ob + ko, c = cb * ib + ci;
+                            out[t] = (k < K && c < C) ? w[(((long)k * C + c) * R + r) * S + s] : 0.f;
+                        }
+}
+
+}  // namespace neo
+
+using namespace neo;
+
+namespace {
+
+constexpr long kMaxElems = std::numeric_limits<int>::max();
+
+bool valid_block(int b) {
+    return b == 0 || b == 1 || b == 2 || b == 4 || b == 8 || b == 16 || b == 32 || b == 64;
+}
+
+long blocked_elems(long N, long C, long H, long W, int blk) {
+    return blk ? N * ((C + blk - 1) / blk) * blk * H * W : N * C * H * W;
+}
+
+#define CHECK_PTR(p)                                                                        \
+    do {                                                                                    \
+        if (!(p)) return fail(NEO_ERR_INVALID_ARG, std::string(__func__) + ": " #p " is NULL"); \
+        if (!aligned16(p))                                                                  \
+            return fail(NEO_ERR_ALIGN, std::string(__func__) + ": " #p " not 16-byte aligned"); \
+    } while (0)
+
+#define CHECK_POS(v)                                                                       \
+    do {                                                                                   \
+        if ((v) <= 0)                                                                      \
+            return fail(NEO_ERR_INVALID_ARG, std::string(__func__) + ": " #v " must be > 0"); \
+    } while (0)
+
+#define CHECK_SIZE(e)                                                                       \
+    do {                                                                                    \
+        if ((e) > kMaxElems)                                                                \
+            return fail(NEO_ERR_UNSUPPORTED,                                                \
+                        std::string(__func__) + ": tensor exceeds 2^31-1 elements");       \
+    } while (0)
+
+int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
+
+}  // namespace
+
+extern "C" {
+
+const char* neo_last_error(void) { return g_err.c_str(); }
+
+int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* w_packed, int K,
+                       int R, int S, const float* bias, int stride_h, int stride_w, int pad_h,
+                       int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
+                       int y_cblk_total, neo_stream_t stream) {
+    CHECK_PTR(x);
+    CHECK_PTR(w_packed);
+    CHECK_PTR(y);
+    if (bias) CHECK_PTR(bias);
+    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    CHECK_POS(K); CHECK_POS(R); CHECK_POS(S);
+    CHECK_POS(stride_h); CHECK_POS(stride_w);
+    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_blocked: negative pad");
+    const int act = ep ? ep->act : NEO_ACT_NONE;
+    if (act != NEO_ACT_NONE && act != NEO_ACT_RELU)
+        return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_blocked: unknown activation");
+    const float* res = ep ? ep->residual : nullptr;
+    if (res) CHECK_PTR(res);
+    const int OH = out_dim(H, R, stride_h, pad_h), OW = out_dim(W, S, stride_w, pad_w);
+    if (H + 2 * pad_h < R || W + 2 * pad_w < S || OH < 1 || OW < 1)
+        return fail(NEO_ERR_SHAPE, "neo_conv2d_blocked: empty output (window larger than padded input)");
+    const int KB = cdiv(K, 16);
+    if (y_cblk_offset < 0 || y_cblk_total < KB || y_cblk_offset + KB > y_cblk_total)
+        return fail(NEO_ERR_SHAPE, "neo_conv2d_blocked: output channel-block view out of range");
+    CHECK_SIZE(blocked_elems(N, C, H, W, 16));
+    CHECK_SIZE((long)N * y_cblk_total * 16 * OH * OW);
+    CHECK_SIZE((long)KB * 16 * cdiv(C, 16) * 16 * R * S);
+    ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
+                y_cblk_offset, y_cblk_total, act};
+    hipError_t e = launch_conv2d(s, x, w_packed, bias, res, y, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_blocked launch");
+}
+
+int neo_layout_transform(const float* src, int src_block, float* dst, int dst_block, int N,
+                         int C, int H, int W, neo_stream_t stream) {
+    if (!src || !dst) return fail(NEO_ERR_INVALID_ARG, "neo_layout_transform: NULL buffer");
+    if (!valid_block(src_block) || !valid_block(dst_block))
+        return fail(NEO_ERR_INVALID_ARG, "neo_layout_transform: block must be 0,1,2,4,8,16,32,64");
+    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    if (((src_block == 16) || (dst_block == 16)) && (!aligned16(src) || !aligned16(dst)))
+        return fail(NEO_ERR_ALIGN, "neo_layout_transform: buffers not 16-byte aligned");
+    CHECK_SIZE(blocked_elems(N, C, H, W, src_block));
+    CHECK_SIZE(blocked_elems(N, C, H, W, dst_block));
+    const long sb = blocked_elems(N, C, H, W, src_block) * 4, db = blocked_elems(N, C, H, W, dst_block) * 4;
+    const char* s0 = (const char*)src;
+    const char* d0 = (const char*)dst;
+    if (s0 < d0 + db && d0 < s0 + sb)
+        return fail(NEO_ERR_INVALID_ARG, "neo_layout_transform: src and dst overlap");
+    hipError_t e = launch_layout_transform(src, src_block, dst, dst_block, N, C, H, W, 0,
+                                           dst_block ? cdiv(C, dst_block) : C, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_layout_transform launch");
+}
+
+int neo_pack_filter(const float* w_kcrs, int K, int C, int R, int S, int ic_bn, int oc_bn,
+                    float* w_packed, neo_stream_t stream) {
+    if (!w_kcrs || !w_packed) return fail(NEO_ERR_INVALID_ARG, "neo_pack_filter: NULL buffer");
+    CHECK_POS(K); CHECK_POS(C); CHECK_POS(R); CHECK_POS(S);
+    if (!valid_block(ic_bn) || !valid_block(oc_bn) || ic_bn == 0 || oc_bn == 0)
+        return fail(NEO_ERR_INVALID_ARG, "neo_pack_filter: ic_bn/oc_bn must be 1,2,4,8,16,32,64");
+    CHECK_SIZE((long)cdiv(K, oc_bn) * oc_bn * cdiv(C, ic_bn) * ic_bn * R * S);
+    hipError_t e = launch_pack_filter(w_kcrs, K, C, R, S, ic_bn, oc_bn, w_packed, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_pack_filter launch");
+}
+
+int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,
+                const float* mean, const float* var, float eps, int K, int C, int R, int S,
+                float* w_out, float* bias_out) {
+    if (!w || !gamma || !beta || !mean || !var || !w_out || !bias_out)
+        return fail(NEO_ERR_INVALID_ARG, "neo_fold_bn: NULL pointer");
+    CHECK_POS(K); CHECK_POS(C); CHECK_POS(R); CHECK_POS(S);
+    if (!(eps >= 0.f)) return fail(NEO_ERR_INVALID_ARG, "neo_fold_bn: eps must be >= 0");
+    for (int k = 0; k < K; ++k)
+        if (!((double)var[k] + (double)eps > 0.0))
+            return fail(NEO_ERR_INVALID_ARG, "neo_fold_bn: var + eps must be > 0");
+    fold_bn_host(w, bias, gamma, beta, mean, var, eps, K, C, R, S, w_out, bias_out);
+    return NEO_OK;
+}
+
+static int pool_common(const char* fn, bool is_max, const float* x, int N, int C, int H, int W,
+                       int R, int S, int sh, int sw, int ph, int pw, float* y, int y_off,
+                       int y_tot, neo_stream_t stream) {
+    if (!x || !y) return fail(NEO_ERR_INVALID_ARG, std::string(fn) + ": NULL buffer");
+    if (!aligned16(x) || !aligned16(y)) return fail(NEO_ERR_ALIGN, std::string(fn) + ": unaligned buffer");
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || R <= 0 || S <= 0 || sh <= 0 || sw <= 0 || ph < 0 ||
+        pw < 0)
+        return fail(NEO_ERR_INVALID_ARG, std::string(fn) + ": non-positive size");
+    if (ph >= R || pw >= S) return fail(NEO_ERR_INVALID_ARG, std::string(fn) + ": pad must be < window");
+    const int OH = out_dim(H, R, sh, ph), OW = out_dim(W, S, sw, pw);
+    if (H + 2 * ph < R || W + 2 * pw < S || OH < 1 || OW < 1)
+        return fail(NEO_ERR_SHAPE, std::string(fn) + ": empty output");
+    const int CB = cdiv(C, 16);
+    if (y_off < 0 || y_off + CB > y_tot)
+        return fail(NEO_ERR_SHAPE, std::string(fn) + ": output channel-block view out of range");
+    if (blocked_elems(N, C, H, W, 16) > kMaxElems || (long)N * y_tot * 16 * OH * OW > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, std::string(fn) + ": tensor exceeds 2^31-1 elements");
+    PoolShape s{N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot};
+    hipError_t e = is_max ? launch_maxpool(s, x, y, (hipStream_t)stream)
+                          : launch_avgpool(s, x, y, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, fn);
+}
+
+int neo_maxpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S, int stride_h,
+                          int stride_w, int pad_h, int pad_w, float* y, int y_cblk_offset,
+                          int y_cblk_total, neo_stream_t stream) {
+    return pool_common("neo_maxpool2d_blocked", true, x, N, C, H, W, R, S, stride_h, stride_w,
+                       pad_h, pad_w, y, y_cblk_offset, y_cblk_total, stream);
+}
+
+int neo_avgpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S, int stride_h,
+                          int stride_w, int pad_h, int pad_w, float* y, int y_cblk_offset,
+                          int y_cblk_total, neo_stream_t stream) {
+    return pool_common("neo_avgpool2d_blocked", false, x, N, C, H, W, R, S, stride_h, stride_w,
+                       pad_h, pad_w, y, y_cblk_offset, y_cblk_total, stream);
+}
+
+int neo_global_avgpool_blocked(const float* x, int N, int C, int H, int W, float* y,
+                               neo_stream_t stream) {
+    CHECK_PTR(x);
+    CHECK_PTR(y);
+    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    CHECK_SIZE(blocked_elems(N, C, H, W, 16));
+    hipError_t e = launch_gap(x, N, C, H, W, y, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_global_avgpool_blocked launch");
+}
+
+int neo_dense(const float* x, int N, int IN, const float* w, int OUT, const float* bias, int act,
+              float* y, neo_stream_t stream) {
+    if (!x || !w || !y) return fail(NEO_ERR_INVALID_ARG, "neo_dense: NULL buffer");
+    CHECK_POS(N); CHECK_POS(IN); CHECK_POS(OUT);
+    if (act != NEO_ACT_NONE && act != NEO_ACT_RELU)
+        return fail(NEO_ERR_INVALID_ARG, "neo_dense: unknown activation");
+    CHECK_SIZE((long)N * IN);
+    CHECK_SIZE((long)OUT * IN);
+    CHECK_SIZE((long)N * OUT);
+    hipError_t e = launch_dense(x, N, IN, w, OUT, bias, act, y, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_dense launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+// Internal declarations of libneo: kernel launchers (no validation; the ABI
+// layer and the planner validate first) and the error helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/neo.h"
+
+namespace neo {
+
+// ---- errors -------------------------------------------------------------------------
+void set_error(const std::string& msg);
+int fail(int code, const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// ---- convolution ----------------------------------------------------------------------
+struct ConvShape {
+    int N, C, H, W;      // input (C real channels; CB = ceil(C/16) blocks)
+    int K, R, S;         // filter
+    int sh, sw, ph, pw;  // stride, pad
+    int OH, OW;
+    int y_off, y_tot;    // output channel-block view
+    int act;
+};
+
+// Launch the blocked convolution.  x: NCHW16c, w: KCRS[16]c[16]k, bias:
+// [KB*16] or null, res: NCHW16c [N][KB][OH][OW][16] or null, y: NCHW16c view.
+hipError_t launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias,
+                         const float* res, float* y, hipStream_t st);
+
+// ---- layout ---------------------------------------------------------------------------
+// dst_off / dst_tot: destination channel view in destination units (channels
+// for the default layout, blocks for a blocked one), so a transform can write
+// into a slice of a concatenation buffer.  Pass 0 and the full extent
+// (C, or ceil(C/db)) for a plain destination.
+hipError_t launch_layout_transform(const float* src, int sb, float* dst, int db, int N, int C,
+                                   int H, int W, int dst_off, int dst_tot, hipStream_t st);
+hipError_t launch_pack_filter(const float* w, int K, int C, int R, int S, int ib, int ob,
+                              float* out, hipStream_t st);
+
+// ---- pools ----------------------------------------------------------------------------
+struct PoolShape {
+    int N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot;
+};
+hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
+hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
+hipError_t launch_gap(const float* x, int N, int C, int H, int W, float* y, hipStream_t st);
+
+// ---- dense ----------------------------------------------------------------------------
+hipError_t launch_dense(const float* x, int N, int IN, const float* w, int OUT,
+                        const float* bias, int act, float* y, hipStream_t st);
+
+// ---- host helpers -----------------------------------------------------------------------
+void fold_bn_host(const float* w, const float* bias, const float* gamma, const float* beta,
+                  const float* mean, const float* var, float eps, int K, int C, int R, int S,
+                  float* w_out, float* bias_out);
+void pack_filter_host(const float* w, int K, int C, int R, int S, int ib, int ob, float* out);
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace neo

@@ -1,0 +1,749 @@
+// Graph plan and runtime: layout-transformation elimination (Section 3.2).
+//
+// The planner walks the network in topological order and infers the layout of
+// every value from the operation categories of Section 3.2:
+//   - layout tolerant (convolution, max/avg pooling, global average pooling):
+//     run in NCHW16c, one constant block for every convolution;
+//   - layout oblivious (concatenation): follows its inputs (NCHW16c when every
+//     input has a whole number of 16-channel blocks, otherwise it needs the
+//     default layout);
+//   - layout dependent (flatten, dense, the network output): default layout.
+// A LayoutTransform step is inserted only where a consumer needs a layout the
+// value does not have yet (once per value and layout), so a CNN gets one
+// transform at its input and one before flatten.  Parameters are prepared once
+// (Section 3.2: model parameters are pre-transformed at compile time): batch
+// norm folded, filters packed to KCRS[16]c[16]k.  Concatenation costs no
+// step: its producers write straight into channel slices of its buffer.
+#include <algorithm>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <queue>
+#include <set>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "neo_internal.h"
+
+using namespace neo;
+
+namespace {
+
+enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY };
+
+struct Val {
+    int N = 0, C = 0, H = 0, W = 0;
+    int layout = 0;     // 0 = NCHW, 16 = NCHW16c
+    int node = -1;      // node whose result this is (a version of it)
+    int alias_of = -1;  // shares the storage of this value (identity transform, flatten)
+    int buf = -1;       // root buffer, or kExtIn
+    int c_off = 0;      // view offset in the root buffer (blocks if blocked, else channels)
+    int c_tot = 0;      // channel extent of the root buffer (same unit as c_off)
+    bool view = false;  // written into a slice of a concat buffer
+    int consumers = 0;
+};
+
+constexpr int kExtIn = -2;
+
+struct Step {
+    int kind;
+    int node;         // originating node (transforms: the consumer that needed it)
+    int in = -1, out = -1, res = -1;
+    ConvShape cs{};
+    PoolShape ps{};
+    long w_off = -1, b_off = -1;
+    int src_block = 0, dst_block = 0;
+    int dense_in = 0, dense_out = 0, act = 0;
+};
+
+struct Xform {
+    int from_val, to_val, from_layout, to_layout, consumer_node;
+    bool alias;
+};
+
+struct NodeInfo {
+    neo_node nd;
+    std::vector<int> inputs;
+    int N = 0, C = 0, H = 0, W = 0;
+    int val = -1;  // canonical value of the node
+};
+
+const char* op_name(int op) {
+    static const char* names[] = {"input", "conv", "maxpool", "avgpool", "gap",
+                                  "concat", "flatten", "dense", "output"};
+    return (op >= 0 && op <= 8) ? names[op] : "?";
+}
+
+}  // namespace
+
+struct neo_plan {
+    unsigned flags = 0;
+    int N = 0, C = 0, H = 0, W = 0, block = 16;
+    std::vector<NodeInfo> nodes;  // original order
+    std::vector<int> order;       // topological order
+    std::vector<Val> vals;
+    std::vector<Step> steps;
+    std::vector<Xform> xforms;
+    std::vector<long> buf_bytes, buf_off;
+    int ext_out_buf = -1;  // buffer replaced by the caller's output pointer
+    long act_bytes = 0;
+    std::vector<float> params;  // host copy of prepared parameters
+    float* d_params = nullptr;
+    char* d_act = nullptr;
+    int out_val = -1;
+    int out_dims[4] = {0, 0, 0, 0};
+    int input_val = -1;
+};
+
+namespace {
+
+std::mutex g_plans_mu;
+std::set<const neo_plan*> g_plans;
+
+bool live(const neo_plan* p) {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    return p && g_plans.count(p);
+}
+
+long align_up(long v, long a) { return (v + a - 1) / a * a; }
+
+long val_elems_root(const Val& v) {
+    // element count of a full (non-view) buffer holding v
+    return v.layout ? (long)v.N * cdiv(v.C, 16) * 16 * v.H * v.W : (long)v.N * v.C * v.H * v.W;
+}
+
+int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
+
+struct Builder {
+    neo_plan* P;
+    std::vector<std::map<int, int>> versions;  // node -> layout -> value
+
+    int new_val(int node, int N, int C, int H, int W, int layout) {
+        Val v;
+        v.N = N; v.C = C; v.H = H; v.W = W;
+        v.layout = layout;
+        v.node = node;
+        P->vals.push_back(v);
+        return (int)P->vals.size() - 1;
+    }
+
+    // The version of node `nid`'s value in `layout`, inserting a transform
+    // for consumer `consumer` if needed.
+    int get(int nid, int layout, int consumer) {
+        auto& m = versions[nid];
+        auto it = m.find(layout);
+        if (it != m.end()) return it->second;
+        const int src = P->nodes[nid].val;
+        const Val s = P->vals[src];
+        const int v = new_val(nid, s.N, s.C, s.H, s.W, layout);
+        const bool identity = s.H * s.W == 1 && s.C % 16 == 0 &&
+                              P->nodes[consumer].nd.op != NEO_OP_CONCAT;
+        Xform x{src, v, s.layout, layout, consumer, identity};
+        P->xforms.push_back(x);
+        if (identity) {
+            P->vals[v].alias_of = src;
+        } else {
+            Step st{};
+            st.kind = ST_TRANSFORM;
+            st.node = consumer;
+            st.in = src;
+            st.out = v;
+            st.src_block = s.layout;
+            st.dst_block = layout;
+            P->steps.push_back(st);
+        }
+        m[layout] = v;
+        return v;
+    }
+
+    // Register a node's produced value; in a naive plan a blocked result is
+    // transformed back to the default layout right away.
+    void produce(int nid, int v) {
+        versions[nid][P->vals[v].layout] = v;
+        P->nodes[nid].val = v;
+        if ((P->flags & NEO_PLAN_NAIVE) && P->vals[v].layout == 16) {
+            // the blocked result is only read by its transform back; every
+            // blocked consumer transforms the default-layout copy again
+            const int pv = get(nid, 0, nid);
+            P->nodes[nid].val = pv;
+            versions[nid].erase(16);
+        }
+    }
+};
+
+int add_params(neo_plan* P, const std::vector<float>& a) {
+    const long off = align_up((long)P->params.size(), 64);
+    P->params.resize(off + a.size(), 0.f);
+    std::copy(a.begin(), a.end(), P->params.begin() + off);
+    return (int)off;
+}
+
+int build(neo_plan* P, const neo_node* nodes, int n) {
+    // ---- validate and copy nodes ----------------------------------------------------
+    int n_in = 0, n_out = 0;
+    P->nodes.resize(n);
+    for (int i = 0; i < n; ++i) {
+        const neo_node& d = nodes[i];
+        NodeInfo& ni = P->nodes[i];
+        ni.nd = d;
+        if (d.op < NEO_OP_INPUT || d.op > NEO_OP_OUTPUT)
+            return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": unknown op");
+        if (d.n_inputs < 0 || (d.n_inputs > 0 && !d.inputs))
+            return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": bad inputs");
+        for (int j = 0; j < d.n_inputs; ++j) {
+            if (d.inputs[j] < 0 || d.inputs[j] >= n || d.inputs[j] == i)
+                return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": input id out of range");
+            ni.inputs.push_back(d.inputs[j]);
+        }
+        const int want = d.op == NEO_OP_INPUT ? 0 : (d.op == NEO_OP_CONCAT ? -1 : 1);
+        if ((want >= 0 && d.n_inputs != want) || (want < 0 && d.n_inputs < 1))
+            return fail(NEO_ERR_INVALID_ARG, std::string("node ") + std::to_string(i) + " (" +
+                                                 op_name(d.op) + "): wrong number of inputs");
+        if (d.op == NEO_OP_CONV) {
+            if (d.residual < -1 || d.residual >= n || d.residual == i)
+                return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": bad residual id");
+            if (!d.w) return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": conv without weights");
+            const bool any = d.bn_gamma || d.bn_beta || d.bn_mean || d.bn_var;
+            const bool all = d.bn_gamma && d.bn_beta && d.bn_mean && d.bn_var;
+            if (any && !all)
+                return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": partial batch-norm parameters");
+        }
+        if (d.op == NEO_OP_DENSE && !d.w)
+            return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": dense without weights");
+        if ((d.op == NEO_OP_CONV || d.op == NEO_OP_DENSE) && d.act != NEO_ACT_NONE && d.act != NEO_ACT_RELU)
+            return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": unknown activation");
+        n_in += d.op == NEO_OP_INPUT;
+        n_out += d.op == NEO_OP_OUTPUT;
+    }
+    if (n_in != 1 || n_out != 1)
+        return fail(NEO_ERR_INVALID_ARG, "plan needs exactly one input and one output node");
+
+    // ---- topological order (Kahn; ties by node id) -----------------------------------
+    std::vector<std::vector<int>> succ(n);
+    std::vector<int> indeg(n, 0);
+    for (int i = 0; i < n; ++i) {
+        std::vector<int> deps = P->nodes[i].inputs;
+        if (P->nodes[i].nd.op == NEO_OP_CONV && P->nodes[i].nd.residual >= 0)
+            deps.push_back(P->nodes[i].nd.residual);
+        for (int d : deps) {
+            succ[d].push_back(i);
+            ++indeg[i];
+        }
+    }
+    std::priority_queue<int, std::vector<int>, std::greater<int>> ready;
+    for (int i = 0; i < n; ++i)
+        if (!indeg[i]) ready.push(i);
+    while (!ready.empty()) {
+        const int i = ready.top();
+        ready.pop();
+        P->order.push_back(i);
+        for (int s : succ[i])
+            if (--indeg[s] == 0) ready.push(s);
+    }
+    if ((int)P->order.size() != n) return fail(NEO_ERR_INVALID_ARG, "network has a cycle");
+
+    // ---- shapes, layouts, steps -------------------------------------------------------
+    Builder B{P, std::vector<std::map<int, int>>(n)};
+    const bool naive = P->flags & NEO_PLAN_NAIVE;
+    for (int id : P->order) {
+        NodeInfo& ni = P->nodes[id];
+        const neo_node& d = ni.nd;
+        const std::string where = std::string("node ") + std::to_string(id) + " (" + op_name(d.op) + "): ";
+        auto in_shape = [&](int j) { return &P->nodes[ni.inputs[j]]; };
+        switch (d.op) {
+            case NEO_OP_INPUT: {
+                ni.N = P->N; ni.C = P->C; ni.H = P->H; ni.W = P->W;
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 0);
+                P->vals[v].buf = kExtIn;
+                P->input_val = v;
+                B.versions[id][0] = v;
+                ni.val = v;
+                break;
+            }
+            case NEO_OP_CONV: {
+                const NodeInfo* a = in_shape(0);
+                if (d.K <= 0 || d.R <= 0 || d.S <= 0 || d.stride_h <= 0 || d.stride_w <= 0 ||
+                    d.pad_h < 0 || d.pad_w < 0)
+                    return fail(NEO_ERR_INVALID_ARG, where + "bad conv parameters");
+                const int OH = out_dim(a->H, d.R, d.stride_h, d.pad_h);
+                const int OW = out_dim(a->W, d.S, d.stride_w, d.pad_w);
+                if (a->H + 2 * d.pad_h < d.R || a->W + 2 * d.pad_w < d.S || OH < 1 || OW < 1)
+                    return fail(NEO_ERR_SHAPE, where + "empty output");
+                ni.N = a->N; ni.C = d.K; ni.H = OH; ni.W = OW;
+                Step st{};
+                st.kind = ST_CONV;
+                st.node = id;
+                st.in = B.get(ni.inputs[0], 16, id);
+                if (d.residual >= 0) {
+                    const NodeInfo* r = &P->nodes[d.residual];
+                    if (r->N != ni.N || r->C != ni.C || r->H != ni.H || r->W != ni.W)
+                        return fail(NEO_ERR_SHAPE, where + "residual shape differs from the output");
+                    st.res = B.get(d.residual, 16, id);
+                }
+                const int C = a->C;
+                std::vector<float> w((long)d.K * C * d.R * d.S), b(cdiv(d.K, 16) * 16, 0.f);
+                bool has_b = false;
+                if (d.bn_gamma) {
+                    for (int k = 0; k < d.K; ++k)
+                        if (!((double)d.bn_var[k] + (double)d.bn_eps > 0.0))
+                            return fail(NEO_ERR_INVALID_ARG, where + "var + eps must be > 0");
+                    fold_bn_host(d.w, d.bias, d.bn_gamma, d.bn_beta, d.bn_mean, d.bn_var, d.bn_eps,
+                                 d.K, C, d.R, d.S, w.data(), b.data());
+                    has_b = true;
+                } else {
+                    std::copy(d.w, d.w + w.size(), w.begin());
+                    if (d.bias) {
+                        std::copy(d.bias, d.bias + d.K, b.begin());
+                        has_b = true;
+                    }
+                }
+                std::vector<float> wp((long)cdiv(d.K, 16) * cdiv(C, 16) * d.R * d.S * 256);
+                pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
+                st.w_off = add_params(P, wp);
+                if (has_b) st.b_off = add_params(P, b);
+                st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
+                                  d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
+                st.out = v;
+                P->steps.push_back(st);
+                B.produce(id, v);
+                break;
+            }
+            case NEO_OP_MAXPOOL:
+            case NEO_OP_AVGPOOL: {
+                const NodeInfo* a = in_shape(0);
+                if (d.R <= 0 || d.S <= 0 || d.stride_h <= 0 || d.stride_w <= 0 || d.pad_h < 0 ||
+                    d.pad_w < 0 || d.pad_h >= d.R || d.pad_w >= d.S)
+                    return fail(NEO_ERR_INVALID_ARG, where + "bad pool parameters");
+                const int OH = out_dim(a->H, d.R, d.stride_h, d.pad_h);
+                const int OW = out_dim(a->W, d.S, d.stride_w, d.pad_w);
+                if (a->H + 2 * d.pad_h < d.R || a->W + 2 * d.pad_w < d.S || OH < 1 || OW < 1)
+                    return fail(NEO_ERR_SHAPE, where + "empty output");
+                ni.N = a->N; ni.C = a->C; ni.H = OH; ni.W = OW;
+                Step st{};
+                st.kind = d.op == NEO_OP_MAXPOOL ? ST_MAXPOOL : ST_AVGPOOL;
+                st.node = id;
+                st.in = B.get(ni.inputs[0], 16, id);
+                st.ps = PoolShape{ni.N, ni.C, a->H, a->W, d.R, d.S, d.stride_h, d.stride_w,
+                                  d.pad_h, d.pad_w, OH, OW, 0, cdiv(ni.C, 16)};
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
+                st.out = v;
+                P->steps.push_back(st);
+                B.produce(id, v);
+                break;
+            }
+            case NEO_OP_GAP: {
+                const NodeInfo* a = in_shape(0);
+                ni.N = a->N; ni.C = a->C; ni.H = 1; ni.W = 1;
+                Step st{};
+                st.kind = ST_GAP;
+                st.node = id;
+                st.in = B.get(ni.inputs[0], 16, id);
+                const int v = B.new_val(id, ni.N, ni.C, 1, 1, 16);
+                st.out = v;
+                P->steps.push_back(st);
+                B.produce(id, v);
+                break;
+            }
+            case NEO_OP_CONCAT: {
+                const NodeInfo* a0 = in_shape(0);
+                int C = 0;
+                bool whole = true;
+                for (size_t j = 0; j < ni.inputs.size(); ++j) {
+                    const NodeInfo* a = in_shape(j);
+                    if (a->N != a0->N || a->H != a0->H || a->W != a0->W)
+                        return fail(NEO_ERR_SHAPE, where + "inputs differ in N, H or W");
+                    C += a->C;
+                    whole = whole && (a->C % 16 == 0);
+                }
+                ni.N = a0->N; ni.C = C; ni.H = a0->H; ni.W = a0->W;
+                const int layout = (whole && !naive) ? 16 : 0;
+                for (size_t j = 0; j < ni.inputs.size(); ++j) B.get(ni.inputs[j], layout, id);
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, layout);
+                B.versions[id][layout] = v;
+                ni.val = v;
+                break;
+            }
+            case NEO_OP_FLATTEN: {
+                const NodeInfo* a = in_shape(0);
+                ni.N = a->N; ni.C = a->C * a->H * a->W; ni.H = 1; ni.W = 1;
+                const int src = B.get(ni.inputs[0], 0, id);
+                const int v = B.new_val(id, ni.N, ni.C, 1, 1, 0);
+                P->vals[v].alias_of = src;
+                B.versions[id][0] = v;
+                ni.val = v;
+                break;
+            }
+            case NEO_OP_DENSE: {
+                const NodeInfo* a = in_shape(0);
+                if (a->H != 1 || a->W != 1)
+                    return fail(NEO_ERR_SHAPE, where + "input must be flat (insert a flatten)");
+                if (d.K <= 0) return fail(NEO_ERR_INVALID_ARG, where + "K must be > 0");
+                ni.N = a->N; ni.C = d.K; ni.H = 1; ni.W = 1;
+                Step st{};
+                st.kind = ST_DENSE;
+                st.node = id;
+                st.in = B.get(ni.inputs[0], 0, id);
+                st.dense_in = a->C;
+                st.dense_out = d.K;
+                st.act = d.act;
+                std::vector<float> w(d.w, d.w + (long)d.K * a->C);
+                st.w_off = add_params(P, w);
+                if (d.bias) st.b_off = add_params(P, std::vector<float>(d.bias, d.bias + d.K));
+                const int v = B.new_val(id, ni.N, ni.C, 1, 1, 0);
+                st.out = v;
+                P->steps.push_back(st);
+                B.produce(id, v);
+                break;
+            }
+            case NEO_OP_OUTPUT: {
+                const NodeInfo* a = in_shape(0);
+                ni.N = a->N; ni.C = a->C; ni.H = a->H; ni.W = a->W;
+                const int src = B.get(ni.inputs[0], 0, id);
+                P->out_val = src;
+                ni.val = src;
+                P->out_dims[0] = ni.N; P->out_dims[1] = ni.C; P->out_dims[2] = ni.H; P->out_dims[3] = ni.W;
+                break;
+            }
+        }
+    }
+
+    // ---- consumer counts (a concat input may have no other reader) --------------------
+    for (const Step& st : P->steps) {
+        if (st.in >= 0) P->vals[st.in].consumers++;
+        if (st.res >= 0) P->vals[st.res].consumers++;
+    }
+    for (auto& v : P->vals)
+        if (v.alias_of >= 0) P->vals[v.alias_of].consumers++;
+    P->vals[P->out_val].consumers++;
+    for (int id : P->order) {
+        const NodeInfo& ni = P->nodes[id];
+        if (ni.nd.op != NEO_OP_CONCAT) continue;
+        const int layout = P->vals[ni.val].layout;
+        for (int j : ni.inputs) P->vals[B.versions[j][layout]].consumers++;
+    }
+
+    // ---- storage: concat views (outermost concat first), then own buffers ------------
+    for (auto it = P->order.rbegin(); it != P->order.rend(); ++it) {
+        const NodeInfo& ni = P->nodes[*it];
+        if (ni.nd.op != NEO_OP_CONCAT) continue;
+        Val& cv = P->vals[ni.val];
+        if (!cv.view) {
+            cv.c_off = 0;
+            cv.c_tot = cv.layout ? cdiv(cv.C, 16) : cv.C;
+        }
+        int off = cv.c_off;
+        for (int j : ni.inputs) {
+            const int u = B.versions[j][cv.layout];
+            Val& uv = P->vals[u];
+            if (uv.buf == kExtIn || uv.alias_of >= 0 || uv.view || uv.consumers != 1)
+                return fail(NEO_ERR_UNSUPPORTED,
+                            "concat node " + std::to_string(*it) + ": input " + std::to_string(j) +
+                                " is read elsewhere or is the network input (no in-place slice)");
+            uv.view = true;
+            uv.c_off = off;
+            uv.c_tot = cv.c_tot;
+            uv.buf = -3 - ni.val;  // resolved below to the concat value's root
+            off += cv.layout ? cdiv(uv.C, 16) : uv.C;
+        }
+    }
+    // own buffers for roots
+    for (size_t i = 0; i < P->vals.size(); ++i) {
+        Val& v = P->vals[i];
+        if (v.alias_of >= 0 || v.buf == kExtIn || v.view) continue;
+        v.buf = (int)P->buf_bytes.size();
+        v.c_off = 0;
+        v.c_tot = v.layout ? cdiv(v.C, 16) : v.C;
+        P->buf_bytes.push_back(val_elems_root(v) * 4);
+    }
+    // resolve views (a view's concat value may itself be a view: walk outward)
+    for (size_t i = 0; i < P->vals.size(); ++i) {
+        Val& v = P->vals[i];
+        int b = v.buf;
+        while (b <= -3) b = P->vals[-3 - b].buf;
+        v.buf = b;
+    }
+    // aliases share their source's storage (units converted if the layout differs;
+    // only 1x1 spatial maps with whole blocks are aliased, where both coincide)
+    for (size_t i = 0; i < P->vals.size(); ++i) {
+        Val& v = P->vals[i];
+        if (v.alias_of < 0) continue;
+        int r = v.alias_of;
+        while (P->vals[r].alias_of >= 0) r = P->vals[r].alias_of;
+        const Val& s = P->vals[r];
+        v.buf = s.buf;
+        v.view = s.view;
+        const int f_s = s.layout ? 16 : 1, f_v = v.layout ? 16 : 1;
+        v.c_off = s.c_off * f_s / f_v;
+        v.c_tot = s.c_tot * f_s / f_v;
+    }
+    // the output goes straight into the caller's buffer when its storage is a
+    // whole buffer of exactly the output's size; otherwise a copy step is added
+    {
+        const Val& o = P->vals[P->out_val];
+        const long out_bytes = (long)o.N * o.C * o.H * o.W * 4;
+        if (o.buf >= 0 && !o.view && P->buf_bytes[o.buf] == out_bytes) {
+            P->ext_out_buf = o.buf;
+        } else {
+            Step st{};
+            st.kind = ST_COPY;
+            st.node = P->order.back();
+            st.in = P->out_val;
+            P->steps.push_back(st);
+        }
+    }
+    long off = 0;
+    for (long b : P->buf_bytes) {
+        P->buf_off.push_back(off);
+        off += align_up(b, 256);
+    }
+    P->act_bytes = off;
+    // step output views
+    for (Step& st : P->steps) {
+        if (st.kind == ST_CONV) {
+            st.cs.y_off = P->vals[st.out].c_off;
+            st.cs.y_tot = P->vals[st.out].c_tot;
+        } else if (st.kind == ST_MAXPOOL || st.kind == ST_AVGPOOL) {
+            st.ps.y_off = P->vals[st.out].c_off;
+            st.ps.y_tot = P->vals[st.out].c_tot;
+        }
+    }
+    return NEO_OK;
+}
+
+float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
+    const Val& val = P->vals[v];
+    if (val.buf == kExtIn) return const_cast<float*>(x_in);
+    if (val.buf == P->ext_out_buf) return y_out;
+    return reinterpret_cast<float*>(P->d_act + P->buf_off[val.buf]);
+}
+
+std::string describe(const neo_plan* P) {
+    std::ostringstream o;
+    auto lay = [](int l) { return l ? "NCHW16c" : "NCHW"; };
+    o << "{\"input\":[" << P->N << "," << P->C << "," << P->H << "," << P->W << "],";
+    o << "\"block\":" << P->block << ",\"naive\":" << ((P->flags & NEO_PLAN_NAIVE) ? "true" : "false");
+    o << ",\"host_only\":" << ((P->flags & NEO_PLAN_HOST_ONLY) ? "true" : "false");
+    o << ",\"output\":[" << P->out_dims[0] << "," << P->out_dims[1] << "," << P->out_dims[2] << ","
+      << P->out_dims[3] << "]";
+    o << ",\"order\":[";
+    for (size_t i = 0; i < P->order.size(); ++i) o << (i ? "," : "") << P->order[i];
+    o << "],\"nodes\":[";
+    for (size_t i = 0; i < P->nodes.size(); ++i) {
+        const NodeInfo& ni = P->nodes[i];
+        const Val& v = P->vals[ni.val];
+        o << (i ? "," : "") << "{\"id\":" << i << ",\"op\":\"" << op_name(ni.nd.op)
+          << "\",\"shape\":[" << ni.N << "," << ni.C << "," << ni.H << "," << ni.W
+          << "],\"layout\":\"" << lay(v.layout) << "\",\"value\":" << ni.val << "}";
+    }
+    o << "],\"values\":[";
+    for (size_t i = 0; i < P->vals.size(); ++i) {
+        const Val& v = P->vals[i];
+        o << (i ? "," : "") << "{\"id\":" << i << ",\"node\":" << v.node << ",\"layout\":\""
+          << lay(v.layout) << "\",\"shape\":[" << v.N << "," << v.C << "," << v.H << "," << v.W
+          << "],\"buf\":" << v.buf << ",\"c_off\":" << v.c_off << ",\"c_tot\":" << v.c_tot
+          << ",\"view\":" << (v.view ? "true" : "false") << ",\"alias_of\":" << v.alias_of << "}";
+    }
+    o << "],\"transforms\":[";
+    for (size_t i = 0; i < P->xforms.size(); ++i) {
+        const Xform& x = P->xforms[i];
+        o << (i ? "," : "") << "{\"from_value\":" << x.from_val << ",\"to_value\":" << x.to_val
+          << ",\"from\":\"" << lay(x.from_layout) << "\",\"to\":\"" << lay(x.to_layout)
+          << "\",\"before_node\":" << x.consumer_node << ",\"alias\":" << (x.alias ? "true" : "false")
+          << "}";
+    }
+    o << "],\"n_transforms\":" << P->xforms.size() << ",\"steps\":[";
+    static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy"};
+    for (size_t i = 0; i < P->steps.size(); ++i) {
+        const Step& s = P->steps[i];
+        o << (i ? "," : "") << "{\"kind\":\"" << kinds[s.kind] << "\",\"node\":" << s.node
+          << ",\"in\":" << s.in << ",\"out\":" << s.out << ",\"res\":" << s.res;
+        if (s.kind == ST_CONV) {
+            const ConvShape& c = s.cs;
+            o << ",\"conv\":{\"N\":" << c.N << ",\"C\":" << c.C << ",\"H\":" << c.H << ",\"W\":" << c.W
+              << ",\"K\":" << c.K << ",\"R\":" << c.R << ",\"S\":" << c.S << ",\"stride\":[" << c.sh
+              << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
+              << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
+              << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false") << "}";
+        }
+        if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
+        if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
+        o << "}";
+    }
+    o << "],\"buffers\":[";
+    for (size_t i = 0; i < P->buf_bytes.size(); ++i) o << (i ? "," : "") << P->buf_bytes[i];
+    o << "],\"activation_bytes\":" << P->act_bytes << ",\"param_bytes\":" << P->params.size() * 4
+      << ",\"output_buffer\":" << P->ext_out_buf << "}";
+    return o.str();
+}
+
+}  // namespace
+
+extern "C" {
+
+int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
+                    unsigned flags, neo_plan** out) {
+    if (!out) return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: out is NULL");
+    *out = nullptr;
+    if (!nodes || n_nodes <= 0) return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: no nodes");
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: non-positive input shape");
+    if (block != 16) return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16");
+    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE))
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
+    neo_plan* P = new (std::nothrow) neo_plan();
+    if (!P) return fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
+    P->flags = flags;
+    P->N = N; P->C = C; P->H = H; P->W = W; P->block = block;
+    int rc;
+    try {
+        rc = build(P, nodes, n_nodes);
+    } catch (const std::bad_alloc&) {
+        rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
+    } catch (const std::exception& e) {
+        rc = fail(NEO_ERR_INVALID_ARG, std::string("neo_plan_create: ") + e.what());
+    }
+    if (rc != NEO_OK) {
+        delete P;
+        return rc;
+    }
+    if (!(flags & NEO_PLAN_HOST_ONLY)) {
+        hipError_t e = hipMalloc(&P->d_params, std::max<size_t>(P->params.size() * 4, 256));
+        if (e != hipSuccess) {
+            delete P;
+            return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: parameter allocation")
+                                            : hip_fail(e, "neo_plan_create: hipMalloc");
+        }
+        e = hipMalloc(&P->d_act, std::max<long>(P->act_bytes, 256));
+        if (e != hipSuccess) {
+            (void)hipFree(P->d_params);
+            delete P;
+            return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: activation allocation")
+                                            : hip_fail(e, "neo_plan_create: hipMalloc");
+        }
+        e = hipMemcpy(P->d_params, P->params.data(), P->params.size() * 4, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(P->d_params);
+            (void)hipFree(P->d_act);
+            delete P;
+            return hip_fail(e, "neo_plan_create: parameter upload");
+        }
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_plans_mu);
+        g_plans.insert(P);
+    }
+    *out = P;
+    return NEO_OK;
+}
+
+int neo_plan_describe(const neo_plan* plan, char* buf, size_t len) {
+    if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_describe: not a live plan");
+    const std::string s = describe(plan);
+    if (buf && len) {
+        const size_t n = std::min(len - 1, s.size());
+        std::memcpy(buf, s.data(), n);
+        buf[n] = 0;
+    }
+    return (int)s.size();
+}
+
+int neo_plan_output_shape(const neo_plan* plan, int* dims) {
+    if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_output_shape: not a live plan");
+    if (!dims) return fail(NEO_ERR_INVALID_ARG, "neo_plan_output_shape: dims is NULL");
+    for (int i = 0; i < 4; ++i) dims[i] = plan->out_dims[i];
+    return NEO_OK;
+}
+
+int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, float* bias) {
+    if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_conv_params: not a live plan");
+    for (const Step& s : plan->steps) {
+        if (s.kind != ST_CONV || s.node != node_id) continue;
+        const long wn = (long)cdiv(s.cs.K, 16) * cdiv(s.cs.C, 16) * s.cs.R * s.cs.S * 256;
+        if (w_packed) std::copy(plan->params.begin() + s.w_off, plan->params.begin() + s.w_off + wn, w_packed);
+        if (bias) {
+            const long bn = (long)cdiv(s.cs.K, 16) * 16;
+            if (s.b_off >= 0)
+                std::copy(plan->params.begin() + s.b_off, plan->params.begin() + s.b_off + bn, bias);
+            else
+                std::fill(bias, bias + bn, 0.f);
+        }
+        return NEO_OK;
+    }
+    return fail(NEO_ERR_INVALID_ARG, "neo_plan_conv_params: node is not a conv of this plan");
+}
+
+int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t stream) {
+    if (!live(P)) return fail(NEO_ERR_STATE, "neo_run_graph: not a live plan");
+    if (P->flags & NEO_PLAN_HOST_ONLY) return fail(NEO_ERR_STATE, "neo_run_graph: host-only plan");
+    if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_graph: NULL buffer");
+    if (!aligned16(x_nchw) || !aligned16(y_out))
+        return fail(NEO_ERR_ALIGN, "neo_run_graph: buffers must be 16-byte aligned");
+    hipStream_t st = (hipStream_t)stream;
+    for (const Step& s : P->steps) {
+        hipError_t e = hipSuccess;
+        const float* prm = P->d_params;
+        switch (s.kind) {
+            case ST_TRANSFORM: {
+                const Val& in = P->vals[s.in];
+                const Val& out = P->vals[s.out];
+                float* dst = val_ptr(P, s.out, x_nchw, y_out);
+                e = launch_layout_transform(val_ptr(P, s.in, x_nchw, y_out), in.layout, dst,
+                                            out.layout, in.N, in.C, in.H, in.W, out.c_off,
+                                            out.c_tot, st);
+                break;
+            }
+            case ST_CONV:
+                e = launch_conv2d(s.cs, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off,
+                                  s.b_off >= 0 ? prm + s.b_off : nullptr,
+                                  s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
+                                  val_ptr(P, s.out, x_nchw, y_out), st);
+                break;
+            case ST_MAXPOOL:
+                e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
+                break;
+            case ST_AVGPOOL:
+                e = launch_avgpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
+                break;
+            case ST_GAP: {
+                const Val& in = P->vals[s.in];
+                e = launch_gap(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                               val_ptr(P, s.out, x_nchw, y_out), st);
+                break;
+            }
+            case ST_DENSE: {
+                const Val& in = P->vals[s.in];
+                e = launch_dense(val_ptr(P, s.in, x_nchw, y_out), in.N, s.dense_in, prm + s.w_off,
+                                 s.dense_out, s.b_off >= 0 ? prm + s.b_off : nullptr, s.act,
+                                 val_ptr(P, s.out, x_nchw, y_out), st);
+                break;
+            }
+            case ST_COPY: {
+                const Val& o = P->vals[s.in];
+                const long bytes = (long)o.N * o.C * o.H * o.W * 4;
+                e = hipMemcpyAsync(y_out, val_ptr(P, s.in, x_nchw, y_out), bytes,
+                                   hipMemcpyDeviceToDevice, st);
+                break;
+            }
+        }
+        if (e != hipSuccess) return hip_fail(e, "neo_run_graph: launch");
+    }
+    return NEO_OK;
+}
+
+void neo_plan_destroy(neo_plan* plan) {
+    {
+        std::lock_guard<std::mutex> lk(g_plans_mu);
+        if (!plan || !g_plans.count(plan)) return;
+        g_plans.erase(plan);
+    }
+    if (plan->d_params || plan->d_act) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(plan->d_params);
+        (void)hipFree(plan->d_act);
+    }
+    delete plan;
+}
+
+}  // extern "C"

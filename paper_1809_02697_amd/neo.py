@@ -1,0 +1,355 @@
+"""Python binding of libneo (ctypes).  Argument marshalling only: every
+operation runs in the HIP kernels of ``libneo.so``; there is no fallback.
+
+Device tensors are ``torch`` float32 CUDA (HIP) tensors; torch supplies the
+memory and the current stream.  Names follow the C-ABI in ``include/neo.h``.
+"""
+from __future__ import annotations
+
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libneo.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "neo.h")
+
+OK = 0
+ERR_NAMES = {-1: "NEO_ERR_INVALID_ARG", -2: "NEO_ERR_SHAPE", -3: "NEO_ERR_ALIGN",
+             -4: "NEO_ERR_UNSUPPORTED", -5: "NEO_ERR_HIP", -6: "NEO_ERR_OOM", -7: "NEO_ERR_STATE"}
+ACT = {"none": 0, "relu": 1}
+OPS = {"input": 0, "conv": 1, "maxpool": 2, "avgpool": 3, "gap": 4, "concat": 5, "flatten": 6,
+       "dense": 7, "output": 8}
+PLAN_HOST_ONLY = 1
+PLAN_NAIVE = 2
+BLOCK = 16
+
+
+class NeoError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Epilogue(ctypes.Structure):
+    _fields_ = [("act", ctypes.c_int), ("residual", ctypes.c_void_p)]
+
+
+class Node(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int), ("n_inputs", ctypes.c_int),
+                ("inputs", ctypes.POINTER(ctypes.c_int)),
+                ("K", ctypes.c_int), ("R", ctypes.c_int), ("S", ctypes.c_int),
+                ("stride_h", ctypes.c_int), ("stride_w", ctypes.c_int),
+                ("pad_h", ctypes.c_int), ("pad_w", ctypes.c_int),
+                ("act", ctypes.c_int), ("residual", ctypes.c_int),
+                ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("bn_gamma", ctypes.c_void_p), ("bn_beta", ctypes.c_void_p),
+                ("bn_mean", ctypes.c_void_p), ("bn_var", ctypes.c_void_p),
+                ("bn_eps", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libneo.so; raises if it has not been built (no fallback path)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_1809_02697_amd.build` (no CPU fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, F, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    sig = {
+        "neo_conv2d_blocked": [P, I, I, I, I, P, I, I, I, P, I, I, I, I,
+                               ctypes.POINTER(Epilogue), P, I, I, P],
+        "neo_layout_transform": [P, I, P, I, I, I, I, I, P],
+        "neo_pack_filter": [P, I, I, I, I, I, I, P, P],
+        "neo_fold_bn": [P, P, P, P, P, P, F, I, I, I, I, P, P],
+        "neo_maxpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
+        "neo_avgpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
+        "neo_global_avgpool_blocked": [P, I, I, I, I, P, P],
+        "neo_dense": [P, I, I, P, I, P, I, P, P],
+        "neo_plan_create": [ctypes.POINTER(Node), I, I, I, I, I, I, ctypes.c_uint,
+                            ctypes.POINTER(P)],
+        "neo_plan_describe": [P, ctypes.c_char_p, S],
+        "neo_plan_output_shape": [P, ctypes.POINTER(I)],
+        "neo_plan_conv_params": [P, I, P, P],
+        "neo_run_graph": [P, P, P, P],
+        "neo_plan_destroy": [P],
+        "neo_last_error": [],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = I
+    L.neo_plan_destroy.restype = None
+    L.neo_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def header_symbols():
+    """Names of the functions declared in include/neo.h."""
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(neo_[a-z0-9_]+)\s*\(", txt)))
+
+
+def last_error():
+    return lib().neo_last_error().decode()
+
+
+def _check(rc):
+    if rc < 0:
+        raise NeoError(rc, last_error())
+    return rc
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dptr(t, name="tensor"):
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device (cuda) tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _pair(v):
+    return tuple(v) if isinstance(v, (tuple, list)) else (v, v)
+
+
+def cblocks(C, block=BLOCK):
+    return -(-C // block)
+
+
+def out_size(n, k, s, p):
+    return (n + 2 * p - k) // s + 1
+
+
+# --------------------------------------------------------------------------------------
+# Single operations
+# --------------------------------------------------------------------------------------
+def conv2d_blocked(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
+                   residual=None, out=None, y_cblk_offset=0, y_cblk_total=None, stream=None):
+    """x: [N][ceil(C/16)][H][W][16]; w_packed: KCRS[16]c[16]k.  Returns out."""
+    import torch
+    (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
+    N, CB, H, W, blk = x.shape
+    OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
+    KB = cblocks(K)
+    tot = KB if y_cblk_total is None else y_cblk_total
+    if out is None:
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=x.device,
+                          dtype=torch.float32)
+    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
+                  residual.data_ptr() if residual is not None else None)
+    if residual is not None:
+        _dptr(residual, "residual")
+    _check(lib().neo_conv2d_blocked(_dptr(x, "x"), N, C, H, W, _dptr(w_packed, "w_packed"), K,
+                                    R, S, _dptr(bias, "bias"), sh, sw, ph, pw, ctypes.byref(ep),
+                                    _dptr(out, "out"), y_cblk_offset, tot, _stream(stream)))
+    return out
+
+
+def layout_transform(src, src_block, dst_block, N, C, H, W, out=None, stream=None):
+    import torch
+    if out is None:
+        shape = (N, C, H, W) if dst_block == 0 else (N, cblocks(C, dst_block), H, W, dst_block)
+        out = torch.empty(shape, device=src.device, dtype=torch.float32)
+    _check(lib().neo_layout_transform(_dptr(src, "src"), src_block, _dptr(out, "out"), dst_block,
+                                      N, C, H, W, _stream(stream)))
+    return out
+
+
+def to_blocked(x, block=BLOCK, stream=None):
+    N, C, H, W = x.shape
+    return layout_transform(x, 0, block, N, C, H, W, stream=stream)
+
+
+def from_blocked(xb, C, stream=None):
+    N, CB, H, W, blk = xb.shape
+    return layout_transform(xb, blk, 0, N, C, H, W, stream=stream)
+
+
+def pack_filter(w, ic_bn=BLOCK, oc_bn=BLOCK, out=None, stream=None):
+    """w: device KCRS [K][C][R][S] -> KCRS[ic_bn]c[oc_bn]k."""
+    import torch
+    K, C, R, S = w.shape
+    if out is None:
+        out = torch.empty((cblocks(K, oc_bn), cblocks(C, ic_bn), R, S, ic_bn, oc_bn),
+                          device=w.device, dtype=torch.float32)
+    _check(lib().neo_pack_filter(_dptr(w, "w"), K, C, R, S, ic_bn, oc_bn, _dptr(out, "out"),
+                                 _stream(stream)))
+    return out
+
+
+def _hp(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def fold_bn(w, bias, gamma, beta, mean, var, eps):
+    """Host batch-norm fold (numpy float32 in, numpy float32 out)."""
+    w = np.ascontiguousarray(w, np.float32)
+    K, C, R, S = w.shape
+    arrs = [None if bias is None else np.ascontiguousarray(bias, np.float32)] + \
+           [np.ascontiguousarray(a, np.float32) for a in (gamma, beta, mean, var)]
+    w_out = np.empty_like(w)
+    b_out = np.empty(K, np.float32)
+    _check(lib().neo_fold_bn(_hp(w), *[_hp(a) for a in arrs], float(eps), K, C, R, S,
+                             _hp(w_out), _hp(b_out)))
+    return w_out, b_out
+
+
+def _pool(fn, x, C, R, S, stride, pad, out, y_cblk_offset, y_cblk_total, stream):
+    import torch
+    (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
+    N, CB, H, W, _ = x.shape
+    OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
+    tot = CB if y_cblk_total is None else y_cblk_total
+    if out is None:
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=x.device,
+                          dtype=torch.float32)
+    _check(fn(_dptr(x, "x"), N, C, H, W, R, S, sh, sw, ph, pw, _dptr(out, "out"), y_cblk_offset,
+              tot, _stream(stream)))
+    return out
+
+
+def maxpool2d_blocked(x, C, R, S, stride, pad=0, out=None, y_cblk_offset=0, y_cblk_total=None,
+                      stream=None):
+    return _pool(lib().neo_maxpool2d_blocked, x, C, R, S, stride, pad, out, y_cblk_offset,
+                 y_cblk_total, stream)
+
+
+def avgpool2d_blocked(x, C, R, S, stride, pad=0, out=None, y_cblk_offset=0, y_cblk_total=None,
+                      stream=None):
+    return _pool(lib().neo_avgpool2d_blocked, x, C, R, S, stride, pad, out, y_cblk_offset,
+                 y_cblk_total, stream)
+
+
+def global_avgpool_blocked(x, C, out=None, stream=None):
+    import torch
+    N, CB, H, W, _ = x.shape
+    if out is None:
+        out = torch.empty((N, CB, 1, 1, BLOCK), device=x.device, dtype=torch.float32)
+    _check(lib().neo_global_avgpool_blocked(_dptr(x, "x"), N, C, H, W, _dptr(out, "out"),
+                                            _stream(stream)))
+    return out
+
+
+def dense(x, w, bias=None, act="none", out=None, stream=None):
+    """x device [N][IN], w device [OUT][IN] -> [N][OUT]."""
+    import torch
+    N, IN = x.shape
+    OUT = w.shape[0]
+    if out is None:
+        out = torch.empty((N, OUT), device=x.device, dtype=torch.float32)
+    _check(lib().neo_dense(_dptr(x, "x"), N, IN, _dptr(w, "w"), OUT, _dptr(bias, "bias"),
+                           ACT[act] if isinstance(act, str) else int(act), _dptr(out, "out"),
+                           _stream(stream)))
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# Graph plan
+# --------------------------------------------------------------------------------------
+class Plan:
+    """A plan built from a network description (``workloads.Graph``)."""
+
+    def __init__(self, graph, input_shape=None, flags=0, block=BLOCK):
+        L = lib()
+        shape = tuple(input_shape or graph.input_shape)
+        keep = []
+        arr = (Node * len(graph.nodes))()
+        for i, n in enumerate(graph.nodes):
+            d = arr[i]
+            d.op = OPS[n.op]
+            ins = (ctypes.c_int * max(1, len(n.inputs)))(*n.inputs)
+            keep.append(ins)
+            d.n_inputs = len(n.inputs)
+            d.inputs = ctypes.cast(ins, ctypes.POINTER(ctypes.c_int))
+            d.K, d.R, d.S = n.K, n.R, n.S
+            d.stride_h, d.stride_w = n.stride
+            d.pad_h, d.pad_w = n.pad
+            d.act = ACT[n.act]
+            d.residual = n.residual
+
+            def host(a):
+                if a is None:
+                    return None
+                a = np.ascontiguousarray(a, np.float32)
+                keep.append(a)
+                return ctypes.c_void_p(a.ctypes.data)
+
+            d.w = host(n.w)
+            d.bias = host(n.bias)
+            if n.bn is not None:
+                d.bn_gamma, d.bn_beta = host(n.bn["gamma"]), host(n.bn["beta"])
+                d.bn_mean, d.bn_var = host(n.bn["mean"]), host(n.bn["var"])
+                d.bn_eps = float(n.bn["eps"])
+        h = ctypes.c_void_p()
+        _check(L.neo_plan_create(arr, len(graph.nodes), *shape, block, flags, ctypes.byref(h)))
+        self._h = h
+        self.flags = flags
+        self.input_shape = shape
+        dims = (ctypes.c_int * 4)()
+        _check(L.neo_plan_output_shape(h, dims))
+        self.output_shape = tuple(dims)
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise NeoError(-7, "plan destroyed")
+        return self._h
+
+    def describe(self):
+        L = lib()
+        n = _check(L.neo_plan_describe(self.handle, None, 0))
+        buf = ctypes.create_string_buffer(n + 1)
+        _check(L.neo_plan_describe(self.handle, buf, n + 1))
+        return json.loads(buf.value.decode())
+
+    def conv_params(self, node_id, K, C, R, S):
+        wp = np.empty((cblocks(K), cblocks(C), R, S, BLOCK, BLOCK), np.float32)
+        b = np.empty(cblocks(K) * BLOCK, np.float32)
+        _check(lib().neo_plan_conv_params(self.handle, node_id, _hp(wp), _hp(b)))
+        return wp, b
+
+    def run(self, x, out=None, stream=None):
+        """x: device NCHW input -> device output of ``output_shape``
+        ([N, C] after flatten/dense, else [N, C, H, W])."""
+        import torch
+        if tuple(x.shape) != self.input_shape:
+            raise ValueError(f"input shape {tuple(x.shape)} != plan input {self.input_shape}")
+        if out is None:
+            N, C, H, W = self.output_shape
+            shape = (N, C) if (H, W) == (1, 1) else (N, C, H, W)
+            out = torch.empty(shape, device=x.device, dtype=torch.float32)
+        _check(lib().neo_run_graph(self.handle, _dptr(x, "x"), _dptr(out, "out"),
+                                   _stream(stream)))
+        return out
+
+    def destroy(self):
+        if self._h is not None:
+            lib().neo_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass

@@ -1,0 +1,228 @@
+"""Host-side tests of libneo (no GPU): exported symbols, argument validation,
+batch-norm folding and the graph planner (host-only plans)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle as orc
+from paper_1809_02697_amd import neo
+from paper_1809_02697_amd import workloads as wl
+
+L = neo.lib()
+P = ctypes.c_void_p
+
+
+def test_library_exports_every_header_symbol():
+    names = neo.header_symbols()
+    assert len(names) >= 15
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, missing
+
+
+# ---- argument validation (returns before any device work) ------------------------------
+FAKE = P(0x10000)       # 16-byte aligned, never dereferenced on these paths
+MIS = P(0x10004)
+
+
+def conv_call(x=FAKE, w=FAKE, y=FAKE, N=1, C=16, H=8, W=8, K=16, R=3, S=3, st=(1, 1), pd=(1, 1),
+              ep=None, yo=0, yt=1):
+    return L.neo_conv2d_blocked(x, N, C, H, W, w, K, R, S, None, st[0], st[1], pd[0], pd[1],
+                                ep, y, yo, yt, None)
+
+
+def test_conv_argument_errors():
+    assert conv_call(x=None) == -1
+    assert conv_call(x=MIS) == -3
+    assert "x" in neo.last_error()
+    assert conv_call(C=0) == -1
+    assert conv_call(st=(0, 1)) == -1
+    assert conv_call(pd=(-1, 0)) == -1
+    assert conv_call(H=2, pd=(0, 0)) == -2          # window larger than input
+    assert conv_call(yt=0) == -2                     # output view too small
+    assert conv_call(yo=1, yt=1) == -2
+    bad_act = neo.Epilogue(7, None)
+    assert conv_call(ep=ctypes.byref(bad_act)) == -1
+    res_mis = neo.Epilogue(1, 0x10004)
+    assert conv_call(ep=ctypes.byref(res_mis)) == -3
+    assert conv_call(N=4096, C=4096, H=64, W=64) == -4   # > 2^31 elements
+
+
+def test_other_argument_errors():
+    assert L.neo_layout_transform(FAKE, 3, FAKE, 16, 1, 3, 4, 4, None) == -1
+    assert L.neo_layout_transform(FAKE, 0, FAKE, 16, 1, 3, 4, 4, None) == -1  # overlap
+    assert L.neo_pack_filter(None, 4, 4, 3, 3, 16, 16, FAKE, None) == -1
+    assert L.neo_pack_filter(FAKE, 4, 4, 3, 3, 0, 16, P(0x20000), None) == -1
+    assert L.neo_maxpool2d_blocked(FAKE, 1, 16, 8, 8, 3, 3, 2, 2, 3, 1, P(0x20000), 0, 1,
+                                   None) == -1     # pad >= window
+    assert L.neo_avgpool2d_blocked(FAKE, 1, 16, 8, 8, 3, 3, 1, 1, 1, 1, P(0x20000), 1, 1,
+                                   None) == -2     # view out of range
+    assert L.neo_dense(FAKE, 1, 8, FAKE, 4, None, 3, P(0x20000), None) == -1
+    assert L.neo_global_avgpool_blocked(MIS, 1, 16, 2, 2, FAKE, None) == -3
+
+
+# ---- batch-norm fold ----------------------------------------------------------------------
+def test_fold_bn_matches_unfolded_batchnorm():
+    c = wl.conv_case(7, 9, 3, 3, 1, 1, 10, 9, seed=3)
+    wf, bf = neo.fold_bn(c.w, c.bias, c.bn["gamma"], c.bn["beta"], c.bn["mean"], c.bn["var"],
+                         c.bn["eps"])
+    # folded conv vs conv -> bias -> batch norm (oracle, unfolded)
+    ref = orc.batchnorm(orc.bias_add(orc.conv2d(c.x, c.w, 1, 1), c.bias), c.bn["gamma"],
+                        c.bn["beta"], c.bn["mean"], c.bn["var"], c.bn["eps"])
+    got = orc.bias_add(orc.conv2d(c.x, wf, 1, 1), bf)
+    np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-5)
+    # exact form: one double multiply, one rounding
+    scale = c.bn["gamma"].astype(np.float64) / np.sqrt(c.bn["var"].astype(np.float64) +
+                                                      np.float64(np.float32(c.bn["eps"])))
+    np.testing.assert_array_equal(wf, (c.w.astype(np.float64) *
+                                       scale[:, None, None, None]).astype(np.float32))
+
+
+def test_fold_bn_errors():
+    w = np.ones((2, 1, 1, 1), np.float32)
+    one = np.ones(2, np.float32)
+    with pytest.raises(neo.NeoError):
+        neo.fold_bn(w, None, one, one, one, -one, 0.0)     # var + eps <= 0
+
+
+# ---- planner (host-only plans) -------------------------------------------------------------
+def host_plan(g, flags=0):
+    return neo.Plan(g, flags=neo.PLAN_HOST_ONLY | flags)
+
+
+def test_resnet50_plan_has_two_transforms():
+    g = wl.resnet50(1)
+    p = host_plan(g)
+    d = p.describe()
+    assert d["n_transforms"] == 2
+    t_in, t_out = d["transforms"]
+    assert (t_in["from"], t_in["to"], t_in["alias"]) == ("NCHW", "NCHW16c", False)
+    assert g.nodes[t_in["before_node"]].name == "conv1"
+    # after global average pooling the map is 1x1 with 2048 = 128 blocks: the
+    # transform back is the identity in memory
+    assert (t_out["from"], t_out["to"], t_out["alias"]) == ("NCHW16c", "NCHW", True)
+    assert g.nodes[t_out["before_node"]].op == "flatten"
+    kinds = [s["kind"] for s in d["steps"]]
+    assert kinds.count("conv") == 53 and kinds.count("transform") == 1
+    assert kinds == ["transform"] + ["conv", "maxpool"] + [k for k in kinds[3:]]
+    assert kinds[-2:] == ["gap", "dense"]
+    for n in d["nodes"]:
+        if n["op"] in ("conv", "maxpool", "gap"):
+            assert n["layout"] == "NCHW16c"
+    assert d["output"] == [1, 1000, 1, 1]
+    assert d["output_buffer"] >= 0                # the dense layer writes the caller's buffer
+    p.destroy()
+
+
+def test_vgg16_plan_exit_transform_is_real():
+    g = wl.vgg16(1)
+    d = host_plan(g).describe()
+    assert d["n_transforms"] == 2
+    t_out = d["transforms"][1]
+    assert t_out["alias"] is False and t_out["from"] == "NCHW16c"
+    kinds = [s["kind"] for s in d["steps"]]
+    assert kinds.count("transform") == 2 and kinds.count("dense") == 3
+
+
+def test_inception_plan_concat_views():
+    g = wl.inception_v3(1)
+    d = host_plan(g).describe()
+    assert d["n_transforms"] == 2
+    kinds = [s["kind"] for s in d["steps"]]
+    assert kinds.count("conv") == 94 and "copy" not in kinds
+    vals = d["values"]
+    # every concat input is written in place into its concat buffer, at the
+    # running channel-block offset
+    for i in g.node_ids("concat"):
+        cval = vals[d["nodes"][i]["value"]]
+        off = cval["c_off"]
+        for j in g.nodes[i].inputs:
+            v = vals[d["nodes"][j]["value"]]
+            assert v["view"] and v["buf"] == cval["buf"] and v["c_tot"] == cval["c_tot"]
+            assert v["c_off"] == off
+            off += -(-v["shape"][1] // 16)
+        assert off - cval["c_off"] == cval["shape"][1] // 16
+
+
+def test_naive_plan_wraps_every_blocked_op():
+    g = wl.resnet50(1)
+    d = host_plan(g, neo.PLAN_NAIVE).describe()
+    kinds = [s["kind"] for s in d["steps"]]
+    # every conv / pool / gap result goes back to NCHW, and every blocked input
+    # (including residuals) comes from NCHW again
+    n_blocked_ops = 53 + 1 + 1
+    assert d["n_transforms"] >= 2 * n_blocked_ops
+    assert kinds.count("conv") == 53
+
+
+def test_plan_conv_params_are_folded_and_packed():
+    g = wl.tiny_graph()
+    p = host_plan(g)
+    for i, n in enumerate(g.nodes):
+        if n.op != "conv":
+            continue
+        C = n.w.shape[1]
+        wp, b = p.conv_params(i, n.K, C, n.R, n.S)
+        if n.bn is not None:
+            scale = n.bn["gamma"].astype(np.float64) / np.sqrt(
+                n.bn["var"].astype(np.float64) + np.float64(np.float32(n.bn["eps"])))
+            wf = (n.w.astype(np.float64) * scale[:, None, None, None]).astype(np.float32)
+            bias = np.zeros(n.K) if n.bias is None else n.bias.astype(np.float64)
+            bf = ((bias - n.bn["mean"]) * scale + n.bn["beta"]).astype(np.float32)
+        else:
+            wf, bf = n.w, n.bias
+        np.testing.assert_array_equal(wp, orc.pack_filter(wf, 16, 16))
+        want_b = np.zeros(-(-n.K // 16) * 16, np.float32)
+        want_b[:n.K] = bf
+        np.testing.assert_array_equal(b, want_b)
+
+
+def test_plan_errors():
+    g = wl.tiny_graph()
+    # concat input that is also read by another node cannot be written in place
+    bad = wl.tiny_graph()
+    cat = bad.node_ids("concat")[0]
+    first = bad.nodes[cat].inputs[0]
+    bad.nodes[cat + 1].inputs = (first,)            # c4 now reads a concat input
+    with pytest.raises(neo.NeoError) as e:
+        host_plan(bad)
+    assert e.value.code == -4
+    # a cycle
+    cyc = wl.tiny_graph()
+    cyc.nodes[1].inputs = (2,)
+    with pytest.raises(neo.NeoError):
+        host_plan(cyc)
+    # block other than 16
+    with pytest.raises(neo.NeoError) as e:
+        neo.Plan(g, flags=neo.PLAN_HOST_ONLY, block=8)
+    assert e.value.code == -4
+    # running a host-only plan
+    p = host_plan(g)
+    assert L.neo_run_graph(p.handle, FAKE, FAKE, None) == -7
+    h = p.handle
+    p.destroy()
+    assert L.neo_plan_describe(h, None, 0) == -7     # destroyed handle
+
+
+def test_plan_accepts_any_node_order():
+    g = wl.tiny_graph()
+    d1 = host_plan(g).describe()
+    # reverse the node list, remapping ids
+    n = len(g.nodes)
+    perm = list(reversed(range(n)))
+    inv = {old: new for new, old in enumerate(perm)}
+    import copy
+    g2 = copy.deepcopy(g)
+    g2.nodes = [copy.deepcopy(g.nodes[o]) for o in perm]
+    for nd in g2.nodes:
+        nd.inputs = tuple(inv[i] for i in nd.inputs)
+        if nd.residual >= 0:
+            nd.residual = inv[nd.residual]
+    d2 = host_plan(g2).describe()
+    assert d2["n_transforms"] == d1["n_transforms"]
+    # another valid topological order: same steps, possibly interleaved differently
+    assert sorted(s["kind"] for s in d2["steps"]) == sorted(s["kind"] for s in d1["steps"])
+    pos = {v: i for i, v in enumerate(d2["order"])}
+    for i, nd in enumerate(g2.nodes):
+        for j in nd.inputs:
+            assert pos[j] < pos[i]

@@ -1,0 +1,111 @@
+"""GPU parity of whole networks through neo_run_graph (the layout plan of
+Section 3.2) against the oracle's reference graph executor."""
+import numpy as np
+import pytest
+
+import oracle as orc
+from paper_1809_02697_amd import workloads as wl
+
+from gpu_util import assert_close, dev, host, rel_l2, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def neo():
+    torch_cuda()
+    from paper_1809_02697_amd import neo as n
+    n.lib()
+    return n
+
+
+def run_plan(neo, g, flags=0, x=None):
+    p = neo.Plan(g, flags=flags)
+    y = host(p.run(dev(g.x if x is None else x)))
+    p.destroy()
+    return y
+
+
+@pytest.mark.parametrize("builder", [wl.tiny_graph, wl.vgg_like_tiny])
+def test_small_graphs(neo, builder):
+    g = builder()
+    ref = orc.run_graph(g)
+    y = run_plan(neo, g)
+    assert_close(y.reshape(ref.shape), ref, g.name)
+
+
+@pytest.mark.parametrize("builder", [wl.tiny_graph, wl.vgg_like_tiny])
+def test_naive_plan_bit_identical(neo, builder):
+    """Eliminating the transforms does not change a single bit (the transforms
+    are exact permutations and the kernels are the same)."""
+    g = builder()
+    np.testing.assert_array_equal(run_plan(neo, g), run_plan(neo, g, neo.PLAN_NAIVE))
+
+
+def test_plan_reusable_and_output_shape(neo):
+    g = wl.tiny_graph()
+    p = neo.Plan(g)
+    assert p.output_shape == (2, 10, 1, 1)
+    a = host(p.run(dev(g.x)))
+    b = host(p.run(dev(g.x)))
+    np.testing.assert_array_equal(a, b)
+    p.destroy()
+
+
+def _teacher_forced_convs(neo, g, limit=None):
+    """Every conv node of g on the GPU, fed the oracle's own input (and
+    residual), with the plan's folded and packed parameters."""
+    vals = orc.run_graph(g, keep=True)
+    p = neo.Plan(g)
+    worst = 0.0
+    n_done = 0
+    for i, n in enumerate(g.nodes):
+        if n.op != "conv":
+            continue
+        x = vals[n.inputs[0]]
+        C = x.shape[1]
+        wp, b = p.conv_params(i, n.K, C, n.R, n.S)
+        res = vals[n.residual] if n.residual >= 0 else None
+        yb = neo.conv2d_blocked(neo.to_blocked(dev(x)), C, dev(wp), n.K, n.R, n.S, bias=dev(b),
+                                stride=n.stride, pad=n.pad, act=n.act,
+                                residual=neo.to_blocked(dev(res)) if res is not None else None)
+        y = orc.from_blocked(host(yb), n.K)
+        worst = max(worst, assert_close(y, vals[i], n.name))
+        n_done += 1
+        if limit and n_done >= limit:
+            break
+    p.destroy()
+    return worst
+
+
+@pytest.mark.parametrize("model", ["resnet50", "vgg16", "inception_v3"])
+def test_teacher_forced_layers(neo, model):
+    g = wl.MODELS[model](1)
+    w = _teacher_forced_convs(neo, g)
+    print(f"{model}: worst per-layer rel L2 {w:.2e}")
+
+
+@pytest.mark.parametrize("model", ["resnet50", "vgg16", "inception_v3"])
+def test_end_to_end_batch1(neo, model):
+    g = wl.MODELS[model](1)
+    ref = orc.run_graph(g)
+    y = run_plan(neo, g)
+    print(f"{model} b1: rel L2 {rel_l2(y, ref):.2e}, max abs {np.abs(y - ref).max():.2e}")
+    assert_close(y, ref, model)
+    assert (np.argmax(y, 1) == np.argmax(ref, 1)).all()
+
+
+@pytest.mark.parametrize("model", ["resnet50", "vgg16"])
+def test_end_to_end_batch32_sampled(neo, model):
+    """Batch 32 on the GPU; images 0 and 31 checked against the oracle run on
+    those images alone (images are independent)."""
+    g = wl.MODELS[model](32)
+    y = run_plan(neo, g)
+    for i in (0, 31):
+        ref = orc.run_graph(g, x=g.x[i:i + 1])
+        assert_close(y[i:i + 1], ref, f"{model} image {i}")
+
+
+def test_naive_plan_bit_identical_resnet50(neo):
+    g = wl.resnet50(1)
+    np.testing.assert_array_equal(run_plan(neo, g), run_plan(neo, g, neo.PLAN_NAIVE))

@@ -1,0 +1,210 @@
+"""GPU parity of the single operations, called through the C-ABI, against the
+CPU oracle on seeded inputs (teacher forced: the GPU op gets the oracle's
+float32 input)."""
+import numpy as np
+import pytest
+
+import oracle as orc
+from paper_1809_02697_amd import workloads as wl
+
+from gpu_util import assert_close, dev, host, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def neo():
+    torch_cuda()
+    from paper_1809_02697_amd import neo as n
+    n.lib()
+    return n
+
+
+# ---- layout transform and filter packing: bit-exact -----------------------------------------
+@pytest.mark.parametrize("N,C,H,W", [(1, 64, 56, 56), (2, 3, 7, 5), (1, 1, 1, 1), (3, 17, 4, 9),
+                                     (1, 33, 13, 11), (2, 80, 5, 5), (1, 2048, 7, 7),
+                                     (1, 5, 1, 3)])
+def test_layout_roundtrip_bit_exact(neo, N, C, H, W):
+    rng = np.random.default_rng([N, C, H, W])
+    x = rng.uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    xb = neo.to_blocked(dev(x))
+    hb = host(xb)
+    np.testing.assert_array_equal(hb, orc.to_blocked(x, 16))
+    lanes = hb.transpose(0, 1, 4, 2, 3).reshape(N, -1, H, W)[:, C:]
+    assert (lanes == 0).all() and not np.signbit(lanes).any()
+    np.testing.assert_array_equal(host(neo.from_blocked(xb, C)), x)
+
+
+@pytest.mark.parametrize("sb,db", [(0, 4), (0, 32), (16, 32), (32, 8), (4, 0), (8, 16), (16, 16)])
+def test_layout_any_blocks(neo, sb, db):
+    N, C, H, W = 2, 37, 5, 6
+    rng = np.random.default_rng(sb * 100 + db)
+    x = rng.uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    src = x if sb == 0 else orc.to_blocked(x, sb)
+    out = neo.layout_transform(dev(src), sb, db, N, C, H, W)
+    want = x if db == 0 else orc.to_blocked(x, db)
+    np.testing.assert_array_equal(host(out), want)
+
+
+@pytest.mark.parametrize("K,C,R,S,ib,ob", [(64, 64, 3, 3, 16, 16), (5, 3, 7, 7, 16, 16),
+                                           (40, 17, 1, 7, 16, 16), (20, 5, 3, 2, 4, 16),
+                                           (33, 48, 1, 1, 32, 8)])
+def test_pack_filter_bit_exact(neo, K, C, R, S, ib, ob):
+    w = np.random.default_rng(K * C).normal(0, 1, (K, C, R, S)).astype(np.float32)
+    np.testing.assert_array_equal(host(neo.pack_filter(dev(w), ib, ob)),
+                                  orc.pack_filter(w, ib, ob))
+
+
+# ---- convolution -----------------------------------------------------------------------------
+def run_case(neo, c, fold=True):
+    """Run one LayerCase on the GPU: fold (host) -> pack (device) -> conv."""
+    if c.bn is not None and fold:
+        w, b = neo.fold_bn(c.w, c.bias, c.bn["gamma"], c.bn["beta"], c.bn["mean"], c.bn["var"],
+                           c.bn["eps"])
+    else:
+        w, b = c.w, c.bias
+    K = c.K
+    bp = None
+    if b is not None:
+        bpad = np.zeros(-(-K // 16) * 16, np.float32)
+        bpad[:K] = b
+        bp = dev(bpad)
+    wp = neo.pack_filter(dev(w))
+    xb = neo.to_blocked(dev(c.x))
+    res = neo.to_blocked(dev(c.residual)) if c.epilogue == "res" else None
+    act = "relu" if c.epilogue in ("relu", "res", "bias_relu") else "none"
+    yb = neo.conv2d_blocked(xb, c.C, wp, K, c.R, c.S, bias=bp, stride=c.stride, pad=c.pad,
+                            act=act, residual=res)
+    return yb
+
+
+def test_config1_single_conv(neo):
+    """3x3, 64->64, 56x56, bias + ReLU, compared in NCHW after the round trip."""
+    g = wl.single_conv(0)
+    n = g.nodes[1]
+    ref = orc.run_graph(g)
+    c = wl.LayerCase("cfg1", 64, 64, 3, 3, (1, 1), (1, 1), 56, 56, 1, "bias_relu", 1, g.x, n.w,
+                     n.bias, None, None)
+    y = host(neo.from_blocked(run_case(neo, c), 64))
+    assert_close(y, ref, "config 1")
+
+
+@pytest.mark.parametrize("lid", [c[0] for c in wl.RESNET50_LAYERS])
+def test_config2_resnet50_layer(neo, lid):
+    case = {c.id: c for c in wl.resnet50_layer_sweep(1)}[lid]
+    ref = orc.layer_forward(case)
+    yb = host(run_case(neo, case))
+    y = orc.from_blocked(yb, case.K)
+    assert_close(y, ref, lid)
+    # padded output lanes stay +0.0
+    lanes = yb.transpose(0, 1, 4, 2, 3).reshape(yb.shape[0], -1, *yb.shape[2:4])[:, case.K:]
+    assert (lanes == 0).all()
+
+
+EDGE = [
+    # C, K, R, S, stride, pad, H, W, N, epilogue
+    (5, 7, 3, 3, 1, 1, 9, 11, 2, "relu"),          # ragged C and K, N = 2
+    (17, 40, 3, 3, 2, 1, 15, 13, 1, "relu"),       # C one past a block, stride 2, odd sizes
+    (33, 20, 1, 7, (1, 1), (0, 3), 17, 17, 1, "relu"),   # 1x7
+    (20, 33, 7, 1, (1, 1), (3, 0), 17, 17, 1, "none"),   # 7x1
+    (48, 64, 5, 5, 1, 2, 35, 35, 1, "relu"),        # 5x5 (Inception A)
+    (32, 32, 3, 3, 2, 0, 149, 149, 1, "relu"),      # valid padding, stride 2
+    (3, 32, 3, 3, 2, 0, 299, 299, 1, "relu"),       # Inception stem: small-C path
+    (3, 64, 7, 7, 2, 3, 64, 64, 2, "relu"),         # ResNet stem shape, N = 2
+    (4, 16, 3, 3, 1, 1, 8, 8, 1, "none"),           # C = 4: small-C path, whole quad
+    (6, 16, 3, 3, 1, 1, 8, 8, 1, "none"),           # C = 6: regular path, padded block
+    (64, 256, 1, 1, 1, 0, 7, 7, 3, "res"),          # residual, N = 3, M = 147 ragged
+    (128, 96, 1, 1, 2, 0, 9, 9, 1, "none"),         # 1x1 stride 2 on odd size
+    (2048, 1000, 1, 1, 1, 0, 1, 1, 1, "none"),      # 1x1 spatial (dense-like)
+    (16, 16, 3, 3, 1, 2, 3, 3, 1, "relu"),          # pad larger than half the window
+    (64, 64, 3, 3, 1, 1, 1, 1, 1, "relu"),          # 1x1 input, 3x3 window
+    (16, 16, 2, 2, 2, 0, 6, 6, 1, "relu"),          # even window
+]
+
+
+@pytest.mark.parametrize("e", EDGE, ids=[f"C{e[0]}K{e[1]}_{e[2]}x{e[3]}_H{e[6]}N{e[8]}" for e in EDGE])
+def test_conv_edge_cases(neo, e):
+    C, K, R, S, st, pd, H, W, N, epi = e
+    st = st if isinstance(st, tuple) else (st, st)
+    pd = pd if isinstance(pd, tuple) else (pd, pd)
+    OH, OW = orc.out_size(H, R, st[0], pd[0]), orc.out_size(W, S, st[1], pd[1])
+    c = wl.conv_case(C, K, R, S, st, pd, H, W, N=N, epilogue=epi, out_hw=(OH, OW))
+    ref = orc.layer_forward(c)
+    y = orc.from_blocked(host(run_case(neo, c)), K)
+    assert_close(y, ref, str(e))
+
+
+def test_conv_delta_kernel_bit_exact(neo):
+    """Delta filter: the output is the shifted input, exactly."""
+    C, H, W = 32, 10, 9
+    x = np.random.default_rng(1).uniform(-1, 1, (1, C, H, W)).astype(np.float32)
+    w = np.zeros((C, C, 3, 3), np.float32)
+    for k in range(C):
+        w[k, k, 0, 2] = 1
+    xb = neo.to_blocked(dev(x))
+    y = host(neo.from_blocked(neo.conv2d_blocked(xb, C, neo.pack_filter(dev(w)), C, 3, 3,
+                                                 stride=1, pad=1), C))
+    np.testing.assert_array_equal(y, orc.conv2d(x, w, 1, 1))
+
+
+def test_conv_writes_concat_slice_only(neo):
+    """y_cblk_offset / total: the conv writes its blocks and nothing else."""
+    c = wl.conv_case(16, 32, 3, 3, 1, 1, 8, 8, epilogue="relu", with_bn=False)
+    ref = orc.layer_forward(c)
+    torch = torch_cuda()
+    out = torch.full((1, 5, 8, 8, 16), 7.0, device="cuda")
+    bpad = dev(c.bias)
+    neo.conv2d_blocked(neo.to_blocked(dev(c.x)), 16, neo.pack_filter(dev(c.w)), 32, 3, 3,
+                       bias=bpad, stride=1, pad=1, act="relu", out=out, y_cblk_offset=2,
+                       y_cblk_total=5)
+    o = host(out)
+    assert (o[:, [0, 1, 4]] == 7.0).all()
+    assert_close(orc.from_blocked(o[:, 2:4], 32), ref, "slice")
+
+
+# ---- pools --------------------------------------------------------------------------------
+POOLS = [("max", 3, 2, 1, 64, 112, 112, 1), ("max", 2, 2, 0, 64, 224, 224, 1),
+         ("max", 3, 2, 0, 288, 35, 35, 1), ("max", 3, 2, 0, 5, 9, 8, 2),
+         ("avg", 3, 1, 1, 192, 35, 35, 1), ("avg", 3, 1, 1, 37, 6, 7, 2),
+         ("avg", 2, 2, 1, 16, 5, 5, 1)]
+
+
+@pytest.mark.parametrize("p", POOLS, ids=[f"{p[0]}{p[1]}s{p[2]}p{p[3]}C{p[4]}H{p[5]}" for p in POOLS])
+def test_pool(neo, p):
+    kind, R, st, pd, C, H, W, N = p
+    x = np.random.default_rng(C * H).uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    xb = neo.to_blocked(dev(x))
+    if kind == "max":
+        y = neo.maxpool2d_blocked(xb, C, R, R, st, pd)
+        ref = orc.maxpool2d(x, R, R, st, pd)
+        np.testing.assert_array_equal(orc.from_blocked(host(y), C), ref)
+    else:
+        y = neo.avgpool2d_blocked(xb, C, R, R, st, pd)
+        ref = orc.avgpool2d(x, R, R, st, pd)
+        assert_close(orc.from_blocked(host(y), C), ref, "avgpool")
+    lanes = host(y).transpose(0, 1, 4, 2, 3).reshape(N, -1, *host(y).shape[2:4])[:, C:]
+    assert (lanes == 0).all()
+
+
+@pytest.mark.parametrize("N,C,H,W", [(1, 2048, 7, 7), (1, 2048, 8, 8), (2, 40, 5, 3),
+                                     (1, 16, 1, 1), (32, 512, 7, 7)])
+def test_global_avgpool(neo, N, C, H, W):
+    x = np.random.default_rng(C).uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    y = neo.global_avgpool_blocked(neo.to_blocked(dev(x)), C)
+    assert_close(orc.from_blocked(host(y), C), orc.global_avgpool(x), "gap")
+
+
+# ---- dense -----------------------------------------------------------------------------------
+@pytest.mark.parametrize("N,IN,OUT,act", [(1, 2048, 1000, "none"), (1, 25088, 4096, "relu"),
+                                          (32, 4096, 1000, "none"), (3, 37, 19, "relu"),
+                                          (17, 64, 10, "none"), (1, 5, 3, "none")])
+def test_dense(neo, N, IN, OUT, act):
+    rng = np.random.default_rng(IN + OUT)
+    x = rng.uniform(-1, 1, (N, IN)).astype(np.float32)
+    w = rng.normal(0, np.sqrt(2 / IN), (OUT, IN)).astype(np.float32)
+    b = rng.normal(0, 0.1, OUT).astype(np.float32)
+    ref = orc.dense(x, w, b)
+    if act == "relu":
+        ref = orc.relu(ref)
+    y = host(neo.dense(dev(x), dev(w), dev(b), act=act))
+    assert_close(y, ref, "dense")
