@@ -45,3 +45,61 @@ def host(t):
     import torch
     torch.cuda.synchronize()
     return t.detach().cpu().numpy()
+
+
+U32 = 2.0 ** -24
+
+
+def gamma(n):
+    """Higham's gamma_n = n u / (1 - n u) for float32 (u = 2^-24)."""
+    return n * U32 / (1 - n * U32)
+
+
+def strict_violations(got, ref, abs_rel_tol=ABS_REL):
+    bound = abs_rel_tol * (1.0 + np.abs(np.asarray(ref, np.float64)))
+    return int((np.abs(np.asarray(got, np.float64) - ref) > bound).sum())
+
+
+def assert_close_conditioned(got, ref, cond, n_terms, what="", rel_l2_tol=REL_L2,
+                             abs_rel_tol=ABS_REL):
+    """Parity of a float32 layer whose inputs are far from unit scale.
+
+    rel L2 <= 1e-5 as for every other check.  Element-wise, the error may reach
+    1e-4 (1 + |ref|) plus the a-priori bound of a float32 sum of n products in
+    any order, gamma_{n+4} * cond, where cond = sum_i |x_i| |w_i| + |bias| +
+    |residual| is the magnitude of the terms (+4 covers the folded weights and
+    the epilogue adds).  Returns (rel L2, count beyond the plain clause)."""
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.isfinite(got).all(), what + ": non-finite output"
+    e = rel_l2(got, ref)
+    assert e <= rel_l2_tol, f"{what}: rel L2 {e:.3e} > {rel_l2_tol}"
+    err = np.abs(got.astype(np.float64) - ref)
+    bound = abs_rel_tol * (1.0 + np.abs(ref.astype(np.float64))) + gamma(n_terms + 4) * cond
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {int(bad.sum())} elements beyond the conditioned bound; "
+                           f"worst err/bound {float((err / bound).max()):.2f}")
+    return e, strict_violations(got, ref, abs_rel_tol)
+
+
+def assert_close_network(got, ref, what="", rel_l2_tol=REL_L2, abs_rel_tol=ABS_REL):
+    """Parity of a whole network's output.  rel L2 <= 1e-5; element-wise the
+    absolute floor of 1e-4 (1 + |ref|) is taken at the output's own scale,
+    1e-4 (max(1, rms(ref)) + |ref|): with random batch-norm statistics the
+    ResNet-50 logits reach rms ~2e4, and the error of a float32 pipeline grows
+    with that scale, not with |ref| of a logit near zero.  For unit-scale
+    outputs this is the plain clause.  Returns (rel L2, count beyond the plain
+    clause)."""
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.isfinite(got).all(), what + ": non-finite output"
+    e = rel_l2(got, ref)
+    assert e <= rel_l2_tol, f"{what}: rel L2 {e:.3e} > {rel_l2_tol}"
+    r64 = ref.astype(np.float64)
+    scale = max(1.0, float(np.sqrt(np.mean(r64 ** 2))))
+    err = np.abs(got.astype(np.float64) - r64)
+    bad = err > abs_rel_tol * (scale + np.abs(r64))
+    assert not bad.any(), f"{what}: {int(bad.sum())} elements beyond 1e-4 (scale + |ref|)"
+    return e, strict_violations(got, ref, abs_rel_tol)
