@@ -197,7 +197,13 @@ enum neo_plan_flags {
     /* Transform around every blocked operation instead of keeping the blocked
      * layout between them (the baseline the paper's elimination improves on).
      * Results are bit-identical to the default plan. */
-    NEO_PLAN_NAIVE = 2
+    NEO_PLAN_NAIVE = 2,
+    /* neo_run_graph replays a HIP graph of the launch list instead of
+     * launching every step from the host.  The graph is captured (on a
+     * private stream of the plan) at the first run and again whenever x_nchw
+     * or y_out differ from the previous run; a replay is one hipGraphLaunch on
+     * the caller's stream.  Results are bit-identical to eager runs. */
+    NEO_PLAN_HIPGRAPH = 4
 };
 
 /*

@@ -29,10 +29,24 @@ struct ConvShape {
     int act;
 };
 
+// Launch configuration: register tile (fk channel blocks x fp pixel groups of
+// 16 per wave) and the number of workgroups the reduction is split over.
+struct ConvConfig {
+    int fk, fp, split;
+};
+ConvConfig choose_conv_config(const ConvShape& s);
+// Workspace for a split reduction: partial tiles (bytes) and arrival counters
+// (ints, zero before the first launch; every launch leaves them zero).
+size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);
+size_t conv_counter_count(const ConvShape& s, const ConvConfig& c);
+
 // Launch the blocked convolution.  x: NCHW16c, w: KCRS[16]c[16]k, bias:
 // [KB*16] or null, res: NCHW16c [N][KB][OH][OW][16] or null, y: NCHW16c view.
-hipError_t launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias,
-                         const float* res, float* y, hipStream_t st);
+// ws / cnt: workspace of at least conv_workspace_bytes / conv_counter_count
+// (a split is only used when both are given).
+hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
+                         const float* bias, const float* res, float* y, float* ws, int* cnt,
+                         hipStream_t st);
 
 // ---- layout ---------------------------------------------------------------------------
 // dst_off / dst_tot: destination channel view in destination units (channels

@@ -51,6 +51,7 @@ struct Step {
     int node;         // originating node (transforms: the consumer that needed it)
     int in = -1, out = -1, res = -1;
     ConvShape cs{};
+    ConvConfig cc{1, 1, 1};
     PoolShape ps{};
     long w_off = -1, b_off = -1;
     int src_block = 0, dst_block = 0;
@@ -91,9 +92,18 @@ struct neo_plan {
     std::vector<float> params;  // host copy of prepared parameters
     float* d_params = nullptr;
     char* d_act = nullptr;
+    // split-reduction workspace shared by the conv steps (they run in order)
+    size_t ws_bytes = 0, cnt_n = 0;
+    float* d_ws = nullptr;
+    int* d_cnt = nullptr;
     int out_val = -1;
     int out_dims[4] = {0, 0, 0, 0};
     int input_val = -1;
+    // NEO_PLAN_HIPGRAPH: captured launch list for (graph_x, graph_y)
+    hipStream_t cap_stream = nullptr;
+    hipGraphExec_t graph_exec = nullptr;
+    const float* graph_x = nullptr;
+    float* graph_y = nullptr;
 };
 
 namespace {
@@ -304,6 +314,9 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 if (has_b) st.b_off = add_params(P, b);
                 st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
                                   d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
+                st.cc = choose_conv_config(st.cs);
+                P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.cc));
+                P->cnt_n = std::max(P->cnt_n, conv_counter_count(st.cs, st.cc));
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
                 st.out = v;
                 P->steps.push_back(st);
@@ -525,6 +538,7 @@ std::string describe(const neo_plan* P) {
     o << "{\"input\":[" << P->N << "," << P->C << "," << P->H << "," << P->W << "],";
     o << "\"block\":" << P->block << ",\"naive\":" << ((P->flags & NEO_PLAN_NAIVE) ? "true" : "false");
     o << ",\"host_only\":" << ((P->flags & NEO_PLAN_HOST_ONLY) ? "true" : "false");
+    o << ",\"hipgraph\":" << ((P->flags & NEO_PLAN_HIPGRAPH) ? "true" : "false");
     o << ",\"output\":[" << P->out_dims[0] << "," << P->out_dims[1] << "," << P->out_dims[2] << ","
       << P->out_dims[3] << "]";
     o << ",\"order\":[";
@@ -565,7 +579,8 @@ std::string describe(const neo_plan* P) {
               << ",\"K\":" << c.K << ",\"R\":" << c.R << ",\"S\":" << c.S << ",\"stride\":[" << c.sh
               << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
-              << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false") << "}";
+              << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
+              << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
@@ -590,7 +605,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: non-positive input shape");
     if (block != 16) return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16");
-    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE))
+    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     neo_plan* P = new (std::nothrow) neo_plan();
     if (!P) return fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
@@ -623,11 +638,17 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                                             : hip_fail(e, "neo_plan_create: hipMalloc");
         }
         e = hipMemcpy(P->d_params, P->params.data(), P->params.size() * 4, hipMemcpyHostToDevice);
+        if (e == hipSuccess && P->ws_bytes) e = hipMalloc(&P->d_ws, P->ws_bytes);
+        if (e == hipSuccess && P->cnt_n) e = hipMalloc(&P->d_cnt, P->cnt_n * sizeof(int));
+        if (e == hipSuccess && P->cnt_n) e = hipMemset(P->d_cnt, 0, P->cnt_n * sizeof(int));
         if (e != hipSuccess) {
             (void)hipFree(P->d_params);
             (void)hipFree(P->d_act);
+            if (P->d_ws) (void)hipFree(P->d_ws);
+            if (P->d_cnt) (void)hipFree(P->d_cnt);
             delete P;
-            return hip_fail(e, "neo_plan_create: parameter upload");
+            return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: workspace")
+                                            : hip_fail(e, "neo_plan_create: parameter upload");
         }
     }
     {
@@ -674,13 +695,7 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
     return fail(NEO_ERR_INVALID_ARG, "neo_plan_conv_params: node is not a conv of this plan");
 }
 
-int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t stream) {
-    if (!live(P)) return fail(NEO_ERR_STATE, "neo_run_graph: not a live plan");
-    if (P->flags & NEO_PLAN_HOST_ONLY) return fail(NEO_ERR_STATE, "neo_run_graph: host-only plan");
-    if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_graph: NULL buffer");
-    if (!aligned16(x_nchw) || !aligned16(y_out))
-        return fail(NEO_ERR_ALIGN, "neo_run_graph: buffers must be 16-byte aligned");
-    hipStream_t st = (hipStream_t)stream;
+static int enqueue_steps(neo_plan* P, const float* x_nchw, float* y_out, hipStream_t st) {
     for (const Step& s : P->steps) {
         hipError_t e = hipSuccess;
         const float* prm = P->d_params;
@@ -695,10 +710,10 @@ int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t s
                 break;
             }
             case ST_CONV:
-                e = launch_conv2d(s.cs, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off,
+                e = launch_conv2d(s.cs, s.cc, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off,
                                   s.b_off >= 0 ? prm + s.b_off : nullptr,
                                   s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
-                                  val_ptr(P, s.out, x_nchw, y_out), st);
+                                  val_ptr(P, s.out, x_nchw, y_out), P->d_ws, P->d_cnt, st);
                 break;
             case ST_MAXPOOL:
                 e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
@@ -732,6 +747,58 @@ int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t s
     return NEO_OK;
 }
 
+static void drop_graph(neo_plan* P) {
+    if (P->graph_exec) (void)hipGraphExecDestroy(P->graph_exec);
+    P->graph_exec = nullptr;
+    P->graph_x = nullptr;
+    P->graph_y = nullptr;
+}
+
+// Capture the launch list for (x, y) on the plan's private stream.
+static int capture(neo_plan* P, const float* x_nchw, float* y_out) {
+    drop_graph(P);
+    hipError_t e;
+    if (!P->cap_stream) {
+        e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "neo_run_graph: capture stream");
+    }
+    e = hipStreamBeginCapture(P->cap_stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return hip_fail(e, "neo_run_graph: begin capture");
+    const int rc = enqueue_steps(P, x_nchw, y_out, P->cap_stream);
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(P->cap_stream, &g);
+    if (rc != NEO_OK) {
+        if (g) (void)hipGraphDestroy(g);
+        return rc;
+    }
+    if (e != hipSuccess) return hip_fail(e, "neo_run_graph: end capture");
+    e = hipGraphInstantiate(&P->graph_exec, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+        P->graph_exec = nullptr;
+        return hip_fail(e, "neo_run_graph: instantiate");
+    }
+    P->graph_x = x_nchw;
+    P->graph_y = y_out;
+    return NEO_OK;
+}
+
+int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t stream) {
+    if (!live(P)) return fail(NEO_ERR_STATE, "neo_run_graph: not a live plan");
+    if (P->flags & NEO_PLAN_HOST_ONLY) return fail(NEO_ERR_STATE, "neo_run_graph: host-only plan");
+    if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_graph: NULL buffer");
+    if (!aligned16(x_nchw) || !aligned16(y_out))
+        return fail(NEO_ERR_ALIGN, "neo_run_graph: buffers must be 16-byte aligned");
+    hipStream_t st = (hipStream_t)stream;
+    if (!(P->flags & NEO_PLAN_HIPGRAPH)) return enqueue_steps(P, x_nchw, y_out, st);
+    if (!P->graph_exec || P->graph_x != x_nchw || P->graph_y != y_out) {
+        const int rc = capture(P, x_nchw, y_out);
+        if (rc != NEO_OK) return rc;
+    }
+    hipError_t e = hipGraphLaunch(P->graph_exec, st);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_run_graph: graph launch");
+}
+
 void neo_plan_destroy(neo_plan* plan) {
     {
         std::lock_guard<std::mutex> lk(g_plans_mu);
@@ -740,8 +807,12 @@ void neo_plan_destroy(neo_plan* plan) {
     }
     if (plan->d_params || plan->d_act) {
         (void)hipDeviceSynchronize();
+        drop_graph(plan);
+        if (plan->cap_stream) (void)hipStreamDestroy(plan->cap_stream);
         (void)hipFree(plan->d_params);
         (void)hipFree(plan->d_act);
+        if (plan->d_ws) (void)hipFree(plan->d_ws);
+        if (plan->d_cnt) (void)hipFree(plan->d_cnt);
     }
     delete plan;
 }

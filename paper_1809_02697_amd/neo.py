@@ -25,6 +25,7 @@ OPS = {"input": 0, "conv": 1, "maxpool": 2, "avgpool": 3, "gap": 4, "concat": 5,
        "dense": 7, "output": 8}
 PLAN_HOST_ONLY = 1
 PLAN_NAIVE = 2
+PLAN_HIPGRAPH = 4
 BLOCK = 16
 
 

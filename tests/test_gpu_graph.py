@@ -125,3 +125,23 @@ def test_end_to_end_batch32_sampled(neo, model):
 def test_naive_plan_bit_identical_resnet50(neo):
     g = wl.resnet50(1)
     np.testing.assert_array_equal(run_plan(neo, g), run_plan(neo, g, neo.PLAN_NAIVE))
+
+
+def test_hipgraph_replay_bit_identical(neo):
+    """Graph replays (several, with eager work and synchronizations between
+    them) give exactly the eager result; a new output pointer recaptures."""
+    torch = torch_cuda()
+    g = wl.tiny_graph()
+    eager = run_plan(neo, g)
+    p = neo.Plan(g, flags=neo.PLAN_HIPGRAPH)
+    x = dev(g.x)
+    for i in range(4):
+        y = p.run(x)                      # fresh output tensor: recapture each time
+        torch.ones(1000, device="cuda").sum()
+        np.testing.assert_array_equal(host(y), eager)
+    out = torch.empty_like(y)
+    for i in range(3):
+        out.fill_(-1.0)
+        p.run(x, out)
+        np.testing.assert_array_equal(host(out), eager)
+    p.destroy()

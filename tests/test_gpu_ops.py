@@ -208,3 +208,40 @@ def test_dense(neo, N, IN, OUT, act):
         ref = orc.relu(ref)
     y = host(neo.dense(dev(x), dev(w), dev(b), act=act))
     assert_close(y, ref, "dense")
+
+
+CONFIGS = [(fk, fp, sp) for fk in (1, 2, 4) for fp in (1, 2, 4) for sp in (1, 3, 8)]
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=[f"fk{c[0]}fp{c[1]}s{c[2]}" for c in CONFIGS])
+def test_conv_every_launch_config(neo, cfg, monkeypatch):
+    """Every register tile and reduction split (forced through the tuning
+    override) on ragged shapes: odd K, M not a multiple of the tile, C with a
+    padded block, and the small-C path."""
+    monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d" % cfg)
+    for (C, K, R, st, pd, H, N, epi) in [(40, 72, 3, 1, 1, 11, 2, "res"),
+                                         (3, 24, 3, 2, 1, 17, 1, "relu"),
+                                         (130, 20, 1, 1, 0, 5, 3, "none")]:
+        OH = orc.out_size(H, R, st, pd)
+        c = wl.conv_case(C, K, R, R, st, pd, H, H, N=N, epilogue=epi, out_hw=(OH, OH))
+        ref = orc.layer_forward(c)
+        for _ in range(2):   # the second launch reuses the self-reset counters
+            y = orc.from_blocked(host(run_case(neo, c)), K)
+            assert_close(y, ref, f"{cfg} C{C} K{K}")
+
+
+def test_conv_long_reduction_without_step_table(neo):
+    """7x7 over 48 blocks x 49 taps = 2352 steps, more than one workgroup's
+    step table holds without a split: the decode fallback."""
+    c = wl.conv_case(768, 16, 7, 7, 1, 3, 9, 9, epilogue="relu")
+    import os
+    old = os.environ.get("NEO_CONV_CONFIG")
+    os.environ["NEO_CONV_CONFIG"] = "1,1,1"
+    try:
+        y = orc.from_blocked(host(run_case(neo, c)), 16)
+    finally:
+        if old is None:
+            os.environ.pop("NEO_CONV_CONFIG")
+        else:
+            os.environ["NEO_CONV_CONFIG"] = old
+    assert_close(y, orc.layer_forward(c), "long reduction")
