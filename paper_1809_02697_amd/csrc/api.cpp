@@ -53,6 +53,20 @@ void pack_filter_host(const float* w, int K, int C, int R, int S, int ib, int ob
                         }
 }
 
+void blocks_to_mfma_order(const float* in, long n_blocks, float* out) {
+    for (long b = 0; b < n_blocks; ++b)
+        for (int c = 0; c < 16; ++c)
+            for (int k = 0; k < 16; ++k)
+                out[b * 256 + ((c / 4) * 16 + k) * 4 + c % 4] = in[b * 256 + c * 16 + k];
+}
+
+void blocks_from_mfma_order(const float* in, long n_blocks, float* out) {
+    for (long b = 0; b < n_blocks; ++b)
+        for (int c = 0; c < 16; ++c)
+            for (int k = 0; k < 16; ++k)
+                out[b * 256 + c * 16 + k] = in[b * 256 + ((c / 4) * 16 + k) * 4 + c % 4];
+}
+
 }  // namespace neo
 
 using namespace neo;
@@ -93,56 +107,43 @@ int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
 
 // Split-reduction workspace of the standalone convolution call, one per
 // (device, stream) so that calls on different streams never share it; calls
-// on one stream are ordered by the stream.  Grows on demand (hipMalloc, and a
-// synchronous clear of the counters), so the first call of a given size must
-// not be made while the stream is being captured into a graph.
+// on one stream are ordered by the stream.  Grows on demand (hipMalloc), so
+// the first call of a given size must not be made while the stream is being
+// captured into a graph.
 struct StreamWs {
     float* ws = nullptr;
-    int* cnt = nullptr;
-    size_t ws_bytes = 0, cnt_n = 0;
+    size_t bytes = 0;
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, StreamWs> g_ws;
 
-int stream_workspace(hipStream_t st, size_t bytes, size_t counters, float** ws, int** cnt) {
+int stream_workspace(hipStream_t st, size_t bytes, float** ws) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "neo_conv2d_blocked: hipGetDevice");
     std::lock_guard<std::mutex> lk(g_ws_mu);
     StreamWs& w = g_ws[{dev, st}];
-    if (w.ws_bytes < bytes) {
+    if (w.bytes < bytes) {
         if (w.ws) (void)hipFree(w.ws);
         w.ws = nullptr;
-        w.ws_bytes = 0;
+        w.bytes = 0;
         e = hipMalloc(&w.ws, bytes);
         if (e != hipSuccess) return fail(NEO_ERR_OOM, "neo_conv2d_blocked: workspace allocation");
-        w.ws_bytes = bytes;
-    }
-    if (w.cnt_n < counters) {
-        if (w.cnt) (void)hipFree(w.cnt);
-        w.cnt = nullptr;
-        w.cnt_n = 0;
-        e = hipMalloc(&w.cnt, counters * sizeof(int));
-        if (e != hipSuccess) return fail(NEO_ERR_OOM, "neo_conv2d_blocked: counter allocation");
-        e = hipMemset(w.cnt, 0, counters * sizeof(int));
-        if (e != hipSuccess) return hip_fail(e, "neo_conv2d_blocked: counter clear");
-        w.cnt_n = counters;
+        w.bytes = bytes;
     }
     *ws = w.ws;
-    *cnt = w.cnt;
     return NEO_OK;
 }
 
-// Optional override of the launch configuration, "fk,fp,split", for tuning
-// sweeps of the standalone call.
+// Optional override of the launch configuration, "fk,fp,split[,waves]", for
+// tuning sweeps of the standalone call.
 bool env_config(ConvConfig* c) {
     const char* v = std::getenv("NEO_CONV_CONFIG");
     if (!v || !*v) return false;
-    int fk, fp, sp;
-    if (std::sscanf(v, "%d,%d,%d", &fk, &fp, &sp) != 3) return false;
-    if ((fk != 1 && fk != 2 && fk != 4) || (fp != 1 && fp != 2 && fp != 4) || sp < 1 || sp > 64)
-        return false;
-    *c = ConvConfig{fk, fp, sp};
+    ConvConfig t{1, 1, 1, 4};
+    const int n = std::sscanf(v, "%d,%d,%d,%d", &t.fk, &t.fp, &t.split, &t.waves);
+    if (n < 3 || !conv_config_valid(t)) return false;
+    *c = t;
     return true;
 }
 
@@ -178,6 +179,8 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
     CHECK_SIZE(blocked_elems(N, C, H, W, 16));
     CHECK_SIZE((long)N * y_cblk_total * 16 * OH * OW);
     CHECK_SIZE((long)KB * 16 * cdiv(C, 16) * 16 * R * S);
+    if (blocked_elems(N, C, H, W, 16) >= (1L << 29) || (long)KB * cdiv(C, 16) * R * S * 256 >= (1L << 29))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_blocked: input or filter of 2 GiB or more");
     ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
                 y_cblk_offset, y_cblk_total, act};
     ConvConfig cfg = choose_conv_config(s);
@@ -185,13 +188,12 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
     const int T = cdiv(C, 16) * R * S;
     if (cfg.split > T) cfg.split = T;
     float* ws = nullptr;
-    int* cnt = nullptr;
     if (cfg.split > 1) {
-        const int rc = stream_workspace((hipStream_t)stream, conv_workspace_bytes(s, cfg),
-                                        conv_counter_count(s, cfg), &ws, &cnt);
+        const int rc = stream_workspace((hipStream_t)stream, conv_workspace_bytes(s, cfg), &ws);
         if (rc != NEO_OK) return rc;
     }
-    hipError_t e = launch_conv2d(s, cfg, x, w_packed, bias, res, y, ws, cnt, (hipStream_t)stream);
+    hipError_t e = launch_conv2d(s, cfg, x, w_packed, false, bias, res, y, ws,
+                                 (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_blocked launch");
 }
 

@@ -20,23 +20,27 @@
 //
 // Input loads: for k-step t the lane needs x[pixel i][channel 4g+t]; one float4
 // load at channel offset 4g covers t = 0..3 (the reduction order over the 16
-// channels of a block is free).  Filter loads: the KCRS[16]c[16]k block of one
-// (kb, cb, r, s) is [16 c][16 k]; the lane reads w[c = 4g+t][k = i], 16
-// consecutive floats per c row.
+// channels of a block is free).  Filter loads: in the KCRS[16]c[16]k block
+// [16 c][16 k] of one (kb, cb, r, s) the lane reads w[c = 4g+t][k = i] (four
+// dwords 64 bytes apart); plans store each block as [c/4][k][c%4] instead, so
+// the same four values are one float4.
 //
 // Work split.  Algorithm 1 parallelizes over disjoint output chunks only; at
 // batch 1 that leaves too few chunks for 1024 SIMDs, so the reduction is split
 // as well:
-//   - across the 4 waves of a workgroup (step st goes to wave st % 4), summed
-//     through LDS in wave order;
-//   - across SPLIT workgroups (grid z), each owning a contiguous range of
-//     steps.  Every workgroup writes its partial tile to a workspace and bumps
-//     a per-tile counter; the workgroup that arrives last sums the SPLIT
-//     partials in split order (so the result does not depend on arrival
-//     order), resets the counter to 0 for the next launch and runs the
-//     epilogue.  No workgroup ever waits for another.
+//   - across the WAVES waves of a workgroup, each owning a contiguous run of
+//     steps, summed through LDS in wave order;
+//   - optionally across SPLIT workgroups, each owning a contiguous range of
+//     steps and writing its raw partial tile to a workspace; a second kernel
+//     adds the SPLIT partials in split order (deterministic) and runs the
+//     epilogue.  The kernel boundary makes the partials visible across XCDs
+//     (whose L2s are not coherent) without a per-workgroup device-scope
+//     release, which measured ~20 ns of serialized time per workgroup.
 // Loads run D steps ahead of the MFMAs (a register ring sized to the tile), so
-// each wave keeps D-1 steps of loads in flight while it computes.
+// each wave keeps D-1 steps of loads in flight while it computes.  The step
+// bookkeeping is scalar and incremental (see Loader): measured on MI355X, a
+// per-step lane-offset computation, an LDS table or integer divisions per step
+// cost more than the MFMAs themselves at batch 1.
 // The epilogue (bias, residual, ReLU) runs in registers before the single store.
 #include <algorithm>
 #include <cmath>
@@ -54,12 +58,14 @@ struct ConvArgs {
     const float* bias;
     const float* res;
     float* y;
-    float* ws;     // split partials [SPLIT][tiles][FK*FP][64 lanes][4]
-    int* cnt;      // per-tile arrival counters (0 between launches)
+    float* ws;  // split partials [SPLIT][N][KB][OH][OW][16]
     int N, CB, H, W, KB, R, S, RS, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
+    int x_bytes, w_bytes;
 };
 
-constexpr int kWaves = 4;
+constexpr int kXcds = 8;
+constexpr unsigned kRsrcWord3 = 0x00020000;    // raw buffer, gfx9 family
+constexpr unsigned kOutOfRange = 0x80000000u;  // buffer offset that reads as 0
 
 template <int FK, int FP, bool SMALLC>
 struct Operands;
@@ -67,7 +73,7 @@ struct Operands;
 template <int FK, int FP>
 struct Operands<FK, FP, false> {
     v4f b[FP];
-    float a[FK][4];
+    v4f a[FK];
 };
 
 template <int FK, int FP>
@@ -76,72 +82,110 @@ struct Operands<FK, FP, true> {
     float a[FK];
 };
 
-// One reduction step (channel block cb, kernel entry r, s): the input offset
-// relative to the pixel's own address, (cb*H*W + r*W + s)*16 floats, and the
-// tap (r, s) for the zero-padding test.  Built once per workgroup in LDS so
-// the inner loop never divides.
-struct StepInfo {
-    int dx;
-    short r, s;
-};
+__device__ inline int cdiv_d(int a, int b) { return (a + b - 1) / b; }
 
-constexpr int kMaxTableSteps = 2048;
+__device__ inline v4f ld4(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, int imm) {
+    return __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, voff + imm, soff, 0));
+}
+__device__ inline float ld1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, int imm) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff + imm, soff, 0));
+}
 
-template <int FK, int FP, bool SMALLC, bool PW>
-struct Tile {
-    // per-lane pixel coordinates of the FP pixel groups (lanes past the last
-    // pixel are clamped to pixel 0: their results are never stored)
-    int pbase[FP], pih[FP], piw[FP];
-    const float* wbase[FK];  // channel blocks past K are clamped to block 0
+// Per-wave loader.  Reduction steps are taken tap-major, st = rs*CB + cb
+// (kernel entry rs = r*S + s outer, channel block cb inner), so within one tap
+// the zero-padding test and the per-lane offsets do not change and a step only
+// advances two scalar offsets: input += H*W*64 bytes, filter += R*S*1 KB.  The
+// per-lane part is recomputed once per tap.  All loads are buffer loads; a
+// zero-padding tap gets an out-of-range lane offset, for which the hardware
+// returns 0.  Every load is issued unconditionally, so the number of loads in
+// flight is static and the compiler waits only for the step it is about to
+// use.
+//   WMFMA:  filter blocks stored [c/4][k][c%4] (one float4 per lane) instead
+//           of the KCRS[16]c[16]k block [c][k] (four dwords, 64 bytes apart).
+template <int FK, int FP, bool SMALLC, bool WMFMA>
+struct Loader {
+    __amdgpu_buffer_rsrc_t xr, wr;
+    int xoff[FP];                 // byte offset of the lane's pixel at (cb, r, s) = 0 (may be < 0)
+    unsigned rowm[FP], colm[FP];  // bit r / s set when that tap row / column is inside
+    int pih[FP], piw[FP];
+    unsigned woff[FK];            // byte offset of the lane's element in filter block (kb, 0, 0)
+    bool wide_taps;               // more than 32 taps per axis: explicit test
+    // position of the next step to load (wave-uniform)
+    int st, cb, rs, r, s;
+    int sx, sw;                   // step byte offsets: input cb*H*W*64, filter (cb*RS + rs)*1024
+    unsigned toff[FP];            // lane offset of the current tap, or out of range
 
-    // Every load is issued unconditionally (zero-padding taps read a clamped
-    // address and are zeroed by a select) so the number of loads in flight
-    // is static and the compiler waits only for the step it is about to use.
-    // PW: 1x1 window, no padding: every tap is in bounds and step st is
-    // channel block st.
-    __device__ void load(const ConvArgs& a, const StepInfo (&tab)[PW ? 1 : kMaxTableSteps],
-                         bool use_tab, int k_lo, int st, int g, int li,
-                         Operands<FK, FP, SMALLC>& o) const {
-        int dx, r = 0, s = 0;
-        if constexpr (PW) {
-            dx = st * a.H * a.W * 16;
-        } else if (use_tab) {
-            const StepInfo e = tab[st - k_lo];
-            dx = e.dx;
-            r = e.r;
-            s = e.s;
-        } else {
-            // range longer than the table: decode (uniform, slower)
-            const int cb = st / a.RS;
-            const int rs = st - cb * a.RS;
-            r = rs / a.S;
-            s = rs - r * a.S;
-            dx = ((cb * a.H + r) * a.W + s) * 16;
-        }
+    __device__ void set_tap(const ConvArgs& a) {
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
-            bool ok = true;
-            if constexpr (!PW) {
+            bool ok;
+            if (!wide_taps)
+                ok = ((rowm[p] >> r) & (colm[p] >> s) & 1u) != 0;
+            else
                 ok = (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
+            toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + s) * 64) : kOutOfRange;
+        }
+    }
+    // The step state is wave-uniform; readfirstlane pins it to scalar
+    // registers (otherwise the compiler may keep it in vector registers and
+    // wrap every buffer load, whose soffset must be scalar, in a waterfall
+    // loop).
+    __device__ void pin() {
+        st = __builtin_amdgcn_readfirstlane(st);
+        cb = __builtin_amdgcn_readfirstlane(cb);
+        rs = __builtin_amdgcn_readfirstlane(rs);
+        r = __builtin_amdgcn_readfirstlane(r);
+        s = __builtin_amdgcn_readfirstlane(s);
+        sx = __builtin_amdgcn_readfirstlane(sx);
+        sw = __builtin_amdgcn_readfirstlane(sw);
+    }
+    __device__ void seek(const ConvArgs& a, int st0) {
+        st = st0;
+        rs = st0 / a.CB;
+        cb = st0 - rs * a.CB;
+        r = rs / a.S;
+        s = rs - r * a.S;
+        sx = cb * a.H * a.W * 64;
+        sw = (cb * a.RS + rs) * 1024;
+        pin();
+        set_tap(a);
+    }
+    __device__ void next(const ConvArgs& a) {
+        ++st;
+        if (++cb < a.CB) {
+            sx += a.H * a.W * 64;
+            sw += a.RS * 1024;
+        } else {
+            cb = 0;
+            ++rs;
+            sx = 0;
+            sw = rs * 1024;
+            if (++s == a.S) {
+                s = 0;
+                ++r;
             }
-            const float* src = a.x + (ok ? pbase[p] + dx : 0);
-            if constexpr (!SMALLC) {
-                const v4f v = *reinterpret_cast<const v4f*>(src + 4 * g);
+            pin();
+            set_tap(a);
+        }
+        pin();
+    }
+    __device__ void load(Operands<FK, FP, SMALLC>& o) const {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) o.b[p][i] = ok ? v[i] : 0.f;
-            } else {
-                const float v = src[g];
-                o.b[p] = ok ? v : 0.f;
-            }
+        for (int p = 0; p < FP; ++p) {
+            if constexpr (!SMALLC)
+                o.b[p] = ld4(xr, toff[p], sx, 0);
+            else
+                o.b[p] = ld1(xr, toff[p], sx, 0);
         }
 #pragma unroll
         for (int f = 0; f < FK; ++f) {
-            const float* wp = wbase[f] + st * 256;
-            if constexpr (!SMALLC) {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) o.a[f][t] = wp[(4 * g + t) * 16 + li];
+            if constexpr (SMALLC) {
+                o.a[f] = ld1(wr, woff[f], sw, 0);
+            } else if constexpr (WMFMA) {
+                o.a[f] = ld4(wr, woff[f], sw, 0);
             } else {
-                o.a[f] = wp[g * 16 + li];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) o.a[f][t] = ld1(wr, woff[f], sw, t * 64);
             }
         }
     }
@@ -175,38 +219,65 @@ __device__ inline void mma(const Operands<FK, FP, SMALLC>& o, v4f (&acc)[FK][FP]
     }
 }
 
-template <int FK, int FP, bool SMALLC, bool PW>
-__global__ __launch_bounds__(256) void conv2d_mfma(ConvArgs a) {
+template <int FK, int FP, bool SMALLC, bool WMFMA, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int li = lane & 15;
     const int g = lane >> 4;
-    const int m0 = blockIdx.x * (16 * FP);
-    const int kb0 = blockIdx.y * FK;
+    // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+    // L2.  Give every XCD a contiguous run of the logical order
+    // (split, channel tile, pixel tile), so the pixel tiles that share a
+    // filter slice run on one XCD and read it from that XCD's L2.
+    const int G = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    const int q = G / kXcds, rmd = G % kXcds;
+    const int u = xcd * q + min(xcd, rmd) + slot;
+    const int npx = cdiv_d(a.M, 16 * FP), nkb = cdiv_d(a.KB, FK);
+    const int pxt = u % npx;
+    const int kbt = (u / npx) % nkb;
+    const int z = u / (npx * nkb);
+    const int m0 = pxt * (16 * FP);
+    const int kb0 = kbt * FK;
     const int ohw = a.OH * a.OW;
 
-    Tile<FK, FP, SMALLC, PW> tl;
+    Loader<FK, FP, SMALLC, WMFMA> tl;
+    tl.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
+    tl.wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
+    tl.wide_taps = a.R > 32 || a.S > 32;
     bool pv[FP];
     int pn[FP];
 #pragma unroll
     for (int p = 0; p < FP; ++p) {
         const int m = m0 + 16 * p + li;
-        pv[p] = m < a.M;
+        pv[p] = m < a.M;  // lanes past the last pixel load pixel 0 and never store
         const int mm = pv[p] ? m : 0;
         const int n = mm / ohw;
         const int rem = mm - n * ohw;
         const int oh = rem / a.OW;
         pn[p] = n;
-        tl.pih[p] = oh * a.sh - a.ph;
-        tl.piw[p] = (rem - oh * a.OW) * a.sw - a.pw;
-        // address of (cb = 0, r = 0, s = 0) for this pixel; may lie outside the
-        // tensor when the tap is padding (then it is never dereferenced)
-        tl.pbase[p] = ((n * a.CB * a.H + tl.pih[p]) * a.W + tl.piw[p]) * 16;
+        const int ih0 = oh * a.sh - a.ph;
+        const int iw0 = (rem - oh * a.OW) * a.sw - a.pw;
+        tl.pih[p] = ih0;
+        tl.piw[p] = iw0;
+        unsigned rm = 0, cm = 0;
+        for (int r = 0; r < a.R && r < 32; ++r) rm |= ((unsigned)(ih0 + r) < (unsigned)a.H ? 1u : 0u) << r;
+        for (int c = 0; c < a.S && c < 32; ++c) cm |= ((unsigned)(iw0 + c) < (unsigned)a.W ? 1u : 0u) << c;
+        tl.rowm[p] = rm;
+        tl.colm[p] = cm;
+        // byte offset of this pixel's (cb = 0, r = 0, s = 0) element; only used
+        // (with a step offset added) when the tap is inside the input
+        tl.xoff[p] = ((n * a.CB * a.H + ih0) * a.W + iw0) * 64 + (SMALLC ? 4 * g : 16 * g);
     }
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
-        const int kb = kb0 + f;
-        tl.wbase[f] = a.w + (kb < a.KB ? kb : 0) * a.CB * a.RS * 256;
+        const int kb = kb0 + f < a.KB ? kb0 + f : 0;  // past K: clamped, never stored
+        int e;
+        if constexpr (SMALLC)
+            e = WMFMA ? li * 4 + g : g * 16 + li;  // channel c = g of the block
+        else
+            e = WMFMA ? (g * 16 + li) * 4 : (4 * g) * 16 + li;
+        tl.woff[f] = (unsigned)((kb * a.CB * a.RS * 256 + e) * 4);
     }
 
     v4f acc[FK][FP];
@@ -215,49 +286,39 @@ __global__ __launch_bounds__(256) void conv2d_mfma(ConvArgs a) {
 #pragma unroll
         for (int p = 0; p < FP; ++p) acc[f][p] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // this workgroup's contiguous range of reduction steps; this wave takes
-    // every 4th of them
-    const int z = blockIdx.z;
+    // this workgroup's contiguous range of reduction steps, cut into one
+    // contiguous run per wave
     const int k_lo = (int)(((long)a.T * z) / a.split);
     const int k_hi = (int)(((long)a.T * (z + 1)) / a.split);
-    const int first = k_lo + wave;
-    const int nj = first < k_hi ? (k_hi - first + kWaves - 1) / kWaves : 0;
-
-    __shared__ StepInfo tab[PW ? 1 : kMaxTableSteps];
-    const bool use_tab = !PW && k_hi - k_lo <= kMaxTableSteps;
-    if (use_tab) {
-        for (int i = threadIdx.x; i < k_hi - k_lo; i += blockDim.x) {
-            const int st = k_lo + i;
-            const int cb = st / a.RS;
-            const int rs = st - cb * a.RS;
-            const int r = rs / a.S;
-            const int sx = rs - r * a.S;
-            tab[i] = StepInfo{((cb * a.H + r) * a.W + sx) * 16, (short)r, (short)sx};
-        }
-        __syncthreads();
-    }
+    const int w_lo = k_lo + (int)(((long)(k_hi - k_lo) * wave) / WAVES);
+    const int w_hi = k_lo + (int)(((long)(k_hi - k_lo) * (wave + 1)) / WAVES);
+    const int nj = w_hi - w_lo;
 
     if (nj > 0) {
         constexpr int D = pipe_depth<FK, FP, SMALLC>();
-        const int last = first + kWaves * (nj - 1);
+        // the loader runs D - 1 steps ahead; past the wave's last step it
+        // stays there (those loads are never consumed)
+        tl.seek(a, w_lo);
         Operands<FK, FP, SMALLC> buf[D];
 #pragma unroll
-        for (int i = 0; i < D - 1; ++i) tl.load(a, tab, use_tab, k_lo, min(first + kWaves * i, last), g, li, buf[i]);
+        for (int i = 0; i < D - 1; ++i) {
+            tl.load(buf[i]);
+            if (tl.st < w_hi - 1) tl.next(a);
+        }
         for (int j0 = 0; j0 < nj; j0 += D) {
 #pragma unroll
-            for (int u = 0; u < D; ++u) {
-                const int j = j0 + u;
+            for (int uu = 0; uu < D; ++uu) {
+                const int j = j0 + uu;
                 // refill the slot consumed one step ago with step j + D - 1
-                // (past the end: the last step again, never used)
-                tl.load(a, tab, use_tab, k_lo, min(first + kWaves * (j + D - 1), last), g, li,
-                        buf[(u + D - 1) % D]);
-                if (j < nj) mma<FK, FP, SMALLC>(buf[u], acc);
+                tl.load(buf[(uu + D - 1) % D]);
+                if (tl.st < w_hi - 1) tl.next(a);
+                if (j < nj) mma<FK, FP, SMALLC>(buf[uu], acc);
             }
         }
     }
 
-    // Sum the four waves' partial tiles (fixed order: wave 0 + 1 + 2 + 3).
-    __shared__ v4f red[kWaves - 1][FK * FP][64];
+    // Sum the waves' partial tiles in wave order: 0 + 1 + 2 + ...
+    __shared__ v4f red[WAVES - 1][FK * FP][64];
     if (wave > 0) {
 #pragma unroll
         for (int f = 0; f < FK; ++f)
@@ -270,30 +331,29 @@ __global__ __launch_bounds__(256) void conv2d_mfma(ConvArgs a) {
     for (int f = 0; f < FK; ++f)
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
-            const int q = f * FP + p;
-            acc[f][p] = ((acc[f][p] + red[0][q][lane]) + red[1][q][lane]) + red[2][q][lane];
+            const int qq = f * FP + p;
+#pragma unroll
+            for (int w = 0; w < WAVES - 1; ++w) acc[f][p] += red[w][qq][lane];
         }
 
     if (a.split > 1) {
-        const int tiles = gridDim.x * gridDim.y;
-        const int tile = blockIdx.y * gridDim.x + blockIdx.x;
-        v4f* part = reinterpret_cast<v4f*>(a.ws);
+        // raw partial sums of split z, in the output's own blocked layout; the
+        // reduce kernel adds the splits in order and runs the epilogue
+        float* part = a.ws + (long)z * a.N * a.KB * ohw * 16;
 #pragma unroll
-        for (int q = 0; q < FK * FP; ++q)
-            part[((z * tiles + tile) * FK * FP + q) * 64 + lane] = acc[q / FP][q % FP];
-        __threadfence();
-        int old = 0;
-        if (lane == 0) old = atomicAdd(a.cnt + tile, 1);
-        old = __shfl(old, 0, 64);
-        if (old != a.split - 1) return;
-        __threadfence();
+        for (int f = 0; f < FK; ++f) {
+            const int kb = kb0 + f;
+            if (kb >= a.KB) continue;
 #pragma unroll
-        for (int q = 0; q < FK * FP; ++q) {
-            v4f s = part[(tile * FK * FP + q) * 64 + lane];
-            for (int zz = 1; zz < a.split; ++zz) s += part[((zz * tiles + tile) * FK * FP + q) * 64 + lane];
-            acc[q / FP][q % FP] = s;
+            for (int p = 0; p < FP; ++p) {
+                if (!pv[p]) continue;
+                const int oh = (tl.pih[p] + a.ph) / a.sh;
+                const int ow = (tl.piw[p] + a.pw) / a.sw;
+                *reinterpret_cast<v4f*>(part + (((pn[p] * a.KB + kb) * a.OH + oh) * a.OW + ow) * 16 +
+                                        4 * g) = acc[f][p];
+            }
         }
-        if (lane == 0) atomicExch(a.cnt + tile, 0);
+        return;
     }
 
 #pragma unroll
@@ -323,73 +383,123 @@ __global__ __launch_bounds__(256) void conv2d_mfma(ConvArgs a) {
     }
 }
 
-template <int FK, int FP, bool SMALLC, bool PW>
+// Second pass of a split reduction: y = act(sum_z part[z] + bias + res), the
+// splits added in order z = 0, 1, ... (deterministic).  One thread per
+// (pixel, 4-channel quad).
+__global__ __launch_bounds__(256) void split_reduce(ConvArgs a) {
+    const int ohw = a.OH * a.OW;
+    const int total = a.N * a.KB * ohw * 4;
+    const long zstride = (long)a.N * a.KB * ohw * 16;
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
+        const int qd = t & 3;
+        const int pix = t >> 2;  // (n*KB + kb)*OH*OW + oh*OW + ow
+        const int sp = pix % ohw;
+        const int nk = pix / ohw;
+        const int kb = nk % a.KB, n = nk / a.KB;
+        v4f o = *reinterpret_cast<const v4f*>(a.ws + pix * 16 + 4 * qd);
+        for (int z = 1; z < a.split; ++z)
+            o += *reinterpret_cast<const v4f*>(a.ws + z * zstride + pix * 16 + 4 * qd);
+        if (a.bias) o += *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * qd);
+        if (a.res) o += *reinterpret_cast<const v4f*>(a.res + pix * 16 + 4 * qd);
+        if (a.act == NEO_ACT_RELU) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
+        }
+        *reinterpret_cast<v4f*>(a.y + ((n * a.y_tot + a.y_off + kb) * ohw + sp) * 16 + 4 * qd) = o;
+    }
+}
+
+template <int FK, int FP, bool SMALLC, bool WMFMA, int WAVES>
 hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
-    dim3 grid(cdiv(a.M, 16 * FP), cdiv(a.KB, FK), a.split);
-    hipLaunchKernelGGL((conv2d_mfma<FK, FP, SMALLC, PW>), grid, dim3(256), 0, st, a);
+    const int wgs = cdiv(a.M, 16 * FP) * cdiv(a.KB, FK) * a.split;
+    hipLaunchKernelGGL((conv2d_mfma<FK, FP, SMALLC, WMFMA, WAVES>), dim3(wgs), dim3(WAVES * 64), 0,
+                       st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.split == 1) return e;
+    const long total = (long)a.N * a.KB * a.OH * a.OW * 4;
+    long blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(split_reduce, dim3((unsigned)blocks), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
-template <bool SMALLC, bool PW>
-hipError_t dispatch(int fk, int fp, const ConvArgs& a, hipStream_t st) {
-    switch (fk * 8 + fp) {
-        case 1 * 8 + 1: return launch_t<1, 1, SMALLC, PW>(a, st);
-        case 1 * 8 + 2: return launch_t<1, 2, SMALLC, PW>(a, st);
-        case 1 * 8 + 4: return launch_t<1, 4, SMALLC, PW>(a, st);
-        case 2 * 8 + 1: return launch_t<2, 1, SMALLC, PW>(a, st);
-        case 2 * 8 + 2: return launch_t<2, 2, SMALLC, PW>(a, st);
-        case 2 * 8 + 4: return launch_t<2, 4, SMALLC, PW>(a, st);
-        case 4 * 8 + 1: return launch_t<4, 1, SMALLC, PW>(a, st);
-        case 4 * 8 + 2: return launch_t<4, 2, SMALLC, PW>(a, st);
-        case 4 * 8 + 4: return launch_t<4, 4, SMALLC, PW>(a, st);
+// LDS for the cross-wave sum is (WAVES - 1) * FK * FP KB; the instantiated
+// combinations keep it at or below 48 KB.
+template <int FK, int FP, bool SMALLC, bool WMFMA>
+hipError_t by_waves(int waves, const ConvArgs& a, hipStream_t st) {
+    if constexpr (FK * FP <= 2) {
+        if (waves == 16) return launch_t<FK, FP, SMALLC, WMFMA, 16>(a, st);
+    }
+    if constexpr (FK * FP <= 4) {
+        if (waves == 8) return launch_t<FK, FP, SMALLC, WMFMA, 8>(a, st);
+    }
+    if (waves == 4) return launch_t<FK, FP, SMALLC, WMFMA, 4>(a, st);
+    return hipErrorInvalidValue;
+}
+
+template <bool SMALLC, bool WMFMA>
+hipError_t dispatch(const ConvConfig& c, const ConvArgs& a, hipStream_t st) {
+    switch (c.fk * 8 + c.fp) {
+        case 1 * 8 + 1: return by_waves<1, 1, SMALLC, WMFMA>(c.waves, a, st);
+        case 1 * 8 + 2: return by_waves<1, 2, SMALLC, WMFMA>(c.waves, a, st);
+        case 1 * 8 + 4: return by_waves<1, 4, SMALLC, WMFMA>(c.waves, a, st);
+        case 2 * 8 + 1: return by_waves<2, 1, SMALLC, WMFMA>(c.waves, a, st);
+        case 2 * 8 + 2: return by_waves<2, 2, SMALLC, WMFMA>(c.waves, a, st);
+        case 2 * 8 + 4: return by_waves<2, 4, SMALLC, WMFMA>(c.waves, a, st);
+        case 4 * 8 + 1: return by_waves<4, 1, SMALLC, WMFMA>(c.waves, a, st);
+        case 4 * 8 + 2: return by_waves<4, 2, SMALLC, WMFMA>(c.waves, a, st);
+        case 4 * 8 + 4: return by_waves<4, 4, SMALLC, WMFMA>(c.waves, a, st);
         default: return hipErrorInvalidValue;
     }
 }
 
 }  // namespace
 
-// Cost model for the launch configuration (FK, FP, SPLIT) of one shape.
-// Per SIMD: the MFMA cycles it must issue (padded tiles included) and the
-// serial chain of one wave (steps x (MFMA cycles + exposed load latency));
-// waves resident on a SIMD overlap each other's latency.  A split adds the
-// partial round trip through L2 and the last-arrival pass.
+bool conv_config_valid(const ConvConfig& c) {
+    const bool tile = (c.fk == 1 || c.fk == 2 || c.fk == 4) && (c.fp == 1 || c.fp == 2 || c.fp == 4);
+    const bool waves = c.waves == 4 || (c.waves == 8 && c.fk * c.fp <= 4) ||
+                       (c.waves == 16 && c.fk * c.fp <= 2);
+    return tile && waves && c.split >= 1 && c.split <= 64;
+}
+
+// Cost model for the launch configuration of one shape, in microseconds: a
+// per-launch floor, plus the longest chain of reduction steps any wave walks
+// (each step: its MFMAs, or the measured ~300-cycle bookkeeping-and-load
+// chain when a SIMD has a single wave, shared between resident waves), plus
+// the extra kernel and partial round trip of a split.
 ConvConfig choose_conv_config(const ConvShape& s) {
     const int KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
     const bool smallc = s.C <= 4;
     const int T = cdiv(s.C, 16) * s.R * s.S;
-    const double kSimds = 1024.0, kLat = 700.0, kClk = 2.4e3;  // cycles, cycles/us
-    ConvConfig best{1, 1, 1};
+    const double kClk = 2400.0;  // cycles per microsecond
+    ConvConfig best{1, 1, 1, 4};
     double best_t = 1e30;
-    static const int fks[] = {1, 2, 4}, fps[] = {1, 2, 4};
-    // A split pays a device-scope release per workgroup (the partials must be
-    // visible across XCDs, whose L2s are not coherent), which measured ~20 ns
-    // of serialized time per workgroup on MI355X: it never wins at these
-    // sizes, so the model only considers unsplit launches for now.
-    static const int splits[] = {1};
+    static const int fks[] = {1, 2, 4}, fps[] = {1, 2, 4}, wvs[] = {4, 8, 16};
+    static const int splits[] = {1, 2, 3, 4, 6, 8};
     for (int fk : fks) {
         if (fk > 1 && fk > KB) continue;
         for (int fp : fps) {
             if (fp > 1 && fp > MP) continue;
             const long tiles = (long)cdiv(MP, fp) * cdiv(KB, fk);
-            for (int sp : splits) {
-                if (sp > 1 && T / sp < 2 * kWaves) continue;
-                const long wgs = tiles * sp;
-                const double steps = std::ceil((double)T / sp / kWaves);
-                const double mfma_step = (smallc ? 1.0 : 4.0) * fk * fp * 32.0;
-                const double waves_per_simd = std::max(1.0, wgs * kWaves / kSimds);
-                const double rounds = std::ceil(waves_per_simd / 8.0);
-                const double resident = std::min(8.0, waves_per_simd);
-                // latency hidden by the prefetch ring and by other resident waves
-                const double per_step = std::max(mfma_step * resident, kLat / 4.0);
-                double t = rounds * steps * per_step / kClk;
-                t += 1.0;  // launch + epilogue
-                if (sp > 1) {
-                    const double bytes = 2.0 * sp * tiles * fk * fp * 1024.0;
-                    t += bytes / 4.0e6 + 0.8;  // ~4 TB/s L2 round trip + last-arrival pass
-                }
-                if (t < best_t * 0.98) {
-                    best_t = t;
-                    best = ConvConfig{fk, fp, sp};
+            for (int wv : wvs) {
+                for (int sp : splits) {
+                    const ConvConfig c{fk, fp, sp, wv};
+                    if (!conv_config_valid(c)) continue;
+                    if (sp > 1 && T / sp < wv) continue;
+                    const long wgs = tiles * sp;
+                    const double steps = std::ceil((double)T / sp / wv);
+                    const double waves_per_simd = (double)wgs * wv / 1024.0;
+                    const double resident = std::max(1.0, std::min(8.0, waves_per_simd));
+                    const double rounds = std::max(1.0, std::ceil(waves_per_simd / 8.0));
+                    const double mfma = (smallc ? 1.0 : 4.0) * fk * fp * 32.0;
+                    const double chain = 300.0 + 40.0 * (fk + fp);
+                    const double per_step = std::max(mfma * resident, chain);
+                    double t = 3.5 + rounds * steps * per_step / kClk;
+                    if (sp > 1) t += 2.0 + 2.0 * sp * s.N * KB * s.OH * s.OW * 64.0 / 4.0e6;
+                    if (t < best_t * 0.98) {
+                        best_t = t;
+                        best = c;
+                    }
                 }
             }
         }
@@ -399,18 +509,13 @@ ConvConfig choose_conv_config(const ConvShape& s) {
 
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c) {
     if (c.split <= 1) return 0;
-    const long tiles = (long)cdiv(cdiv(s.N * s.OH * s.OW, 16), c.fp) * cdiv(cdiv(s.K, 16), c.fk);
-    return (size_t)c.split * tiles * c.fk * c.fp * 1024;
-}
-
-size_t conv_counter_count(const ConvShape& s, const ConvConfig& c) {
-    if (c.split <= 1) return 0;
-    return (size_t)cdiv(cdiv(s.N * s.OH * s.OW, 16), c.fp) * cdiv(cdiv(s.K, 16), c.fk);
+    return (size_t)c.split * s.N * cdiv(s.K, 16) * s.OH * s.OW * 64;
 }
 
 hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
-                         const float* bias, const float* res, float* y, float* ws, int* cnt,
+                         bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st) {
+    if (!conv_config_valid(c)) return hipErrorInvalidValue;
     ConvArgs a;
     a.x = x;
     a.w = w;
@@ -418,7 +523,6 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.res = res;
     a.y = y;
     a.ws = ws;
-    a.cnt = cnt;
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.H = s.H;
@@ -438,11 +542,11 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.y_tot = s.y_tot;
     a.act = s.act;
     a.T = a.CB * a.RS;
-    a.split = (c.split > 1 && ws && cnt) ? c.split : 1;
-    const bool pw = s.R == 1 && s.S == 1 && s.ph == 0 && s.pw == 0;
-    if (s.C <= 4) return dispatch<true, false>(c.fk, c.fp, a, st);
-    if (pw) return dispatch<false, true>(c.fk, c.fp, a, st);
-    return dispatch<false, false>(c.fk, c.fp, a, st);
+    a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
+    a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 64);
+    a.w_bytes = (int)((long)a.KB * a.CB * a.RS * 1024);
+    if (wmfma) return s.C <= 4 ? dispatch<true, true>(c, a, st) : dispatch<false, true>(c, a, st);
+    return s.C <= 4 ? dispatch<true, false>(c, a, st) : dispatch<false, false>(c, a, st);
 }
 
 }  // namespace neo

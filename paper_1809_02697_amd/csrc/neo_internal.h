@@ -30,22 +30,24 @@ struct ConvShape {
 };
 
 // Launch configuration: register tile (fk channel blocks x fp pixel groups of
-// 16 per wave) and the number of workgroups the reduction is split over.
+// 16 per wave), the number of workgroups the reduction is split over, and the
+// waves per workgroup (which split each workgroup's reduction range again).
 struct ConvConfig {
-    int fk, fp, split;
+    int fk, fp, split, waves;
 };
+bool conv_config_valid(const ConvConfig& c);
 ConvConfig choose_conv_config(const ConvShape& s);
-// Workspace for a split reduction: partial tiles (bytes) and arrival counters
-// (ints, zero before the first launch; every launch leaves them zero).
+// Workspace of a split reduction (partial sums of every split), in bytes.
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);
-size_t conv_counter_count(const ConvShape& s, const ConvConfig& c);
 
-// Launch the blocked convolution.  x: NCHW16c, w: KCRS[16]c[16]k, bias:
-// [KB*16] or null, res: NCHW16c [N][KB][OH][OW][16] or null, y: NCHW16c view.
-// ws / cnt: workspace of at least conv_workspace_bytes / conv_counter_count
-// (a split is only used when both are given).
+// Launch the blocked convolution.  x: NCHW16c; w: KCRS[16]c[16]k, or with
+// wmfma the same blocks with each 16x16 block stored [c/4][k][c%4] (see
+// pack_filter_mfma_host); bias: [KB*16] or null; res: NCHW16c
+// [N][KB][OH][OW][16] or null; y: NCHW16c view.  ws: workspace of at least
+// conv_workspace_bytes (a split is only used when it is given).  x and w must
+// each be below 2 GiB.
 hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
-                         const float* bias, const float* res, float* y, float* ws, int* cnt,
+                         bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st);
 
 // ---- layout ---------------------------------------------------------------------------
@@ -75,6 +77,10 @@ void fold_bn_host(const float* w, const float* bias, const float* gamma, const f
                   const float* mean, const float* var, float eps, int K, int C, int R, int S,
                   float* w_out, float* bias_out);
 void pack_filter_host(const float* w, int K, int C, int R, int S, int ib, int ob, float* out);
+// Reorder each 16x16 block of a KCRS[16]c[16]k filter from [c][k] to
+// [c/4][k][c%4] (in place is not allowed), and back.
+void blocks_to_mfma_order(const float* in, long n_blocks, float* out);
+void blocks_from_mfma_order(const float* in, long n_blocks, float* out);
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

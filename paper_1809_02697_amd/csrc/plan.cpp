@@ -51,7 +51,7 @@ struct Step {
     int node;         // originating node (transforms: the consumer that needed it)
     int in = -1, out = -1, res = -1;
     ConvShape cs{};
-    ConvConfig cc{1, 1, 1};
+    ConvConfig cc{1, 1, 1, 4};
     PoolShape ps{};
     long w_off = -1, b_off = -1;
     int src_block = 0, dst_block = 0;
@@ -93,9 +93,8 @@ struct neo_plan {
     float* d_params = nullptr;
     char* d_act = nullptr;
     // split-reduction workspace shared by the conv steps (they run in order)
-    size_t ws_bytes = 0, cnt_n = 0;
+    size_t ws_bytes = 0;
     float* d_ws = nullptr;
-    int* d_cnt = nullptr;
     int out_val = -1;
     int out_dims[4] = {0, 0, 0, 0};
     int input_val = -1;
@@ -308,15 +307,18 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                         has_b = true;
                     }
                 }
-                std::vector<float> wp((long)cdiv(d.K, 16) * cdiv(C, 16) * d.R * d.S * 256);
+                const long nblk = (long)cdiv(d.K, 16) * cdiv(C, 16) * d.R * d.S;
+                std::vector<float> wp(nblk * 256), wm(nblk * 256);
                 pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
-                st.w_off = add_params(P, wp);
+                blocks_to_mfma_order(wp.data(), nblk, wm.data());  // one float4 per lane
+                st.w_off = add_params(P, wm);
+                if (nblk * 256 >= (1L << 29) || (long)ni.N * cdiv(C, 16) * a->H * a->W * 16 >= (1L << 29))
+                    return fail(NEO_ERR_UNSUPPORTED, where + "input or filter of 2 GiB or more");
                 if (has_b) st.b_off = add_params(P, b);
                 st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
                                   d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
                 st.cc = choose_conv_config(st.cs);
                 P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.cc));
-                P->cnt_n = std::max(P->cnt_n, conv_counter_count(st.cs, st.cc));
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
                 st.out = v;
                 P->steps.push_back(st);
@@ -580,7 +582,8 @@ std::string describe(const neo_plan* P) {
               << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
               << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
-              << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split << "}";
+              << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
+              << ",\"waves\":" << s.cc.waves << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
@@ -639,13 +642,10 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         }
         e = hipMemcpy(P->d_params, P->params.data(), P->params.size() * 4, hipMemcpyHostToDevice);
         if (e == hipSuccess && P->ws_bytes) e = hipMalloc(&P->d_ws, P->ws_bytes);
-        if (e == hipSuccess && P->cnt_n) e = hipMalloc(&P->d_cnt, P->cnt_n * sizeof(int));
-        if (e == hipSuccess && P->cnt_n) e = hipMemset(P->d_cnt, 0, P->cnt_n * sizeof(int));
         if (e != hipSuccess) {
             (void)hipFree(P->d_params);
             (void)hipFree(P->d_act);
             if (P->d_ws) (void)hipFree(P->d_ws);
-            if (P->d_cnt) (void)hipFree(P->d_cnt);
             delete P;
             return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: workspace")
                                             : hip_fail(e, "neo_plan_create: parameter upload");
@@ -681,8 +681,8 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
     if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_conv_params: not a live plan");
     for (const Step& s : plan->steps) {
         if (s.kind != ST_CONV || s.node != node_id) continue;
-        const long wn = (long)cdiv(s.cs.K, 16) * cdiv(s.cs.C, 16) * s.cs.R * s.cs.S * 256;
-        if (w_packed) std::copy(plan->params.begin() + s.w_off, plan->params.begin() + s.w_off + wn, w_packed);
+        const long nblk = (long)cdiv(s.cs.K, 16) * cdiv(s.cs.C, 16) * s.cs.R * s.cs.S;
+        if (w_packed) blocks_from_mfma_order(plan->params.data() + s.w_off, nblk, w_packed);
         if (bias) {
             const long bn = (long)cdiv(s.cs.K, 16) * 16;
             if (s.b_off >= 0)
@@ -710,10 +710,10 @@ static int enqueue_steps(neo_plan* P, const float* x_nchw, float* y_out, hipStre
                 break;
             }
             case ST_CONV:
-                e = launch_conv2d(s.cs, s.cc, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off,
+                e = launch_conv2d(s.cs, s.cc, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off, true,
                                   s.b_off >= 0 ? prm + s.b_off : nullptr,
                                   s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
-                                  val_ptr(P, s.out, x_nchw, y_out), P->d_ws, P->d_cnt, st);
+                                  val_ptr(P, s.out, x_nchw, y_out), P->d_ws, st);
                 break;
             case ST_MAXPOOL:
                 e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
@@ -812,7 +812,6 @@ void neo_plan_destroy(neo_plan* plan) {
         (void)hipFree(plan->d_params);
         (void)hipFree(plan->d_act);
         if (plan->d_ws) (void)hipFree(plan->d_ws);
-        if (plan->d_cnt) (void)hipFree(plan->d_cnt);
     }
     delete plan;
 }

@@ -210,15 +210,16 @@ def test_dense(neo, N, IN, OUT, act):
     assert_close(y, ref, "dense")
 
 
-CONFIGS = [(fk, fp, sp) for fk in (1, 2, 4) for fp in (1, 2, 4) for sp in (1, 3, 8)]
+CONFIGS = [(fk, fp, sp, wv) for fk in (1, 2, 4) for fp in (1, 2, 4) for wv in (4, 8, 16)
+           for sp in (1, 3) if wv == 4 or (wv == 8 and fk * fp <= 4) or (wv == 16 and fk * fp <= 2)]
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=[f"fk{c[0]}fp{c[1]}s{c[2]}" for c in CONFIGS])
+@pytest.mark.parametrize("cfg", CONFIGS, ids=[f"fk{c[0]}fp{c[1]}s{c[2]}w{c[3]}" for c in CONFIGS])
 def test_conv_every_launch_config(neo, cfg, monkeypatch):
-    """Every register tile and reduction split (forced through the tuning
-    override) on ragged shapes: odd K, M not a multiple of the tile, C with a
-    padded block, and the small-C path."""
-    monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d" % cfg)
+    """Every register tile, waves per workgroup and reduction split (forced
+    through the tuning override) on ragged shapes: odd K, M not a multiple of
+    the tile, C with a padded block, and the small-C path."""
+    monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d,%d" % cfg)
     for (C, K, R, st, pd, H, N, epi) in [(40, 72, 3, 1, 1, 11, 2, "res"),
                                          (3, 24, 3, 2, 1, 17, 1, "relu"),
                                          (130, 20, 1, 1, 0, 5, 3, "none")]:
