@@ -1,21 +1,24 @@
 """Benchmark: ResNet-50 batch-1 fp32 inference through the blocked-layout plan.
 
 One step = one forward pass of ResNet-50 (224x224, batch 1) through
-``neo_run_graph``: the entry layout transform, 53 blocked convolutions with
-their fused epilogues, max pool, global average pool, the exit transform
-(aliased) and the dense layer.  Input and parameters are resident in HBM
-before the timed region.
+``neo_run_graph`` on a tuned plan replayed as a HIP graph: the entry layout
+transform, 53 blocked convolutions with their fused epilogues, max pool,
+global average pool, the exit transform (aliased) and the dense layer.  Input,
+output and parameters are resident in HBM before the timed region.
 
-Printed JSON line (rank 0, one line):
-  value      conv TFLOP/s over the whole step (8.174 GFLOP of convolution per
-             image / step time); ``latency_ms`` is the step time itself
-  roofline   the dominant kernel (conv2d_blocked): algorithmic FLOPs per
-             launch / average launch duration, measured with HIP events on the
-             launch stream over the 23 distinct ResNet-50 layers weighted by
-             their use count (53 launches per forward)
-  layers     the per-layer sweep (TFLOP/s, algorithmic GB/s, % of the binding
-             roofline)
-  cpu_baseline  the CPU oracle timed on this host on a bounded sample
+Printed JSON line:
+  value        conv TFLOP/s over the whole step (8.174 GFLOP of convolution
+               per image / step time); ``latency_ms`` is the step time
+  roofline     the dominant kernel, conv2d_blocked: algorithmic FLOPs per
+               launch / average launch duration, the duration measured with
+               HIP events around graph replays of each conv step of the plan
+               (repeated back-to-back launches on the plan's stream)
+  layers       per distinct conv shape: us, TFLOP/s, algorithmic GB/s, % of
+               the binding roofline, and the launch configuration
+  models       end-to-end latency of ResNet-50 / VGG-16 / Inception-v3 at
+               batch 1 and ResNet-50 at batch 32, and the transform-elimination
+               ablation (a plan that transforms around every blocked operation)
+  cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
 import argparse
 import json
@@ -45,92 +48,129 @@ def conv_costs(C, K, R, S, H, W, st, pd, N=1, residual=False):
     return flops, nbytes, OH, OW
 
 
-def build_plan_inputs(neo, torch, flags=0):
-    from paper_1809_02697_amd import workloads as wl
-    g = wl.resnet50(1)
-    plan = neo.Plan(g, flags=flags)
-    x = torch.from_numpy(g.x).cuda()
-    out = torch.empty((1, 1000), device="cuda")
-    flops = 0
-    d = plan.describe()
-    for s in d["steps"]:
+def plan_conv_flops(desc):
+    tot = 0
+    for s in desc["steps"]:
         if s["kind"] == "conv":
             c = s["conv"]
-            flops += conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"],
-                                c["pad"])[0]
-    return g, plan, x, out, flops
+            tot += conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"], c["pad"],
+                              N=c["N"])[0]
+    return tot
 
 
-def layer_sweep(neo, torch, reps):
-    """Config 2: the 23 distinct ResNet-50 layers, each timed alone with HIP
-    events around every launch (torch events on the launch stream)."""
-    from paper_1809_02697_amd import workloads as wl
-    rows = []
+def time_graph(torch, fn, reps, rounds=3):
+    """Average time of fn() over `reps` back-to-back launches captured in one
+    graph, best of `rounds` replays, HIP events on the replay stream (us)."""
+    cap = torch.cuda.Stream()
+    with torch.cuda.stream(cap):
+        fn()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=cap):
+        for _ in range(reps):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    for c in wl.resnet50_layer_sweep(1):
-        w, b = neo.fold_bn(c.w, c.bias, c.bn["gamma"], c.bn["beta"], c.bn["mean"], c.bn["var"],
-                           c.bn["eps"])
-        bpad = np.zeros(neo.cblocks(c.K) * 16, np.float32)
-        bpad[:c.K] = b
-        wp = neo.pack_filter(torch.from_numpy(w).cuda())
-        bias = torch.from_numpy(bpad).cuda()
-        xb = neo.to_blocked(torch.from_numpy(c.x).cuda())
-        res = neo.to_blocked(torch.from_numpy(c.residual).cuda()) if c.epilogue == "res" else None
-        act = "none" if c.epilogue == "none" else "relu"
-        flops, nbytes, OH, OW = conv_costs(c.C, c.K, c.R, c.S, c.H, c.W, c.stride, c.pad,
-                                           residual=res is not None)
-        y = torch.empty((1, neo.cblocks(c.K), OH, OW, 16), device="cuda")
-
-        def launch():
-            neo.conv2d_blocked(xb, c.C, wp, c.K, c.R, c.S, bias=bias, stride=c.stride,
-                               pad=c.pad, act=act, residual=res, out=y)
-
-        # `reps` back-to-back launches captured in one graph, so host launch
-        # cost never shows between kernels; HIP events on the launch stream
-        # bracket each replay.  Warm up on the capture stream first: the
-        # library sizes its per-stream split workspace there, outside capture.
-        cap = torch.cuda.Stream()
-        with torch.cuda.stream(cap):
-            for _ in range(3):
-                launch()
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=cap):
-            for _ in range(reps):
-                launch()
+    best = 1e30
+    for _ in range(rounds):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         graph.replay()
+        e1.record(stream)
         torch.cuda.synchronize()
-        t = []
-        for _ in range(3):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            graph.replay()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            t.append(e0.elapsed_time(e1) * 1e3 / reps)
-        t = np.array(t)
-        us = float(np.mean(t))
-        del graph
-        tf = flops / (us * 1e-6) / 1e12
-        gbs = nbytes / (us * 1e-6) / 1e9
-        ai = flops / nbytes
+        best = min(best, e0.elapsed_time(e1) * 1e3 / reps)
+    del graph
+    return best
+
+
+def e2e_ms(torch, plan, x, out, steps, warmup):
+    for _ in range(warmup):
+        plan.run(x, out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        plan.run(x, out)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def layer_table(torch, plan, x, out, reps):
+    """Each conv step of the plan timed alone (its kernel(s) as the plan
+    launches them), grouped by distinct shape."""
+    d = plan.describe()
+    plan.run(x, out)      # intermediate buffers hold real activations
+    torch.cuda.synchronize()
+    rows = {}
+    for i, s in enumerate(d["steps"]):
+        if s["kind"] != "conv":
+            continue
+        c = s["conv"]
+        key = (c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"], c["W"],
+               c["N"])
+        us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
+        if key in rows:
+            rows[key]["uses"] += 1
+            rows[key]["_t"].append(us)
+            continue
+        flops, nbytes, OH, OW = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"],
+                                           c["stride"], c["pad"], N=c["N"], residual=s["res"] >= 0)
+        rows[key] = dict(shape=f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} "
+                               f"{c['H']}->{OH}", uses=1, flops=flops, bytes=nbytes,
+                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"]), _t=[us])
+    out_rows = []
+    for r in rows.values():
+        us = float(np.mean(r.pop("_t")))
+        tf = r["flops"] / (us * 1e-6) / 1e12
+        gbs = r["bytes"] / (us * 1e-6) / 1e9
+        ai = r["flops"] / r["bytes"]
         roof = min(PEAK_FP32_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
-        rows.append(dict(id=c.id, shape=f"{c.C}->{c.K} {c.R}x{c.S}/s{c.stride[0]} {c.H}->{OH}",
-                         uses=c.uses, us=round(us, 2), us_min=round(float(t.min()), 2),
-                         gflop=round(flops / 1e9, 4), tflops=round(tf, 2),
-                         alg_gbs=round(gbs, 1),
-                         bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_FP32_TFLOPS else "hbm",
-                         pct_mfma=round(100 * tf / PEAK_FP32_TFLOPS, 1),
-                         pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1),
-                         pct_roof=round(100 * tf / roof, 1)))
-    return rows
+        r.update(us=round(us, 2), gflop=round(r["flops"] / 1e9, 4), tflops=round(tf, 2),
+                 alg_gbs=round(gbs, 1),
+                 bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_FP32_TFLOPS else "hbm",
+                 pct_mfma=round(100 * tf / PEAK_FP32_TFLOPS, 1),
+                 pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1))
+        out_rows.append(r)
+    return out_rows
+
+
+def model_latencies(neo, torch, wl, steps):
+    """End-to-end latency of each model (tuned, graph replay) and the
+    transform-elimination ablation at batch 1."""
+    res = {}
+    for name, builder, batch in [("resnet50", wl.resnet50, 1), ("vgg16", wl.vgg16, 1),
+                                 ("inception_v3", wl.inception_v3, 1), ("resnet50", wl.resnet50, 32)]:
+        g = builder(batch)
+        x = torch.from_numpy(g.x).cuda()
+        entry = {}
+        for label, flags in [("eliminated", 0), ("naive", neo.PLAN_NAIVE)]:
+            if batch > 1 and label == "naive":
+                continue
+            p = neo.Plan(g, flags=flags | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+            out = p.run(x)
+            ms = e2e_ms(torch, p, x, out, steps, 3)
+            d = p.describe()
+            entry[label] = dict(ms=round(ms, 4), n_transforms=d["n_transforms"],
+                                launches=len(d["steps"]))
+            if label == "eliminated":
+                flops = plan_conv_flops(d)
+                entry["conv_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
+                entry["images_per_s"] = round(batch / (ms * 1e-3), 1)
+            p.destroy()
+        if "naive" in entry:
+            entry["elimination_speedup"] = round(entry["naive"]["ms"] / entry["eliminated"]["ms"], 3)
+        res[f"{name}_b{batch}"] = entry
+        del g, x
+        print(f"[bench] {name} b{batch}: {entry}", file=sys.stderr, flush=True)
+    return res
 
 
 def cpu_baseline(g, budget_s=12.0):
     """The oracle (plain C direct convolution, OpenMP on all host cores) on
     whole ResNet-50 batch-1 forwards until ~budget_s of work."""
     import oracle
-    from paper_1809_02697_amd import workloads as wl  # noqa: F401
     flops = 8_174_272_512
     n = 0
     t0 = time.perf_counter()
@@ -151,9 +191,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--layer-reps", type=int, default=50)
+    ap.add_argument("--layer-reps", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-layers", action="store_true", help="skip the per-layer sweep")
+    ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
+    ap.add_argument("--no-models", action="store_true", help="skip the other models and ablation")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the batch-1 path has no cross-GPU work "
@@ -162,52 +203,42 @@ def main():
 
     import torch
     from paper_1809_02697_amd import neo
+    from paper_1809_02697_amd import workloads as wl
     neo.lib()
     assert torch.cuda.is_available(), "no GPU"
-    g, plan, x, out, conv_flops = build_plan_inputs(neo, torch, neo.PLAN_HIPGRAPH)
-    print(f"[bench] plan built: {len(plan.describe()['steps'])} steps", file=sys.stderr, flush=True)
 
-    for _ in range(args.warmup):
-        plan.run(x, out)
-    torch.cuda.synchronize()
+    g = wl.resnet50(1)
     t0 = time.perf_counter()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    for _ in range(args.steps):
-        plan.run(x, out)
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    print(f"[bench] e2e {ms:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})", file=sys.stderr,
-          flush=True)
-    # the same plan launched step by step from the host, for reference
-    eager = neo.Plan(g)
-    for _ in range(3):
-        eager.run(x, out)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        eager.run(x, out)
-    ev1.record()
-    torch.cuda.synchronize()
-    ms_eager = ev0.elapsed_time(ev1) / args.steps
-    eager.destroy()
+    plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+    t_plan = time.perf_counter() - t0
+    x = torch.from_numpy(g.x).cuda()
+    out = torch.empty((1, 1000), device="cuda")
+    desc = plan.describe()
+    conv_flops = plan_conv_flops(desc)
+    print(f"[bench] plan built and tuned in {t_plan:.1f} s: {len(desc['steps'])} steps",
+          file=sys.stderr, flush=True)
+
+    ms = e2e_ms(torch, plan, x, out, args.steps, args.warmup)
+    print(f"[bench] e2e {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     layers, roofline = None, None
     if not args.no_layers:
-        layers = layer_sweep(neo, torch, args.layer_reps)
-        tot_f = sum(r["gflop"] * 1e9 * r["uses"] for r in layers)
+        layers = layer_table(torch, plan, x, out, args.layer_reps)
+        tot_f = sum(r["flops"] * r["uses"] for r in layers)
         tot_t = sum(r["us"] * 1e-6 * r["uses"] for r in layers)
         n_launch = sum(r["uses"] for r in layers)
-        achieved = (tot_f / n_launch) / (tot_t / n_launch) / 1e12
+        achieved = tot_f / tot_t / 1e12
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
                         unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4), traffic=None,
                         kernel="conv2d_blocked", launches_per_step=n_launch,
                         avg_launch_us=round(tot_t / n_launch * 1e6, 2),
                         flop_per_launch=round(tot_f / n_launch))
-        print(f"[bench] conv sweep: {achieved:.2f} TFLOP/s over {n_launch} launches",
+        for r in layers:
+            del r["flops"], r["bytes"]
+        print(f"[bench] conv layers: {achieved:.2f} TFLOP/s over {n_launch} launches",
               file=sys.stderr, flush=True)
+
+    models = None if args.no_models else model_latencies(neo, torch, wl, 20)
 
     cpu = None
     if not args.no_cpu:
@@ -224,19 +255,20 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "latency_ms": round(ms, 4),
-        "latency_ms_eager_launch": round(ms_eager, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "fp32",
         "data": "synthetic",
         "config": {"workload": "ResNet-50 forward, batch 1, 3x224x224 fp32, NCHW16c plan "
-                               "(1 transform in, 1 out), seed 2; hipGraph replay",
+                               "(1 transform in, 1 out), tuned, hipGraph replay, seed 2",
                    "global_batch": 1, "conv_gflop_per_step": round(conv_flops / 1e9, 4),
-                   "cache": "warm (working set resident in the 256 MB MALL)"},
+                   "cache": "warm (working set resident in the 256 MB MALL)",
+                   "plan_build_s": round(t_plan, 2)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layers": layers,
+        "models": models,
     }
     print(json.dumps(rec))
     plan.destroy()

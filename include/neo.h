@@ -203,7 +203,12 @@ enum neo_plan_flags {
      * private stream of the plan) at the first run and again whenever x_nchw
      * or y_out differ from the previous run; a replay is one hipGraphLaunch on
      * the caller's stream.  Results are bit-identical to eager runs. */
-    NEO_PLAN_HIPGRAPH = 4
+    NEO_PLAN_HIPGRAPH = 4,
+    /* Local search (Section 3.3.1): at plan creation, time every candidate
+     * launch configuration of each convolution workload not yet in the
+     * results database on this GPU and keep the fastest (see neo_tune_db_*).
+     * Untuned workloads use a cost model.  Needs a device plan. */
+    NEO_PLAN_TUNE = 8
 };
 
 /*
@@ -242,9 +247,28 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
  */
 int neo_run_graph(neo_plan* plan, const float* x_nchw, float* y_out, neo_stream_t stream);
 
+/* Run step `step` (0 <= step < number of steps in neo_plan_describe) of the
+ * launch list alone, with the same arguments as neo_run_graph; the steps
+ * before it must have run for its input to be meaningful.  For timing single
+ * layers as the plan launches them. */
+int neo_run_step(neo_plan* plan, int step, const float* x_nchw, float* y_out, neo_stream_t stream);
+
 /* Free the plan and its device memory (synchronizes the device first).
  * NULL is ignored.  Later use of the handle returns NEO_ERR_STATE. */
 void neo_plan_destroy(neo_plan* plan);
+
+/* ------------------------------------------------------------------------------------ */
+/* Results database of the local search (Section 3.3.1: results are kept per workload    */
+/* and processor type so that a workload is searched once)                               */
+/* ------------------------------------------------------------------------------------ */
+/* Process-wide table: (GPU architecture, N, C, H, W, K, R, S, strides, pads, filter
+ * order) -> launch configuration and its measured time.  Text file, one workload per
+ * line.  save returns the number of entries written, load the number read (entries
+ * are merged; a malformed line fails the whole load with NEO_ERR_INVALID_ARG). */
+int neo_tune_db_save(const char* path);
+int neo_tune_db_load(const char* path);
+void neo_tune_db_clear(void);
+int neo_tune_db_size(void);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* neo_last_error(void);

@@ -184,6 +184,7 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
     ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
                 y_cblk_offset, y_cblk_total, act};
     ConvConfig cfg = choose_conv_config(s);
+    (void)tuned_config(s, false, &cfg);
     env_config(&cfg);
     const int T = cdiv(C, 16) * R * S;
     if (cfg.split > T) cfg.split = T;

@@ -52,6 +52,25 @@ namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
+// Division by a runtime constant d >= 1 for dividends below 2^31, as a
+// multiply-high and a shift (Granlund and Montgomery's round-up method,
+// Hacker's Delight 10-9): s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1,
+// n / d = (mulhi(n, m) + n) >> s.  The parameters are computed on the host.
+struct FastDiv {
+    unsigned d, m, s;
+};
+
+FastDiv make_fastdiv(unsigned d) {
+    unsigned s = 0;
+    while ((1ull << s) < d) ++s;
+    const unsigned long long m = ((1ull << 32) * ((1ull << s) - d)) / d + 1;
+    return FastDiv{d, (unsigned)m, s};
+}
+
+__device__ inline int fdiv(int n, const FastDiv& f) {
+    return (int)((__umulhi((unsigned)n, f.m) + (unsigned)n) >> f.s);
+}
+
 struct ConvArgs {
     const float* x;
     const float* w;
@@ -61,6 +80,7 @@ struct ConvArgs {
     float* ws;  // split partials [SPLIT][N][KB][OH][OW][16]
     int N, CB, H, W, KB, R, S, RS, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
     int x_bytes, w_bytes;
+    FastDiv div_ohw, div_ow, div_npx, div_nkb;
 };
 
 constexpr int kXcds = 8;
@@ -82,7 +102,15 @@ struct Operands<FK, FP, true> {
     float a[FK];
 };
 
-__device__ inline int cdiv_d(int a, int b) { return (a + b - 1) / b; }
+// Bits [max(lo, 0), min(hi, n, 32)) set.
+__device__ inline unsigned run_mask(int lo, int hi, int n) {
+    lo = lo < 0 ? 0 : lo;
+    hi = hi > n ? n : hi;
+    hi = hi > 32 ? 32 : hi;
+    if (hi <= lo) return 0u;
+    const unsigned top = hi >= 32 ? 0xffffffffu : ((1u << hi) - 1u);
+    return top & ~((1u << lo) - 1u);
+}
 
 __device__ inline v4f ld4(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, int imm) {
     return __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, voff + imm, soff, 0));
@@ -233,10 +261,11 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
     const int q = G / kXcds, rmd = G % kXcds;
     const int u = xcd * q + min(xcd, rmd) + slot;
-    const int npx = cdiv_d(a.M, 16 * FP), nkb = cdiv_d(a.KB, FK);
-    const int pxt = u % npx;
-    const int kbt = (u / npx) % nkb;
-    const int z = u / (npx * nkb);
+    const int npx = a.div_npx.d, nkb = a.div_nkb.d;
+    const int u_px = fdiv(u, a.div_npx);
+    const int pxt = u - u_px * npx;
+    const int z = fdiv(u_px, a.div_nkb);
+    const int kbt = u_px - z * nkb;
     const int m0 = pxt * (16 * FP);
     const int kb0 = kbt * FK;
     const int ohw = a.OH * a.OW;
@@ -252,19 +281,17 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
         const int m = m0 + 16 * p + li;
         pv[p] = m < a.M;  // lanes past the last pixel load pixel 0 and never store
         const int mm = pv[p] ? m : 0;
-        const int n = mm / ohw;
+        const int n = fdiv(mm, a.div_ohw);
         const int rem = mm - n * ohw;
-        const int oh = rem / a.OW;
+        const int oh = fdiv(rem, a.div_ow);
         pn[p] = n;
         const int ih0 = oh * a.sh - a.ph;
         const int iw0 = (rem - oh * a.OW) * a.sw - a.pw;
         tl.pih[p] = ih0;
         tl.piw[p] = iw0;
-        unsigned rm = 0, cm = 0;
-        for (int r = 0; r < a.R && r < 32; ++r) rm |= ((unsigned)(ih0 + r) < (unsigned)a.H ? 1u : 0u) << r;
-        for (int c = 0; c < a.S && c < 32; ++c) cm |= ((unsigned)(iw0 + c) < (unsigned)a.W ? 1u : 0u) << c;
-        tl.rowm[p] = rm;
-        tl.colm[p] = cm;
+        // taps r with 0 <= ih0 + r < H form the run [-ih0, H - ih0) of [0, R)
+        tl.rowm[p] = run_mask(-ih0, a.H - ih0, a.R);
+        tl.colm[p] = run_mask(-iw0, a.W - iw0, a.S);
         // byte offset of this pixel's (cb = 0, r = 0, s = 0) element; only used
         // (with a step offset added) when the tap is inside the input
         tl.xoff[p] = ((n * a.CB * a.H + ih0) * a.W + iw0) * 64 + (SMALLC ? 4 * g : 16 * g);
@@ -285,6 +312,29 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     for (int f = 0; f < FK; ++f)
 #pragma unroll
         for (int p = 0; p < FP; ++p) acc[f][p] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // The epilogue's bias and residual reads are issued now, by the wave that
+    // runs the epilogue, so their latency hides under the reduction.
+    constexpr bool kPrefetch = FK * FP <= 4;
+    v4f pre_b[kPrefetch ? FK : 1], pre_r[kPrefetch ? FK : 1][kPrefetch ? FP : 1];
+    if constexpr (kPrefetch) {
+        if (wave == 0 && a.split == 1) {
+#pragma unroll
+            for (int f = 0; f < FK; ++f) {
+                const int kb = kb0 + f < a.KB ? kb0 + f : 0;
+                pre_b[f] = a.bias ? *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g)
+                                  : v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int p = 0; p < FP; ++p) {
+                    const int oh = (tl.pih[p] + a.ph) / a.sh;
+                    const int ow = (tl.piw[p] + a.pw) / a.sw;
+                    pre_r[f][p] = a.res ? *reinterpret_cast<const v4f*>(
+                                              a.res + (((pn[p] * a.KB + kb) * a.OH + oh) * a.OW + ow) * 16 + 4 * g)
+                                        : v4f{0.f, 0.f, 0.f, 0.f};
+                }
+            }
+        }
+    }
 
     // this workgroup's contiguous range of reduction steps, cut into one
     // contiguous run per wave
@@ -361,7 +411,10 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
         const int kb = kb0 + f;
         if (kb >= a.KB) continue;
         v4f bb = v4f{0.f, 0.f, 0.f, 0.f};
-        if (a.bias) bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
+        if constexpr (kPrefetch)
+            bb = pre_b[f];
+        else if (a.bias)
+            bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
             if (!pv[p]) continue;
@@ -369,7 +422,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
             const int oh = (tl.pih[p] + a.ph) / a.sh;
             const int ow = (tl.piw[p] + a.pw) / a.sw;
             v4f o = acc[f][p] + bb;
-            if (a.res) {
+            if constexpr (kPrefetch) {
+                o += pre_r[f][p];
+            } else if (a.res) {
                 o += *reinterpret_cast<const v4f*>(
                     a.res + (((n * a.KB + kb) * a.OH + oh) * a.OW + ow) * 16 + 4 * g);
             }
@@ -545,6 +600,10 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
     a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 64);
     a.w_bytes = (int)((long)a.KB * a.CB * a.RS * 1024);
+    a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
+    a.div_ow = make_fastdiv((unsigned)s.OW);
+    a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
+    a.div_nkb = make_fastdiv((unsigned)cdiv(a.KB, c.fk));
     if (wmfma) return s.C <= 4 ? dispatch<true, true>(c, a, st) : dispatch<false, true>(c, a, st);
     return s.C <= 4 ? dispatch<true, false>(c, a, st) : dispatch<false, false>(c, a, st);
 }

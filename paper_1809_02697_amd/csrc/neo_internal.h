@@ -50,6 +50,12 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st);
 
+// Local search (tune.cpp): the database's configuration for a shape, if any;
+// and a search that times every candidate with the given buffers on `st`.
+bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out);
+int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
+              const float* res, float* y, hipStream_t st, ConvConfig* best);
+
 // ---- layout ---------------------------------------------------------------------------
 // dst_off / dst_tot: destination channel view in destination units (channels
 // for the default layout, blocks for a blocked one), so a transform can write

@@ -52,6 +52,7 @@ struct Step {
     int in = -1, out = -1, res = -1;
     ConvShape cs{};
     ConvConfig cc{1, 1, 1, 4};
+    bool tuned = false;
     PoolShape ps{};
     long w_off = -1, b_off = -1;
     int src_block = 0, dst_block = 0;
@@ -104,6 +105,8 @@ struct neo_plan {
     const float* graph_x = nullptr;
     float* graph_y = nullptr;
 };
+
+static int tune_plan(neo_plan* P);
 
 namespace {
 
@@ -318,7 +321,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
                                   d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
                 st.cc = choose_conv_config(st.cs);
-                P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.cc));
+                if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
                 st.out = v;
                 P->steps.push_back(st);
@@ -583,7 +586,7 @@ std::string describe(const neo_plan* P) {
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
               << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
               << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
-              << ",\"waves\":" << s.cc.waves << "}";
+              << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false") << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
@@ -608,8 +611,10 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: non-positive input shape");
     if (block != 16) return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16");
-    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH))
+    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
+    if ((flags & NEO_PLAN_TUNE) && (flags & NEO_PLAN_HOST_ONLY))
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning needs a device plan");
     neo_plan* P = new (std::nothrow) neo_plan();
     if (!P) return fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     P->flags = flags;
@@ -641,14 +646,31 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                                             : hip_fail(e, "neo_plan_create: hipMalloc");
         }
         e = hipMemcpy(P->d_params, P->params.data(), P->params.size() * 4, hipMemcpyHostToDevice);
-        if (e == hipSuccess && P->ws_bytes) e = hipMalloc(&P->d_ws, P->ws_bytes);
         if (e != hipSuccess) {
             (void)hipFree(P->d_params);
             (void)hipFree(P->d_act);
-            if (P->d_ws) (void)hipFree(P->d_ws);
             delete P;
-            return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: workspace")
-                                            : hip_fail(e, "neo_plan_create: parameter upload");
+            return hip_fail(e, "neo_plan_create: parameter upload");
+        }
+        if (flags & NEO_PLAN_TUNE) {
+            const int trc = tune_plan(P);
+            if (trc != NEO_OK) {
+                (void)hipFree(P->d_params);
+                (void)hipFree(P->d_act);
+                if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
+                delete P;
+                return trc;
+            }
+        }
+        for (const Step& st : P->steps)
+            if (st.kind == ST_CONV) P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.cc));
+        if (P->ws_bytes) e = hipMalloc(&P->d_ws, P->ws_bytes);
+        if (e != hipSuccess) {
+            (void)hipFree(P->d_params);
+            (void)hipFree(P->d_act);
+            if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
+            delete P;
+            return fail(NEO_ERR_OOM, "neo_plan_create: workspace");
         }
     }
     {
@@ -695,8 +717,9 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
     return fail(NEO_ERR_INVALID_ARG, "neo_plan_conv_params: node is not a conv of this plan");
 }
 
-static int enqueue_steps(neo_plan* P, const float* x_nchw, float* y_out, hipStream_t st) {
-    for (const Step& s : P->steps) {
+static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* y_out,
+                        hipStream_t st) {
+    {
         hipError_t e = hipSuccess;
         const float* prm = P->d_params;
         switch (s.kind) {
@@ -745,6 +768,46 @@ static int enqueue_steps(neo_plan* P, const float* x_nchw, float* y_out, hipStre
         if (e != hipSuccess) return hip_fail(e, "neo_run_graph: launch");
     }
     return NEO_OK;
+}
+
+static int enqueue_steps(neo_plan* P, const float* x_nchw, float* y_out, hipStream_t st) {
+    for (const Step& s : P->steps) {
+        const int rc = enqueue_step(P, s, x_nchw, y_out, st);
+        if (rc != NEO_OK) return rc;
+    }
+    return NEO_OK;
+}
+
+// Local search for every conv step (NEO_PLAN_TUNE), with the plan's own
+// buffers, on its private stream; then size the split workspace for the
+// chosen configurations.
+static int tune_plan(neo_plan* P) {
+    hipError_t e;
+    if (!P->cap_stream) {
+        e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "neo_plan_create: tuning stream");
+    }
+    // stand-in input / output of the network's shapes (contents do not matter)
+    const Val& in = P->vals[P->input_val];
+    const Val& out = P->vals[P->out_val];
+    float *xin = nullptr, *yout = nullptr;
+    e = hipMalloc(&xin, std::max<size_t>((size_t)in.N * in.C * in.H * in.W * 4, 256));
+    if (e == hipSuccess) e = hipMalloc(&yout, std::max<size_t>((size_t)out.N * out.C * out.H * out.W * 4, 256));
+    if (e == hipSuccess) e = hipMemset(xin, 0, (size_t)in.N * in.C * in.H * in.W * 4);
+    int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: tuning buffers");
+    for (Step& s : P->steps) {
+        if (rc != NEO_OK) break;
+        if (s.kind != ST_CONV || s.tuned) continue;
+        const float* prm = P->d_params;
+        rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
+                       s.b_off >= 0 ? prm + s.b_off : nullptr,
+                       s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
+                       val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc);
+        s.tuned = rc == NEO_OK;
+    }
+    if (xin) (void)hipFree(xin);
+    if (yout) (void)hipFree(yout);
+    return rc;
 }
 
 static void drop_graph(neo_plan* P) {
@@ -797,6 +860,17 @@ int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t s
     }
     hipError_t e = hipGraphLaunch(P->graph_exec, st);
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_run_graph: graph launch");
+}
+
+int neo_run_step(neo_plan* P, int step, const float* x_nchw, float* y_out, neo_stream_t stream) {
+    if (!live(P)) return fail(NEO_ERR_STATE, "neo_run_step: not a live plan");
+    if (P->flags & NEO_PLAN_HOST_ONLY) return fail(NEO_ERR_STATE, "neo_run_step: host-only plan");
+    if (step < 0 || step >= (int)P->steps.size())
+        return fail(NEO_ERR_INVALID_ARG, "neo_run_step: step out of range");
+    if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_step: NULL buffer");
+    if (!aligned16(x_nchw) || !aligned16(y_out))
+        return fail(NEO_ERR_ALIGN, "neo_run_step: buffers must be 16-byte aligned");
+    return enqueue_step(P, P->steps[step], x_nchw, y_out, (hipStream_t)stream);
 }
 
 void neo_plan_destroy(neo_plan* plan) {

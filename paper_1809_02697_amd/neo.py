@@ -26,6 +26,7 @@ OPS = {"input": 0, "conv": 1, "maxpool": 2, "avgpool": 3, "gap": 4, "concat": 5,
 PLAN_HOST_ONLY = 1
 PLAN_NAIVE = 2
 PLAN_HIPGRAPH = 4
+PLAN_TUNE = 8
 BLOCK = 16
 
 
@@ -81,6 +82,11 @@ def lib():
         "neo_plan_output_shape": [P, ctypes.POINTER(I)],
         "neo_plan_conv_params": [P, I, P, P],
         "neo_run_graph": [P, P, P, P],
+        "neo_run_step": [P, I, P, P, P],
+        "neo_tune_db_save": [ctypes.c_char_p],
+        "neo_tune_db_load": [ctypes.c_char_p],
+        "neo_tune_db_clear": [],
+        "neo_tune_db_size": [],
         "neo_plan_destroy": [P],
         "neo_last_error": [],
     }
@@ -89,6 +95,7 @@ def lib():
         f.argtypes = args
         f.restype = I
     L.neo_plan_destroy.restype = None
+    L.neo_tune_db_clear.restype = None
     L.neo_last_error.restype = ctypes.c_char_p
     _lib = L
     return L
@@ -265,6 +272,22 @@ def dense(x, w, bias=None, act="none", out=None, stream=None):
     return out
 
 
+def tune_db_save(path):
+    return _check(lib().neo_tune_db_save(str(path).encode()))
+
+
+def tune_db_load(path):
+    return _check(lib().neo_tune_db_load(str(path).encode()))
+
+
+def tune_db_clear():
+    lib().neo_tune_db_clear()
+
+
+def tune_db_size():
+    return lib().neo_tune_db_size()
+
+
 # --------------------------------------------------------------------------------------
 # Graph plan
 # --------------------------------------------------------------------------------------
@@ -343,6 +366,11 @@ class Plan:
         _check(lib().neo_run_graph(self.handle, _dptr(x, "x"), _dptr(out, "out"),
                                    _stream(stream)))
         return out
+
+    def run_step(self, step, x, out, stream=None):
+        """Launch one step of the plan's launch list (for timing single layers)."""
+        _check(lib().neo_run_step(self.handle, step, _dptr(x, "x"), _dptr(out, "out"),
+                                  _stream(stream)))
 
     def destroy(self):
         if self._h is not None:

@@ -226,3 +226,32 @@ def test_plan_accepts_any_node_order():
     for i, nd in enumerate(g2.nodes):
         for j in nd.inputs:
             assert pos[j] < pos[i]
+
+
+def test_tune_db_roundtrip_and_errors(tmp_path):
+    neo.tune_db_clear()
+    assert neo.tune_db_size() == 0
+    p = tmp_path / "db.txt"
+    p.write_text("# arch N C H W K R S sh sw ph pw wmfma fk fp split waves us\n"
+                 "gfx950 1 64 56 56 64 3 3 1 1 1 1 1 2 2 1 4 7.5\n"
+                 "gfx950 1 512 7 7 512 3 3 1 1 1 1 1 2 1 4 8 10.5\n")
+    assert neo.tune_db_load(p) == 2
+    assert neo.tune_db_size() == 2
+    q = tmp_path / "out.txt"
+    assert neo.tune_db_save(q) == 2
+    lines = sorted(l for l in q.read_text().splitlines() if l)
+    assert lines[0].split()[:13] == "gfx950 1 512 7 7 512 3 3 1 1 1 1 1".split()
+    bad = tmp_path / "bad.txt"
+    bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 3 2 1 4 7.5\n")   # fk = 3 is not a kernel
+    with pytest.raises(neo.NeoError):
+        neo.tune_db_load(bad)
+    with pytest.raises(neo.NeoError):
+        neo.tune_db_load(tmp_path / "missing.txt")
+    neo.tune_db_clear()
+    assert neo.tune_db_size() == 0
+
+
+def test_tuning_needs_a_device_plan():
+    with pytest.raises(neo.NeoError) as e:
+        neo.Plan(wl.tiny_graph(), flags=neo.PLAN_HOST_ONLY | neo.PLAN_TUNE)
+    assert e.value.code == -1

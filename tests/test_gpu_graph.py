@@ -145,3 +145,38 @@ def test_hipgraph_replay_bit_identical(neo):
         p.run(x, out)
         np.testing.assert_array_equal(host(out), eager)
     p.destroy()
+
+
+def test_tuned_plan_matches_oracle_and_fills_db(neo, tmp_path):
+    """Local search at plan creation: every conv workload timed and stored;
+    the tuned plan still matches the oracle; the database persists."""
+    neo.tune_db_clear()
+    g = wl.tiny_graph()
+    p = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+    d = p.describe()
+    convs = [s for s in d["steps"] if s["kind"] == "conv"]
+    assert all(s["conv"]["tuned"] for s in convs)
+    n_shapes = len({tuple(sorted((k, str(v)) for k, v in s["conv"].items()
+                                 if k not in ("tile", "split", "waves", "tuned", "y_off", "y_tot",
+                                              "act", "bias"))) for s in convs})
+    assert neo.tune_db_size() == n_shapes
+    y = host(p.run(dev(g.x)))
+    assert_close(y.reshape(-1, 10), orc.run_graph(g), "tuned tiny")
+    p.destroy()
+    path = tmp_path / "db.txt"
+    assert neo.tune_db_save(path) == n_shapes
+    neo.tune_db_clear()
+    assert neo.tune_db_load(path) == n_shapes
+    p2 = neo.Plan(g)                       # untuned flags: configurations come from the db
+    assert all(s["conv"]["tuned"] for s in p2.describe()["steps"] if s["kind"] == "conv")
+    p2.destroy()
+
+
+def test_tuned_resnet50_end_to_end(neo):
+    g = wl.resnet50(1)
+    p = neo.Plan(g, flags=neo.PLAN_TUNE)
+    y = host(p.run(dev(g.x)))
+    p.destroy()
+    ref = orc.run_graph(g)
+    e, strict = assert_close_network(y, ref, "tuned resnet50")
+    print(f"\ntuned resnet50 b1: rel L2 {e:.2e}, beyond 1e-4(1+|ref|): {strict}")
