@@ -167,6 +167,21 @@ def model_latencies(neo, torch, wl, steps):
     return res
 
 
+def measured_traffic():
+    """HBM/fabric bytes per conv launch from the committed counter summary,
+    or None when the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "conv2d_blocked_resnet50_b1_traffic.json")
+    src = os.path.join(ROOT, "paper_1809_02697_amd", "csrc", "conv.hip")
+    try:
+        t = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]:
+        return None
+    return t["traffic_bytes_per_launch"]
+
+
 def cpu_baseline(g, budget_s=12.0):
     """The oracle (plain C direct convolution, OpenMP on all host cores) on
     whole ResNet-50 batch-1 forwards until ~budget_s of work."""
@@ -195,6 +210,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-models", action="store_true", help="skip the other models and ablation")
+    ap.add_argument("--tune-db", help="load this local-search results file before planning")
+    ap.add_argument("--save-tune-db", help="write the local-search results here at the end")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the batch-1 path has no cross-GPU work "
@@ -207,6 +224,8 @@ def main():
     neo.lib()
     assert torch.cuda.is_available(), "no GPU"
 
+    if args.tune_db:
+        neo.tune_db_load(args.tune_db)
     g = wl.resnet50(1)
     t0 = time.perf_counter()
     plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
@@ -229,7 +248,8 @@ def main():
         n_launch = sum(r["uses"] for r in layers)
         achieved = tot_f / tot_t / 1e12
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
-                        unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4), traffic=None,
+                        unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4),
+                        traffic=measured_traffic(),
                         kernel="conv2d_blocked", launches_per_step=n_launch,
                         avg_launch_us=round(tot_t / n_launch * 1e6, 2),
                         flop_per_launch=round(tot_f / n_launch))
@@ -272,6 +292,8 @@ def main():
     }
     print(json.dumps(rec))
     plan.destroy()
+    if args.save_tune_db:
+        neo.tune_db_save(args.save_tune_db)
 
 
 if __name__ == "__main__":

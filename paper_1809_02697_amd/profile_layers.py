@@ -1,0 +1,45 @@
+"""Workload for hardware-counter passes over the ResNet-50 batch-1 plan.
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT -o fetch -- \
+        python -m paper_1809_02697_amd.profile_layers
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT -o write -- \
+        python -m paper_1809_02697_amd.profile_layers
+
+Builds and tunes the plan (the same flags as bench.py), runs one forward,
+then a plain device-to-device copy of COPY_MB megabytes (the calibration
+kernel: it reads and writes exactly that many bytes) and then every step of
+the plan once, in order.  The dispatches after the copy are one forward pass.
+``paper_1809_02697_amd.profile_summary`` turns the counter files into the
+per-launch traffic figures.
+"""
+import sys
+
+COPY_MB = 64
+
+
+def main():
+    import torch
+
+    from paper_1809_02697_amd import neo
+    from paper_1809_02697_amd import workloads as wl
+
+    g = wl.resnet50(1)
+    plan = neo.Plan(g, flags=neo.PLAN_TUNE)
+    x = torch.from_numpy(g.x).cuda()
+    out = torch.empty((1, 1000), device="cuda")
+    plan.run(x, out)
+    torch.cuda.synchronize()
+    a = torch.ones(COPY_MB * 2 ** 18, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    n = len(plan.describe()["steps"])
+    for i in range(n):
+        plan.run_step(i, x, out)
+    torch.cuda.synchronize()
+    print(f"profiled {n} steps after a {COPY_MB} MB copy", file=sys.stderr)
+    plan.destroy()
+
+
+if __name__ == "__main__":
+    main()
