@@ -1,4 +1,5 @@
 // C-ABI entry points of libneo: argument validation, then the launchers.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -65,6 +66,53 @@ void blocks_from_mfma_order(const float* in, long n_blocks, float* out) {
         for (int c = 0; c < 16; ++c)
             for (int k = 0; k < 16; ++k)
                 out[b * 256 + c * 16 + k] = in[b * 256 + ((c / 4) * 16 + k) * 4 + c % 4];
+}
+
+long kernel_filter_floats(const ConvShape& s) {
+    const long KB = cdiv(s.K, 16);
+    if (conv_small_c(s)) return KB * s.R * cdiv(s.S, 4) * 256;
+    return KB * cdiv(s.C, 16) * s.R * s.S * 256;
+}
+
+// Small-channel order: the block of (kb, r, u) holds, for lane (k, g), the
+// float4 w[k][c = 0..3][r][s = 4u + g]; the KCRS[16]c[16]k source has one
+// channel block, its block (kb, r, s) at ((kb * R + r) * S + s) * 256, [c][k].
+void to_kernel_order(const float* packed, const ConvShape& s, float* out) {
+    if (!conv_small_c(s)) {
+        blocks_to_mfma_order(packed, kernel_filter_floats(s) / 256, out);
+        return;
+    }
+    const int KB = cdiv(s.K, 16), U = cdiv(s.S, 4);
+    for (int kb = 0; kb < KB; ++kb)
+        for (int r = 0; r < s.R; ++r)
+            for (int u = 0; u < U; ++u)
+                for (int g = 0; g < 4; ++g)
+                    for (int k = 0; k < 16; ++k)
+                        for (int c = 0; c < 4; ++c) {
+                            const int sc = 4 * u + g;
+                            const long o = (((long)(kb * s.R + r) * U + u) * 4 + g) * 64 + k * 4 + c;
+                            out[o] = sc < s.S
+                                         ? packed[((long)(kb * s.R + r) * s.S + sc) * 256 + c * 16 + k]
+                                         : 0.f;
+                        }
+}
+
+void from_kernel_order(const float* in, const ConvShape& s, float* packed) {
+    if (!conv_small_c(s)) {
+        blocks_from_mfma_order(in, kernel_filter_floats(s) / 256, packed);
+        return;
+    }
+    const int KB = cdiv(s.K, 16), U = cdiv(s.S, 4);
+    std::fill(packed, packed + (long)KB * s.R * s.S * 256, 0.f);  // channels 4..15 are padding
+    for (int kb = 0; kb < KB; ++kb)
+        for (int r = 0; r < s.R; ++r)
+            for (int sc = 0; sc < s.S; ++sc)
+                for (int k = 0; k < 16; ++k)
+                    for (int c = 0; c < 4; ++c) {
+                        const int u = sc / 4, g = sc % 4;
+                        packed[((long)(kb * s.R + r) * s.S + sc) * 256 + c * 16 + k] =
+                            in[(((long)(kb * s.R + r) * U + u) * 4 + g) * 64 + k * 4 + c];
+                    }
 }
 
 }  // namespace neo

@@ -42,6 +42,15 @@
 // per-step lane-offset computation, an LDS table or integer divisions per step
 // cost more than the MFMAs themselves at batch 1.
 // The epilogue (bias, residual, ReLU) runs in registers before the single store.
+//
+// Small-channel path (C <= 4, the network stems).  A channel block would be
+// three quarters padding, and one k-step per kernel entry would need a scalar
+// load per lane and entry.  Instead a reduction step is (filter row r, group u
+// of 4 filter columns): lane group g takes column s = 4u + g and loads the
+// float4 of channels 0..3 of its pixel's input at (r, s), component t feeding
+// k-step t.  So the 16 reduction elements of a step are 4 columns x 4
+// channels, every operand is one float4 per lane as on the main path, and a
+// padding column s >= S reads as 0 like a padding tap.
 #include <algorithm>
 #include <cmath>
 
@@ -78,7 +87,7 @@ struct ConvArgs {
     const float* res;
     float* y;
     float* ws;  // split partials [SPLIT][N][KB][OH][OW][16]
-    int N, CB, H, W, KB, R, S, RS, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
+    int N, CB, H, W, KB, R, S, RS, U, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
     int x_bytes, w_bytes;
     FastDiv div_ohw, div_ow, div_npx, div_nkb;
 };
@@ -87,19 +96,10 @@ constexpr int kXcds = 8;
 constexpr unsigned kRsrcWord3 = 0x00020000;    // raw buffer, gfx9 family
 constexpr unsigned kOutOfRange = 0x80000000u;  // buffer offset that reads as 0
 
-template <int FK, int FP, bool SMALLC>
-struct Operands;
-
 template <int FK, int FP>
-struct Operands<FK, FP, false> {
-    v4f b[FP];
-    v4f a[FK];
-};
-
-template <int FK, int FP>
-struct Operands<FK, FP, true> {
-    float b[FP];
-    float a[FK];
+struct Operands {
+    v4f b[FP];  // input: lane's pixel, 4 reduction elements (k-steps t = 0..3)
+    v4f a[FK];  // filter: lane's output channel, the same 4 reduction elements
 };
 
 // Bits [max(lo, 0), min(hi, n, 32)) set.
@@ -130,6 +130,9 @@ __device__ inline float ld1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, i
 // use.
 //   WMFMA:  filter blocks stored [c/4][k][c%4] (one float4 per lane) instead
 //           of the KCRS[16]c[16]k block [c][k] (four dwords, 64 bytes apart).
+//   SMALLC: steps st = r*U + u over filter rows and groups of 4 columns; the
+//           lane's column s = 4u + g varies by lane group, so the padding
+//           test runs every step (it is a few VALU operations).
 template <int FK, int FP, bool SMALLC, bool WMFMA>
 struct Loader {
     __amdgpu_buffer_rsrc_t xr, wr;
@@ -138,20 +141,41 @@ struct Loader {
     int pih[FP], piw[FP];
     unsigned woff[FK];            // byte offset of the lane's element in filter block (kb, 0, 0)
     bool wide_taps;               // more than 32 taps per axis: explicit test
+    int lg;                       // lane group g (small-channel column offset)
     // position of the next step to load (wave-uniform)
-    int st, cb, rs, r, s;
+    int st, cb, rs, r, s;         // small-channel path: s holds the column group u
     int sx, sw;                   // step byte offsets: input cb*H*W*64, filter (cb*RS + rs)*1024
     unsigned toff[FP];            // lane offset of the current tap, or out of range
+    unsigned wtoff[FK];           // small-channel, KCRS[16]c[16]k filter: lane offset or out of range
 
     __device__ void set_tap(const ConvArgs& a) {
+        if constexpr (SMALLC) {
+            const int sc = 4 * s + lg;
+            const bool cok = sc < a.S;
 #pragma unroll
-        for (int p = 0; p < FP; ++p) {
-            bool ok;
-            if (!wide_taps)
-                ok = ((rowm[p] >> r) & (colm[p] >> s) & 1u) != 0;
-            else
-                ok = (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
-            toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + s) * 64) : kOutOfRange;
+            for (int p = 0; p < FP; ++p) {
+                bool ok;
+                if (!wide_taps)
+                    ok = cok && (((rowm[p] >> r) & (colm[p] >> sc) & 1u) != 0);
+                else
+                    ok = cok && (unsigned)(pih[p] + r) < (unsigned)a.H &&
+                         (unsigned)(piw[p] + sc) < (unsigned)a.W;
+                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + sc) * 64) : kOutOfRange;
+            }
+            if constexpr (!WMFMA) {
+#pragma unroll
+                for (int f = 0; f < FK; ++f) wtoff[f] = cok ? woff[f] : kOutOfRange;
+            }
+        } else {
+#pragma unroll
+            for (int p = 0; p < FP; ++p) {
+                bool ok;
+                if (!wide_taps)
+                    ok = ((rowm[p] >> r) & (colm[p] >> s) & 1u) != 0;
+                else
+                    ok = (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
+                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + s) * 64) : kOutOfRange;
+            }
         }
     }
     // The step state is wave-uniform; readfirstlane pins it to scalar
@@ -167,20 +191,41 @@ struct Loader {
         sx = __builtin_amdgcn_readfirstlane(sx);
         sw = __builtin_amdgcn_readfirstlane(sw);
     }
+    // filter step offset of the small-channel path at (r, u)
+    __device__ int small_sw(const ConvArgs& a) const {
+        return WMFMA ? (r * a.U + s) * 1024 : (r * a.S + 4 * s) * 1024;
+    }
     __device__ void seek(const ConvArgs& a, int st0) {
         st = st0;
-        rs = st0 / a.CB;
-        cb = st0 - rs * a.CB;
-        r = rs / a.S;
-        s = rs - r * a.S;
-        sx = cb * a.H * a.W * 64;
-        sw = (cb * a.RS + rs) * 1024;
+        if constexpr (SMALLC) {
+            r = st0 / a.U;
+            s = st0 - r * a.U;
+            cb = 0;
+            rs = 0;
+            sx = 0;
+            sw = small_sw(a);
+        } else {
+            rs = st0 / a.CB;
+            cb = st0 - rs * a.CB;
+            r = rs / a.S;
+            s = rs - r * a.S;
+            sx = cb * a.H * a.W * 64;
+            sw = (cb * a.RS + rs) * 1024;
+        }
         pin();
         set_tap(a);
     }
     __device__ void next(const ConvArgs& a) {
         ++st;
-        if (++cb < a.CB) {
+        if constexpr (SMALLC) {
+            if (++s == a.U) {
+                s = 0;
+                ++r;
+            }
+            sw = small_sw(a);
+            pin();
+            set_tap(a);
+        } else if (++cb < a.CB) {
             sx += a.H * a.W * 64;
             sw += a.RS * 1024;
         } else {
@@ -197,54 +242,40 @@ struct Loader {
         }
         pin();
     }
-    __device__ void load(Operands<FK, FP, SMALLC>& o) const {
+    __device__ void load(Operands<FK, FP>& o) const {
 #pragma unroll
-        for (int p = 0; p < FP; ++p) {
-            if constexpr (!SMALLC)
-                o.b[p] = ld4(xr, toff[p], sx, 0);
-            else
-                o.b[p] = ld1(xr, toff[p], sx, 0);
-        }
+        for (int p = 0; p < FP; ++p) o.b[p] = ld4(xr, toff[p], sx, 0);
 #pragma unroll
         for (int f = 0; f < FK; ++f) {
-            if constexpr (SMALLC) {
-                o.a[f] = ld1(wr, woff[f], sw, 0);
-            } else if constexpr (WMFMA) {
+            if constexpr (WMFMA) {
                 o.a[f] = ld4(wr, woff[f], sw, 0);
             } else {
+                const unsigned off = SMALLC ? wtoff[f] : woff[f];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) o.a[f][t] = ld1(wr, woff[f], sw, t * 64);
+                for (int t = 0; t < 4; ++t) o.a[f][t] = ld1(wr, off, sw, t * 64);
             }
         }
     }
 };
 
 // Depth of the load ring: as many steps in flight as about 72 VGPRs allow.
-template <int FK, int FP, bool SMALLC>
+template <int FK, int FP>
 constexpr int pipe_depth() {
-    const int regs = SMALLC ? (FK + FP) : 4 * (FK + FP);
+    const int regs = 4 * (FK + FP);
     const int d = 72 / regs;
     return d < 2 ? 2 : (d > 8 ? 8 : d);
 }
 
-template <int FK, int FP, bool SMALLC>
-__device__ inline void mma(const Operands<FK, FP, SMALLC>& o, v4f (&acc)[FK][FP]) {
-    if constexpr (!SMALLC) {
+template <int FK, int FP>
+__device__ inline void mma(const Operands<FK, FP>& o, v4f (&acc)[FK][FP]) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int f = 0; f < FK; ++f)
-#pragma unroll
-                for (int p = 0; p < FP; ++p)
-                    acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[f][t], o.b[p][t], acc[f][p],
-                                                                     0, 0, 0);
-    } else {
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int f = 0; f < FK; ++f)
 #pragma unroll
             for (int p = 0; p < FP; ++p)
-                acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[f], o.b[p], acc[f][p], 0, 0, 0);
-    }
+                acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[f][t], o.b[p][t], acc[f][p],
+                                                                 0, 0, 0);
 }
 
 template <int FK, int FP, bool SMALLC, bool WMFMA, int WAVES>
@@ -274,6 +305,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     tl.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
     tl.wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
     tl.wide_taps = a.R > 32 || a.S > 32;
+    tl.lg = g;
     bool pv[FP];
     int pn[FP];
 #pragma unroll
@@ -294,17 +326,20 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
         tl.colm[p] = run_mask(-iw0, a.W - iw0, a.S);
         // byte offset of this pixel's (cb = 0, r = 0, s = 0) element; only used
         // (with a step offset added) when the tap is inside the input
-        tl.xoff[p] = ((n * a.CB * a.H + ih0) * a.W + iw0) * 64 + (SMALLC ? 4 * g : 16 * g);
+        tl.xoff[p] = ((n * a.CB * a.H + ih0) * a.W + iw0) * 64 + (SMALLC ? 0 : 16 * g);
     }
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kb0 + f < a.KB ? kb0 + f : 0;  // past K: clamped, never stored
-        int e;
-        if constexpr (SMALLC)
-            e = WMFMA ? li * 4 + g : g * 16 + li;  // channel c = g of the block
-        else
-            e = WMFMA ? (g * 16 + li) * 4 : (4 * g) * 16 + li;
-        tl.woff[f] = (unsigned)((kb * a.CB * a.RS * 256 + e) * 4);
+        if constexpr (SMALLC) {
+            // kernel order: block (kb, r, u), lane's float4 at (g*16 + k)*4;
+            // KCRS[16]c[16]k: block (kb, r, s = 4u + g), element [c][k]
+            tl.woff[f] = WMFMA ? (unsigned)((kb * a.R * a.U * 256 + (g * 16 + li) * 4) * 4)
+                               : (unsigned)((kb * a.RS * 256 + g * 256 + li) * 4);
+        } else {
+            const int e = WMFMA ? (g * 16 + li) * 4 : (4 * g) * 16 + li;
+            tl.woff[f] = (unsigned)((kb * a.CB * a.RS * 256 + e) * 4);
+        }
     }
 
     v4f acc[FK][FP];
@@ -345,11 +380,11 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int nj = w_hi - w_lo;
 
     if (nj > 0) {
-        constexpr int D = pipe_depth<FK, FP, SMALLC>();
+        constexpr int D = pipe_depth<FK, FP>();
         // the loader runs D - 1 steps ahead; past the wave's last step it
         // stays there (those loads are never consumed)
         tl.seek(a, w_lo);
-        Operands<FK, FP, SMALLC> buf[D];
+        Operands<FK, FP> buf[D];
 #pragma unroll
         for (int i = 0; i < D - 1; ++i) {
             tl.load(buf[i]);
@@ -362,7 +397,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
                 // refill the slot consumed one step ago with step j + D - 1
                 tl.load(buf[(uu + D - 1) % D]);
                 if (tl.st < w_hi - 1) tl.next(a);
-                if (j < nj) mma<FK, FP, SMALLC>(buf[uu], acc);
+                if (j < nj) mma<FK, FP>(buf[uu], acc);
             }
         }
     }
@@ -524,8 +559,7 @@ bool conv_config_valid(const ConvConfig& c) {
 // the extra kernel and partial round trip of a split.
 ConvConfig choose_conv_config(const ConvShape& s) {
     const int KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
-    const bool smallc = s.C <= 4;
-    const int T = cdiv(s.C, 16) * s.R * s.S;
+    const int T = conv_steps(s);
     const double kClk = 2400.0;  // cycles per microsecond
     ConvConfig best{1, 1, 1, 4};
     double best_t = 1e30;
@@ -546,7 +580,7 @@ ConvConfig choose_conv_config(const ConvShape& s) {
                     const double waves_per_simd = (double)wgs * wv / 1024.0;
                     const double resident = std::max(1.0, std::min(8.0, waves_per_simd));
                     const double rounds = std::max(1.0, std::ceil(waves_per_simd / 8.0));
-                    const double mfma = (smallc ? 1.0 : 4.0) * fk * fp * 32.0;
+                    const double mfma = 4.0 * fk * fp * 32.0;
                     const double chain = 300.0 + 40.0 * (fk + fp);
                     const double per_step = std::max(mfma * resident, chain);
                     double t = 3.5 + rounds * steps * per_step / kClk;
@@ -586,6 +620,7 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.R = s.R;
     a.S = s.S;
     a.RS = s.R * s.S;
+    a.U = cdiv(s.S, 4);
     a.sh = s.sh;
     a.sw = s.sw;
     a.ph = s.ph;
@@ -596,16 +631,17 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.y_off = s.y_off;
     a.y_tot = s.y_tot;
     a.act = s.act;
-    a.T = a.CB * a.RS;
+    a.T = conv_steps(s);
     a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
     a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 64);
-    a.w_bytes = (int)((long)a.KB * a.CB * a.RS * 1024);
+    a.w_bytes = (int)((wmfma ? kernel_filter_floats(s) : (long)a.KB * a.CB * a.RS * 256) * 4);
     a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
     a.div_nkb = make_fastdiv((unsigned)cdiv(a.KB, c.fk));
-    if (wmfma) return s.C <= 4 ? dispatch<true, true>(c, a, st) : dispatch<false, true>(c, a, st);
-    return s.C <= 4 ? dispatch<true, false>(c, a, st) : dispatch<false, false>(c, a, st);
+    const bool small = conv_small_c(s);
+    if (wmfma) return small ? dispatch<true, true>(c, a, st) : dispatch<false, true>(c, a, st);
+    return small ? dispatch<true, false>(c, a, st) : dispatch<false, false>(c, a, st);
 }
 
 }  // namespace neo

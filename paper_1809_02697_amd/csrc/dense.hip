@@ -5,9 +5,14 @@
 // features), B = 16 rows of x (batch), D[4g+v][i] = y[batch i][feature 4g+v].
 // Both operands are row-major along the reduction axis, so each lane loads one
 // float4 per operand per 16-wide reduction chunk.  The chunks are split over
-// the 4 waves of a workgroup and summed through LDS in a fixed order.  At batch
-// 1 the layer is a weight stream (HBM bound); U chunks of loads are issued
-// before their MFMAs to keep enough bytes in flight.
+// the 4 waves of a workgroup and summed through LDS in a fixed order; U chunks
+// of loads are issued before their MFMAs to keep enough bytes in flight.
+//
+// Up to 4 batch rows the layer is a matrix-vector product, a pure weight
+// stream (HBM bound), and a 16-wide MFMA tile would waste 15/16 of its batch
+// lanes while giving too few workgroups to keep HBM busy.  That case runs
+// dense_rows: one wave per output feature, so the grid has OUT/4 workgroups
+// and every lane keeps G float4 loads of its row in flight.
 #include "neo_internal.h"
 
 namespace neo {
@@ -130,6 +135,79 @@ __global__ __launch_bounds__(256) void dense_mfma(DenseArgs a) {
     }
 }
 
+constexpr int kG = 8;  // float4 chunks of a row in flight per lane
+
+// One wave per output feature o: lane l accumulates the chunks l, l+64, ...
+// of row o against the same chunks of each batch row, then the wave adds its
+// lanes in a fixed butterfly order.  NB >= N batch rows, compile-time.
+template <int NB, bool VEC>
+__global__ __launch_bounds__(256) void dense_rows(DenseArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (o >= a.OUT) return;  // whole wave
+    const float* wr = a.w + (long)o * a.IN;
+    float acc[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) acc[n] = 0.f;
+    if constexpr (VEC) {
+        const int n4 = a.IN >> 2;
+        const v4f* w4 = reinterpret_cast<const v4f*>(wr);
+        const v4f* x4 = reinterpret_cast<const v4f*>(a.x);
+        int k = lane;
+        for (; k + 64 * (kG - 1) < n4; k += 64 * kG) {
+            v4f wv[kG], xv[kG][NB];
+#pragma unroll
+            for (int g = 0; g < kG; ++g) wv[g] = w4[k + 64 * g];
+#pragma unroll
+            for (int g = 0; g < kG; ++g)
+#pragma unroll
+                for (int n = 0; n < NB; ++n)
+                    xv[g][n] = n < a.N ? x4[(long)n * n4 + k + 64 * g] : v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int g = 0; g < kG; ++g)
+#pragma unroll
+                for (int n = 0; n < NB; ++n)
+                    acc[n] += wv[g].x * xv[g][n].x + wv[g].y * xv[g][n].y + wv[g].z * xv[g][n].z +
+                              wv[g].w * xv[g][n].w;
+        }
+        for (; k < n4; k += 64) {
+            const v4f wv = w4[k];
+#pragma unroll
+            for (int n = 0; n < NB; ++n) {
+                if (n >= a.N) break;
+                const v4f xv = x4[(long)n * n4 + k];
+                acc[n] += wv.x * xv.x + wv.y * xv.y + wv.z * xv.z + wv.w * xv.w;
+            }
+        }
+    } else {
+        for (int k = lane; k < a.IN; k += 64) {
+            const float wv = wr[k];
+#pragma unroll
+            for (int n = 0; n < NB; ++n)
+                if (n < a.N) acc[n] += wv * a.x[(long)n * a.IN + k];
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+        for (int n = 0; n < NB; ++n) acc[n] += __shfl_xor(acc[n], off, 64);
+    if (lane != 0) return;
+    const float b = a.bias ? a.bias[o] : 0.f;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+        if (n >= a.N) break;
+        float r = acc[n] + b;
+        if (a.act == NEO_ACT_RELU) r = r > 0.f ? r : 0.f;
+        a.y[(long)n * a.OUT + o] = r;
+    }
+}
+
+template <int NB, bool VEC>
+hipError_t launch_rows(const DenseArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL((dense_rows<NB, VEC>), dim3(cdiv(a.OUT, 4)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 template <int FO, int FN, bool VEC>
 hipError_t launch_t(const DenseArgs& a, hipStream_t st) {
     dim3 grid(cdiv(a.OUT, 16 * FO), cdiv(a.N, 16 * FN));
@@ -139,6 +217,9 @@ hipError_t launch_t(const DenseArgs& a, hipStream_t st) {
 
 template <bool VEC>
 hipError_t dispatch(const DenseArgs& a, hipStream_t st) {
+    if (a.N == 1) return launch_rows<1, VEC>(a, st);
+    if (a.N == 2) return launch_rows<2, VEC>(a, st);
+    if (a.N <= 4) return launch_rows<4, VEC>(a, st);
     if (a.N <= 16) return launch_t<1, 1, VEC>(a, st);
     return launch_t<1, 2, VEC>(a, st);
 }

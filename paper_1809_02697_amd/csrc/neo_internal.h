@@ -36,13 +36,20 @@ struct ConvConfig {
     int fk, fp, split, waves;
 };
 bool conv_config_valid(const ConvConfig& c);
+// Inputs with at most 4 channels (network stems) take the small-channel path:
+// a reduction step is (filter row r, group u of 4 filter columns) instead of
+// (channel block, kernel entry).
+inline bool conv_small_c(const ConvShape& s) { return s.C <= 4; }
+// Reduction steps of one output tile.
+inline int conv_steps(const ConvShape& s) {
+    return conv_small_c(s) ? s.R * cdiv(s.S, 4) : cdiv(s.C, 16) * s.R * s.S;
+}
 ConvConfig choose_conv_config(const ConvShape& s);
 // Workspace of a split reduction (partial sums of every split), in bytes.
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);
 
 // Launch the blocked convolution.  x: NCHW16c; w: KCRS[16]c[16]k, or with
-// wmfma the same blocks with each 16x16 block stored [c/4][k][c%4] (see
-// pack_filter_mfma_host); bias: [KB*16] or null; res: NCHW16c
+// wmfma the kernel's own filter order (to_kernel_order); bias: [KB*16] or null; res: NCHW16c
 // [N][KB][OH][OW][16] or null; y: NCHW16c view.  ws: workspace of at least
 // conv_workspace_bytes (a split is only used when it is given).  x and w must
 // each be below 2 GiB.
@@ -87,6 +94,14 @@ void pack_filter_host(const float* w, int K, int C, int R, int S, int ib, int ob
 // [c/4][k][c%4] (in place is not allowed), and back.
 void blocks_to_mfma_order(const float* in, long n_blocks, float* out);
 void blocks_from_mfma_order(const float* in, long n_blocks, float* out);
+// The filter order the kernel reads with wmfma, from and to KCRS[16]c[16]k:
+// C > 4: every block in MFMA order (blocks_to_mfma_order);
+// C <= 4: [KB][R][ceil(S/4)][4 g][16 k][4 c], filter column s = 4u + g,
+//         zero where s >= S.
+// kernel_filter_floats is the size of the kernel order in floats.
+long kernel_filter_floats(const ConvShape& s);
+void to_kernel_order(const float* packed, const ConvShape& s, float* out);
+void from_kernel_order(const float* in, const ConvShape& s, float* packed);
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

@@ -311,15 +311,15 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                     }
                 }
                 const long nblk = (long)cdiv(d.K, 16) * cdiv(C, 16) * d.R * d.S;
-                std::vector<float> wp(nblk * 256), wm(nblk * 256);
-                pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
-                blocks_to_mfma_order(wp.data(), nblk, wm.data());  // one float4 per lane
-                st.w_off = add_params(P, wm);
                 if (nblk * 256 >= (1L << 29) || (long)ni.N * cdiv(C, 16) * a->H * a->W * 16 >= (1L << 29))
                     return fail(NEO_ERR_UNSUPPORTED, where + "input or filter of 2 GiB or more");
-                if (has_b) st.b_off = add_params(P, b);
                 st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
                                   d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
+                std::vector<float> wp(nblk * 256), wm(kernel_filter_floats(st.cs));
+                pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
+                to_kernel_order(wp.data(), st.cs, wm.data());  // one float4 per lane and k-quad
+                st.w_off = add_params(P, wm);
+                if (has_b) st.b_off = add_params(P, b);
                 st.cc = choose_conv_config(st.cs);
                 if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
@@ -703,8 +703,7 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
     if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_conv_params: not a live plan");
     for (const Step& s : plan->steps) {
         if (s.kind != ST_CONV || s.node != node_id) continue;
-        const long nblk = (long)cdiv(s.cs.K, 16) * cdiv(s.cs.C, 16) * s.cs.R * s.cs.S;
-        if (w_packed) blocks_from_mfma_order(plan->params.data() + s.w_off, nblk, w_packed);
+        if (w_packed) from_kernel_order(plan->params.data() + s.w_off, s.cs, w_packed);
         if (bias) {
             const long bn = (long)cdiv(s.cs.K, 16) * 16;
             if (s.b_off >= 0)

@@ -1,6 +1,8 @@
 // Layout-tolerant pooling on NCHW16c (Section 3.2): max, average, global
 // average.  One thread per (output pixel, 4-channel quad) moves float4s, so a
 // wave reads and writes 16 pixels x 64 bytes = 1 KB contiguous per access.
+// Max pooling ignores taps outside the input (as if padded with -inf); average
+// pooling divides by the number of taps inside it.
 // Padded channel lanes hold 0 in the input and stay 0 in the output.
 #include "neo_internal.h"
 
@@ -9,7 +11,11 @@ namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-template <bool MAX>
+// Taps of a KR x KS window (0 = the window from the shape, a runtime loop).
+// With a compile-time window every tap's load is issued before any is used:
+// a tap outside the input loads pixel (0, 0) of the block and is discarded by
+// a select, so the loads of one output are in flight together.
+template <bool MAX, int KR, int KS>
 __global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, float* __restrict__ y,
                                                 PoolShape s, int CB) {
     const int total = s.N * CB * s.OH * s.OW * 4;
@@ -23,26 +29,53 @@ __global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, flo
         const int cb = r_ % CB;
         const int n = r_ / CB;
         const float* xb = x + (n * CB + cb) * s.H * s.W * 16 + 4 * q;
+        const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
         v4f acc;
         if (MAX)
             acc = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
         else
             acc = v4f{0.f, 0.f, 0.f, 0.f};
         int cnt = 0;
-        for (int r = 0; r < s.R; ++r) {
-            const int ih = oh * s.sh - s.ph + r;
-            if ((unsigned)ih >= (unsigned)s.H) continue;
-            for (int c = 0; c < s.S; ++c) {
-                const int iw = ow * s.sw - s.pw + c;
-                if ((unsigned)iw >= (unsigned)s.W) continue;
-                const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * 16);
-                if (MAX) {
+        if constexpr (KR > 0) {
+            v4f v[KR][KS];
+            bool ok[KR][KS];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
-                } else {
-                    acc += v;
+            for (int r = 0; r < KR; ++r)
+#pragma unroll
+                for (int c = 0; c < KS; ++c) {
+                    const int ih = ih0 + r, iw = iw0 + c;
+                    ok[r][c] = (unsigned)ih < (unsigned)s.H && (unsigned)iw < (unsigned)s.W;
+                    v[r][c] = *reinterpret_cast<const v4f*>(xb + (ok[r][c] ? ih * s.W + iw : 0) * 16);
                 }
-                ++cnt;
+#pragma unroll
+            for (int r = 0; r < KR; ++r)
+#pragma unroll
+                for (int c = 0; c < KS; ++c) {
+                    if (!ok[r][c]) continue;
+                    if (MAX) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) acc[i] = v[r][c][i] > acc[i] ? v[r][c][i] : acc[i];
+                    } else {
+                        acc += v[r][c];
+                    }
+                    ++cnt;
+                }
+        } else {
+            for (int r = 0; r < s.R; ++r) {
+                const int ih = ih0 + r;
+                if ((unsigned)ih >= (unsigned)s.H) continue;
+                for (int c = 0; c < s.S; ++c) {
+                    const int iw = iw0 + c;
+                    if ((unsigned)iw >= (unsigned)s.W) continue;
+                    const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * 16);
+                    if (MAX) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
+                    } else {
+                        acc += v;
+                    }
+                    ++cnt;
+                }
             }
         }
         if (!MAX) {
@@ -66,7 +99,15 @@ __global__ __launch_bounds__(256) void gap_b16(const float* __restrict__ x, floa
     const int q = lane & 3, slot = lane >> 2;
     const float* xb = x + wave_id * HW * 16 + 4 * q;
     v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
-    for (int p = slot; p < HW; p += 16) acc += *reinterpret_cast<const v4f*>(xb + p * 16);
+    int p = slot;
+    for (; p + 48 < HW; p += 64) {  // four pixels of the slot in flight
+        v4f v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const v4f*>(xb + (p + 16 * u) * 16);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += v[u];
+    }
+    for (; p < HW; p += 16) acc += *reinterpret_cast<const v4f*>(xb + p * 16);
 #pragma unroll
     for (int off = 4; off < 64; off <<= 1) {
 #pragma unroll
@@ -89,18 +130,25 @@ inline dim3 grid_for(long total) {
 
 }  // namespace
 
-hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
+template <bool MAX>
+hipError_t launch_pool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
     const int CB = cdiv(s.C, 16);
-    hipLaunchKernelGGL(pool_b16<true>, grid_for((long)s.N * CB * s.OH * s.OW * 4), dim3(256), 0,
-                       st, x, y, s, CB);
+    const dim3 g = grid_for((long)s.N * CB * s.OH * s.OW * 4), b(256);
+    if (s.R == 3 && s.S == 3)
+        hipLaunchKernelGGL((pool_b16<MAX, 3, 3>), g, b, 0, st, x, y, s, CB);
+    else if (s.R == 2 && s.S == 2)
+        hipLaunchKernelGGL((pool_b16<MAX, 2, 2>), g, b, 0, st, x, y, s, CB);
+    else
+        hipLaunchKernelGGL((pool_b16<MAX, 0, 0>), g, b, 0, st, x, y, s, CB);
     return hipGetLastError();
 }
 
+hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
+    return launch_pool<true>(s, x, y, st);
+}
+
 hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
-    const int CB = cdiv(s.C, 16);
-    hipLaunchKernelGGL(pool_b16<false>, grid_for((long)s.N * CB * s.OH * s.OW * 4), dim3(256), 0,
-                       st, x, y, s, CB);
-    return hipGetLastError();
+    return launch_pool<false>(s, x, y, st);
 }
 
 hipError_t launch_gap(const float* x, int N, int C, int H, int W, float* y, hipStream_t st) {

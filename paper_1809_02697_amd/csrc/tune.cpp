@@ -55,7 +55,7 @@ Key key_of(const ConvShape& s, bool wmfma, const std::string& arch) {
 // and keep the partials workspace below 64 MB.
 std::vector<ConvConfig> candidates(const ConvShape& s) {
     std::vector<ConvConfig> out;
-    const int T = cdiv(s.C, 16) * s.R * s.S, KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
+    const int T = conv_steps(s), KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
     for (int fk : {1, 2, 4})
         for (int fp : {1, 2, 4})
             for (int wv : {4, 8, 16})

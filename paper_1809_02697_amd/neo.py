@@ -64,6 +64,11 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_1809_02697_amd.build` (no CPU fallback exists)")
+    # torch first: libneo then binds to the HIP runtime torch already mapped
+    # (same soname), so the process holds one HIP runtime.  Loaded the other
+    # way round, the system runtime and torch's bundled one are both mapped,
+    # and the second one to initialise can fail to see the device.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, I, F, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     sig = {

@@ -1,11 +1,14 @@
 """Workload for hardware-counter passes over the ResNet-50 batch-1 plan.
 
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT -o fetch -- \
-        python -m paper_1809_02697_amd.profile_layers
+        python -m paper_1809_02697_amd.profile_layers [TUNE_DB]
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT -o write -- \
-        python -m paper_1809_02697_amd.profile_layers
+        python -m paper_1809_02697_amd.profile_layers [TUNE_DB]
 
-Builds and tunes the plan (the same flags as bench.py), runs one forward,
+Builds and tunes the plan (the same flags as bench.py; with TUNE_DB, a
+local-search results file written by ``bench.py --save-tune-db``, the
+configurations come from the file and no tuning launches are profiled), runs
+one forward,
 then a plain device-to-device copy of COPY_MB megabytes (the calibration
 kernel: it reads and writes exactly that many bytes) and then every step of
 the plan once, in order.  The dispatches after the copy are one forward pass.
@@ -23,6 +26,8 @@ def main():
     from paper_1809_02697_amd import neo
     from paper_1809_02697_amd import workloads as wl
 
+    if len(sys.argv) > 1:
+        neo.tune_db_load(sys.argv[1])
     g = wl.resnet50(1)
     plan = neo.Plan(g, flags=neo.PLAN_TUNE)
     x = torch.from_numpy(g.x).cuda()

@@ -155,11 +155,18 @@ def test_naive_plan_wraps_every_blocked_op():
     assert kinds.count("conv") == 53
 
 
-def test_plan_conv_params_are_folded_and_packed():
-    g = wl.tiny_graph()
+@pytest.mark.parametrize("make", ["tiny", "vgg_tiny", "resnet50_stem"])
+def test_plan_conv_params_are_folded_and_packed(make):
+    """The plan stores filters in the kernel's own order (MFMA order, or the
+    small-channel order for C <= 4); reading them back gives the folded
+    KCRS[16]c[16]k filter exactly."""
+    g = {"tiny": wl.tiny_graph, "vgg_tiny": wl.vgg_like_tiny,
+         "resnet50_stem": lambda: wl.resnet50(1)}[make]()
     p = host_plan(g)
     for i, n in enumerate(g.nodes):
         if n.op != "conv":
+            continue
+        if make == "resnet50_stem" and n.w.shape[1] > 4:
             continue
         C = n.w.shape[1]
         wp, b = p.conv_params(i, n.K, C, n.R, n.S)

@@ -119,6 +119,8 @@ EDGE = [
     (16, 16, 3, 3, 1, 2, 3, 3, 1, "relu"),          # pad larger than half the window
     (64, 64, 3, 3, 1, 1, 1, 1, 1, "relu"),          # 1x1 input, 3x3 window
     (16, 16, 2, 2, 2, 0, 6, 6, 1, "relu"),          # even window
+    (2, 5, 3, 11, (1, 2), (1, 5), 9, 13, 1, "relu"),  # small-C, 3 column groups, ragged K
+    (1, 24, 5, 5, 1, 2, 10, 9, 2, "none"),          # one input channel
 ]
 
 
@@ -166,7 +168,8 @@ def test_conv_writes_concat_slice_only(neo):
 POOLS = [("max", 3, 2, 1, 64, 112, 112, 1), ("max", 2, 2, 0, 64, 224, 224, 1),
          ("max", 3, 2, 0, 288, 35, 35, 1), ("max", 3, 2, 0, 5, 9, 8, 2),
          ("avg", 3, 1, 1, 192, 35, 35, 1), ("avg", 3, 1, 1, 37, 6, 7, 2),
-         ("avg", 2, 2, 1, 16, 5, 5, 1)]
+         ("avg", 2, 2, 1, 16, 5, 5, 1), ("max", 5, 1, 2, 20, 9, 9, 1),
+         ("avg", 5, 2, 2, 33, 11, 10, 1)]
 
 
 @pytest.mark.parametrize("p", POOLS, ids=[f"{p[0]}{p[1]}s{p[2]}p{p[3]}C{p[4]}H{p[5]}" for p in POOLS])
@@ -186,7 +189,7 @@ def test_pool(neo, p):
     assert (lanes == 0).all()
 
 
-@pytest.mark.parametrize("N,C,H,W", [(1, 2048, 7, 7), (1, 2048, 8, 8), (2, 40, 5, 3),
+@pytest.mark.parametrize("N,C,H,W", [(1, 2048, 7, 7), (1, 2048, 8, 8), (2, 40, 5, 3), (1, 48, 13, 11),
                                      (1, 16, 1, 1), (32, 512, 7, 7)])
 def test_global_avgpool(neo, N, C, H, W):
     x = np.random.default_rng(C).uniform(-1, 1, (N, C, H, W)).astype(np.float32)
@@ -197,7 +200,9 @@ def test_global_avgpool(neo, N, C, H, W):
 # ---- dense -----------------------------------------------------------------------------------
 @pytest.mark.parametrize("N,IN,OUT,act", [(1, 2048, 1000, "none"), (1, 25088, 4096, "relu"),
                                           (32, 4096, 1000, "none"), (3, 37, 19, "relu"),
-                                          (17, 64, 10, "none"), (1, 5, 3, "none")])
+                                          (17, 64, 10, "none"), (1, 5, 3, "none"),
+                                          (2, 4100, 37, "relu"), (4, 4100, 130, "none"),
+                                          (5, 4096, 33, "relu")])
 def test_dense(neo, N, IN, OUT, act):
     rng = np.random.default_rng(IN + OUT)
     x = rng.uniform(-1, 1, (N, IN)).astype(np.float32)
