@@ -350,7 +350,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
 
     // The epilogue's bias and residual reads are issued now, by the wave that
     // runs the epilogue, so their latency hides under the reduction.
-    constexpr bool kPrefetch = FK * FP <= 4;
+    constexpr bool kPrefetch = FK * FP <= (WAVES <= 2 ? 8 : 4);
     v4f pre_b[kPrefetch ? FK : 1], pre_r[kPrefetch ? FK : 1][kPrefetch ? FP : 1];
     if constexpr (kPrefetch) {
         if (wave == 0 && a.split == 1) {
@@ -403,23 +403,25 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     }
 
     // Sum the waves' partial tiles in wave order: 0 + 1 + 2 + ...
-    __shared__ v4f red[WAVES - 1][FK * FP][64];
-    if (wave > 0) {
+    if constexpr (WAVES > 1) {
+        __shared__ v4f red[WAVES - 1][FK * FP][64];
+        if (wave > 0) {
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p) red[wave - 1][f * FP + p][lane] = acc[f][p];
+        }
+        __syncthreads();
+        if (wave != 0) return;
 #pragma unroll
         for (int f = 0; f < FK; ++f)
 #pragma unroll
-            for (int p = 0; p < FP; ++p) red[wave - 1][f * FP + p][lane] = acc[f][p];
+            for (int p = 0; p < FP; ++p) {
+                const int qq = f * FP + p;
+#pragma unroll
+                for (int w = 0; w < WAVES - 1; ++w) acc[f][p] += red[w][qq][lane];
+            }
     }
-    __syncthreads();
-    if (wave != 0) return;
-#pragma unroll
-    for (int f = 0; f < FK; ++f)
-#pragma unroll
-        for (int p = 0; p < FP; ++p) {
-            const int qq = f * FP + p;
-#pragma unroll
-            for (int w = 0; w < WAVES - 1; ++w) acc[f][p] += red[w][qq][lane];
-        }
 
     if (a.split > 1) {
         // raw partial sums of split z, in the output's own blocked layout; the
@@ -514,9 +516,13 @@ hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
 }
 
 // LDS for the cross-wave sum is (WAVES - 1) * FK * FP KB; the instantiated
-// combinations keep it at or below 48 KB.
+// combinations keep it at or below 48 KB.  One or two waves per workgroup
+// suit short reductions (a 1x1 layer over few channels), where splitting the
+// reduction across more waves buys nothing but the LDS sum.
 template <int FK, int FP, bool SMALLC, bool WMFMA>
 hipError_t by_waves(int waves, const ConvArgs& a, hipStream_t st) {
+    if (waves == 1) return launch_t<FK, FP, SMALLC, WMFMA, 1>(a, st);
+    if (waves == 2) return launch_t<FK, FP, SMALLC, WMFMA, 2>(a, st);
     if constexpr (FK * FP <= 2) {
         if (waves == 16) return launch_t<FK, FP, SMALLC, WMFMA, 16>(a, st);
     }
@@ -547,8 +553,8 @@ hipError_t dispatch(const ConvConfig& c, const ConvArgs& a, hipStream_t st) {
 
 bool conv_config_valid(const ConvConfig& c) {
     const bool tile = (c.fk == 1 || c.fk == 2 || c.fk == 4) && (c.fp == 1 || c.fp == 2 || c.fp == 4);
-    const bool waves = c.waves == 4 || (c.waves == 8 && c.fk * c.fp <= 4) ||
-                       (c.waves == 16 && c.fk * c.fp <= 2);
+    const bool waves = c.waves == 1 || c.waves == 2 || c.waves == 4 ||
+                       (c.waves == 8 && c.fk * c.fp <= 4) || (c.waves == 16 && c.fk * c.fp <= 2);
     return tile && waves && c.split >= 1 && c.split <= 64;
 }
 
@@ -563,7 +569,7 @@ ConvConfig choose_conv_config(const ConvShape& s) {
     const double kClk = 2400.0;  // cycles per microsecond
     ConvConfig best{1, 1, 1, 4};
     double best_t = 1e30;
-    static const int fks[] = {1, 2, 4}, fps[] = {1, 2, 4}, wvs[] = {4, 8, 16};
+    static const int fks[] = {1, 2, 4}, fps[] = {1, 2, 4}, wvs[] = {1, 2, 4, 8, 16};
     static const int splits[] = {1, 2, 3, 4, 6, 8};
     for (int fk : fks) {
         if (fk > 1 && fk > KB) continue;

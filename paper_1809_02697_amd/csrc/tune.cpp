@@ -58,7 +58,7 @@ std::vector<ConvConfig> candidates(const ConvShape& s) {
     const int T = conv_steps(s), KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
     for (int fk : {1, 2, 4})
         for (int fp : {1, 2, 4})
-            for (int wv : {4, 8, 16})
+            for (int wv : {1, 2, 4, 8, 16})
                 for (int sp : {1, 2, 4, 8}) {
                     const ConvConfig c{fk, fp, sp, wv};
                     if (!conv_config_valid(c)) continue;
