@@ -13,8 +13,13 @@ Printed JSON line:
                launch / average launch duration, the duration measured with
                HIP events around graph replays of each conv step of the plan
                (repeated back-to-back launches on the plan's stream)
+  latency      per-forward latency over 1000 single runs: mean, standard
+               error, median (warm caches: the batch-1 working set stays in
+               the 256 MB MALL between runs)
   layers       per distinct conv shape: us, TFLOP/s, algorithmic GB/s, % of
-               the binding roofline, and the launch configuration
+               the binding roofline, and the launch configuration (warm);
+               cold_us / cold_hbm_gbs: the same launch after a 512 MB write
+               has flushed the caches, so its operands come from HBM
   models       end-to-end latency of ResNet-50 / VGG-16 / Inception-v3 at
                batch 1 and ResNet-50 at batch 32, and the transform-elimination
                ablation (a plan that transforms around every blocked operation)
@@ -84,6 +89,29 @@ def time_graph(torch, fn, reps, rounds=3):
     return best
 
 
+_FLUSH = None
+
+
+def time_cold(torch, fn, reps):
+    """Average time of fn() with caches cold: before each launch a 512 MB
+    buffer (twice the 256 MB MALL, far above the L2s) is overwritten, so the
+    launch's operands come from HBM.  HIP events bracket the launch alone."""
+    global _FLUSH
+    if _FLUSH is None:
+        _FLUSH = torch.empty(128 * 2 ** 20, device="cuda")
+    stream = torch.cuda.current_stream()
+    tot = 0.0
+    for _ in range(reps):
+        _FLUSH.fill_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tot += e0.elapsed_time(e1) * 1e3
+    return tot / reps
+
+
 def e2e_ms(torch, plan, x, out, steps, warmup):
     for _ in range(warmup):
         plan.run(x, out)
@@ -95,6 +123,49 @@ def e2e_ms(torch, plan, x, out, steps, warmup):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / steps
+
+
+def e2e_stats(torch, plan, x, out, runs):
+    """Per-run latency over `runs` back-to-back forwards, each bracketed by
+    its own pair of HIP events (the mean +- standard error and the median,
+    as the paper reports the mean of 1000 runs with its standard error)."""
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(runs)]
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        e0.record(stream)
+        plan.run(x, out)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+    return dict(runs=runs, mean_ms=round(float(t.mean()), 4),
+                se_ms=round(float(t.std(ddof=1) / np.sqrt(runs)), 5),
+                median_ms=round(float(np.median(t)), 4), min_ms=round(float(t.min()), 4))
+
+
+def engine_clock(torch=None, plan=None, x=None, out=None, busy_runs=4000):
+    """GPU engine clock as rocm-smi reports it (best effort), sampled while
+    `busy_runs` forwards (about a second of work) are executing, since the
+    clock drops when the GPU idles."""
+    import subprocess
+    if plan is not None:
+        torch.cuda.synchronize()
+        for _ in range(busy_runs):
+            plan.run(x, out)
+        time.sleep(0.2)
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True,
+                           timeout=30)
+        d = json.loads(r.stdout)
+        card = d[sorted(d)[0]]
+        return {k: v for k, v in card.items() if "sclk" in k.lower() or "fclk" in k.lower()
+                or "mclk" in k.lower()}
+    except Exception as e:  # rocm-smi missing or not parseable: report why
+        return {"error": type(e).__name__}
+    finally:
+        if plan is not None:
+            torch.cuda.synchronize()
 
 
 def layer_table(torch, plan, x, out, reps):
@@ -111,18 +182,22 @@ def layer_table(torch, plan, x, out, reps):
         key = (c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"], c["W"],
                c["N"])
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
+        cold = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4))
         if key in rows:
             rows[key]["uses"] += 1
             rows[key]["_t"].append(us)
+            rows[key]["_c"].append(cold)
             continue
         flops, nbytes, OH, OW = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"],
                                            c["stride"], c["pad"], N=c["N"], residual=s["res"] >= 0)
         rows[key] = dict(shape=f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} "
                                f"{c['H']}->{OH}", uses=1, flops=flops, bytes=nbytes,
-                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"]), _t=[us])
+                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"]), _t=[us],
+                         _c=[cold])
     out_rows = []
     for r in rows.values():
         us = float(np.mean(r.pop("_t")))
+        cold = float(np.mean(r.pop("_c")))
         tf = r["flops"] / (us * 1e-6) / 1e12
         gbs = r["bytes"] / (us * 1e-6) / 1e9
         ai = r["flops"] / r["bytes"]
@@ -131,7 +206,9 @@ def layer_table(torch, plan, x, out, reps):
                  alg_gbs=round(gbs, 1),
                  bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_FP32_TFLOPS else "hbm",
                  pct_mfma=round(100 * tf / PEAK_FP32_TFLOPS, 1),
-                 pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1))
+                 pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1),
+                 cold_us=round(cold, 2),
+                 cold_hbm_gbs=round(r["bytes"] / (cold * 1e-6) / 1e9, 1))
         out_rows.append(r)
     return out_rows
 
@@ -207,6 +284,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--layer-reps", type=int, default=20)
+    ap.add_argument("--latency-runs", type=int, default=1000,
+                    help="single-forward latency samples (mean, standard error, median)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-models", action="store_true", help="skip the other models and ablation")
@@ -239,6 +318,10 @@ def main():
 
     ms = e2e_ms(torch, plan, x, out, args.steps, args.warmup)
     print(f"[bench] e2e {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    stats = e2e_stats(torch, plan, x, out, args.latency_runs)
+    print(f"[bench] latency over {stats['runs']} runs: {stats}", file=sys.stderr, flush=True)
+    clock = engine_clock(torch, plan, x, out)
+    print(f"[bench] engine clock under load: {clock}", file=sys.stderr, flush=True)
 
     layers, roofline = None, None
     if not args.no_layers:
@@ -275,6 +358,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "latency_ms": round(ms, 4),
+        "latency": stats,
+        "engine_clock": clock,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
