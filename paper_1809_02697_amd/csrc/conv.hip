@@ -36,6 +36,12 @@
 //     epilogue.  The kernel boundary makes the partials visible across XCDs
 //     (whose L2s are not coherent) without a per-workgroup device-scope
 //     release, which measured ~20 ns of serialized time per workgroup.
+// Grouped steps.  A step's bookkeeping (advancing the scalar offsets, the loop
+// and ring guards) costs about as many issue cycles as the 4 MFMAs of a one-
+// tile step, measured on MI355X.  Small register tiles therefore take G
+// channel blocks per step (G = 4 for a 1x1 tile, 2 for a 2-tile one, when G
+// divides the channel blocks), so a step issues 4*G*FK*FP MFMAs for one round
+// of bookkeeping.
 // Loads run D steps ahead of the MFMAs (a register ring sized to the tile), so
 // each wave keeps D-1 steps of loads in flight while it computes.  The step
 // bookkeeping is scalar and incremental (see Loader): measured on MI355X, a
@@ -87,7 +93,7 @@ struct ConvArgs {
     const float* res;
     float* y;
     float* ws;  // split partials [SPLIT][N][KB][OH][OW][16]
-    int N, CB, H, W, KB, R, S, RS, U, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
+    int N, CB, CBG, H, W, KB, R, S, RS, U, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
     int x_bytes, w_bytes;
     FastDiv div_ohw, div_ow, div_npx, div_nkb;
 };
@@ -96,10 +102,10 @@ constexpr int kXcds = 8;
 constexpr unsigned kRsrcWord3 = 0x00020000;    // raw buffer, gfx9 family
 constexpr unsigned kOutOfRange = 0x80000000u;  // buffer offset that reads as 0
 
-template <int FK, int FP>
+template <int FK, int FP, int G>
 struct Operands {
-    v4f b[FP];  // input: lane's pixel, 4 reduction elements (k-steps t = 0..3)
-    v4f a[FK];  // filter: lane's output channel, the same 4 reduction elements
+    v4f b[G][FP];  // input: lane's pixel, 4 reduction elements (k-steps t = 0..3) per block
+    v4f a[G][FK];  // filter: lane's output channel, the same 4 reduction elements
 };
 
 // Bits [max(lo, 0), min(hi, n, 32)) set.
@@ -133,7 +139,7 @@ __device__ inline float ld1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, i
 //   SMALLC: steps st = r*U + u over filter rows and groups of 4 columns; the
 //           lane's column s = 4u + g varies by lane group, so the padding
 //           test runs every step (it is a few VALU operations).
-template <int FK, int FP, bool SMALLC, bool WMFMA>
+template <int FK, int FP, int G, bool SMALLC, bool WMFMA>
 struct Loader {
     __amdgpu_buffer_rsrc_t xr, wr;
     int xoff[FP];                 // byte offset of the lane's pixel at (cb, r, s) = 0 (may be < 0)
@@ -145,6 +151,7 @@ struct Loader {
     // position of the next step to load (wave-uniform)
     int st, cb, rs, r, s;         // small-channel path: s holds the column group u
     int sx, sw;                   // step byte offsets: input cb*H*W*64, filter (cb*RS + rs)*1024
+    int dx, dw;                   // one channel block further: H*W*64 and RS*1024 bytes
     unsigned toff[FP];            // lane offset of the current tap, or out of range
     unsigned wtoff[FK];           // small-channel, KCRS[16]c[16]k filter: lane offset or out of range
 
@@ -205,13 +212,15 @@ struct Loader {
             sx = 0;
             sw = small_sw(a);
         } else {
-            rs = st0 / a.CB;
-            cb = st0 - rs * a.CB;
+            rs = st0 / a.CBG;
+            cb = (st0 - rs * a.CBG) * G;
             r = rs / a.S;
             s = rs - r * a.S;
             sx = cb * a.H * a.W * 64;
             sw = (cb * a.RS + rs) * 1024;
         }
+        dx = __builtin_amdgcn_readfirstlane(a.H * a.W * 64);
+        dw = __builtin_amdgcn_readfirstlane(a.RS * 1024);
         pin();
         set_tap(a);
     }
@@ -225,9 +234,9 @@ struct Loader {
             sw = small_sw(a);
             pin();
             set_tap(a);
-        } else if (++cb < a.CB) {
-            sx += a.H * a.W * 64;
-            sw += a.RS * 1024;
+        } else if ((cb += G) < a.CB) {
+            sx += G * dx;
+            sw += G * dw;
         } else {
             cb = 0;
             ++rs;
@@ -242,43 +251,50 @@ struct Loader {
         }
         pin();
     }
-    __device__ void load(Operands<FK, FP>& o) const {
+    __device__ void load(Operands<FK, FP, G>& o) const {
 #pragma unroll
-        for (int p = 0; p < FP; ++p) o.b[p] = ld4(xr, toff[p], sx, 0);
+        for (int i = 0; i < G; ++i) {
+            const int sxi = sx + i * dx, swi = sw + i * dw;
 #pragma unroll
-        for (int f = 0; f < FK; ++f) {
-            if constexpr (WMFMA) {
-                o.a[f] = ld4(wr, woff[f], sw, 0);
-            } else {
-                const unsigned off = SMALLC ? wtoff[f] : woff[f];
+            for (int p = 0; p < FP; ++p) o.b[i][p] = ld4(xr, toff[p], sxi, 0);
 #pragma unroll
-                for (int t = 0; t < 4; ++t) o.a[f][t] = ld1(wr, off, sw, t * 64);
+            for (int f = 0; f < FK; ++f) {
+                if constexpr (WMFMA) {
+                    o.a[i][f] = ld4(wr, woff[f], swi, 0);
+                } else {
+                    const unsigned off = SMALLC ? wtoff[f] : woff[f];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) o.a[i][f][t] = ld1(wr, off, swi, t * 64);
+                }
             }
         }
     }
 };
 
-// Depth of the load ring: as many steps in flight as about 72 VGPRs allow.
-template <int FK, int FP>
+// Depth of the load ring: as many steps in flight as about 72 VGPRs allow
+// (96 for grouped steps, which are G times longer).
+template <int FK, int FP, int G>
 constexpr int pipe_depth() {
-    const int regs = 4 * (FK + FP);
-    const int d = 72 / regs;
+    const int regs = 4 * G * (FK + FP);
+    const int d = (G > 1 ? 96 : 72) / regs;
     return d < 2 ? 2 : (d > 8 ? 8 : d);
 }
 
-template <int FK, int FP>
-__device__ inline void mma(const Operands<FK, FP>& o, v4f (&acc)[FK][FP]) {
+template <int FK, int FP, int G>
+__device__ inline void mma(const Operands<FK, FP, G>& o, v4f (&acc)[FK][FP]) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int i = 0; i < G; ++i)
 #pragma unroll
-        for (int f = 0; f < FK; ++f)
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int p = 0; p < FP; ++p)
-                acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[f][t], o.b[p][t], acc[f][p],
-                                                                 0, 0, 0);
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p)
+                    acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[i][f][t], o.b[i][p][t],
+                                                                     acc[f][p], 0, 0, 0);
 }
 
-template <int FK, int FP, bool SMALLC, bool WMFMA, int WAVES>
+template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES>
 __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -288,9 +304,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     // L2.  Give every XCD a contiguous run of the logical order
     // (split, channel tile, pixel tile), so the pixel tiles that share a
     // filter slice run on one XCD and read it from that XCD's L2.
-    const int G = gridDim.x;
+    const int nwg = gridDim.x;
     const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-    const int q = G / kXcds, rmd = G % kXcds;
+    const int q = nwg / kXcds, rmd = nwg % kXcds;
     const int u = xcd * q + min(xcd, rmd) + slot;
     const int npx = a.div_npx.d, nkb = a.div_nkb.d;
     const int u_px = fdiv(u, a.div_npx);
@@ -301,7 +317,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int kb0 = kbt * FK;
     const int ohw = a.OH * a.OW;
 
-    Loader<FK, FP, SMALLC, WMFMA> tl;
+    Loader<FK, FP, G, SMALLC, WMFMA> tl;
     tl.xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
     tl.wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
     tl.wide_taps = a.R > 32 || a.S > 32;
@@ -380,11 +396,11 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     const int nj = w_hi - w_lo;
 
     if (nj > 0) {
-        constexpr int D = pipe_depth<FK, FP>();
+        constexpr int D = pipe_depth<FK, FP, G>();
         // the loader runs D - 1 steps ahead; past the wave's last step it
         // stays there (those loads are never consumed)
         tl.seek(a, w_lo);
-        Operands<FK, FP> buf[D];
+        Operands<FK, FP, G> buf[D];
 #pragma unroll
         for (int i = 0; i < D - 1; ++i) {
             tl.load(buf[i]);
@@ -397,7 +413,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
                 // refill the slot consumed one step ago with step j + D - 1
                 tl.load(buf[(uu + D - 1) % D]);
                 if (tl.st < w_hi - 1) tl.next(a);
-                if (j < nj) mma<FK, FP>(buf[uu], acc);
+                if (j < nj) mma<FK, FP, G>(buf[uu], acc);
             }
         }
     }
@@ -501,11 +517,11 @@ __global__ __launch_bounds__(256) void split_reduce(ConvArgs a) {
     }
 }
 
-template <int FK, int FP, bool SMALLC, bool WMFMA, int WAVES>
+template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES>
 hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
     const int wgs = cdiv(a.M, 16 * FP) * cdiv(a.KB, FK) * a.split;
-    hipLaunchKernelGGL((conv2d_mfma<FK, FP, SMALLC, WMFMA, WAVES>), dim3(wgs), dim3(WAVES * 64), 0,
-                       st, a);
+    hipLaunchKernelGGL((conv2d_mfma<FK, FP, G, SMALLC, WMFMA, WAVES>), dim3(wgs), dim3(WAVES * 64),
+                       0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.split == 1) return e;
     const long total = (long)a.N * a.KB * a.OH * a.OW * 4;
@@ -519,37 +535,64 @@ hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
 // combinations keep it at or below 48 KB.  One or two waves per workgroup
 // suit short reductions (a 1x1 layer over few channels), where splitting the
 // reduction across more waves buys nothing but the LDS sum.
-template <int FK, int FP, bool SMALLC, bool WMFMA>
+template <int FK, int FP, int G, bool SMALLC, bool WMFMA>
 hipError_t by_waves(int waves, const ConvArgs& a, hipStream_t st) {
-    if (waves == 1) return launch_t<FK, FP, SMALLC, WMFMA, 1>(a, st);
-    if (waves == 2) return launch_t<FK, FP, SMALLC, WMFMA, 2>(a, st);
+    if (waves == 1) return launch_t<FK, FP, G, SMALLC, WMFMA, 1>(a, st);
+    if (waves == 2) return launch_t<FK, FP, G, SMALLC, WMFMA, 2>(a, st);
     if constexpr (FK * FP <= 2) {
-        if (waves == 16) return launch_t<FK, FP, SMALLC, WMFMA, 16>(a, st);
+        if (waves == 16) return launch_t<FK, FP, G, SMALLC, WMFMA, 16>(a, st);
     }
     if constexpr (FK * FP <= 4) {
-        if (waves == 8) return launch_t<FK, FP, SMALLC, WMFMA, 8>(a, st);
+        if (waves == 8) return launch_t<FK, FP, G, SMALLC, WMFMA, 8>(a, st);
     }
-    if (waves == 4) return launch_t<FK, FP, SMALLC, WMFMA, 4>(a, st);
+    if (waves == 4) return launch_t<FK, FP, G, SMALLC, WMFMA, 4>(a, st);
+    return hipErrorInvalidValue;
+}
+
+// Channel blocks per step: instantiated for G up to 4 / (FK * FP) (1 on the
+// small-channel path, whose step is not a channel block).
+template <int FK, int FP, bool SMALLC, bool WMFMA>
+hipError_t by_group(int g, int waves, const ConvArgs& a, hipStream_t st) {
+    if constexpr (!SMALLC && FK * FP == 1) {
+        if (g == 4) return by_waves<FK, FP, 4, SMALLC, WMFMA>(waves, a, st);
+    }
+    if constexpr (!SMALLC && FK * FP <= 2) {
+        if (g == 2) return by_waves<FK, FP, 2, SMALLC, WMFMA>(waves, a, st);
+    }
+    if (g == 1) return by_waves<FK, FP, 1, SMALLC, WMFMA>(waves, a, st);
     return hipErrorInvalidValue;
 }
 
 template <bool SMALLC, bool WMFMA>
-hipError_t dispatch(const ConvConfig& c, const ConvArgs& a, hipStream_t st) {
+hipError_t dispatch(const ConvConfig& c, int g, const ConvArgs& a, hipStream_t st) {
     switch (c.fk * 8 + c.fp) {
-        case 1 * 8 + 1: return by_waves<1, 1, SMALLC, WMFMA>(c.waves, a, st);
-        case 1 * 8 + 2: return by_waves<1, 2, SMALLC, WMFMA>(c.waves, a, st);
-        case 1 * 8 + 4: return by_waves<1, 4, SMALLC, WMFMA>(c.waves, a, st);
-        case 2 * 8 + 1: return by_waves<2, 1, SMALLC, WMFMA>(c.waves, a, st);
-        case 2 * 8 + 2: return by_waves<2, 2, SMALLC, WMFMA>(c.waves, a, st);
-        case 2 * 8 + 4: return by_waves<2, 4, SMALLC, WMFMA>(c.waves, a, st);
-        case 4 * 8 + 1: return by_waves<4, 1, SMALLC, WMFMA>(c.waves, a, st);
-        case 4 * 8 + 2: return by_waves<4, 2, SMALLC, WMFMA>(c.waves, a, st);
-        case 4 * 8 + 4: return by_waves<4, 4, SMALLC, WMFMA>(c.waves, a, st);
+        case 1 * 8 + 1: return by_group<1, 1, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 1 * 8 + 2: return by_group<1, 2, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 1 * 8 + 4: return by_group<1, 4, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 2 * 8 + 1: return by_group<2, 1, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 2 * 8 + 2: return by_group<2, 2, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 2 * 8 + 4: return by_group<2, 4, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 4 * 8 + 1: return by_group<4, 1, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 4 * 8 + 2: return by_group<4, 2, SMALLC, WMFMA>(g, c.waves, a, st);
+        case 4 * 8 + 4: return by_group<4, 4, SMALLC, WMFMA>(g, c.waves, a, st);
         default: return hipErrorInvalidValue;
     }
 }
 
 }  // namespace
+
+int conv_group(const ConvShape& s, const ConvConfig& c) {
+    if (conv_small_c(s)) return 1;
+    const int CB = cdiv(s.C, 16);
+    int g = c.fk * c.fp == 1 ? 4 : (c.fk * c.fp == 2 ? 2 : 1);
+    while (CB % g) g /= 2;
+    return g;
+}
+
+int conv_steps(const ConvShape& s, const ConvConfig& c) {
+    if (conv_small_c(s)) return s.R * cdiv(s.S, 4);
+    return cdiv(s.C, 16) / conv_group(s, c) * s.R * s.S;
+}
 
 bool conv_config_valid(const ConvConfig& c) {
     const bool tile = (c.fk == 1 || c.fk == 2 || c.fk == 4) && (c.fp == 1 || c.fp == 2 || c.fp == 4);
@@ -565,7 +608,6 @@ bool conv_config_valid(const ConvConfig& c) {
 // the extra kernel and partial round trip of a split.
 ConvConfig choose_conv_config(const ConvShape& s) {
     const int KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
-    const int T = conv_steps(s);
     const double kClk = 2400.0;  // cycles per microsecond
     ConvConfig best{1, 1, 1, 4};
     double best_t = 1e30;
@@ -580,13 +622,14 @@ ConvConfig choose_conv_config(const ConvShape& s) {
                 for (int sp : splits) {
                     const ConvConfig c{fk, fp, sp, wv};
                     if (!conv_config_valid(c)) continue;
+                    const int T = conv_steps(s, c), G = conv_group(s, c);
                     if (sp > 1 && T / sp < wv) continue;
                     const long wgs = tiles * sp;
                     const double steps = std::ceil((double)T / sp / wv);
                     const double waves_per_simd = (double)wgs * wv / 1024.0;
                     const double resident = std::max(1.0, std::min(8.0, waves_per_simd));
                     const double rounds = std::max(1.0, std::ceil(waves_per_simd / 8.0));
-                    const double mfma = 4.0 * fk * fp * 32.0;
+                    const double mfma = 4.0 * G * fk * fp * 32.0;
                     const double chain = 300.0 + 40.0 * (fk + fp);
                     const double per_step = std::max(mfma * resident, chain);
                     double t = 3.5 + rounds * steps * per_step / kClk;
@@ -637,7 +680,9 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.y_off = s.y_off;
     a.y_tot = s.y_tot;
     a.act = s.act;
-    a.T = conv_steps(s);
+    const int G = conv_group(s, c);
+    a.CBG = a.CB / G;
+    a.T = conv_steps(s, c);
     a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
     a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 64);
     a.w_bytes = (int)((wmfma ? kernel_filter_floats(s) : (long)a.KB * a.CB * a.RS * 256) * 4);
@@ -646,8 +691,8 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
     a.div_nkb = make_fastdiv((unsigned)cdiv(a.KB, c.fk));
     const bool small = conv_small_c(s);
-    if (wmfma) return small ? dispatch<true, true>(c, a, st) : dispatch<false, true>(c, a, st);
-    return small ? dispatch<true, false>(c, a, st) : dispatch<false, false>(c, a, st);
+    if (wmfma) return small ? dispatch<true, true>(c, G, a, st) : dispatch<false, true>(c, G, a, st);
+    return small ? dispatch<true, false>(c, G, a, st) : dispatch<false, false>(c, G, a, st);
 }
 
 }  // namespace neo

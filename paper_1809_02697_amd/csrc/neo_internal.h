@@ -40,10 +40,10 @@ bool conv_config_valid(const ConvConfig& c);
 // a reduction step is (filter row r, group u of 4 filter columns) instead of
 // (channel block, kernel entry).
 inline bool conv_small_c(const ConvShape& s) { return s.C <= 4; }
-// Reduction steps of one output tile.
-inline int conv_steps(const ConvShape& s) {
-    return conv_small_c(s) ? s.R * cdiv(s.S, 4) : cdiv(s.C, 16) * s.R * s.S;
-}
+// Channel blocks per reduction step for a launch configuration (1 on the
+// small-channel path), and the reduction steps of one output tile.
+int conv_group(const ConvShape& s, const ConvConfig& c);
+int conv_steps(const ConvShape& s, const ConvConfig& c);
 ConvConfig choose_conv_config(const ConvShape& s);
 // Workspace of a split reduction (partial sums of every split), in bytes.
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);

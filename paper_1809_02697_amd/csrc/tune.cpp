@@ -55,7 +55,7 @@ Key key_of(const ConvShape& s, bool wmfma, const std::string& arch) {
 // and keep the partials workspace below 64 MB.
 std::vector<ConvConfig> candidates(const ConvShape& s) {
     std::vector<ConvConfig> out;
-    const int T = conv_steps(s), KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
+    const int KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
     for (int fk : {1, 2, 4})
         for (int fp : {1, 2, 4})
             for (int wv : {1, 2, 4, 8, 16})
@@ -64,7 +64,7 @@ std::vector<ConvConfig> candidates(const ConvShape& s) {
                     if (!conv_config_valid(c)) continue;
                     if (fk > 1 && fk > KB) continue;
                     if (fp > 1 && fp > MP) continue;
-                    if (T / sp < wv) continue;
+                    if (conv_steps(s, c) / sp < wv) continue;
                     if (sp > 1 && conv_workspace_bytes(s, c) > (64u << 20)) continue;
                     out.push_back(c);
                 }

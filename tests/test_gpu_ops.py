@@ -223,11 +223,14 @@ CONFIGS = [(fk, fp, sp, wv) for fk in (1, 2, 4) for fp in (1, 2, 4) for wv in (1
 def test_conv_every_launch_config(neo, cfg, monkeypatch):
     """Every register tile, waves per workgroup and reduction split (forced
     through the tuning override) on ragged shapes: odd K, M not a multiple of
-    the tile, C with a padded block, and the small-C path."""
+    the tile, C with a padded block, the small-C path, and channel-block counts
+    that make small tiles take 4 or 2 blocks per step."""
     monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d,%d" % cfg)
     for (C, K, R, st, pd, H, N, epi) in [(40, 72, 3, 1, 1, 11, 2, "res"),
                                          (3, 24, 3, 2, 1, 17, 1, "relu"),
-                                         (130, 20, 1, 1, 0, 5, 3, "none")]:
+                                         (130, 20, 1, 1, 0, 5, 3, "none"),
+                                         (64, 40, 3, 1, 1, 9, 2, "res"),      # 4 blocks: G = 4
+                                         (96, 24, 1, 2, 0, 7, 1, "relu")]:    # 6 blocks: G = 2
         OH = orc.out_size(H, R, st, pd)
         c = wl.conv_case(C, K, R, R, st, pd, H, H, N=N, epilogue=epi, out_hw=(OH, OH))
         ref = orc.layer_forward(c)
