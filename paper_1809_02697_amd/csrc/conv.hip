@@ -406,11 +406,24 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
             tl.load(buf[i]);
             if (tl.st < w_hi - 1) tl.next(a);
         }
-        for (int j0 = 0; j0 < nj; j0 += D) {
+        // Steady state: while two more rings of steps remain, the loader never
+        // reaches the wave's last step and every slot is consumed, so the
+        // ring runs without guards.  At block j0 the loader stands at step
+        // j0 + D - 1 and loads up to j0 + 2D - 2 < nj - 1.
+        int j0 = 0;
+        for (; j0 + 2 * D <= nj; j0 += D) {
+#pragma unroll
+            for (int uu = 0; uu < D; ++uu) {
+                // refill the slot consumed one step ago with step j0 + uu + D - 1
+                tl.load(buf[(uu + D - 1) % D]);
+                tl.next(a);
+                mma<FK, FP, G>(buf[uu], acc);
+            }
+        }
+        for (; j0 < nj; j0 += D) {
 #pragma unroll
             for (int uu = 0; uu < D; ++uu) {
                 const int j = j0 + uu;
-                // refill the slot consumed one step ago with step j + D - 1
                 tl.load(buf[(uu + D - 1) % D]);
                 if (tl.st < w_hi - 1) tl.next(a);
                 if (j < nj) mma<FK, FP, G>(buf[uu], acc);
