@@ -10,6 +10,9 @@
  *   - the graph-level plan of Section 3.2, which keeps every convolution in
  *     NCHW[x]c with one constant x and inserts layout transforms only before
  *     the first blocked operation and before layout-dependent operations;
+ *   - the global search of Section 3.3.2 (Algorithm 2), which lets every
+ *     convolution choose its own input and output blocks (ic_bn, oc_bn) and
+ *     pays the layout transforms that choice needs;
  *   - the memory-bound operations the paper fuses into the convolution (bias,
  *     batch norm folded into the weights, residual add, ReLU; Sections 2.2
  *     and 3).
@@ -94,6 +97,29 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
                        int y_cblk_total, neo_stream_t stream);
 
 /*
+ * The same convolution with the input in NCHW[x_block]c and the output in
+ * NCHW[y_block]c (Section 3.1.1: the output layout NCHW[y]c may use another
+ * split factor than the input's NCHW[x]c; Algorithm 1's x and y):
+ *   x        device [N][ceil(C/x_block)][H][W][x_block], padding lanes +0.0
+ *   y        device NCHW[y_block]c with `y_blk_total` blocks of y_block
+ *            channels; the output occupies blocks [y_blk_offset,
+ *            y_blk_offset + ceil(K/y_block)); its padding lanes (k >= K) are
+ *            written as +0.0
+ *   ep->residual  NULL or device [N][ceil(K/y_block)][OH][OW][y_block]
+ *   w_packed, bias as for neo_conv2d_blocked (the filter is always
+ *            KCRS[16]c[16]k: its block size is the kernel's MFMA tile, not a
+ *            property of the feature maps).
+ * x_block: 16, 32 or 64; when C <= 4 also 4 or 8.  y_block: 16, 32 or 64.
+ * Other blocks return NEO_ERR_UNSUPPORTED.  The arithmetic does not depend on
+ * the blocks: with the same launch configuration (the default cost model does
+ * not look at the blocks) results are bit-identical to neo_conv2d_blocked's.
+ */
+int neo_conv2d_nchwxc(const float* x, int x_block, int N, int C, int H, int W,
+                      const float* w_packed, int K, int R, int S, const float* bias, int stride_h,
+                      int stride_w, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
+                      int y_block, int y_blk_offset, int y_blk_total, neo_stream_t stream);
+
+/*
  * LayoutTransform node (Section 3.2): NCHW <-> NCHW[x]c, or NCHW[x]c ->
  * NCHW[x']c.  A block of 0 means plain NCHW; a block x > 0 means
  * [N][ceil(C/x)][H][W][x] with zero-filled padding lanes.  Blocks: 0, 1, 2,
@@ -146,6 +172,19 @@ int neo_avgpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int
 int neo_global_avgpool_blocked(const float* x, int N, int C, int H, int W, float* y,
                                neo_stream_t stream);
 
+/* The pools on NCHW[block]c for block 4, 8, 16, 32 or 64 (Section 3.2: pooling
+ * is layout tolerant, it runs in the layout its input arrives in).  Input and
+ * output use the same block; y_blk_offset / y_blk_total count blocks of that
+ * size.  Results do not depend on the block. */
+int neo_maxpool2d_nchwxc(const float* x, int block, int N, int C, int H, int W, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                         int y_blk_offset, int y_blk_total, neo_stream_t stream);
+int neo_avgpool2d_nchwxc(const float* x, int block, int N, int C, int H, int W, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                         int y_blk_offset, int y_blk_total, neo_stream_t stream);
+int neo_global_avgpool_nchwxc(const float* x, int block, int N, int C, int H, int W, float* y,
+                              neo_stream_t stream);
+
 /*
  * Dense (fully connected) layer after Flatten, a layout-dependent operation
  * that consumes the default layout (Section 3.2):
@@ -185,6 +224,11 @@ typedef struct neo_node {
     const float* bias;   /* [K] or NULL */
     const float* bn_gamma, *bn_beta, *bn_mean, *bn_var; /* [K] each, or all NULL */
     float bn_eps;
+    /* conv: the scheme's split factors (Section 3.3.1's ic_bn, oc_bn), i.e. the
+     * blocks of its input and output layouts; 0 and 0 = the plan's choice (the
+     * plan's block, or the global search's).  Both 0 or both set; see
+     * neo_conv2d_nchwxc for the blocks allowed. */
+    int ic_bn, oc_bn;
 } neo_node;
 
 typedef struct neo_plan neo_plan;
@@ -208,7 +252,16 @@ enum neo_plan_flags {
      * launch configuration of each convolution workload not yet in the
      * results database on this GPU and keep the fastest (see neo_tune_db_*).
      * Untuned workloads use a cost model.  Needs a device plan. */
-    NEO_PLAN_TUNE = 8
+    NEO_PLAN_TUNE = 8,
+    /* Global search (Section 3.3.2, Algorithm 2): every conv without a given
+     * scheme chooses (ic_bn, oc_bn) among its candidates -- the factors of its
+     * channel counts that the kernel supports (16, 32, 64; 4 for an input of
+     * at most 4 channels), always including the plan's block -- by the local
+     * search's measured time of each scheme plus the measured time of every
+     * layout transform the choice implies, minimised over the whole network by
+     * neo_layout_search's dynamic program.  Implies NEO_PLAN_TUNE; needs a
+     * device plan. */
+    NEO_PLAN_GLOBAL_SEARCH = 16
 };
 
 /*
@@ -220,7 +273,10 @@ enum neo_plan_flags {
  * LayoutTransform steps only where a consumer needs another layout, fold
  * batch norm, pre-pack the filters, and allocate device buffers (concat
  * inputs are written in place into channel slices of the concat buffer).
- * `block` must be 16.  On success *out owns all device memory of the plan.
+ * `block` (16, 32 or 64) is the split factor of every conv without a scheme
+ * of its own (ic_bn = oc_bn = 0) when NEO_PLAN_GLOBAL_SEARCH is not given;
+ * layout-tolerant operations run in the layout their input arrives in.  On
+ * success *out owns all device memory of the plan.
  */
 int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
                     unsigned flags, neo_plan** out);
@@ -269,6 +325,42 @@ int neo_tune_db_save(const char* path);
 int neo_tune_db_load(const char* path);
 void neo_tune_db_clear(void);
 int neo_tune_db_size(void);
+
+/* ------------------------------------------------------------------------------------ */
+/* Global search (Section 3.3.2, Algorithm 2), host only                                 */
+/* ------------------------------------------------------------------------------------ */
+/* Layouts are indexed over the blocks {0 (NCHW), 4, 8, 16, 32, 64}. */
+#define NEO_SEARCH_NB 6
+
+/*
+ * Choose every conv's scheme (ic_bn, oc_bn) minimising the total of the
+ * schemes' execution times and the layout-transform times they imply, for the
+ * network `nodes` with input (N, C, H, W), using the plan's layout rules:
+ * a conv reads its input in ic_bn and its residual in oc_bn and writes
+ * oc_bn; pooling runs in its input's layout (`block` if that is NCHW); a
+ * concat takes its first input's layout when every part is a whole number of
+ * its blocks (else `block`, else NCHW) and converts the other parts;
+ * flatten, dense and the output need NCHW; a value transformed once serves
+ * every later reader of that layout; a transform of a 1x1 map whose channel
+ * count both blocks divide is free (an alias), except into a concat.
+ *   conv_time   host [n_nodes][NB][NB]: conv_time[v][i][j] = time of conv
+ *               node v with ic_bn = block i, oc_bn = block j; a negative or
+ *               non-finite entry means "not a candidate"; rows of other nodes
+ *               are ignored
+ *   xform_time  host [n_nodes][NB][NB]: time of transforming node v's value
+ *               from block i to block j (non-negative)
+ *   ic_bn, oc_bn  host [n_nodes] out: the chosen blocks of each conv (0 for
+ *               other nodes)
+ *   cost        host out (may be NULL): the minimum total
+ * The program is Algorithm 2 with, as its memorised state, the layouts of
+ * every value still to be read later; it is exact.  It returns
+ * NEO_ERR_UNSUPPORTED if the number of states exceeds 2^20 (the paper then
+ * switches to an approximate solver), NEO_ERR_SHAPE if no assignment is
+ * feasible.  Synchronous, CPU only.
+ */
+int neo_layout_search(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
+                      const double* conv_time, const double* xform_time, int* ic_bn, int* oc_bn,
+                      double* cost);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* neo_last_error(void);

@@ -127,10 +127,12 @@ def _concat_layout(graph, shapes, v, first_layout, default_block):
     return 0
 
 
-def plan_cost(graph, schemes, conv_time, xform_time, default_block=16):
+def plan_cost(graph, schemes, conv_time, xform_time, default_block=16, transforms=None):
     """Cost of one assignment {conv node: (ic_bn, oc_bn)}: walk the nodes,
     give every value the layout its producer leaves it in, and pay a transform
-    for each (value, layout) a consumer needs that the value does not have."""
+    for each (value, layout) a consumer needs that the value does not have.
+    If ``transforms`` is a list, every transform is appended to it as
+    (value's node, from block, to block, is_alias)."""
     shapes = infer_shapes(graph)
     native = {}
     have = {}
@@ -141,7 +143,10 @@ def plan_cost(graph, schemes, conv_time, xform_time, default_block=16):
         if layout in have[u]:
             return
         have[u].add(layout)
-        if not _alias(shapes[u], native[u], layout, into_concat):
+        alias = _alias(shapes[u], native[u], layout, into_concat)
+        if transforms is not None:
+            transforms.append((u, native[u], layout, alias))
+        if not alias:
             total += xform_time[u][_bi(native[u])][_bi(layout)]
 
     for v in topo_order(graph):

@@ -201,10 +201,10 @@ extern "C" {
 
 const char* neo_last_error(void) { return g_err.c_str(); }
 
-int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* w_packed, int K,
-                       int R, int S, const float* bias, int stride_h, int stride_w, int pad_h,
-                       int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
-                       int y_cblk_total, neo_stream_t stream) {
+int neo_conv2d_nchwxc(const float* x, int x_block, int N, int C, int H, int W,
+                      const float* w_packed, int K, int R, int S, const float* bias, int stride_h,
+                      int stride_w, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
+                      int y_block, int y_blk_offset, int y_blk_total, neo_stream_t stream) {
     CHECK_PTR(x);
     CHECK_PTR(w_packed);
     CHECK_PTR(y);
@@ -212,25 +212,31 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
     CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
     CHECK_POS(K); CHECK_POS(R); CHECK_POS(S);
     CHECK_POS(stride_h); CHECK_POS(stride_w);
-    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_blocked: negative pad");
+    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_nchwxc: negative pad");
     const int act = ep ? ep->act : NEO_ACT_NONE;
     if (act != NEO_ACT_NONE && act != NEO_ACT_RELU)
-        return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_blocked: unknown activation");
+        return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_nchwxc: unknown activation");
     const float* res = ep ? ep->residual : nullptr;
     if (res) CHECK_PTR(res);
     const int OH = out_dim(H, R, stride_h, pad_h), OW = out_dim(W, S, stride_w, pad_w);
     if (H + 2 * pad_h < R || W + 2 * pad_w < S || OH < 1 || OW < 1)
-        return fail(NEO_ERR_SHAPE, "neo_conv2d_blocked: empty output (window larger than padded input)");
-    const int KB = cdiv(K, 16);
-    if (y_cblk_offset < 0 || y_cblk_total < KB || y_cblk_offset + KB > y_cblk_total)
-        return fail(NEO_ERR_SHAPE, "neo_conv2d_blocked: output channel-block view out of range");
-    CHECK_SIZE(blocked_elems(N, C, H, W, 16));
-    CHECK_SIZE((long)N * y_cblk_total * 16 * OH * OW);
-    CHECK_SIZE((long)KB * 16 * cdiv(C, 16) * 16 * R * S);
-    if (blocked_elems(N, C, H, W, 16) >= (1L << 29) || (long)KB * cdiv(C, 16) * R * S * 256 >= (1L << 29))
-        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_blocked: input or filter of 2 GiB or more");
+        return fail(NEO_ERR_SHAPE, "neo_conv2d_nchwxc: empty output (window larger than padded input)");
     ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
-                y_cblk_offset, y_cblk_total, act};
+                y_blk_offset, y_blk_total, act};
+    s.xb = x_block;
+    s.yb = y_block;
+    if (!conv_blocks_valid(s))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_nchwxc: blocks must be 16, 32 or 64 "
+                                         "(input 4 or 8 too when C <= 4)");
+    const int KY = cdiv(K, y_block);
+    if (y_blk_offset < 0 || y_blk_total < KY || y_blk_offset + KY > y_blk_total)
+        return fail(NEO_ERR_SHAPE, "neo_conv2d_nchwxc: output channel-block view out of range");
+    CHECK_SIZE(blocked_elems(N, C, H, W, x_block));
+    CHECK_SIZE((long)N * y_blk_total * y_block * OH * OW);
+    CHECK_SIZE((long)cdiv(K, 16) * 16 * cdiv(C, 16) * 16 * R * S);
+    if (blocked_elems(N, C, H, W, x_block) >= (1L << 29) ||
+        (long)cdiv(K, 16) * cdiv(C, 16) * R * S * 256 >= (1L << 29))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_nchwxc: input or filter of 2 GiB or more");
     ConvConfig cfg = choose_conv_config(s);
     (void)tuned_config(s, false, &cfg);
     env_config(&cfg);
@@ -243,7 +249,15 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
     }
     hipError_t e = launch_conv2d(s, cfg, x, w_packed, false, bias, res, y, ws,
                                  (hipStream_t)stream);
-    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_blocked launch");
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_nchwxc launch");
+}
+
+int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* w_packed, int K,
+                       int R, int S, const float* bias, int stride_h, int stride_w, int pad_h,
+                       int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
+                       int y_cblk_total, neo_stream_t stream) {
+    return neo_conv2d_nchwxc(x, 16, N, C, H, W, w_packed, K, R, S, bias, stride_h, stride_w, pad_h,
+                             pad_w, ep, y, 16, y_cblk_offset, y_cblk_total, stream);
 }
 
 int neo_layout_transform(const float* src, int src_block, float* dst, int dst_block, int N,
@@ -252,7 +266,7 @@ int neo_layout_transform(const float* src, int src_block, float* dst, int dst_bl
     if (!valid_block(src_block) || !valid_block(dst_block))
         return fail(NEO_ERR_INVALID_ARG, "neo_layout_transform: block must be 0,1,2,4,8,16,32,64");
     CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
-    if (((src_block == 16) || (dst_block == 16)) && (!aligned16(src) || !aligned16(dst)))
+    if ((src_block >= 4 || dst_block >= 4) && (!aligned16(src) || !aligned16(dst)))
         return fail(NEO_ERR_ALIGN, "neo_layout_transform: buffers not 16-byte aligned");
     CHECK_SIZE(blocked_elems(N, C, H, W, src_block));
     CHECK_SIZE(blocked_elems(N, C, H, W, dst_block));
@@ -291,8 +305,8 @@ int neo_fold_bn(const float* w, const float* bias, const float* gamma, const flo
     return NEO_OK;
 }
 
-static int pool_common(const char* fn, bool is_max, const float* x, int N, int C, int H, int W,
-                       int R, int S, int sh, int sw, int ph, int pw, float* y, int y_off,
+static int pool_common(const char* fn, bool is_max, const float* x, int blk, int N, int C, int H,
+                       int W, int R, int S, int sh, int sw, int ph, int pw, float* y, int y_off,
                        int y_tot, neo_stream_t stream) {
     if (!x || !y) return fail(NEO_ERR_INVALID_ARG, std::string(fn) + ": NULL buffer");
     if (!aligned16(x) || !aligned16(y)) return fail(NEO_ERR_ALIGN, std::string(fn) + ": unaligned buffer");
@@ -303,12 +317,15 @@ static int pool_common(const char* fn, bool is_max, const float* x, int N, int C
     const int OH = out_dim(H, R, sh, ph), OW = out_dim(W, S, sw, pw);
     if (H + 2 * ph < R || W + 2 * pw < S || OH < 1 || OW < 1)
         return fail(NEO_ERR_SHAPE, std::string(fn) + ": empty output");
-    const int CB = cdiv(C, 16);
+    if (!pow2_block(blk))
+        return fail(NEO_ERR_UNSUPPORTED, std::string(fn) + ": block must be 4, 8, 16, 32 or 64");
+    const int CB = cdiv(C, blk);
     if (y_off < 0 || y_off + CB > y_tot)
         return fail(NEO_ERR_SHAPE, std::string(fn) + ": output channel-block view out of range");
-    if (blocked_elems(N, C, H, W, 16) > kMaxElems || (long)N * y_tot * 16 * OH * OW > kMaxElems)
+    if (blocked_elems(N, C, H, W, blk) > kMaxElems || (long)N * y_tot * blk * OH * OW > kMaxElems)
         return fail(NEO_ERR_UNSUPPORTED, std::string(fn) + ": tensor exceeds 2^31-1 elements");
     PoolShape s{N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot};
+    s.xb = blk;
     hipError_t e = is_max ? launch_maxpool(s, x, y, (hipStream_t)stream)
                           : launch_avgpool(s, x, y, (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, fn);
@@ -317,25 +334,46 @@ static int pool_common(const char* fn, bool is_max, const float* x, int N, int C
 int neo_maxpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S, int stride_h,
                           int stride_w, int pad_h, int pad_w, float* y, int y_cblk_offset,
                           int y_cblk_total, neo_stream_t stream) {
-    return pool_common("neo_maxpool2d_blocked", true, x, N, C, H, W, R, S, stride_h, stride_w,
+    return pool_common("neo_maxpool2d_blocked", true, x, 16, N, C, H, W, R, S, stride_h, stride_w,
                        pad_h, pad_w, y, y_cblk_offset, y_cblk_total, stream);
 }
 
 int neo_avgpool2d_blocked(const float* x, int N, int C, int H, int W, int R, int S, int stride_h,
                           int stride_w, int pad_h, int pad_w, float* y, int y_cblk_offset,
                           int y_cblk_total, neo_stream_t stream) {
-    return pool_common("neo_avgpool2d_blocked", false, x, N, C, H, W, R, S, stride_h, stride_w,
+    return pool_common("neo_avgpool2d_blocked", false, x, 16, N, C, H, W, R, S, stride_h, stride_w,
                        pad_h, pad_w, y, y_cblk_offset, y_cblk_total, stream);
+}
+
+int neo_maxpool2d_nchwxc(const float* x, int block, int N, int C, int H, int W, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                         int y_blk_offset, int y_blk_total, neo_stream_t stream) {
+    return pool_common("neo_maxpool2d_nchwxc", true, x, block, N, C, H, W, R, S, stride_h,
+                       stride_w, pad_h, pad_w, y, y_blk_offset, y_blk_total, stream);
+}
+
+int neo_avgpool2d_nchwxc(const float* x, int block, int N, int C, int H, int W, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, float* y,
+                         int y_blk_offset, int y_blk_total, neo_stream_t stream) {
+    return pool_common("neo_avgpool2d_nchwxc", false, x, block, N, C, H, W, R, S, stride_h,
+                       stride_w, pad_h, pad_w, y, y_blk_offset, y_blk_total, stream);
+}
+
+int neo_global_avgpool_nchwxc(const float* x, int block, int N, int C, int H, int W, float* y,
+                              neo_stream_t stream) {
+    CHECK_PTR(x);
+    CHECK_PTR(y);
+    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    if (!pow2_block(block))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_global_avgpool_nchwxc: block must be 4, 8, 16, 32 or 64");
+    CHECK_SIZE(blocked_elems(N, C, H, W, block));
+    hipError_t e = launch_gap(x, block, N, C, H, W, y, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_global_avgpool_nchwxc launch");
 }
 
 int neo_global_avgpool_blocked(const float* x, int N, int C, int H, int W, float* y,
                                neo_stream_t stream) {
-    CHECK_PTR(x);
-    CHECK_PTR(y);
-    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
-    CHECK_SIZE(blocked_elems(N, C, H, W, 16));
-    hipError_t e = launch_gap(x, N, C, H, W, y, (hipStream_t)stream);
-    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_global_avgpool_blocked launch");
+    return neo_global_avgpool_nchwxc(x, 16, N, C, H, W, y, stream);
 }
 
 int neo_dense(const float* x, int N, int IN, const float* w, int OUT, const float* bias, int act,

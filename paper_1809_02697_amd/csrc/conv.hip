@@ -94,9 +94,26 @@ struct ConvArgs {
     float* y;
     float* ws;  // split partials [SPLIT][N][KB][OH][OW][16]
     int N, CB, CBG, H, W, KB, R, S, RS, U, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act, T, split;
+    // Input NCHW[xb]c: XB blocks per image, xpb bytes per pixel block; the
+    // reduction's 16-channel group j starts at byte (j >> lq) * dblk +
+    // (j & qm) * 64 of the image (xb >= 16: Q = xb / 16 groups per block).
+    int xb, XB, xpb, lq, qm, dblk;
+    // Output and residual NCHW[yb]c (lyb = log2 yb): y_off / y_tot in blocks
+    // of yb; KBk 16-channel groups are stored (the ones past KB are the zero
+    // padding of the last block); the residual has KY blocks.
+    int yb, lyb, KBk, KY;
     int x_bytes, w_bytes;
     FastDiv div_ohw, div_ow, div_npx, div_nkb;
 };
+
+// Byte offset of the reduction's 16-channel group j inside an input image.
+__device__ inline int xgroup(const ConvArgs& a, int j) { return (j >> a.lq) * a.dblk + ((j & a.qm) << 6); }
+
+// Float index of channels c..c+3 (c a multiple of 4) of pixel pix = oh * OW +
+// ow of image n in an NCHW[yb]c tensor of `tot` blocks per image.
+__device__ inline int yindex(const ConvArgs& a, int n, int tot, int c, int pix) {
+    return ((n * tot + (c >> a.lyb)) * (a.OH * a.OW) + pix) * a.yb + (c & (a.yb - 1));
+}
 
 constexpr int kXcds = 8;
 constexpr unsigned kRsrcWord3 = 0x00020000;    // raw buffer, gfx9 family
@@ -142,7 +159,7 @@ __device__ inline float ld1(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff, i
 template <int FK, int FP, int G, bool SMALLC, bool WMFMA>
 struct Loader {
     __amdgpu_buffer_rsrc_t xr, wr;
-    int xoff[FP];                 // byte offset of the lane's pixel at (cb, r, s) = 0 (may be < 0)
+    int xoff[FP];                 // byte offset of the lane's pixel at (group, r, s) = 0 (may be < 0)
     unsigned rowm[FP], colm[FP];  // bit r / s set when that tap row / column is inside
     int pih[FP], piw[FP];
     unsigned woff[FK];            // byte offset of the lane's element in filter block (kb, 0, 0)
@@ -150,8 +167,9 @@ struct Loader {
     int lg;                       // lane group g (small-channel column offset)
     // position of the next step to load (wave-uniform)
     int st, cb, rs, r, s;         // small-channel path: s holds the column group u
-    int sx, sw;                   // step byte offsets: input cb*H*W*64, filter (cb*RS + rs)*1024
-    int dx, dw;                   // one channel block further: H*W*64 and RS*1024 bytes
+    int sx, sw;                   // step byte offsets: input group cb, filter (cb*RS + rs)*1024
+    int dw;                       // one channel group further in the filter: RS*1024 bytes
+    int ioff[G];                  // input offset of group cb + i from group cb (cb % G == 0)
     unsigned toff[FP];            // lane offset of the current tap, or out of range
     unsigned wtoff[FK];           // small-channel, KCRS[16]c[16]k filter: lane offset or out of range
 
@@ -167,7 +185,7 @@ struct Loader {
                 else
                     ok = cok && (unsigned)(pih[p] + r) < (unsigned)a.H &&
                          (unsigned)(piw[p] + sc) < (unsigned)a.W;
-                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + sc) * 64) : kOutOfRange;
+                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + sc) * a.xpb) : kOutOfRange;
             }
             if constexpr (!WMFMA) {
 #pragma unroll
@@ -181,7 +199,7 @@ struct Loader {
                     ok = ((rowm[p] >> r) & (colm[p] >> s) & 1u) != 0;
                 else
                     ok = (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
-                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + s) * 64) : kOutOfRange;
+                toff[p] = ok ? (unsigned)(xoff[p] + (r * a.W + s) * a.xpb) : kOutOfRange;
             }
         }
     }
@@ -216,11 +234,14 @@ struct Loader {
             cb = (st0 - rs * a.CBG) * G;
             r = rs / a.S;
             s = rs - r * a.S;
-            sx = cb * a.H * a.W * 64;
+            sx = xgroup(a, cb);
             sw = (cb * a.RS + rs) * 1024;
         }
-        dx = __builtin_amdgcn_readfirstlane(a.H * a.W * 64);
         dw = __builtin_amdgcn_readfirstlane(a.RS * 1024);
+        // cb stays a multiple of G and G, Q are powers of two, so group cb + i
+        // (i < G) lies xgroup(i) bytes past group cb
+#pragma unroll
+        for (int i = 0; i < G; ++i) ioff[i] = __builtin_amdgcn_readfirstlane(xgroup(a, i));
         pin();
         set_tap(a);
     }
@@ -235,7 +256,7 @@ struct Loader {
             pin();
             set_tap(a);
         } else if ((cb += G) < a.CB) {
-            sx += G * dx;
+            sx = xgroup(a, cb);
             sw += G * dw;
         } else {
             cb = 0;
@@ -254,7 +275,7 @@ struct Loader {
     __device__ void load(Operands<FK, FP, G>& o) const {
 #pragma unroll
         for (int i = 0; i < G; ++i) {
-            const int sxi = sx + i * dx, swi = sw + i * dw;
+            const int sxi = sx + ioff[i], swi = sw + i * dw;
 #pragma unroll
             for (int p = 0; p < FP; ++p) o.b[i][p] = ld4(xr, toff[p], sxi, 0);
 #pragma unroll
@@ -340,13 +361,14 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
         // taps r with 0 <= ih0 + r < H form the run [-ih0, H - ih0) of [0, R)
         tl.rowm[p] = run_mask(-ih0, a.H - ih0, a.R);
         tl.colm[p] = run_mask(-iw0, a.W - iw0, a.S);
-        // byte offset of this pixel's (cb = 0, r = 0, s = 0) element; only used
-        // (with a step offset added) when the tap is inside the input
-        tl.xoff[p] = ((n * a.CB * a.H + ih0) * a.W + iw0) * 64 + (SMALLC ? 0 : 16 * g);
+        // byte offset of this pixel's (group 0, r = 0, s = 0) element, the lane's
+        // channel quad 4g..4g+3 of the group; only used (with a step offset
+        // added) when the tap is inside the input
+        tl.xoff[p] = ((n * a.XB * a.H + ih0) * a.W + iw0) * a.xpb + (SMALLC ? 0 : 16 * g);
     }
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
-        const int kb = kb0 + f < a.KB ? kb0 + f : 0;  // past K: clamped, never stored
+        const int kb = kb0 + f < a.KB ? kb0 + f : 0;  // past K: clamped, result stored as zero
         if constexpr (SMALLC) {
             // kernel order: block (kb, r, u), lane's float4 at (g*16 + k)*4;
             // KCRS[16]c[16]k: block (kb, r, s = 4u + g), element [c][k]
@@ -380,7 +402,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
                     const int oh = (tl.pih[p] + a.ph) / a.sh;
                     const int ow = (tl.piw[p] + a.pw) / a.sw;
                     pre_r[f][p] = a.res ? *reinterpret_cast<const v4f*>(
-                                              a.res + (((pn[p] * a.KB + kb) * a.OH + oh) * a.OW + ow) * 16 + 4 * g)
+                                              a.res + yindex(a, pn[p], a.KY, kb * 16 + 4 * g, oh * a.OW + ow))
                                         : v4f{0.f, 0.f, 0.f, 0.f};
                 }
             }
@@ -475,11 +497,13 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kb0 + f;
-        if (kb >= a.KB) continue;
+        if (kb >= a.KBk) continue;
+        // groups past the last real one only fill the last output block with zeros
+        const bool real = kb < a.KB;
         v4f bb = v4f{0.f, 0.f, 0.f, 0.f};
         if constexpr (kPrefetch)
             bb = pre_b[f];
-        else if (a.bias)
+        else if (a.bias && real)
             bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
@@ -492,14 +516,15 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
                 o += pre_r[f][p];
             } else if (a.res) {
                 o += *reinterpret_cast<const v4f*>(
-                    a.res + (((n * a.KB + kb) * a.OH + oh) * a.OW + ow) * 16 + 4 * g);
+                    a.res + yindex(a, n, a.KY, kb * 16 + 4 * g, oh * a.OW + ow));
             }
             if (a.act == NEO_ACT_RELU) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
             }
+            if (!real) o = v4f{0.f, 0.f, 0.f, 0.f};
             *reinterpret_cast<v4f*>(
-                a.y + (((n * a.y_tot + a.y_off + kb) * a.OH + oh) * a.OW + ow) * 16 + 4 * g) = o;
+                a.y + yindex(a, n, a.y_tot, a.y_off * a.yb + kb * 16 + 4 * g, oh * a.OW + ow)) = o;
         }
     }
 }
@@ -509,35 +534,39 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
 // (pixel, 4-channel quad).
 __global__ __launch_bounds__(256) void split_reduce(ConvArgs a) {
     const int ohw = a.OH * a.OW;
-    const int total = a.N * a.KB * ohw * 4;
+    const int total = a.N * a.KBk * ohw * 4;
     const long zstride = (long)a.N * a.KB * ohw * 16;
     for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
         const int qd = t & 3;
-        const int pix = t >> 2;  // (n*KB + kb)*OH*OW + oh*OW + ow
+        const int pix = t >> 2;  // (n*KBk + kb)*OH*OW + oh*OW + ow
         const int sp = pix % ohw;
         const int nk = pix / ohw;
-        const int kb = nk % a.KB, n = nk / a.KB;
-        v4f o = *reinterpret_cast<const v4f*>(a.ws + pix * 16 + 4 * qd);
-        for (int z = 1; z < a.split; ++z)
-            o += *reinterpret_cast<const v4f*>(a.ws + z * zstride + pix * 16 + 4 * qd);
-        if (a.bias) o += *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * qd);
-        if (a.res) o += *reinterpret_cast<const v4f*>(a.res + pix * 16 + 4 * qd);
-        if (a.act == NEO_ACT_RELU) {
+        const int kb = nk % a.KBk, n = nk / a.KBk;
+        v4f o = v4f{0.f, 0.f, 0.f, 0.f};
+        if (kb < a.KB) {  // past KB: the zero padding of the last output block
+            const int part = ((n * a.KB + kb) * ohw + sp) * 16 + 4 * qd;
+            o = *reinterpret_cast<const v4f*>(a.ws + part);
+            for (int z = 1; z < a.split; ++z)
+                o += *reinterpret_cast<const v4f*>(a.ws + z * zstride + part);
+            if (a.bias) o += *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * qd);
+            if (a.res) o += *reinterpret_cast<const v4f*>(a.res + yindex(a, n, a.KY, kb * 16 + 4 * qd, sp));
+            if (a.act == NEO_ACT_RELU) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
+                for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
+            }
         }
-        *reinterpret_cast<v4f*>(a.y + ((n * a.y_tot + a.y_off + kb) * ohw + sp) * 16 + 4 * qd) = o;
+        *reinterpret_cast<v4f*>(a.y + yindex(a, n, a.y_tot, a.y_off * a.yb + kb * 16 + 4 * qd, sp)) = o;
     }
 }
 
 template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES>
 hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
-    const int wgs = cdiv(a.M, 16 * FP) * cdiv(a.KB, FK) * a.split;
+    const int wgs = cdiv(a.M, 16 * FP) * cdiv(a.KBk, FK) * a.split;
     hipLaunchKernelGGL((conv2d_mfma<FK, FP, G, SMALLC, WMFMA, WAVES>), dim3(wgs), dim3(WAVES * 64),
                        0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.split == 1) return e;
-    const long total = (long)a.N * a.KB * a.OH * a.OW * 4;
+    const long total = (long)a.N * a.KBk * a.OH * a.OW * 4;
     long blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(split_reduce, dim3((unsigned)blocks), dim3(256), 0, st, a);
@@ -666,7 +695,7 @@ size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c) {
 hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st) {
-    if (!conv_config_valid(c)) return hipErrorInvalidValue;
+    if (!conv_config_valid(c) || !conv_blocks_valid(s)) return hipErrorInvalidValue;
     ConvArgs a;
     a.x = x;
     a.w = w;
@@ -697,12 +726,23 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.CBG = a.CB / G;
     a.T = conv_steps(s, c);
     a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
-    a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 64);
+    a.xb = s.xb;
+    a.XB = cdiv(s.C, s.xb);
+    a.xpb = s.xb * 4;
+    const int Q = s.xb >= 16 ? s.xb / 16 : 1;
+    a.lq = ilog2(Q);
+    a.qm = Q - 1;
+    a.dblk = s.H * s.W * a.xpb;
+    a.yb = s.yb;
+    a.lyb = ilog2(s.yb);
+    a.KY = cdiv(s.K, s.yb);
+    a.KBk = a.KY * s.yb / 16;
+    a.x_bytes = (int)((long)s.N * a.XB * s.H * s.W * a.xpb);
     a.w_bytes = (int)((wmfma ? kernel_filter_floats(s) : (long)a.KB * a.CB * a.RS * 256) * 4);
     a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
-    a.div_nkb = make_fastdiv((unsigned)cdiv(a.KB, c.fk));
+    a.div_nkb = make_fastdiv((unsigned)cdiv(a.KBk, c.fk));
     const bool small = conv_small_c(s);
     if (wmfma) return small ? dispatch<true, true>(c, G, a, st) : dispatch<false, true>(c, G, a, st);
     return small ? dispatch<true, false>(c, G, a, st) : dispatch<false, false>(c, G, a, st);

@@ -6,7 +6,9 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <functional>
 #include <string>
+#include <vector>
 
 #include "../../include/neo.h"
 
@@ -18,15 +20,23 @@ int fail(int code, const std::string& msg);
 int hip_fail(hipError_t e, const char* what);
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+// log2 of a power of two
+inline int ilog2(int v) {
+    int l = 0;
+    while ((1 << l) < v) ++l;
+    return l;
+}
+inline bool pow2_block(int b) { return b == 4 || b == 8 || b == 16 || b == 32 || b == 64; }
 
 // ---- convolution ----------------------------------------------------------------------
 struct ConvShape {
-    int N, C, H, W;      // input (C real channels; CB = ceil(C/16) blocks)
+    int N, C, H, W;      // input (C real channels)
     int K, R, S;         // filter
     int sh, sw, ph, pw;  // stride, pad
     int OH, OW;
-    int y_off, y_tot;    // output channel-block view
+    int y_off, y_tot;    // output channel-block view, in blocks of yb
     int act;
+    int xb = 16, yb = 16;  // input layout NCHW[xb]c, output (and residual) NCHW[yb]c
 };
 
 // Launch configuration: register tile (fk channel blocks x fp pixel groups of
@@ -40,6 +50,13 @@ bool conv_config_valid(const ConvConfig& c);
 // a reduction step is (filter row r, group u of 4 filter columns) instead of
 // (channel block, kernel entry).
 inline bool conv_small_c(const ConvShape& s) { return s.C <= 4; }
+// Blocks the kernel reads and writes: output 16, 32 or 64; input 16, 32 or 64
+// (any of 4..64 on the small-channel path, which reads channels 0..3 only).
+inline bool conv_blocks_valid(const ConvShape& s) {
+    const bool yok = s.yb == 16 || s.yb == 32 || s.yb == 64;
+    const bool xok = conv_small_c(s) ? pow2_block(s.xb) : (s.xb == 16 || s.xb == 32 || s.xb == 64);
+    return xok && yok;
+}
 // Channel blocks per reduction step for a launch configuration (1 on the
 // small-channel path), and the reduction steps of one output tile.
 int conv_group(const ConvShape& s, const ConvConfig& c);
@@ -48,20 +65,22 @@ ConvConfig choose_conv_config(const ConvShape& s);
 // Workspace of a split reduction (partial sums of every split), in bytes.
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);
 
-// Launch the blocked convolution.  x: NCHW16c; w: KCRS[16]c[16]k, or with
-// wmfma the kernel's own filter order (to_kernel_order); bias: [KB*16] or null; res: NCHW16c
-// [N][KB][OH][OW][16] or null; y: NCHW16c view.  ws: workspace of at least
-// conv_workspace_bytes (a split is only used when it is given).  x and w must
-// each be below 2 GiB.
+// Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
+// wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
+// or null; res: NCHW[yb]c [N][ceil(K/yb)][OH][OW][yb] or null; y: NCHW[yb]c
+// view (padding lanes of the last block written as 0).  ws: workspace of at
+// least conv_workspace_bytes (a split is only used when it is given).  x and w
+// must each be below 2 GiB.
 hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st);
 
-// Local search (tune.cpp): the database's configuration for a shape, if any;
-// and a search that times every candidate with the given buffers on `st`.
+// Local search (tune.cpp): the database's configuration for a shape (with its
+// blocks), if any; and a search that times every candidate with the given
+// buffers on `st` and returns the fastest with its time per launch in us.
 bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out);
 int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
-              const float* res, float* y, hipStream_t st, ConvConfig* best);
+              const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
 
 // ---- layout ---------------------------------------------------------------------------
 // dst_off / dst_tot: destination channel view in destination units (channels
@@ -74,12 +93,36 @@ hipError_t launch_pack_filter(const float* w, int K, int C, int R, int S, int ib
                               float* out, hipStream_t st);
 
 // ---- pools ----------------------------------------------------------------------------
+// Input and output in NCHW[xb]c (xb in 4..64); y_off / y_tot in blocks.
 struct PoolShape {
     int N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot;
+    int xb = 16;
 };
 hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
 hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
-hipError_t launch_gap(const float* x, int N, int C, int H, int W, float* y, hipStream_t st);
+hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st);
+
+// ---- global layout search (search.cpp) -----------------------------------------------------
+struct SearchNode {
+    int op = 0;
+    std::vector<int> inputs;
+    int residual = -1;
+    int N = 0, C = 0, H = 0, W = 0;  // shape of the node's value
+};
+// conv: (node, ic index, oc index) -> time, not finite or < 0 = no candidate;
+// transform: (node, from index, to index) -> time.  Indices into kSearchBlocks.
+using SearchCost = std::function<double(int, int, int)>;
+extern const int kSearchBlocks[NEO_SEARCH_NB];
+int search_block_index(int block);
+// A transform that leaves the bytes where they are (1x1 map whose channel
+// count both blocks divide), unless it writes into a concat slice.
+bool layout_alias(int C, int H, int W, int src, int dst, bool into_concat);
+// Algorithm 2 over `order` (a topological order of g); ic / oc receive the
+// chosen blocks (0 for non-conv nodes), cost the optimum, max_states the
+// widest layer of the program.
+int layout_search_dp(const std::vector<SearchNode>& g, const std::vector<int>& order,
+                     int default_block, const SearchCost& conv_cost, const SearchCost& xform_cost,
+                     std::vector<int>* ic, std::vector<int>* oc, double* cost, long* max_states);
 
 // ---- dense ----------------------------------------------------------------------------
 hipError_t launch_dense(const float* x, int N, int IN, const float* w, int OUT,

@@ -1,20 +1,27 @@
-// Graph plan and runtime: layout-transformation elimination (Section 3.2).
+// Graph plan and runtime: layout-transformation elimination (Section 3.2) and
+// the global layout search (Section 3.3.2).
 //
 // The planner walks the network in topological order and infers the layout of
 // every value from the operation categories of Section 3.2:
-//   - layout tolerant (convolution, max/avg pooling, global average pooling):
-//     run in NCHW16c, one constant block for every convolution;
-//   - layout oblivious (concatenation): follows its inputs (NCHW16c when every
-//     input has a whole number of 16-channel blocks, otherwise it needs the
-//     default layout);
+//   - convolution: runs in NCHW[x]c, reading its input in NCHW[ic_bn]c and its
+//     residual in NCHW[oc_bn]c and writing NCHW[oc_bn]c, where (ic_bn, oc_bn)
+//     is its scheme: given by the caller, chosen by the global search, or
+//     (block, block) with one constant block for every convolution;
+//   - layout tolerant (max/avg pooling, global average pooling): run in the
+//     layout their input arrives in (the plan's block if that is NCHW);
+//   - layout oblivious (concatenation): takes the layout of its first input
+//     when every input is a whole number of its blocks (else the plan's block,
+//     else NCHW) and the other inputs are converted to it;
 //   - layout dependent (flatten, dense, the network output): default layout.
 // A LayoutTransform step is inserted only where a consumer needs a layout the
-// value does not have yet (once per value and layout), so a CNN gets one
-// transform at its input and one before flatten.  Parameters are prepared once
-// (Section 3.2: model parameters are pre-transformed at compile time): batch
-// norm folded, filters packed to KCRS[16]c[16]k.  Concatenation costs no
-// step: its producers write straight into channel slices of its buffer.
+// value does not have yet (once per value and layout), so with one block a
+// CNN gets one transform at its input and one before flatten.  Parameters are
+// prepared once (Section 3.2: model parameters are pre-transformed at compile
+// time): batch norm folded, filters packed to KCRS[16]c[16]k.  Concatenation
+// costs no step: its producers write straight into channel slices of its
+// buffer.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -34,7 +41,7 @@ enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE,
 
 struct Val {
     int N = 0, C = 0, H = 0, W = 0;
-    int layout = 0;     // 0 = NCHW, 16 = NCHW16c
+    int layout = 0;     // 0 = NCHW, x > 0 = NCHW[x]c
     int node = -1;      // node whose result this is (a version of it)
     int alias_of = -1;  // shares the storage of this value (identity transform, flatten)
     int buf = -1;       // root buffer, or kExtIn
@@ -68,7 +75,8 @@ struct NodeInfo {
     neo_node nd;
     std::vector<int> inputs;
     int N = 0, C = 0, H = 0, W = 0;
-    int val = -1;  // canonical value of the node
+    int val = -1;         // canonical value of the node
+    int ic = 0, oc = 0;   // conv scheme (input / output block), 0 = not chosen yet
 };
 
 const char* op_name(int op) {
@@ -104,6 +112,12 @@ struct neo_plan {
     hipGraphExec_t graph_exec = nullptr;
     const float* graph_x = nullptr;
     float* graph_y = nullptr;
+    // NEO_PLAN_GLOBAL_SEARCH: predicted totals (us) of the chosen schemes and of
+    // every conv at the plan's block, schemes measured, largest DP layer
+    bool searched = false;
+    double search_cost = 0, fixed_cost = 0;
+    int search_schemes = 0;
+    long search_states = 0;
 };
 
 static int tune_plan(neo_plan* P);
@@ -122,10 +136,14 @@ long align_up(long v, long a) { return (v + a - 1) / a * a; }
 
 long val_elems_root(const Val& v) {
     // element count of a full (non-view) buffer holding v
-    return v.layout ? (long)v.N * cdiv(v.C, 16) * 16 * v.H * v.W : (long)v.N * v.C * v.H * v.W;
+    return v.layout ? (long)v.N * cdiv(v.C, v.layout) * v.layout * v.H * v.W
+                    : (long)v.N * v.C * v.H * v.W;
 }
 
 int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
+
+// Channel extent of a value in units of its layout (blocks, or channels).
+int units(int C, int layout) { return layout ? cdiv(C, layout) : C; }
 
 struct Builder {
     neo_plan* P;
@@ -141,7 +159,7 @@ struct Builder {
     }
 
     // The version of node `nid`'s value in `layout`, inserting a transform
-    // for consumer `consumer` if needed.
+    // (from the node's canonical value) for consumer `consumer` if needed.
     int get(int nid, int layout, int consumer) {
         auto& m = versions[nid];
         auto it = m.find(layout);
@@ -149,8 +167,8 @@ struct Builder {
         const int src = P->nodes[nid].val;
         const Val s = P->vals[src];
         const int v = new_val(nid, s.N, s.C, s.H, s.W, layout);
-        const bool identity = s.H * s.W == 1 && s.C % 16 == 0 &&
-                              P->nodes[consumer].nd.op != NEO_OP_CONCAT;
+        const bool identity = layout_alias(s.C, s.H, s.W, s.layout, layout,
+                                           P->nodes[consumer].nd.op == NEO_OP_CONCAT);
         Xform x{src, v, s.layout, layout, consumer, identity};
         P->xforms.push_back(x);
         if (identity) {
@@ -172,14 +190,15 @@ struct Builder {
     // Register a node's produced value; in a naive plan a blocked result is
     // transformed back to the default layout right away.
     void produce(int nid, int v) {
-        versions[nid][P->vals[v].layout] = v;
+        const int lay = P->vals[v].layout;
+        versions[nid][lay] = v;
         P->nodes[nid].val = v;
-        if ((P->flags & NEO_PLAN_NAIVE) && P->vals[v].layout == 16) {
+        if ((P->flags & NEO_PLAN_NAIVE) && lay != 0) {
             // the blocked result is only read by its transform back; every
             // blocked consumer transforms the default-layout copy again
             const int pv = get(nid, 0, nid);
             P->nodes[nid].val = pv;
-            versions[nid].erase(16);
+            versions[nid].erase(lay);
         }
     }
 };
@@ -191,8 +210,10 @@ int add_params(neo_plan* P, const std::vector<float>& a) {
     return (int)off;
 }
 
-int build(neo_plan* P, const neo_node* nodes, int n) {
-    // ---- validate and copy nodes ----------------------------------------------------
+// ---- pass 1: validate, copy, order, shapes ----------------------------------------------
+// need_params: convs and dense layers must carry weights (a plan); the layout
+// search alone needs only the structure.
+int parse(neo_plan* P, const neo_node* nodes, int n, bool need_params) {
     int n_in = 0, n_out = 0;
     P->nodes.resize(n);
     for (int i = 0; i < n; ++i) {
@@ -215,13 +236,18 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
         if (d.op == NEO_OP_CONV) {
             if (d.residual < -1 || d.residual >= n || d.residual == i)
                 return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": bad residual id");
-            if (!d.w) return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": conv without weights");
+            if (need_params && !d.w)
+                return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": conv without weights");
             const bool any = d.bn_gamma || d.bn_beta || d.bn_mean || d.bn_var;
             const bool all = d.bn_gamma && d.bn_beta && d.bn_mean && d.bn_var;
             if (any && !all)
                 return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": partial batch-norm parameters");
+            if ((d.ic_bn == 0) != (d.oc_bn == 0))
+                return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": ic_bn and oc_bn must both be 0 or both set");
+            ni.ic = d.ic_bn;
+            ni.oc = d.oc_bn;
         }
-        if (d.op == NEO_OP_DENSE && !d.w)
+        if (need_params && d.op == NEO_OP_DENSE && !d.w)
             return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": dense without weights");
         if ((d.op == NEO_OP_CONV || d.op == NEO_OP_DENSE) && d.act != NEO_ACT_NONE && d.act != NEO_ACT_RELU)
             return fail(NEO_ERR_INVALID_ARG, "node " + std::to_string(i) + ": unknown activation");
@@ -231,7 +257,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
     if (n_in != 1 || n_out != 1)
         return fail(NEO_ERR_INVALID_ARG, "plan needs exactly one input and one output node");
 
-    // ---- topological order (Kahn; ties by node id) -----------------------------------
+    // topological order (Kahn; ties by node id)
     std::vector<std::vector<int>> succ(n);
     std::vector<int> indeg(n, 0);
     for (int i = 0; i < n; ++i) {
@@ -255,17 +281,104 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
     }
     if ((int)P->order.size() != n) return fail(NEO_ERR_INVALID_ARG, "network has a cycle");
 
-    // ---- shapes, layouts, steps -------------------------------------------------------
-    Builder B{P, std::vector<std::map<int, int>>(n)};
-    const bool naive = P->flags & NEO_PLAN_NAIVE;
+    // shapes
     for (int id : P->order) {
         NodeInfo& ni = P->nodes[id];
         const neo_node& d = ni.nd;
         const std::string where = std::string("node ") + std::to_string(id) + " (" + op_name(d.op) + "): ";
-        auto in_shape = [&](int j) { return &P->nodes[ni.inputs[j]]; };
+        const NodeInfo* a = ni.inputs.empty() ? nullptr : &P->nodes[ni.inputs[0]];
+        switch (d.op) {
+            case NEO_OP_INPUT:
+                ni.N = P->N; ni.C = P->C; ni.H = P->H; ni.W = P->W;
+                break;
+            case NEO_OP_CONV:
+            case NEO_OP_MAXPOOL:
+            case NEO_OP_AVGPOOL: {
+                const bool conv = d.op == NEO_OP_CONV;
+                if ((conv && d.K <= 0) || d.R <= 0 || d.S <= 0 || d.stride_h <= 0 || d.stride_w <= 0 ||
+                    d.pad_h < 0 || d.pad_w < 0)
+                    return fail(NEO_ERR_INVALID_ARG, where + (conv ? "bad conv parameters" : "bad pool parameters"));
+                if (!conv && (d.pad_h >= d.R || d.pad_w >= d.S))
+                    return fail(NEO_ERR_INVALID_ARG, where + "bad pool parameters");
+                const int OH = out_dim(a->H, d.R, d.stride_h, d.pad_h);
+                const int OW = out_dim(a->W, d.S, d.stride_w, d.pad_w);
+                if (a->H + 2 * d.pad_h < d.R || a->W + 2 * d.pad_w < d.S || OH < 1 || OW < 1)
+                    return fail(NEO_ERR_SHAPE, where + "empty output");
+                ni.N = a->N; ni.C = conv ? d.K : a->C; ni.H = OH; ni.W = OW;
+                if (conv && d.residual >= 0) {
+                    const NodeInfo* r = &P->nodes[d.residual];
+                    if (r->N != ni.N || r->C != ni.C || r->H != ni.H || r->W != ni.W)
+                        return fail(NEO_ERR_SHAPE, where + "residual shape differs from the output");
+                }
+                if (conv && ni.ic) {
+                    ConvShape cs{};
+                    cs.C = a->C;
+                    cs.xb = ni.ic;
+                    cs.yb = ni.oc;
+                    if (!conv_blocks_valid(cs))
+                        return fail(NEO_ERR_UNSUPPORTED, where + "ic_bn / oc_bn not supported by the kernel");
+                }
+                break;
+            }
+            case NEO_OP_GAP:
+                ni.N = a->N; ni.C = a->C; ni.H = 1; ni.W = 1;
+                break;
+            case NEO_OP_CONCAT: {
+                int C = 0;
+                for (int j : ni.inputs) {
+                    const NodeInfo* b = &P->nodes[j];
+                    if (b->N != a->N || b->H != a->H || b->W != a->W)
+                        return fail(NEO_ERR_SHAPE, where + "inputs differ in N, H or W");
+                    C += b->C;
+                }
+                ni.N = a->N; ni.C = C; ni.H = a->H; ni.W = a->W;
+                break;
+            }
+            case NEO_OP_FLATTEN:
+                ni.N = a->N; ni.C = a->C * a->H * a->W; ni.H = 1; ni.W = 1;
+                break;
+            case NEO_OP_DENSE:
+                if (a->H != 1 || a->W != 1)
+                    return fail(NEO_ERR_SHAPE, where + "input must be flat (insert a flatten)");
+                if (d.K <= 0) return fail(NEO_ERR_INVALID_ARG, where + "K must be > 0");
+                ni.N = a->N; ni.C = d.K; ni.H = 1; ni.W = 1;
+                break;
+            case NEO_OP_OUTPUT:
+                ni.N = a->N; ni.C = a->C; ni.H = a->H; ni.W = a->W;
+                break;
+        }
+    }
+    return NEO_OK;
+}
+
+// The network as the layout search sees it.
+std::vector<SearchNode> search_nodes(const neo_plan* P) {
+    std::vector<SearchNode> g(P->nodes.size());
+    for (size_t i = 0; i < P->nodes.size(); ++i) {
+        const NodeInfo& ni = P->nodes[i];
+        g[i].op = ni.nd.op;
+        g[i].inputs = ni.inputs;
+        g[i].residual = ni.nd.op == NEO_OP_CONV ? ni.nd.residual : -1;
+        g[i].N = ni.N; g[i].C = ni.C; g[i].H = ni.H; g[i].W = ni.W;
+    }
+    return g;
+}
+
+// ---- pass 2: steps, values, buffers --------------------------------------------------------
+int build_steps(neo_plan* P) {
+    const int n = (int)P->nodes.size();
+    Builder B{P, std::vector<std::map<int, int>>(n)};
+    const bool naive = P->flags & NEO_PLAN_NAIVE;
+    const int D = P->block;
+    for (int id : P->order) {
+        NodeInfo& ni = P->nodes[id];
+        const neo_node& d = ni.nd;
+        const std::string where = std::string("node ") + std::to_string(id) + " (" + op_name(d.op) + "): ";
+        const NodeInfo* a = ni.inputs.empty() ? nullptr : &P->nodes[ni.inputs[0]];
+        // layout of an input as it arrives (its canonical value)
+        auto arriving = [&](int j) { return P->vals[P->nodes[ni.inputs[j]].val].layout; };
         switch (d.op) {
             case NEO_OP_INPUT: {
-                ni.N = P->N; ni.C = P->C; ni.H = P->H; ni.W = P->W;
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 0);
                 P->vals[v].buf = kExtIn;
                 P->input_val = v;
@@ -274,25 +387,15 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 break;
             }
             case NEO_OP_CONV: {
-                const NodeInfo* a = in_shape(0);
-                if (d.K <= 0 || d.R <= 0 || d.S <= 0 || d.stride_h <= 0 || d.stride_w <= 0 ||
-                    d.pad_h < 0 || d.pad_w < 0)
-                    return fail(NEO_ERR_INVALID_ARG, where + "bad conv parameters");
-                const int OH = out_dim(a->H, d.R, d.stride_h, d.pad_h);
-                const int OW = out_dim(a->W, d.S, d.stride_w, d.pad_w);
-                if (a->H + 2 * d.pad_h < d.R || a->W + 2 * d.pad_w < d.S || OH < 1 || OW < 1)
-                    return fail(NEO_ERR_SHAPE, where + "empty output");
-                ni.N = a->N; ni.C = d.K; ni.H = OH; ni.W = OW;
+                if (!ni.ic) {
+                    ni.ic = D;
+                    ni.oc = D;
+                }
                 Step st{};
                 st.kind = ST_CONV;
                 st.node = id;
-                st.in = B.get(ni.inputs[0], 16, id);
-                if (d.residual >= 0) {
-                    const NodeInfo* r = &P->nodes[d.residual];
-                    if (r->N != ni.N || r->C != ni.C || r->H != ni.H || r->W != ni.W)
-                        return fail(NEO_ERR_SHAPE, where + "residual shape differs from the output");
-                    st.res = B.get(d.residual, 16, id);
-                }
+                st.in = B.get(ni.inputs[0], ni.ic, id);
+                if (d.residual >= 0) st.res = B.get(d.residual, ni.oc, id);
                 const int C = a->C;
                 std::vector<float> w((long)d.K * C * d.R * d.S), b(cdiv(d.K, 16) * 16, 0.f);
                 bool has_b = false;
@@ -311,10 +414,13 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                     }
                 }
                 const long nblk = (long)cdiv(d.K, 16) * cdiv(C, 16) * d.R * d.S;
-                if (nblk * 256 >= (1L << 29) || (long)ni.N * cdiv(C, 16) * a->H * a->W * 16 >= (1L << 29))
+                if (nblk * 256 >= (1L << 29) ||
+                    (long)ni.N * cdiv(C, ni.ic) * ni.ic * a->H * a->W >= (1L << 29))
                     return fail(NEO_ERR_UNSUPPORTED, where + "input or filter of 2 GiB or more");
                 st.cs = ConvShape{ni.N, C, a->H, a->W, d.K, d.R, d.S, d.stride_h, d.stride_w,
-                                  d.pad_h, d.pad_w, OH, OW, 0, cdiv(d.K, 16), d.act};
+                                  d.pad_h, d.pad_w, ni.H, ni.W, 0, cdiv(d.K, ni.oc), d.act};
+                st.cs.xb = ni.ic;
+                st.cs.yb = ni.oc;
                 std::vector<float> wp(nblk * 256), wm(kernel_filter_floats(st.cs));
                 pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
                 to_kernel_order(wp.data(), st.cs, wm.data());  // one float4 per lane and k-quad
@@ -322,7 +428,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 if (has_b) st.b_off = add_params(P, b);
                 st.cc = choose_conv_config(st.cs);
                 if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
-                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, ni.oc);
                 st.out = v;
                 P->steps.push_back(st);
                 B.produce(id, v);
@@ -330,53 +436,45 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
             }
             case NEO_OP_MAXPOOL:
             case NEO_OP_AVGPOOL: {
-                const NodeInfo* a = in_shape(0);
-                if (d.R <= 0 || d.S <= 0 || d.stride_h <= 0 || d.stride_w <= 0 || d.pad_h < 0 ||
-                    d.pad_w < 0 || d.pad_h >= d.R || d.pad_w >= d.S)
-                    return fail(NEO_ERR_INVALID_ARG, where + "bad pool parameters");
-                const int OH = out_dim(a->H, d.R, d.stride_h, d.pad_h);
-                const int OW = out_dim(a->W, d.S, d.stride_w, d.pad_w);
-                if (a->H + 2 * d.pad_h < d.R || a->W + 2 * d.pad_w < d.S || OH < 1 || OW < 1)
-                    return fail(NEO_ERR_SHAPE, where + "empty output");
-                ni.N = a->N; ni.C = a->C; ni.H = OH; ni.W = OW;
+                const int lay = arriving(0) ? arriving(0) : D;
                 Step st{};
                 st.kind = d.op == NEO_OP_MAXPOOL ? ST_MAXPOOL : ST_AVGPOOL;
                 st.node = id;
-                st.in = B.get(ni.inputs[0], 16, id);
+                st.in = B.get(ni.inputs[0], lay, id);
                 st.ps = PoolShape{ni.N, ni.C, a->H, a->W, d.R, d.S, d.stride_h, d.stride_w,
-                                  d.pad_h, d.pad_w, OH, OW, 0, cdiv(ni.C, 16)};
-                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, 16);
+                                  d.pad_h, d.pad_w, ni.H, ni.W, 0, cdiv(ni.C, lay)};
+                st.ps.xb = lay;
+                const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, lay);
                 st.out = v;
                 P->steps.push_back(st);
                 B.produce(id, v);
                 break;
             }
             case NEO_OP_GAP: {
-                const NodeInfo* a = in_shape(0);
-                ni.N = a->N; ni.C = a->C; ni.H = 1; ni.W = 1;
+                const int lay = arriving(0) ? arriving(0) : D;
                 Step st{};
                 st.kind = ST_GAP;
                 st.node = id;
-                st.in = B.get(ni.inputs[0], 16, id);
-                const int v = B.new_val(id, ni.N, ni.C, 1, 1, 16);
+                st.in = B.get(ni.inputs[0], lay, id);
+                const int v = B.new_val(id, ni.N, ni.C, 1, 1, lay);
                 st.out = v;
                 P->steps.push_back(st);
                 B.produce(id, v);
                 break;
             }
             case NEO_OP_CONCAT: {
-                const NodeInfo* a0 = in_shape(0);
-                int C = 0;
-                bool whole = true;
-                for (size_t j = 0; j < ni.inputs.size(); ++j) {
-                    const NodeInfo* a = in_shape(j);
-                    if (a->N != a0->N || a->H != a0->H || a->W != a0->W)
-                        return fail(NEO_ERR_SHAPE, where + "inputs differ in N, H or W");
-                    C += a->C;
-                    whole = whole && (a->C % 16 == 0);
+                auto whole = [&](int L) {
+                    for (int j : ni.inputs)
+                        if (P->nodes[j].C % L) return false;
+                    return true;
+                };
+                int layout = 0;
+                if (!naive) {
+                    if (arriving(0) > 0 && whole(arriving(0)))
+                        layout = arriving(0);
+                    else if (whole(D))
+                        layout = D;
                 }
-                ni.N = a0->N; ni.C = C; ni.H = a0->H; ni.W = a0->W;
-                const int layout = (whole && !naive) ? 16 : 0;
                 for (size_t j = 0; j < ni.inputs.size(); ++j) B.get(ni.inputs[j], layout, id);
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, layout);
                 B.versions[id][layout] = v;
@@ -384,8 +482,6 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 break;
             }
             case NEO_OP_FLATTEN: {
-                const NodeInfo* a = in_shape(0);
-                ni.N = a->N; ni.C = a->C * a->H * a->W; ni.H = 1; ni.W = 1;
                 const int src = B.get(ni.inputs[0], 0, id);
                 const int v = B.new_val(id, ni.N, ni.C, 1, 1, 0);
                 P->vals[v].alias_of = src;
@@ -394,11 +490,6 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 break;
             }
             case NEO_OP_DENSE: {
-                const NodeInfo* a = in_shape(0);
-                if (a->H != 1 || a->W != 1)
-                    return fail(NEO_ERR_SHAPE, where + "input must be flat (insert a flatten)");
-                if (d.K <= 0) return fail(NEO_ERR_INVALID_ARG, where + "K must be > 0");
-                ni.N = a->N; ni.C = d.K; ni.H = 1; ni.W = 1;
                 Step st{};
                 st.kind = ST_DENSE;
                 st.node = id;
@@ -416,8 +507,6 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
                 break;
             }
             case NEO_OP_OUTPUT: {
-                const NodeInfo* a = in_shape(0);
-                ni.N = a->N; ni.C = a->C; ni.H = a->H; ni.W = a->W;
                 const int src = B.get(ni.inputs[0], 0, id);
                 P->out_val = src;
                 ni.val = src;
@@ -449,7 +538,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
         Val& cv = P->vals[ni.val];
         if (!cv.view) {
             cv.c_off = 0;
-            cv.c_tot = cv.layout ? cdiv(cv.C, 16) : cv.C;
+            cv.c_tot = units(cv.C, cv.layout);
         }
         int off = cv.c_off;
         for (int j : ni.inputs) {
@@ -463,7 +552,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
             uv.c_off = off;
             uv.c_tot = cv.c_tot;
             uv.buf = -3 - ni.val;  // resolved below to the concat value's root
-            off += cv.layout ? cdiv(uv.C, 16) : uv.C;
+            off += units(uv.C, cv.layout);
         }
     }
     // own buffers for roots
@@ -472,7 +561,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
         if (v.alias_of >= 0 || v.buf == kExtIn || v.view) continue;
         v.buf = (int)P->buf_bytes.size();
         v.c_off = 0;
-        v.c_tot = v.layout ? cdiv(v.C, 16) : v.C;
+        v.c_tot = units(v.C, v.layout);
         P->buf_bytes.push_back(val_elems_root(v) * 4);
     }
     // resolve views (a view's concat value may itself be a view: walk outward)
@@ -482,8 +571,9 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
         while (b <= -3) b = P->vals[-3 - b].buf;
         v.buf = b;
     }
-    // aliases share their source's storage (units converted if the layout differs;
-    // only 1x1 spatial maps with whole blocks are aliased, where both coincide)
+    // aliases share their source's storage (units converted if the layout
+    // differs; only 1x1 maps whose channel count both blocks divide are
+    // aliased, where the two layouts coincide)
     for (size_t i = 0; i < P->vals.size(); ++i) {
         Val& v = P->vals[i];
         if (v.alias_of < 0) continue;
@@ -492,7 +582,7 @@ int build(neo_plan* P, const neo_node* nodes, int n) {
         const Val& s = P->vals[r];
         v.buf = s.buf;
         v.view = s.view;
-        const int f_s = s.layout ? 16 : 1, f_v = v.layout ? 16 : 1;
+        const int f_s = s.layout ? s.layout : 1, f_v = v.layout ? v.layout : 1;
         v.c_off = s.c_off * f_s / f_v;
         v.c_tot = s.c_tot * f_s / f_v;
     }
@@ -539,7 +629,7 @@ float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
 
 std::string describe(const neo_plan* P) {
     std::ostringstream o;
-    auto lay = [](int l) { return l ? "NCHW16c" : "NCHW"; };
+    auto lay = [](int l) { return l ? "NCHW" + std::to_string(l) + "c" : std::string("NCHW"); };
     o << "{\"input\":[" << P->N << "," << P->C << "," << P->H << "," << P->W << "],";
     o << "\"block\":" << P->block << ",\"naive\":" << ((P->flags & NEO_PLAN_NAIVE) ? "true" : "false");
     o << ",\"host_only\":" << ((P->flags & NEO_PLAN_HOST_ONLY) ? "true" : "false");
@@ -585,6 +675,7 @@ std::string describe(const neo_plan* P) {
               << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
               << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
+              << ",\"ic_bn\":" << c.xb << ",\"oc_bn\":" << c.yb
               << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
               << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false") << "}";
         }
@@ -595,13 +686,225 @@ std::string describe(const neo_plan* P) {
     o << "],\"buffers\":[";
     for (size_t i = 0; i < P->buf_bytes.size(); ++i) o << (i ? "," : "") << P->buf_bytes[i];
     o << "],\"activation_bytes\":" << P->act_bytes << ",\"param_bytes\":" << P->params.size() * 4
-      << ",\"output_buffer\":" << P->ext_out_buf << "}";
+      << ",\"output_buffer\":" << P->ext_out_buf;
+    if (P->searched)
+        o << ",\"search\":{\"cost_us\":" << P->search_cost << ",\"fixed_block_cost_us\":"
+          << P->fixed_cost << ",\"schemes_measured\":" << P->search_schemes
+          << ",\"max_states\":" << P->search_states << "}";
+    o << "}";
     return o.str();
+}
+
+// Candidate split factors of a channel count (Section 3.3.1: its factors) among
+// the blocks the conv kernel implements, always with the plan's block; an
+// input of at most 4 channels (the small-channel path) also takes 4.
+std::vector<int> candidate_blocks(int C, int D, bool input_side) {
+    std::vector<int> out;
+    if (input_side && C <= 4) out.push_back(4);
+    for (int b : {16, 32, 64})
+        if (b == D || (!(input_side && C <= 4) && C % b == 0 && b < C)) out.push_back(b);
+    return out;
+}
+
+// Average time of `reps` back-to-back launches of fn captured in one graph,
+// best of 3 replays, on stream st (us); a negative value on a HIP error.
+template <class F>
+double time_launches(hipStream_t st, F fn, int reps = 10) {
+    hipError_t e = fn();
+    if (e != hipSuccess) return -1;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+    for (int i = 0; i < reps && e == hipSuccess; ++i) e = fn();
+    hipError_t e2 = hipStreamEndCapture(st, &g);
+    if (e == hipSuccess) e = e2;
+    if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    if (g) (void)hipGraphDestroy(g);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (e == hipSuccess) e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    float best = 1e30f;
+    for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+        e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e0, st);
+        if (e == hipSuccess) e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e1, st);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e == hipSuccess) best = std::min(best, t);
+    }
+    if (ge) (void)hipGraphExecDestroy(ge);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    return e == hipSuccess ? best * 1000.0 / reps : -1;
+}
+
+// NEO_PLAN_GLOBAL_SEARCH: measure every candidate scheme of every conv without
+// a given scheme (the local search, its best launch configuration and time
+// per (workload, ic_bn, oc_bn)) and every layout transform the program asks
+// about, on zero-filled scratch buffers, then run the program and fix each
+// conv's scheme.
+int search_schemes(neo_plan* P) {
+    hipError_t e;
+    if (!P->cap_stream) {
+        e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "neo_plan_create: search stream");
+    }
+    const hipStream_t st = P->cap_stream;
+    long max_act = 0, max_w = 0, max_b = 16;
+    for (const NodeInfo& ni : P->nodes) {
+        max_act = std::max(max_act, (long)ni.N * cdiv(ni.C, 64) * 64 * ni.H * ni.W);
+        if (ni.nd.op != NEO_OP_CONV) continue;
+        const NodeInfo& a = P->nodes[ni.inputs[0]];
+        ConvShape cs{};
+        cs.C = a.C;
+        cs.K = ni.nd.K;
+        cs.R = ni.nd.R;
+        cs.S = ni.nd.S;
+        max_w = std::max(max_w, kernel_filter_floats(cs));
+        max_b = std::max(max_b, (long)cdiv(ni.nd.K, 16) * 16);
+    }
+    float *X = nullptr, *Y = nullptr, *Rz = nullptr, *Wt = nullptr, *Bz = nullptr;
+    e = hipMalloc(&X, max_act * 4);
+    if (e == hipSuccess) e = hipMalloc(&Y, max_act * 4);
+    if (e == hipSuccess) e = hipMalloc(&Rz, max_act * 4);
+    if (e == hipSuccess) e = hipMalloc(&Wt, max_w * 4);
+    if (e == hipSuccess) e = hipMalloc(&Bz, max_b * 4);
+    for (auto* b : {X, Y, Rz})
+        if (e == hipSuccess) e = hipMemset(b, 0, max_act * 4);
+    if (e == hipSuccess) e = hipMemset(Wt, 0, max_w * 4);
+    if (e == hipSuccess) e = hipMemset(Bz, 0, max_b * 4);
+    int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: search buffers");
+
+    const int D = P->block;
+    std::map<std::vector<int>, double> xmemo;
+    std::map<std::vector<int>, double> cmemo;
+    int measured = 0;
+    auto conv_cost = [&](int v, int i, int j) -> double {
+        const NodeInfo& ni = P->nodes[v];
+        const int ib = kSearchBlocks[i], ob = kSearchBlocks[j];
+        const NodeInfo& a = P->nodes[ni.inputs[0]];
+        if (ni.ic) {  // the caller's scheme
+            if (ib != ni.ic || ob != ni.oc) return INFINITY;
+        } else {
+            const std::vector<int> ci = candidate_blocks(a.C, D, true), co = candidate_blocks(ni.C, D, false);
+            if (std::find(ci.begin(), ci.end(), ib) == ci.end() ||
+                std::find(co.begin(), co.end(), ob) == co.end())
+                return INFINITY;
+        }
+        const neo_node& d = ni.nd;
+        ConvShape cs{ni.N, a.C, a.H, a.W, d.K, d.R, d.S, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
+                     ni.H, ni.W, 0, cdiv(d.K, ob), d.act};
+        cs.xb = ib;
+        cs.yb = ob;
+        const bool has_res = d.residual >= 0, has_b = d.bn_gamma || d.bias;
+        const std::vector<int> key{cs.N, cs.C, cs.H, cs.W, cs.K, cs.R, cs.S, cs.sh, cs.sw, cs.ph, cs.pw,
+                                   ib, ob, has_res, has_b, cs.act};
+        auto it = cmemo.find(key);
+        if (it != cmemo.end()) return it->second;
+        if (rc != NEO_OK) return INFINITY;
+        ConvConfig cfg{};
+        float us = 0.f;
+        rc = tune_conv(cs, true, X, Wt, has_b ? Bz : nullptr, has_res ? Rz : nullptr, Y, st, &cfg, &us);
+        const double t = rc == NEO_OK ? us : INFINITY;
+        ++measured;
+        cmemo[key] = t;
+        return t;
+    };
+    auto xform_cost = [&](int v, int i, int j) -> double {
+        const NodeInfo& ni = P->nodes[v];
+        const int sb = kSearchBlocks[i], db = kSearchBlocks[j];
+        const std::vector<int> key{ni.N, ni.C, ni.H, ni.W, sb, db};
+        auto it = xmemo.find(key);
+        if (it != xmemo.end()) return it->second;
+        if (rc != NEO_OK) return INFINITY;
+        const double t = time_launches(st, [&]() {
+            return launch_layout_transform(X, sb, Y, db, ni.N, ni.C, ni.H, ni.W, 0, units(ni.C, db), st);
+        });
+        if (t < 0) rc = fail(NEO_ERR_HIP, "neo_plan_create: transform timing failed");
+        xmemo[key] = t < 0 ? INFINITY : t;
+        return xmemo[key];
+    };
+    std::vector<int> ic, oc;
+    double best = 0, fixed = 0;
+    long states = 0, fixed_states = 0;
+    const std::vector<SearchNode> g = search_nodes(P);
+    if (rc == NEO_OK)
+        rc = layout_search_dp(g, P->order, D, conv_cost, xform_cost, &ic, &oc, &best, &states);
+    if (rc == NEO_OK) {
+        // the same program restricted to the plan's block everywhere (Section 3.2)
+        std::vector<int> fi, fo;
+        const int di = search_block_index(D);
+        auto fixed_cost = [&](int v, int i, int j) -> double {
+            if (P->nodes[v].ic) return conv_cost(v, i, j);
+            return (i == di && j == di) ? conv_cost(v, i, j) : INFINITY;
+        };
+        rc = layout_search_dp(g, P->order, D, fixed_cost, xform_cost, &fi, &fo, &fixed, &fixed_states);
+    }
+    (void)hipStreamSynchronize(st);
+    for (float* b : {X, Y, Rz, Wt, Bz})
+        if (b) (void)hipFree(b);
+    if (rc != NEO_OK) return rc;
+    for (size_t v = 0; v < P->nodes.size(); ++v) {
+        NodeInfo& ni = P->nodes[v];
+        if (ni.nd.op != NEO_OP_CONV || ni.ic) continue;
+        ni.ic = ic[v];
+        ni.oc = oc[v];
+    }
+    P->searched = true;
+    P->search_cost = best;
+    P->fixed_cost = fixed;
+    P->search_schemes = measured;
+    P->search_states = states;
+    return NEO_OK;
 }
 
 }  // namespace
 
 extern "C" {
+
+int neo_layout_search(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
+                      const double* conv_time, const double* xform_time, int* ic_bn, int* oc_bn,
+                      double* cost) {
+    if (!nodes || n_nodes <= 0 || !conv_time || !xform_time || !ic_bn || !oc_bn)
+        return fail(NEO_ERR_INVALID_ARG, "neo_layout_search: NULL argument");
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
+        return fail(NEO_ERR_INVALID_ARG, "neo_layout_search: non-positive input shape");
+    if (block != 16 && block != 32 && block != 64)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_layout_search: block must be 16, 32 or 64");
+    constexpr int NB = NEO_SEARCH_NB;
+    try {
+        neo_plan P;
+        P.N = N; P.C = C; P.H = H; P.W = W; P.block = block;
+        int rc = parse(&P, nodes, n_nodes, false);
+        if (rc != NEO_OK) return rc;
+        for (long i = 0; i < (long)n_nodes * NB * NB; ++i)
+            if (!(xform_time[i] >= 0))
+                return fail(NEO_ERR_INVALID_ARG, "neo_layout_search: transform times must be >= 0");
+        auto conv_cost = [&](int v, int i, int j) -> double {
+            const NodeInfo& ni = P.nodes[v];
+            if (ni.ic && (kSearchBlocks[i] != ni.ic || kSearchBlocks[j] != ni.oc)) return INFINITY;
+            const double t = conv_time[((long)v * NB + i) * NB + j];
+            return (std::isfinite(t) && t >= 0) ? t : INFINITY;
+        };
+        auto xform_cost = [&](int v, int i, int j) { return xform_time[((long)v * NB + i) * NB + j]; };
+        std::vector<int> ic, oc;
+        double best = 0;
+        long states = 0;
+        rc = layout_search_dp(search_nodes(&P), P.order, block, conv_cost, xform_cost, &ic, &oc, &best,
+                              &states);
+        if (rc != NEO_OK) return rc;
+        for (int v = 0; v < n_nodes; ++v) {
+            ic_bn[v] = ic[v];
+            oc_bn[v] = oc[v];
+        }
+        if (cost) *cost = best;
+        return NEO_OK;
+    } catch (const std::bad_alloc&) {
+        return fail(NEO_ERR_OOM, "neo_layout_search: host allocation failed");
+    }
+}
 
 int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int W, int block,
                     unsigned flags, neo_plan** out) {
@@ -610,24 +913,32 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (!nodes || n_nodes <= 0) return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: no nodes");
     if (N <= 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: non-positive input shape");
-    if (block != 16) return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16");
-    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE))
+    if (block != 16 && block != 32 && block != 64)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
+    if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
+                            NEO_PLAN_GLOBAL_SEARCH))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
-    if ((flags & NEO_PLAN_TUNE) && (flags & NEO_PLAN_HOST_ONLY))
-        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning needs a device plan");
+    if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
+    if ((flags & NEO_PLAN_GLOBAL_SEARCH) && (flags & NEO_PLAN_NAIVE))
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: the global search plans without the naive transforms");
+    if (flags & NEO_PLAN_GLOBAL_SEARCH) flags |= NEO_PLAN_TUNE;
     neo_plan* P = new (std::nothrow) neo_plan();
     if (!P) return fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     P->flags = flags;
     P->N = N; P->C = C; P->H = H; P->W = W; P->block = block;
     int rc;
     try {
-        rc = build(P, nodes, n_nodes);
+        rc = parse(P, nodes, n_nodes, true);
+        if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
+        if (rc == NEO_OK) rc = build_steps(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     } catch (const std::exception& e) {
         rc = fail(NEO_ERR_INVALID_ARG, std::string("neo_plan_create: ") + e.what());
     }
     if (rc != NEO_OK) {
+        if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
         delete P;
         return rc;
     }
@@ -745,7 +1056,7 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 break;
             case ST_GAP: {
                 const Val& in = P->vals[s.in];
-                e = launch_gap(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                e = launch_gap(val_ptr(P, s.in, x_nchw, y_out), in.layout, in.N, in.C, in.H, in.W,
                                val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
             }
@@ -801,7 +1112,7 @@ static int tune_plan(neo_plan* P) {
         rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
                        s.b_off >= 0 ? prm + s.b_off : nullptr,
                        s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
-                       val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc);
+                       val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
         s.tuned = rc == NEO_OK;
     }
     if (xin) (void)hipFree(xin);

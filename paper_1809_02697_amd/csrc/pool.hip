@@ -1,6 +1,7 @@
-// Layout-tolerant pooling on NCHW16c (Section 3.2): max, average, global
-// average.  One thread per (output pixel, 4-channel quad) moves float4s, so a
-// wave reads and writes 16 pixels x 64 bytes = 1 KB contiguous per access.
+// Layout-tolerant pooling on NCHW[x]c (Section 3.2): max, average, global
+// average, for any block x of 4..64 channels.  One thread per (output pixel,
+// 4-channel quad) moves float4s: the x/4 quads of a pixel block are
+// neighbouring lanes, so a wave reads and writes 1 KB contiguous per access.
 // Max pooling ignores taps outside the input (as if padded with -inf); average
 // pooling divides by the number of taps inside it.
 // Padded channel lanes hold 0 in the input and stay 0 in the output.
@@ -15,20 +16,22 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // With a compile-time window every tap's load is issued before any is used:
 // a tap outside the input loads pixel (0, 0) of the block and is discarded by
 // a select, so the loads of one output are in flight together.
+// lq = log2(x / 4): quads per pixel block.
 template <bool MAX, int KR, int KS>
-__global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, float* __restrict__ y,
-                                                PoolShape s, int CB) {
-    const int total = s.N * CB * s.OH * s.OW * 4;
+__global__ __launch_bounds__(256) void pool_blk(const float* __restrict__ x, float* __restrict__ y,
+                                                PoolShape s, int CB, int lq) {
+    const int total = (s.N * CB * s.OH * s.OW) << lq;
+    const int X = s.xb;
     for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
-        const int q = t & 3;
-        int r_ = t >> 2;
+        const int q = t & ((1 << lq) - 1);
+        int r_ = t >> lq;
         const int ow = r_ % s.OW;
         r_ /= s.OW;
         const int oh = r_ % s.OH;
         r_ /= s.OH;
         const int cb = r_ % CB;
         const int n = r_ / CB;
-        const float* xb = x + (n * CB + cb) * s.H * s.W * 16 + 4 * q;
+        const float* xb = x + (n * CB + cb) * s.H * s.W * X + 4 * q;
         const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
         v4f acc;
         if (MAX)
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, flo
                 for (int c = 0; c < KS; ++c) {
                     const int ih = ih0 + r, iw = iw0 + c;
                     ok[r][c] = (unsigned)ih < (unsigned)s.H && (unsigned)iw < (unsigned)s.W;
-                    v[r][c] = *reinterpret_cast<const v4f*>(xb + (ok[r][c] ? ih * s.W + iw : 0) * 16);
+                    v[r][c] = *reinterpret_cast<const v4f*>(xb + (ok[r][c] ? ih * s.W + iw : 0) * X);
                 }
 #pragma unroll
             for (int r = 0; r < KR; ++r)
@@ -67,7 +70,7 @@ __global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, flo
                 for (int c = 0; c < s.S; ++c) {
                     const int iw = iw0 + c;
                     if ((unsigned)iw >= (unsigned)s.W) continue;
-                    const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * 16);
+                    const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * X);
                     if (MAX) {
 #pragma unroll
                         for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
@@ -83,41 +86,51 @@ __global__ __launch_bounds__(256) void pool_b16(const float* __restrict__ x, flo
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
         }
-        *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * 16 +
+        *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X +
                                 4 * q) = acc;
     }
 }
 
-// One wave per (n, channel block): lane = 4 * pixel_slot + quad; each lane sums
-// the pixels p = slot, slot + 16, ... of its quad, then the 16 slots are summed
-// with cross-lane shuffles in a fixed tree order.
-__global__ __launch_bounds__(256) void gap_b16(const float* __restrict__ x, float* __restrict__ y,
-                                               int NCB, int HW) {
+// One wave per (n, 16-channel group j) whatever the block x: lane = 4 *
+// pixel_slot + quad; each lane sums the pixels p = slot, slot + 16, ... of its
+// quad's channels, then the 16 slots are summed with cross-lane shuffles in a
+// fixed tree order -- the same order for every block, so the result does not
+// depend on the layout.  Channel c = 16 j + 4 q sits in block c / x at lane
+// c % x (lx = log2 x); quads past the last block (x < 16) are idle.
+__global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, float* __restrict__ y,
+                                               int N, int G16, int XB, int lx, int HW) {
     const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (wave_id >= NCB) return;
+    if (wave_id >= N * G16) return;
+    const int n = wave_id / G16, j = wave_id - n * G16;
     const int lane = threadIdx.x & 63;
     const int q = lane & 3, slot = lane >> 2;
-    const float* xb = x + wave_id * HW * 16 + 4 * q;
+    const int X = 1 << lx;
+    const int c = 16 * j + 4 * q;
+    const bool ok = c < (XB << lx);
+    const int blk = n * XB + (c >> lx), sub = c & (X - 1);
+    const float* xb = x + (long)blk * HW * X + sub;
     v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
-    int p = slot;
-    for (; p + 48 < HW; p += 64) {  // four pixels of the slot in flight
-        v4f v[4];
+    if (ok) {
+        int p = slot;
+        for (; p + 48 < HW; p += 64) {  // four pixels of the slot in flight
+            v4f v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const v4f*>(xb + (p + 16 * u) * 16);
+            for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const v4f*>(xb + (p + 16 * u) * X);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc += v[u];
+            for (int u = 0; u < 4; ++u) acc += v[u];
+        }
+        for (; p < HW; p += 16) acc += *reinterpret_cast<const v4f*>(xb + p * X);
     }
-    for (; p < HW; p += 16) acc += *reinterpret_cast<const v4f*>(xb + p * 16);
 #pragma unroll
     for (int off = 4; off < 64; off <<= 1) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] += __shfl_xor(acc[i], off, 64);
     }
-    if (slot == 0) {
+    if (slot == 0 && ok) {
         const float d = (float)HW;
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
-        *reinterpret_cast<v4f*>(y + wave_id * 16 + 4 * q) = acc;
+        *reinterpret_cast<v4f*>(y + blk * X + sub) = acc;
     }
 }
 
@@ -132,14 +145,15 @@ inline dim3 grid_for(long total) {
 
 template <bool MAX>
 hipError_t launch_pool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
-    const int CB = cdiv(s.C, 16);
-    const dim3 g = grid_for((long)s.N * CB * s.OH * s.OW * 4), b(256);
+    if (!pow2_block(s.xb)) return hipErrorInvalidValue;
+    const int CB = cdiv(s.C, s.xb), lq = ilog2(s.xb / 4);
+    const dim3 g = grid_for(((long)s.N * CB * s.OH * s.OW) << lq), b(256);
     if (s.R == 3 && s.S == 3)
-        hipLaunchKernelGGL((pool_b16<MAX, 3, 3>), g, b, 0, st, x, y, s, CB);
+        hipLaunchKernelGGL((pool_blk<MAX, 3, 3>), g, b, 0, st, x, y, s, CB, lq);
     else if (s.R == 2 && s.S == 2)
-        hipLaunchKernelGGL((pool_b16<MAX, 2, 2>), g, b, 0, st, x, y, s, CB);
+        hipLaunchKernelGGL((pool_blk<MAX, 2, 2>), g, b, 0, st, x, y, s, CB, lq);
     else
-        hipLaunchKernelGGL((pool_b16<MAX, 0, 0>), g, b, 0, st, x, y, s, CB);
+        hipLaunchKernelGGL((pool_blk<MAX, 0, 0>), g, b, 0, st, x, y, s, CB, lq);
     return hipGetLastError();
 }
 
@@ -151,9 +165,11 @@ hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStrea
     return launch_pool<false>(s, x, y, st);
 }
 
-hipError_t launch_gap(const float* x, int N, int C, int H, int W, float* y, hipStream_t st) {
-    const int NCB = N * cdiv(C, 16);
-    hipLaunchKernelGGL(gap_b16, dim3(cdiv(NCB, 4)), dim3(256), 0, st, x, y, NCB, H * W);
+hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st) {
+    if (!pow2_block(xb)) return hipErrorInvalidValue;
+    const int XB = cdiv(C, xb), G16 = cdiv(XB * xb, 16);
+    hipLaunchKernelGGL(gap_blk, dim3(cdiv(N * G16, 4)), dim3(256), 0, st, x, y, N, G16, XB,
+                       ilog2(xb), H * W);
     return hipGetLastError();
 }
 

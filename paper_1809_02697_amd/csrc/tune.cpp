@@ -4,7 +4,8 @@
 // per (workload, CPU type) so that a workload is searched once.  Here a
 // schedule is a launch configuration of the blocked MFMA kernel (register
 // tile, waves per workgroup, reduction split), a workload is the convolution
-// shape, and the "CPU type" is the GPU architecture name.
+// shape with its input and output blocks (ic_bn, oc_bn), and the "CPU type" is
+// the GPU architecture name.
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
@@ -23,8 +24,8 @@ namespace {
 
 struct Key {
     std::string arch;
-    int N, C, H, W, K, R, S, sh, sw, ph, pw, wmfma;
-    auto tie() const { return std::tie(arch, N, C, H, W, K, R, S, sh, sw, ph, pw, wmfma); }
+    int N, C, H, W, K, R, S, sh, sw, ph, pw, wmfma, xb, yb;
+    auto tie() const { return std::tie(arch, N, C, H, W, K, R, S, sh, sw, ph, pw, wmfma, xb, yb); }
     bool operator<(const Key& o) const { return tie() < o.tie(); }
 };
 
@@ -47,7 +48,8 @@ std::string device_arch() {
 }
 
 Key key_of(const ConvShape& s, bool wmfma, const std::string& arch) {
-    return Key{arch, s.N, s.C, s.H, s.W, s.K, s.R, s.S, s.sh, s.sw, s.ph, s.pw, wmfma ? 1 : 0};
+    return Key{arch, s.N, s.C, s.H, s.W, s.K, s.R, s.S, s.sh, s.sw, s.ph, s.pw, wmfma ? 1 : 0,
+               s.xb, s.yb};
 }
 
 // Candidate schedules: every register tile and waves-per-workgroup the kernel
@@ -85,15 +87,17 @@ bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out) {
 // Time every candidate on `st` (a stream that is not the legacy null stream)
 // with the caller's buffers: each candidate's launches are captured into a
 // graph of `reps` launches and replayed between two events.  Keeps the
-// fastest in the database and returns it.
+// fastest in the database and returns it with its time per launch (us_out may
+// be null).
 int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
-              const float* res, float* y, hipStream_t st, ConvConfig* best_out) {
+              const float* res, float* y, hipStream_t st, ConvConfig* best_out, float* us_out) {
     const std::string arch = device_arch();
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_db.find(key_of(s, wmfma, arch));
         if (it != g_db.end()) {
             *best_out = it->second.cfg;
+            if (us_out) *us_out = it->second.us;
             return NEO_OK;
         }
     }
@@ -159,6 +163,7 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
         g_db[key_of(s, wmfma, arch)] = Entry{best, best_us};
     }
     *best_out = best;
+    if (us_out) *us_out = best_us;
     return NEO_OK;
 }
 
@@ -169,7 +174,7 @@ using namespace neo;
 extern "C" {
 
 // Text format, one workload per line:
-//   arch N C H W K R S sh sw ph pw wmfma fk fp split waves us
+//   arch N C H W K R S sh sw ph pw wmfma xb yb fk fp split waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -180,8 +185,8 @@ int neo_tune_db_save(const char* path) {
         const Entry& v = kv.second;
         f << k.arch << ' ' << k.N << ' ' << k.C << ' ' << k.H << ' ' << k.W << ' ' << k.K << ' ' << k.R
           << ' ' << k.S << ' ' << k.sh << ' ' << k.sw << ' ' << k.ph << ' ' << k.pw << ' ' << k.wmfma
-          << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split << ' ' << v.cfg.waves << ' '
-          << v.us << '\n';
+          << ' ' << k.xb << ' ' << k.yb << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split
+          << ' ' << v.cfg.waves << ' ' << v.us << '\n';
     }
     return f ? (int)g_db.size() : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
@@ -200,8 +205,9 @@ int neo_tune_db_load(const char* path) {
         Key k;
         Entry v;
         if (!(is >> k.arch >> k.N >> k.C >> k.H >> k.W >> k.K >> k.R >> k.S >> k.sh >> k.sw >> k.ph >>
-              k.pw >> k.wmfma >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >> v.us) ||
-            !conv_config_valid(v.cfg))
+              k.pw >> k.wmfma >> k.xb >> k.yb >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >>
+              v.us) ||
+            !conv_config_valid(v.cfg) || !pow2_block(k.xb) || !pow2_block(k.yb))
             return fail(NEO_ERR_INVALID_ARG,
                         "neo_tune_db_load: malformed line " + std::to_string(lineno));
         add[k] = v;

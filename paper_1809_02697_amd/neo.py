@@ -27,7 +27,9 @@ PLAN_HOST_ONLY = 1
 PLAN_NAIVE = 2
 PLAN_HIPGRAPH = 4
 PLAN_TUNE = 8
+PLAN_GLOBAL_SEARCH = 16
 BLOCK = 16
+SEARCH_BLOCKS = (0, 4, 8, 16, 32, 64)   # layout index space of neo_layout_search
 
 
 class NeoError(RuntimeError):
@@ -50,7 +52,7 @@ class Node(ctypes.Structure):
                 ("w", ctypes.c_void_p), ("bias", ctypes.c_void_p),
                 ("bn_gamma", ctypes.c_void_p), ("bn_beta", ctypes.c_void_p),
                 ("bn_mean", ctypes.c_void_p), ("bn_var", ctypes.c_void_p),
-                ("bn_eps", ctypes.c_float)]
+                ("bn_eps", ctypes.c_float), ("ic_bn", ctypes.c_int), ("oc_bn", ctypes.c_int)]
 
 
 _lib = None
@@ -74,6 +76,12 @@ def lib():
     sig = {
         "neo_conv2d_blocked": [P, I, I, I, I, P, I, I, I, P, I, I, I, I,
                                ctypes.POINTER(Epilogue), P, I, I, P],
+        "neo_conv2d_nchwxc": [P, I, I, I, I, I, P, I, I, I, P, I, I, I, I,
+                              ctypes.POINTER(Epilogue), P, I, I, I, P],
+        "neo_maxpool2d_nchwxc": [P, I, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
+        "neo_avgpool2d_nchwxc": [P, I, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
+        "neo_global_avgpool_nchwxc": [P, I, I, I, I, I, P, P],
+        "neo_layout_search": [ctypes.POINTER(Node), I, I, I, I, I, I, P, P, P, P, P],
         "neo_layout_transform": [P, I, P, I, I, I, I, I, P],
         "neo_pack_filter": [P, I, I, I, I, I, I, P, P],
         "neo_fold_bn": [P, P, P, P, P, P, F, I, I, I, I, P, P],
@@ -179,6 +187,29 @@ def conv2d_blocked(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="non
     return out
 
 
+def conv2d_nchwxc(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
+                  residual=None, out=None, y_block=BLOCK, y_blk_offset=0, y_blk_total=None,
+                  stream=None):
+    """x: [N][ceil(C/xb)][H][W][xb] (xb from x's last dim); output NCHW[y_block]c."""
+    import torch
+    (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
+    N, XB, H, W, xb = x.shape
+    OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
+    tot = cblocks(K, y_block) if y_blk_total is None else y_blk_total
+    if out is None:
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), y_block), device=x.device,
+                          dtype=torch.float32)
+    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
+                  residual.data_ptr() if residual is not None else None)
+    if residual is not None:
+        _dptr(residual, "residual")
+    _check(lib().neo_conv2d_nchwxc(_dptr(x, "x"), xb, N, C, H, W, _dptr(w_packed, "w_packed"), K,
+                                   R, S, _dptr(bias, "bias"), sh, sw, ph, pw, ctypes.byref(ep),
+                                   _dptr(out, "out"), y_block, y_blk_offset, tot,
+                                   _stream(stream)))
+    return out
+
+
 def layout_transform(src, src_block, dst_block, N, C, H, W, out=None, stream=None):
     import torch
     if out is None:
@@ -228,17 +259,41 @@ def fold_bn(w, bias, gamma, beta, mean, var, eps):
     return w_out, b_out
 
 
-def _pool(fn, x, C, R, S, stride, pad, out, y_cblk_offset, y_cblk_total, stream):
+def _pool(fn, x, C, R, S, stride, pad, out, y_cblk_offset, y_cblk_total, stream, blocked=False):
     import torch
     (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
-    N, CB, H, W, _ = x.shape
+    N, CB, H, W, blk = x.shape
     OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
     tot = CB if y_cblk_total is None else y_cblk_total
     if out is None:
-        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=x.device,
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), blk), device=x.device,
                           dtype=torch.float32)
-    _check(fn(_dptr(x, "x"), N, C, H, W, R, S, sh, sw, ph, pw, _dptr(out, "out"), y_cblk_offset,
+    pre = (_dptr(x, "x"), blk) if blocked else (_dptr(x, "x"),)
+    _check(fn(*pre, N, C, H, W, R, S, sh, sw, ph, pw, _dptr(out, "out"), y_cblk_offset,
               tot, _stream(stream)))
+    return out
+
+
+def maxpool2d_nchwxc(x, C, R, S, stride, pad=0, out=None, y_blk_offset=0, y_blk_total=None,
+                     stream=None):
+    """x: [N][ceil(C/b)][H][W][b], block b from x's last dim."""
+    return _pool(lib().neo_maxpool2d_nchwxc, x, C, R, S, stride, pad, out, y_blk_offset,
+                 y_blk_total, stream, blocked=True)
+
+
+def avgpool2d_nchwxc(x, C, R, S, stride, pad=0, out=None, y_blk_offset=0, y_blk_total=None,
+                     stream=None):
+    return _pool(lib().neo_avgpool2d_nchwxc, x, C, R, S, stride, pad, out, y_blk_offset,
+                 y_blk_total, stream, blocked=True)
+
+
+def global_avgpool_nchwxc(x, C, out=None, stream=None):
+    import torch
+    N, CB, H, W, blk = x.shape
+    if out is None:
+        out = torch.empty((N, CB, 1, 1, blk), device=x.device, dtype=torch.float32)
+    _check(lib().neo_global_avgpool_nchwxc(_dptr(x, "x"), blk, N, C, H, W, _dptr(out, "out"),
+                                           _stream(stream)))
     return out
 
 
@@ -296,40 +351,71 @@ def tune_db_size():
 # --------------------------------------------------------------------------------------
 # Graph plan
 # --------------------------------------------------------------------------------------
-class Plan:
-    """A plan built from a network description (``workloads.Graph``)."""
+def _node_array(graph, schemes=None, keep=None, with_params=True):
+    """ctypes neo_node array of a network description; schemes: {conv node id:
+    (ic_bn, oc_bn)}.  Host arrays referenced by the nodes are appended to keep."""
+    keep = [] if keep is None else keep
+    schemes = schemes or {}
+    arr = (Node * len(graph.nodes))()
+    for i, n in enumerate(graph.nodes):
+        d = arr[i]
+        d.op = OPS[n.op]
+        ins = (ctypes.c_int * max(1, len(n.inputs)))(*n.inputs)
+        keep.append(ins)
+        d.n_inputs = len(n.inputs)
+        d.inputs = ctypes.cast(ins, ctypes.POINTER(ctypes.c_int))
+        d.K, d.R, d.S = n.K, n.R, n.S
+        d.stride_h, d.stride_w = n.stride
+        d.pad_h, d.pad_w = n.pad
+        d.act = ACT[n.act]
+        d.residual = n.residual
+        d.ic_bn, d.oc_bn = schemes.get(i, (0, 0))
+        if not with_params:
+            continue
 
-    def __init__(self, graph, input_shape=None, flags=0, block=BLOCK):
+        def host(a):
+            if a is None:
+                return None
+            a = np.ascontiguousarray(a, np.float32)
+            keep.append(a)
+            return ctypes.c_void_p(a.ctypes.data)
+
+        d.w = host(n.w)
+        d.bias = host(n.bias)
+        if n.bn is not None:
+            d.bn_gamma, d.bn_beta = host(n.bn["gamma"]), host(n.bn["beta"])
+            d.bn_mean, d.bn_var = host(n.bn["mean"]), host(n.bn["var"])
+            d.bn_eps = float(n.bn["eps"])
+    return arr
+
+
+def layout_search(graph, conv_time, xform_time, block=BLOCK, schemes=None):
+    """Algorithm 2 on the host (neo_layout_search).  conv_time, xform_time:
+    arrays [n_nodes][6][6] over SEARCH_BLOCKS (conv_time inf / negative = not a
+    candidate).  Returns (cost, {conv node: (ic_bn, oc_bn)})."""
+    L = lib()
+    n = len(graph.nodes)
+    ct = np.ascontiguousarray(conv_time, np.float64).reshape(n, 6, 6)
+    xt = np.ascontiguousarray(xform_time, np.float64).reshape(n, 6, 6)
+    ic = np.zeros(n, np.int32)
+    oc = np.zeros(n, np.int32)
+    cost = ctypes.c_double()
+    arr = _node_array(graph, schemes, with_params=False)
+    _check(L.neo_layout_search(arr, n, *graph.input_shape, block, _hp(ct), _hp(xt), _hp(ic),
+                               _hp(oc), ctypes.byref(cost)))
+    return cost.value, {i: (int(ic[i]), int(oc[i])) for i in range(n)
+                        if graph.nodes[i].op == "conv"}
+
+
+class Plan:
+    """A plan built from a network description (``workloads.Graph``).
+    schemes: {conv node id: (ic_bn, oc_bn)} fixing those convs' layouts."""
+
+    def __init__(self, graph, input_shape=None, flags=0, block=BLOCK, schemes=None):
         L = lib()
         shape = tuple(input_shape or graph.input_shape)
         keep = []
-        arr = (Node * len(graph.nodes))()
-        for i, n in enumerate(graph.nodes):
-            d = arr[i]
-            d.op = OPS[n.op]
-            ins = (ctypes.c_int * max(1, len(n.inputs)))(*n.inputs)
-            keep.append(ins)
-            d.n_inputs = len(n.inputs)
-            d.inputs = ctypes.cast(ins, ctypes.POINTER(ctypes.c_int))
-            d.K, d.R, d.S = n.K, n.R, n.S
-            d.stride_h, d.stride_w = n.stride
-            d.pad_h, d.pad_w = n.pad
-            d.act = ACT[n.act]
-            d.residual = n.residual
-
-            def host(a):
-                if a is None:
-                    return None
-                a = np.ascontiguousarray(a, np.float32)
-                keep.append(a)
-                return ctypes.c_void_p(a.ctypes.data)
-
-            d.w = host(n.w)
-            d.bias = host(n.bias)
-            if n.bn is not None:
-                d.bn_gamma, d.bn_beta = host(n.bn["gamma"]), host(n.bn["beta"])
-                d.bn_mean, d.bn_var = host(n.bn["mean"]), host(n.bn["var"])
-                d.bn_eps = float(n.bn["eps"])
+        arr = _node_array(graph, schemes, keep)
         h = ctypes.c_void_p()
         _check(L.neo_plan_create(arr, len(graph.nodes), *shape, block, flags, ctypes.byref(h)))
         self._h = h

@@ -239,17 +239,20 @@ def test_tune_db_roundtrip_and_errors(tmp_path):
     neo.tune_db_clear()
     assert neo.tune_db_size() == 0
     p = tmp_path / "db.txt"
-    p.write_text("# arch N C H W K R S sh sw ph pw wmfma fk fp split waves us\n"
-                 "gfx950 1 64 56 56 64 3 3 1 1 1 1 1 2 2 1 4 7.5\n"
-                 "gfx950 1 512 7 7 512 3 3 1 1 1 1 1 2 1 4 8 10.5\n")
+    p.write_text("# arch N C H W K R S sh sw ph pw wmfma xb yb fk fp split waves us\n"
+                 "gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 2 2 1 4 7.5\n"
+                 "gfx950 1 512 7 7 512 3 3 1 1 1 1 1 32 16 2 1 4 8 10.5\n")
     assert neo.tune_db_load(p) == 2
     assert neo.tune_db_size() == 2
     q = tmp_path / "out.txt"
     assert neo.tune_db_save(q) == 2
     lines = sorted(l for l in q.read_text().splitlines() if l)
-    assert lines[0].split()[:13] == "gfx950 1 512 7 7 512 3 3 1 1 1 1 1".split()
+    assert lines[0].split()[:15] == "gfx950 1 512 7 7 512 3 3 1 1 1 1 1 32 16".split()
     bad = tmp_path / "bad.txt"
-    bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 3 2 1 4 7.5\n")   # fk = 3 is not a kernel
+    bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 3 2 1 4 7.5\n")   # fk = 3 is not a kernel
+    with pytest.raises(neo.NeoError):
+        neo.tune_db_load(bad)
+    bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 12 16 2 2 1 4 7.5\n")   # no 12 block
     with pytest.raises(neo.NeoError):
         neo.tune_db_load(bad)
     with pytest.raises(neo.NeoError):
