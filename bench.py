@@ -1,10 +1,13 @@
 """Benchmark: ResNet-50 batch-1 fp32 inference through the blocked-layout plan.
 
 One step = one forward pass of ResNet-50 (224x224, batch 1) through
-``neo_run_graph`` on a tuned plan replayed as a HIP graph: the entry layout
-transform, 53 blocked convolutions with their fused epilogues, max pool,
-global average pool, the exit transform (aliased) and the dense layer.  Input,
-output and parameters are resident in HBM before the timed region.
+``neo_run_graph`` on the full method's plan -- local search of every conv's
+launch configuration, global layout search over each conv's (ic_bn, oc_bn),
+transforms only where the chosen layouts differ -- replayed as a HIP graph:
+the entry layout transform, 53 blocked convolutions with their fused
+epilogues, max pool, global average pool, the exit transform (aliased) and
+the dense layer.  Input, output and parameters are resident in HBM before the
+timed region.
 
 Printed JSON line:
   value        conv TFLOP/s over the whole step (8.174 GFLOP of convolution
@@ -21,8 +24,11 @@ Printed JSON line:
                cold_us / cold_hbm_gbs: the same launch after a 512 MB write
                has flushed the caches, so its operands come from HBM
   models       end-to-end latency of ResNet-50 / VGG-16 / Inception-v3 at
-               batch 1 and ResNet-50 at batch 32, and the transform-elimination
-               ablation (a plan that transforms around every blocked operation)
+               batch 1 and ResNet-50 at batch 32 for the ablation of Table 3:
+               "naive" (transforms around every blocked operation), "eliminated"
+               (one block for every conv, transforms only at the ends) and
+               "searched" (the global layout search); all with tuned launch
+               configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
 import argparse
@@ -51,6 +57,24 @@ def conv_costs(C, K, R, S, H, W, st, pd, N=1, residual=False):
         touched = N * C * H * W
     nbytes = 4 * (touched + K * C * R * S + N * K * OH * OW * (2 if residual else 1) + K)
     return flops, nbytes, OH, OW
+
+
+def plan_schemes(desc):
+    """{conv node: (ic_bn, oc_bn)} of a plan description."""
+    return {s["node"]: (s["conv"]["ic_bn"], s["conv"]["oc_bn"]) for s in desc["steps"]
+            if s["kind"] == "conv"}
+
+
+def headline_plan(neo, g, tune_db=None):
+    """The full method's plan for g.  With a results file from an earlier run
+    (``--tune-db``) the schemes it chose are reused from ``<file>.schemes.json``
+    (so a profiling run executes the same plan); otherwise the global search
+    chooses them."""
+    path = (tune_db or "") + ".schemes.json"
+    if tune_db and os.path.exists(path):
+        sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
+        return neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH, schemes=sch)
+    return neo.Plan(g, flags=neo.PLAN_GLOBAL_SEARCH | neo.PLAN_HIPGRAPH)
 
 
 def plan_conv_flops(desc):
@@ -180,7 +204,7 @@ def layer_table(torch, plan, x, out, reps):
             continue
         c = s["conv"]
         key = (c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"], c["W"],
-               c["N"])
+               c["N"], c["ic_bn"], c["oc_bn"])
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
         cold = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4))
         if key in rows:
@@ -192,7 +216,8 @@ def layer_table(torch, plan, x, out, reps):
                                            c["stride"], c["pad"], N=c["N"], residual=s["res"] >= 0)
         rows[key] = dict(shape=f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} "
                                f"{c['H']}->{OH}", uses=1, flops=flops, bytes=nbytes,
-                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"]), _t=[us],
+                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"],
+                                     ic_bn=c["ic_bn"], oc_bn=c["oc_bn"]), _t=[us],
                          _c=[cold])
     out_rows = []
     for r in rows.values():
@@ -213,31 +238,53 @@ def layer_table(torch, plan, x, out, reps):
     return out_rows
 
 
+def scheme_summary(d):
+    """Histogram of the convs' (ic_bn, oc_bn) in a plan description."""
+    h = {}
+    for s in d["steps"]:
+        if s["kind"] == "conv":
+            k = f"{s['conv']['ic_bn']}/{s['conv']['oc_bn']}"
+            h[k] = h.get(k, 0) + 1
+    return dict(sorted(h.items()))
+
+
 def model_latencies(neo, torch, wl, steps):
-    """End-to-end latency of each model (tuned, graph replay) and the
-    transform-elimination ablation at batch 1."""
+    """End-to-end latency of each model (tuned, graph replay) for the three
+    plans of the Table 3 ablation; ResNet-50 also at fixed blocks 32 and 64."""
     res = {}
     for name, builder, batch in [("resnet50", wl.resnet50, 1), ("vgg16", wl.vgg16, 1),
                                  ("inception_v3", wl.inception_v3, 1), ("resnet50", wl.resnet50, 32)]:
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        for label, flags in [("eliminated", 0), ("naive", neo.PLAN_NAIVE)]:
-            if batch > 1 and label == "naive":
-                continue
-            p = neo.Plan(g, flags=flags | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+        plans = [("eliminated", 0, 16)]
+        if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
+            plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
+        if name == "resnet50":
+            plans += [("eliminated_x32", 0, 32), ("eliminated_x64", 0, 64)]
+        for label, flags, block in plans:
+            t0 = time.perf_counter()
+            p = neo.Plan(g, flags=flags | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH, block=block)
+            t_plan = time.perf_counter() - t0
             out = p.run(x)
             ms = e2e_ms(torch, p, x, out, steps, 3)
             d = p.describe()
             entry[label] = dict(ms=round(ms, 4), n_transforms=d["n_transforms"],
-                                launches=len(d["steps"]))
-            if label == "eliminated":
+                                launches=len(d["steps"]), plan_s=round(t_plan, 1))
+            if label == "searched":
+                entry[label]["schemes"] = scheme_summary(d)
+                entry[label]["predicted_us"] = round(d["search"]["cost_us"], 1)
+                entry[label]["predicted_fixed16_us"] = round(d["search"]["fixed_block_cost_us"], 1)
+                entry[label]["schemes_measured"] = d["search"]["schemes_measured"]
+            if label == ("searched" if batch == 1 else "eliminated"):
                 flops = plan_conv_flops(d)
                 entry["conv_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
                 entry["images_per_s"] = round(batch / (ms * 1e-3), 1)
             p.destroy()
         if "naive" in entry:
             entry["elimination_speedup"] = round(entry["naive"]["ms"] / entry["eliminated"]["ms"], 3)
+        if "searched" in entry:
+            entry["search_speedup"] = round(entry["eliminated"]["ms"] / entry["searched"]["ms"], 3)
         res[f"{name}_b{batch}"] = entry
         del g, x
         print(f"[bench] {name} b{batch}: {entry}", file=sys.stderr, flush=True)
@@ -307,7 +354,7 @@ def main():
         neo.tune_db_load(args.tune_db)
     g = wl.resnet50(1)
     t0 = time.perf_counter()
-    plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+    plan = headline_plan(neo, g, args.tune_db)
     t_plan = time.perf_counter() - t0
     x = torch.from_numpy(g.x).cuda()
     out = torch.empty((1, 1000), device="cuda")
@@ -365,11 +412,12 @@ def main():
         "vs_baseline": None,
         "dtype": "fp32",
         "data": "synthetic",
-        "config": {"workload": "ResNet-50 forward, batch 1, 3x224x224 fp32, NCHW16c plan "
-                               "(1 transform in, 1 out), tuned, hipGraph replay, seed 2",
+        "config": {"workload": "ResNet-50 forward, batch 1, 3x224x224 fp32, NCHW[x]c plan with "
+                               "globally searched per-conv blocks, tuned, hipGraph replay, seed 2",
                    "global_batch": 1, "conv_gflop_per_step": round(conv_flops / 1e9, 4),
                    "cache": "warm (working set resident in the 256 MB MALL)",
-                   "plan_build_s": round(t_plan, 2)},
+                   "plan_build_s": round(t_plan, 2), "schemes": scheme_summary(desc),
+                   "n_transforms": desc["n_transforms"]},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layers": layers,
@@ -379,6 +427,8 @@ def main():
     plan.destroy()
     if args.save_tune_db:
         neo.tune_db_save(args.save_tune_db)
+        with open(args.save_tune_db + ".schemes.json", "w") as f:
+            json.dump({str(k): list(v) for k, v in plan_schemes(desc).items()}, f)
 
 
 if __name__ == "__main__":

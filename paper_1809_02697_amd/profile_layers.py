@@ -5,10 +5,10 @@
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT -o write -- \
         python -m paper_1809_02697_amd.profile_layers [TUNE_DB]
 
-Builds and tunes the plan (the same flags as bench.py; with TUNE_DB, a
-local-search results file written by ``bench.py --save-tune-db``, the
-configurations come from the file and no tuning launches are profiled), runs
-one forward,
+Builds the plan bench.py times (with TUNE_DB, a local-search results file
+written by ``bench.py --save-tune-db``, the launch configurations and the
+global search's schemes come from that run, so no tuning launches are
+profiled), runs one forward,
 then a plain device-to-device copy of COPY_MB megabytes (the calibration
 kernel: it reads and writes exactly that many bytes) and then every step of
 the plan once, in order.  The dispatches after the copy are one forward pass.
@@ -23,13 +23,15 @@ COPY_MB = 64
 def main():
     import torch
 
+    from bench import headline_plan
     from paper_1809_02697_amd import neo
     from paper_1809_02697_amd import workloads as wl
 
-    if len(sys.argv) > 1:
-        neo.tune_db_load(sys.argv[1])
+    db = sys.argv[1] if len(sys.argv) > 1 else None
+    if db:
+        neo.tune_db_load(db)
     g = wl.resnet50(1)
-    plan = neo.Plan(g, flags=neo.PLAN_TUNE)
+    plan = headline_plan(neo, g, db)
     x = torch.from_numpy(g.x).cuda()
     out = torch.empty((1, 1000), device="cuda")
     plan.run(x, out)

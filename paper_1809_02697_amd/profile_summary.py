@@ -5,7 +5,7 @@
 RUN_DIR holds (names as written by the commands below):
   prof_bench/bench_kernel_stats.csv, prof_bench/bench_kernel_trace.csv
       rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_bench -o bench --
-          python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt
+          python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt --latency-runs 100
   pmc/fetch_counter_collection.csv, pmc/write_counter_collection.csv
       rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch --
           python -m paper_1809_02697_amd.profile_layers        (and WRITE_SIZE / -o write)
@@ -123,13 +123,13 @@ def main(run_dir):
     md = ["# conv2d_blocked, ResNet-50 batch 1 (53 conv launches per forward)", "",
           "Commands (run from the repository root on one MI355X; RUN_DIR = gpurun_out):", "",
           "```",
-          "python bench.py --no-cpu --save-tune-db RUN_DIR/tune_db.txt > RUN_DIR/bench.log",
+          "python bench.py --save-tune-db RUN_DIR/tune_db.txt > RUN_DIR/bench.log",
           "rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_bench -o bench -- "
-          "python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt",
+          "python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt --latency-runs 100",
           "rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch -- "
-          "python -m paper_1809_02697_amd.profile_layers",
+          "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
           "rocprofv3 --pmc WRITE_SIZE --output-format csv -d RUN_DIR/pmc -o write -- "
-          "python -m paper_1809_02697_amd.profile_layers",
+          "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
           "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
           "```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
