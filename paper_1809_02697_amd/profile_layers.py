@@ -31,7 +31,7 @@ def main():
     if db:
         neo.tune_db_load(db)
     g = wl.resnet50(1)
-    plan = headline_plan(neo, g, db)
+    plan, _ = headline_plan(neo, g, db, torch)
     x = torch.from_numpy(g.x).cuda()
     out = torch.empty((1, 1000), device="cuda")
     plan.run(x, out)

@@ -31,11 +31,15 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SRC = os.path.join(HERE, "csrc", "conv.hip")
+KERNEL_SRCS = [os.path.join(HERE, "csrc", f) for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip")]
 
 
 def kernel_hash():
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """sha256[:16] of the conv kernel's sources (templates and instantiations)."""
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def _rows(path):
