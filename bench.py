@@ -210,7 +210,7 @@ def engine_clock(torch=None, plan=None, x=None, out=None, busy_runs=4000):
             torch.cuda.synchronize()
 
 
-def layer_table(torch, plan, x, out, reps):
+def layer_table(torch, plan, x, out, reps, cold=True):
     """Each conv step of the plan timed alone (its kernel(s) as the plan
     launches them), grouped by distinct shape."""
     d = plan.describe()
@@ -224,11 +224,11 @@ def layer_table(torch, plan, x, out, reps):
         key = (c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"], c["W"],
                c["N"], c["ic_bn"], c["oc_bn"])
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
-        cold = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4))
+        cold_us = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4)) if cold else 0.0
         if key in rows:
             rows[key]["uses"] += 1
             rows[key]["_t"].append(us)
-            rows[key]["_c"].append(cold)
+            rows[key]["_c"].append(cold_us)
             continue
         flops, nbytes, OH, OW = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"],
                                            c["stride"], c["pad"], N=c["N"], residual=s["res"] >= 0)
@@ -236,11 +236,11 @@ def layer_table(torch, plan, x, out, reps):
                                f"{c['H']}->{OH}", uses=1, flops=flops, bytes=nbytes,
                          config=dict(tile=c["tile"], split=c["split"], waves=c["waves"],
                                      ic_bn=c["ic_bn"], oc_bn=c["oc_bn"]), _t=[us],
-                         _c=[cold])
+                         _c=[cold_us])
     out_rows = []
     for r in rows.values():
         us = float(np.mean(r.pop("_t")))
-        cold = float(np.mean(r.pop("_c")))
+        cold_us = float(np.mean(r.pop("_c")))
         tf = r["flops"] / (us * 1e-6) / 1e12
         gbs = r["bytes"] / (us * 1e-6) / 1e9
         ai = r["flops"] / r["bytes"]
@@ -249,9 +249,10 @@ def layer_table(torch, plan, x, out, reps):
                  alg_gbs=round(gbs, 1),
                  bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_FP32_TFLOPS else "hbm",
                  pct_mfma=round(100 * tf / PEAK_FP32_TFLOPS, 1),
-                 pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1),
-                 cold_us=round(cold, 2),
-                 cold_hbm_gbs=round(r["bytes"] / (cold * 1e-6) / 1e9, 1))
+                 pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1))
+        if cold:
+            r.update(cold_us=round(cold_us, 2),
+                     cold_hbm_gbs=round(r["bytes"] / (cold_us * 1e-6) / 1e9, 1))
         out_rows.append(r)
     return out_rows
 
@@ -407,6 +408,22 @@ def main():
 
     models = None if args.no_models else model_latencies(neo, torch, wl, 20)
 
+    layers_b32 = None
+    if not args.no_layers and not args.no_models:
+        # the same kernels with the per-launch floor amortized over 32 images
+        g32 = wl.resnet50(32)
+        p32 = neo.Plan(g32, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+        x32 = torch.from_numpy(g32.x).cuda()
+        o32 = p32.run(x32)
+        layers_b32 = layer_table(torch, p32, x32, o32, 10, cold=False)
+        tf32 = sum(r["flops"] * r["uses"] for r in layers_b32) / \
+            sum(r["us"] * 1e-6 * r["uses"] for r in layers_b32) / 1e12
+        for r in layers_b32:
+            del r["flops"], r["bytes"]
+        p32.destroy()
+        del g32, x32
+        print(f"[bench] batch-32 conv layers: {tf32:.2f} TFLOP/s", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(g)
@@ -439,6 +456,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layers": layers,
+        "layers_b32": layers_b32,
         "models": models,
     }
     print(json.dumps(rec))

@@ -776,6 +776,15 @@ int search_schemes(neo_plan* P) {
     if (e == hipSuccess) e = hipMemset(Wt, 0, max_w * 4);
     if (e == hipSuccess) e = hipMemset(Bz, 0, max_b * 4);
     int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: search buffers");
+    // the first failed measurement (the program itself only sees an infinite time)
+    int merr = NEO_OK;
+    std::string merr_msg;
+    auto measure_failed = [&](int code) {
+        if (merr == NEO_OK) {
+            merr = code;
+            merr_msg = neo_last_error();
+        }
+    };
 
     const int D = P->block;
     std::map<std::vector<int>, double> xmemo;
@@ -803,11 +812,13 @@ int search_schemes(neo_plan* P) {
                                    ib, ob, has_res, has_b, cs.act};
         auto it = cmemo.find(key);
         if (it != cmemo.end()) return it->second;
-        if (rc != NEO_OK) return INFINITY;
+        if (merr != NEO_OK) return INFINITY;
         ConvConfig cfg{};
         float us = 0.f;
-        rc = tune_conv(cs, true, X, Wt, has_b ? Bz : nullptr, has_res ? Rz : nullptr, Y, st, &cfg, &us);
-        const double t = rc == NEO_OK ? us : INFINITY;
+        const int trc = tune_conv(cs, true, X, Wt, has_b ? Bz : nullptr, has_res ? Rz : nullptr, Y, st,
+                                  &cfg, &us);
+        if (trc != NEO_OK) measure_failed(trc);
+        const double t = trc == NEO_OK ? us : INFINITY;
         ++measured;
         cmemo[key] = t;
         return t;
@@ -818,11 +829,11 @@ int search_schemes(neo_plan* P) {
         const std::vector<int> key{ni.N, ni.C, ni.H, ni.W, sb, db};
         auto it = xmemo.find(key);
         if (it != xmemo.end()) return it->second;
-        if (rc != NEO_OK) return INFINITY;
+        if (merr != NEO_OK) return INFINITY;
         const double t = time_launches(st, [&]() {
             return launch_layout_transform(X, sb, Y, db, ni.N, ni.C, ni.H, ni.W, 0, units(ni.C, db), st);
         });
-        if (t < 0) rc = fail(NEO_ERR_HIP, "neo_plan_create: transform timing failed");
+        if (t < 0) measure_failed(fail(NEO_ERR_HIP, "neo_plan_create: transform timing failed"));
         xmemo[key] = t < 0 ? INFINITY : t;
         return xmemo[key];
     };
@@ -845,6 +856,7 @@ int search_schemes(neo_plan* P) {
     (void)hipStreamSynchronize(st);
     for (float* b : {X, Y, Rz, Wt, Bz})
         if (b) (void)hipFree(b);
+    if (merr != NEO_OK) return fail(merr, merr_msg);
     if (rc != NEO_OK) return rc;
     for (size_t v = 0; v < P->nodes.size(); ++v) {
         NodeInfo& ni = P->nodes[v];
