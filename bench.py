@@ -27,8 +27,9 @@ Printed JSON line:
                batch 1 and ResNet-50 at batch 32 for the ablation of Table 3:
                "naive" (transforms around every blocked operation), "eliminated"
                (one block for every conv, transforms only at the ends) and
-               "searched" (the global layout search); all with tuned launch
-               configurations
+               "searched" (the global layout search); plus "grouped" (the
+               eliminated plan with sibling convs fused into one launch); all
+               with tuned launch configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
 import argparse
@@ -61,25 +62,30 @@ def conv_costs(C, K, R, S, H, W, st, pd, N=1, residual=False):
 
 def plan_schemes(desc):
     """{conv node: (ic_bn, oc_bn)} of a plan description."""
-    return {s["node"]: (s["conv"]["ic_bn"], s["conv"]["oc_bn"]) for s in desc["steps"]
-            if s["kind"] == "conv"}
+    out = {}
+    for s in desc["steps"]:
+        for m in (s["members"] if s["kind"] == "conv_group" else [s] if s["kind"] == "conv" else []):
+            out[m["node"]] = (m["conv"]["ic_bn"], m["conv"]["oc_bn"])
+    return out
 
 
 def headline_plan(neo, g, tune_db=None, torch=None):
     """The plan bench.py times, and how it was chosen.  The global search
     (Section 3.3.2) chooses every conv's scheme from per-conv times measured
     in isolation; the resulting plan and the one-block plan (Section 3.2, all
-    convs in NCHW16c) are then both timed end to end and the faster is kept,
+    convs in NCHW16c) -- both with sibling convs fused into one launch --
+    are then both timed end to end and the faster is kept,
     so a search decision that the isolated timings mispredict cannot make the
     step slower.  With a results file from an earlier run (``--tune-db``) the
     schemes that run kept are reused from ``<file>.schemes.json`` (so a
     profiling run executes the same plan)."""
     path = (tune_db or "") + ".schemes.json"
+    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP
     if tune_db and os.path.exists(path):
         sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
-        return neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH, schemes=sch), {"from": path}
-    searched = neo.Plan(g, flags=neo.PLAN_GLOBAL_SEARCH | neo.PLAN_HIPGRAPH)
-    fixed = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+        return neo.Plan(g, flags=neo.PLAN_TUNE | base, schemes=sch), {"from": path}
+    searched = neo.Plan(g, flags=neo.PLAN_GLOBAL_SEARCH | base)
+    fixed = neo.Plan(g, flags=neo.PLAN_TUNE | base)
     x = torch.from_numpy(g.x).cuda()
     out = torch.empty(searched.output_shape[:2], device="cuda")
     t_s = min(e2e_ms(torch, searched, x, out, 100, 10) for _ in range(3))
@@ -95,14 +101,40 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     return keep, info
 
 
-def plan_conv_flops(desc):
-    tot = 0
-    for s in desc["steps"]:
+def conv_launches(desc):
+    """The plan's conv launches: (step index, [(conv fields, has residual)],
+    launch configuration) -- one conv, or the members of a fused group."""
+    out = []
+    for i, s in enumerate(desc["steps"]):
         if s["kind"] == "conv":
             c = s["conv"]
-            tot += conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"], c["pad"],
-                              N=c["N"])[0]
-    return tot
+            out.append((i, [(c, s["res"] >= 0)],
+                        dict(tile=c["tile"], split=c["split"], waves=c["waves"], ic_bn=c["ic_bn"],
+                             oc_bn=c["oc_bn"])))
+        elif s["kind"] == "conv_group":
+            out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
+                        dict(tile=s["tile"], split=1, waves=s["waves"], ic_bn=16, oc_bn=16,
+                             group=len(s["members"]))))
+    return out
+
+
+def launch_costs(members):
+    """Algorithmic FLOPs and bytes of one launch (summed over its convs)."""
+    f = b = 0
+    for c, res in members:
+        ff, bb, _, _ = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"],
+                                  c["pad"], N=c["N"], residual=res)
+        f, b = f + ff, b + bb
+    return f, b
+
+
+def conv_label(c):
+    OH = (c["H"] + 2 * c["pad"][0] - c["R"]) // c["stride"][0] + 1
+    return f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} {c['H']}->{OH}"
+
+
+def plan_conv_flops(desc):
+    return sum(launch_costs(m)[0] for _, m, _ in conv_launches(desc))
 
 
 def time_graph(torch, fn, reps, rounds=3):
@@ -217,12 +249,9 @@ def layer_table(torch, plan, x, out, reps, cold=True):
     plan.run(x, out)      # intermediate buffers hold real activations
     torch.cuda.synchronize()
     rows = {}
-    for i, s in enumerate(d["steps"]):
-        if s["kind"] != "conv":
-            continue
-        c = s["conv"]
-        key = (c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"], c["W"],
-               c["N"], c["ic_bn"], c["oc_bn"])
+    for i, members, cfg in conv_launches(d):
+        key = tuple((c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"],
+                     c["W"], c["N"], c["ic_bn"], c["oc_bn"]) for c, _ in members)
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
         cold_us = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4)) if cold else 0.0
         if key in rows:
@@ -230,13 +259,9 @@ def layer_table(torch, plan, x, out, reps, cold=True):
             rows[key]["_t"].append(us)
             rows[key]["_c"].append(cold_us)
             continue
-        flops, nbytes, OH, OW = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"],
-                                           c["stride"], c["pad"], N=c["N"], residual=s["res"] >= 0)
-        rows[key] = dict(shape=f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} "
-                               f"{c['H']}->{OH}", uses=1, flops=flops, bytes=nbytes,
-                         config=dict(tile=c["tile"], split=c["split"], waves=c["waves"],
-                                     ic_bn=c["ic_bn"], oc_bn=c["oc_bn"]), _t=[us],
-                         _c=[cold_us])
+        flops, nbytes = launch_costs(members)
+        rows[key] = dict(shape=" + ".join(conv_label(c) for c, _ in members), uses=1, flops=flops,
+                         bytes=nbytes, config=cfg, _t=[us], _c=[cold_us])
     out_rows = []
     for r in rows.values():
         us = float(np.mean(r.pop("_t")))
@@ -260,10 +285,8 @@ def layer_table(torch, plan, x, out, reps, cold=True):
 def scheme_summary(d):
     """Histogram of the convs' (ic_bn, oc_bn) in a plan description."""
     h = {}
-    for s in d["steps"]:
-        if s["kind"] == "conv":
-            k = f"{s['conv']['ic_bn']}/{s['conv']['oc_bn']}"
-            h[k] = h.get(k, 0) + 1
+    for ic, oc in plan_schemes(d).values():
+        h[f"{ic}/{oc}"] = h.get(f"{ic}/{oc}", 0) + 1
     return dict(sorted(h.items()))
 
 
@@ -276,7 +299,7 @@ def model_latencies(neo, torch, wl, steps):
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        plans = [("eliminated", 0, 16)]
+        plans = [("eliminated", 0, 16), ("grouped", neo.PLAN_GROUP, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
         if name == "resnet50":
@@ -304,6 +327,7 @@ def model_latencies(neo, torch, wl, steps):
             entry["elimination_speedup"] = round(entry["naive"]["ms"] / entry["eliminated"]["ms"], 3)
         if "searched" in entry:
             entry["search_speedup"] = round(entry["eliminated"]["ms"] / entry["searched"]["ms"], 3)
+        entry["group_speedup"] = round(entry["eliminated"]["ms"] / entry["grouped"]["ms"], 3)
         res[f"{name}_b{batch}"] = entry
         del g, x
         print(f"[bench] {name} b{batch}: {entry}", file=sys.stderr, flush=True)
@@ -398,7 +422,8 @@ def main():
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
                         unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4),
                         traffic=measured_traffic(),
-                        kernel="conv2d_blocked", launches_per_step=n_launch,
+                        kernel="conv2d_blocked (single and fused-group launches)",
+                        launches_per_step=n_launch,
                         avg_launch_us=round(tot_t / n_launch * 1e6, 2),
                         flop_per_launch=round(tot_f / n_launch))
         for r in layers:
@@ -465,6 +490,8 @@ def main():
         neo.tune_db_save(args.save_tune_db)
         with open(args.save_tune_db + ".schemes.json", "w") as f:
             json.dump({str(k): list(v) for k, v in plan_schemes(desc).items()}, f)
+        with open(args.save_tune_db + ".plan.json", "w") as f:
+            json.dump(desc, f)
 
 
 if __name__ == "__main__":

@@ -261,7 +261,16 @@ enum neo_plan_flags {
      * layout transform the choice implies, minimised over the whole network by
      * neo_layout_search's dynamic program.  Implies NEO_PLAN_TUNE; needs a
      * device plan. */
-    NEO_PLAN_GLOBAL_SEARCH = 16
+    NEO_PLAN_GLOBAL_SEARCH = 16,
+    /* Horizontal fusion (not in the paper; for batch-1 latency on a GPU,
+     * where one small conv cannot fill the device and a launch costs more
+     * than its work): convolutions that read the same value, and whose
+     * residual is ready by the first of them, run as one launch (up to 4;
+     * NCHW16c convs of more than 4 input channels).  The members share one
+     * launch configuration (tuned for the group with NEO_PLAN_TUNE), so their
+     * results match the oracle but are not bit-identical to an ungrouped
+     * plan's. */
+    NEO_PLAN_GROUP = 32
 };
 
 /*

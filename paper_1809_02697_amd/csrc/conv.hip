@@ -7,6 +7,8 @@ namespace neo {
 
 using namespace conv_detail;
 
+static_assert(kMaxGroup == kMaxGroupConvs, "group size");
+
 extern template hipError_t conv_detail::dispatch_all<true>(const ConvConfig&, int, bool, bool,
                                                            const ConvArgs&, hipStream_t);
 
@@ -79,10 +81,12 @@ size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c) {
     return (size_t)c.split * s.N * cdiv(s.K, 16) * s.OH * s.OW * 64;
 }
 
-hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
-                         bool wmfma, const float* bias, const float* res, float* y, float* ws,
-                         hipStream_t st) {
-    if (!conv_config_valid(c) || !conv_blocks_valid(s)) return hipErrorInvalidValue;
+namespace {
+
+// Kernel arguments of one convolution for launch configuration c with G
+// channel groups per reduction step.
+ConvArgs make_args(const ConvShape& s, const ConvConfig& c, int G, const float* x, const float* w,
+                   bool wmfma, const float* bias, const float* res, float* y, float* ws) {
     ConvArgs a;
     a.x = x;
     a.w = w;
@@ -109,9 +113,8 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.y_off = s.y_off;
     a.y_tot = s.y_tot;
     a.act = s.act;
-    const int G = conv_group(s, c);
     a.CBG = a.CB / G;
-    a.T = conv_steps(s, c);
+    a.T = conv_small_c(s) ? s.R * cdiv(s.S, 4) : a.CBG * s.R * s.S;
     a.split = (c.split > 1 && ws) ? std::min(c.split, a.T) : 1;
     a.xb = s.xb;
     a.XB = cdiv(s.C, s.xb);
@@ -130,9 +133,83 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
     a.div_nkb = make_fastdiv((unsigned)cdiv(a.KBk, c.fk));
+    return a;
+}
+
+}  // namespace
+
+hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
+                         bool wmfma, const float* bias, const float* res, float* y, float* ws,
+                         hipStream_t st) {
+    if (!conv_config_valid(c) || !conv_blocks_valid(s)) return hipErrorInvalidValue;
+    const int G = conv_group(s, c);
+    const ConvArgs a = make_args(s, c, G, x, w, wmfma, bias, res, y, ws);
     const bool small = conv_small_c(s);
     if (s.xb == 16 && s.yb == 16) return dispatch_all<false>(c, G, small, wmfma, a, st);
     return dispatch_all<true>(c, G, small, wmfma, a, st);
+}
+
+bool conv_group_eligible(const ConvShape& s) { return !conv_small_c(s) && s.xb == 16 && s.yb == 16; }
+
+int conv_group_steps_min(const ConvShape* s, int n, const ConvConfig& c) {
+    int G = 4, steps = 1 << 30;
+    for (int i = 0; i < n; ++i) G = std::min(G, conv_group(s[i], c));
+    for (int i = 0; i < n; ++i) steps = std::min(steps, cdiv(s[i].C, 16) / G * s[i].R * s[i].S);
+    return steps;
+}
+
+bool conv_group_config_valid(const ConvShape* s, int n, const ConvConfig& c) {
+    if (n < 1 || n > kMaxGroupConvs || c.split != 1 || !conv_config_valid(c)) return false;
+    for (int i = 0; i < n; ++i) {
+        if (!conv_group_eligible(s[i])) return false;
+        const int KB = cdiv(s[i].K, 16), MP = cdiv(s[i].N * s[i].OH * s[i].OW, 16);
+        if ((c.fk > 1 && c.fk > KB) || (c.fp > 1 && c.fp > MP)) return false;
+    }
+    return conv_group_steps_min(s, n, c) >= c.waves;
+}
+
+ConvConfig choose_group_config(const ConvShape* s, int n) {
+    // the cost model's choice for the member with the most work, made valid
+    // for every member (no split, a tile and wave count all can use)
+    int big = 0;
+    double most = -1;
+    for (int i = 0; i < n; ++i) {
+        const double f = (double)s[i].N * s[i].OH * s[i].OW * s[i].K * s[i].C * s[i].R * s[i].S;
+        if (f > most) {
+            most = f;
+            big = i;
+        }
+    }
+    ConvConfig c = choose_conv_config(s[big]);
+    c.split = 1;
+    for (int fk : {c.fk, 2, 1})
+        for (int fp : {c.fp, 2, 1})
+            for (int wv : {c.waves, 4, 2, 1}) {
+                const ConvConfig t{fk, fp, 1, wv};
+                if (conv_group_config_valid(s, n, t)) return t;
+            }
+    return ConvConfig{1, 1, 1, 1};
+}
+
+hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, const float* const* x,
+                             const float* const* w, const float* const* bias,
+                             const float* const* res, float* const* y, hipStream_t st) {
+    if (!conv_group_config_valid(s, n, c)) return hipErrorInvalidValue;
+    int G = 4;
+    for (int i = 0; i < n; ++i) G = std::min(G, conv_group(s[i], c));
+    ConvGroupArgs ga;
+    ga.n = n;
+    ga.start[0] = 0;
+    for (int i = 0; i < n; ++i) {
+        ga.a[i] = make_args(s[i], c, G, x[i], w[i], true, bias[i], res[i], y[i], nullptr);
+        const int wgs = cdiv(ga.a[i].M, 16 * c.fp) * cdiv(ga.a[i].KBk, c.fk);
+        ga.start[i + 1] = ga.start[i] + wgs;
+    }
+    for (int i = n; i < kMaxGroup; ++i) {
+        ga.a[i] = ga.a[n - 1];
+        ga.start[i + 1] = ga.start[n];
+    }
+    return dispatch_group(c, G, ga, ga.start[n], st);
 }
 
 }  // namespace neo

@@ -346,20 +346,24 @@ __device__ inline void mma(const Operands<FK, FP, G>& o, v4f (&acc)[FK][FP]) {
                                                                      acc[f][p], 0, 0, 0);
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2.
+// The logical workgroup index gives every XCD a contiguous run of the logical
+// order (member, split, channel tile, pixel tile), so the pixel tiles that
+// share a filter slice run on one XCD and read it from that XCD's L2.
+__device__ inline int xcd_order() {
+    const int nwg = gridDim.x;
+    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+    const int q = nwg / kXcds, rmd = nwg % kXcds;
+    return xcd * q + min(xcd, rmd) + slot;
+}
+
+// One workgroup's output tile: logical workgroup u of the convolution a.
 template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES, bool XY>
-__global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
+__device__ __forceinline__ void conv_tile(const ConvArgs& a, const int u) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int li = lane & 15;
     const int g = lane >> 4;
-    // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
-    // L2.  Give every XCD a contiguous run of the logical order
-    // (split, channel tile, pixel tile), so the pixel tiles that share a
-    // filter slice run on one XCD and read it from that XCD's L2.
-    const int nwg = gridDim.x;
-    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
-    const int q = nwg / kXcds, rmd = nwg % kXcds;
-    const int u = xcd * q + min(xcd, rmd) + slot;
     const int npx = a.div_npx.d, nkb = a.div_nkb.d;
     const int u_px = fdiv(u, a.div_npx);
     const int pxt = u - u_px * npx;
@@ -560,6 +564,31 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
     }
 }
 
+template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES, bool XY>
+__global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
+    conv_tile<FK, FP, G, SMALLC, WMFMA, WAVES, XY>(a, xcd_order());
+}
+
+// Several independent convolutions in one launch (horizontal fusion, for
+// batch 1 where each is too small to fill the chip and a launch costs more
+// than its work): member m owns logical workgroups [start[m], start[m+1]).
+// Every member uses the same kernel parameters and no split reduction.
+constexpr int kMaxGroup = 4;
+struct ConvGroupArgs {
+    ConvArgs a[kMaxGroup];
+    int start[kMaxGroup + 1];
+    int n;
+};
+
+template <int FK, int FP, int G, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void conv2d_mfma_group(ConvGroupArgs ga) {
+    const int u = xcd_order();
+    int m = 0;
+    while (m + 1 < ga.n && u >= ga.start[m + 1]) ++m;
+    m = __builtin_amdgcn_readfirstlane(m);
+    conv_tile<FK, FP, G, false, true, WAVES, false>(ga.a[m], u - ga.start[m]);
+}
+
 // Second pass of a split reduction: y = act(sum_z part[z] + bias + res), the
 // splits added in order z = 0, 1, ... (deterministic).  One thread per
 // (pixel, 4-channel quad).
@@ -654,6 +683,43 @@ hipError_t dispatch(const ConvConfig& c, int g, const ConvArgs& a, hipStream_t s
     }
 }
 
+
+// Group launches: the NCHW16c family only, no split (conv_group.hip).
+template <int FK, int FP, int G, int WAVES>
+hipError_t launch_group_t(const ConvGroupArgs& ga, int wgs, hipStream_t st) {
+    hipLaunchKernelGGL((conv2d_mfma_group<FK, FP, G, WAVES>), dim3(wgs), dim3(WAVES * 64), 0, st, ga);
+    return hipGetLastError();
+}
+
+template <int FK, int FP, int G>
+hipError_t group_by_waves(int waves, const ConvGroupArgs& ga, int wgs, hipStream_t st) {
+    if (waves == 1) return launch_group_t<FK, FP, G, 1>(ga, wgs, st);
+    if (waves == 2) return launch_group_t<FK, FP, G, 2>(ga, wgs, st);
+    if (waves == 4) return launch_group_t<FK, FP, G, 4>(ga, wgs, st);
+    if constexpr (FK * FP <= 4) {
+        if (waves == 8) return launch_group_t<FK, FP, G, 8>(ga, wgs, st);
+    }
+    if constexpr (FK * FP <= 2) {
+        if (waves == 16) return launch_group_t<FK, FP, G, 16>(ga, wgs, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int FK, int FP>
+hipError_t group_by_g(int g, int waves, const ConvGroupArgs& ga, int wgs, hipStream_t st) {
+    if constexpr (FK * FP == 1) {
+        if (g == 4) return group_by_waves<FK, FP, 4>(waves, ga, wgs, st);
+    }
+    if constexpr (FK * FP <= 2) {
+        if (g == 2) return group_by_waves<FK, FP, 2>(waves, ga, wgs, st);
+    }
+    if (g == 1) return group_by_waves<FK, FP, 1>(waves, ga, wgs, st);
+    return hipErrorInvalidValue;
+}
+
+// Defined in conv_group.hip.
+hipError_t dispatch_group(const ConvConfig& c, int g, const ConvGroupArgs& ga, int wgs,
+                          hipStream_t st);
 
 // Every launch configuration and path of one kernel family: XY = false for
 // NCHW16c in and out, XY = true for any other pair of blocks.  Instantiated

@@ -75,6 +75,23 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st);
 
+// Several independent convolutions in one launch (horizontal fusion): NCHW16c
+// in and out, more than 4 input channels, one launch configuration for all
+// (no split).  x[i], w[i] (kernel filter order), bias[i], res[i], y[i] as for
+// launch_conv2d.
+constexpr int kMaxGroupConvs = 4;
+bool conv_group_eligible(const ConvShape& s);
+bool conv_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);
+ConvConfig choose_group_config(const ConvShape* s, int n);
+hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, const float* const* x,
+                             const float* const* w, const float* const* bias,
+                             const float* const* res, float* const* y, hipStream_t st);
+// Local search over the configurations valid for every member of a group;
+// results are kept per group of workloads for the process.
+int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,
+                    const float* const* bias, const float* const* res, float* const* y,
+                    hipStream_t st, ConvConfig* best, float* us);
+
 // Local search (tune.cpp): the database's configuration for a shape (with its
 // blocks), if any; and a search that times every candidate with the given
 // buffers on `st` and returns the fastest with its time per launch in us.

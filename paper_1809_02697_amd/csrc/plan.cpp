@@ -22,6 +22,8 @@
 // buffer.
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -37,7 +39,7 @@ using namespace neo;
 
 namespace {
 
-enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY };
+enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY, ST_CONV_GROUP };
 
 struct Val {
     int N = 0, C = 0, H = 0, W = 0;
@@ -64,6 +66,7 @@ struct Step {
     long w_off = -1, b_off = -1;
     int src_block = 0, dst_block = 0;
     int dense_in = 0, dense_out = 0, act = 0;
+    std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's)
 };
 
 struct Xform {
@@ -620,6 +623,67 @@ int build_steps(neo_plan* P) {
     return NEO_OK;
 }
 
+// NEO_PLAN_GROUP: convs that read the same value (siblings) and whose residual
+// is ready by the first of them become one launch (up to kMaxGroupConvs).
+// A later sibling moves up to the first one's place: its input and residual
+// exist there, and its readers all come after its old place.  Only NCHW16c
+// convs of more than 4 input channels take part (one kernel family).
+void group_siblings(neo_plan* P) {
+    std::vector<Step>& S = P->steps;
+    std::vector<int> producer(P->vals.size(), -1);  // step writing each value
+    for (size_t i = 0; i < S.size(); ++i)
+        if (S[i].out >= 0) producer[S[i].out] = (int)i;
+    auto ready_at = [&](int v, int i) {  // value v computed before step i
+        if (v < 0) return true;
+        int r = v;
+        while (P->vals[r].alias_of >= 0) r = P->vals[r].alias_of;
+        return producer[r] < i;  // -1: the network input
+    };
+    std::vector<Step> out;
+    std::vector<bool> taken(S.size(), false);
+    for (size_t i = 0; i < S.size(); ++i) {
+        if (taken[i]) continue;
+        Step st = S[i];
+        if (st.kind == ST_CONV && conv_group_eligible(st.cs)) {
+            std::vector<size_t> mem{i};
+            for (size_t j = i + 1; j < S.size() && mem.size() < (size_t)kMaxGroupConvs; ++j) {
+                const Step& o = S[j];
+                if (taken[j] || o.kind != ST_CONV || o.in != st.in || !conv_group_eligible(o.cs)) continue;
+                if (!ready_at(o.res, (int)i)) continue;
+                mem.push_back(j);
+            }
+            if (mem.size() > 1) {
+                Step grp{};
+                grp.kind = ST_CONV_GROUP;
+                grp.node = st.node;
+                grp.in = st.in;
+                for (size_t j : mem) {
+                    grp.members.push_back(S[j]);
+                    taken[j] = true;
+                }
+                std::vector<ConvShape> shp;
+                for (const Step& m : grp.members) shp.push_back(m.cs);
+                grp.cc = choose_group_config(shp.data(), (int)shp.size());
+                // launch-configuration sweeps: "fk,fp,waves" for every group it suits
+                if (const char* e = std::getenv("NEO_GROUP_CONFIG")) {
+                    ConvConfig t{1, 1, 1, 1};
+                    if (std::sscanf(e, "%d,%d,%d", &t.fk, &t.fp, &t.waves) == 3 &&
+                        conv_group_config_valid(shp.data(), (int)shp.size(), t)) {
+                        grp.cc = t;
+                        grp.tuned = true;  // kept as given, not searched
+                    }
+                }
+                for (Step& m : grp.members) m.cc = grp.cc;
+                out.push_back(grp);
+                continue;
+            }
+        }
+        taken[i] = true;
+        out.push_back(st);
+    }
+    S.swap(out);
+}
+
 float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     const Val& val = P->vals[v];
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
@@ -663,14 +727,15 @@ std::string describe(const neo_plan* P) {
           << "}";
     }
     o << "],\"n_transforms\":" << P->xforms.size() << ",\"steps\":[";
-    static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy"};
+    static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy",
+                                  "conv_group"};
     for (size_t i = 0; i < P->steps.size(); ++i) {
         const Step& s = P->steps[i];
         o << (i ? "," : "") << "{\"kind\":\"" << kinds[s.kind] << "\",\"node\":" << s.node
           << ",\"in\":" << s.in << ",\"out\":" << s.out << ",\"res\":" << s.res;
-        if (s.kind == ST_CONV) {
+        auto conv_json = [&](const Step& s) {
             const ConvShape& c = s.cs;
-            o << ",\"conv\":{\"N\":" << c.N << ",\"C\":" << c.C << ",\"H\":" << c.H << ",\"W\":" << c.W
+            o << "{\"N\":" << c.N << ",\"C\":" << c.C << ",\"H\":" << c.H << ",\"W\":" << c.W
               << ",\"K\":" << c.K << ",\"R\":" << c.R << ",\"S\":" << c.S << ",\"stride\":[" << c.sh
               << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
@@ -678,6 +743,22 @@ std::string describe(const neo_plan* P) {
               << ",\"ic_bn\":" << c.xb << ",\"oc_bn\":" << c.yb
               << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
               << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false") << "}";
+        };
+        if (s.kind == ST_CONV) {
+            o << ",\"conv\":";
+            conv_json(s);
+        }
+        if (s.kind == ST_CONV_GROUP) {
+            o << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"waves\":" << s.cc.waves
+              << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"members\":[";
+            for (size_t m = 0; m < s.members.size(); ++m) {
+                const Step& ms = s.members[m];
+                o << (m ? "," : "") << "{\"node\":" << ms.node << ",\"in\":" << ms.in
+                  << ",\"out\":" << ms.out << ",\"res\":" << ms.res << ",\"conv\":";
+                conv_json(ms);
+                o << "}";
+            }
+            o << "]";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
@@ -928,7 +1009,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (block != 16 && block != 32 && block != 64)
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
-                            NEO_PLAN_GLOBAL_SEARCH))
+                            NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -944,6 +1025,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_siblings(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     } catch (const std::exception& e) {
@@ -1024,8 +1106,14 @@ int neo_plan_output_shape(const neo_plan* plan, int* dims) {
 
 int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, float* bias) {
     if (!live(plan)) return fail(NEO_ERR_STATE, "neo_plan_conv_params: not a live plan");
+    std::vector<const Step*> convs;
     for (const Step& s : plan->steps) {
-        if (s.kind != ST_CONV || s.node != node_id) continue;
+        if (s.kind == ST_CONV) convs.push_back(&s);
+        for (const Step& m : s.members) convs.push_back(&m);
+    }
+    for (const Step* sp : convs) {
+        const Step& s = *sp;
+        if (s.node != node_id) continue;
         if (w_packed) from_kernel_order(plan->params.data() + s.w_off, s.cs, w_packed);
         if (bias) {
             const long bn = (long)cdiv(s.cs.K, 16) * 16;
@@ -1060,6 +1148,23 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                                   s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
                                   val_ptr(P, s.out, x_nchw, y_out), P->d_ws, st);
                 break;
+            case ST_CONV_GROUP: {
+                ConvShape shp[kMaxGroupConvs];
+                const float *xs[kMaxGroupConvs], *ws[kMaxGroupConvs], *bs[kMaxGroupConvs], *rs[kMaxGroupConvs];
+                float* ys[kMaxGroupConvs];
+                const int n = (int)s.members.size();
+                for (int m = 0; m < n; ++m) {
+                    const Step& ms = s.members[m];
+                    shp[m] = ms.cs;
+                    xs[m] = val_ptr(P, ms.in, x_nchw, y_out);
+                    ws[m] = prm + ms.w_off;
+                    bs[m] = ms.b_off >= 0 ? prm + ms.b_off : nullptr;
+                    rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, x_nchw, y_out) : nullptr;
+                    ys[m] = val_ptr(P, ms.out, x_nchw, y_out);
+                }
+                e = launch_conv_group(shp, n, s.cc, xs, ws, bs, rs, ys, st);
+                break;
+            }
             case ST_MAXPOOL:
                 e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
@@ -1119,6 +1224,29 @@ static int tune_plan(neo_plan* P) {
     int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: tuning buffers");
     for (Step& s : P->steps) {
         if (rc != NEO_OK) break;
+        if (s.kind == ST_CONV_GROUP && !s.tuned) {
+            ConvShape shp[kMaxGroupConvs];
+            const float *xs[kMaxGroupConvs], *ws[kMaxGroupConvs], *bs[kMaxGroupConvs], *rs[kMaxGroupConvs];
+            float* ys[kMaxGroupConvs];
+            const int n = (int)s.members.size();
+            const float* prm = P->d_params;
+            for (int m = 0; m < n; ++m) {
+                const Step& ms = s.members[m];
+                shp[m] = ms.cs;
+                xs[m] = val_ptr(P, ms.in, xin, yout);
+                ws[m] = prm + ms.w_off;
+                bs[m] = ms.b_off >= 0 ? prm + ms.b_off : nullptr;
+                rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, xin, yout) : nullptr;
+                ys[m] = val_ptr(P, ms.out, xin, yout);
+            }
+            rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, P->cap_stream, &s.cc, nullptr);
+            s.tuned = rc == NEO_OK;
+            for (Step& m : s.members) {
+                m.cc = s.cc;
+                m.tuned = s.tuned;
+            }
+            continue;
+        }
         if (s.kind != ST_CONV || s.tuned) continue;
         const float* prm = P->d_params;
         rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,

@@ -167,6 +167,80 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
     return NEO_OK;
 }
 
+namespace {
+std::map<std::vector<int>, Entry> g_group_db;  // per process: group of workloads -> config
+}
+
+int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,
+                    const float* const* bias, const float* const* res, float* const* y,
+                    hipStream_t st, ConvConfig* best_out, float* us_out) {
+    std::vector<int> key;
+    for (int i = 0; i < n; ++i)
+        key.insert(key.end(), {s[i].N, s[i].C, s[i].H, s[i].W, s[i].K, s[i].R, s[i].S, s[i].sh,
+                               s[i].sw, s[i].ph, s[i].pw});
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_group_db.find(key);
+        if (it != g_group_db.end()) {
+            *best_out = it->second.cfg;
+            if (us_out) *us_out = it->second.us;
+            return NEO_OK;
+        }
+    }
+    hipEvent_t e0, e1;
+    (void)hipEventCreate(&e0);
+    (void)hipEventCreate(&e1);
+    const int reps = 10;
+    ConvConfig best = choose_group_config(s, n);
+    float best_us = 1e30f;
+    hipError_t e = hipSuccess;
+    for (int fk : {1, 2, 4})
+        for (int fp : {1, 2, 4})
+            for (int wv : {1, 2, 4, 8, 16}) {
+                const ConvConfig c{fk, fp, 1, wv};
+                if (e != hipSuccess || !conv_group_config_valid(s, n, c)) continue;
+                e = launch_conv_group(s, n, c, x, w, bias, res, y, st);  // warm-up
+                if (e != hipSuccess) break;
+                hipGraph_t g = nullptr;
+                hipGraphExec_t ge = nullptr;
+                e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+                for (int i = 0; i < reps && e == hipSuccess; ++i)
+                    e = launch_conv_group(s, n, c, x, w, bias, res, y, st);
+                hipError_t e2 = hipStreamEndCapture(st, &g);
+                if (e == hipSuccess) e = e2;
+                if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+                if (g) (void)hipGraphDestroy(g);
+                float ms = 1e30f;
+                for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+                    e = hipGraphLaunch(ge, st);
+                    if (e == hipSuccess) e = hipEventRecord(e0, st);
+                    if (e == hipSuccess) e = hipGraphLaunch(ge, st);
+                    if (e == hipSuccess) e = hipEventRecord(e1, st);
+                    if (e == hipSuccess) e = hipEventSynchronize(e1);
+                    float t = 0.f;
+                    if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+                    if (e == hipSuccess) ms = std::min(ms, t);
+                }
+                if (ge) (void)hipGraphExecDestroy(ge);
+                const float us = ms * 1000.f / reps;
+                if (e == hipSuccess && us < best_us) {
+                    best_us = us;
+                    best = c;
+                }
+            }
+    (void)hipStreamSynchronize(st);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (e != hipSuccess) return hip_fail(e, "group tuning");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_group_db[key] = Entry{best, best_us};
+    }
+    *best_out = best;
+    if (us_out) *us_out = best_us;
+    return NEO_OK;
+}
+
 }  // namespace neo
 
 using namespace neo;
@@ -221,6 +295,7 @@ int neo_tune_db_load(const char* path) {
 void neo_tune_db_clear(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     g_db.clear();
+    g_group_db.clear();
 }
 
 int neo_tune_db_size(void) {

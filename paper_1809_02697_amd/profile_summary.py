@@ -31,7 +31,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SRCS = [os.path.join(HERE, "csrc", f) for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip")]
+KERNEL_SRCS = [os.path.join(HERE, "csrc", f)
+               for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip")]
 
 
 def kernel_hash():
@@ -57,13 +58,11 @@ def forward_dispatches(path):
     return copy, fwd
 
 
-def conv_steps():
-    from paper_1809_02697_amd import neo
-    from paper_1809_02697_amd import workloads as wl
-    p = neo.Plan(wl.resnet50(1), flags=neo.PLAN_HOST_ONLY)
-    d = p.describe()
-    p.destroy()
-    return [s for s in d["steps"] if s["kind"] == "conv"]
+def conv_launches(run_dir):
+    """The conv launches of the plan the bench run timed (its description is
+    saved next to the results file): one conv or a fused group each."""
+    from bench import conv_launches as launches
+    return launches(json.load(open(os.path.join(run_dir, "tune_db.txt.plan.json"))))
 
 
 def per_conv(fwd):
@@ -80,7 +79,7 @@ def per_conv(fwd):
 
 def main(run_dir):
     sys.path.insert(0, ROOT)
-    from bench import conv_costs
+    from bench import conv_label, launch_costs
     from paper_1809_02697_amd.profile_layers import COPY_MB
     copy_bytes = COPY_MB * 2 ** 20
 
@@ -90,20 +89,18 @@ def main(run_dir):
     fw = copy_bytes / (w_copy * 1024.0)
     fetch = per_conv(f_fwd)
     write = per_conv(w_fwd)
-    steps = conv_steps()
-    assert len(fetch) == len(write) == len(steps) == 53, (len(fetch), len(write), len(steps))
+    steps = conv_launches(run_dir)
+    n_convs = sum(len(m) for _, m, _ in steps)
+    assert n_convs == 53 and len(fetch) == len(write) == len(steps), (len(fetch), len(write), len(steps))
 
     layer_rows = []
     tot_alg = tot_traffic = 0.0
-    for s, fv, wv in zip(steps, fetch, write):
-        c = s["conv"]
-        _, alg, OH, _ = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"],
-                                   c["pad"], N=c["N"], residual=s["res"] >= 0)
+    for (_, members, _), fv, wv in zip(steps, fetch, write):
+        alg = launch_costs(members)[1]
         rd, wr = fv * 1024 * ff, wv * 1024 * fw
         tot_alg += alg
         tot_traffic += rd + wr
-        layer_rows.append((f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} {c['H']}->{OH}",
-                           alg, rd, wr))
+        layer_rows.append((" + ".join(conv_label(c) for c, _ in members), alg, rd, wr))
 
     trace = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_trace.csv"))
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
@@ -115,7 +112,7 @@ def main(run_dir):
     ev_avg = bench["roofline"]["avg_launch_us"]
 
     n = len(steps)
-    traffic = dict(kernel="conv2d_blocked", workload="ResNet-50 batch 1, 53 conv launches",
+    traffic = dict(kernel="conv2d_blocked", workload=f"ResNet-50 batch 1, 53 convs in {n} launches",
                    kernel_source_sha256=kernel_hash(),
                    traffic_bytes_per_launch=round(tot_traffic / n),
                    alg_bytes_per_launch=round(tot_alg / n),
@@ -124,7 +121,7 @@ def main(run_dir):
     with open(os.path.join(PROFILES, "conv2d_blocked_resnet50_b1_traffic.json"), "w") as f:
         json.dump(traffic, f, indent=1)
 
-    md = ["# conv2d_blocked, ResNet-50 batch 1 (53 conv launches per forward)", "",
+    md = [f"# conv2d_blocked, ResNet-50 batch 1 (53 convs in {n} launches per forward)", "",
           "Commands (run from the repository root on one MI355X; RUN_DIR = gpurun_out):", "",
           "```",
           "python bench.py --save-tune-db RUN_DIR/tune_db.txt > RUN_DIR/bench.log",
@@ -138,7 +135,8 @@ def main(run_dir):
           "```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
           "## Launch duration", "",
-          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma + its split_reduce pass, "
+          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma or conv2d_mfma_group + its "
+          f"split_reduce pass, "
           f"{len(conv_d)} conv dispatches): **{trace_avg:.2f} us**",
           f"- bench.py HIP events (graph replays of each conv step, weighted by use): "
           f"**{ev_avg:.2f} us** (ratio {trace_avg / ev_avg:.3f})",

@@ -1,0 +1,96 @@
+"""Host-side checks of horizontal fusion (NEO_PLAN_GROUP): which convs share
+a launch, that the launch list stays a valid order, and that every conv of
+the network is launched exactly once."""
+import numpy as np
+import pytest
+
+from paper_1809_02697_amd import neo
+from paper_1809_02697_amd import workloads as wl
+
+
+def _plan(g, flags=0):
+    p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_GROUP | flags)
+    d = p.describe()
+    p.destroy()
+    return d
+
+
+def _launch_items(d):
+    """(step index, reads, writes) per launched conv or other step."""
+    for i, s in enumerate(d["steps"]):
+        if s["kind"] == "conv_group":
+            for m in s["members"]:
+                yield i, [m["in"]] + ([m["res"]] if m["res"] >= 0 else []), m["out"], m
+        else:
+            yield i, [s["in"]] + ([s["res"]] if s["res"] >= 0 else []), s["out"], s
+
+
+@pytest.mark.parametrize("build,groups,sizes", [
+    (lambda: wl.resnet50(1), 4, [2, 2, 2, 2]),
+    (lambda: wl.inception_v3(1), 15, None),
+    (wl.tiny_graph, 2, [2, 2]),
+    (lambda: wl.vgg16(1), 0, [])])
+def test_group_structure(build, groups, sizes):
+    g = build()
+    d = _plan(g)
+    grp = [s for s in d["steps"] if s["kind"] == "conv_group"]
+    assert len(grp) == groups
+    if sizes is not None:
+        assert [len(s["members"]) for s in grp] == sizes
+    conv_nodes = sorted(i for i, n in enumerate(g.nodes) if n.op == "conv")
+    launched = sorted(m["node"] for s in d["steps"] if s["kind"] in ("conv", "conv_group")
+                      for m in (s["members"] if s["kind"] == "conv_group" else [s]))
+    assert launched == conv_nodes
+    for s in grp:
+        ins = {m["in"] for m in s["members"]}
+        assert len(ins) == 1                         # siblings of one value
+        assert all((m["conv"]["tile"], m["conv"]["waves"]) == (s["tile"], s["waves"])
+                   for m in s["members"])
+        assert all(m["conv"]["split"] == 1 and m["conv"]["ic_bn"] == 16 and m["conv"]["oc_bn"] == 16
+                   for m in s["members"])
+
+
+@pytest.mark.parametrize("build", [lambda: wl.resnet50(1), lambda: wl.inception_v3(1),
+                                   wl.tiny_graph])
+def test_grouped_launch_list_is_a_valid_order(build):
+    """Every value a step reads is the network input or was written by an
+    earlier step (the members of a group are independent, so never by the
+    same step)."""
+    g = build()
+    d = _plan(g)
+    vals = d["values"]
+    root = {}
+    for v in vals:
+        r = v["id"]
+        while vals[r]["alias_of"] >= 0:
+            r = vals[r]["alias_of"]
+        root[v["id"]] = r
+    written = {}
+    for i, _, out, _ in _launch_items(d):
+        if out >= 0:
+            written[root[out]] = i
+    # a concatenation has no step: it is complete once its inputs (written
+    # into slices of its buffer) are; nested concats first (node order)
+    for c, n in enumerate(g.nodes):
+        if n.op != "concat":
+            continue
+        cv = [v for v in vals if v["node"] == c][0]
+        parts = [written.get(root[u["id"]], 1 << 30) for u in vals
+                 if u["node"] in n.inputs and u["view"] and u["buf"] == cv["buf"]]
+        written[root[cv["id"]]] = max(parts)
+    for i, reads, _, item in _launch_items(d):
+        for r in reads:
+            rr = root[r]
+            if vals[rr]["buf"] == -2:                # the network input
+                continue
+            assert written.get(rr, 1 << 30) < i, (i, item.get("node"), r)
+
+
+def test_group_config_override(monkeypatch):
+    g = wl.resnet50(1)
+    monkeypatch.setenv("NEO_GROUP_CONFIG", "2,1,1")
+    d = _plan(g)
+    assert all((s["tile"], s["waves"]) == ([2, 1], 1) for s in d["steps"] if s["kind"] == "conv_group")
+    monkeypatch.setenv("NEO_GROUP_CONFIG", "4,4,16")     # not valid for these groups: ignored
+    d = _plan(g)
+    assert all(s["waves"] != 16 for s in d["steps"] if s["kind"] == "conv_group")
