@@ -637,7 +637,10 @@ void group_siblings(neo_plan* P) {
         if (v < 0) return true;
         int r = v;
         while (P->vals[r].alias_of >= 0) r = P->vals[r].alias_of;
-        return producer[r] < i;  // -1: the network input
+        if (P->vals[r].buf == kExtIn) return true;
+        // no step of its own (a concatenation, written slice by slice): taken
+        // as not ready, so such a residual keeps its conv out of the group
+        return producer[r] >= 0 && producer[r] < i;
     };
     std::vector<Step> out;
     std::vector<bool> taken(S.size(), false);

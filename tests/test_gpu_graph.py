@@ -180,3 +180,28 @@ def test_tuned_resnet50_end_to_end(neo):
     ref = orc.run_graph(g)
     e, strict = assert_close_network(y, ref, "tuned resnet50")
     print(f"\ntuned resnet50 b1: rel L2 {e:.2e}, beyond 1e-4(1+|ref|): {strict}")
+
+
+def test_bench_headline_plan_matches_oracle(neo):
+    """The plan bench.py times for ResNet-50 batch 1 -- global search, sibling
+    fusion, tuned, graph replay, the faster of the searched and one-block
+    plans -- against the oracle, replayed several times."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+    torch = torch_cuda()
+    g = wl.resnet50(1)
+    p, info = bench.headline_plan(neo, g, None, torch)
+    x = dev(g.x)
+    out = torch.empty((1, 1000), device="cuda")
+    ref = orc.run_graph(g)
+    first = None
+    for _ in range(3):
+        p.run(x, out)
+        y = host(out)
+        first = y if first is None else first
+        np.testing.assert_array_equal(y, first)
+    p.destroy()
+    e, strict = assert_close_network(first, ref, "bench headline plan")
+    print(f"\nheadline plan ({info['kept']}): rel L2 {e:.2e}, beyond 1e-4(1+|ref|): {strict}")

@@ -101,3 +101,12 @@ def test_tuned_grouped_resnet50_graph_replay(neo):
         torch.ones(1000, device="cuda").sum()
         np.testing.assert_array_equal(host(out), eager)
     p.destroy()
+
+
+def test_concat_residual_group_matches_oracle(neo):
+    from test_group_host import concat_residual_graph
+    g = concat_residual_graph()
+    ref = orc.run_graph(g)
+    y, d = _run(neo, g, neo.PLAN_GROUP)
+    assert any(s["kind"] == "conv_group" for s in d["steps"])
+    assert_close(y.reshape(ref.shape), ref, "concat residual")

@@ -94,3 +94,26 @@ def test_group_config_override(monkeypatch):
     monkeypatch.setenv("NEO_GROUP_CONFIG", "4,4,16")     # not valid for these groups: ignored
     d = _plan(g)
     assert all(s["waves"] != 16 for s in d["steps"] if s["kind"] == "conv_group")
+
+
+def concat_residual_graph():
+    """x read by three convs; the third adds the concatenation of the first
+    two as its residual, so it must not join their launch."""
+    b = wl._Builder("catres", (1, 16, 9, 9), np.random.Generator(np.random.PCG64(5)))
+    x = b.conv(0, 32, 3, pad=1, name="stem")
+    c1 = b.conv(x, 16, 1, name="c1")
+    c2 = b.conv(x, 16, 3, pad=1, name="c2")
+    cat = b.concat([c1, c2], name="cat")
+    a = b.conv(x, 32, 1, residual=cat, name="a")
+    b.output(a)
+    return b.finish(lambda rng: rng.normal(0, 1, (1, 16, 9, 9)).astype(np.float32))
+
+
+def test_concat_residual_keeps_its_conv_out_of_the_group():
+    g = concat_residual_graph()
+    d = _plan(g)
+    grp = [s for s in d["steps"] if s["kind"] == "conv_group"]
+    assert len(grp) == 1
+    assert sorted(m["node"] for m in grp[0]["members"]) == [2, 3]
+    names = [g.nodes[s["node"]].name for s in d["steps"] if s["kind"] == "conv"]
+    assert "a" in names
