@@ -9,6 +9,8 @@ import oracle as orc
 from paper_1809_02697_amd import neo
 from paper_1809_02697_amd import workloads as wl
 
+import nets
+
 L = neo.lib()
 P = ctypes.c_void_p
 
@@ -91,7 +93,7 @@ def host_plan(g, flags=0):
 
 
 def test_resnet50_plan_has_two_transforms():
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     p = host_plan(g)
     d = p.describe()
     assert d["n_transforms"] == 2
@@ -115,7 +117,7 @@ def test_resnet50_plan_has_two_transforms():
 
 
 def test_vgg16_plan_exit_transform_is_real():
-    g = wl.vgg16(1)
+    g = nets.vgg16()
     d = host_plan(g).describe()
     assert d["n_transforms"] == 2
     t_out = d["transforms"][1]
@@ -125,7 +127,7 @@ def test_vgg16_plan_exit_transform_is_real():
 
 
 def test_inception_plan_concat_views():
-    g = wl.inception_v3(1)
+    g = nets.inception_v3()
     d = host_plan(g).describe()
     assert d["n_transforms"] == 2
     kinds = [s["kind"] for s in d["steps"]]
@@ -145,7 +147,7 @@ def test_inception_plan_concat_views():
 
 
 def test_naive_plan_wraps_every_blocked_op():
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     d = host_plan(g, neo.PLAN_NAIVE).describe()
     kinds = [s["kind"] for s in d["steps"]]
     # every conv / pool / gap result goes back to NCHW, and every blocked input
@@ -161,7 +163,7 @@ def test_plan_conv_params_are_folded_and_packed(make):
     small-channel order for C <= 4); reading them back gives the folded
     KCRS[16]c[16]k filter exactly."""
     g = {"tiny": wl.tiny_graph, "vgg_tiny": wl.vgg_like_tiny,
-         "resnet50_stem": lambda: wl.resnet50(1)}[make]()
+         "resnet50_stem": lambda: nets.resnet50()}[make]()
     p = host_plan(g)
     for i, n in enumerate(g.nodes):
         if n.op != "conv":

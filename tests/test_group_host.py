@@ -7,6 +7,8 @@ import pytest
 from paper_1809_02697_amd import neo
 from paper_1809_02697_amd import workloads as wl
 
+import nets
+
 
 def _plan(g, flags=0):
     p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_GROUP | flags)
@@ -26,10 +28,10 @@ def _launch_items(d):
 
 
 @pytest.mark.parametrize("build,groups,sizes", [
-    (lambda: wl.resnet50(1), 4, [2, 2, 2, 2]),
-    (lambda: wl.inception_v3(1), 15, None),
+    (lambda: nets.resnet50(), 4, [2, 2, 2, 2]),
+    (lambda: nets.inception_v3(), 15, None),
     (wl.tiny_graph, 2, [2, 2]),
-    (lambda: wl.vgg16(1), 0, [])])
+    (lambda: nets.vgg16(), 0, [])])
 def test_group_structure(build, groups, sizes):
     g = build()
     d = _plan(g)
@@ -50,7 +52,7 @@ def test_group_structure(build, groups, sizes):
                    for m in s["members"])
 
 
-@pytest.mark.parametrize("build", [lambda: wl.resnet50(1), lambda: wl.inception_v3(1),
+@pytest.mark.parametrize("build", [lambda: nets.resnet50(), lambda: nets.inception_v3(),
                                    wl.tiny_graph])
 def test_grouped_launch_list_is_a_valid_order(build):
     """Every value a step reads is the network input or was written by an
@@ -87,7 +89,7 @@ def test_grouped_launch_list_is_a_valid_order(build):
 
 
 def test_group_config_override(monkeypatch):
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     monkeypatch.setenv("NEO_GROUP_CONFIG", "2,1,1")
     d = _plan(g)
     assert all((s["tile"], s["waves"]) == ([2, 1], 1) for s in d["steps"] if s["kind"] == "conv_group")

@@ -11,6 +11,8 @@ from oracle import search as S
 from paper_1809_02697_amd import neo
 from paper_1809_02697_amd import workloads as wl
 
+import nets
+
 from test_search_oracle import chain_graph, concat_graph, random_tables, residual_graph
 
 NB = len(S.BLOCKS)
@@ -41,9 +43,9 @@ def test_search_matches_oracle_integer_costs(name, make, seed):
     assert S.plan_cost(g, got, ct, xt) == best
 
 
-@pytest.mark.parametrize("build", [wl.resnet50, wl.vgg16, wl.inception_v3])
+@pytest.mark.parametrize("build", [nets.resnet50, nets.vgg16, nets.inception_v3])
 def test_search_matches_oracle_on_networks(build):
-    g = build(1)
+    g = build()
     for seed in (3, 4):
         ct, xt = random_tables(g, np.random.default_rng(seed), integer=True, p_drop=0.2)
         best, _ = S.global_search(g, ct, xt)
@@ -59,7 +61,7 @@ def test_search_matches_oracle_on_networks(build):
 
 
 def test_search_respects_given_schemes_and_block():
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     ct, xt = random_tables(g, np.random.default_rng(9), integer=True, p_drop=0.0)
     convs = S.conv_nodes(g)
     fixed = {convs[3]: (32, 32), convs[10]: (16, 64)}
@@ -122,8 +124,8 @@ def _random_schemes(g, rng, blocks=(16, 32, 64)):
 
 @pytest.mark.parametrize("build,seed", [(wl.tiny_graph, 0), (wl.tiny_graph, 1),
                                         (wl.vgg_like_tiny, 2), (residual_graph, 3),
-                                        (concat_graph, 4), (lambda: wl.resnet50(1), 5),
-                                        (lambda: wl.inception_v3(1), 6)])
+                                        (concat_graph, 4), (lambda: nets.resnet50(), 5),
+                                        (lambda: nets.inception_v3(), 6)])
 def test_plan_layouts_follow_the_search_rules(build, seed):
     """The plan inserts exactly the transforms the oracle's accounting pays
     for (and the aliases it counts as free), for random schemes."""
@@ -150,7 +152,7 @@ def test_plan_layouts_follow_the_search_rules(build, seed):
 def test_fixed_block_plans():
     """block 32 / 64: every conv in that block; ResNet-50 still has one
     transform in and one (aliased) out."""
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     for b in (32, 64):
         d, got = _plan_transforms(g, None, block=b)
         assert [t[1:] for t in got] == sorted([(0, b, False), (b, 0, True)])

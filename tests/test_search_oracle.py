@@ -10,6 +10,8 @@ import pytest
 from oracle import search as S
 from paper_1809_02697_amd import workloads as wl
 
+import nets
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 NB = len(S.BLOCKS)
 
@@ -227,7 +229,7 @@ def test_chain_reduces_to_the_recurrence():
 def test_fixed_block_assignment_is_section_3_2_plan():
     """All CONVs in 16 on ResNet-50: the only transform paid is the entry
     (the exit after the global pool is an alias), as in Section 3.2."""
-    g = wl.resnet50(1)
+    g = nets.resnet50()
     convs = S.conv_nodes(g)
     ct = [[[1.0] * NB for _ in range(NB)] for _ in g.nodes]
     xt = [[[1000.0] * NB for _ in range(NB)] for _ in g.nodes]
@@ -248,8 +250,8 @@ def test_search_on_real_networks_beats_or_ties_fixed_layout():
     most the cost of every fixed-16 assignment, and equals plan_cost of the
     assignment it returns."""
     rng = np.random.default_rng(5)
-    for build in (wl.resnet50, wl.vgg16, wl.inception_v3):
-        g = build(1)
+    for build in (nets.resnet50, nets.vgg16, nets.inception_v3):
+        g = build()
         ct, xt = random_tables(g, rng, integer=False, p_drop=0.0)
         best, sch = S.global_search(g, ct, xt)
         assert math.isclose(S.plan_cost(g, sch, ct, xt), best, rel_tol=1e-12)

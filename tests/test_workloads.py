@@ -6,6 +6,8 @@ import pytest
 
 from paper_1809_02697_amd import workloads as wl
 
+import nets
+
 
 def _out(n, k, s, p):
     return (n + 2 * p - k) // s + 1
@@ -65,7 +67,7 @@ def conv_flops(convs, N=1):
 
 @pytest.fixture(scope="module")
 def r50():
-    return wl.resnet50(1)
+    return nets.resnet50()
 
 
 def test_resnet50_invariants(r50):
@@ -91,7 +93,7 @@ def test_resnet50_distinct_shapes_are_the_layer_sweep(r50):
 
 
 def test_vgg16_invariants():
-    g = wl.vgg16(1)
+    g = nets.vgg16()
     shp, convs = walk(g)
     assert len(convs) == 13 and len(set(convs)) == 9
     assert conv_flops(convs) == 30_693_261_312
@@ -100,7 +102,7 @@ def test_vgg16_invariants():
 
 
 def test_inception_v3_invariants():
-    g = wl.inception_v3(1)
+    g = nets.inception_v3()
     shp, convs = walk(g)
     assert len(convs) == 94
     assert len(set(convs)) == 43
