@@ -28,7 +28,7 @@ Printed JSON line:
                "naive" (transforms around every blocked operation), "eliminated"
                (one block for every conv, transforms only at the ends) and
                "searched" (the global layout search); plus "grouped" (the
-               eliminated plan with sibling convs fused into one launch); all
+               eliminated plan with independent convs fused into one launch); all
                with tuned launch configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
@@ -73,7 +73,7 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     """The plan bench.py times, and how it was chosen.  The global search
     (Section 3.3.2) chooses every conv's scheme from per-conv times measured
     in isolation; the resulting plan and the one-block plan (Section 3.2, all
-    convs in NCHW16c) -- both with sibling convs fused into one launch --
+    convs in NCHW16c) -- both with independent convs fused into launches --
     are then both timed end to end and the faster is kept,
     so a search decision that the isolated timings mispredict cannot make the
     step slower.  With a results file from an earlier run (``--tune-db``) the

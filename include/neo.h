@@ -264,12 +264,16 @@ enum neo_plan_flags {
     NEO_PLAN_GLOBAL_SEARCH = 16,
     /* Horizontal fusion (not in the paper; for batch-1 latency on a GPU,
      * where one small conv cannot fill the device and a launch costs more
-     * than its work): convolutions that read the same value, and whose
-     * residual is ready by the first of them, run as one launch (up to 4;
-     * NCHW16c convs of more than 4 input channels).  The members share one
-     * launch configuration (tuned for the group with NEO_PLAN_TUNE), so their
-     * results match the oracle but are not bit-identical to an ungrouped
-     * plan's. */
+     * than its work): the launch list is list-scheduled in rounds -- a step
+     * joins the first round after every step that writes storage it reads --
+     * and the NCHW16c convs of more than 4 input channels of one round run as
+     * one launch (up to 4, in their original order; with sibling convs and
+     * parallel branches such as an Inception module's this fuses convs of
+     * different inputs).  The members share one launch configuration (tuned
+     * for the group with NEO_PLAN_TUNE, which also splits a group back into
+     * its members when their own best launches take less time one after
+     * another), so their results match the oracle but are not bit-identical
+     * to an ungrouped plan's. */
     NEO_PLAN_GROUP = 32
 };
 
@@ -327,9 +331,11 @@ void neo_plan_destroy(neo_plan* plan);
 /* and processor type so that a workload is searched once)                               */
 /* ------------------------------------------------------------------------------------ */
 /* Process-wide table: (GPU architecture, N, C, H, W, K, R, S, strides, pads, filter
- * order) -> launch configuration and its measured time.  Text file, one workload per
- * line.  save returns the number of entries written, load the number read (entries
- * are merged; a malformed line fails the whole load with NEO_ERR_INVALID_ARG). */
+ * order, input and output block) -> launch configuration and its measured time, and
+ * (GPU architecture, the shapes of a fused launch's convs) -> the group's configuration
+ * and time.  Text file, one entry per line.  save returns the number of entries
+ * written, load the number read, size the number held (entries are merged; a malformed
+ * line fails the whole load with NEO_ERR_INVALID_ARG). */
 int neo_tune_db_save(const char* path);
 int neo_tune_db_load(const char* path);
 void neo_tune_db_clear(void);

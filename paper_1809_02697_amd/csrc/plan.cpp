@@ -623,66 +623,89 @@ int build_steps(neo_plan* P) {
     return NEO_OK;
 }
 
-// NEO_PLAN_GROUP: convs that read the same value (siblings) and whose residual
-// is ready by the first of them become one launch (up to kMaxGroupConvs).
-// A later sibling moves up to the first one's place: its input and residual
-// exist there, and its readers all come after its old place.  Only NCHW16c
-// convs of more than 4 input channels take part (one kernel family).
-void group_siblings(neo_plan* P) {
+// NEO_PLAN_GROUP: list scheduling of the steps.  Every value has storage of
+// its own or a slice of a concatenation's, and none is reused, so a step has
+// to wait only for the earlier steps that wrote storage it reads.  The steps
+// are taken in rounds: each round holds every step whose producers ran in an
+// earlier round; its NCHW16c convs of more than 4 input channels become
+// launches of up to kMaxGroupConvs convs (in their original order), its other
+// steps run one by one.  Convs of one round are independent, so one grid can
+// run them all; at small batch sizes that fills the GPU where each alone
+// would not, and saves launches.
+void group_ready_convs(neo_plan* P) {
     std::vector<Step>& S = P->steps;
-    std::vector<int> producer(P->vals.size(), -1);  // step writing each value
-    for (size_t i = 0; i < S.size(); ++i)
-        if (S[i].out >= 0) producer[S[i].out] = (int)i;
-    auto ready_at = [&](int v, int i) {  // value v computed before step i
-        if (v < 0) return true;
-        int r = v;
-        while (P->vals[r].alias_of >= 0) r = P->vals[r].alias_of;
-        if (P->vals[r].buf == kExtIn) return true;
-        // no step of its own (a concatenation, written slice by slice): taken
-        // as not ready, so such a residual keeps its conv out of the group
-        return producer[r] >= 0 && producer[r] < i;
+    const int n = (int)S.size();
+    struct Extent {
+        int buf;
+        long lo, hi;  // channel range in the root buffer
     };
+    auto extent = [&](int v) {
+        const Val& x = P->vals[v];
+        const long f = x.layout ? x.layout : 1;
+        return Extent{x.buf, x.c_off * f, (x.c_off + units(x.C, x.layout)) * f};
+    };
+    auto overlap = [](const Extent& a, const Extent& b) {
+        return a.buf == b.buf && a.buf != kExtIn && a.lo < b.hi && b.lo < a.hi;
+    };
+    std::vector<std::vector<int>> deps(n);
+    for (int j = 0; j < n; ++j) {
+        std::vector<Extent> reads;
+        if (S[j].in >= 0) reads.push_back(extent(S[j].in));
+        if (S[j].res >= 0) reads.push_back(extent(S[j].res));
+        for (int i = 0; i < j; ++i) {
+            if (S[i].out < 0) continue;
+            const Extent w = extent(S[i].out);
+            for (const Extent& r : reads)
+                if (overlap(w, r)) {
+                    deps[j].push_back(i);
+                    break;
+                }
+        }
+    }
+    std::vector<char> done(n, 0);
     std::vector<Step> out;
-    std::vector<bool> taken(S.size(), false);
-    for (size_t i = 0; i < S.size(); ++i) {
-        if (taken[i]) continue;
-        Step st = S[i];
-        if (st.kind == ST_CONV && conv_group_eligible(st.cs)) {
-            std::vector<size_t> mem{i};
-            for (size_t j = i + 1; j < S.size() && mem.size() < (size_t)kMaxGroupConvs; ++j) {
-                const Step& o = S[j];
-                if (taken[j] || o.kind != ST_CONV || o.in != st.in || !conv_group_eligible(o.cs)) continue;
-                if (!ready_at(o.res, (int)i)) continue;
-                mem.push_back(j);
-            }
-            if (mem.size() > 1) {
-                Step grp{};
-                grp.kind = ST_CONV_GROUP;
-                grp.node = st.node;
-                grp.in = st.in;
-                for (size_t j : mem) {
-                    grp.members.push_back(S[j]);
-                    taken[j] = true;
-                }
-                std::vector<ConvShape> shp;
-                for (const Step& m : grp.members) shp.push_back(m.cs);
-                grp.cc = choose_group_config(shp.data(), (int)shp.size());
-                // launch-configuration sweeps: "fk,fp,waves" for every group it suits
-                if (const char* e = std::getenv("NEO_GROUP_CONFIG")) {
-                    ConvConfig t{1, 1, 1, 1};
-                    if (std::sscanf(e, "%d,%d,%d", &t.fk, &t.fp, &t.waves) == 3 &&
-                        conv_group_config_valid(shp.data(), (int)shp.size(), t)) {
-                        grp.cc = t;
-                        grp.tuned = true;  // kept as given, not searched
-                    }
-                }
-                for (Step& m : grp.members) m.cc = grp.cc;
-                out.push_back(grp);
+    for (int left = n; left > 0;) {
+        std::vector<int> ready, convs;
+        for (int j = 0; j < n; ++j) {
+            if (done[j]) continue;
+            bool ok = true;
+            for (int d : deps[j]) ok = ok && done[d];
+            if (ok) ready.push_back(j);
+        }
+        for (int j : ready) {
+            if (S[j].kind == ST_CONV && conv_group_eligible(S[j].cs))
+                convs.push_back(j);
+            else
+                out.push_back(S[j]);
+        }
+        for (size_t k = 0; k < convs.size(); k += kMaxGroupConvs) {
+            const size_t e = std::min(convs.size(), k + kMaxGroupConvs);
+            if (e - k == 1) {
+                out.push_back(S[convs[k]]);
                 continue;
             }
+            Step grp{};
+            grp.kind = ST_CONV_GROUP;
+            grp.node = S[convs[k]].node;
+            grp.in = S[convs[k]].in;
+            for (size_t m = k; m < e; ++m) grp.members.push_back(S[convs[m]]);
+            std::vector<ConvShape> shp;
+            for (const Step& m : grp.members) shp.push_back(m.cs);
+            grp.cc = choose_group_config(shp.data(), (int)shp.size());
+            // launch-configuration sweeps: "fk,fp,waves" for every group it suits
+            if (const char* ev = std::getenv("NEO_GROUP_CONFIG")) {
+                ConvConfig t{1, 1, 1, 1};
+                if (std::sscanf(ev, "%d,%d,%d", &t.fk, &t.fp, &t.waves) == 3 &&
+                    conv_group_config_valid(shp.data(), (int)shp.size(), t)) {
+                    grp.cc = t;
+                    grp.tuned = true;  // kept as given, not searched
+                }
+            }
+            for (Step& m : grp.members) m.cc = grp.cc;
+            out.push_back(grp);
         }
-        taken[i] = true;
-        out.push_back(st);
+        for (int j : ready) done[j] = 1;
+        left -= (int)ready.size();
     }
     S.swap(out);
 }
@@ -1028,7 +1051,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
-        if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_siblings(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     } catch (const std::exception& e) {
@@ -1225,6 +1248,7 @@ static int tune_plan(neo_plan* P) {
     if (e == hipSuccess) e = hipMalloc(&yout, std::max<size_t>((size_t)out.N * out.C * out.H * out.W * 4, 256));
     if (e == hipSuccess) e = hipMemset(xin, 0, (size_t)in.N * in.C * in.H * in.W * 4);
     int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: tuning buffers");
+    std::vector<Step> next;
     for (Step& s : P->steps) {
         if (rc != NEO_OK) break;
         if (s.kind == ST_CONV_GROUP && !s.tuned) {
@@ -1242,22 +1266,45 @@ static int tune_plan(neo_plan* P) {
                 rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, xin, yout) : nullptr;
                 ys[m] = val_ptr(P, ms.out, xin, yout);
             }
-            rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, P->cap_stream, &s.cc, nullptr);
-            s.tuned = rc == NEO_OK;
-            for (Step& m : s.members) {
-                m.cc = s.cc;
-                m.tuned = s.tuned;
+            float group_us = 0.f, alone_us = 0.f;
+            rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, P->cap_stream, &s.cc, &group_us);
+            // the fused launch stays only where it beats the members' own best
+            // launches one after another
+            ConvConfig own[kMaxGroupConvs];
+            for (int m = 0; m < n && rc == NEO_OK; ++m) {
+                float us = 0.f;
+                rc = tune_conv(shp[m], true, xs[m], ws[m], bs[m], rs[m], ys[m], P->cap_stream, &own[m], &us);
+                alone_us += us;
+            }
+            if (rc != NEO_OK) break;
+            s.tuned = true;
+            if (group_us < alone_us) {
+                for (Step& m : s.members) {
+                    m.cc = s.cc;
+                    m.tuned = true;
+                }
+                next.push_back(s);
+            } else {
+                for (int m = 0; m < n; ++m) {
+                    Step ms = s.members[m];
+                    ms.cc = own[m];
+                    ms.tuned = true;
+                    next.push_back(ms);
+                }
             }
             continue;
         }
-        if (s.kind != ST_CONV || s.tuned) continue;
-        const float* prm = P->d_params;
-        rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
-                       s.b_off >= 0 ? prm + s.b_off : nullptr,
-                       s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
-                       val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
-        s.tuned = rc == NEO_OK;
+        if (s.kind == ST_CONV && !s.tuned) {
+            const float* prm = P->d_params;
+            rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
+                           s.b_off >= 0 ? prm + s.b_off : nullptr,
+                           s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
+                           val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
+            s.tuned = rc == NEO_OK;
+        }
+        next.push_back(s);
     }
+    if (rc == NEO_OK) P->steps.swap(next);
     if (xin) (void)hipFree(xin);
     if (yout) (void)hipFree(yout);
     return rc;

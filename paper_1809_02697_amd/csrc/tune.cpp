@@ -168,16 +168,19 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
 }
 
 namespace {
-std::map<std::vector<int>, Entry> g_group_db;  // per process: group of workloads -> config
+// one launch of several convs: architecture and the members' shapes -> config
+using GroupKey = std::pair<std::string, std::vector<int>>;
+std::map<GroupKey, Entry> g_group_db;
+constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
 }
 
 int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,
                     const float* const* bias, const float* const* res, float* const* y,
                     hipStream_t st, ConvConfig* best_out, float* us_out) {
-    std::vector<int> key;
+    GroupKey key{device_arch(), {}};
     for (int i = 0; i < n; ++i)
-        key.insert(key.end(), {s[i].N, s[i].C, s[i].H, s[i].W, s[i].K, s[i].R, s[i].S, s[i].sh,
-                               s[i].sw, s[i].ph, s[i].pw});
+        key.second.insert(key.second.end(), {s[i].N, s[i].C, s[i].H, s[i].W, s[i].K, s[i].R, s[i].S,
+                                             s[i].sh, s[i].sw, s[i].ph, s[i].pw});
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_group_db.find(key);
@@ -249,11 +252,14 @@ extern "C" {
 
 // Text format, one workload per line:
 //   arch N C H W K R S sh sw ph pw wmfma xb yb fk fp split waves us
+// and one line per fused launch of n NCHW16c convs:
+//   group arch n (N C H W K R S sh sw ph pw) x n fk fp split waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
     if (!f) return fail(NEO_ERR_INVALID_ARG, std::string("neo_tune_db_save: cannot open ") + path);
     std::lock_guard<std::mutex> lk(g_mu);
+    f.precision(9);  // times round-trip exactly, so a reload makes the same choices
     for (const auto& kv : g_db) {
         const Key& k = kv.first;
         const Entry& v = kv.second;
@@ -262,7 +268,16 @@ int neo_tune_db_save(const char* path) {
           << ' ' << k.xb << ' ' << k.yb << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split
           << ' ' << v.cfg.waves << ' ' << v.us << '\n';
     }
-    return f ? (int)g_db.size() : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
+    for (const auto& kv : g_group_db) {
+        const std::vector<int>& k = kv.first.second;
+        const Entry& v = kv.second;
+        f << "group " << kv.first.first << ' ' << k.size() / kGroupShapeInts;
+        for (int x : k) f << ' ' << x;
+        f << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split << ' ' << v.cfg.waves << ' '
+          << v.us << '\n';
+    }
+    return f ? (int)(g_db.size() + g_group_db.size())
+             : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
 int neo_tune_db_load(const char* path) {
@@ -272,12 +287,33 @@ int neo_tune_db_load(const char* path) {
     std::string line;
     int n = 0, lineno = 0;
     std::map<Key, Entry> add;
+    std::map<GroupKey, Entry> add_group;
     while (std::getline(f, line)) {
         ++lineno;
         if (line.empty() || line[0] == '#') continue;
         std::istringstream is(line);
         Key k;
         Entry v;
+        if (line.compare(0, 6, "group ") == 0) {
+            std::string tag;
+            GroupKey gk;
+            int members = 0;
+            bool ok = (bool)(is >> tag >> gk.first >> members) && members >= 1 &&
+                      members <= kMaxGroupConvs;
+            for (int i = 0; ok && i < members * kGroupShapeInts; ++i) {
+                int x = 0;
+                ok = (bool)(is >> x);
+                gk.second.push_back(x);
+            }
+            ok = ok && (is >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >> v.us) &&
+                 v.cfg.split == 1 && conv_config_valid(v.cfg);
+            if (!ok)
+                return fail(NEO_ERR_INVALID_ARG,
+                            "neo_tune_db_load: malformed line " + std::to_string(lineno));
+            add_group[gk] = v;
+            ++n;
+            continue;
+        }
         if (!(is >> k.arch >> k.N >> k.C >> k.H >> k.W >> k.K >> k.R >> k.S >> k.sh >> k.sw >> k.ph >>
               k.pw >> k.wmfma >> k.xb >> k.yb >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >>
               v.us) ||
@@ -289,6 +325,7 @@ int neo_tune_db_load(const char* path) {
     }
     std::lock_guard<std::mutex> lk(g_mu);
     for (const auto& kv : add) g_db[kv.first] = kv.second;
+    for (const auto& kv : add_group) g_group_db[kv.first] = kv.second;
     return n;
 }
 
@@ -300,7 +337,7 @@ void neo_tune_db_clear(void) {
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
-    return (int)g_db.size();
+    return (int)(g_db.size() + g_group_db.size());
 }
 
 }  // extern "C"

@@ -183,7 +183,7 @@ def test_tuned_resnet50_end_to_end(neo):
 
 
 def test_bench_headline_plan_matches_oracle(neo):
-    """The plan bench.py times for ResNet-50 batch 1 -- global search, sibling
+    """The plan bench.py times for ResNet-50 batch 1 -- global search, horizontal
     fusion, tuned, graph replay, the faster of the searched and one-block
     plans -- against the oracle, replayed several times."""
     import os

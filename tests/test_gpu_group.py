@@ -1,5 +1,6 @@
-"""GPU parity of horizontally fused launches (NEO_PLAN_GROUP): sibling convs
-that read the same value run as one launch with a shared launch
+"""GPU parity of horizontally fused launches (NEO_PLAN_GROUP): the NCHW16c
+convs of one round of the list schedule (siblings of one value, and the
+parallel branches of a module) run as one launch with a shared launch
 configuration.  Checked against the oracle for every configuration the group
 kernel instantiates, on the three networks, tuned, and under graph replay."""
 import numpy as np
@@ -101,6 +102,60 @@ def test_tuned_grouped_resnet50_graph_replay(neo):
         torch.ones(1000, device="cuda").sum()
         np.testing.assert_array_equal(host(out), eager)
     p.destroy()
+
+
+def _db_times(path):
+    """{conv shape: us} and {tuple of member shapes: us} from a saved results
+    file (shape = N C H W K R S sh sw ph pw)."""
+    convs, groups = {}, {}
+    for line in open(path).read().splitlines():
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if f[0] == "group":
+            n = int(f[2])
+            ints = tuple(int(v) for v in f[3:3 + 11 * n])
+            groups[tuple(ints[11 * i:11 * i + 11] for i in range(n))] = float(f[-1])
+        elif f[13:15] == ["16", "16"] and f[12] == "1":
+            convs[tuple(int(v) for v in f[1:12])] = float(f[-1])
+    return convs, groups
+
+
+def _shape(c):
+    return (c["N"], c["C"], c["H"], c["W"], c["K"], c["R"], c["S"], c["stride"][0], c["stride"][1],
+            c["pad"][0], c["pad"][1])
+
+
+def test_tuned_inception_keeps_only_faster_groups(neo, tmp_path):
+    """With NEO_PLAN_TUNE a fused launch stays only where its measured time
+    is below the sum of its members' own best times; the tuned plan matches
+    the oracle, and a plan rebuilt from the saved results file in a clean
+    database is the same launch list."""
+    neo.tune_db_clear()
+    g = wl.inception_v3(1)
+    ref = orc.run_graph(g)
+    y, d = _run(neo, g, neo.PLAN_GROUP | neo.PLAN_TUNE)
+    assert_close_network(y.reshape(ref.shape), ref, "tuned grouped inception")
+    path = tmp_path / "db.txt"
+    neo.tune_db_save(path)
+    convs, groups = _db_times(path)
+    kept = set()
+    for s in d["steps"]:
+        if s["kind"] != "conv_group":
+            continue
+        key = tuple(_shape(m["conv"]) for m in s["members"])
+        kept.add(key)
+        assert groups[key] < sum(convs[k] for k in key)
+    for key, us in groups.items():
+        if key not in kept:
+            assert us >= sum(convs[k] for k in key)
+    print(f"\n{len(kept)} of {len(groups)} tuned groups kept")
+    neo.tune_db_clear()
+    neo.tune_db_load(path)
+    _, d2 = _run(neo, g, neo.PLAN_GROUP | neo.PLAN_TUNE)
+    strip = lambda d: [(s["kind"], s["node"], s.get("tile"), s.get("waves"),
+                        s.get("conv", {}).get("tile")) for s in d["steps"]]
+    assert strip(d2) == strip(d)
 
 
 def test_concat_residual_group_matches_oracle(neo):

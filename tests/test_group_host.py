@@ -1,6 +1,7 @@
 """Host-side checks of horizontal fusion (NEO_PLAN_GROUP): which convs share
-a launch, that the launch list stays a valid order, and that every conv of
-the network is launched exactly once."""
+a launch (the NCHW16c convs of one round of the list schedule: every step
+whose producers ran in earlier rounds), that the launch list stays a valid
+order, and that every conv of the network is launched exactly once."""
 import numpy as np
 import pytest
 
@@ -29,7 +30,8 @@ def _launch_items(d):
 
 @pytest.mark.parametrize("build,groups,sizes", [
     (lambda: nets.resnet50(), 4, [2, 2, 2, 2]),
-    (lambda: nets.inception_v3(), 15, None),
+    (lambda: nets.inception_v3(), 27, [3, 3, 3, 3, 3, 3, 2, 3, 3, 2, 3, 3, 2, 3, 3, 2, 3, 3, 2, 2, 2,
+                                       3, 4, 2, 3, 4, 2]),
     (wl.tiny_graph, 2, [2, 2]),
     (lambda: nets.vgg16(), 0, [])])
 def test_group_structure(build, groups, sizes):
@@ -44,8 +46,6 @@ def test_group_structure(build, groups, sizes):
                       for m in (s["members"] if s["kind"] == "conv_group" else [s]))
     assert launched == conv_nodes
     for s in grp:
-        ins = {m["in"] for m in s["members"]}
-        assert len(ins) == 1                         # siblings of one value
         assert all((m["conv"]["tile"], m["conv"]["waves"]) == (s["tile"], s["waves"])
                    for m in s["members"])
         assert all(m["conv"]["split"] == 1 and m["conv"]["ic_bn"] == 16 and m["conv"]["oc_bn"] == 16
@@ -86,6 +86,41 @@ def test_grouped_launch_list_is_a_valid_order(build):
             if vals[rr]["buf"] == -2:                # the network input
                 continue
             assert written.get(rr, 1 << 30) < i, (i, item.get("node"), r)
+
+
+def _names(g, d):
+    return [[g.nodes[m["node"]].name for m in s["members"]] if s["kind"] == "conv_group"
+            else g.nodes[s["node"]].name for s in d["steps"]]
+
+
+def test_parallel_branches_share_launches():
+    """Inception's first module: the three 1x1 convs that read the module's
+    input form round one; the second convs of two branches and the pooling
+    branch's 1x1 (three different inputs) form round two; the last conv of
+    the double-3x3 branch runs alone.  The module's average pool is ready
+    with round one and is launched before it."""
+    g = nets.inception_v3()
+    names = _names(g, _plan(g))
+    i = names.index("Mixed_5b.avgpool")
+    assert names[i + 1:i + 4] == [
+        ["Mixed_5b.branch1x1", "Mixed_5b.branch5x5_1", "Mixed_5b.branch3x3dbl_1"],
+        ["Mixed_5b.branch5x5_2", "Mixed_5b.branch3x3dbl_2", "Mixed_5b.branch_pool"],
+        "Mixed_5b.branch3x3dbl_3"]
+    # a 7x7-factorised module: five rounds of convs instead of ten launches
+    i = names.index("Mixed_6b.avgpool")
+    assert names[i + 1:i + 6] == [
+        ["Mixed_6b.branch1x1", "Mixed_6b.branch7x7_1", "Mixed_6b.branch7x7dbl_1"],
+        ["Mixed_6b.branch7x7_2", "Mixed_6b.branch7x7dbl_2", "Mixed_6b.branch_pool"],
+        ["Mixed_6b.branch7x7_3", "Mixed_6b.branch7x7dbl_3"],
+        "Mixed_6b.branch7x7dbl_4", "Mixed_6b.branch7x7dbl_5"]
+
+
+def test_ungrouped_plan_keeps_node_order():
+    g = nets.inception_v3()
+    d = neo.Plan(g, flags=neo.PLAN_HOST_ONLY)
+    names = [n for n in _names(g, d.describe()) if not isinstance(n, list)]
+    d.destroy()
+    assert names.index("Mixed_5b.branch3x3dbl_3") < names.index("Mixed_5b.branch_pool")
 
 
 def test_group_config_override(monkeypatch):
