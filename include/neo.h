@@ -269,11 +269,12 @@ enum neo_plan_flags {
      * and the NCHW16c convs of more than 4 input channels of one round run as
      * one launch (up to 4, in their original order; with sibling convs and
      * parallel branches such as an Inception module's this fuses convs of
-     * different inputs).  The members share one launch configuration (tuned
-     * for the group with NEO_PLAN_TUNE, which also splits a group back into
-     * its members when their own best launches take less time one after
-     * another), so their results match the oracle but are not bit-identical
-     * to an ungrouped plan's. */
+     * different inputs), and a pooling step of the round runs in extra
+     * workgroups of such a launch (bit-identical to its own kernel).  The
+     * members share one launch configuration (tuned for the launch with
+     * NEO_PLAN_TUNE, which also takes the pool out, or splits the convs into
+     * launches of their own, when that measures faster), so their results
+     * match the oracle but are not bit-identical to an ungrouped plan's. */
     NEO_PLAN_GROUP = 32
 };
 
@@ -331,9 +332,10 @@ void neo_plan_destroy(neo_plan* plan);
 /* and processor type so that a workload is searched once)                               */
 /* ------------------------------------------------------------------------------------ */
 /* Process-wide table: (GPU architecture, N, C, H, W, K, R, S, strides, pads, filter
- * order, input and output block) -> launch configuration and its measured time, and
- * (GPU architecture, the shapes of a fused launch's convs) -> the group's configuration
- * and time.  Text file, one entry per line.  save returns the number of entries
+ * order, input and output block) -> launch configuration and its measured time;
+ * (GPU architecture, the shapes of a fused launch's convs and pooling step) -> the
+ * launch's configuration and time; (GPU architecture, a pooling step's shape) -> its
+ * time alone.  Text file, one entry per line.  save returns the number of entries
  * written, load the number read, size the number held (entries are merged; a malformed
  * line fails the whole load with NEO_ERR_INVALID_ARG). */
 int neo_tune_db_save(const char* path);

@@ -193,8 +193,10 @@ ConvConfig choose_group_config(const ConvShape* s, int n) {
 
 hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, const float* const* x,
                              const float* const* w, const float* const* bias,
-                             const float* const* res, float* const* y, hipStream_t st) {
+                             const float* const* res, float* const* y, const GroupPool* pool,
+                             hipStream_t st) {
     if (!conv_group_config_valid(s, n, c)) return hipErrorInvalidValue;
+    if (pool && !pow2_block(pool->s.xb)) return hipErrorInvalidValue;
     int G = 4;
     for (int i = 0; i < n; ++i) G = std::min(G, conv_group(s[i], c));
     ConvGroupArgs ga;
@@ -209,7 +211,25 @@ hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, con
         ga.a[i] = ga.a[n - 1];
         ga.start[i + 1] = ga.start[n];
     }
-    return dispatch_group(c, G, ga, ga.start[n], st);
+    PoolPart& pp = ga.pool;
+    pp = PoolPart{};
+    if (pool) {
+        const PoolShape& ps = pool->s;
+        pp.x = pool->x;
+        pp.y = pool->y;
+        pp.s = ps;
+        pp.CB = cdiv(ps.C, ps.xb);
+        pp.lq = ilog2(ps.xb / 4);
+        const long total = ((long)ps.N * pp.CB * ps.OH * ps.OW) << pp.lq;
+        if (total >= (1L << 31)) return hipErrorInvalidValue;
+        pp.total = (int)total;
+        pp.max = pool->max ? 1 : 0;
+        pp.k33 = ps.R == 3 && ps.S == 3;
+        // one output quad per thread, at most 1024 workgroups (then grid-stride)
+        const long per = 64L * c.waves;
+        pp.wgs = (int)std::min<long>(1024, std::max<long>(1, (total + per - 1) / per));
+    }
+    return dispatch_group(c, G, ga, ga.start[n] + pp.wgs, st);
 }
 
 }  // namespace neo

@@ -63,6 +63,7 @@
 #include <cmath>
 
 #include "neo_internal.h"
+#include "pool_kernel.h"
 
 namespace neo {
 namespace conv_detail {
@@ -350,12 +351,13 @@ __device__ inline void mma(const Operands<FK, FP, G>& o, v4f (&acc)[FK][FP]) {
 // The logical workgroup index gives every XCD a contiguous run of the logical
 // order (member, split, channel tile, pixel tile), so the pixel tiles that
 // share a filter slice run on one XCD and read it from that XCD's L2.
-__device__ inline int xcd_order() {
-    const int nwg = gridDim.x;
-    const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+// (For workgroup b of the first nwg of the grid.)
+__device__ inline int xcd_order(int b, int nwg) {
+    const int xcd = b % kXcds, slot = b / kXcds;
     const int q = nwg / kXcds, rmd = nwg % kXcds;
     return xcd * q + min(xcd, rmd) + slot;
 }
+__device__ inline int xcd_order() { return xcd_order(blockIdx.x, gridDim.x); }
 
 // One workgroup's output tile: logical workgroup u of the convolution a.
 template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES, bool XY>
@@ -573,16 +575,42 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
 // batch 1 where each is too small to fill the chip and a launch costs more
 // than its work): member m owns logical workgroups [start[m], start[m+1]).
 // Every member uses the same kernel parameters and no split reduction.
+// A pooling step may ride along in workgroups past the convs' (wgs of them,
+// grid-stride over its output quads, the same arithmetic as the pooling
+// kernel); it is independent of the convs.  Those workgroups come last in
+// dispatch order, which spreads them over the XCDs.
 constexpr int kMaxGroup = 4;
+struct PoolPart {
+    const float* x;
+    float* y;
+    PoolShape s;
+    int CB, lq, total, max, k33, wgs;  // wgs = 0: no pooling step
+};
 struct ConvGroupArgs {
     ConvArgs a[kMaxGroup];
     int start[kMaxGroup + 1];
     int n;
+    PoolPart pool;
 };
+
+template <bool MAX, int K>
+__device__ inline void pool_part_run(const PoolPart& p, int wg) {
+    for (int t = wg * blockDim.x + threadIdx.x; t < p.total; t += p.wgs * blockDim.x)
+        pool_detail::pool_elem<MAX, K, K>(p.x, p.y, p.s, p.CB, p.lq, t);
+}
 
 template <int FK, int FP, int G, int WAVES>
 __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma_group(ConvGroupArgs ga) {
-    const int u = xcd_order();
+    const int nconv = ga.start[ga.n];
+    if ((int)blockIdx.x >= nconv) {
+        const int wg = blockIdx.x - nconv;
+        if (ga.pool.max)
+            ga.pool.k33 ? pool_part_run<true, 3>(ga.pool, wg) : pool_part_run<true, 0>(ga.pool, wg);
+        else
+            ga.pool.k33 ? pool_part_run<false, 3>(ga.pool, wg) : pool_part_run<false, 0>(ga.pool, wg);
+        return;
+    }
+    const int u = xcd_order(blockIdx.x, nconv);
     int m = 0;
     while (m + 1 < ga.n && u >= ga.start[m + 1]) ++m;
     m = __builtin_amdgcn_readfirstlane(m);

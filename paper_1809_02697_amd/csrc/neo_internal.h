@@ -75,22 +75,40 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st);
 
+// Pooling on NCHW[xb]c (xb in 4..64); y_off / y_tot: output view in blocks.
+struct PoolShape {
+    int N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot;
+    int xb = 16;
+};
+
+// A pooling step run by the last workgroups of a fused conv launch (it is
+// independent of the launch's convs).
+struct GroupPool {
+    PoolShape s;
+    bool max;
+    const float* x;
+    float* y;
+};
+
 // Several independent convolutions in one launch (horizontal fusion): NCHW16c
 // in and out, more than 4 input channels, one launch configuration for all
 // (no split).  x[i], w[i] (kernel filter order), bias[i], res[i], y[i] as for
-// launch_conv2d.
+// launch_conv2d; pool (may be null) runs in extra workgroups of the launch.
 constexpr int kMaxGroupConvs = 4;
 bool conv_group_eligible(const ConvShape& s);
 bool conv_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);
 ConvConfig choose_group_config(const ConvShape* s, int n);
 hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, const float* const* x,
                              const float* const* w, const float* const* bias,
-                             const float* const* res, float* const* y, hipStream_t st);
-// Local search over the configurations valid for every member of a group;
-// results are kept per group of workloads for the process.
+                             const float* const* res, float* const* y, const GroupPool* pool,
+                             hipStream_t st);
+// Local search over the configurations valid for every member of a group
+// (with its pool, if any); results are kept per group of workloads.
 int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,
                     const float* const* bias, const float* const* res, float* const* y,
-                    hipStream_t st, ConvConfig* best, float* us);
+                    const GroupPool* pool, hipStream_t st, ConvConfig* best, float* us);
+// Time per launch of a pooling step alone (kept in the results database).
+int tune_pool(const GroupPool& p, hipStream_t st, float* us);
 
 // Local search (tune.cpp): the database's configuration for a shape (with its
 // blocks), if any; and a search that times every candidate with the given
@@ -110,11 +128,6 @@ hipError_t launch_pack_filter(const float* w, int K, int C, int R, int S, int ib
                               float* out, hipStream_t st);
 
 // ---- pools ----------------------------------------------------------------------------
-// Input and output in NCHW[xb]c (xb in 4..64); y_off / y_tot in blocks.
-struct PoolShape {
-    int N, C, H, W, R, S, sh, sw, ph, pw, OH, OW, y_off, y_tot;
-    int xb = 16;
-};
 hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
 hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st);

@@ -67,6 +67,7 @@ struct Step {
     int src_block = 0, dst_block = 0;
     int dense_in = 0, dense_out = 0, act = 0;
     std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's)
+    std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1)
 };
 
 struct Xform {
@@ -628,8 +629,10 @@ int build_steps(neo_plan* P) {
 // to wait only for the earlier steps that wrote storage it reads.  The steps
 // are taken in rounds: each round holds every step whose producers ran in an
 // earlier round; its NCHW16c convs of more than 4 input channels become
-// launches of up to kMaxGroupConvs convs (in their original order), its other
-// steps run one by one.  Convs of one round are independent, so one grid can
+// launches of up to kMaxGroupConvs convs (in their original order), and each
+// of its pooling steps rides along in one of those launches (in workgroups
+// after the convs'; a lone conv becomes a one-conv launch for it); its other
+// steps run one by one.  Steps of one round are independent, so one grid can
 // run them all; at small batch sizes that fills the GPU where each alone
 // would not, and saves launches.
 void group_ready_convs(neo_plan* P) {
@@ -662,10 +665,14 @@ void group_ready_convs(neo_plan* P) {
                 }
         }
     }
+    // a pooling step of the round rides along in one of its conv launches
+    // (NEO_GROUP_POOLS=0 keeps pools in launches of their own)
+    const char* gp = std::getenv("NEO_GROUP_POOLS");
+    const bool pools_ride = !(gp && gp[0] == '0');
     std::vector<char> done(n, 0);
     std::vector<Step> out;
     for (int left = n; left > 0;) {
-        std::vector<int> ready, convs;
+        std::vector<int> ready, convs, pools;
         for (int j = 0; j < n; ++j) {
             if (done[j]) continue;
             bool ok = true;
@@ -675,16 +682,21 @@ void group_ready_convs(neo_plan* P) {
         for (int j : ready) {
             if (S[j].kind == ST_CONV && conv_group_eligible(S[j].cs))
                 convs.push_back(j);
+            else if (pools_ride && (S[j].kind == ST_MAXPOOL || S[j].kind == ST_AVGPOOL))
+                pools.push_back(j);
             else
                 out.push_back(S[j]);
         }
+        size_t next_pool = 0;
         for (size_t k = 0; k < convs.size(); k += kMaxGroupConvs) {
             const size_t e = std::min(convs.size(), k + kMaxGroupConvs);
-            if (e - k == 1) {
+            const bool with_pool = next_pool < pools.size();
+            if (e - k == 1 && !with_pool) {
                 out.push_back(S[convs[k]]);
                 continue;
             }
             Step grp{};
+            if (with_pool) grp.pools.push_back(S[pools[next_pool++]]);
             grp.kind = ST_CONV_GROUP;
             grp.node = S[convs[k]].node;
             grp.in = S[convs[k]].in;
@@ -704,6 +716,7 @@ void group_ready_convs(neo_plan* P) {
             for (Step& m : grp.members) m.cc = grp.cc;
             out.push_back(grp);
         }
+        for (; next_pool < pools.size(); ++next_pool) out.push_back(S[pools[next_pool]]);
         for (int j : ready) done[j] = 1;
         left -= (int)ready.size();
     }
@@ -715,6 +728,17 @@ float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
     if (val.buf == P->ext_out_buf) return y_out;
     return reinterpret_cast<float*>(P->d_act + P->buf_off[val.buf]);
+}
+
+// The pooling step riding in a fused conv launch, with its buffers.
+bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_out, GroupPool* gp) {
+    if (s.pools.empty()) return false;
+    const Step& ps = s.pools[0];
+    gp->s = ps.ps;
+    gp->max = ps.kind == ST_MAXPOOL;
+    gp->x = val_ptr(P, ps.in, x_in, y_out);
+    gp->y = val_ptr(P, ps.out, x_in, y_out);
+    return true;
 }
 
 std::string describe(const neo_plan* P) {
@@ -785,6 +809,9 @@ std::string describe(const neo_plan* P) {
                 o << "}";
             }
             o << "]";
+            for (const Step& ps : s.pools)
+                o << ",\"pool\":{\"kind\":\"" << kinds[ps.kind] << "\",\"node\":" << ps.node
+                  << ",\"in\":" << ps.in << ",\"out\":" << ps.out << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
@@ -1188,7 +1215,9 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, x_nchw, y_out) : nullptr;
                     ys[m] = val_ptr(P, ms.out, x_nchw, y_out);
                 }
-                e = launch_conv_group(shp, n, s.cc, xs, ws, bs, rs, ys, st);
+                GroupPool gp;
+                const bool has_pool = group_pool(P, s, x_nchw, y_out, &gp);
+                e = launch_conv_group(shp, n, s.cc, xs, ws, bs, rs, ys, has_pool ? &gp : nullptr, st);
                 break;
             }
             case ST_MAXPOOL:
@@ -1266,10 +1295,20 @@ static int tune_plan(neo_plan* P) {
                 rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, xin, yout) : nullptr;
                 ys[m] = val_ptr(P, ms.out, xin, yout);
             }
-            float group_us = 0.f, alone_us = 0.f;
-            rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, P->cap_stream, &s.cc, &group_us);
-            // the fused launch stays only where it beats the members' own best
-            // launches one after another
+            GroupPool gp;
+            const bool has_pool = group_pool(P, s, xin, yout, &gp);
+            // candidates, each a launch list for this step's work:
+            //   fused:  the convs and the pool in one launch
+            //   split:  the convs in one launch, the pool alone (n > 1)
+            //   alone:  every conv and the pool in launches of their own
+            float fused_us = 0.f, split_us = 0.f, alone_us = 0.f, pool_us = 0.f;
+            ConvConfig fused_cc = s.cc, split_cc = s.cc;
+            rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, has_pool ? &gp : nullptr, P->cap_stream,
+                                 &fused_cc, &fused_us);
+            if (rc == NEO_OK && has_pool) rc = tune_pool(gp, P->cap_stream, &pool_us);
+            if (rc == NEO_OK && has_pool && n > 1)
+                rc = tune_conv_group(shp, n, xs, ws, bs, rs, ys, nullptr, P->cap_stream, &split_cc,
+                                     &split_us);
             ConvConfig own[kMaxGroupConvs];
             for (int m = 0; m < n && rc == NEO_OK; ++m) {
                 float us = 0.f;
@@ -1277,21 +1316,32 @@ static int tune_plan(neo_plan* P) {
                 alone_us += us;
             }
             if (rc != NEO_OK) break;
-            s.tuned = true;
-            if (group_us < alone_us) {
-                for (Step& m : s.members) {
-                    m.cc = s.cc;
-                    m.tuned = true;
-                }
-                next.push_back(s);
+            alone_us += pool_us;
+            split_us += pool_us;
+            const bool split_ok = has_pool && n > 1;
+            Step keep = s;
+            keep.tuned = true;
+            if (fused_us < alone_us && (!split_ok || fused_us <= split_us)) {
+                keep.cc = fused_cc;
+            } else if (split_ok && split_us < alone_us) {
+                next.push_back(s.pools[0]);
+                keep.pools.clear();
+                keep.cc = split_cc;
             } else {
+                if (has_pool) next.push_back(s.pools[0]);
                 for (int m = 0; m < n; ++m) {
                     Step ms = s.members[m];
                     ms.cc = own[m];
                     ms.tuned = true;
                     next.push_back(ms);
                 }
+                continue;
             }
+            for (Step& m : keep.members) {
+                m.cc = keep.cc;
+                m.tuned = true;
+            }
+            next.push_back(keep);
             continue;
         }
         if (s.kind == ST_CONV && !s.tuned) {

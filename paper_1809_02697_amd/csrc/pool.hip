@@ -5,90 +5,20 @@
 // Max pooling ignores taps outside the input (as if padded with -inf); average
 // pooling divides by the number of taps inside it.
 // Padded channel lanes hold 0 in the input and stay 0 in the output.
-#include "neo_internal.h"
+#include "pool_kernel.h"
 
 namespace neo {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-// Taps of a KR x KS window (0 = the window from the shape, a runtime loop).
-// With a compile-time window every tap's load is issued before any is used:
-// a tap outside the input loads pixel (0, 0) of the block and is discarded by
-// a select, so the loads of one output are in flight together.
-// lq = log2(x / 4): quads per pixel block.
+// One thread per output quad (pool_elem), grid-stride.
 template <bool MAX, int KR, int KS>
 __global__ __launch_bounds__(256) void pool_blk(const float* __restrict__ x, float* __restrict__ y,
                                                 PoolShape s, int CB, int lq) {
     const int total = (s.N * CB * s.OH * s.OW) << lq;
-    const int X = s.xb;
-    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
-        const int q = t & ((1 << lq) - 1);
-        int r_ = t >> lq;
-        const int ow = r_ % s.OW;
-        r_ /= s.OW;
-        const int oh = r_ % s.OH;
-        r_ /= s.OH;
-        const int cb = r_ % CB;
-        const int n = r_ / CB;
-        const float* xb = x + (n * CB + cb) * s.H * s.W * X + 4 * q;
-        const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
-        v4f acc;
-        if (MAX)
-            acc = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        else
-            acc = v4f{0.f, 0.f, 0.f, 0.f};
-        int cnt = 0;
-        if constexpr (KR > 0) {
-            v4f v[KR][KS];
-            bool ok[KR][KS];
-#pragma unroll
-            for (int r = 0; r < KR; ++r)
-#pragma unroll
-                for (int c = 0; c < KS; ++c) {
-                    const int ih = ih0 + r, iw = iw0 + c;
-                    ok[r][c] = (unsigned)ih < (unsigned)s.H && (unsigned)iw < (unsigned)s.W;
-                    v[r][c] = *reinterpret_cast<const v4f*>(xb + (ok[r][c] ? ih * s.W + iw : 0) * X);
-                }
-#pragma unroll
-            for (int r = 0; r < KR; ++r)
-#pragma unroll
-                for (int c = 0; c < KS; ++c) {
-                    if (!ok[r][c]) continue;
-                    if (MAX) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) acc[i] = v[r][c][i] > acc[i] ? v[r][c][i] : acc[i];
-                    } else {
-                        acc += v[r][c];
-                    }
-                    ++cnt;
-                }
-        } else {
-            for (int r = 0; r < s.R; ++r) {
-                const int ih = ih0 + r;
-                if ((unsigned)ih >= (unsigned)s.H) continue;
-                for (int c = 0; c < s.S; ++c) {
-                    const int iw = iw0 + c;
-                    if ((unsigned)iw >= (unsigned)s.W) continue;
-                    const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * X);
-                    if (MAX) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
-                    } else {
-                        acc += v;
-                    }
-                    ++cnt;
-                }
-            }
-        }
-        if (!MAX) {
-            const float d = (float)cnt;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
-        }
-        *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X +
-                                4 * q) = acc;
-    }
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x)
+        pool_detail::pool_elem<MAX, KR, KS>(x, y, s, CB, lq, t);
 }
 
 // One wave per (n, 16-channel group j) whatever the block x: lane = 4 *

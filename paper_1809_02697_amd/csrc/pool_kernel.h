@@ -1,0 +1,95 @@
+// Max and average pooling of one output quad on NCHW[x]c (Section 3.2: a
+// layout-tolerant operation), shared by the pooling kernel and by fused conv
+// launches that run a pooling step in their last workgroups, so both compute
+// the same bits.
+#pragma once
+
+#include <cmath>
+
+#include "neo_internal.h"
+
+namespace neo {
+namespace pool_detail {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Thread index t = (((n * CB + cb) * OH + oh) * OW + ow) * (x / 4) + quad, for
+// t < (N * CB * OH * OW) << lq (lq = log2(x / 4)).  Taps outside the input are
+// skipped (max: as if padded with -inf; average: divided by the taps inside).
+// With a compile-time KR x KS window every tap's load is issued before any is
+// used: a tap outside the input loads pixel (0, 0) of the block and is
+// discarded by a select, so the loads of one output are in flight together;
+// KR = 0 walks the window from the shape.  Both walk the taps row by row, so
+// the sums are the same.
+template <bool MAX, int KR, int KS>
+__device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __restrict__ y,
+                                          const PoolShape& s, int CB, int lq, int t) {
+    const int X = s.xb;
+    const int q = t & ((1 << lq) - 1);
+    int r_ = t >> lq;
+    const int ow = r_ % s.OW;
+    r_ /= s.OW;
+    const int oh = r_ % s.OH;
+    r_ /= s.OH;
+    const int cb = r_ % CB;
+    const int n = r_ / CB;
+    const float* xb = x + (n * CB + cb) * s.H * s.W * X + 4 * q;
+    const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
+    v4f acc;
+    if (MAX)
+        acc = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    else
+        acc = v4f{0.f, 0.f, 0.f, 0.f};
+    int cnt = 0;
+    if constexpr (KR > 0) {
+        v4f v[KR][KS];
+        bool ok[KR][KS];
+#pragma unroll
+        for (int r = 0; r < KR; ++r)
+#pragma unroll
+            for (int c = 0; c < KS; ++c) {
+                const int ih = ih0 + r, iw = iw0 + c;
+                ok[r][c] = (unsigned)ih < (unsigned)s.H && (unsigned)iw < (unsigned)s.W;
+                v[r][c] = *reinterpret_cast<const v4f*>(xb + (ok[r][c] ? ih * s.W + iw : 0) * X);
+            }
+#pragma unroll
+        for (int r = 0; r < KR; ++r)
+#pragma unroll
+            for (int c = 0; c < KS; ++c) {
+                if (!ok[r][c]) continue;
+                if (MAX) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] = v[r][c][i] > acc[i] ? v[r][c][i] : acc[i];
+                } else {
+                    acc += v[r][c];
+                }
+                ++cnt;
+            }
+    } else {
+        for (int r = 0; r < s.R; ++r) {
+            const int ih = ih0 + r;
+            if ((unsigned)ih >= (unsigned)s.H) continue;
+            for (int c = 0; c < s.S; ++c) {
+                const int iw = iw0 + c;
+                if ((unsigned)iw >= (unsigned)s.W) continue;
+                const v4f v = *reinterpret_cast<const v4f*>(xb + (ih * s.W + iw) * X);
+                if (MAX) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
+                } else {
+                    acc += v;
+                }
+                ++cnt;
+            }
+        }
+    }
+    if (!MAX) {
+        const float d = (float)cnt;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
+    }
+    *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X + 4 * q) = acc;
+}
+
+}  // namespace pool_detail
+}  // namespace neo

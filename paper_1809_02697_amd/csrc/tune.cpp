@@ -84,11 +84,71 @@ bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out) {
     return true;
 }
 
-// Time every candidate on `st` (a stream that is not the legacy null stream)
-// with the caller's buffers: each candidate's launches are captured into a
-// graph of `reps` launches and replayed between two events.  Keeps the
-// fastest in the database and returns it with its time per launch (us_out may
-// be null).
+namespace {
+
+// Time per launch of `launch` on `st` (a stream that is not the legacy null
+// stream): one warm-up launch (it also surfaces a launch error before
+// capture), then `reps` launches captured into a graph, replayed three times
+// between two events; the fastest replay counts.
+template <typename F>
+hipError_t time_launch(F launch, hipStream_t st, hipEvent_t e0, hipEvent_t e1, float* us) {
+    const int reps = 10;
+    hipError_t e = launch();
+    if (e != hipSuccess) return e;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+    for (int i = 0; i < reps && e == hipSuccess; ++i) e = launch();
+    hipError_t e2 = hipStreamEndCapture(st, &g);
+    if (e == hipSuccess) e = e2;
+    if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    if (g) (void)hipGraphDestroy(g);
+    float ms = 1e30f;
+    for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+        e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e0, st);
+        if (e == hipSuccess) e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e1, st);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e == hipSuccess) ms = std::min(ms, t);
+    }
+    if (ge) (void)hipGraphExecDestroy(ge);
+    *us = ms * 1000.f / reps;
+    return e;
+}
+
+struct Events {
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    Events() {
+        (void)hipEventCreate(&e0);
+        (void)hipEventCreate(&e1);
+    }
+    ~Events() {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+    }
+};
+
+// one launch of several convs (and a pooling step): architecture and the
+// members' shapes -> config; a pooling step alone: architecture and shape -> time
+using GroupKey = std::pair<std::string, std::vector<int>>;
+std::map<GroupKey, Entry> g_group_db;
+std::map<GroupKey, float> g_pool_db;
+constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
+constexpr int kPoolShapeInts = 12;   // max N C H W R S sh sw ph pw xb
+
+std::vector<int> pool_ints(const GroupPool& p) {
+    const PoolShape& s = p.s;
+    return {p.max ? 1 : 0, s.N, s.C, s.H, s.W, s.R, s.S, s.sh, s.sw, s.ph, s.pw, s.xb};
+}
+
+}  // namespace
+
+// Time every candidate with the caller's buffers on `st`.  Keeps the fastest
+// in the database and returns it with its time per launch (us_out may be
+// null).
 int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
               const float* res, float* y, hipStream_t st, ConvConfig* best_out, float* us_out) {
     const std::string arch = device_arch();
@@ -108,56 +168,24 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
     hipError_t e = hipSuccess;
     if (ws_bytes) e = hipMalloc(&ws, ws_bytes);
     if (e != hipSuccess) return fail(NEO_ERR_OOM, "tuning workspace allocation");
-    hipEvent_t e0, e1;
-    (void)hipEventCreate(&e0);
-    (void)hipEventCreate(&e1);
-    const int reps = 10;
     ConvConfig best = choose_conv_config(s);
     float best_us = 1e30f;
-    int rc = NEO_OK;
-    for (const ConvConfig& c : cands) {
-        // warm-up launch (also surfaces a launch error before capture)
-        e = launch_conv2d(s, c, x, w, wmfma, bias, res, y, ws, st);
-        if (e != hipSuccess) {
-            rc = hip_fail(e, "tuning launch");
-            break;
+    {
+        Events ev;
+        for (const ConvConfig& c : cands) {
+            float us = 0.f;
+            e = time_launch([&] { return launch_conv2d(s, c, x, w, wmfma, bias, res, y, ws, st); }, st,
+                            ev.e0, ev.e1, &us);
+            if (e != hipSuccess) break;
+            if (us < best_us) {
+                best_us = us;
+                best = c;
+            }
         }
-        hipGraph_t g = nullptr;
-        hipGraphExec_t ge = nullptr;
-        e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
-        for (int i = 0; i < reps && e == hipSuccess; ++i)
-            e = launch_conv2d(s, c, x, w, wmfma, bias, res, y, ws, st);
-        hipError_t e2 = hipStreamEndCapture(st, &g);
-        if (e == hipSuccess) e = e2;
-        if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
-        if (g) (void)hipGraphDestroy(g);
-        float ms = 1e30f;
-        for (int r = 0; r < 3 && e == hipSuccess; ++r) {
-            e = hipGraphLaunch(ge, st);
-            if (e == hipSuccess) e = hipEventRecord(e0, st);
-            if (e == hipSuccess) e = hipGraphLaunch(ge, st);
-            if (e == hipSuccess) e = hipEventRecord(e1, st);
-            if (e == hipSuccess) e = hipEventSynchronize(e1);
-            float t = 0.f;
-            if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
-            if (e == hipSuccess) ms = std::min(ms, t);
-        }
-        if (ge) (void)hipGraphExecDestroy(ge);
-        if (e != hipSuccess) {
-            rc = hip_fail(e, "tuning timing");
-            break;
-        }
-        const float us = ms * 1000.f / reps;
-        if (us < best_us) {
-            best_us = us;
-            best = c;
-        }
+        (void)hipStreamSynchronize(st);
     }
-    (void)hipStreamSynchronize(st);
-    (void)hipEventDestroy(e0);
-    (void)hipEventDestroy(e1);
     if (ws) (void)hipFree(ws);
-    if (rc != NEO_OK) return rc;
+    if (e != hipSuccess) return hip_fail(e, "tuning");
     {
         std::lock_guard<std::mutex> lk(g_mu);
         g_db[key_of(s, wmfma, arch)] = Entry{best, best_us};
@@ -167,20 +195,17 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
     return NEO_OK;
 }
 
-namespace {
-// one launch of several convs: architecture and the members' shapes -> config
-using GroupKey = std::pair<std::string, std::vector<int>>;
-std::map<GroupKey, Entry> g_group_db;
-constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
-}
-
 int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,
                     const float* const* bias, const float* const* res, float* const* y,
-                    hipStream_t st, ConvConfig* best_out, float* us_out) {
+                    const GroupPool* pool, hipStream_t st, ConvConfig* best_out, float* us_out) {
     GroupKey key{device_arch(), {}};
     for (int i = 0; i < n; ++i)
         key.second.insert(key.second.end(), {s[i].N, s[i].C, s[i].H, s[i].W, s[i].K, s[i].R, s[i].S,
                                              s[i].sh, s[i].sw, s[i].ph, s[i].pw});
+    if (pool) {
+        const std::vector<int> pi = pool_ints(*pool);
+        key.second.insert(key.second.end(), pi.begin(), pi.end());
+    }
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_group_db.find(key);
@@ -190,50 +215,26 @@ int tune_conv_group(const ConvShape* s, int n, const float* const* x, const floa
             return NEO_OK;
         }
     }
-    hipEvent_t e0, e1;
-    (void)hipEventCreate(&e0);
-    (void)hipEventCreate(&e1);
-    const int reps = 10;
     ConvConfig best = choose_group_config(s, n);
     float best_us = 1e30f;
     hipError_t e = hipSuccess;
-    for (int fk : {1, 2, 4})
-        for (int fp : {1, 2, 4})
-            for (int wv : {1, 2, 4, 8, 16}) {
-                const ConvConfig c{fk, fp, 1, wv};
-                if (e != hipSuccess || !conv_group_config_valid(s, n, c)) continue;
-                e = launch_conv_group(s, n, c, x, w, bias, res, y, st);  // warm-up
-                if (e != hipSuccess) break;
-                hipGraph_t g = nullptr;
-                hipGraphExec_t ge = nullptr;
-                e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
-                for (int i = 0; i < reps && e == hipSuccess; ++i)
-                    e = launch_conv_group(s, n, c, x, w, bias, res, y, st);
-                hipError_t e2 = hipStreamEndCapture(st, &g);
-                if (e == hipSuccess) e = e2;
-                if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
-                if (g) (void)hipGraphDestroy(g);
-                float ms = 1e30f;
-                for (int r = 0; r < 3 && e == hipSuccess; ++r) {
-                    e = hipGraphLaunch(ge, st);
-                    if (e == hipSuccess) e = hipEventRecord(e0, st);
-                    if (e == hipSuccess) e = hipGraphLaunch(ge, st);
-                    if (e == hipSuccess) e = hipEventRecord(e1, st);
-                    if (e == hipSuccess) e = hipEventSynchronize(e1);
-                    float t = 0.f;
-                    if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
-                    if (e == hipSuccess) ms = std::min(ms, t);
+    {
+        Events ev;
+        for (int fk : {1, 2, 4})
+            for (int fp : {1, 2, 4})
+                for (int wv : {1, 2, 4, 8, 16}) {
+                    const ConvConfig c{fk, fp, 1, wv};
+                    if (e != hipSuccess || !conv_group_config_valid(s, n, c)) continue;
+                    float us = 0.f;
+                    e = time_launch([&] { return launch_conv_group(s, n, c, x, w, bias, res, y, pool, st); },
+                                    st, ev.e0, ev.e1, &us);
+                    if (e == hipSuccess && us < best_us) {
+                        best_us = us;
+                        best = c;
+                    }
                 }
-                if (ge) (void)hipGraphExecDestroy(ge);
-                const float us = ms * 1000.f / reps;
-                if (e == hipSuccess && us < best_us) {
-                    best_us = us;
-                    best = c;
-                }
-            }
-    (void)hipStreamSynchronize(st);
-    (void)hipEventDestroy(e0);
-    (void)hipEventDestroy(e1);
+        (void)hipStreamSynchronize(st);
+    }
     if (e != hipSuccess) return hip_fail(e, "group tuning");
     {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -241,6 +242,33 @@ int tune_conv_group(const ConvShape* s, int n, const float* const* x, const floa
     }
     *best_out = best;
     if (us_out) *us_out = best_us;
+    return NEO_OK;
+}
+
+int tune_pool(const GroupPool& p, hipStream_t st, float* us_out) {
+    const GroupKey key{device_arch(), pool_ints(p)};
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_pool_db.find(key);
+        if (it != g_pool_db.end()) {
+            *us_out = it->second;
+            return NEO_OK;
+        }
+    }
+    float us = 0.f;
+    hipError_t e;
+    {
+        Events ev;
+        e = time_launch([&] { return p.max ? launch_maxpool(p.s, p.x, p.y, st) : launch_avgpool(p.s, p.x, p.y, st); },
+                        st, ev.e0, ev.e1, &us);
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "pool timing");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_pool_db[key] = us;
+    }
+    *us_out = us;
     return NEO_OK;
 }
 
@@ -252,8 +280,11 @@ extern "C" {
 
 // Text format, one workload per line:
 //   arch N C H W K R S sh sw ph pw wmfma xb yb fk fp split waves us
-// and one line per fused launch of n NCHW16c convs:
-//   group arch n (N C H W K R S sh sw ph pw) x n fk fp split waves us
+// one line per fused launch of n NCHW16c convs and m (0 or 1) pooling steps:
+//   group arch n m (N C H W K R S sh sw ph pw) x n (max N C H W R S sh sw ph pw xb) x m
+//         fk fp split waves us
+// and one line per pooling step timed alone:
+//   pool arch max N C H W R S sh sw ph pw xb us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -271,12 +302,20 @@ int neo_tune_db_save(const char* path) {
     for (const auto& kv : g_group_db) {
         const std::vector<int>& k = kv.first.second;
         const Entry& v = kv.second;
-        f << "group " << kv.first.first << ' ' << k.size() / kGroupShapeInts;
+        // 11 n + 12 m ints with n <= 4, m <= 1: m is the remainder's sign
+        const size_t m = k.size() % kGroupShapeInts ? 1 : 0;
+        f << "group " << kv.first.first << ' ' << (k.size() - m * kPoolShapeInts) / kGroupShapeInts
+          << ' ' << m;
         for (int x : k) f << ' ' << x;
         f << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split << ' ' << v.cfg.waves << ' '
           << v.us << '\n';
     }
-    return f ? (int)(g_db.size() + g_group_db.size())
+    for (const auto& kv : g_pool_db) {
+        f << "pool " << kv.first.first;
+        for (int x : kv.first.second) f << ' ' << x;
+        f << ' ' << kv.second << '\n';
+    }
+    return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -288,6 +327,16 @@ int neo_tune_db_load(const char* path) {
     int n = 0, lineno = 0;
     std::map<Key, Entry> add;
     std::map<GroupKey, Entry> add_group;
+    std::map<GroupKey, float> add_pool;
+    auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
+        for (int i = 0; i < count; ++i) {
+            int x = 0;
+            if (!(is >> x)) return false;
+            out.push_back(x);
+        }
+        return true;
+    };
+    const std::string bad = "neo_tune_db_load: malformed line ";
     while (std::getline(f, line)) {
         ++lineno;
         if (line.empty() || line[0] == '#') continue;
@@ -297,20 +346,25 @@ int neo_tune_db_load(const char* path) {
         if (line.compare(0, 6, "group ") == 0) {
             std::string tag;
             GroupKey gk;
-            int members = 0;
-            bool ok = (bool)(is >> tag >> gk.first >> members) && members >= 1 &&
-                      members <= kMaxGroupConvs;
-            for (int i = 0; ok && i < members * kGroupShapeInts; ++i) {
-                int x = 0;
-                ok = (bool)(is >> x);
-                gk.second.push_back(x);
-            }
+            int members = 0, pools = -1;
+            bool ok = (bool)(is >> tag >> gk.first >> members >> pools) && members >= 1 &&
+                      members <= kMaxGroupConvs && (pools == 0 || pools == 1);
+            ok = ok && read_ints(is, members * kGroupShapeInts + pools * kPoolShapeInts, gk.second);
             ok = ok && (is >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >> v.us) &&
                  v.cfg.split == 1 && conv_config_valid(v.cfg);
-            if (!ok)
-                return fail(NEO_ERR_INVALID_ARG,
-                            "neo_tune_db_load: malformed line " + std::to_string(lineno));
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
             add_group[gk] = v;
+            ++n;
+            continue;
+        }
+        if (line.compare(0, 5, "pool ") == 0) {
+            std::string tag;
+            GroupKey pk;
+            float us = 0.f;
+            bool ok = (bool)(is >> tag >> pk.first) && read_ints(is, kPoolShapeInts, pk.second) &&
+                      (bool)(is >> us) && pow2_block(pk.second.back());
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_pool[pk] = us;
             ++n;
             continue;
         }
@@ -326,6 +380,7 @@ int neo_tune_db_load(const char* path) {
     std::lock_guard<std::mutex> lk(g_mu);
     for (const auto& kv : add) g_db[kv.first] = kv.second;
     for (const auto& kv : add_group) g_group_db[kv.first] = kv.second;
+    for (const auto& kv : add_pool) g_pool_db[kv.first] = kv.second;
     return n;
 }
 
@@ -333,11 +388,12 @@ void neo_tune_db_clear(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     g_db.clear();
     g_group_db.clear();
+    g_pool_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
-    return (int)(g_db.size() + g_group_db.size());
+    return (int)(g_db.size() + g_group_db.size() + g_pool_db.size());
 }
 
 }  // extern "C"

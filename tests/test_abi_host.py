@@ -264,24 +264,33 @@ def test_tune_db_roundtrip_and_errors(tmp_path):
 
 
 def test_tune_db_group_entries(tmp_path):
-    """Fused launches are stored with their members' shapes, so a later
-    process rebuilds the same plan from the file."""
+    """Fused launches are stored with their members' shapes (and their
+    pooling step's), pooling steps with their time alone, so a later process
+    rebuilds the same plan from the file."""
     neo.tune_db_clear()
     p = tmp_path / "db.txt"
-    grp = ("group gfx950 2 1 192 35 35 64 1 1 1 1 0 0 1 48 35 35 64 5 5 1 1 2 2 "
+    grp = ("group gfx950 2 0 1 192 35 35 64 1 1 1 1 0 0 1 48 35 35 64 5 5 1 1 2 2 "
            "2 1 1 4 6.25")
-    p.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 2 2 1 4 7.5\n" + grp + "\n")
-    assert neo.tune_db_load(p) == 2
-    assert neo.tune_db_size() == 2
+    grp_pool = ("group gfx950 1 1 1 192 35 35 64 1 1 1 1 0 0 0 1 192 35 35 3 3 1 1 1 1 16 "
+                "1 1 1 2 5.5")
+    pool = "pool gfx950 0 1 192 35 35 3 3 1 1 1 1 16 3.125"
+    p.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 2 2 1 4 7.5\n" + grp + "\n" + grp_pool +
+                 "\n" + pool + "\n")
+    assert neo.tune_db_load(p) == 4
+    assert neo.tune_db_size() == 4
     q = tmp_path / "out.txt"
-    assert neo.tune_db_save(q) == 2
-    out = [l for l in q.read_text().splitlines() if l.startswith("group ")]
-    assert len(out) == 1 and out[0].split()[:27] == grp.split()[:27]
-    assert float(out[0].split()[-1]) == 6.25
+    assert neo.tune_db_save(q) == 4
+    lines = q.read_text().splitlines()
+    for want in (grp, grp_pool, pool):
+        got = [l for l in lines if l.split()[:-1] == want.split()[:-1]]
+        assert len(got) == 1 and float(got[0].split()[-1]) == float(want.split()[-1])
     bad = tmp_path / "bad.txt"
     for line in (grp.replace(" 2 1 1 4 6.25", " 2 1 2 4 6.25"),      # a group never splits
-                 grp.replace("gfx950 2 ", "gfx950 5 "),                # more than 4 members
-                 grp.rsplit(" ", 3)[0]):                              # truncated
+                 grp.replace("gfx950 2 0 ", "gfx950 5 0 "),            # more than 4 members
+                 grp.replace("gfx950 2 0 ", "gfx950 2 2 "),            # at most one pool
+                 grp.rsplit(" ", 3)[0],                               # truncated
+                 pool.replace(" 16 3.125", " 12 3.125"),              # no 12-channel block
+                 pool.rsplit(" ", 2)[0]):                             # truncated
         bad.write_text(line + "\n")
         with pytest.raises(neo.NeoError):
             neo.tune_db_load(bad)

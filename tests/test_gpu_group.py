@@ -105,20 +105,24 @@ def test_tuned_grouped_resnet50_graph_replay(neo):
 
 
 def _db_times(path):
-    """{conv shape: us} and {tuple of member shapes: us} from a saved results
-    file (shape = N C H W K R S sh sw ph pw)."""
-    convs, groups = {}, {}
+    """From a saved results file: {conv shape: us} (NCHW16c convs), {(member
+    shapes, pool shape or None): us} and {pool shape: us}; conv shape = N C H
+    W K R S sh sw ph pw, pool shape = max N C H W R S sh sw ph pw xb."""
+    convs, groups, pools = {}, {}, {}
     for line in open(path).read().splitlines():
         f = line.split()
         if not f or f[0].startswith("#"):
             continue
         if f[0] == "group":
-            n = int(f[2])
-            ints = tuple(int(v) for v in f[3:3 + 11 * n])
-            groups[tuple(ints[11 * i:11 * i + 11] for i in range(n))] = float(f[-1])
+            n, m = int(f[2]), int(f[3])
+            ints = [int(v) for v in f[4:4 + 11 * n + 12 * m]]
+            mem = tuple(tuple(ints[11 * i:11 * i + 11]) for i in range(n))
+            groups[(mem, tuple(ints[11 * n:]) if m else None)] = float(f[-1])
+        elif f[0] == "pool":
+            pools[tuple(int(v) for v in f[2:14])] = float(f[-1])
         elif f[13:15] == ["16", "16"] and f[12] == "1":
             convs[tuple(int(v) for v in f[1:12])] = float(f[-1])
-    return convs, groups
+    return convs, groups, pools
 
 
 def _shape(c):
@@ -126,36 +130,146 @@ def _shape(c):
             c["pad"][0], c["pad"][1])
 
 
-def test_tuned_inception_keeps_only_faster_groups(neo, tmp_path):
-    """With NEO_PLAN_TUNE a fused launch stays only where its measured time
-    is below the sum of its members' own best times; the tuned plan matches
-    the oracle, and a plan rebuilt from the saved results file in a clean
+def _pool_shape(g, d, p):
+    n = g.nodes[p["node"]]
+    v = d["values"][p["in"]]
+    N, C, H, W = v["shape"]
+    return (1 if p["kind"] == "maxpool" else 0, N, C, H, W, n.R, n.S, n.stride[0], n.stride[1],
+            n.pad[0], n.pad[1], int(v["layout"][4:-1]))
+
+
+def _expected_launches(g, d0, convs, groups, pools):
+    """The launch list the keep-or-split rule makes of the untuned plan d0:
+    a fused launch (convs and pool) stays when it beats the members' and the
+    pool's own launches and, with more than one conv, the convs fused with
+    the pool alone; otherwise the cheaper of the two."""
+    out = []
+    for s in d0["steps"]:
+        if s["kind"] != "conv_group":
+            out.append((s["kind"], s["node"]))
+            continue
+        mem = tuple(_shape(m["conv"]) for m in s["members"])
+        pool = _pool_shape(g, d0, s["pool"]) if "pool" in s else None
+        pool_us = pools[pool] if pool else 0.0
+        alone = sum(convs[k] for k in mem) + pool_us
+        fused = groups[(mem, pool)]
+        split = groups[(mem, None)] + pool_us if pool and len(mem) > 1 else None
+        nodes = tuple(m["node"] for m in s["members"])
+        if fused < alone and (split is None or fused <= split):
+            out.append(("conv_group", nodes, s["pool"]["node"] if pool else None))
+        elif split is not None and split < alone:
+            out += [(s["pool"]["kind"], s["pool"]["node"]), ("conv_group", nodes, None)]
+        else:
+            out += ([(s["pool"]["kind"], s["pool"]["node"])] if pool else []) + \
+                   [("conv", m["node"]) for m in s["members"]]
+    return out
+
+
+def _launches(d):
+    return [("conv_group", tuple(m["node"] for m in s["members"]),
+             s["pool"]["node"] if "pool" in s else None) if s["kind"] == "conv_group"
+            else (s["kind"], s["node"]) for s in d["steps"]]
+
+
+def test_tuned_inception_keeps_only_faster_launches(neo, tmp_path):
+    """With NEO_PLAN_TUNE every fused launch (convs, and a pooling step
+    riding along) is kept, split from its pool, or split into single
+    launches by the measured times in the results database; the tuned plan
+    matches the oracle, and a plan rebuilt from the saved file in a clean
     database is the same launch list."""
     neo.tune_db_clear()
     g = wl.inception_v3(1)
     ref = orc.run_graph(g)
+    p0 = neo.Plan(g, flags=neo.PLAN_GROUP)
+    d0 = p0.describe()
+    p0.destroy()
     y, d = _run(neo, g, neo.PLAN_GROUP | neo.PLAN_TUNE)
     assert_close_network(y.reshape(ref.shape), ref, "tuned grouped inception")
     path = tmp_path / "db.txt"
     neo.tune_db_save(path)
-    convs, groups = _db_times(path)
-    kept = set()
-    for s in d["steps"]:
-        if s["kind"] != "conv_group":
-            continue
-        key = tuple(_shape(m["conv"]) for m in s["members"])
-        kept.add(key)
-        assert groups[key] < sum(convs[k] for k in key)
-    for key, us in groups.items():
-        if key not in kept:
-            assert us >= sum(convs[k] for k in key)
-    print(f"\n{len(kept)} of {len(groups)} tuned groups kept")
+    convs, groups, pools = _db_times(path)
+    assert _launches(d) == _expected_launches(g, d0, convs, groups, pools)
+    kept = sum(1 for s in d["steps"] if s["kind"] == "conv_group")
+    print(f"\n{kept} fused launches kept, {sum(1 for s in d['steps'] if 'pool' in s)} with a pool")
     neo.tune_db_clear()
     neo.tune_db_load(path)
     _, d2 = _run(neo, g, neo.PLAN_GROUP | neo.PLAN_TUNE)
-    strip = lambda d: [(s["kind"], s["node"], s.get("tile"), s.get("waves"),
+    strip = lambda d: [(s["kind"], s["node"], s.get("tile"), s.get("waves"), s.get("pool", {}).get("node"),
                         s.get("conv", {}).get("tile")) for s in d["steps"]]
     assert strip(d2) == strip(d)
+
+
+def pool_graph(seed=13, N=2):
+    """Pooling steps that share a round with convs: a 3x3/s1/p1 average pool
+    next to two branch heads (3x3 convs over 256 channels, so every wave
+    count up to 16 is a valid configuration for them), a 2x2/s2 max pool (the generic window path)
+    next to two convs of different inputs, and a 3x3/s2 average pool over a
+    ragged channel count (40) next to two more; a second pool in the first
+    round (a 3x3/s2 max pool writing into a concatenation) runs alone."""
+    b = wl._Builder("pools", (N, 24, 15, 13), np.random.Generator(np.random.PCG64(seed)))
+    x = b.conv(0, 256, 3, pad=1, name="stem")
+    a1 = b.conv(x, 32, 3, stride=2, name="a1")
+    a2 = b.conv(x, 16, 3, pad=1, name="a2")
+    ap = b.pool("avgpool", x, 3, 1, pad=1, name="ap")
+    mp = b.pool("maxpool", x, 3, 2, name="mp")
+    a3 = b.conv(a2, 32, 3, stride=2, name="a3")
+    ap2 = b.conv(ap, 32, 1, name="ap2")
+    m2 = b.pool("maxpool", ap2, 2, 2, name="m2")
+    c1 = b.conv(ap2, 40, 3, pad=1, name="c1")
+    cat = b.concat([a1, mp, a3], name="cat")
+    z = b.conv(cat, 16, 1, name="z")
+    q = b.pool("avgpool", c1, 3, 2, name="q")
+    c2 = b.conv(c1, 16, 1, name="c2")
+    c3 = b.conv(c1, 16, 3, stride=2, name="c3")
+    s = b.concat([b.gap(z), b.gap(m2), b.gap(q), b.gap(c2), b.gap(c3)], name="cat2")
+    s = b.flatten(s, 16 + 32 + 40 + 16 + 16)
+    b.output(b.dense(s, 10, name="fc"))
+    return b.finish(lambda rng: rng.normal(0, 1, (N, 24, 15, 13)).astype(np.float32))
+
+
+@pytest.mark.parametrize("cfg", [(1, 1, 1), (1, 1, 2), (1, 2, 4), (1, 1, 16), (2, 1, 2)],
+                         ids=lambda c: "fk%dfp%dw%d" % c)
+def test_pools_ride_bit_identical(neo, cfg, monkeypatch):
+    """A pooling step run by a fused conv launch gives the same bits as in a
+    launch of its own, for workgroups of 64 to 1024 threads."""
+    monkeypatch.setenv("NEO_GROUP_CONFIG", "%d,%d,%d" % cfg)
+    g = pool_graph()
+    ref = orc.run_graph(g)
+    y, d = _run(neo, g, neo.PLAN_GROUP)
+    assert sum(1 for s in d["steps"] if "pool" in s) == 3
+    assert_close(y.reshape(ref.shape), ref, f"pools ride {cfg}")
+    monkeypatch.setenv("NEO_GROUP_POOLS", "0")
+    y0, d0 = _run(neo, g, neo.PLAN_GROUP)
+    assert not any("pool" in s for s in d0["steps"])
+    np.testing.assert_array_equal(y, y0)
+
+
+def test_pool_rides_with_a_lone_conv(neo):
+    """A round of one conv and one pooling step becomes a one-conv fused
+    launch carrying the pool."""
+    b = wl._Builder("lone", (1, 32, 11, 9), np.random.Generator(np.random.PCG64(17)))
+    x = b.conv(0, 48, 3, pad=1, name="stem")
+    a = b.conv(x, 24, 3, stride=2, name="a")
+    m = b.pool("maxpool", x, 3, 2, name="m")
+    s = b.concat([b.gap(a), b.gap(m)], name="cat")
+    s = b.flatten(s, 24 + 48)
+    b.output(b.dense(s, 10, name="fc"))
+    g = b.finish(lambda rng: rng.normal(0, 1, (1, 32, 11, 9)).astype(np.float32))
+    ref = orc.run_graph(g)
+    y, d = _run(neo, g, neo.PLAN_GROUP)
+    grp = [s for s in d["steps"] if s["kind"] == "conv_group"]
+    assert len(grp) == 1 and len(grp[0]["members"]) == 1 and "pool" in grp[0]
+    assert_close(y.reshape(ref.shape), ref, "lone conv with pool")
+
+
+@pytest.mark.parametrize("builder", [wl.tiny_graph, lambda: wl.inception_v3(1)])
+def test_pools_ride_network_bit_identical(neo, builder, monkeypatch):
+    g = builder()
+    y, d = _run(neo, g, neo.PLAN_GROUP)
+    assert any("pool" in s for s in d["steps"])
+    monkeypatch.setenv("NEO_GROUP_POOLS", "0")
+    y0, _ = _run(neo, g, neo.PLAN_GROUP)
+    np.testing.assert_array_equal(y, y0)
 
 
 def test_concat_residual_group_matches_oracle(neo):

@@ -19,28 +19,35 @@ def _plan(g, flags=0):
 
 
 def _launch_items(d):
-    """(step index, reads, writes) per launched conv or other step."""
+    """(step index, reads, writes) per launched conv, pooling or other step."""
     for i, s in enumerate(d["steps"]):
         if s["kind"] == "conv_group":
             for m in s["members"]:
                 yield i, [m["in"]] + ([m["res"]] if m["res"] >= 0 else []), m["out"], m
+            if "pool" in s:
+                yield i, [s["pool"]["in"]], s["pool"]["out"], s["pool"]
         else:
             yield i, [s["in"]] + ([s["res"]] if s["res"] >= 0 else []), s["out"], s
 
 
-@pytest.mark.parametrize("build,groups,sizes", [
-    (lambda: nets.resnet50(), 4, [2, 2, 2, 2]),
+@pytest.mark.parametrize("build,groups,sizes,pools", [
+    (lambda: nets.resnet50(), 4, [2, 2, 2, 2], 0),
     (lambda: nets.inception_v3(), 27, [3, 3, 3, 3, 3, 3, 2, 3, 3, 2, 3, 3, 2, 3, 3, 2, 3, 3, 2, 2, 2,
-                                       3, 4, 2, 3, 4, 2]),
-    (wl.tiny_graph, 2, [2, 2]),
-    (lambda: nets.vgg16(), 0, [])])
-def test_group_structure(build, groups, sizes):
+                                       3, 4, 2, 3, 4, 2], 11),
+    (wl.tiny_graph, 2, [2, 2], 1),
+    (lambda: nets.vgg16(), 0, [], 0)])
+def test_group_structure(build, groups, sizes, pools):
     g = build()
     d = _plan(g)
     grp = [s for s in d["steps"] if s["kind"] == "conv_group"]
     assert len(grp) == groups
     if sizes is not None:
         assert [len(s["members"]) for s in grp] == sizes
+    assert sum(1 for s in grp if "pool" in s) == pools
+    # every pooling node runs exactly once, alone or in a conv launch
+    pooled = sorted([s["pool"]["node"] for s in grp if "pool" in s] +
+                    [s["node"] for s in d["steps"] if s["kind"] in ("maxpool", "avgpool")])
+    assert pooled == sorted(i for i, n in enumerate(g.nodes) if n.op in ("maxpool", "avgpool"))
     conv_nodes = sorted(i for i, n in enumerate(g.nodes) if n.op == "conv")
     launched = sorted(m["node"] for s in d["steps"] if s["kind"] in ("conv", "conv_group")
                       for m in (s["members"] if s["kind"] == "conv_group" else [s]))
@@ -89,30 +96,52 @@ def test_grouped_launch_list_is_a_valid_order(build):
 
 
 def _names(g, d):
-    return [[g.nodes[m["node"]].name for m in s["members"]] if s["kind"] == "conv_group"
-            else g.nodes[s["node"]].name for s in d["steps"]]
+    """Per launch: the node name of a single step, or the names of a fused
+    launch's convs followed by its pooling step's."""
+    return [[g.nodes[m["node"]].name for m in s["members"]] +
+            ([g.nodes[s["pool"]["node"]].name] if "pool" in s else [])
+            if s["kind"] == "conv_group" else g.nodes[s["node"]].name for s in d["steps"]]
+
+
+def _first(names, name):
+    return next(i for i, n in enumerate(names) if n == name or (isinstance(n, list) and name in n))
 
 
 def test_parallel_branches_share_launches():
     """Inception's first module: the three 1x1 convs that read the module's
-    input form round one; the second convs of two branches and the pooling
+    input, and the module's average pool, form round one (the pool runs in
+    the convs' launch); the second convs of two branches and the pooling
     branch's 1x1 (three different inputs) form round two; the last conv of
-    the double-3x3 branch runs alone.  The module's average pool is ready
-    with round one and is launched before it."""
+    the double-3x3 branch runs alone."""
     g = nets.inception_v3()
     names = _names(g, _plan(g))
-    i = names.index("Mixed_5b.avgpool")
-    assert names[i + 1:i + 4] == [
-        ["Mixed_5b.branch1x1", "Mixed_5b.branch5x5_1", "Mixed_5b.branch3x3dbl_1"],
+    i = _first(names, "Mixed_5b.branch1x1")
+    assert names[i:i + 3] == [
+        ["Mixed_5b.branch1x1", "Mixed_5b.branch5x5_1", "Mixed_5b.branch3x3dbl_1", "Mixed_5b.avgpool"],
         ["Mixed_5b.branch5x5_2", "Mixed_5b.branch3x3dbl_2", "Mixed_5b.branch_pool"],
         "Mixed_5b.branch3x3dbl_3"]
-    # a 7x7-factorised module: five rounds of convs instead of ten launches
-    i = names.index("Mixed_6b.avgpool")
-    assert names[i + 1:i + 6] == [
-        ["Mixed_6b.branch1x1", "Mixed_6b.branch7x7_1", "Mixed_6b.branch7x7dbl_1"],
+    # a 7x7-factorised module: five launches instead of eleven
+    i = _first(names, "Mixed_6b.branch1x1")
+    assert names[i:i + 5] == [
+        ["Mixed_6b.branch1x1", "Mixed_6b.branch7x7_1", "Mixed_6b.branch7x7dbl_1", "Mixed_6b.avgpool"],
         ["Mixed_6b.branch7x7_2", "Mixed_6b.branch7x7dbl_2", "Mixed_6b.branch_pool"],
         ["Mixed_6b.branch7x7_3", "Mixed_6b.branch7x7dbl_3"],
         "Mixed_6b.branch7x7dbl_4", "Mixed_6b.branch7x7dbl_5"]
+    # a reduction module: the max pool rides with the two branch heads
+    i = _first(names, "Mixed_6a.branch3x3")
+    assert names[i] == ["Mixed_6a.branch3x3", "Mixed_6a.branch3x3dbl_1", "Mixed_6a.maxpool"]
+
+
+def test_pools_alone_when_asked(monkeypatch):
+    """NEO_GROUP_POOLS=0 keeps every pooling step in a launch of its own,
+    ahead of its round's conv launches."""
+    monkeypatch.setenv("NEO_GROUP_POOLS", "0")
+    g = nets.inception_v3()
+    d = _plan(g)
+    assert not any("pool" in s for s in d["steps"] if s["kind"] == "conv_group")
+    names = _names(g, d)
+    i = names.index("Mixed_5b.avgpool")
+    assert names[i + 1] == ["Mixed_5b.branch1x1", "Mixed_5b.branch5x5_1", "Mixed_5b.branch3x3dbl_1"]
 
 
 def test_ungrouped_plan_keeps_node_order():
