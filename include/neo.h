@@ -109,7 +109,8 @@ int neo_conv2d_blocked(const float* x, int N, int C, int H, int W, const float* 
  *   w_packed, bias as for neo_conv2d_blocked (the filter is always
  *            KCRS[16]c[16]k: its block size is the kernel's MFMA tile, not a
  *            property of the feature maps).
- * x_block: 16, 32 or 64; when C <= 4 also 4 or 8.  y_block: 16, 32 or 64.
+ * x_block: 16, 32 or 64; when C <= 4 also 1 (NCHW1c, which is plain NCHW:
+ * x is [N][C][H][W]), 4, 8.  y_block: 16, 32 or 64.
  * Other blocks return NEO_ERR_UNSUPPORTED.  The arithmetic does not depend on
  * the blocks: with the same launch configuration (the default cost model does
  * not look at the blocks) results are bit-identical to neo_conv2d_blocked's.
@@ -227,7 +228,9 @@ typedef struct neo_node {
     /* conv: the scheme's split factors (Section 3.3.1's ic_bn, oc_bn), i.e. the
      * blocks of its input and output layouts; 0 and 0 = the plan's choice (the
      * plan's block, or the global search's).  Both 0 or both set; see
-     * neo_conv2d_nchwxc for the blocks allowed. */
+     * neo_conv2d_nchwxc for the blocks allowed.  ic_bn = 1 (C <= 4): the conv
+     * reads its input in the default layout NCHW, which NCHW1c is, so no
+     * transform is inserted for an NCHW input such as the network's. */
     int ic_bn, oc_bn;
 } neo_node;
 
@@ -255,8 +258,8 @@ enum neo_plan_flags {
     NEO_PLAN_TUNE = 8,
     /* Global search (Section 3.3.2, Algorithm 2): every conv without a given
      * scheme chooses (ic_bn, oc_bn) among its candidates -- the factors of its
-     * channel counts that the kernel supports (16, 32, 64; 4 for an input of
-     * at most 4 channels), always including the plan's block -- by the local
+     * channel counts that the kernel supports (16, 32, 64; 1 and 4 for an
+     * input of at most 4 channels), always including the plan's block -- by the local
      * search's measured time of each scheme plus the measured time of every
      * layout transform the choice implies, minimised over the whole network by
      * neo_layout_search's dynamic program.  Implies NEO_PLAN_TUNE; needs a
@@ -367,7 +370,9 @@ int neo_tune_db_size(void);
  *   xform_time  host [n_nodes][NB][NB]: time of transforming node v's value
  *               from block i to block j (non-negative)
  *   ic_bn, oc_bn  host [n_nodes] out: the chosen blocks of each conv (0 for
- *               other nodes)
+ *               other nodes).  A conv's ic_bn of 0 means it reads the
+ *               default layout; in a plan's nodes that scheme is ic_bn = 1
+ *               (and a node's given ic_bn = 1 is block 0 here).
  *   cost        host out (may be NULL): the minimum total
  * The program is Algorithm 2 with, as its memorised state, the layouts of
  * every value still to be read later; it is exact.  It returns

@@ -227,7 +227,7 @@ int neo_conv2d_nchwxc(const float* x, int x_block, int N, int C, int H, int W,
     s.yb = y_block;
     if (!conv_blocks_valid(s))
         return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_nchwxc: blocks must be 16, 32 or 64 "
-                                         "(input 4 or 8 too when C <= 4)");
+                                         "(input 1, 4 or 8 too when C <= 4)");
     const int KY = cdiv(K, y_block);
     if (y_blk_offset < 0 || y_blk_total < KY || y_blk_offset + KY > y_blk_total)
         return fail(NEO_ERR_SHAPE, "neo_conv2d_nchwxc: output channel-block view out of range");

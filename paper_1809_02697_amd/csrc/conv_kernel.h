@@ -56,7 +56,9 @@
 // float4 of channels 0..3 of its pixel's input at (r, s), component t feeding
 // k-step t.  So the 16 reduction elements of a step are 4 columns x 4
 // channels, every operand is one float4 per lane as on the main path, and a
-// padding column s >= S reads as 0 like a padding tap.
+// padding column s >= S reads as 0 like a padding tap.  An NCHW input
+// (NCHW1c, block 1) needs no transform: the lane loads its pixel's channels
+// one plane apart, and the channels past C read as 0.
 #pragma once
 
 #include <algorithm>
@@ -198,6 +200,7 @@ struct Loader {
     int ioff[G];                  // XY: input offset of group cb + i from group cb (cb % G == 0)
     unsigned toff[FP];            // lane offset of the current tap, or out of range
     unsigned wtoff[FK];           // small-channel, KCRS[16]c[16]k filter: lane offset or out of range
+    int plain_c, plane;           // small-channel NCHW input: its channels (0 otherwise), bytes per channel
 
     __device__ void set_tap(const ConvArgs& a) {
         if constexpr (SMALLC) {
@@ -309,7 +312,17 @@ struct Loader {
         for (int i = 0; i < G; ++i) {
             const int sxi = sx + (XY ? ioff[i] : i * dx), swi = sw + i * dw;
 #pragma unroll
-            for (int p = 0; p < FP; ++p) o.b[i][p] = ld4(xr, toff[p], sxi, 0);
+            for (int p = 0; p < FP; ++p) {
+                if constexpr (SMALLC && XY) {
+                    if (plain_c) {  // NCHW: the pixel's channels lie a plane apart; the rest are 0
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            o.b[i][p][t] = t < plain_c ? ld1(xr, toff[p], sxi + t * plane, 0) : 0.f;
+                        continue;
+                    }
+                }
+                o.b[i][p] = ld4(xr, toff[p], sxi, 0);
+            }
 #pragma unroll
             for (int f = 0; f < FK; ++f) {
                 if constexpr (WMFMA) {
@@ -380,6 +393,8 @@ __device__ __forceinline__ void conv_tile(const ConvArgs& a, const int u) {
     tl.wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
     tl.wide_taps = a.R > 32 || a.S > 32;
     tl.lg = g;
+    tl.plain_c = __builtin_amdgcn_readfirstlane(XY && a.xb == 1 ? (a.XB < 4 ? a.XB : 4) : 0);
+    tl.plane = __builtin_amdgcn_readfirstlane(a.H * a.W * 4);
     bool pv[FP];
     int pn[FP];
 #pragma unroll

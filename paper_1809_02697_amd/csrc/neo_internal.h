@@ -51,10 +51,12 @@ bool conv_config_valid(const ConvConfig& c);
 // (channel block, kernel entry).
 inline bool conv_small_c(const ConvShape& s) { return s.C <= 4; }
 // Blocks the kernel reads and writes: output 16, 32 or 64; input 16, 32 or 64
-// (any of 4..64 on the small-channel path, which reads channels 0..3 only).
+// (on the small-channel path, which reads channels 0..3 only, any of 4..64,
+// or 1: NCHW1c, which is NCHW itself).
 inline bool conv_blocks_valid(const ConvShape& s) {
     const bool yok = s.yb == 16 || s.yb == 32 || s.yb == 64;
-    const bool xok = conv_small_c(s) ? pow2_block(s.xb) : (s.xb == 16 || s.xb == 32 || s.xb == 64);
+    const bool xok = conv_small_c(s) ? (s.xb == 1 || pow2_block(s.xb))
+                                     : (s.xb == 16 || s.xb == 32 || s.xb == 64);
     return xok && yok;
 }
 // Channel blocks per reduction step for a launch configuration (1 on the

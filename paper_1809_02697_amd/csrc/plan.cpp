@@ -148,6 +148,11 @@ int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
 
 // Channel extent of a value in units of its layout (blocks, or channels).
 int units(int C, int layout) { return layout ? cdiv(C, layout) : C; }
+// A conv's input block 1 (NCHW1c) is the default layout in memory: the conv
+// reads that version of its input, and a search choosing the default layout
+// for a conv input names it block 1.
+int read_layout(int ic) { return ic == 1 ? 0 : ic; }
+int scheme_block(int ic) { return ic == 0 ? 1 : ic; }
 
 struct Builder {
     neo_plan* P;
@@ -398,7 +403,7 @@ int build_steps(neo_plan* P) {
                 Step st{};
                 st.kind = ST_CONV;
                 st.node = id;
-                st.in = B.get(ni.inputs[0], ni.ic, id);
+                st.in = B.get(ni.inputs[0], read_layout(ni.ic), id);
                 if (d.residual >= 0) st.res = B.get(d.residual, ni.oc, id);
                 const int C = a->C;
                 std::vector<float> w((long)d.K * C * d.R * d.S), b(cdiv(d.K, 16) * 16, 0.f);
@@ -834,7 +839,10 @@ std::string describe(const neo_plan* P) {
 // input of at most 4 channels (the small-channel path) also takes 4.
 std::vector<int> candidate_blocks(int C, int D, bool input_side) {
     std::vector<int> out;
-    if (input_side && C <= 4) out.push_back(4);
+    if (input_side && C <= 4) {  // the default layout (read as NCHW1c, no transform) or NCHW4c
+        out.push_back(0);
+        out.push_back(4);
+    }
     for (int b : {16, 32, 64})
         if (b == D || (!(input_side && C <= 4) && C % b == 0 && b < C)) out.push_back(b);
     return out;
@@ -929,7 +937,7 @@ int search_schemes(neo_plan* P) {
         const int ib = kSearchBlocks[i], ob = kSearchBlocks[j];
         const NodeInfo& a = P->nodes[ni.inputs[0]];
         if (ni.ic) {  // the caller's scheme
-            if (ib != ni.ic || ob != ni.oc) return INFINITY;
+            if (ib != read_layout(ni.ic) || ob != ni.oc) return INFINITY;
         } else {
             const std::vector<int> ci = candidate_blocks(a.C, D, true), co = candidate_blocks(ni.C, D, false);
             if (std::find(ci.begin(), ci.end(), ib) == ci.end() ||
@@ -939,7 +947,7 @@ int search_schemes(neo_plan* P) {
         const neo_node& d = ni.nd;
         ConvShape cs{ni.N, a.C, a.H, a.W, d.K, d.R, d.S, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
                      ni.H, ni.W, 0, cdiv(d.K, ob), d.act};
-        cs.xb = ib;
+        cs.xb = scheme_block(ib);
         cs.yb = ob;
         const bool has_res = d.residual >= 0, has_b = d.bn_gamma || d.bias;
         const std::vector<int> key{cs.N, cs.C, cs.H, cs.W, cs.K, cs.R, cs.S, cs.sh, cs.sw, cs.ph, cs.pw,
@@ -995,7 +1003,7 @@ int search_schemes(neo_plan* P) {
     for (size_t v = 0; v < P->nodes.size(); ++v) {
         NodeInfo& ni = P->nodes[v];
         if (ni.nd.op != NEO_OP_CONV || ni.ic) continue;
-        ni.ic = ic[v];
+        ni.ic = scheme_block(ic[v]);
         ni.oc = oc[v];
     }
     P->searched = true;
@@ -1030,7 +1038,7 @@ int neo_layout_search(const neo_node* nodes, int n_nodes, int N, int C, int H, i
                 return fail(NEO_ERR_INVALID_ARG, "neo_layout_search: transform times must be >= 0");
         auto conv_cost = [&](int v, int i, int j) -> double {
             const NodeInfo& ni = P.nodes[v];
-            if (ni.ic && (kSearchBlocks[i] != ni.ic || kSearchBlocks[j] != ni.oc)) return INFINITY;
+            if (ni.ic && (kSearchBlocks[i] != read_layout(ni.ic) || kSearchBlocks[j] != ni.oc)) return INFINITY;
             const double t = conv_time[((long)v * NB + i) * NB + j];
             return (std::isfinite(t) && t >= 0) ? t : INFINITY;
         };

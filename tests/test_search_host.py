@@ -116,7 +116,7 @@ def _random_schemes(g, rng, blocks=(16, 32, 64)):
     out = {}
     for v in S.conv_nodes(g):
         C, K = shapes[g.nodes[v].inputs[0]][1], g.nodes[v].K
-        ics = [4, 16] if C <= 4 else [b for b in blocks if C % b == 0 or b == 16]
+        ics = [1, 4, 16] if C <= 4 else [b for b in blocks if C % b == 0 or b == 16]
         ocs = [b for b in blocks if K % b == 0 or b == 16]
         out[v] = (int(rng.choice(ics)), int(rng.choice(ocs)))
     return out
@@ -142,7 +142,9 @@ def test_plan_layouts_follow_the_search_rules(build, seed):
     d, got = _plan_transforms(g, sch)
     want = []
     ct = [[[0.0] * NB for _ in range(NB)] for _ in g.nodes]
-    S.plan_cost(g, sch, ct, ct, transforms=want)
+    # a conv input block of 1 (NCHW1c) is the default layout, block 0
+    S.plan_cost(g, {v: (0 if a == 1 else a, b) for v, (a, b) in sch.items()}, ct, ct,
+                transforms=want)
     assert got == sorted(want)
     steps = {s["node"]: s for s in d["steps"] if s["kind"] == "conv"}
     for v, (a, b) in sch.items():
@@ -160,6 +162,18 @@ def test_fixed_block_plans():
                    for s in d["steps"] if s["kind"] == "conv")
 
 
+def test_nchw_stem_needs_no_entry_transform():
+    """ResNet-50 with the stem's input block 1: the stem reads the network's
+    NCHW input itself, so only the exit transform (an alias) remains."""
+    g = nets.resnet50()
+    stem = S.conv_nodes(g)[0]
+    d, got = _plan_transforms(g, {stem: (1, 16)})
+    assert [t[1:] for t in got] == [(16, 0, True)]
+    st = next(s for s in d["steps"] if s["kind"] == "conv" and s["node"] == stem)
+    assert (st["conv"]["ic_bn"], st["conv"]["oc_bn"]) == (1, 16)
+    assert d["values"][st["in"]]["buf"] == -2          # the caller's input buffer
+
+
 def test_plan_scheme_errors():
     g = wl.tiny_graph()
     with pytest.raises(neo.NeoError) as e:
@@ -170,6 +184,9 @@ def test_plan_scheme_errors():
     assert e.value.code == -4
     with pytest.raises(neo.NeoError) as e:
         neo.Plan(g, flags=neo.PLAN_HOST_ONLY, schemes={3: (16, 4)})    # outputs: 16..64
+    assert e.value.code == -4
+    with pytest.raises(neo.NeoError) as e:
+        neo.Plan(g, flags=neo.PLAN_HOST_ONLY, schemes={3: (1, 16)})    # NCHW input: C <= 4 only
     assert e.value.code == -4
     with pytest.raises(neo.NeoError):
         neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_GLOBAL_SEARCH)
