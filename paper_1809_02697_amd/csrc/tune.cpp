@@ -47,6 +47,15 @@ std::string device_arch() {
     return colon == std::string::npos ? a : a.substr(0, colon);
 }
 
+// The input and output blocks of a stored workload are ones the kernel takes.
+bool key_blocks_valid(const Key& k) {
+    ConvShape s{};
+    s.C = k.C;
+    s.xb = k.xb;
+    s.yb = k.yb;
+    return conv_blocks_valid(s);
+}
+
 Key key_of(const ConvShape& s, bool wmfma, const std::string& arch) {
     return Key{arch, s.N, s.C, s.H, s.W, s.K, s.R, s.S, s.sh, s.sw, s.ph, s.pw, wmfma ? 1 : 0,
                s.xb, s.yb};
@@ -371,7 +380,7 @@ int neo_tune_db_load(const char* path) {
         if (!(is >> k.arch >> k.N >> k.C >> k.H >> k.W >> k.K >> k.R >> k.S >> k.sh >> k.sw >> k.ph >>
               k.pw >> k.wmfma >> k.xb >> k.yb >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >>
               v.us) ||
-            !conv_config_valid(v.cfg) || !pow2_block(k.xb) || !pow2_block(k.yb))
+            !conv_config_valid(v.cfg) || !key_blocks_valid(k))
             return fail(NEO_ERR_INVALID_ARG,
                         "neo_tune_db_load: malformed line " + std::to_string(lineno));
         add[k] = v;

@@ -257,6 +257,12 @@ def test_tune_db_roundtrip_and_errors(tmp_path):
     bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 12 16 2 2 1 4 7.5\n")   # no 12 block
     with pytest.raises(neo.NeoError):
         neo.tune_db_load(bad)
+    bad.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 1 16 2 2 1 4 7.5\n")    # NCHW: C <= 4 only
+    with pytest.raises(neo.NeoError):
+        neo.tune_db_load(bad)
+    stem = tmp_path / "stem.txt"                                               # the stem reading NCHW
+    stem.write_text("gfx950 1 3 224 224 64 7 7 2 2 3 3 1 1 16 4 1 1 1 8.25\n")
+    assert neo.tune_db_load(stem) == 1
     with pytest.raises(neo.NeoError):
         neo.tune_db_load(tmp_path / "missing.txt")
     neo.tune_db_clear()
