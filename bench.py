@@ -28,7 +28,8 @@ Printed JSON line:
                "naive" (transforms around every blocked operation), "eliminated"
                (one block for every conv, transforms only at the ends) and
                "searched" (the global layout search); plus "grouped" (the
-               eliminated plan with independent convs fused into one launch); all
+               eliminated plan with independent convs fused into launches, pools
+               riding along, and a global pool folded into its neighbours); all
                with tuned launch configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
@@ -73,14 +74,15 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     """The plan bench.py times, and how it was chosen.  The global search
     (Section 3.3.2) chooses every conv's scheme from per-conv times measured
     in isolation; the resulting plan and the one-block plan (Section 3.2, all
-    convs in NCHW16c) -- both with independent convs fused into launches --
+    convs in NCHW16c) -- both with independent convs fused into launches and
+    the global pool folded into the last conv and the dense layer --
     are then both timed end to end and the faster is kept,
     so a search decision that the isolated timings mispredict cannot make the
     step slower.  With a results file from an earlier run (``--tune-db``) the
     schemes that run kept are reused from ``<file>.schemes.json`` (so a
     profiling run executes the same plan)."""
     path = (tune_db or "") + ".schemes.json"
-    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP
+    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP
     if tune_db and os.path.exists(path):
         sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
         return neo.Plan(g, flags=neo.PLAN_TUNE | base, schemes=sch), {"from": path}
@@ -122,8 +124,10 @@ def launch_costs(members):
     """Algorithmic FLOPs and bytes of one launch (summed over its convs)."""
     f = b = 0
     for c, res in members:
-        ff, bb, _, _ = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"],
-                                  c["pad"], N=c["N"], residual=res)
+        ff, bb, OH, OW = conv_costs(c["C"], c["K"], c["R"], c["S"], c["H"], c["W"], c["stride"],
+                                    c["pad"], N=c["N"], residual=res)
+        if c.get("gap_sums"):   # writes per-16-pixel channel sums, not its outputs
+            bb += 4 * c["K"] * (-(-OH * OW // 16) - OH * OW)
         f, b = f + ff, b + bb
     return f, b
 
@@ -299,7 +303,7 @@ def model_latencies(neo, torch, wl, steps):
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        plans = [("eliminated", 0, 16), ("grouped", neo.PLAN_GROUP, 16)]
+        plans = [("eliminated", 0, 16), ("grouped", neo.PLAN_GROUP | neo.PLAN_FUSE_GAP, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
         if name == "resnet50":

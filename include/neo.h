@@ -278,7 +278,15 @@ enum neo_plan_flags {
      * NEO_PLAN_TUNE, which also takes the pool out, or splits the convs into
      * launches of their own, when that measures faster), so their results
      * match the oracle but are not bit-identical to an ungrouped plan's. */
-    NEO_PLAN_GROUP = 32
+    NEO_PLAN_GROUP = 32,
+    /* Fold a global average pool into its neighbours (not in the paper; one
+     * launch less at batch 1): when its input is one image's output of a
+     * conv that nothing else reads, and only dense layers read its result
+     * (through a flatten), the conv writes the channel sums of every 16 output
+     * pixels instead of its outputs, and each dense layer takes their mean as
+     * its input.  Results match the oracle but are not bit-identical to an
+     * unfolded plan's (the sums run in another order). */
+    NEO_PLAN_FUSE_GAP = 64
 };
 
 /*

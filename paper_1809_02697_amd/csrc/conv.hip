@@ -133,6 +133,7 @@ ConvArgs make_args(const ConvShape& s, const ConvConfig& c, int G, const float* 
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
     a.div_nkb = make_fastdiv((unsigned)cdiv(a.KBk, c.fk));
+    a.gap = s.gap;
     return a;
 }
 
@@ -142,14 +143,18 @@ hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st) {
     if (!conv_config_valid(c) || !conv_blocks_valid(s)) return hipErrorInvalidValue;
+    if (s.gap && s.N != 1) return hipErrorInvalidValue;
     const int G = conv_group(s, c);
-    const ConvArgs a = make_args(s, c, G, x, w, wmfma, bias, res, y, ws);
+    // a folded global pool writes its sums in the kernel's epilogue: no split
+    const ConvArgs a = make_args(s, c, G, x, w, wmfma, bias, res, y, s.gap ? nullptr : ws);
     const bool small = conv_small_c(s);
     if (s.xb == 16 && s.yb == 16) return dispatch_all<false>(c, G, small, wmfma, a, st);
     return dispatch_all<true>(c, G, small, wmfma, a, st);
 }
 
-bool conv_group_eligible(const ConvShape& s) { return !conv_small_c(s) && s.xb == 16 && s.yb == 16; }
+bool conv_group_eligible(const ConvShape& s) {
+    return !conv_small_c(s) && s.xb == 16 && s.yb == 16 && !s.gap;
+}
 
 int conv_group_steps_min(const ConvShape* s, int n, const ConvConfig& c) {
     int G = 4, steps = 1 << 30;

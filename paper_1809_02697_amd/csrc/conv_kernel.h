@@ -108,6 +108,9 @@ struct ConvArgs {
     // padding of the last block); the residual has KY blocks.
     int yb, lyb, KBk, KY;
     int x_bytes, w_bytes;
+    // 1: global average pooling folded in -- y receives per-16-pixel channel
+    // sums [ceil(M / 16)][KB * 16] instead of the outputs (one image, no split)
+    int gap;
     FastDiv div_ohw, div_ow, div_npx, div_nkb;
 };
 
@@ -546,6 +549,24 @@ __device__ __forceinline__ void conv_tile(const ConvArgs& a, const int u) {
         return;
     }
 
+    // act(acc + bias + residual) of pixel group p, channel quad of output group kb
+    auto out_value = [&](const v4f& sum, const v4f& bb, const v4f& pre, int p, int kb) {
+        v4f o = sum + bb;
+        if constexpr (kPrefetch) {
+            o += pre;
+        } else if (a.res) {
+            const int oh = (tl.pih[p] + a.ph) / a.sh;
+            const int ow = (tl.piw[p] + a.pw) / a.sw;
+            o += *reinterpret_cast<const v4f*>(
+                a.res + yindex<XY>(a, pn[p], rblocks<XY>(a), kb * 16 + 4 * g, oh * a.OW + ow));
+        }
+        if (a.act == NEO_ACT_RELU) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
+        }
+        return o;
+    };
+
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kb0 + f;
@@ -559,24 +580,28 @@ __device__ __forceinline__ void conv_tile(const ConvArgs& a, const int u) {
             bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
+            const v4f pre = pre_r[kPrefetch ? f : 0][kPrefetch ? p : 0];
+            if (a.gap) {
+                // Global average pooling folded in (one image): instead of the
+                // outputs, the sum of this group's 16 pixels per channel, row
+                // m / 16 of a [pixel group][KB * 16] table, summed over the 16
+                // lanes that hold them in a fixed order.
+                const int m = m0 + 16 * p;
+                if (!real || m >= a.M) continue;  // the whole wave
+                v4f o = pv[p] ? out_value(acc[f][p], bb, pre, p, kb) : v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) o[v] += __shfl_xor(o[v], off, 16);
+                if (li == 0) *reinterpret_cast<v4f*>(a.y + (long)(m >> 4) * a.KB * 16 + kb * 16 + 4 * g) = o;
+                continue;
+            }
             if (!pv[p]) continue;
-            const int n = pn[p];
             const int oh = (tl.pih[p] + a.ph) / a.sh;
             const int ow = (tl.piw[p] + a.pw) / a.sw;
-            v4f o = acc[f][p] + bb;
-            if constexpr (kPrefetch) {
-                o += pre_r[f][p];
-            } else if (a.res) {
-                o += *reinterpret_cast<const v4f*>(
-                    a.res + yindex<XY>(a, n, rblocks<XY>(a), kb * 16 + 4 * g, oh * a.OW + ow));
-            }
-            if (a.act == NEO_ACT_RELU) {
-#pragma unroll
-                for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
-            }
-            if (!real) o = v4f{0.f, 0.f, 0.f, 0.f};
+            const v4f o = real ? out_value(acc[f][p], bb, pre, p, kb) : v4f{0.f, 0.f, 0.f, 0.f};
             *reinterpret_cast<v4f*>(
-                a.y + yindex<XY>(a, n, a.y_tot, a.y_off * (XY ? a.yb : 16) + kb * 16 + 4 * g, oh * a.OW + ow)) = o;
+                a.y + yindex<XY>(a, pn[p], a.y_tot, a.y_off * (XY ? a.yb : 16) + kb * 16 + 4 * g, oh * a.OW + ow)) = o;
         }
     }
 }

@@ -26,7 +26,17 @@ struct DenseArgs {
     const float* bias;
     float* y;
     int N, IN, OUT, act, T;  // T = number of 16-wide reduction chunks
+    // x is the mean of `parts` rows (stride xs4 float4s): scale * (row 0 + row 1 + ...)
+    int parts, xs4;
+    float scale;
 };
+
+// float4 k of the mean of the input's rows (in row order)
+__device__ inline v4f rows_mean4(const DenseArgs& a, const v4f* x4, int k) {
+    v4f s = x4[k];
+    for (int t = 1; t < a.parts; ++t) s += x4[(long)t * a.xs4 + k];
+    return s * a.scale;
+}
 
 constexpr int kWaves = 4;
 constexpr int kU = 4;
@@ -136,12 +146,22 @@ __global__ __launch_bounds__(256) void dense_mfma(DenseArgs a) {
 }
 
 constexpr int kG = 8;  // float4 chunks of a row in flight per lane
+constexpr int kMaxPartsIn = 16384;  // an input summed into LDS: at most 64 KB
 
 // One wave per output feature o: lane l accumulates the chunks l, l+64, ...
 // of row o against the same chunks of each batch row, then the wave adds its
 // lanes in a fixed butterfly order.  NB >= N batch rows, compile-time.
-template <int NB, bool VEC>
+// PARTS (one batch row): the workgroup first sums the input's rows into LDS
+// once, and its waves read the input from there.
+template <int NB, bool VEC, bool PARTS = false>
 __global__ __launch_bounds__(256) void dense_rows(DenseArgs a) {
+    extern __shared__ v4f xsum[];  // PARTS: IN / 4 float4s
+    if constexpr (PARTS) {
+        const int n4 = a.IN >> 2;
+        const v4f* x4 = reinterpret_cast<const v4f*>(a.x);
+        for (int k = threadIdx.x; k < n4; k += blockDim.x) xsum[k] = rows_mean4(a, x4, k);
+        __syncthreads();
+    }
     const int lane = threadIdx.x & 63;
     const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (o >= a.OUT) return;  // whole wave
@@ -161,8 +181,12 @@ __global__ __launch_bounds__(256) void dense_rows(DenseArgs a) {
 #pragma unroll
             for (int g = 0; g < kG; ++g)
 #pragma unroll
-                for (int n = 0; n < NB; ++n)
-                    xv[g][n] = n < a.N ? x4[(long)n * n4 + k + 64 * g] : v4f{0.f, 0.f, 0.f, 0.f};
+                for (int n = 0; n < NB; ++n) {
+                    if constexpr (PARTS)
+                        xv[g][n] = xsum[k + 64 * g];
+                    else
+                        xv[g][n] = n < a.N ? x4[(long)n * n4 + k + 64 * g] : v4f{0.f, 0.f, 0.f, 0.f};
+                }
 #pragma unroll
             for (int g = 0; g < kG; ++g)
 #pragma unroll
@@ -175,11 +199,12 @@ __global__ __launch_bounds__(256) void dense_rows(DenseArgs a) {
 #pragma unroll
             for (int n = 0; n < NB; ++n) {
                 if (n >= a.N) break;
-                const v4f xv = x4[(long)n * n4 + k];
+                const v4f xv = PARTS ? xsum[k] : x4[(long)n * n4 + k];
                 acc[n] += wv.x * xv.x + wv.y * xv.y + wv.z * xv.z + wv.w * xv.w;
             }
         }
     } else {
+        static_assert(!PARTS, "partial rows need aligned float4 rows");
         for (int k = lane; k < a.IN; k += 64) {
             const float wv = wr[k];
 #pragma unroll
@@ -226,9 +251,20 @@ hipError_t dispatch(const DenseArgs& a, hipStream_t st) {
 
 }  // namespace
 
+hipError_t launch_dense_parts(const float* x, int parts, int xstride, float scale, int IN,
+                              const float* w, int OUT, const float* bias, int act, float* y,
+                              hipStream_t st) {
+    if (parts < 1 || xstride < IN || xstride % 4 || IN % 4 || IN > kMaxPartsIn || !aligned16(x) ||
+        !aligned16(w))
+        return hipErrorInvalidValue;
+    DenseArgs a{x, w, bias, y, 1, IN, OUT, act, cdiv(IN, 16), parts, xstride / 4, scale};
+    hipLaunchKernelGGL((dense_rows<1, true, true>), dim3(cdiv(OUT, 4)), dim3(256), IN * 4, st, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_dense(const float* x, int N, int IN, const float* w, int OUT,
                         const float* bias, int act, float* y, hipStream_t st) {
-    DenseArgs a{x, w, bias, y, N, IN, OUT, act, cdiv(IN, 16)};
+    DenseArgs a{x, w, bias, y, N, IN, OUT, act, cdiv(IN, 16), 0, 0, 1.f};
     const bool vec = (IN % 4 == 0) && aligned16(x) && aligned16(w);
     return vec ? dispatch<true>(a, st) : dispatch<false>(a, st);
 }

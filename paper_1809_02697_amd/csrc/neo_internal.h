@@ -37,6 +37,9 @@ struct ConvShape {
     int y_off, y_tot;    // output channel-block view, in blocks of yb
     int act;
     int xb = 16, yb = 16;  // input layout NCHW[xb]c, output (and residual) NCHW[yb]c
+    // 1: global average pooling folded in (N = 1): y receives, instead of the
+    // outputs, the channel sums of every 16 pixels, [ceil(OH*OW/16)][ceil(K/16)*16]
+    int gap = 0;
 };
 
 // Launch configuration: register tile (fk channel blocks x fp pixel groups of
@@ -159,6 +162,13 @@ int layout_search_dp(const std::vector<SearchNode>& g, const std::vector<int>& o
 // ---- dense ----------------------------------------------------------------------------
 hipError_t launch_dense(const float* x, int N, int IN, const float* w, int OUT,
                         const float* bias, int act, float* y, hipStream_t st);
+// The same layer on an input that is the mean of `parts` rows of x (row stride
+// xstride floats): x_in = scale * (row 0 + row 1 + ...), summed in row order --
+// the per-16-pixel sums of a conv with global average pooling folded in.  N = 1,
+// IN <= 16384.
+hipError_t launch_dense_parts(const float* x, int parts, int xstride, float scale, int IN,
+                              const float* w, int OUT, const float* bias, int act, float* y,
+                              hipStream_t st);
 
 // ---- host helpers -----------------------------------------------------------------------
 void fold_bn_host(const float* w, const float* bias, const float* gamma, const float* beta,

@@ -66,6 +66,10 @@ struct Step {
     long w_off = -1, b_off = -1;
     int src_block = 0, dst_block = 0;
     int dense_in = 0, dense_out = 0, act = 0;
+    // ST_DENSE fed by a conv with global average pooling folded in: its input
+    // value holds gap_parts rows of channel sums (row stride gap_stride floats)
+    int gap_parts = 0, gap_stride = 0;
+    float gap_scale = 1.f;
     std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's)
     std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1)
 };
@@ -728,6 +732,71 @@ void group_ready_convs(neo_plan* P) {
     S.swap(out);
 }
 
+// NEO_PLAN_FUSE_GAP: a global average pool whose input is one image's output
+// of a conv step (read by nothing else) and whose result only dense layers
+// read (through a flatten, and the transform to NCHW before it) is folded
+// into both: the conv writes, instead of
+// its outputs, the channel sums of every 16 pixels, and each dense layer
+// reads their mean.  One launch less, and the conv's output never goes to
+// memory.
+void fuse_gap(neo_plan* P) {
+    std::vector<Step>& S = P->steps;
+    auto root = [&](int v) {
+        while (P->vals[v].alias_of >= 0) v = P->vals[v].alias_of;
+        return v;
+    };
+    std::vector<char> drop(S.size(), 0);
+    for (size_t j = 0; j < S.size(); ++j) {
+        if (S[j].kind != ST_GAP) continue;
+        const int in = S[j].in, g = S[j].out;
+        const Val& iv = P->vals[in];
+        // (the dense layer sums the input's rows in 64 KB of LDS)
+        if (iv.N != 1 || iv.view || iv.alias_of >= 0 || iv.consumers != 1 || iv.C % 4 || iv.C > 16384)
+            continue;
+        int pi = -1;
+        for (size_t i = 0; i < j; ++i)
+            if (S[i].out == in) pi = (int)i;
+        if (pi < 0 || S[pi].kind != ST_CONV) continue;
+        // the pooled value and its transforms (a 1x1 map: to NCHW for the
+        // flatten); every reader must be a dense layer or such a transform
+        std::vector<int> pooled{g};
+        auto is_pooled = [&](int v) {
+            return v >= 0 && std::find(pooled.begin(), pooled.end(), root(v)) != pooled.end();
+        };
+        std::vector<size_t> dense, xforms;
+        bool ok = true;
+        for (size_t k = j + 1; k < S.size() && ok; ++k) {
+            if (is_pooled(S[k].res)) ok = false;
+            if (!is_pooled(S[k].in)) continue;
+            if (S[k].kind == ST_TRANSFORM) {
+                pooled.push_back(S[k].out);
+                xforms.push_back(k);
+            } else if (S[k].kind == ST_DENSE && S[k].dense_in == iv.C) {
+                dense.push_back(k);
+            } else {
+                ok = false;
+            }
+        }
+        ok = ok && !is_pooled(P->out_val);
+        for (size_t v = 0; v < P->vals.size(); ++v) ok = ok && !(P->vals[v].view && is_pooled((int)v));
+        if (!ok || dense.empty()) continue;
+        S[pi].cs.gap = 1;
+        const int hw = iv.H * iv.W;
+        for (size_t k : dense) {
+            S[k].in = in;  // reads the conv's sums (and so runs after it)
+            S[k].gap_parts = cdiv(hw, 16);
+            S[k].gap_stride = cdiv(iv.C, 16) * 16;
+            S[k].gap_scale = 1.f / (float)hw;
+        }
+        drop[j] = 1;
+        for (size_t k : xforms) drop[k] = 1;
+    }
+    std::vector<Step> out;
+    for (size_t j = 0; j < S.size(); ++j)
+        if (!drop[j]) out.push_back(S[j]);
+    S.swap(out);
+}
+
 float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     const Val& val = P->vals[v];
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
@@ -797,7 +866,9 @@ std::string describe(const neo_plan* P) {
               << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
               << ",\"ic_bn\":" << c.xb << ",\"oc_bn\":" << c.yb
               << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
-              << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false") << "}";
+              << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false");
+            if (c.gap) o << ",\"gap_sums\":true";
+            o << "}";
         };
         if (s.kind == ST_CONV) {
             o << ",\"conv\":";
@@ -819,7 +890,11 @@ std::string describe(const neo_plan* P) {
                   << ",\"in\":" << ps.in << ",\"out\":" << ps.out << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
-        if (s.kind == ST_DENSE) o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out << "}";
+        if (s.kind == ST_DENSE) {
+            o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out;
+            if (s.gap_parts) o << ",\"gap_parts\":" << s.gap_parts;
+            o << "}";
+        }
         o << "}";
     }
     o << "],\"buffers\":[";
@@ -1070,7 +1145,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (block != 16 && block != 32 && block != 64)
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
-                            NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP))
+                            NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -1086,6 +1161,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
@@ -1242,9 +1318,15 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
             }
             case ST_DENSE: {
                 const Val& in = P->vals[s.in];
-                e = launch_dense(val_ptr(P, s.in, x_nchw, y_out), in.N, s.dense_in, prm + s.w_off,
-                                 s.dense_out, s.b_off >= 0 ? prm + s.b_off : nullptr, s.act,
-                                 val_ptr(P, s.out, x_nchw, y_out), st);
+                if (s.gap_parts)
+                    e = launch_dense_parts(val_ptr(P, s.in, x_nchw, y_out), s.gap_parts, s.gap_stride,
+                                           s.gap_scale, s.dense_in, prm + s.w_off, s.dense_out,
+                                           s.b_off >= 0 ? prm + s.b_off : nullptr, s.act,
+                                           val_ptr(P, s.out, x_nchw, y_out), st);
+                else
+                    e = launch_dense(val_ptr(P, s.in, x_nchw, y_out), in.N, s.dense_in, prm + s.w_off,
+                                     s.dense_out, s.b_off >= 0 ? prm + s.b_off : nullptr, s.act,
+                                     val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
             }
             case ST_COPY: {
@@ -1354,7 +1436,11 @@ static int tune_plan(neo_plan* P) {
         }
         if (s.kind == ST_CONV && !s.tuned) {
             const float* prm = P->d_params;
-            rc = tune_conv(s.cs, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
+            // a conv with the global pool folded in is timed as a plain conv
+            // (its launch then runs the configuration without a split)
+            ConvShape ts = s.cs;
+            ts.gap = 0;
+            rc = tune_conv(ts, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
                            s.b_off >= 0 ? prm + s.b_off : nullptr,
                            s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
                            val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
