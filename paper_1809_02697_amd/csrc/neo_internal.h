@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstddef>
 #include <cstdint>
 #include <functional>
@@ -121,6 +122,52 @@ int tune_pool(const GroupPool& p, hipStream_t st, float* us);
 bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out);
 int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
               const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
+
+// ---- timing (local search, global search) ----------------------------------------------
+// Time per launch of `launch` on `st` (a stream that is not the legacy null
+// stream): one warm-up launch (it also surfaces a launch error before
+// capture), then `reps` launches captured into a graph, replayed three times
+// between two events; the fastest replay counts.
+template <typename F>
+hipError_t time_launch(F launch, hipStream_t st, hipEvent_t e0, hipEvent_t e1, float* us) {
+    const int reps = 10;
+    hipError_t e = launch();
+    if (e != hipSuccess) return e;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+    for (int i = 0; i < reps && e == hipSuccess; ++i) e = launch();
+    hipError_t e2 = hipStreamEndCapture(st, &g);
+    if (e == hipSuccess) e = e2;
+    if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    if (g) (void)hipGraphDestroy(g);
+    float ms = 1e30f;
+    for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+        e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e0, st);
+        if (e == hipSuccess) e = hipGraphLaunch(ge, st);
+        if (e == hipSuccess) e = hipEventRecord(e1, st);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e == hipSuccess) ms = std::min(ms, t);
+    }
+    if (ge) (void)hipGraphExecDestroy(ge);
+    *us = ms * 1000.f / reps;
+    return e;
+}
+
+struct Events {
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    Events() {
+        (void)hipEventCreate(&e0);
+        (void)hipEventCreate(&e1);
+    }
+    ~Events() {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+    }
+};
 
 // ---- layout ---------------------------------------------------------------------------
 // dst_off / dst_tot: destination channel view in destination units (channels

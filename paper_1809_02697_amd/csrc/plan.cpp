@@ -923,40 +923,6 @@ std::vector<int> candidate_blocks(int C, int D, bool input_side) {
     return out;
 }
 
-// Average time of `reps` back-to-back launches of fn captured in one graph,
-// best of 3 replays, on stream st (us); a negative value on a HIP error.
-template <class F>
-double time_launches(hipStream_t st, F fn, int reps = 10) {
-    hipError_t e = fn();
-    if (e != hipSuccess) return -1;
-    hipGraph_t g = nullptr;
-    hipGraphExec_t ge = nullptr;
-    e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
-    for (int i = 0; i < reps && e == hipSuccess; ++i) e = fn();
-    hipError_t e2 = hipStreamEndCapture(st, &g);
-    if (e == hipSuccess) e = e2;
-    if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
-    if (g) (void)hipGraphDestroy(g);
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (e == hipSuccess) e = hipEventCreate(&e0);
-    if (e == hipSuccess) e = hipEventCreate(&e1);
-    float best = 1e30f;
-    for (int r = 0; r < 3 && e == hipSuccess; ++r) {
-        e = hipGraphLaunch(ge, st);
-        if (e == hipSuccess) e = hipEventRecord(e0, st);
-        if (e == hipSuccess) e = hipGraphLaunch(ge, st);
-        if (e == hipSuccess) e = hipEventRecord(e1, st);
-        if (e == hipSuccess) e = hipEventSynchronize(e1);
-        float t = 0.f;
-        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
-        if (e == hipSuccess) best = std::min(best, t);
-    }
-    if (ge) (void)hipGraphExecDestroy(ge);
-    if (e0) (void)hipEventDestroy(e0);
-    if (e1) (void)hipEventDestroy(e1);
-    return e == hipSuccess ? best * 1000.0 / reps : -1;
-}
-
 // NEO_PLAN_GLOBAL_SEARCH: measure every candidate scheme of every conv without
 // a given scheme (the local search, its best launch configuration and time
 // per (workload, ic_bn, oc_bn)) and every layout transform the program asks
@@ -1004,6 +970,7 @@ int search_schemes(neo_plan* P) {
     };
 
     const int D = P->block;
+    Events ev;
     std::map<std::vector<int>, double> xmemo;
     std::map<std::vector<int>, double> cmemo;
     int measured = 0;
@@ -1047,11 +1014,12 @@ int search_schemes(neo_plan* P) {
         auto it = xmemo.find(key);
         if (it != xmemo.end()) return it->second;
         if (merr != NEO_OK) return INFINITY;
-        const double t = time_launches(st, [&]() {
+        float us = 0.f;
+        const hipError_t te = time_launch([&]() {
             return launch_layout_transform(X, sb, Y, db, ni.N, ni.C, ni.H, ni.W, 0, units(ni.C, db), st);
-        });
-        if (t < 0) measure_failed(fail(NEO_ERR_HIP, "neo_plan_create: transform timing failed"));
-        xmemo[key] = t < 0 ? INFINITY : t;
+        }, st, ev.e0, ev.e1, &us);
+        if (te != hipSuccess) measure_failed(hip_fail(te, "neo_plan_create: transform timing"));
+        xmemo[key] = te != hipSuccess ? INFINITY : us;
         return xmemo[key];
     };
     std::vector<int> ic, oc;
