@@ -29,7 +29,8 @@ Printed JSON line:
                (one block for every conv, transforms only at the ends) and
                "searched" (the global layout search); plus "grouped" (the
                eliminated plan with independent convs fused into launches, pools
-               riding along, and a global pool folded into its neighbours); all
+               riding along, a global pool folded into its neighbours, and
+               pairs of pointwise convs fused); all
                with tuned launch configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
@@ -65,7 +66,8 @@ def plan_schemes(desc):
     """{conv node: (ic_bn, oc_bn)} of a plan description."""
     out = {}
     for s in desc["steps"]:
-        for m in (s["members"] if s["kind"] == "conv_group" else [s] if s["kind"] == "conv" else []):
+        for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair")
+                  else [s] if s["kind"] == "conv" else []):
             out[m["node"]] = (m["conv"]["ic_bn"], m["conv"]["oc_bn"])
     return out
 
@@ -74,15 +76,16 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     """The plan bench.py times, and how it was chosen.  The global search
     (Section 3.3.2) chooses every conv's scheme from per-conv times measured
     in isolation; the resulting plan and the one-block plan (Section 3.2, all
-    convs in NCHW16c) -- both with independent convs fused into launches and
-    the global pool folded into the last conv and the dense layer --
+    convs in NCHW16c) -- both with independent convs fused into launches,
+    the global pool folded into the last conv and the dense layer, and pairs
+    of pointwise convs in one launch --
     are then both timed end to end and the faster is kept,
     so a search decision that the isolated timings mispredict cannot make the
     step slower.  With a results file from an earlier run (``--tune-db``) the
     schemes that run kept are reused from ``<file>.schemes.json`` (so a
     profiling run executes the same plan)."""
     path = (tune_db or "") + ".schemes.json"
-    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP
+    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS
     if tune_db and os.path.exists(path):
         sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
         return neo.Plan(g, flags=neo.PLAN_TUNE | base, schemes=sch), {"from": path}
@@ -117,6 +120,9 @@ def conv_launches(desc):
             out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
                         dict(tile=s["tile"], split=1, waves=s["waves"], ic_bn=16, oc_bn=16,
                              group=len(s["members"]))))
+        elif s["kind"] == "conv_pair":
+            out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
+                        dict(pair=True, split=1, waves=8, ic_bn=16, oc_bn=16)))
     return out
 
 
@@ -303,7 +309,8 @@ def model_latencies(neo, torch, wl, steps):
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        plans = [("eliminated", 0, 16), ("grouped", neo.PLAN_GROUP | neo.PLAN_FUSE_GAP, 16)]
+        fused = neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS
+        plans = [("eliminated", 0, 16), ("grouped", fused, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
         if name == "resnet50":

@@ -123,6 +123,19 @@ bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out);
 int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, const float* bias,
               const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
 
+// Two pointwise convolutions in one launch (conv_pair.hip): a (1x1 stride 1,
+// NCHW16c, optional residual) whose output y = b's input is also stored, then
+// b (1x1 stride 1, no residual).  Shapes with a kernel: 64 -> 256 -> 64
+// channels (ceil(C/16) = 4, 16, 4).  Filters in kernel order.
+bool conv_pair_eligible(const ConvShape& a, const ConvShape& b);
+hipError_t launch_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const float* wa,
+                            const float* ba, const float* res, float* y, const float* wb,
+                            const float* bb, float* z, hipStream_t st);
+// Time per launch of a pair (results database).
+int tune_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const float* wa,
+                   const float* ba, const float* res, float* y, const float* wb, const float* bb,
+                   float* z, hipStream_t st, float* us);
+
 // ---- timing (local search, global search) ----------------------------------------------
 // Time per launch of `launch` on `st` (a stream that is not the legacy null
 // stream): one warm-up launch (it also surfaces a launch error before

@@ -39,7 +39,8 @@ using namespace neo;
 
 namespace {
 
-enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY, ST_CONV_GROUP };
+enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY, ST_CONV_GROUP,
+                ST_CONV_PAIR };
 
 struct Val {
     int N = 0, C = 0, H = 0, W = 0;
@@ -59,6 +60,7 @@ struct Step {
     int kind;
     int node;         // originating node (transforms: the consumer that needed it)
     int in = -1, out = -1, res = -1;
+    int out2 = -1;    // ST_CONV_PAIR: the second conv's output (out is the first's)
     ConvShape cs{};
     ConvConfig cc{1, 1, 1, 4};
     bool tuned = false;
@@ -70,7 +72,8 @@ struct Step {
     // value holds gap_parts rows of channel sums (row stride gap_stride floats)
     int gap_parts = 0, gap_stride = 0;
     float gap_scale = 1.f;
-    std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's)
+    std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's);
+                                // ST_CONV_PAIR: the two convs, in order
     std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1)
 };
 
@@ -665,13 +668,13 @@ void group_ready_convs(neo_plan* P) {
         if (S[j].in >= 0) reads.push_back(extent(S[j].in));
         if (S[j].res >= 0) reads.push_back(extent(S[j].res));
         for (int i = 0; i < j; ++i) {
-            if (S[i].out < 0) continue;
-            const Extent w = extent(S[i].out);
-            for (const Extent& r : reads)
-                if (overlap(w, r)) {
-                    deps[j].push_back(i);
-                    break;
-                }
+            bool dep = false;
+            for (int o : {S[i].out, S[i].out2}) {
+                if (o < 0) continue;
+                const Extent w = extent(o);
+                for (const Extent& r : reads) dep = dep || overlap(w, r);
+            }
+            if (dep) deps[j].push_back(i);
         }
     }
     // a pooling step of the round rides along in one of its conv launches
@@ -797,6 +800,41 @@ void fuse_gap(neo_plan* P) {
     S.swap(out);
 }
 
+// NEO_PLAN_FUSE_PAIRS: a pointwise conv whose output is the input of a later
+// pointwise conv with a kernel for the pair (conv_pair_eligible) runs with it
+// in one launch, at the first conv's place (the second reads nothing else, so
+// its inputs are ready there).  The first output is still stored; other
+// readers keep reading it.  Tuning splits a pair that measures slower than
+// its two convs alone.
+void fuse_pairs(neo_plan* P) {
+    std::vector<Step>& S = P->steps;
+    std::vector<char> taken(S.size(), 0);
+    std::vector<Step> out;
+    for (size_t i = 0; i < S.size(); ++i) {
+        if (taken[i]) continue;
+        bool paired = false;
+        for (size_t j = i + 1; j < S.size() && S[i].kind == ST_CONV && !paired; ++j) {
+            const Step& b = S[j];
+            if (taken[j] || b.kind != ST_CONV || b.in != S[i].out || b.res >= 0 ||
+                P->vals[S[i].out].view || !conv_pair_eligible(S[i].cs, b.cs))
+                continue;
+            Step pr{};
+            pr.kind = ST_CONV_PAIR;
+            pr.node = S[i].node;
+            pr.in = S[i].in;
+            pr.res = S[i].res;
+            pr.out = S[i].out;
+            pr.out2 = b.out;
+            pr.members = {S[i], b};
+            taken[j] = 1;
+            out.push_back(pr);
+            paired = true;
+        }
+        if (!paired) out.push_back(S[i]);
+    }
+    S.swap(out);
+}
+
 float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     const Val& val = P->vals[v];
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
@@ -852,7 +890,7 @@ std::string describe(const neo_plan* P) {
     }
     o << "],\"n_transforms\":" << P->xforms.size() << ",\"steps\":[";
     static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy",
-                                  "conv_group"};
+                                  "conv_group", "conv_pair"};
     for (size_t i = 0; i < P->steps.size(); ++i) {
         const Step& s = P->steps[i];
         o << (i ? "," : "") << "{\"kind\":\"" << kinds[s.kind] << "\",\"node\":" << s.node
@@ -888,6 +926,17 @@ std::string describe(const neo_plan* P) {
             for (const Step& ps : s.pools)
                 o << ",\"pool\":{\"kind\":\"" << kinds[ps.kind] << "\",\"node\":" << ps.node
                   << ",\"in\":" << ps.in << ",\"out\":" << ps.out << "}";
+        }
+        if (s.kind == ST_CONV_PAIR) {
+            o << ",\"out2\":" << s.out2 << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"members\":[";
+            for (size_t m = 0; m < s.members.size(); ++m) {
+                const Step& ms = s.members[m];
+                o << (m ? "," : "") << "{\"node\":" << ms.node << ",\"in\":" << ms.in
+                  << ",\"out\":" << ms.out << ",\"res\":" << ms.res << ",\"conv\":";
+                conv_json(ms);
+                o << "}";
+            }
+            o << "]";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) {
@@ -1113,7 +1162,8 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (block != 16 && block != 32 && block != 64)
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
-                            NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP))
+                            NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP |
+                            NEO_PLAN_FUSE_PAIRS))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -1130,6 +1180,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
@@ -1272,6 +1323,16 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 e = launch_conv_group(shp, n, s.cc, xs, ws, bs, rs, ys, has_pool ? &gp : nullptr, st);
                 break;
             }
+            case ST_CONV_PAIR: {
+                const Step &a = s.members[0], &b = s.members[1];
+                e = launch_conv_pair(a.cs, b.cs, val_ptr(P, a.in, x_nchw, y_out), prm + a.w_off,
+                                     a.b_off >= 0 ? prm + a.b_off : nullptr,
+                                     a.res >= 0 ? val_ptr(P, a.res, x_nchw, y_out) : nullptr,
+                                     val_ptr(P, a.out, x_nchw, y_out), prm + b.w_off,
+                                     b.b_off >= 0 ? prm + b.b_off : nullptr,
+                                     val_ptr(P, b.out, x_nchw, y_out), st);
+                break;
+            }
             case ST_MAXPOOL:
                 e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
@@ -1400,6 +1461,36 @@ static int tune_plan(neo_plan* P) {
                 m.tuned = true;
             }
             next.push_back(keep);
+            continue;
+        }
+        if (s.kind == ST_CONV_PAIR && !s.tuned) {
+            // the pair stays only where it beats its two convs' own best launches
+            const float* prm = P->d_params;
+            Step a = s.members[0], b = s.members[1];
+            const float* ba = a.b_off >= 0 ? prm + a.b_off : nullptr;
+            const float* bb = b.b_off >= 0 ? prm + b.b_off : nullptr;
+            const float* res = a.res >= 0 ? val_ptr(P, a.res, xin, yout) : nullptr;
+            float pair_us = 0.f, a_us = 0.f, b_us = 0.f;
+            rc = tune_conv_pair(a.cs, b.cs, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
+                                val_ptr(P, a.out, xin, yout), prm + b.w_off, bb,
+                                val_ptr(P, b.out, xin, yout), P->cap_stream, &pair_us);
+            if (rc == NEO_OK)
+                rc = tune_conv(a.cs, true, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
+                               val_ptr(P, a.out, xin, yout), P->cap_stream, &a.cc, &a_us);
+            if (rc == NEO_OK)
+                rc = tune_conv(b.cs, true, val_ptr(P, b.in, xin, yout), prm + b.w_off, bb, nullptr,
+                               val_ptr(P, b.out, xin, yout), P->cap_stream, &b.cc, &b_us);
+            if (rc != NEO_OK) break;
+            a.tuned = b.tuned = true;
+            if (pair_us < a_us + b_us) {
+                Step keep = s;
+                keep.members = {a, b};
+                keep.tuned = true;
+                next.push_back(keep);
+            } else {
+                next.push_back(a);
+                next.push_back(b);
+            }
             continue;
         }
         if (s.kind == ST_CONV && !s.tuned) {

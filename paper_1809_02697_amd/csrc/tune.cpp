@@ -100,6 +100,8 @@ namespace {
 using GroupKey = std::pair<std::string, std::vector<int>>;
 std::map<GroupKey, Entry> g_group_db;
 std::map<GroupKey, float> g_pool_db;
+std::map<GroupKey, float> g_pair_db;  // two pointwise convs in one launch -> time
+constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
 constexpr int kPoolShapeInts = 12;   // max N C H W R S sh sw ph pw xb
 
@@ -209,6 +211,39 @@ int tune_conv_group(const ConvShape* s, int n, const float* const* x, const floa
     return NEO_OK;
 }
 
+int tune_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const float* wa,
+                   const float* ba, const float* res, float* y, const float* wb, const float* bb,
+                   float* z, hipStream_t st, float* us_out) {
+    GroupKey key{device_arch(), {}};
+    for (const ConvShape* s : {&a, &b})
+        key.second.insert(key.second.end(), {s->N, s->C, s->H, s->W, s->K, s->R, s->S, s->sh, s->sw,
+                                             s->ph, s->pw});
+    key.second.push_back(res ? 1 : 0);
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_pair_db.find(key);
+        if (it != g_pair_db.end()) {
+            *us_out = it->second;
+            return NEO_OK;
+        }
+    }
+    float us = 0.f;
+    hipError_t e;
+    {
+        Events ev;
+        e = time_launch([&] { return launch_conv_pair(a, b, x, wa, ba, res, y, wb, bb, z, st); }, st,
+                        ev.e0, ev.e1, &us);
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "pair timing");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_pair_db[key] = us;
+    }
+    *us_out = us;
+    return NEO_OK;
+}
+
 int tune_pool(const GroupPool& p, hipStream_t st, float* us_out) {
     const GroupKey key{device_arch(), pool_ints(p)};
     {
@@ -247,8 +282,10 @@ extern "C" {
 // one line per fused launch of n NCHW16c convs and m (0 or 1) pooling steps:
 //   group arch n m (N C H W K R S sh sw ph pw) x n (max N C H W R S sh sw ph pw xb) x m
 //         fk fp split waves us
-// and one line per pooling step timed alone:
+// one line per pooling step timed alone:
 //   pool arch max N C H W R S sh sw ph pw xb us
+// and one line per pair of pointwise convs in one launch:
+//   pair arch (N C H W K R S sh sw ph pw) x 2 residual us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -274,12 +311,14 @@ int neo_tune_db_save(const char* path) {
         f << ' ' << v.cfg.fk << ' ' << v.cfg.fp << ' ' << v.cfg.split << ' ' << v.cfg.waves << ' '
           << v.us << '\n';
     }
-    for (const auto& kv : g_pool_db) {
-        f << "pool " << kv.first.first;
-        for (int x : kv.first.second) f << ' ' << x;
-        f << ' ' << kv.second << '\n';
+    for (const auto* db : {&g_pool_db, &g_pair_db}) {
+        for (const auto& kv : *db) {
+            f << (db == &g_pool_db ? "pool " : "pair ") << kv.first.first;
+            for (int x : kv.first.second) f << ' ' << x;
+            f << ' ' << kv.second << '\n';
+        }
     }
-    return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size())
+    return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -291,7 +330,7 @@ int neo_tune_db_load(const char* path) {
     int n = 0, lineno = 0;
     std::map<Key, Entry> add;
     std::map<GroupKey, Entry> add_group;
-    std::map<GroupKey, float> add_pool;
+    std::map<GroupKey, float> add_pool, add_pair;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -321,6 +360,17 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 5, "pair ") == 0) {
+            std::string tag;
+            GroupKey pk;
+            float us = 0.f;
+            const bool ok = (bool)(is >> tag >> pk.first) && read_ints(is, kPairInts, pk.second) &&
+                            (bool)(is >> us);
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_pair[pk] = us;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -345,6 +395,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add) g_db[kv.first] = kv.second;
     for (const auto& kv : add_group) g_group_db[kv.first] = kv.second;
     for (const auto& kv : add_pool) g_pool_db[kv.first] = kv.second;
+    for (const auto& kv : add_pair) g_pair_db[kv.first] = kv.second;
     return n;
 }
 
@@ -353,11 +404,12 @@ void neo_tune_db_clear(void) {
     g_db.clear();
     g_group_db.clear();
     g_pool_db.clear();
+    g_pair_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
-    return (int)(g_db.size() + g_group_db.size() + g_pool_db.size());
+    return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size());
 }
 
 }  // extern "C"

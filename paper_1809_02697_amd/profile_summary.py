@@ -32,7 +32,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(HERE, "csrc", f)
-               for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip")]
+               for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip")]
 
 
 def kernel_hash():
@@ -65,12 +65,16 @@ def conv_launches(run_dir):
     return launches(json.load(open(os.path.join(run_dir, "tune_db.txt.plan.json"))))
 
 
+def is_conv(name):
+    return "conv2d_mfma" in name or "conv1x1_pair" in name
+
+
 def per_conv(fwd):
-    """Group dispatches into conv launches: a conv2d_mfma dispatch and the
-    split_reduce dispatch that may follow it."""
+    """Group dispatches into conv launches: a conv dispatch (single, fused
+    group or pair) and the split_reduce dispatch that may follow it."""
     out = []
     for name, v in fwd:
-        if "conv2d_mfma" in name:
+        if is_conv(name):
             out.append(v)
         elif "split_reduce" in name and out:
             out[-1] += v
@@ -104,7 +108,7 @@ def main(run_dir):
 
     trace = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_trace.csv"))
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-    conv_d = [dur(r) for r in trace if "conv2d_mfma" in r["Kernel_Name"]]
+    conv_d = [dur(r) for r in trace if is_conv(r["Kernel_Name"])]
     red_d = [dur(r) for r in trace if "split_reduce" in r["Kernel_Name"]]
     trace_avg = (sum(conv_d) + sum(red_d)) / len(conv_d)
     stats = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_stats.csv"))

@@ -26,6 +26,10 @@ def _launch_items(d):
                 yield i, [m["in"]] + ([m["res"]] if m["res"] >= 0 else []), m["out"], m
             if "pool" in s:
                 yield i, [s["pool"]["in"]], s["pool"]["out"], s["pool"]
+        elif s["kind"] == "conv_pair":       # the second conv reads the first's output inside
+            a, b = s["members"]
+            yield i, [a["in"]] + ([a["res"]] if a["res"] >= 0 else []), a["out"], a
+            yield i, [], b["out"], b
         else:
             yield i, [s["in"]] + ([s["res"]] if s["res"] >= 0 else []), s["out"], s
 
