@@ -433,7 +433,7 @@ def main():
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
                         unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4),
                         traffic=measured_traffic(),
-                        kernel="conv2d_blocked (single and fused-group launches)",
+                        kernel="conv2d_blocked (single, fused-group and pointwise-pair launches)",
                         launches_per_step=n_launch,
                         avg_launch_us=round(tot_t / n_launch * 1e6, 2),
                         flop_per_launch=round(tot_f / n_launch))

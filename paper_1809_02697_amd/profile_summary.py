@@ -139,7 +139,7 @@ def main(run_dir):
           "```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
           "## Launch duration", "",
-          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma or conv2d_mfma_group + its "
+          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma, conv2d_mfma_group or conv1x1_pair + its "
           f"split_reduce pass, "
           f"{len(conv_d)} conv dispatches): **{trace_avg:.2f} us**",
           f"- bench.py HIP events (graph replays of each conv step, weighted by use): "
