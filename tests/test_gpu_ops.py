@@ -202,7 +202,8 @@ def test_global_avgpool(neo, N, C, H, W):
                                           (32, 4096, 1000, "none"), (3, 37, 19, "relu"),
                                           (17, 64, 10, "none"), (1, 5, 3, "none"),
                                           (2, 4100, 37, "relu"), (4, 4100, 130, "none"),
-                                          (5, 4096, 33, "relu")])
+                                          (5, 4096, 33, "relu"), (1, 2048, 4099, "relu"),
+                                          (2, 4100, 4096, "none")])
 def test_dense(neo, N, IN, OUT, act):
     rng = np.random.default_rng(IN + OUT)
     x = rng.uniform(-1, 1, (N, IN)).astype(np.float32)
