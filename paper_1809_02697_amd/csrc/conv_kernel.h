@@ -42,7 +42,7 @@
 // channel blocks per step (G = 4 for a 1x1 tile, 2 for a 2-tile one, when G
 // divides the channel blocks), so a step issues 4*G*FK*FP MFMAs for one round
 // of bookkeeping.
-// Loads run D steps ahead of the MFMAs (a register ring sized to the tile), so
+// Loads run D steps ahead of the MFMAs (a register ring of D = 2 slots), so
 // each wave keeps D-1 steps of loads in flight while it computes.  The step
 // bookkeeping is scalar and incremental (see Loader): measured on MI355X, a
 // per-step lane-offset computation, an LDS table or integer divisions per step
@@ -340,13 +340,14 @@ struct Loader {
     }
 };
 
-// Depth of the load ring: as many steps in flight as about 72 VGPRs allow
-// (96 for grouped steps, which are G times longer).
+// Depth of the load ring: two slots, i.e. the next step's operands load
+// while this step's MFMAs run.  Measured on MI355X over every ResNet-50
+// layer, tuned: sizing the ring to ~72 VGPRs (3 to 8 slots) was 7 % slower
+// end to end at batch 1 and 32, twice that budget slower still; the fewer
+// registers a wave holds, the more waves share each SIMD and hide latency.
 template <int FK, int FP, int G>
 constexpr int pipe_depth() {
-    const int regs = 4 * G * (FK + FP);
-    const int d = (G > 1 ? 96 : 72) / regs;
-    return d < 2 ? 2 : (d > 8 ? 8 : d);
+    return 2;
 }
 
 template <int FK, int FP, int G>
