@@ -354,7 +354,8 @@ void neo_plan_destroy(neo_plan* plan);
  * order, input and output block) -> launch configuration and its measured time;
  * (GPU architecture, the shapes of a fused launch's convs and pooling step) -> the
  * launch's configuration and time; (GPU architecture, a pooling step's shape) -> its
- * time alone.  Text file, one entry per line.  save returns the number of entries
+ * time alone; (GPU architecture, the shapes of a pair of pointwise convs, residual) ->
+ * the pair's time in one launch.  Text file, one entry per line.  save returns the number of entries
  * written, load the number read, size the number held (entries are merged; a malformed
  * line fails the whole load with NEO_ERR_INVALID_ARG). */
 int neo_tune_db_save(const char* path);

@@ -280,14 +280,15 @@ def test_tune_db_group_entries(tmp_path):
     grp_pool = ("group gfx950 1 1 1 192 35 35 64 1 1 1 1 0 0 0 1 192 35 35 3 3 1 1 1 1 16 "
                 "1 1 1 2 5.5")
     pool = "pool gfx950 0 1 192 35 35 3 3 1 1 1 1 16 3.125"
+    pair = "pair gfx950 1 64 56 56 256 1 1 1 1 0 0 1 256 56 56 64 1 1 1 1 0 0 1 6.0625"
     p.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 2 2 1 4 7.5\n" + grp + "\n" + grp_pool +
-                 "\n" + pool + "\n")
-    assert neo.tune_db_load(p) == 4
-    assert neo.tune_db_size() == 4
+                 "\n" + pool + "\n" + pair + "\n")
+    assert neo.tune_db_load(p) == 5
+    assert neo.tune_db_size() == 5
     q = tmp_path / "out.txt"
-    assert neo.tune_db_save(q) == 4
+    assert neo.tune_db_save(q) == 5
     lines = q.read_text().splitlines()
-    for want in (grp, grp_pool, pool):
+    for want in (grp, grp_pool, pool, pair):
         got = [l for l in lines if l.split()[:-1] == want.split()[:-1]]
         assert len(got) == 1 and float(got[0].split()[-1]) == float(want.split()[-1])
     bad = tmp_path / "bad.txt"
@@ -296,7 +297,8 @@ def test_tune_db_group_entries(tmp_path):
                  grp.replace("gfx950 2 0 ", "gfx950 2 2 "),            # at most one pool
                  grp.rsplit(" ", 3)[0],                               # truncated
                  pool.replace(" 16 3.125", " 12 3.125"),              # no 12-channel block
-                 pool.rsplit(" ", 2)[0]):                             # truncated
+                 pool.rsplit(" ", 2)[0],                              # truncated
+                 pair.rsplit(" ", 2)[0]):                             # truncated
         bad.write_text(line + "\n")
         with pytest.raises(neo.NeoError):
             neo.tune_db_load(bad)
