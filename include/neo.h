@@ -289,8 +289,8 @@ enum neo_plan_flags {
     NEO_PLAN_FUSE_GAP = 64,
     /* Run a pointwise conv and a later pointwise conv that reads its output
      * (1x1, stride 1, NCHW16c; the second without a residual) as one launch
-     * where a kernel exists for the pair's channel counts (64 -> 256 -> 64:
-     * a bottleneck's expanding conv and the next one's reducing conv): each
+     * where a kernel exists for the pair's channel counts (64 -> 256 -> 64 or
+     * 128: a bottleneck's expanding conv and the next one's reducing conv): each
      * workgroup keeps the first conv's output for its 16 pixels in LDS and
      * still stores it.  With NEO_PLAN_TUNE a pair is kept only where it
      * measures faster than its two convs alone.  Not in the paper. */

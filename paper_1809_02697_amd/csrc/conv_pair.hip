@@ -132,8 +132,10 @@ hipError_t launch_pair_t(const PairArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-// The channel-group counts (ceil(C_a/16), ceil(K_a/16), ceil(K_b/16)) with a kernel.
-bool pair_blocks(int cab, int kab, int kbb) { return cab == 4 && kab == 16 && kbb == 4; }
+// The channel-group counts (ceil(C_a/16), ceil(K_a/16), ceil(K_b/16)) with a
+// kernel: 64 -> 256 -> 64 (inside a bottleneck stage) and 64 -> 256 -> 128
+// (into the next stage's first reducing conv).
+bool pair_blocks(int cab, int kab, int kbb) { return cab == 4 && kab == 16 && (kbb == 4 || kbb == 8); }
 
 bool pointwise(const ConvShape& s) {
     return s.R == 1 && s.S == 1 && s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0 && s.xb == 16 &&
@@ -153,6 +155,7 @@ hipError_t launch_conv_pair(const ConvShape& sa, const ConvShape& sb, const floa
     if (!conv_pair_eligible(sa, sb)) return hipErrorInvalidValue;
     if ((long)sa.N * sa.OH * sa.OW * cdiv(sa.K, 16) * 16 >= (1L << 29)) return hipErrorInvalidValue;
     const PairArgs a{x, wa, ba, res, y, wb, bb, z, sa.OH * sa.OW, sa.N * sa.OH * sa.OW, sa.act, sb.act};
+    if (cdiv(sb.K, 16) == 8) return launch_pair_t<8, 4, 16, 8>(a, st);
     return launch_pair_t<8, 4, 16, 4>(a, st);
 }
 

@@ -125,8 +125,9 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
 
 // Two pointwise convolutions in one launch (conv_pair.hip): a (1x1 stride 1,
 // NCHW16c, optional residual) whose output y = b's input is also stored, then
-// b (1x1 stride 1, no residual).  Shapes with a kernel: 64 -> 256 -> 64
-// channels (ceil(C/16) = 4, 16, 4).  Filters in kernel order.
+// b (1x1 stride 1, no residual).  Shapes with a kernel: 64 -> 256 -> 64 and
+// 64 -> 256 -> 128 channels (ceil(C/16) = 4, 16, 4 or 8).  Filters in kernel
+// order.
 bool conv_pair_eligible(const ConvShape& a, const ConvShape& b);
 hipError_t launch_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const float* wa,
                             const float* ba, const float* res, float* y, const float* wb,

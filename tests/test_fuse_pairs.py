@@ -46,7 +46,8 @@ def _valid_order(d):
 def test_resnet50_pairs_at_the_64_channel_width(flags):
     g = nets.resnet50()
     d = _plan(g, flags)
-    assert _pairs(g, d) == [["layer1.0.conv3", "layer1.1.conv1"], ["layer1.1.conv3", "layer1.2.conv1"]]
+    assert _pairs(g, d) == [["layer1.0.conv3", "layer1.1.conv1"], ["layer1.1.conv3", "layer1.2.conv1"],
+                            ["layer1.2.conv3", "layer2.0.conv1"]]
     launched = sorted(m["node"] for s in d["steps"]
                       for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair")
                                 else [s] if s["kind"] == "conv" else []))
@@ -80,6 +81,7 @@ def test_pair_graph_pairs():
     g = pair_graph()
     assert _pairs(g, _plan(g)) == [["a", "b"]]
     assert _pairs(pair_graph(Ca=80), _plan(pair_graph(Ca=80))) == []   # no kernel for 80 -> 256
+    assert _pairs(pair_graph(Kb=96), _plan(pair_graph(Kb=96))) == []   # nor for 256 -> 96
 
 
 # ---- GPU ---------------------------------------------------------------------------------
@@ -102,7 +104,8 @@ def _run(g, flags):
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("Ca,Ka,Kb,N,hw", [(64, 256, 64, 1, 9), (50, 250, 60, 2, 9),
-                                           (64, 256, 64, 2, 56), (49, 241, 49, 1, 5)])
+                                           (64, 256, 64, 2, 56), (49, 241, 49, 1, 5),
+                                           (64, 256, 128, 1, 56), (50, 250, 120, 2, 9)])
 def test_pair_matches_oracle_and_unpaired(gneo, Ca, Ka, Kb, N, hw):
     """Ragged channel counts inside the kernel's blocks, two images whose
     pixels share a 16-pixel tile (81 = 5 * 16 + 1), the 56 x 56 map."""
@@ -172,4 +175,4 @@ def test_resnet50_pairs_tuned_replayed(gneo, tmp_path):
         t = pairs[(_shape(a["conv"]), _shape(b["conv"]), int(a["res"] >= 0))]
         faster = t < convs[_shape(a["conv"])] + convs[_shape(b["conv"])]
         assert ((a["node"], b["node"]) in kept) == faster
-    print(f"\n{len(kept)} of 2 pairs kept")
+    print(f"\n{len(kept)} of 3 pairs kept")
