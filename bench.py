@@ -29,8 +29,8 @@ Printed JSON line:
                (one block for every conv, transforms only at the ends) and
                "searched" (the global layout search); plus "grouped" (the
                eliminated plan with independent convs fused into launches, pools
-               riding along, a global pool folded into its neighbours, and
-               pairs of pointwise convs fused); all
+               riding along, a global pool folded into its neighbours, pairs
+               of pointwise convs and 3x3-led chains fused); all
                with tuned launch configurations
   cpu_baseline the CPU oracle timed on this host on a bounded sample
 """
@@ -66,7 +66,7 @@ def plan_schemes(desc):
     """{conv node: (ic_bn, oc_bn)} of a plan description."""
     out = {}
     for s in desc["steps"]:
-        for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair")
+        for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair", "conv_chain")
                   else [s] if s["kind"] == "conv" else []):
             out[m["node"]] = (m["conv"]["ic_bn"], m["conv"]["oc_bn"])
     return out
@@ -77,15 +77,16 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     (Section 3.3.2) chooses every conv's scheme from per-conv times measured
     in isolation; the resulting plan and the one-block plan (Section 3.2, all
     convs in NCHW16c) -- both with independent convs fused into launches,
-    the global pool folded into the last conv and the dense layer, and pairs
-    of pointwise convs in one launch --
+    the global pool folded into the last conv and the dense layer, pairs
+    of pointwise convs and 3x3-led chains in one launch --
     are then both timed end to end and the faster is kept,
     so a search decision that the isolated timings mispredict cannot make the
     step slower.  With a results file from an earlier run (``--tune-db``) the
     schemes that run kept are reused from ``<file>.schemes.json`` (so a
     profiling run executes the same plan)."""
     path = (tune_db or "") + ".schemes.json"
-    base = neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS
+    base = (neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS |
+            neo.PLAN_FUSE_CHAINS)
     if tune_db and os.path.exists(path):
         sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
         return neo.Plan(g, flags=neo.PLAN_TUNE | base, schemes=sch), {"from": path}
@@ -120,9 +121,14 @@ def conv_launches(desc):
             out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
                         dict(tile=s["tile"], split=1, waves=s["waves"], ic_bn=16, oc_bn=16,
                              group=len(s["members"]))))
-        elif s["kind"] == "conv_pair":
-            out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
-                        dict(pair=True, split=1, waves=8, ic_bn=16, oc_bn=16)))
+        elif s["kind"] in ("conv_pair", "conv_chain"):
+            # every conv after the first reads its input from LDS; a chain's
+            # 3x3 output stays there and is never stored
+            chain = s["kind"] == "conv_chain"
+            ms = [(dict(m["conv"], lds_in=j > 0, lds_out=chain and j == 0), m["res"] >= 0)
+                  for j, m in enumerate(s["members"])]
+            out.append((i, ms, dict(chain=True, split=1, waves=8, ic_bn=16, oc_bn=16) if chain
+                        else dict(pair=True, split=1, waves=8, ic_bn=16, oc_bn=16)))
     return out
 
 
@@ -134,6 +140,10 @@ def launch_costs(members):
                                     c["pad"], N=c["N"], residual=res)
         if c.get("gap_sums"):   # writes per-16-pixel channel sums, not its outputs
             bb += 4 * c["K"] * (-(-OH * OW // 16) - OH * OW)
+        if c.get("lds_in"):     # a pointwise input read from LDS (the launch computed it)
+            bb -= 4 * c["N"] * c["C"] * OH * OW
+        if c.get("lds_out"):    # an output kept in LDS only
+            bb -= 4 * c["N"] * c["K"] * OH * OW
         f, b = f + ff, b + bb
     return f, b
 
@@ -309,7 +319,7 @@ def model_latencies(neo, torch, wl, steps):
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        fused = neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS
+        fused = neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS | neo.PLAN_FUSE_CHAINS
         plans = [("eliminated", 0, 16), ("grouped", fused, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
@@ -433,7 +443,7 @@ def main():
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
                         unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4),
                         traffic=measured_traffic(),
-                        kernel="conv2d_blocked (single, fused-group and pointwise-pair launches)",
+                        kernel="conv2d_blocked (single, fused-group, pointwise-pair and 3x3-chain launches)",
                         launches_per_step=n_launch,
                         avg_launch_us=round(tot_t / n_launch * 1e6, 2),
                         flop_per_launch=round(tot_f / n_launch))

@@ -294,7 +294,18 @@ enum neo_plan_flags {
      * workgroup keeps the first conv's output for its 16 pixels in LDS and
      * still stores it.  With NEO_PLAN_TUNE a pair is kept only where it
      * measures faster than its two convs alone.  Not in the paper. */
-    NEO_PLAN_FUSE_PAIRS = 128
+    NEO_PLAN_FUSE_PAIRS = 128,
+    /* Run a 3x3 conv (stride 1, pad 1, 64 -> 64 channels, no residual) whose
+     * output only a pointwise conv reads, with that conv and, when the
+     * pointwise conv is the first of a pair (NEO_PLAN_FUSE_PAIRS), the pair's
+     * second conv, as one launch: a ResNet bottleneck's 3x3, its expanding
+     * 1x1 with the residual and the next bottleneck's reducing 1x1 at the
+     * 64-channel width.  The 3x3's output stays in LDS and is never stored.
+     * With NEO_PLAN_TUNE a chain is kept only where it measures faster than
+     * the 3x3 alone plus the best launches of the rest.  Results match the
+     * oracle but are not bit-identical to an unchained plan's (the 3x3's sums
+     * run in another order).  Not in the paper. */
+    NEO_PLAN_FUSE_CHAINS = 256
 };
 
 /*
@@ -355,7 +366,8 @@ void neo_plan_destroy(neo_plan* plan);
  * (GPU architecture, the shapes of a fused launch's convs and pooling step) -> the
  * launch's configuration and time; (GPU architecture, a pooling step's shape) -> its
  * time alone; (GPU architecture, the shapes of a pair of pointwise convs, residual) ->
- * the pair's time in one launch.  Text file, one entry per line.  save returns the number of entries
+ * the pair's time in one launch; (GPU architecture, the shapes of a 3x3-led chain of two
+ * or three convs, residual) -> the chain's time in one launch.  Text file, one entry per line.  save returns the number of entries
  * written, load the number read, size the number held (entries are merged; a malformed
  * line fails the whole load with NEO_ERR_INVALID_ARG). */
 int neo_tune_db_save(const char* path);

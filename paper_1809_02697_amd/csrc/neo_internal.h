@@ -137,6 +137,19 @@ int tune_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const
                    const float* ba, const float* res, float* y, const float* wb, const float* bb,
                    float* z, hipStream_t st, float* us);
 
+// A 3x3 convolution, the pointwise expansion that reads its output and,
+// with n = 3, the pointwise reduction after it, in one launch (conv_pair.hip):
+// s[0] 3x3 stride 1 pad 1, 64 -> 64 channels (4 blocks each), no residual,
+// its output never stored; s[1] 64 -> 256 1x1 with optional residual, its
+// output y stored; s[2] as the second conv of a pair, output z.
+bool conv_chain_eligible(const ConvShape* s, int n);
+hipError_t launch_conv_chain(const ConvShape* s, int n, const float* x, const float* w0, const float* b0,
+                             const float* wa, const float* ba, const float* res, float* y,
+                             const float* wb, const float* bb, float* z, hipStream_t st);
+int tune_conv_chain(const ConvShape* s, int n, const float* x, const float* w0, const float* b0,
+                    const float* wa, const float* ba, const float* res, float* y, const float* wb,
+                    const float* bb, float* z, hipStream_t st, float* us);
+
 // ---- timing (local search, global search) ----------------------------------------------
 // Time per launch of `launch` on `st` (a stream that is not the legacy null
 // stream): one warm-up launch (it also surfaces a launch error before

@@ -40,7 +40,7 @@ using namespace neo;
 namespace {
 
 enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY, ST_CONV_GROUP,
-                ST_CONV_PAIR };
+                ST_CONV_PAIR, ST_CONV_CHAIN };
 
 struct Val {
     int N = 0, C = 0, H = 0, W = 0;
@@ -60,7 +60,8 @@ struct Step {
     int kind;
     int node;         // originating node (transforms: the consumer that needed it)
     int in = -1, out = -1, res = -1;
-    int out2 = -1;    // ST_CONV_PAIR: the second conv's output (out is the first's)
+    int out2 = -1;    // ST_CONV_PAIR: the second conv's output (out is the first's);
+                      // ST_CONV_CHAIN: the third conv's output, if any (out is the second's)
     ConvShape cs{};
     ConvConfig cc{1, 1, 1, 4};
     bool tuned = false;
@@ -73,7 +74,8 @@ struct Step {
     int gap_parts = 0, gap_stride = 0;
     float gap_scale = 1.f;
     std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's);
-                                // ST_CONV_PAIR: the two convs, in order
+                                // ST_CONV_PAIR: the two convs, in order;
+                                // ST_CONV_CHAIN: the 3x3 and the one or two pointwise convs
     std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1)
 };
 
@@ -835,6 +837,53 @@ void fuse_pairs(neo_plan* P) {
     S.swap(out);
 }
 
+// NEO_PLAN_FUSE_CHAINS: a 3x3 conv whose output only a pointwise conv reads
+// (alone, or as the first of a pair) runs with it in one launch where a
+// kernel exists for the channel counts (conv_chain_eligible), at the
+// pointwise step's place; the 3x3's output is then never stored.  Tuning
+// splits a chain that measures slower than its parts.
+void fuse_chains(neo_plan* P) {
+    std::vector<Step>& S = P->steps;
+    std::vector<char> drop(S.size(), 0);
+    for (size_t j = 0; j < S.size(); ++j) {
+        Step& X = S[j];
+        std::vector<Step> tail;
+        if (X.kind == ST_CONV_PAIR)
+            tail = X.members;
+        else if (X.kind == ST_CONV)
+            tail = {X};
+        else
+            continue;
+        const int v = tail[0].in;
+        const Val& mv = P->vals[v];
+        if (mv.buf == kExtIn || mv.view || mv.alias_of >= 0 || mv.consumers != 1) continue;
+        for (size_t i = 0; i < j; ++i) {
+            if (drop[i] || S[i].kind != ST_CONV || S[i].out != v || S[i].res >= 0) continue;
+            ConvShape shp[3];
+            shp[0] = S[i].cs;
+            for (size_t m = 0; m < tail.size(); ++m) shp[m + 1] = tail[m].cs;
+            const int n = 1 + (int)tail.size();
+            if (!conv_chain_eligible(shp, n)) break;
+            Step ch{};
+            ch.kind = ST_CONV_CHAIN;
+            ch.node = S[i].node;
+            ch.in = S[i].in;
+            ch.res = tail[0].res;
+            ch.out = tail[0].out;
+            ch.out2 = n == 3 ? tail[1].out : -1;
+            ch.members = {S[i]};
+            ch.members.insert(ch.members.end(), tail.begin(), tail.end());
+            X = ch;
+            drop[i] = 1;
+            break;
+        }
+    }
+    std::vector<Step> out;
+    for (size_t j = 0; j < S.size(); ++j)
+        if (!drop[j]) out.push_back(S[j]);
+    S.swap(out);
+}
+
 float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     const Val& val = P->vals[v];
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
@@ -890,7 +939,7 @@ std::string describe(const neo_plan* P) {
     }
     o << "],\"n_transforms\":" << P->xforms.size() << ",\"steps\":[";
     static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy",
-                                  "conv_group", "conv_pair"};
+                                  "conv_group", "conv_pair", "conv_chain"};
     for (size_t i = 0; i < P->steps.size(); ++i) {
         const Step& s = P->steps[i];
         o << (i ? "," : "") << "{\"kind\":\"" << kinds[s.kind] << "\",\"node\":" << s.node
@@ -927,7 +976,7 @@ std::string describe(const neo_plan* P) {
                 o << ",\"pool\":{\"kind\":\"" << kinds[ps.kind] << "\",\"node\":" << ps.node
                   << ",\"in\":" << ps.in << ",\"out\":" << ps.out << "}";
         }
-        if (s.kind == ST_CONV_PAIR) {
+        if (s.kind == ST_CONV_PAIR || s.kind == ST_CONV_CHAIN) {
             o << ",\"out2\":" << s.out2 << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"members\":[";
             for (size_t m = 0; m < s.members.size(); ++m) {
                 const Step& ms = s.members[m];
@@ -1163,7 +1212,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
                             NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP |
-                            NEO_PLAN_FUSE_PAIRS))
+                            NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -1181,6 +1230,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK) rc = build_steps(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
@@ -1333,6 +1383,20 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                                      val_ptr(P, b.out, x_nchw, y_out), st);
                 break;
             }
+            case ST_CONV_CHAIN: {
+                const int n = (int)s.members.size();
+                ConvShape shp[3];
+                for (int m = 0; m < n; ++m) shp[m] = s.members[m].cs;
+                const Step &c = s.members[0], &a = s.members[1], &b = s.members[n - 1];
+                e = launch_conv_chain(shp, n, val_ptr(P, c.in, x_nchw, y_out), prm + c.w_off,
+                                      c.b_off >= 0 ? prm + c.b_off : nullptr, prm + a.w_off,
+                                      a.b_off >= 0 ? prm + a.b_off : nullptr,
+                                      a.res >= 0 ? val_ptr(P, a.res, x_nchw, y_out) : nullptr,
+                                      val_ptr(P, a.out, x_nchw, y_out), n == 3 ? prm + b.w_off : nullptr,
+                                      n == 3 && b.b_off >= 0 ? prm + b.b_off : nullptr,
+                                      n == 3 ? val_ptr(P, b.out, x_nchw, y_out) : nullptr, st);
+                break;
+            }
             case ST_MAXPOOL:
                 e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
@@ -1396,6 +1460,39 @@ static int tune_plan(neo_plan* P) {
     if (e == hipSuccess) e = hipMalloc(&yout, std::max<size_t>((size_t)out.N * out.C * out.H * out.W * 4, 256));
     if (e == hipSuccess) e = hipMemset(xin, 0, (size_t)in.N * in.C * in.H * in.W * 4);
     int rc = e == hipSuccess ? NEO_OK : fail(NEO_ERR_OOM, "neo_plan_create: tuning buffers");
+    // a pair stays only where it beats its two convs' own best launches;
+    // appends what runs (the pair, or the two convs) and its time
+    auto tune_pair = [&](const Step& s, std::vector<Step>& emit, float* us_out) -> int {
+        const float* prm = P->d_params;
+        Step a = s.members[0], b = s.members[1];
+        const float* ba = a.b_off >= 0 ? prm + a.b_off : nullptr;
+        const float* bb = b.b_off >= 0 ? prm + b.b_off : nullptr;
+        const float* res = a.res >= 0 ? val_ptr(P, a.res, xin, yout) : nullptr;
+        float pair_us = 0.f, a_us = 0.f, b_us = 0.f;
+        int r = tune_conv_pair(a.cs, b.cs, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
+                               val_ptr(P, a.out, xin, yout), prm + b.w_off, bb,
+                               val_ptr(P, b.out, xin, yout), P->cap_stream, &pair_us);
+        if (r == NEO_OK)
+            r = tune_conv(a.cs, true, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
+                          val_ptr(P, a.out, xin, yout), P->cap_stream, &a.cc, &a_us);
+        if (r == NEO_OK)
+            r = tune_conv(b.cs, true, val_ptr(P, b.in, xin, yout), prm + b.w_off, bb, nullptr,
+                          val_ptr(P, b.out, xin, yout), P->cap_stream, &b.cc, &b_us);
+        if (r != NEO_OK) return r;
+        a.tuned = b.tuned = true;
+        if (pair_us < a_us + b_us) {
+            Step keep = s;
+            keep.members = {a, b};
+            keep.tuned = true;
+            emit.push_back(keep);
+            *us_out = pair_us;
+        } else {
+            emit.push_back(a);
+            emit.push_back(b);
+            *us_out = a_us + b_us;
+        }
+        return NEO_OK;
+    };
     std::vector<Step> next;
     for (Step& s : P->steps) {
         if (rc != NEO_OK) break;
@@ -1464,32 +1561,58 @@ static int tune_plan(neo_plan* P) {
             continue;
         }
         if (s.kind == ST_CONV_PAIR && !s.tuned) {
-            // the pair stays only where it beats its two convs' own best launches
+            float us = 0.f;
+            rc = tune_pair(s, next, &us);
+            continue;
+        }
+        if (s.kind == ST_CONV_CHAIN && !s.tuned) {
+            // the chain stays only where it beats the 3x3's own best launch
+            // plus the best of the rest (the pair, or its convs alone)
             const float* prm = P->d_params;
-            Step a = s.members[0], b = s.members[1];
+            const int n = (int)s.members.size();
+            ConvShape shp[3];
+            for (int m = 0; m < n; ++m) shp[m] = s.members[m].cs;
+            Step c = s.members[0];
+            const Step &a = s.members[1], &b = s.members[n - 1];
             const float* ba = a.b_off >= 0 ? prm + a.b_off : nullptr;
-            const float* bb = b.b_off >= 0 ? prm + b.b_off : nullptr;
             const float* res = a.res >= 0 ? val_ptr(P, a.res, xin, yout) : nullptr;
-            float pair_us = 0.f, a_us = 0.f, b_us = 0.f;
-            rc = tune_conv_pair(a.cs, b.cs, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
-                                val_ptr(P, a.out, xin, yout), prm + b.w_off, bb,
-                                val_ptr(P, b.out, xin, yout), P->cap_stream, &pair_us);
+            float chain_us = 0.f, c_us = 0.f, rest_us = 0.f;
+            rc = tune_conv_chain(shp, n, val_ptr(P, c.in, xin, yout), prm + c.w_off,
+                                 c.b_off >= 0 ? prm + c.b_off : nullptr, prm + a.w_off, ba, res,
+                                 val_ptr(P, a.out, xin, yout), n == 3 ? prm + b.w_off : nullptr,
+                                 n == 3 && b.b_off >= 0 ? prm + b.b_off : nullptr,
+                                 n == 3 ? val_ptr(P, b.out, xin, yout) : nullptr, P->cap_stream, &chain_us);
             if (rc == NEO_OK)
-                rc = tune_conv(a.cs, true, val_ptr(P, a.in, xin, yout), prm + a.w_off, ba, res,
-                               val_ptr(P, a.out, xin, yout), P->cap_stream, &a.cc, &a_us);
-            if (rc == NEO_OK)
-                rc = tune_conv(b.cs, true, val_ptr(P, b.in, xin, yout), prm + b.w_off, bb, nullptr,
-                               val_ptr(P, b.out, xin, yout), P->cap_stream, &b.cc, &b_us);
+                rc = tune_conv(c.cs, true, val_ptr(P, c.in, xin, yout), prm + c.w_off,
+                               c.b_off >= 0 ? prm + c.b_off : nullptr, nullptr, val_ptr(P, c.out, xin, yout),
+                               P->cap_stream, &c.cc, &c_us);
+            std::vector<Step> rest;
+            if (rc == NEO_OK && n == 3) {
+                Step pr = s;
+                pr.kind = ST_CONV_PAIR;
+                pr.node = a.node;
+                pr.in = a.in;
+                pr.out2 = b.out;
+                pr.members = {a, b};
+                rc = tune_pair(pr, rest, &rest_us);
+            } else if (rc == NEO_OK) {
+                Step e1 = a;
+                rc = tune_conv(e1.cs, true, val_ptr(P, e1.in, xin, yout), prm + e1.w_off, ba, res,
+                               val_ptr(P, e1.out, xin, yout), P->cap_stream, &e1.cc, &rest_us);
+                e1.tuned = true;
+                rest.push_back(e1);
+            }
             if (rc != NEO_OK) break;
-            a.tuned = b.tuned = true;
-            if (pair_us < a_us + b_us) {
+            c.tuned = true;
+            if (chain_us < c_us + rest_us) {
                 Step keep = s;
-                keep.members = {a, b};
                 keep.tuned = true;
+                keep.members[0] = c;
+                for (size_t m = 1; m < keep.members.size(); ++m) keep.members[m].tuned = true;
                 next.push_back(keep);
             } else {
-                next.push_back(a);
-                next.push_back(b);
+                next.push_back(c);
+                next.insert(next.end(), rest.begin(), rest.end());
             }
             continue;
         }

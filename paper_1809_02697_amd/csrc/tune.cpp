@@ -101,6 +101,7 @@ using GroupKey = std::pair<std::string, std::vector<int>>;
 std::map<GroupKey, Entry> g_group_db;
 std::map<GroupKey, float> g_pool_db;
 std::map<GroupKey, float> g_pair_db;  // two pointwise convs in one launch -> time
+std::map<GroupKey, float> g_chain_db;  // a 3x3-led chain of 2 or 3 convs in one launch -> time
 constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
 constexpr int kPoolShapeInts = 12;   // max N C H W R S sh sw ph pw xb
@@ -244,6 +245,39 @@ int tune_conv_pair(const ConvShape& a, const ConvShape& b, const float* x, const
     return NEO_OK;
 }
 
+int tune_conv_chain(const ConvShape* s, int n, const float* x, const float* w0, const float* b0,
+                    const float* wa, const float* ba, const float* res, float* y, const float* wb,
+                    const float* bb, float* z, hipStream_t st, float* us_out) {
+    GroupKey key{device_arch(), {}};
+    for (int m = 0; m < n; ++m)
+        key.second.insert(key.second.end(), {s[m].N, s[m].C, s[m].H, s[m].W, s[m].K, s[m].R, s[m].S,
+                                             s[m].sh, s[m].sw, s[m].ph, s[m].pw});
+    key.second.push_back(res ? 1 : 0);
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_chain_db.find(key);
+        if (it != g_chain_db.end()) {
+            *us_out = it->second;
+            return NEO_OK;
+        }
+    }
+    float us = 0.f;
+    hipError_t e;
+    {
+        Events ev;
+        e = time_launch([&] { return launch_conv_chain(s, n, x, w0, b0, wa, ba, res, y, wb, bb, z, st); },
+                        st, ev.e0, ev.e1, &us);
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "chain timing");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_chain_db[key] = us;
+    }
+    *us_out = us;
+    return NEO_OK;
+}
+
 int tune_pool(const GroupPool& p, hipStream_t st, float* us_out) {
     const GroupKey key{device_arch(), pool_ints(p)};
     {
@@ -284,8 +318,10 @@ extern "C" {
 //         fk fp split waves us
 // one line per pooling step timed alone:
 //   pool arch max N C H W R S sh sw ph pw xb us
-// and one line per pair of pointwise convs in one launch:
+// one line per pair of pointwise convs in one launch:
 //   pair arch (N C H W K R S sh sw ph pw) x 2 residual us
+// and one line per 3x3-led chain of n (2 or 3) convs in one launch:
+//   chain arch n (N C H W K R S sh sw ph pw) x n residual us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -318,7 +354,13 @@ int neo_tune_db_save(const char* path) {
             f << ' ' << kv.second << '\n';
         }
     }
-    return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size())
+    for (const auto& kv : g_chain_db) {
+        f << "chain " << kv.first.first << ' ' << kv.first.second.size() / kGroupShapeInts;
+        for (int x : kv.first.second) f << ' ' << x;
+        f << ' ' << kv.second << '\n';
+    }
+    return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
+                     g_chain_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -330,7 +372,7 @@ int neo_tune_db_load(const char* path) {
     int n = 0, lineno = 0;
     std::map<Key, Entry> add;
     std::map<GroupKey, Entry> add_group;
-    std::map<GroupKey, float> add_pool, add_pair;
+    std::map<GroupKey, float> add_pool, add_pair, add_chain;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -371,6 +413,18 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 6, "chain ") == 0) {
+            std::string tag;
+            GroupKey ck;
+            int convs = 0;
+            float us = 0.f;
+            const bool ok = (bool)(is >> tag >> ck.first >> convs) && (convs == 2 || convs == 3) &&
+                            read_ints(is, convs * kGroupShapeInts + 1, ck.second) && (bool)(is >> us);
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_chain[ck] = us;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -396,6 +450,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add_group) g_group_db[kv.first] = kv.second;
     for (const auto& kv : add_pool) g_pool_db[kv.first] = kv.second;
     for (const auto& kv : add_pair) g_pair_db[kv.first] = kv.second;
+    for (const auto& kv : add_chain) g_chain_db[kv.first] = kv.second;
     return n;
 }
 
@@ -405,11 +460,13 @@ void neo_tune_db_clear(void) {
     g_group_db.clear();
     g_pool_db.clear();
     g_pair_db.clear();
+    g_chain_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
-    return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size());
+    return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
+                 g_chain_db.size());
 }
 
 }  // extern "C"

@@ -31,6 +31,7 @@ PLAN_GLOBAL_SEARCH = 16
 PLAN_GROUP = 32
 PLAN_FUSE_GAP = 64
 PLAN_FUSE_PAIRS = 128
+PLAN_FUSE_CHAINS = 256
 BLOCK = 16
 SEARCH_BLOCKS = (0, 4, 8, 16, 32, 64)   # layout index space of neo_layout_search
 

@@ -66,12 +66,12 @@ def conv_launches(run_dir):
 
 
 def is_conv(name):
-    return "conv2d_mfma" in name or "conv1x1_pair" in name
+    return "conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name
 
 
 def per_conv(fwd):
     """Group dispatches into conv launches: a conv dispatch (single, fused
-    group or pair) and the split_reduce dispatch that may follow it."""
+    group, pair or chain) and the split_reduce dispatch that may follow it."""
     out = []
     for name, v in fwd:
         if is_conv(name):
@@ -139,7 +139,7 @@ def main(run_dir):
           "```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
           "## Launch duration", "",
-          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma, conv2d_mfma_group or conv1x1_pair + its "
+          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma, conv2d_mfma_group, conv1x1_pair or conv3x3_chain + its "
           f"split_reduce pass, "
           f"{len(conv_d)} conv dispatches): **{trace_avg:.2f} us**",
           f"- bench.py HIP events (graph replays of each conv step, weighted by use): "

@@ -281,14 +281,17 @@ def test_tune_db_group_entries(tmp_path):
                 "1 1 1 2 5.5")
     pool = "pool gfx950 0 1 192 35 35 3 3 1 1 1 1 16 3.125"
     pair = "pair gfx950 1 64 56 56 256 1 1 1 1 0 0 1 256 56 56 64 1 1 1 1 0 0 1 6.0625"
+    chain3 = ("chain gfx950 3 1 64 56 56 64 3 3 1 1 1 1 1 64 56 56 256 1 1 1 1 0 0 "
+              "1 256 56 56 64 1 1 1 1 0 0 1 8.5")
+    chain2 = "chain gfx950 2 1 64 56 56 64 3 3 1 1 1 1 1 64 56 56 256 1 1 1 1 0 0 1 7.25"
     p.write_text("gfx950 1 64 56 56 64 3 3 1 1 1 1 1 16 16 2 2 1 4 7.5\n" + grp + "\n" + grp_pool +
-                 "\n" + pool + "\n" + pair + "\n")
-    assert neo.tune_db_load(p) == 5
-    assert neo.tune_db_size() == 5
+                 "\n" + pool + "\n" + pair + "\n" + chain3 + "\n" + chain2 + "\n")
+    assert neo.tune_db_load(p) == 7
+    assert neo.tune_db_size() == 7
     q = tmp_path / "out.txt"
-    assert neo.tune_db_save(q) == 5
+    assert neo.tune_db_save(q) == 7
     lines = q.read_text().splitlines()
-    for want in (grp, grp_pool, pool, pair):
+    for want in (grp, grp_pool, pool, pair, chain3, chain2):
         got = [l for l in lines if l.split()[:-1] == want.split()[:-1]]
         assert len(got) == 1 and float(got[0].split()[-1]) == float(want.split()[-1])
     bad = tmp_path / "bad.txt"
@@ -298,7 +301,10 @@ def test_tune_db_group_entries(tmp_path):
                  grp.rsplit(" ", 3)[0],                               # truncated
                  pool.replace(" 16 3.125", " 12 3.125"),              # no 12-channel block
                  pool.rsplit(" ", 2)[0],                              # truncated
-                 pair.rsplit(" ", 2)[0]):                             # truncated
+                 pair.rsplit(" ", 2)[0],                              # truncated
+                 chain3.replace("gfx950 3 ", "gfx950 4 "),             # 2 or 3 convs
+                 chain2.replace("gfx950 2 ", "gfx950 3 "),             # count and fields disagree
+                 chain3.rsplit(" ", 2)[0]):                           # truncated
         bad.write_text(line + "\n")
         with pytest.raises(neo.NeoError):
             neo.tune_db_load(bad)

@@ -30,6 +30,12 @@ def _launch_items(d):
             a, b = s["members"]
             yield i, [a["in"]] + ([a["res"]] if a["res"] >= 0 else []), a["out"], a
             yield i, [], b["out"], b
+        elif s["kind"] == "conv_chain":      # the 3x3's output stays inside, never stored
+            c, a = s["members"][:2]
+            yield i, [c["in"]], -1, c
+            yield i, [a["res"]] if a["res"] >= 0 else [], a["out"], a
+            for b in s["members"][2:]:
+                yield i, [], b["out"], b
         else:
             yield i, [s["in"]] + ([s["res"]] if s["res"] >= 0 else []), s["out"], s
 
