@@ -264,14 +264,16 @@ def engine_clock(torch=None, plan=None, x=None, out=None, busy_runs=4000):
 
 def layer_table(torch, plan, x, out, reps, cold=True):
     """Each conv step of the plan timed alone (its kernel(s) as the plan
-    launches them), grouped by distinct shape."""
+    launches them), grouped by distinct shapes, residuals and launch
+    configuration."""
     d = plan.describe()
     plan.run(x, out)      # intermediate buffers hold real activations
     torch.cuda.synchronize()
     rows = {}
     for i, members, cfg in conv_launches(d):
         key = tuple((c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"],
-                     c["W"], c["N"], c["ic_bn"], c["oc_bn"]) for c, _ in members)
+                     c["W"], c["N"], c["ic_bn"], c["oc_bn"], res) for c, res in members)
+        key += (json.dumps(cfg, sort_keys=True),)
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
         cold_us = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4)) if cold else 0.0
         if key in rows:
@@ -280,7 +282,8 @@ def layer_table(torch, plan, x, out, reps, cold=True):
             rows[key]["_c"].append(cold_us)
             continue
         flops, nbytes = launch_costs(members)
-        rows[key] = dict(shape=" + ".join(conv_label(c) for c, _ in members), uses=1, flops=flops,
+        rows[key] = dict(shape=" + ".join(conv_label(c) + (" +res" if res else "") for c, res in members),
+                         uses=1, flops=flops,
                          bytes=nbytes, config=cfg, _t=[us], _c=[cold_us])
     out_rows = []
     for r in rows.values():
