@@ -83,6 +83,8 @@ size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c) {
 
 namespace {
 
+constexpr long kKFirstMinWgs = 1024;  // launches this large take channel tiles first
+
 // Kernel arguments of one convolution for launch configuration c with G
 // channel groups per reduction step.
 ConvArgs make_args(const ConvShape& s, const ConvConfig& c, int G, const float* x, const float* w,
@@ -133,6 +135,12 @@ ConvArgs make_args(const ConvShape& s, const ConvConfig& c, int G, const float* 
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)cdiv(a.M, 16 * c.fp));
     a.div_nkb = make_fastdiv((unsigned)cdiv(a.KBk, c.fk));
+    // Large launches take channel tiles first: the workgroups that read one
+    // input tile then run on one XCD and share its L2.  Measured on MI355X
+    // (tuned, fused plans): from 1024 workgroups up, ResNet-50 batch 32 runs
+    // 2.76 ms against 2.82 ms with pixel tiles first, batch 1 and VGG-16
+    // batch 1 unchanged; from 512 up, batch 1 is 1.3 % slower.
+    a.kfirst = (long)cdiv(a.M, 16 * c.fp) * cdiv(a.KBk, c.fk) >= kKFirstMinWgs;
     a.gap = s.gap;
     return a;
 }

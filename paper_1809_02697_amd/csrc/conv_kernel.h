@@ -112,6 +112,9 @@ struct ConvArgs {
     // sums [ceil(M / 16)][KB * 16] instead of the outputs (one image, no split)
     int gap;
     FastDiv div_ohw, div_ow, div_npx, div_nkb;
+    // 1: logical workgroups take channel tiles first (the workgroups of one
+    // pixel tile adjacent, so on one XCD), 0: pixel tiles first
+    int kfirst;
 };
 
 // Layout arithmetic.  XY = false is the NCHW16c -> NCHW16c kernel, whose
@@ -384,10 +387,18 @@ __device__ __forceinline__ void conv_tile(const ConvArgs& a, const int u) {
     const int li = lane & 15;
     const int g = lane >> 4;
     const int npx = a.div_npx.d, nkb = a.div_nkb.d;
-    const int u_px = fdiv(u, a.div_npx);
-    const int pxt = u - u_px * npx;
-    const int z = fdiv(u_px, a.div_nkb);
-    const int kbt = u_px - z * nkb;
+    int pxt, kbt, z;
+    if (a.kfirst) {
+        const int u_k = fdiv(u, a.div_nkb);
+        kbt = u - u_k * nkb;
+        z = fdiv(u_k, a.div_npx);
+        pxt = u_k - z * npx;
+    } else {
+        const int u_px = fdiv(u, a.div_npx);
+        pxt = u - u_px * npx;
+        z = fdiv(u_px, a.div_nkb);
+        kbt = u_px - z * nkb;
+    }
     const int m0 = pxt * (16 * FP);
     const int kb0 = kbt * FK;
     const int ohw = a.OH * a.OW;

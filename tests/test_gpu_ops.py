@@ -240,6 +240,18 @@ def test_conv_every_launch_config(neo, cfg, monkeypatch):
             assert_close(y, ref, f"{cfg} C{C} K{K}")
 
 
+@pytest.mark.parametrize("cfg", [(1, 1, 1, 4), (2, 1, 3, 2), (2, 2, 1, 1)])
+def test_conv_large_launch_channel_tiles_first(neo, cfg, monkeypatch):
+    """Launches of 1024 or more workgroups take channel tiles first: four
+    images, a ragged last channel tile (K = 72), with and without a split."""
+    monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d,%d" % cfg)
+    c = wl.conv_case(64, 72, 3, 3, 1, 1, 56, 56, N=4, epilogue="res", out_hw=(56, 56))
+    fk, fp, sp, _ = cfg
+    assert -(-4 * 56 * 56 // (16 * fp)) * -(-5 // fk) >= 1024
+    y = orc.from_blocked(host(run_case(neo, c)), 72)
+    assert_close(y, orc.layer_forward(c), f"{cfg} N=4 56x56")
+
+
 def test_conv_long_reduction(neo):
     """7x7 over 48 blocks x 49 taps = 2352 reduction steps: a long tap-major
     walk that crosses every channel block of every tap many times."""
