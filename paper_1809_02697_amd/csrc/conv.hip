@@ -215,13 +215,22 @@ hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, con
     ConvGroupArgs ga;
     ga.n = n;
     ga.start[0] = 0;
-    for (int i = 0; i < n; ++i) {
-        ga.a[i] = make_args(s[i], c, G, x[i], w[i], true, bias[i], res[i], y[i], nullptr);
-        const int wgs = cdiv(ga.a[i].M, 16 * c.fp) * cdiv(ga.a[i].KBk, c.fk);
-        ga.start[i + 1] = ga.start[i] + wgs;
+    // Dispatch order: the members with the most reduction steps per tile
+    // first (they finish last), ties in the given order.  Each member takes
+    // a whole number of rounds over the XCDs.
+    int order[kMaxGroup];
+    for (int i = 0; i < n; ++i) order[i] = i;
+    auto steps = [&](int i) { return cdiv(s[i].C, 16) / G * s[i].R * s[i].S; };
+    std::stable_sort(order, order + n, [&](int p, int q) { return steps(p) > steps(q); });
+    for (int j = 0; j < n; ++j) {
+        const int i = order[j];
+        ga.a[j] = make_args(s[i], c, G, x[i], w[i], true, bias[i], res[i], y[i], nullptr);
+        ga.cnt[j] = cdiv(ga.a[j].M, 16 * c.fp) * cdiv(ga.a[j].KBk, c.fk);
+        ga.start[j + 1] = ga.start[j] + cdiv(ga.cnt[j], kXcds) * kXcds;
     }
     for (int i = n; i < kMaxGroup; ++i) {
         ga.a[i] = ga.a[n - 1];
+        ga.cnt[i] = 0;
         ga.start[i + 1] = ga.start[n];
     }
     PoolPart& pp = ga.pool;

@@ -628,8 +628,14 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma(ConvArgs a) {
 
 // Several independent convolutions in one launch (horizontal fusion, for
 // batch 1 where each is too small to fill the chip and a launch costs more
-// than its work): member m owns logical workgroups [start[m], start[m+1]).
-// Every member uses the same kernel parameters and no split reduction.
+// than its work).  Member m owns the workgroups [start[m], start[m+1]) of
+// the grid, cnt[m] of them real; every start is a multiple of the XCD count,
+// so workgroup start[m] + b runs on XCD b % kXcds and each member is spread
+// over all XCDs (a member's tiles on a few XCDs would share their CUs while
+// the rest idle), its tiles in the same per-XCD order as a launch of its own.
+// The last start[m+1] - start[m] - cnt[m] (< kXcds) workgroups of a member
+// exit at once.  Every member uses the same kernel parameters and no split
+// reduction.
 // A pooling step may ride along in workgroups past the convs' (wgs of them,
 // grid-stride over its output quads, the same arithmetic as the pooling
 // kernel); it is independent of the convs.  Those workgroups come last in
@@ -644,6 +650,7 @@ struct PoolPart {
 struct ConvGroupArgs {
     ConvArgs a[kMaxGroup];
     int start[kMaxGroup + 1];
+    int cnt[kMaxGroup];
     int n;
     PoolPart pool;
 };
@@ -665,11 +672,12 @@ __global__ __launch_bounds__(WAVES * 64) void conv2d_mfma_group(ConvGroupArgs ga
             ga.pool.k33 ? pool_part_run<false, 3>(ga.pool, wg) : pool_part_run<false, 0>(ga.pool, wg);
         return;
     }
-    const int u = xcd_order(blockIdx.x, nconv);
     int m = 0;
-    while (m + 1 < ga.n && u >= ga.start[m + 1]) ++m;
+    while (m + 1 < ga.n && (int)blockIdx.x >= ga.start[m + 1]) ++m;
     m = __builtin_amdgcn_readfirstlane(m);
-    conv_tile<FK, FP, G, false, true, WAVES, false>(ga.a[m], u - ga.start[m]);
+    const int b = blockIdx.x - ga.start[m];
+    if (b >= ga.cnt[m]) return;
+    conv_tile<FK, FP, G, false, true, WAVES, false>(ga.a[m], xcd_order(b, ga.cnt[m]));
 }
 
 // Second pass of a split reduction: y = act(sum_z part[z] + bias + res), the
