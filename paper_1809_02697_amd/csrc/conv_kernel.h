@@ -35,7 +35,11 @@
 //     adds the SPLIT partials in split order (deterministic) and runs the
 //     epilogue.  The kernel boundary makes the partials visible across XCDs
 //     (whose L2s are not coherent) without a per-workgroup device-scope
-//     release, which measured ~20 ns of serialized time per workgroup.
+//     release, which measured ~20 ns of serialized time per workgroup.  A
+//     one-kernel variant (partials stored past the L2, a release, an arrival
+//     counter per tile, the last arrival reducing with coherent loads)
+//     measured 2-4 % slower end to end at batch 1: its serial chain of store
+//     acknowledgement, atomic and loads costs more than the second launch.
 // Grouped steps.  A step's bookkeeping (advancing the scalar offsets, the loop
 // and ring guards) costs about as many issue cycles as the 4 MFMAs of a one-
 // tile step, measured on MI355X.  Small register tiles therefore take G

@@ -240,6 +240,21 @@ def test_conv_every_launch_config(neo, cfg, monkeypatch):
             assert_close(y, ref, f"{cfg} C{C} K{K}")
 
 
+@pytest.mark.parametrize("cfg", [(1, 1, 4, 4), (2, 1, 8, 1), (1, 2, 2, 8)])
+def test_split_reduction_deterministic(neo, cfg, monkeypatch):
+    """Split reductions add every split's partial in split order, so repeated
+    launches (whatever order the workgroups run in) give bit-identical outputs
+    that match the oracle.  ResNet-50's last-stage 3x3 (512 -> 512 at 7x7) at
+    batch 1, with a residual; every launch reuses the split workspace."""
+    monkeypatch.setenv("NEO_CONV_CONFIG", "%d,%d,%d,%d" % cfg)
+    c = wl.conv_case(512, 512, 3, 3, 1, 1, 7, 7, N=1, epilogue="res", out_hw=(7, 7))
+    ref = orc.layer_forward(c)
+    ys = [host(run_case(neo, c)) for _ in range(12)]
+    for i, y in enumerate(ys[1:], 1):
+        np.testing.assert_array_equal(y, ys[0], err_msg=f"{cfg} launch {i}")
+    assert_close(orc.from_blocked(ys[0], 512), ref, f"{cfg} 512x512 3x3 7x7")
+
+
 @pytest.mark.parametrize("cfg", [(1, 1, 1, 4), (2, 1, 3, 2), (2, 2, 1, 1)])
 def test_conv_large_launch_channel_tiles_first(neo, cfg, monkeypatch):
     """Launches of 1024 or more workgroups take channel tiles first: four
