@@ -122,6 +122,28 @@ def test_end_to_end_batch32_sampled(neo, model):
         print(f"\n{model} b32 image {i}: rel L2 {e:.2e}, beyond 1e-4(1+|ref|): {strict}")
 
 
+def test_tuned_fused_resnet50_batch32_sampled(neo):
+    """The batch-32 ResNet-50 plan the bench times (tuned, every fusion, graph
+    replay): images 0, 13 and 31 against the oracle run on those images alone,
+    and two replays bit-identical."""
+    torch = torch_cuda()
+    g = wl.MODELS["resnet50"](32)
+    fl = (neo.PLAN_TUNE | neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP |
+          neo.PLAN_FUSE_PAIRS | neo.PLAN_FUSE_CHAINS)
+    p = neo.Plan(g, flags=fl)
+    x = dev(g.x)
+    out = torch.empty((32, 1000), device="cuda")
+    p.run(x, out)
+    y = host(out)
+    p.run(x, out)
+    np.testing.assert_array_equal(host(out), y)
+    p.destroy()
+    for i in (0, 13, 31):
+        ref = orc.run_graph(g, x=g.x[i:i + 1])
+        e, strict = assert_close_network(y[i:i + 1], ref, f"fused resnet50 b32 image {i}")
+        print(f"\nfused resnet50 b32 image {i}: rel L2 {e:.2e}, beyond 1e-4(1+|ref|): {strict}")
+
+
 def test_naive_plan_bit_identical_resnet50(neo):
     g = wl.resnet50(1)
     np.testing.assert_array_equal(run_plan(neo, g), run_plan(neo, g, neo.PLAN_NAIVE))
