@@ -279,3 +279,38 @@ def test_concat_residual_group_matches_oracle(neo):
     y, d = _run(neo, g, neo.PLAN_GROUP)
     assert any(s["kind"] == "conv_group" for s in d["steps"])
     assert_close(y.reshape(ref.shape), ref, "concat residual")
+
+
+
+def tiny_members_graph(seed=12):
+    """Siblings on a 2x3 map of one image: members of one to three workgroups
+    (fewer than one per XCD) beside a member of up to 19, so most of each
+    small member's padded range exits at once."""
+    b = wl._Builder("tiny_members", (1, 40, 2, 3), np.random.Generator(np.random.PCG64(seed)))
+    x = b.conv(0, 256, 1, name="stem")
+    a1 = b.conv(x, 32, 1, name="a1")                 # 1 pixel tile x 2 channel tiles
+    a2 = b.conv(x, 48, 3, pad=1, name="a2")          # 3 channel tiles
+    a3 = b.conv(x, 304, 1, name="a3")                # 19 channel tiles
+    y = b.concat([a1, a2, a3], name="cat")
+    y = b.gap(y)
+    y = b.flatten(y, 384)
+    b.output(b.dense(y, 10, name="fc"))
+    return b.finish(lambda rng: rng.normal(0, 1, (1, 40, 2, 3)).astype(np.float32))
+
+
+TINY_CFGS = [(1, 1, 1), (1, 1, 4), (2, 1, 1), (2, 1, 4), (2, 1, 8)]
+
+
+@pytest.mark.parametrize("cfg", TINY_CFGS, ids=[f"fk{c[0]}fp{c[1]}w{c[2]}" for c in TINY_CFGS])
+def test_group_members_smaller_than_xcd_count(neo, cfg, monkeypatch):
+    """Each member of a fused launch takes whole rounds over the XCDs; members
+    with fewer workgroups than XCDs leave the rest of their range idle.  The
+    fused launch runs in the forced configuration and matches the oracle."""
+    monkeypatch.setenv("NEO_GROUP_CONFIG", "%d,%d,%d" % cfg)
+    g = tiny_members_graph()
+    ref = orc.run_graph(g)
+    y, d = _run(neo, g, neo.PLAN_GROUP)
+    grp = [s for s in d["steps"] if s["kind"] == "conv_group"]
+    assert len(grp) == 1 and len(grp[0]["members"]) == 3
+    assert grp[0]["tile"] == [cfg[0], cfg[1]] and grp[0]["waves"] == cfg[2]
+    assert_close(y.reshape(ref.shape), ref, f"tiny members {cfg}")
