@@ -155,9 +155,11 @@ int out_dim(int n, int k, int s, int p) { return (n + 2 * p - k) / s + 1; }
 
 // Split-reduction workspace of the standalone convolution call, one per
 // (device, stream) so that calls on different streams never share it; calls
-// on one stream are ordered by the stream.  Grows on demand (hipMalloc), so
-// the first call of a given size must not be made while the stream is being
-// captured into a graph.
+// on one stream are ordered by the stream.  Grows on demand (hipFree of the
+// old buffer, hipMalloc of the new one); a call that would grow it while the
+// stream is being captured into a graph fails with NEO_ERR_STATE and launches
+// nothing (allocation is not capturable), so the first call of a given size
+// must be made outside capture.
 struct StreamWs {
     float* ws = nullptr;
     size_t bytes = 0;
@@ -172,11 +174,26 @@ int stream_workspace(hipStream_t st, size_t bytes, float** ws) {
     std::lock_guard<std::mutex> lk(g_ws_mu);
     StreamWs& w = g_ws[{dev, st}];
     if (w.bytes < bytes) {
-        if (w.ws) (void)hipFree(w.ws);
-        w.ws = nullptr;
-        w.bytes = 0;
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(st, &cap);
+        if (e != hipSuccess) return hip_fail(e, "neo_conv2d_blocked: hipStreamIsCapturing");
+        if (cap != hipStreamCaptureStatusNone)
+            return fail(NEO_ERR_STATE, "neo_conv2d_blocked: the split-reduction workspace must "
+                                       "grow to " + std::to_string(bytes) + " bytes, which "
+                                       "cannot happen during stream capture; make one call of "
+                                       "this size outside capture first");
+        if (w.ws) {
+            e = hipFree(w.ws);
+            w.ws = nullptr;
+            w.bytes = 0;
+            if (e != hipSuccess) return hip_fail(e, "neo_conv2d_blocked: hipFree of the workspace");
+        }
         e = hipMalloc(&w.ws, bytes);
-        if (e != hipSuccess) return fail(NEO_ERR_OOM, "neo_conv2d_blocked: workspace allocation");
+        if (e != hipSuccess) {
+            w.ws = nullptr;
+            return fail(NEO_ERR_OOM, std::string("neo_conv2d_blocked: workspace allocation of ") +
+                                         std::to_string(bytes) + " bytes: " + hipGetErrorString(e));
+        }
         w.bytes = bytes;
     }
     *ws = w.ws;
@@ -197,6 +214,65 @@ bool env_config(ConvConfig* c) {
 
 }  // namespace
 
+namespace neo {
+
+int conv_prepare(const char* fn, const float* x, int x_block, int N, int C, int H, int W,
+                 const float* w_packed, int K, int R, int S, const float* bias, int stride_h,
+                 int stride_w, int pad_h, int pad_w, const neo_epilogue* ep, const float* y,
+                 int y_block, int y_blk_offset, int y_blk_total, ConvShape* shape,
+                 ConvConfig* config, const float** residual) {
+    const std::string f(fn);
+    auto ptr_ok = [&](const void* p, const char* name) {
+        if (!p) return fail(NEO_ERR_INVALID_ARG, f + ": " + name + " is NULL");
+        if (!aligned16(p)) return fail(NEO_ERR_ALIGN, f + ": " + name + " not 16-byte aligned");
+        return (int)NEO_OK;
+    };
+    int rc;
+    if ((rc = ptr_ok(x, "x")) != NEO_OK || (rc = ptr_ok(w_packed, "w_packed")) != NEO_OK ||
+        (rc = ptr_ok(y, "y")) != NEO_OK || (bias && (rc = ptr_ok(bias, "bias")) != NEO_OK))
+        return rc;
+    if (N <= 0 || C <= 0 || H <= 0 || W <= 0 || K <= 0 || R <= 0 || S <= 0 || stride_h <= 0 ||
+        stride_w <= 0)
+        return fail(NEO_ERR_INVALID_ARG, f + ": sizes and strides must be > 0");
+    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, f + ": negative pad");
+    const int act = ep ? ep->act : NEO_ACT_NONE;
+    if (act != NEO_ACT_NONE && act != NEO_ACT_RELU)
+        return fail(NEO_ERR_INVALID_ARG, f + ": unknown activation");
+    const float* res = ep ? ep->residual : nullptr;
+    if (res && (rc = ptr_ok(res, "residual")) != NEO_OK) return rc;
+    const int OH = out_dim(H, R, stride_h, pad_h), OW = out_dim(W, S, stride_w, pad_w);
+    if (H + 2 * pad_h < R || W + 2 * pad_w < S || OH < 1 || OW < 1)
+        return fail(NEO_ERR_SHAPE, f + ": empty output (window larger than padded input)");
+    ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
+                y_blk_offset, y_blk_total, act};
+    s.xb = x_block;
+    s.yb = y_block;
+    if (!conv_blocks_valid(s))
+        return fail(NEO_ERR_UNSUPPORTED, f + ": blocks must be 16, 32 or 64 "
+                                             "(input 1, 4 or 8 too when C <= 4)");
+    const int KY = cdiv(K, y_block);
+    if (y_blk_offset < 0 || y_blk_total < KY || y_blk_offset + KY > y_blk_total)
+        return fail(NEO_ERR_SHAPE, f + ": output channel-block view out of range");
+    if (blocked_elems(N, C, H, W, x_block) > kMaxElems ||
+        (long)N * y_blk_total * y_block * OH * OW > kMaxElems ||
+        (long)cdiv(K, 16) * 16 * cdiv(C, 16) * 16 * R * S > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, f + ": tensor exceeds 2^31-1 elements");
+    if (blocked_elems(N, C, H, W, x_block) >= (1L << 29) ||
+        (long)cdiv(K, 16) * cdiv(C, 16) * R * S * 256 >= (1L << 29))
+        return fail(NEO_ERR_UNSUPPORTED, f + ": input or filter of 2 GiB or more");
+    ConvConfig cfg = choose_conv_config(s);
+    (void)tuned_config(s, false, &cfg);
+    env_config(&cfg);
+    const int T = cdiv(C, 16) * R * S;
+    if (cfg.split > T) cfg.split = T;
+    *shape = s;
+    *config = cfg;
+    *residual = res;
+    return NEO_OK;
+}
+
+}  // namespace neo
+
 extern "C" {
 
 const char* neo_last_error(void) { return g_err.c_str(); }
@@ -205,46 +281,16 @@ int neo_conv2d_nchwxc(const float* x, int x_block, int N, int C, int H, int W,
                       const float* w_packed, int K, int R, int S, const float* bias, int stride_h,
                       int stride_w, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
                       int y_block, int y_blk_offset, int y_blk_total, neo_stream_t stream) {
-    CHECK_PTR(x);
-    CHECK_PTR(w_packed);
-    CHECK_PTR(y);
-    if (bias) CHECK_PTR(bias);
-    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
-    CHECK_POS(K); CHECK_POS(R); CHECK_POS(S);
-    CHECK_POS(stride_h); CHECK_POS(stride_w);
-    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_nchwxc: negative pad");
-    const int act = ep ? ep->act : NEO_ACT_NONE;
-    if (act != NEO_ACT_NONE && act != NEO_ACT_RELU)
-        return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_nchwxc: unknown activation");
-    const float* res = ep ? ep->residual : nullptr;
-    if (res) CHECK_PTR(res);
-    const int OH = out_dim(H, R, stride_h, pad_h), OW = out_dim(W, S, stride_w, pad_w);
-    if (H + 2 * pad_h < R || W + 2 * pad_w < S || OH < 1 || OW < 1)
-        return fail(NEO_ERR_SHAPE, "neo_conv2d_nchwxc: empty output (window larger than padded input)");
-    ConvShape s{N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, OH, OW,
-                y_blk_offset, y_blk_total, act};
-    s.xb = x_block;
-    s.yb = y_block;
-    if (!conv_blocks_valid(s))
-        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_nchwxc: blocks must be 16, 32 or 64 "
-                                         "(input 1, 4 or 8 too when C <= 4)");
-    const int KY = cdiv(K, y_block);
-    if (y_blk_offset < 0 || y_blk_total < KY || y_blk_offset + KY > y_blk_total)
-        return fail(NEO_ERR_SHAPE, "neo_conv2d_nchwxc: output channel-block view out of range");
-    CHECK_SIZE(blocked_elems(N, C, H, W, x_block));
-    CHECK_SIZE((long)N * y_blk_total * y_block * OH * OW);
-    CHECK_SIZE((long)cdiv(K, 16) * 16 * cdiv(C, 16) * 16 * R * S);
-    if (blocked_elems(N, C, H, W, x_block) >= (1L << 29) ||
-        (long)cdiv(K, 16) * cdiv(C, 16) * R * S * 256 >= (1L << 29))
-        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_nchwxc: input or filter of 2 GiB or more");
-    ConvConfig cfg = choose_conv_config(s);
-    (void)tuned_config(s, false, &cfg);
-    env_config(&cfg);
-    const int T = cdiv(C, 16) * R * S;
-    if (cfg.split > T) cfg.split = T;
+    ConvShape s;
+    ConvConfig cfg;
+    const float* res = nullptr;
+    int rc = conv_prepare("neo_conv2d_nchwxc", x, x_block, N, C, H, W, w_packed, K, R, S, bias,
+                          stride_h, stride_w, pad_h, pad_w, ep, y, y_block, y_blk_offset,
+                          y_blk_total, &s, &cfg, &res);
+    if (rc != NEO_OK) return rc;
     float* ws = nullptr;
     if (cfg.split > 1) {
-        const int rc = stream_workspace((hipStream_t)stream, conv_workspace_bytes(s, cfg), &ws);
+        rc = stream_workspace((hipStream_t)stream, conv_workspace_bytes(s, cfg), &ws);
         if (rc != NEO_OK) return rc;
     }
     hipError_t e = launch_conv2d(s, cfg, x, w_packed, false, bias, res, y, ws,

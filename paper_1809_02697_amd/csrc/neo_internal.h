@@ -71,6 +71,17 @@ ConvConfig choose_conv_config(const ConvShape& s);
 // Workspace of a split reduction (partial sums of every split), in bytes.
 size_t conv_workspace_bytes(const ConvShape& s, const ConvConfig& c);
 
+// Validation and launch configuration shared by the standalone convolution
+// entry points: checks every argument (the calling entry point's name `fn`
+// leads each error message), then picks the configuration (cost model,
+// results database, NEO_CONV_CONFIG override).  On NEO_OK fills the shape,
+// the configuration and the residual pointer; nothing is launched.
+int conv_prepare(const char* fn, const float* x, int x_block, int N, int C, int H, int W,
+                 const float* w_packed, int K, int R, int S, const float* bias, int stride_h,
+                 int stride_w, int pad_h, int pad_w, const neo_epilogue* ep, const float* y,
+                 int y_block, int y_blk_offset, int y_blk_total, ConvShape* shape,
+                 ConvConfig* config, const float** residual);
+
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
 // or null; res: NCHW[yb]c [N][ceil(K/yb)][OH][OW][yb] or null; y: NCHW[yb]c

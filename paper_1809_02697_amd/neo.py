@@ -169,49 +169,55 @@ def out_size(n, k, s, p):
 # --------------------------------------------------------------------------------------
 # Single operations
 # --------------------------------------------------------------------------------------
-def conv2d_blocked(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
-                   residual=None, out=None, y_cblk_offset=0, y_cblk_total=None, stream=None):
-    """x: [N][ceil(C/16)][H][W][16]; w_packed: KCRS[16]c[16]k.  Returns out."""
+def _need(t, n, name):
+    """A device buffer the kernels index up to n floats: refuse a shorter one
+    (it would be an out-of-bounds device access)."""
+    if t is not None and t.numel() < n:
+        raise ValueError(f"{name} holds {t.numel()} floats, the call needs {n}")
+
+
+def _conv_common(fn, x, xb, C, w_packed, K, R, S, bias, stride, pad, act, residual, out,
+                 y_block, y_off, y_tot, stream, blocked_abi):
     import torch
     (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
-    N, CB, H, W, blk = x.shape
+    N, XB, H, W, blk = x.shape
+    if blk != xb or XB != cblocks(C, xb):
+        raise ValueError(f"x shape {tuple(x.shape)} is not NCHW[{xb}]c of {C} channels")
     OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
-    KB = cblocks(K)
-    tot = KB if y_cblk_total is None else y_cblk_total
+    tot = cblocks(K, y_block) if y_tot is None else y_tot
     if out is None:
-        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=x.device,
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), y_block), device=x.device,
                           dtype=torch.float32)
+    if OH > 0 and OW > 0:
+        _need(out, N * tot * OH * OW * y_block, "out")
+        _need(residual, N * cblocks(K, y_block) * OH * OW * y_block, "residual")
+    _need(bias, cblocks(K) * BLOCK, "bias")
+    _need(w_packed, cblocks(K) * cblocks(C) * R * S * BLOCK * BLOCK, "w_packed")
     ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
                   residual.data_ptr() if residual is not None else None)
     if residual is not None:
         _dptr(residual, "residual")
-    _check(lib().neo_conv2d_blocked(_dptr(x, "x"), N, C, H, W, _dptr(w_packed, "w_packed"), K,
-                                    R, S, _dptr(bias, "bias"), sh, sw, ph, pw, ctypes.byref(ep),
-                                    _dptr(out, "out"), y_cblk_offset, tot, _stream(stream)))
+    pre = (_dptr(x, "x"),) if blocked_abi else (_dptr(x, "x"), xb)
+    mid = (_dptr(out, "out"),) if blocked_abi else (_dptr(out, "out"), y_block)
+    _check(fn(*pre, N, C, H, W, _dptr(w_packed, "w_packed"), K, R, S, _dptr(bias, "bias"),
+              sh, sw, ph, pw, ctypes.byref(ep), *mid, y_off, tot, _stream(stream)))
     return out
+
+
+def conv2d_blocked(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
+                   residual=None, out=None, y_cblk_offset=0, y_cblk_total=None, stream=None):
+    """x: [N][ceil(C/16)][H][W][16]; w_packed: KCRS[16]c[16]k.  Returns out."""
+    return _conv_common(lib().neo_conv2d_blocked, x, BLOCK, C, w_packed, K, R, S, bias, stride,
+                        pad, act, residual, out, BLOCK, y_cblk_offset, y_cblk_total, stream, True)
 
 
 def conv2d_nchwxc(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
                   residual=None, out=None, y_block=BLOCK, y_blk_offset=0, y_blk_total=None,
                   stream=None):
     """x: [N][ceil(C/xb)][H][W][xb] (xb from x's last dim); output NCHW[y_block]c."""
-    import torch
-    (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
-    N, XB, H, W, xb = x.shape
-    OH, OW = out_size(H, R, sh, ph), out_size(W, S, sw, pw)
-    tot = cblocks(K, y_block) if y_blk_total is None else y_blk_total
-    if out is None:
-        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), y_block), device=x.device,
-                          dtype=torch.float32)
-    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
-                  residual.data_ptr() if residual is not None else None)
-    if residual is not None:
-        _dptr(residual, "residual")
-    _check(lib().neo_conv2d_nchwxc(_dptr(x, "x"), xb, N, C, H, W, _dptr(w_packed, "w_packed"), K,
-                                   R, S, _dptr(bias, "bias"), sh, sw, ph, pw, ctypes.byref(ep),
-                                   _dptr(out, "out"), y_block, y_blk_offset, tot,
-                                   _stream(stream)))
-    return out
+    return _conv_common(lib().neo_conv2d_nchwxc, x, x.shape[-1], C, w_packed, K, R, S, bias,
+                        stride, pad, act, residual, out, y_block, y_blk_offset, y_blk_total,
+                        stream, False)
 
 
 def layout_transform(src, src_block, dst_block, N, C, H, W, out=None, stream=None):
@@ -272,6 +278,10 @@ def _pool(fn, x, C, R, S, stride, pad, out, y_cblk_offset, y_cblk_total, stream,
     if out is None:
         out = torch.empty((N, tot, max(OH, 0), max(OW, 0), blk), device=x.device,
                           dtype=torch.float32)
+    if CB != cblocks(C, blk):
+        raise ValueError(f"x shape {tuple(x.shape)} is not NCHW[{blk}]c of {C} channels")
+    if OH > 0 and OW > 0:
+        _need(out, N * tot * OH * OW * blk, "out")
     pre = (_dptr(x, "x"), blk) if blocked else (_dptr(x, "x"),)
     _check(fn(*pre, N, C, H, W, R, S, sh, sw, ph, pw, _dptr(out, "out"), y_cblk_offset,
               tot, _stream(stream)))
@@ -296,6 +306,7 @@ def global_avgpool_nchwxc(x, C, out=None, stream=None):
     N, CB, H, W, blk = x.shape
     if out is None:
         out = torch.empty((N, CB, 1, 1, blk), device=x.device, dtype=torch.float32)
+    _need(out, N * CB * blk, "out")
     _check(lib().neo_global_avgpool_nchwxc(_dptr(x, "x"), blk, N, C, H, W, _dptr(out, "out"),
                                            _stream(stream)))
     return out
@@ -318,6 +329,7 @@ def global_avgpool_blocked(x, C, out=None, stream=None):
     N, CB, H, W, _ = x.shape
     if out is None:
         out = torch.empty((N, CB, 1, 1, BLOCK), device=x.device, dtype=torch.float32)
+    _need(out, N * CB * BLOCK, "out")
     _check(lib().neo_global_avgpool_blocked(_dptr(x, "x"), N, C, H, W, _dptr(out, "out"),
                                             _stream(stream)))
     return out
@@ -330,6 +342,10 @@ def dense(x, w, bias=None, act="none", out=None, stream=None):
     OUT = w.shape[0]
     if out is None:
         out = torch.empty((N, OUT), device=x.device, dtype=torch.float32)
+    if w.numel() != OUT * IN:
+        raise ValueError(f"w holds {w.numel()} floats, not {OUT} x {IN}")
+    _need(out, N * OUT, "out")
+    _need(bias, OUT, "bias")
     _check(lib().neo_dense(_dptr(x, "x"), N, IN, _dptr(w, "w"), OUT, _dptr(bias, "bias"),
                            ACT[act] if isinstance(act, str) else int(act), _dptr(out, "out"),
                            _stream(stream)))
@@ -458,12 +474,16 @@ class Plan:
             N, C, H, W = self.output_shape
             shape = (N, C) if (H, W) == (1, 1) else (N, C, H, W)
             out = torch.empty(shape, device=x.device, dtype=torch.float32)
+        _need(out, int(np.prod(self.output_shape)), "out")
         _check(lib().neo_run_graph(self.handle, _dptr(x, "x"), _dptr(out, "out"),
                                    _stream(stream)))
         return out
 
     def run_step(self, step, x, out, stream=None):
         """Launch one step of the plan's launch list (for timing single layers)."""
+        if tuple(x.shape) != self.input_shape:
+            raise ValueError(f"input shape {tuple(x.shape)} != plan input {self.input_shape}")
+        _need(out, int(np.prod(self.output_shape)), "out")
         _check(lib().neo_run_step(self.handle, step, _dptr(x, "x"), _dptr(out, "out"),
                                   _stream(stream)))
 

@@ -50,6 +50,36 @@ def test_conv_argument_errors():
     assert conv_call(N=4096, C=4096, H=64, W=64) == -4   # > 2^31 elements
 
 
+def test_binding_refuses_short_buffers():
+    """The Python wrappers refuse an output, bias, residual or filter shorter
+    than the call indexes (a device write or read out of bounds otherwise),
+    before calling the library."""
+    import torch
+    x = torch.zeros((1, 1, 8, 8, 16))
+    wp = torch.zeros((2, 1, 3, 3, 16, 16))
+    with pytest.raises(ValueError, match="out"):
+        neo.conv2d_blocked(x, 16, wp, 32, 3, 3, pad=1, out=torch.zeros(2 * 8 * 8 * 16 - 1))
+    with pytest.raises(ValueError, match="bias"):
+        neo.conv2d_blocked(x, 16, wp, 32, 3, 3, pad=1, bias=torch.zeros(16),
+                           out=torch.zeros((1, 2, 8, 8, 16)))
+    with pytest.raises(ValueError, match="residual"):
+        neo.conv2d_blocked(x, 16, wp, 32, 3, 3, pad=1, residual=torch.zeros(10),
+                                   out=torch.zeros((1, 2, 8, 8, 16)))
+    with pytest.raises(ValueError, match="w_packed"):
+        neo.conv2d_nchwxc(x, 16, wp[:1], 32, 3, 3, pad=1, out=torch.zeros((1, 2, 8, 8, 16)))
+    with pytest.raises(ValueError, match="NCHW"):
+        neo.conv2d_blocked(x, 17, wp, 32, 3, 3, pad=1, out=torch.zeros((1, 2, 8, 8, 16)))
+    with pytest.raises(ValueError, match="out"):
+        neo.maxpool2d_blocked(x, 16, 3, 3, 2, 1, out=torch.zeros(10))
+    with pytest.raises(ValueError, match="out"):
+        neo.dense(torch.zeros((2, 8)), torch.zeros((4, 8)), out=torch.zeros(7))
+    g = wl.tiny_graph()
+    p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY)
+    with pytest.raises(ValueError, match="out"):
+        p.run(torch.zeros(g.input_shape), out=torch.zeros(5))
+    p.destroy()
+
+
 def test_other_argument_errors():
     assert L.neo_layout_transform(FAKE, 3, FAKE, 16, 1, 3, 4, 4, None) == -1
     assert L.neo_layout_transform(FAKE, 0, FAKE, 16, 1, 3, 4, 4, None) == -1  # overlap

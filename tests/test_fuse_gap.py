@@ -118,6 +118,6 @@ def test_resnet50_folded_tuned_replayed(gneo):
         first = y if first is None else first
         np.testing.assert_array_equal(y, first)
     p.destroy()
-    assert_close_network(first, ref, "resnet50 folded pool")
+    assert_close_network(first, ref, "resnet50 folded pool", graph=g)
     y0, _ = _run(g, neo.PLAN_TUNE | neo.PLAN_GROUP)
     assert rel_l2(first, y0) <= 1e-6

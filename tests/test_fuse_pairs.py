@@ -162,7 +162,7 @@ def test_resnet50_pairs_tuned_replayed(gneo, tmp_path):
         first = y if first is None else first
         np.testing.assert_array_equal(y, first)
     p.destroy()
-    assert_close_network(first, ref, "resnet50 with pairs")
+    assert_close_network(first, ref, "resnet50 with pairs", graph=g)
     path = tmp_path / "db.txt"
     neo.tune_db_save(path)
     convs, pairs = _db(path)

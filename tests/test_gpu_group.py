@@ -76,7 +76,7 @@ def test_grouped_network_matches_oracle(neo, builder):
     ref = orc.run_graph(g)
     y, d = _run(neo, g, neo.PLAN_GROUP)
     assert any(s["kind"] == "conv_group" for s in d["steps"])
-    assert_close_network(y.reshape(ref.shape), ref, g.name)
+    assert_close_network(y.reshape(ref.shape), ref, g.name, graph=g)
     y0, _ = _run(neo, g)
     assert rel_l2(y, y0) <= 1e-5
 
@@ -91,7 +91,7 @@ def test_tuned_grouped_resnet50_graph_replay(neo):
     x = dev(g.x)
     eager = host(p.run(x))
     p.destroy()
-    assert_close_network(eager.reshape(ref.shape), ref, "tuned grouped resnet50")
+    assert_close_network(eager.reshape(ref.shape), ref, "tuned grouped resnet50", graph=g)
     p = neo.Plan(g, flags=neo.PLAN_GROUP | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
     d = p.describe()
     assert all(s["tuned"] for s in d["steps"] if s["kind"] == "conv_group")
@@ -184,7 +184,7 @@ def test_tuned_inception_keeps_only_faster_launches(neo, tmp_path):
     d0 = p0.describe()
     p0.destroy()
     y, d = _run(neo, g, neo.PLAN_GROUP | neo.PLAN_TUNE)
-    assert_close_network(y.reshape(ref.shape), ref, "tuned grouped inception")
+    assert_close_network(y.reshape(ref.shape), ref, "tuned grouped inception", graph=g)
     path = tmp_path / "db.txt"
     neo.tune_db_save(path)
     convs, groups, pools = _db_times(path)

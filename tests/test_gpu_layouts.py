@@ -218,7 +218,7 @@ def test_mixed_scheme_plan_is_bit_identical(neo, builder, seed):
     np.testing.assert_array_equal(y, y16)
     assert d["n_transforms"] >= 1
     ref = orc.run_graph(g)
-    assert_close_network(y.reshape(ref.shape), ref, g.name)
+    assert_close_network(y.reshape(ref.shape), ref, g.name, graph=g)
 
 
 @pytest.mark.parametrize("block", [32, 64])
@@ -256,4 +256,4 @@ def test_global_search_plan(neo, builder):
           f"{sorted(set((c['conv']['ic_bn'], c['conv']['oc_bn']) for c in convs))}, "
           f"transforms {d['n_transforms']}")
     ref = orc.run_graph(g)
-    assert_close_network(y.reshape(ref.shape), ref, g.name)
+    assert_close_network(y.reshape(ref.shape), ref, g.name, graph=g)
