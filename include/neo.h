@@ -121,6 +121,31 @@ int neo_conv2d_nchwxc(const float* x, int x_block, int N, int C, int H, int W,
                       int y_block, int y_blk_offset, int y_blk_total, neo_stream_t stream);
 
 /*
+ * neo_conv2d_blocked for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, launch configuration, kernels and results as
+ * neo_conv2d_blocked (bit-identical), but it calls no hipMalloc, hipFree or
+ * allocating library routine: when the configuration splits the reduction
+ * across workgroups, the partial sums go to a fixed device array of
+ * NEO_NOALLOC_SCRATCH_BYTES, one per GPU, held from the library's load until
+ * the process ends (its address is looked up once per device, on the first
+ * call that needs it).
+ *   - A call whose split needs more partial-sum storage than that
+ *     (split * N * ceil(K/16) * OH * OW * 64 bytes) returns
+ *     NEO_ERR_UNSUPPORTED and launches nothing.
+ *   - Every call on one GPU shares that GPU's array, so calls that may run
+ *     at the same time on one GPU (different streams, not ordered by events)
+ *     race on it; calls on one stream are ordered by the stream.  The array
+ *     keeps the last call's partials; nothing in it needs to start at zero.
+ */
+#define NEO_NOALLOC_SCRATCH_BYTES (16 * 1024 * 1024)
+int neo_conv2d_blocked_noalloc(const float* x, int N, int C, int H, int W,
+                               const float* w_packed, int K, int R, int S, const float* bias,
+                               int stride_h, int stride_w, int pad_h, int pad_w,
+                               const neo_epilogue* ep, float* y, int y_cblk_offset,
+                               int y_cblk_total, neo_stream_t stream);
+
+/*
  * LayoutTransform node (Section 3.2): NCHW <-> NCHW[x]c, or NCHW[x]c ->
  * NCHW[x']c.  A block of 0 means plain NCHW; a block x > 0 means
  * [N][ceil(C/x)][H][W][x] with zero-filled padding lanes.  Blocks: 0, 1, 2,

@@ -80,6 +80,8 @@ def lib():
     sig = {
         "neo_conv2d_blocked": [P, I, I, I, I, P, I, I, I, P, I, I, I, I,
                                ctypes.POINTER(Epilogue), P, I, I, P],
+        "neo_conv2d_blocked_noalloc": [P, I, I, I, I, P, I, I, I, P, I, I, I, I,
+                                       ctypes.POINTER(Epilogue), P, I, I, P],
         "neo_conv2d_nchwxc": [P, I, I, I, I, I, P, I, I, I, P, I, I, I, I,
                               ctypes.POINTER(Epilogue), P, I, I, I, P],
         "neo_maxpool2d_nchwxc": [P, I, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
@@ -209,6 +211,17 @@ def conv2d_blocked(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="non
     """x: [N][ceil(C/16)][H][W][16]; w_packed: KCRS[16]c[16]k.  Returns out."""
     return _conv_common(lib().neo_conv2d_blocked, x, BLOCK, C, w_packed, K, R, S, bias, stride,
                         pad, act, residual, out, BLOCK, y_cblk_offset, y_cblk_total, stream, True)
+
+
+def conv2d_blocked_noalloc(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",
+                           residual=None, out=None, y_cblk_offset=0, y_cblk_total=None,
+                           stream=None):
+    """conv2d_blocked whose split-reduction partials use the library's fixed
+    device array (no device allocation inside the call; ``out`` should be
+    passed by a caller that cannot allocate)."""
+    return _conv_common(lib().neo_conv2d_blocked_noalloc, x, BLOCK, C, w_packed, K, R, S, bias,
+                        stride, pad, act, residual, out, BLOCK, y_cblk_offset, y_cblk_total,
+                        stream, True)
 
 
 def conv2d_nchwxc(x, C, w_packed, K, R, S, bias=None, stride=1, pad=0, act="none",

@@ -50,6 +50,19 @@ def test_conv_argument_errors():
     assert conv_call(N=4096, C=4096, H=64, W=64) == -4   # > 2^31 elements
 
 
+def test_noalloc_argument_errors():
+    """The no-alloc convolution validates exactly as the allocating one, before
+    any device work, and names itself in the message."""
+    def call(x=FAKE, C=16, H=8, pd=(1, 1), yt=1):
+        return L.neo_conv2d_blocked_noalloc(x, 1, C, H, 8, FAKE, 16, 3, 3, None, 1, 1, pd[0],
+                                            pd[1], None, FAKE, 0, yt, None)
+    assert call(x=None) == -1 and "neo_conv2d_blocked_noalloc" in neo.last_error()
+    assert call(x=MIS) == -3
+    assert call(C=0) == -1
+    assert call(H=2, pd=(0, 0)) == -2
+    assert call(yt=0) == -2
+
+
 def test_binding_refuses_short_buffers():
     """The Python wrappers refuse an output, bias, residual or filter shorter
     than the call indexes (a device write or read out of bounds otherwise),
@@ -63,7 +76,7 @@ def test_binding_refuses_short_buffers():
         neo.conv2d_blocked(x, 16, wp, 32, 3, 3, pad=1, bias=torch.zeros(16),
                            out=torch.zeros((1, 2, 8, 8, 16)))
     with pytest.raises(ValueError, match="residual"):
-        neo.conv2d_blocked(x, 16, wp, 32, 3, 3, pad=1, residual=torch.zeros(10),
+        neo.conv2d_blocked_noalloc(x, 16, wp, 32, 3, 3, pad=1, residual=torch.zeros(10),
                                    out=torch.zeros((1, 2, 8, 8, 16)))
     with pytest.raises(ValueError, match="w_packed"):
         neo.conv2d_nchwxc(x, 16, wp[:1], 32, 3, 3, pad=1, out=torch.zeros((1, 2, 8, 8, 16)))
