@@ -13,9 +13,12 @@ Printed JSON line:
   value        conv TFLOP/s over the whole step (8.174 GFLOP of convolution
                per image / step time); ``latency_ms`` is the step time
   roofline     the dominant kernel, conv2d_blocked: algorithmic FLOPs per
-               launch / average launch duration, the duration measured with
-               HIP events around graph replays of each conv step of the plan
-               (repeated back-to-back launches on the plan's stream)
+               launch / average launch duration, each conv step of the plan
+               timed with HIP events around back-to-back graph replays on the
+               plan's stream (sum_conv_us: the forward's conv launches summed,
+               at most ms_per_step); a kernel trace of the forwards launched
+               step by step (stepwise_forward_ms) gives the same per-launch
+               durations from the hardware's own timestamps
   latency      per-forward latency over 1000 single runs: mean, standard
                error, median (warm caches: the batch-1 working set stays in
                the 256 MB MALL between runs)
@@ -219,6 +222,33 @@ def e2e_ms(torch, plan, x, out, steps, warmup):
     return e0.elapsed_time(e1) / steps
 
 
+def stepwise_forwards(torch, plan, x, out, runs=20, head_start_cycles=5_000_000):
+    """Forwards launched one step at a time, each step between two HIP events
+    on the plan's stream.  Every forward is queued behind its own spin kernel
+    of `head_start_cycles` (about 2 ms), so the host has enqueued the whole
+    forward before the GPU starts it and the steps run back to back.  The
+    events keep every dispatch from starting before its predecessor has
+    ended, so in a kernel trace each dispatch's timestamps are its own
+    duration inside a forward (queued back to back without them, a dispatch's
+    start stamp can precede the end of the one before, and the durations
+    overlap).  Returns the mean forward span in ms, event markers included."""
+    stream = torch.cuda.current_stream()
+    n = len(plan.describe()["steps"])
+    spans = []
+    for _ in range(runs):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(head_start_cycles)
+        for i, (e0, e1) in enumerate(ev):
+            e0.record(stream)
+            plan.run_step(i, x, out)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        spans.append(ev[0][0].elapsed_time(ev[-1][1]))
+    return float(np.mean(spans))
+
+
 def e2e_stats(torch, plan, x, out, runs):
     """Per-run latency over `runs` back-to-back forwards, each bracketed by
     its own pair of HIP events (the mean +- standard error and the median,
@@ -372,23 +402,69 @@ def measured_traffic():
     return t["traffic_bytes_per_launch"]
 
 
-def cpu_baseline(g, budget_s=12.0):
-    """The oracle (plain C direct convolution, OpenMP on all host cores) on
-    whole ResNet-50 batch-1 forwards until ~budget_s of work."""
-    import oracle
-    flops = 8_174_272_512
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.run_graph(g)
+def cpu_model():
+    """The host CPU's model string (/proc/cpuinfo) and its logical CPU count."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            names = [l.split(":", 1)[1].strip() for l in f if l.startswith("model name")]
+        return (names[0] if names else "unknown"), len(names)
+    except OSError:
+        return "unknown", 0
+
+
+def _timed(fn, budget_s, min_runs=1):
+    """(seconds per call, calls): fn() repeated until budget_s has passed."""
+    n, t0 = 0, time.perf_counter()
+    while n < min_runs or time.perf_counter() - t0 < budget_s:
+        fn()
         n += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
-    return dict(value=round(flops * n / dt / 1e12, 6), unit="TFLOP/s", cores=oracle.num_threads(),
-                kind="oracle", ms_per_forward=round(dt / n * 1e3, 1),
-                sample=f"{n} ResNet-50 batch-1 forward pass(es) through the oracle graph "
-                       f"executor ({dt:.1f} s)")
+    return (time.perf_counter() - t0) / n, n
+
+
+def cpu_baseline(g, budget_s=8.0):
+    """The oracle (plain C direct convolution in double, OpenMP over the host
+    cores; batch norm, bias, residual and ReLU unfused in numpy) on the same
+    workloads as the GPU, on a bounded sample:
+      value      whole ResNet-50 batch-1 forwards until ~budget_s of work;
+      e2e_ms     one forward each of the single conv (configuration 1), VGG-16
+                 and Inception-v3 at batch 1;
+      layers_ms  each of the 23 ResNet-50 layer shapes once (conv + batch norm +
+                 residual + ReLU);
+      single_core  the single conv on one thread."""
+    import oracle
+    from paper_1809_02697_amd import workloads as wl
+    flops = 8_174_272_512
+    model, ncpu = cpu_model()
+    cores = oracle.num_threads()
+    dt, n = _timed(lambda: oracle.run_graph(g), budget_s)
+    out = dict(value=round(flops / dt / 1e12, 6), unit="TFLOP/s", cores=cores,
+               kind="oracle", cpu_model=model, host_logical_cpus=ncpu,
+               ms_per_forward=round(dt * 1e3, 1),
+               sample=f"{n} ResNet-50 batch-1 forward pass(es) through the oracle graph executor "
+                      f"({dt * n:.1f} s); plus one forward each of configuration 1, VGG-16 and "
+                      f"Inception-v3, the 23 layer shapes once, and configuration 1 on one thread")
+    cfg1 = wl.single_conv(0)
+    e2e = {}
+    for name, gg, gf in [("single_conv", cfg1, 231_211_008), ("vgg16_b1", wl.vgg16(1), 30_693_261_312),
+                         ("inception_v3_b1", wl.inception_v3(1), 11_422_336_192)]:
+        t, _ = _timed(lambda: oracle.run_graph(gg), 0.0)
+        e2e[name] = dict(ms=round(t * 1e3, 1), conv_gflops=round(gf / t / 1e9, 2))
+    out["e2e_ms"] = e2e
+    layers = {}
+    for c in wl.resnet50_layer_sweep(1):
+        t, _ = _timed(lambda: oracle.layer_forward(c), 0.0)
+        f = 2 * c.N * c.K * c.C * c.R * c.S * ((c.H + 2 * c.pad[0] - c.R) // c.stride[0] + 1) * \
+            ((c.W + 2 * c.pad[1] - c.S) // c.stride[1] + 1)
+        layers[c.id] = dict(ms=round(t * 1e3, 2), gflops=round(f / t / 1e9, 2))
+    out["layers_ms"] = layers
+    oracle.set_num_threads(1)
+    try:
+        t, _ = _timed(lambda: oracle.run_graph(cfg1), 0.0)
+    finally:
+        oracle.set_num_threads(cores)
+    out["single_core"] = dict(workload="configuration 1 (64->64 3x3, 56x56, bias + ReLU)",
+                              cores=1, ms=round(t * 1e3, 1), gflops=round(231_211_008 / t / 1e9, 3))
+    return out
 
 
 def main():
@@ -397,9 +473,13 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--layer-reps", type=int, default=20)
+    ap.add_argument("--stepwise-runs", type=int, default=20,
+                    help="forwards launched step by step between events (for kernel traces)")
     ap.add_argument("--latency-runs", type=int, default=1000,
                     help="single-forward latency samples (mean, standard error, median)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="skip the engine-clock sample (4000 forwards under load)")
     ap.add_argument("--no-layers", action="store_true", help="skip the per-layer table")
     ap.add_argument("--no-models", action="store_true", help="skip the other models and ablation")
     ap.add_argument("--tune-db", help="load this local-search results file before planning")
@@ -433,8 +513,12 @@ def main():
     print(f"[bench] e2e {ms:.3f} ms/step", file=sys.stderr, flush=True)
     stats = e2e_stats(torch, plan, x, out, args.latency_runs)
     print(f"[bench] latency over {stats['runs']} runs: {stats}", file=sys.stderr, flush=True)
-    clock = engine_clock(torch, plan, x, out)
+    clock = None if args.no_clock else engine_clock(torch, plan, x, out)
     print(f"[bench] engine clock under load: {clock}", file=sys.stderr, flush=True)
+
+    stepwise_ms = stepwise_forwards(torch, plan, x, out, args.stepwise_runs)
+    print(f"[bench] forward launched step by step between events: {stepwise_ms:.4f} ms",
+          file=sys.stderr, flush=True)
 
     layers, roofline = None, None
     if not args.no_layers:
@@ -446,14 +530,18 @@ def main():
         roofline = dict(bound="mfma", achieved=round(achieved, 2), peak=PEAK_FP32_TFLOPS,
                         unit="TFLOP/s", frac=round(achieved / PEAK_FP32_TFLOPS, 4),
                         traffic=measured_traffic(),
-                        kernel="conv2d_blocked (single, fused-group, pointwise-pair and 3x3-chain launches)",
+                        kernel="conv2d_blocked (single, fused-group, pointwise-pair and 3x3-chain "
+                               "launches, each with its split-reduction pass)",
+                        timing=f"HIP events around {args.layer_reps} back-to-back graph replays "
+                               f"of each conv step of the plan, on the plan's stream",
                         launches_per_step=n_launch,
-                        avg_launch_us=round(tot_t / n_launch * 1e6, 2),
+                        avg_launch_us=round(tot_t / n_launch * 1e6, 3),
+                        sum_conv_us=round(tot_t * 1e6, 1),
                         flop_per_launch=round(tot_f / n_launch))
         for r in layers:
             del r["flops"], r["bytes"]
-        print(f"[bench] conv layers: {achieved:.2f} TFLOP/s over {n_launch} launches",
-              file=sys.stderr, flush=True)
+        print(f"[bench] conv layers: {achieved:.2f} TFLOP/s over {n_launch} launches, "
+              f"{tot_t * 1e6:.1f} us per forward", file=sys.stderr, flush=True)
 
     models = None if args.no_models else model_latencies(neo, torch, wl, 20)
 
@@ -488,6 +576,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "latency_ms": round(ms, 4),
+        "stepwise_forward_ms": round(stepwise_ms, 4),
         "latency": stats,
         "engine_clock": clock,
         "higher_is_better": True,

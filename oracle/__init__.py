@@ -62,12 +62,18 @@ def _load():
         lib.orc_global_avgpool.argtypes = [P, I, I, I, I, P]
         lib.orc_dense.argtypes = [P, I, I, P, I, P, P]
         lib.orc_num_threads.restype = I
+        lib.orc_set_num_threads.argtypes = [I]
         _lib = lib
     return _lib
 
 
 def num_threads():
     return _load().orc_num_threads()
+
+
+def set_num_threads(n):
+    """Host threads the C operations use from now on (timing only)."""
+    _load().orc_set_num_threads(int(n))
 
 
 def _c(a):

@@ -130,3 +130,14 @@ int orc_num_threads(void) {
     }
     return t;
 }
+
+/* Thread count of the following parallel regions (n >= 1), for timing the
+ * oracle on a given number of host cores; does not affect any result. */
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

@@ -1,40 +1,63 @@
-"""Workload for hardware-counter passes over the ResNet-50 batch-1 plan.
+"""Workload for hardware-counter passes over the ResNet-50 plan bench.py times.
 
-    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT -o fetch -- \
-        python -m paper_1809_02697_amd.profile_layers [TUNE_DB]
-    rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT -o write -- \
-        python -m paper_1809_02697_amd.profile_layers [TUNE_DB]
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT -o fetch -- \\
+        python -m paper_1809_02697_amd.profile_layers TUNE_DB [--cold] [--batch 32]
+    rocprofv3 --pmc WRITE_SIZE ...                       (the same workload)
+    rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 ... (the same workload)
 
-Builds the plan bench.py times (with TUNE_DB, a local-search results file
-written by ``bench.py --save-tune-db``, the launch configurations and the
-global search's schemes come from that run, so no tuning launches are
-profiled), runs one forward,
-then a plain device-to-device copy of COPY_MB megabytes (the calibration
-kernel: it reads and writes exactly that many bytes) and then every step of
-the plan once, in order.  The dispatches after the copy are one forward pass.
-``paper_1809_02697_amd.profile_summary`` turns the counter files into the
-per-launch traffic figures.
+Builds the plan bench.py times (batch 1: the headline plan; batch 32: the
+tuned one-block plan of the batch-32 layer table).  TUNE_DB is a local-search
+results file written by ``bench.py --save-tune-db``: the launch configurations
+and the global search's schemes come from that run, so no tuning launches are
+profiled.  It runs one forward, then a plain device-to-device copy of COPY_MB
+megabytes (the calibration kernel: it reads and writes exactly that many
+bytes) and then every step of the plan once, in order: the dispatches after
+the copy are one forward pass.  With --cold a 512 MB buffer (twice the 256 MB
+MALL) is overwritten before every step, so each step's operands come from HBM
+and FETCH_SIZE counts HBM reads.  ``paper_1809_02697_amd.profile_summary``
+turns the counter files into per-launch figures.
 """
+import argparse
+import json
 import sys
 
 COPY_MB = 64
+FLUSH_MB = 512
+
+
+def build_plan(neo, torch, wl, db, batch):
+    """(plan, graph) of the run whose results file is `db`."""
+    from bench import headline_plan
+    if db:
+        neo.tune_db_load(db)
+    g = wl.resnet50(batch)
+    if batch == 1:
+        plan, _ = headline_plan(neo, g, db, torch)
+    else:
+        plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+    return plan, g
 
 
 def main():
     import torch
 
-    from bench import headline_plan
     from paper_1809_02697_amd import neo
     from paper_1809_02697_amd import workloads as wl
 
-    db = sys.argv[1] if len(sys.argv) > 1 else None
-    if db:
-        neo.tune_db_load(db)
-    g = wl.resnet50(1)
-    plan, _ = headline_plan(neo, g, db, torch)
+    ap = argparse.ArgumentParser()
+    ap.add_argument("db", nargs="?")
+    ap.add_argument("--cold", action="store_true")
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--describe", help="write the plan's description (JSON) here")
+    args = ap.parse_args()
+    plan, g = build_plan(neo, torch, wl, args.db, args.batch)
+    if args.describe:
+        with open(args.describe, "w") as f:
+            json.dump(plan.describe(), f)
     x = torch.from_numpy(g.x).cuda()
-    out = torch.empty((1, 1000), device="cuda")
+    out = torch.empty(plan.output_shape[:2], device="cuda")
     plan.run(x, out)
+    flush = torch.empty(FLUSH_MB * 2 ** 18, device="cuda") if args.cold else None
     torch.cuda.synchronize()
     a = torch.ones(COPY_MB * 2 ** 18, device="cuda")
     b = torch.empty_like(a)
@@ -42,9 +65,12 @@ def main():
     torch.cuda.synchronize()
     n = len(plan.describe()["steps"])
     for i in range(n):
+        if flush is not None:
+            flush.fill_(1.0)
         plan.run_step(i, x, out)
     torch.cuda.synchronize()
-    print(f"profiled {n} steps after a {COPY_MB} MB copy", file=sys.stderr)
+    print(f"profiled {n} steps after a {COPY_MB} MB copy (batch {args.batch}"
+          f"{', cold' if args.cold else ''})", file=sys.stderr)
     plan.destroy()
 
 

@@ -1,26 +1,39 @@
-"""Summarize rocprofv3 output of the ResNet-50 batch-1 conv kernels into profiles/.
+"""Summarize rocprofv3 output of the ResNet-50 conv kernels into profiles/.
 
     python -m paper_1809_02697_amd.profile_summary RUN_DIR
 
-RUN_DIR holds (names as written by the commands below):
-  prof_bench/bench_kernel_stats.csv, prof_bench/bench_kernel_trace.csv
-      rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_bench -o bench --
-          python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt --latency-runs 100
-  pmc/fetch_counter_collection.csv, pmc/write_counter_collection.csv
-      rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch --
-          python -m paper_1809_02697_amd.profile_layers        (and WRITE_SIZE / -o write)
-  bench.log   the JSON line of a plain `python bench.py --no-cpu --save-tune-db
-              RUN_DIR/tune_db.txt` run on the same box
+RUN_DIR holds (names as written by the commands in COMMANDS below):
+  bench.log       the JSON line of a plain ``python bench.py --save-tune-db
+                  RUN_DIR/tune_db.txt`` run (and the results file it saved)
+  prof_bench/     rocprofv3 --kernel-trace --stats of the same bench command
+                  (profiled, with the saved results file, so the plan is the
+                  one the plain run timed)
+  pmc/            counter passes over profile_layers: FETCH_SIZE and WRITE_SIZE
+                  with warm caches and with every step cold (--cold), and the
+                  MFMA counters at batch 1 and batch 32
 
-Writes profiles/conv2d_blocked_resnet50_b1.md (durations, traffic per layer)
-and profiles/conv2d_blocked_resnet50_b1_traffic.json (bytes per launch, tied to
-the hash of the kernel source it was measured with; bench.py reports it only
-while the source is unchanged).
+Writes
+  profiles/conv2d_blocked_resnet50_b1.md  launch durations, per-layer traffic
+      (warm and cold) and MFMA utilisation at batch 1
+  profiles/conv2d_blocked_resnet50_b32_mfma.md  MFMA utilisation at batch 32
+  profiles/conv2d_blocked_resnet50_b1_traffic.json  bytes per launch, tied to
+      the hash of the kernel source it was measured with (bench.py reports it
+      only while the source is unchanged)
 
-FETCH_SIZE / WRITE_SIZE are KiB moved between L2 and the fabric per dispatch.
-They are calibrated by the same counters on a plain copy of COPY_MB megabytes
-(which reads and writes exactly that many bytes); the figures include reads
-served by the 256 MB MALL, which these counters cannot tell from HBM.
+Launch durations.  The kernel trace's timestamps of the forwards that bench.py
+launches step by step between events (stepwise_forwards: the dispatches after
+its spin kernel) are each launch's own duration inside a forward; their mean
+is compared with bench.py's HIP-event figure.  Under the profiler, graph
+replays are slower and their per-dispatch durations longer, and dispatches
+queued back to back overlap in the trace (a start stamp precedes the end of
+the dispatch before); both are reported, neither is used.
+
+FETCH_SIZE / WRITE_SIZE are KiB moved between L2 and the fabric per dispatch,
+calibrated by the same counters on a plain copy of COPY_MB megabytes (which
+reads and writes exactly that many bytes).  Warm, the figures include reads
+served by the 256 MB MALL; cold (512 MB written before every step), the reads
+come from HBM.  MFMA utilisation is SQ_VALU_MFMA_BUSY_CYCLES summed over the
+SIMDs / (GRBM_GUI_ACTIVE x 1024 SIMDs), rocprofv3's MfmaUtil, per dispatch.
 """
 import csv
 import hashlib
@@ -33,6 +46,31 @@ ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(HERE, "csrc", f)
                for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip")]
+PEAK = 157.3
+SIMDS = 1024         # 256 CUs x 4
+CLOCK_MHZ = 2400.0   # engine clock under load (bench.py's engine_clock)
+
+COMMANDS = [
+    "python bench.py --save-tune-db RUN_DIR/tune_db.txt > RUN_DIR/bench.log",
+    "rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_bench -o bench -- "
+    "python bench.py --no-cpu --no-models --no-clock --tune-db RUN_DIR/tune_db.txt "
+    "--latency-runs 100",
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d RUN_DIR/pmc -o write -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch_cold -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --cold",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d RUN_DIR/pmc -o write_cold -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --cold",
+    "rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+    "--output-format csv -d RUN_DIR/pmc -o mfma -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
+    "rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+    "--output-format csv -d RUN_DIR/pmc -o mfma32 -- python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --batch 32 "
+    "--describe RUN_DIR/plan_b32.json",
+    "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
+]
 
 
 def kernel_hash():
@@ -48,25 +86,34 @@ def _rows(path):
         return list(csv.DictReader(f))
 
 
-def forward_dispatches(path):
-    """Counter values of the dispatches after the last copy kernel (one
-    forward pass, in launch order) and of that copy."""
-    rows = _rows(path)
-    last_copy = max(i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"])
-    copy = float(rows[last_copy]["Counter_Value"])
-    fwd = [(r["Kernel_Name"], float(r["Counter_Value"])) for r in rows[last_copy + 1:]]
-    return copy, fwd
-
-
-def conv_launches(run_dir):
-    """The conv launches of the plan the bench run timed (its description is
-    saved next to the results file): one conv or a fused group each."""
-    from bench import conv_launches as launches
-    return launches(json.load(open(os.path.join(run_dir, "tune_db.txt.plan.json"))))
-
-
 def is_conv(name):
     return "conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name
+
+
+def is_neo(name):
+    return "neo::" in name
+
+
+def _dispatch_values(path, counter=None):
+    """{dispatch id: (kernel name, value)} of a counter file, in dispatch order;
+    `counter` picks one counter of a multi-counter pass."""
+    out = {}
+    for r in _rows(path):
+        if counter and r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        name, v = out.get(d, (r["Kernel_Name"], 0.0))
+        out[d] = (name, v + float(r["Counter_Value"]))
+    return [out[d] for d in sorted(out)]
+
+
+def forward_dispatches(path, counter=None):
+    """Counter values of the dispatches after the last copy kernel (one forward
+    pass, in launch order, the cold pass's flushes dropped) and of that copy."""
+    rows = _dispatch_values(path, counter)
+    last_copy = max(i for i, (n, _) in enumerate(rows) if "copyBuffer" in n)
+    fwd = [(n, v) for n, v in rows[last_copy + 1:] if is_neo(n)]
+    return rows[last_copy][1], fwd
 
 
 def per_conv(fwd):
@@ -81,92 +128,208 @@ def per_conv(fwd):
     return out
 
 
+def per_conv_max(fwd):
+    """Like per_conv for a ratio counter: the conv dispatch's own value."""
+    return [v for name, v in fwd if is_conv(name)]
+
+
+def stepwise_forward_durations(trace_path, n_steps):
+    """Per-launch durations (us) of the conv launches of every forward bench.py
+    launched step by step between events, each behind its own spin kernel: a
+    list of forwards, each a list of conv launch durations (a split_reduce pass
+    added to its conv)."""
+    rows = sorted(_rows(trace_path), key=lambda r: int(r["Start_Timestamp"]))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    out = []
+    spins = [i for i, r in enumerate(rows) if "spin_kernel" in r["Kernel_Name"]]
+    for sp in spins:
+        cur, steps = [], 0
+        for r in rows[sp + 1:]:
+            n = r["Kernel_Name"]
+            if not is_neo(n):
+                break
+            if is_conv(n):
+                cur.append(dur(r))
+            elif "split_reduce" in n and cur:
+                cur[-1] += dur(r)
+            if "split_reduce" not in n:
+                steps += 1
+            if steps == n_steps:
+                out.append(cur)
+                break
+    return out
+
+
+def graph_forward_durations(trace_path, n_steps):
+    """Sum of conv durations per graph-replayed forward before the spin kernel
+    (the profiled e2e and latency runs), and the forward spans.  A forward
+    starts at a dispatch of the kernel that starts the step-by-step ones."""
+    rows = sorted(_rows(trace_path), key=lambda r: int(r["Start_Timestamp"]))
+    spin = min(i for i, r in enumerate(rows) if "spin_kernel" in r["Kernel_Name"])
+    first = next(r["Kernel_Name"] for r in rows[spin + 1:] if is_neo(r["Kernel_Name"]))
+    starts = [i for i in range(spin) if rows[i]["Kernel_Name"] == first]
+    sums, spans = [], []
+    for a, b in zip(starts, starts[1:]):
+        blk = [r for r in rows[a:b] if is_neo(r["Kernel_Name"])]
+        if len([r for r in blk if "split_reduce" not in r["Kernel_Name"]]) != n_steps:
+            continue
+        d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in blk]
+        sums.append(sum(x for r, x in zip(blk, d) if is_conv(r["Kernel_Name"])
+                        or "split_reduce" in r["Kernel_Name"]))
+        spans.append((int(blk[-1]["End_Timestamp"]) - int(blk[0]["Start_Timestamp"])) / 1e3)
+    return sums, spans
+
+
+def _median(v):
+    v = sorted(v)
+    return v[len(v) // 2] if v else float("nan")
+
+
 def main(run_dir):
     sys.path.insert(0, ROOT)
-    from bench import conv_label, launch_costs
+    from bench import conv_label, conv_launches, launch_costs
     from paper_1809_02697_amd.profile_layers import COPY_MB
     copy_bytes = COPY_MB * 2 ** 20
+    pmc = os.path.join(run_dir, "pmc")
 
-    f_copy, f_fwd = forward_dispatches(os.path.join(run_dir, "pmc", "fetch_counter_collection.csv"))
-    w_copy, w_fwd = forward_dispatches(os.path.join(run_dir, "pmc", "write_counter_collection.csv"))
-    ff = copy_bytes / (f_copy * 1024.0)
-    fw = copy_bytes / (w_copy * 1024.0)
-    fetch = per_conv(f_fwd)
-    write = per_conv(w_fwd)
-    steps = conv_launches(run_dir)
-    n_convs = sum(len(m) for _, m, _ in steps)
-    assert n_convs == 53 and len(fetch) == len(write) == len(steps), (len(fetch), len(write), len(steps))
-
-    layer_rows = []
-    tot_alg = tot_traffic = 0.0
-    for (_, members, _), fv, wv in zip(steps, fetch, write):
-        alg = launch_costs(members)[1]
-        rd, wr = fv * 1024 * ff, wv * 1024 * fw
-        tot_alg += alg
-        tot_traffic += rd + wr
-        layer_rows.append((" + ".join(conv_label(c) for c, _ in members), alg, rd, wr))
-
-    trace = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_trace.csv"))
-    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-    conv_d = [dur(r) for r in trace if is_conv(r["Kernel_Name"])]
-    red_d = [dur(r) for r in trace if "split_reduce" in r["Kernel_Name"]]
-    trace_avg = (sum(conv_d) + sum(red_d)) / len(conv_d)
-    stats = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_stats.csv"))
+    desc = json.load(open(os.path.join(run_dir, "tune_db.txt.plan.json")))
+    steps = conv_launches(desc)
+    n_steps = len(desc["steps"])
+    n = len(steps)
     bench = json.loads([l for l in open(os.path.join(run_dir, "bench.log")) if l.startswith("{")][0])
     ev_avg = bench["roofline"]["avg_launch_us"]
+    flops = [launch_costs(m)[0] for _, m, _ in steps]
 
-    n = len(steps)
-    traffic = dict(kernel="conv2d_blocked", workload=f"ResNet-50 batch 1, 53 convs in {n} launches",
-                   kernel_source_sha256=kernel_hash(),
-                   traffic_bytes_per_launch=round(tot_traffic / n),
-                   alg_bytes_per_launch=round(tot_alg / n),
-                   fetch_calibration=round(ff, 4), write_calibration=round(fw, 4))
+    # -- launch durations from the kernel trace -------------------------------------------
+    trace = os.path.join(run_dir, "prof_bench", "bench_kernel_trace.csv")
+    fwds = [f for f in stepwise_forward_durations(trace, n_steps) if len(f) == n]
+    per_launch = [sum(f) / n for f in fwds]
+    tr_avg = _median(per_launch)
+    tr_sum = _median([sum(f) for f in fwds])
+    per_step = [_median([f[i] for f in fwds]) for i in range(n)]
+    g_sums, g_spans = graph_forward_durations(trace, n_steps)
+    tr_tf = sum(flops) / (tr_avg * n * 1e-6) / 1e12
+
+    # -- traffic, warm and cold -------------------------------------------------------------
+    def traffic(tag):
+        f_copy, f_fwd = forward_dispatches(os.path.join(pmc, f"fetch{tag}_counter_collection.csv"))
+        w_copy, w_fwd = forward_dispatches(os.path.join(pmc, f"write{tag}_counter_collection.csv"))
+        ff, fw = copy_bytes / (f_copy * 1024.0), copy_bytes / (w_copy * 1024.0)
+        rd = [v * 1024 * ff for v in per_conv(f_fwd)]
+        wr = [v * 1024 * fw for v in per_conv(w_fwd)]
+        assert len(rd) == len(wr) == n, (tag, len(rd), len(wr), n)
+        return rd, wr, ff, fw
+    rd_w, wr_w, ff, fw = traffic("")
+    rd_c, wr_c, ffc, fwc = traffic("_cold")
+    alg = [launch_costs(m)[1] for _, m, _ in steps]
+    tot_w = sum(rd_w) + sum(wr_w)
+
+    # -- MFMA utilisation -------------------------------------------------------------------
+    def mfma(tag):
+        path = os.path.join(pmc, f"{tag}_counter_collection.csv")
+        _, util = forward_dispatches(path, "MfmaUtil")
+        _, mops = forward_dispatches(path, "SQ_INSTS_VALU_MFMA_MOPS_F32")
+        _, busy = forward_dispatches(path, "SQ_VALU_MFMA_BUSY_CYCLES")
+        return per_conv_max(util), per_conv(mops), per_conv(busy)
+    util1, mops1, busy1 = mfma("mfma")
+    assert len(util1) == n, (len(util1), n)
+    # busy MFMA time per SIMD (us), and the cycles one 16x16x4 fp32 MFMA keeps it busy
+    busy_us = [b / SIMDS / CLOCK_MHZ for b in busy1]
+    cyc_per_mfma = sum(busy1) / (sum(mops1) * 512 / 2048)
+
+    traffic_json = dict(kernel="conv2d_blocked", workload=f"ResNet-50 batch 1, 53 convs in {n} launches",
+                        kernel_source_sha256=kernel_hash(),
+                        traffic_bytes_per_launch=round(tot_w / n),
+                        traffic_bytes_per_launch_cold=round((sum(rd_c) + sum(wr_c)) / n),
+                        alg_bytes_per_launch=round(sum(alg) / n),
+                        fetch_calibration=round(ff, 4), write_calibration=round(fw, 4))
     os.makedirs(PROFILES, exist_ok=True)
     with open(os.path.join(PROFILES, "conv2d_blocked_resnet50_b1_traffic.json"), "w") as f:
-        json.dump(traffic, f, indent=1)
+        json.dump(traffic_json, f, indent=1)
 
     md = [f"# conv2d_blocked, ResNet-50 batch 1 (53 convs in {n} launches per forward)", "",
           "Commands (run from the repository root on one MI355X; RUN_DIR = gpurun_out):", "",
-          "```",
-          "python bench.py --save-tune-db RUN_DIR/tune_db.txt > RUN_DIR/bench.log",
-          "rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_bench -o bench -- "
-          "python bench.py --no-cpu --no-models --tune-db RUN_DIR/tune_db.txt --latency-runs 100",
-          "rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o fetch -- "
-          "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
-          "rocprofv3 --pmc WRITE_SIZE --output-format csv -d RUN_DIR/pmc -o write -- "
-          "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt",
-          "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
-          "```", "",
+          "```"] + COMMANDS + ["```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
           "## Launch duration", "",
-          f"- rocprofv3 kernel trace, mean per conv launch (conv2d_mfma, conv2d_mfma_group, conv1x1_pair or conv3x3_chain + its "
-          f"split_reduce pass, "
-          f"{len(conv_d)} conv dispatches): **{trace_avg:.2f} us**",
-          f"- bench.py HIP events (graph replays of each conv step, weighted by use): "
-          f"**{ev_avg:.2f} us** (ratio {trace_avg / ev_avg:.3f})",
-          f"- bench.py e2e ResNet-50 batch 1: {bench['latency_ms']} ms; conv layers "
-          f"{bench['roofline']['achieved']} TFLOP/s = {100 * bench['roofline']['frac']:.1f} % of "
-          f"157.3 TFLOP/s", "",
-          "rocprofv3 --stats (profiled bench run; all dispatches of the run):", "",
+          f"- Kernel-trace timestamps of the {len(fwds)} forwards the profiled bench run launched "
+          f"step by step between events: median per conv launch (its split_reduce pass included) "
+          f"**{tr_avg:.3f} us**; the {n} conv launches of one forward sum to {tr_sum:.1f} us.",
+          f"- bench.py (unprofiled), HIP events around back-to-back graph replays of each conv step: "
+          f"**{ev_avg:.3f} us** per launch; trace / events = {tr_avg / ev_avg:.3f}.",
+          f"- roofline.frac from the trace: {tr_tf:.2f} TFLOP/s / {PEAK} = "
+          f"**{tr_tf / PEAK:.4f}**; bench.py: {bench['roofline']['achieved']} TFLOP/s, frac "
+          f"**{bench['roofline']['frac']}**.",
+          f"- bench.py e2e ResNet-50 batch 1 (graph replay): {bench['ms_per_step']} ms per forward "
+          f"(step by step between events: {bench.get('stepwise_forward_ms', 'n/a')} ms).  The "
+          f"traced forward's conv launches ({tr_sum:.1f} us) fit in the graph forward.",
+          f"- Under the profiler, graph replays run slower: the {len(g_sums)} profiled graph forwards "
+          f"span {_median(g_spans):.1f} us with {_median(g_sums):.1f} us of conv dispatches "
+          f"({_median(g_sums) / n:.2f} us per launch); these are not used.", "",
+          "rocprofv3 --stats (the profiled bench run; all dispatches of the run):", "",
           "| kernel | calls | avg us | total % |", "|---|---:|---:|---:|"]
+    stats = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_stats.csv"))
     for r in sorted(stats, key=lambda r: -float(r["Percentage"]))[:12]:
         name = r["Name"].replace("void ", "").replace("neo::(anonymous namespace)::", "")
         name = name.split("(neo")[0].split("(float")[0][:70]
         md.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                   f"{float(r['Percentage']):.1f} |")
-    md += ["", "## HBM / fabric traffic per conv launch", "",
-           f"Calibration: a {COPY_MB} MB copy reads {f_copy / 1024:.1f} MiB (FETCH_SIZE) and writes "
-           f"{w_copy / 1024:.1f} MiB (WRITE_SIZE): factors {ff:.3f} / {fw:.3f}.", "",
-           f"- mean per launch: **{tot_traffic / n / 1e6:.3f} MB** measured vs "
-           f"{tot_alg / n / 1e6:.3f} MB algorithmic (ratio {tot_traffic / tot_alg:.2f})", "",
-           "| # | layer | algorithmic MB | read MB | write MB | (read+write)/alg |",
-           "|---:|---|---:|---:|---:|---:|"]
-    for i, (name, alg, rd, wr) in enumerate(layer_rows):
-        md.append(f"| {i} | {name} | {alg / 1e6:.3f} | {rd / 1e6:.3f} | {wr / 1e6:.3f} | "
-                  f"{(rd + wr) / alg:.2f} |")
+    md += ["", "## Per launch: duration in the forward, traffic, MFMA utilisation", "",
+           f"Calibration: a {COPY_MB} MB copy gives factors {ff:.3f} (FETCH_SIZE) / {fw:.3f} "
+           f"(WRITE_SIZE) warm, {ffc:.3f} / {fwc:.3f} cold.", "",
+           f"- warm, mean per launch: **{tot_w / n / 1e6:.3f} MB** measured vs "
+           f"{sum(alg) / n / 1e6:.3f} MB algorithmic (ratio {tot_w / sum(alg):.2f})",
+           f"- cold (HBM), mean per launch: **{(sum(rd_c) + sum(wr_c)) / n / 1e6:.3f} MB** "
+           f"(ratio {(sum(rd_c) + sum(wr_c)) / sum(alg):.2f})",
+           f"- MFMA busy time (SQ_VALU_MFMA_BUSY_CYCLES over {SIMDS} SIMDs at {CLOCK_MHZ:.0f} MHz; "
+           f"{cyc_per_mfma:.1f} busy cycles per 16x16x4 fp32 MFMA) over the traced duration, all "
+           f"launches: **{100 * sum(busy_us) / sum(per_step):.1f} %**.  rocprofv3's MfmaUtil "
+           f"divides by the dispatch's active cycles under counter collection, which at batch 1 "
+           f"are longer than the unprofiled duration, so it reads lower.", "",
+           "| # | layer | us (trace) | TFLOP/s | % peak | alg MB | warm read / write MB | "
+           "cold read / write MB | MFMA busy us | busy / us % | MfmaUtil % | MFMA flop / alg flop |",
+           "|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for i, (_, members, _) in enumerate(steps):
+        name = " + ".join(conv_label(c) for c, _ in members)
+        tf = flops[i] / (per_step[i] * 1e-6) / 1e12
+        md.append(f"| {i} | {name} | {per_step[i]:.2f} | {tf:.1f} | {100 * tf / PEAK:.1f} | "
+                  f"{alg[i] / 1e6:.3f} | {rd_w[i] / 1e6:.3f} / {wr_w[i] / 1e6:.3f} | "
+                  f"{rd_c[i] / 1e6:.3f} / {wr_c[i] / 1e6:.3f} | {busy_us[i]:.2f} | "
+                  f"{100 * busy_us[i] / per_step[i]:.1f} | {util1[i]:.1f} | "
+                  f"{mops1[i] * 512 / flops[i]:.3f} |")
     with open(os.path.join(PROFILES, "conv2d_blocked_resnet50_b1.md"), "w") as f:
         f.write("\n".join(md) + "\n")
-    print(json.dumps(traffic))
+
+    # -- batch 32 ---------------------------------------------------------------------------
+    p32 = os.path.join(pmc, "mfma32_counter_collection.csv")
+    if os.path.exists(p32) and os.path.exists(os.path.join(run_dir, "plan_b32.json")):
+        d32 = json.load(open(os.path.join(run_dir, "plan_b32.json")))
+        s32 = conv_launches(d32)
+        _, util = forward_dispatches(p32, "MfmaUtil")
+        _, mops = forward_dispatches(p32, "SQ_INSTS_VALU_MFMA_MOPS_F32")
+        _, busy = forward_dispatches(p32, "SQ_VALU_MFMA_BUSY_CYCLES")
+        util, mops, busy = per_conv_max(util), per_conv(mops), per_conv(busy)
+        assert len(util) == len(s32), (len(util), len(s32))
+        md = ["# conv2d_blocked, ResNet-50 batch 32: MFMA utilisation per launch", "",
+              "Command (from the repository root; RUN_DIR = gpurun_out; the plan and results file "
+              "of the bench run above):", "", "```", COMMANDS[7], COMMANDS[-1], "```", "",
+              f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
+              "MfmaUtil = busy MFMA cycles summed over the 1024 SIMDs / (GPU active cycles x "
+              "1024), per dispatch (the conv kernel; a split_reduce pass is not counted). "
+              "The last column is the MFMA work executed (SQ_INSTS_VALU_MFMA_MOPS_F32 x 512) over "
+              "the algorithmic FLOPs: above 1 where padded channels or masked pixels are "
+              "multiplied.", "",
+              "| # | layer | MfmaUtil % | MFMA busy us | MFMA flop / alg flop |",
+              "|---:|---|---:|---:|---:|"]
+        for i, (_, members, _) in enumerate(s32):
+            f32 = launch_costs(members)[0]
+            md.append(f"| {i} | {' + '.join(conv_label(c) for c, _ in members)} | {util[i]:.1f} | "
+                      f"{busy[i] / SIMDS / CLOCK_MHZ:.2f} | {mops[i] * 512 / f32:.3f} |")
+        with open(os.path.join(PROFILES, "conv2d_blocked_resnet50_b32_mfma.md"), "w") as f:
+            f.write("\n".join(md) + "\n")
+    print(json.dumps(dict(traffic_json, trace_avg_launch_us=round(tr_avg, 3),
+                          bench_avg_launch_us=ev_avg, trace_frac=round(tr_tf / PEAK, 4),
+                          bench_frac=bench["roofline"]["frac"])))
 
 
 if __name__ == "__main__":
