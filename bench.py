@@ -89,7 +89,7 @@ def headline_plan(neo, g, tune_db=None, torch=None):
     profiling run executes the same plan)."""
     path = (tune_db or "") + ".schemes.json"
     base = (neo.PLAN_HIPGRAPH | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS |
-            neo.PLAN_FUSE_CHAINS)
+            neo.PLAN_FUSE_CHAINS | neo.PLAN_FUSE_POOL)
     if tune_db and os.path.exists(path):
         sch = {int(k): tuple(v) for k, v in json.load(open(path)).items()}
         return neo.Plan(g, flags=neo.PLAN_TUNE | base, schemes=sch), {"from": path}
@@ -124,6 +124,14 @@ def conv_launches(desc):
             out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
                         dict(tile=s["tile"], split=1, waves=s["waves"], ic_bn=16, oc_bn=16,
                              group=len(s["members"]))))
+        elif s["kind"] == "conv_pool":
+            # the conv's output stays in LDS; only the pooled map is written
+            m = s["members"][0]
+            c = dict(m["conv"], lds_out=True, pooled=(s["pool"]["OH"], s["pool"]["OW"]))
+            cfg = s["config"]
+            out.append((i, [(c, False)], dict(tile=cfg["tile"], waves=cfg["waves"],
+                                              pooled_tile=cfg["pooled_tile"], split=1, pool=True,
+                                              ic_bn=c["ic_bn"], oc_bn=c["oc_bn"])))
         elif s["kind"] in ("conv_pair", "conv_chain"):
             # every conv after the first reads its input from LDS; a chain's
             # 3x3 output stays there and is never stored
@@ -147,13 +155,16 @@ def launch_costs(members):
             bb -= 4 * c["N"] * c["C"] * OH * OW
         if c.get("lds_out"):    # an output kept in LDS only
             bb -= 4 * c["N"] * c["K"] * OH * OW
+        if c.get("pooled"):     # ... and its max pooling written instead
+            bb += 4 * c["N"] * c["K"] * c["pooled"][0] * c["pooled"][1]
         f, b = f + ff, b + bb
     return f, b
 
 
 def conv_label(c):
     OH = (c["H"] + 2 * c["pad"][0] - c["R"]) // c["stride"][0] + 1
-    return f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} {c['H']}->{OH}"
+    pool = f" + maxpool ->{c['pooled'][0]}" if c.get("pooled") else ""
+    return f"{c['C']}->{c['K']} {c['R']}x{c['S']}/s{c['stride'][0]} {c['H']}->{OH}{pool}"
 
 
 def plan_conv_flops(desc):
@@ -352,7 +363,8 @@ def model_latencies(neo, torch, wl, steps):
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
-        fused = neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS | neo.PLAN_FUSE_CHAINS
+        fused = (neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS | neo.PLAN_FUSE_CHAINS |
+                 neo.PLAN_FUSE_POOL)
         plans = [("eliminated", 0, 16), ("grouped", fused, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]

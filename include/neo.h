@@ -330,7 +330,16 @@ enum neo_plan_flags {
      * the 3x3 alone plus the best launches of the rest.  Results match the
      * oracle but are not bit-identical to an unchained plan's (the 3x3's sums
      * run in another order).  Not in the paper. */
-    NEO_PLAN_FUSE_CHAINS = 256
+    NEO_PLAN_FUSE_CHAINS = 256,
+    /* A convolution of at most 4 input channels (a network stem) whose
+     * output only a max pooling step reads runs with that pooling in one
+     * launch: the workgroups stage the input patch and the filter in LDS,
+     * keep the conv's output in LDS and write only the pooled map.  The
+     * results are those of the conv with one wave per tile followed by the
+     * pooling, bit for bit.  With NEO_PLAN_TUNE the fused launch is kept only
+     * where it measures faster than the two launches.  Not in the paper: a
+     * batch-1 GPU design choice. */
+    NEO_PLAN_FUSE_POOL = 512
 };
 
 /*

@@ -127,6 +127,28 @@ int tune_conv_group(const ConvShape* s, int n, const float* const* x, const floa
 // Time per launch of a pooling step alone (kept in the results database).
 int tune_pool(const GroupPool& p, hipStream_t st, float* us);
 
+// A small-channel convolution (a network stem) and the max pooling that
+// reads its output, in one launch (conv_pool.hip): the conv's output is kept
+// in LDS and only the pooled map is written, NCHW16c with the pool's view
+// (p.y_off, p.y_tot).  Configuration: fk channel blocks and fp pixel groups
+// per wave, `waves` waves per workgroup, a ty x tx tile of pooled outputs per
+// workgroup.  x: NCHW[xb]c (xb = 1: NCHW); w: the kernel order of the small-
+// channel path (to_kernel_order); results bit-identical to launch_conv2d with
+// one wave and no split followed by launch_maxpool.
+struct ConvPoolConfig {
+    int fk, fp, waves, ty, tx;
+};
+bool conv_pool_eligible(const ConvShape& c, const PoolShape& p);
+bool conv_pool_config_valid(const ConvShape& c, const PoolShape& p, const ConvPoolConfig& k);
+std::vector<ConvPoolConfig> conv_pool_candidates(const ConvShape& c, const PoolShape& p);
+ConvPoolConfig choose_conv_pool_config(const ConvShape& c, const PoolShape& p);
+hipError_t launch_conv_pool(const ConvShape& c, const PoolShape& p, const ConvPoolConfig& k,
+                            const float* x, const float* w, const float* bias, float* y,
+                            hipStream_t st);
+// Local search over conv_pool_candidates; keeps the fastest with its time.
+int tune_conv_pool(const ConvShape& c, const PoolShape& p, const float* x, const float* w,
+                   const float* bias, float* y, hipStream_t st, ConvPoolConfig* best, float* us);
+
 // Local search (tune.cpp): the database's configuration for a shape (with its
 // blocks), if any; and a search that times every candidate with the given
 // buffers on `st` and returns the fastest with its time per launch in us.

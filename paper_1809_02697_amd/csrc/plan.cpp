@@ -40,7 +40,7 @@ using namespace neo;
 namespace {
 
 enum StepKind { ST_TRANSFORM, ST_CONV, ST_MAXPOOL, ST_AVGPOOL, ST_GAP, ST_DENSE, ST_COPY, ST_CONV_GROUP,
-                ST_CONV_PAIR, ST_CONV_CHAIN };
+                ST_CONV_PAIR, ST_CONV_CHAIN, ST_CONV_POOL };
 
 struct Val {
     int N = 0, C = 0, H = 0, W = 0;
@@ -76,7 +76,9 @@ struct Step {
     std::vector<Step> members;  // ST_CONV_GROUP: the convs of one launch (cc is the group's);
                                 // ST_CONV_PAIR: the two convs, in order;
                                 // ST_CONV_CHAIN: the 3x3 and the one or two pointwise convs
-    std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1)
+    std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1);
+                                // ST_CONV_POOL: the max pooling of members[0]'s output
+    ConvPoolConfig cpc{1, 2, 5, 4, 8};  // ST_CONV_POOL
 };
 
 struct Xform {
@@ -884,6 +886,49 @@ void fuse_chains(neo_plan* P) {
     S.swap(out);
 }
 
+// NEO_PLAN_FUSE_POOL: a small-channel conv (a network stem) whose output
+// only a max pooling step reads runs with it in one launch (conv_pool.hip),
+// at the conv's place; the conv's output is then never stored.  Tuning
+// splits the pair back where the two launches measure faster.
+void fuse_conv_pool(neo_plan* P) {
+    std::vector<Step>& S = P->steps;
+    std::vector<char> drop(S.size(), 0);
+    for (size_t i = 0; i < S.size(); ++i) {
+        Step& c = S[i];
+        if (c.kind != ST_CONV || c.res >= 0) continue;
+        const Val& mv = P->vals[c.out];
+        if (mv.buf == kExtIn || mv.buf == P->ext_out_buf || mv.view || mv.alias_of >= 0 ||
+            mv.consumers != 1)
+            continue;
+        for (size_t j = i + 1; j < S.size(); ++j) {
+            if (S[j].kind != ST_MAXPOOL || S[j].in != c.out) continue;
+            if (!conv_pool_eligible(c.cs, S[j].ps)) break;
+            Step f{};
+            f.kind = ST_CONV_POOL;
+            f.node = c.node;
+            f.in = c.in;
+            f.out = S[j].out;
+            f.members = {c};
+            f.pools = {S[j]};
+            f.cpc = choose_conv_pool_config(c.cs, S[j].ps);
+            // launch-configuration override "fk,fp,waves,ty,tx" (tests and sweeps)
+            if (const char* ev = std::getenv("NEO_CONVPOOL_CONFIG")) {
+                ConvPoolConfig k{};
+                if (std::sscanf(ev, "%d,%d,%d,%d,%d", &k.fk, &k.fp, &k.waves, &k.ty, &k.tx) == 5 &&
+                    conv_pool_config_valid(c.cs, S[j].ps, k))
+                    f.cpc = k;
+            }
+            c = f;
+            drop[j] = 1;
+            break;
+        }
+    }
+    std::vector<Step> out;
+    for (size_t j = 0; j < S.size(); ++j)
+        if (!drop[j]) out.push_back(S[j]);
+    S.swap(out);
+}
+
 float* val_ptr(const neo_plan* P, int v, const float* x_in, float* y_out) {
     const Val& val = P->vals[v];
     if (val.buf == kExtIn) return const_cast<float*>(x_in);
@@ -939,7 +984,7 @@ std::string describe(const neo_plan* P) {
     }
     o << "],\"n_transforms\":" << P->xforms.size() << ",\"steps\":[";
     static const char* kinds[] = {"transform", "conv", "maxpool", "avgpool", "gap", "dense", "copy",
-                                  "conv_group", "conv_pair", "conv_chain"};
+                                  "conv_group", "conv_pair", "conv_chain", "conv_pool"};
     for (size_t i = 0; i < P->steps.size(); ++i) {
         const Step& s = P->steps[i];
         o << (i ? "," : "") << "{\"kind\":\"" << kinds[s.kind] << "\",\"node\":" << s.node
@@ -986,6 +1031,20 @@ std::string describe(const neo_plan* P) {
                 o << "}";
             }
             o << "]";
+        }
+        if (s.kind == ST_CONV_POOL) {
+            const Step& ms = s.members[0];
+            const PoolShape& ps = s.pools[0].ps;
+            o << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"config\":{\"tile\":["
+              << s.cpc.fk << "," << s.cpc.fp << "],\"waves\":" << s.cpc.waves << ",\"pooled_tile\":["
+              << s.cpc.ty << "," << s.cpc.tx << "]},\"members\":[{\"node\":" << ms.node
+              << ",\"in\":" << ms.in << ",\"out\":" << ms.out << ",\"res\":" << ms.res
+              << ",\"conv\":";
+            conv_json(ms);
+            o << "}],\"pool\":{\"kind\":\"maxpool\",\"node\":" << s.pools[0].node
+              << ",\"window\":[" << ps.R << "," << ps.S << "],\"stride\":[" << ps.sh << "," << ps.sw
+              << "],\"pad\":[" << ps.ph << "," << ps.pw << "],\"OH\":" << ps.OH << ",\"OW\":" << ps.OW
+              << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) {
@@ -1212,7 +1271,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
                             NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP |
-                            NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS))
+                            NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS | NEO_PLAN_FUSE_POOL))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -1231,6 +1290,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_POOL)) fuse_conv_pool(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
@@ -1395,6 +1455,13 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                                       val_ptr(P, a.out, x_nchw, y_out), n == 3 ? prm + b.w_off : nullptr,
                                       n == 3 && b.b_off >= 0 ? prm + b.b_off : nullptr,
                                       n == 3 ? val_ptr(P, b.out, x_nchw, y_out) : nullptr, st);
+                break;
+            }
+            case ST_CONV_POOL: {
+                const Step& c = s.members[0];
+                e = launch_conv_pool(c.cs, s.pools[0].ps, s.cpc, val_ptr(P, c.in, x_nchw, y_out),
+                                     prm + c.w_off, c.b_off >= 0 ? prm + c.b_off : nullptr,
+                                     val_ptr(P, s.out, x_nchw, y_out), st);
                 break;
             }
             case ST_MAXPOOL:
@@ -1613,6 +1680,38 @@ static int tune_plan(neo_plan* P) {
             } else {
                 next.push_back(c);
                 next.insert(next.end(), rest.begin(), rest.end());
+            }
+            continue;
+        }
+        if (s.kind == ST_CONV_POOL && !s.tuned) {
+            // the fused launch stays only where it beats the conv's and the
+            // pool's own best launches
+            const float* prm = P->d_params;
+            Step c = s.members[0];
+            const Step& pl = s.pools[0];
+            const float* bias = c.b_off >= 0 ? prm + c.b_off : nullptr;
+            float fused_us = 0.f, conv_us = 0.f, pool_us = 0.f;
+            ConvPoolConfig cpc = s.cpc;
+            rc = tune_conv_pool(c.cs, pl.ps, val_ptr(P, c.in, xin, yout), prm + c.w_off, bias,
+                                val_ptr(P, s.out, xin, yout), P->cap_stream, &cpc, &fused_us);
+            if (rc == NEO_OK)
+                rc = tune_conv(c.cs, true, val_ptr(P, c.in, xin, yout), prm + c.w_off, bias, nullptr,
+                               val_ptr(P, c.out, xin, yout), P->cap_stream, &c.cc, &conv_us);
+            if (rc == NEO_OK) {
+                GroupPool gp{pl.ps, true, val_ptr(P, pl.in, xin, yout), val_ptr(P, pl.out, xin, yout)};
+                rc = tune_pool(gp, P->cap_stream, &pool_us);
+            }
+            if (rc != NEO_OK) break;
+            c.tuned = true;
+            if (fused_us < conv_us + pool_us) {
+                Step keep = s;
+                keep.cpc = cpc;
+                keep.tuned = true;
+                keep.members[0] = c;
+                next.push_back(keep);
+            } else {
+                next.push_back(c);
+                next.push_back(pl);
             }
             continue;
         }

@@ -102,6 +102,12 @@ std::map<GroupKey, Entry> g_group_db;
 std::map<GroupKey, float> g_pool_db;
 std::map<GroupKey, float> g_pair_db;  // two pointwise convs in one launch -> time
 std::map<GroupKey, float> g_chain_db;  // a 3x3-led chain of 2 or 3 convs in one launch -> time
+struct PoolEntry {
+    ConvPoolConfig cfg;
+    float us;
+};
+std::map<GroupKey, PoolEntry> g_convpool_db;  // a stem conv and its max pool in one launch
+constexpr int kConvPoolInts = 13 + 12;        // conv N C H W K R S sh sw ph pw xb act, pool ints
 constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
 constexpr int kPoolShapeInts = 12;   // max N C H W R S sh sw ph pw xb
@@ -278,6 +284,49 @@ int tune_conv_chain(const ConvShape* s, int n, const float* x, const float* w0, 
     return NEO_OK;
 }
 
+int tune_conv_pool(const ConvShape& c, const PoolShape& p, const float* x, const float* w,
+                   const float* bias, float* y, hipStream_t st, ConvPoolConfig* best_out,
+                   float* us_out) {
+    GroupKey key{device_arch(), {c.N, c.C, c.H, c.W, c.K, c.R, c.S, c.sh, c.sw, c.ph, c.pw, c.xb,
+                                 c.act}};
+    const std::vector<int> pk = pool_ints(GroupPool{p, true, nullptr, nullptr});
+    key.second.insert(key.second.end(), pk.begin(), pk.end());
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_convpool_db.find(key);
+        if (it != g_convpool_db.end()) {
+            *best_out = it->second.cfg;
+            *us_out = it->second.us;
+            return NEO_OK;
+        }
+    }
+    ConvPoolConfig best = choose_conv_pool_config(c, p);
+    float best_us = 1e30f;
+    hipError_t e = hipSuccess;
+    {
+        Events ev;
+        for (const ConvPoolConfig& k : conv_pool_candidates(c, p)) {
+            float us = 0.f;
+            e = time_launch([&] { return launch_conv_pool(c, p, k, x, w, bias, y, st); }, st, ev.e0,
+                            ev.e1, &us);
+            if (e != hipSuccess) break;
+            if (us < best_us) {
+                best_us = us;
+                best = k;
+            }
+        }
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "conv-pool tuning");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_convpool_db[key] = PoolEntry{best, best_us};
+    }
+    *best_out = best;
+    *us_out = best_us;
+    return NEO_OK;
+}
+
 int tune_pool(const GroupPool& p, hipStream_t st, float* us_out) {
     const GroupKey key{device_arch(), pool_ints(p)};
     {
@@ -320,8 +369,11 @@ extern "C" {
 //   pool arch max N C H W R S sh sw ph pw xb us
 // one line per pair of pointwise convs in one launch:
 //   pair arch (N C H W K R S sh sw ph pw) x 2 residual us
-// and one line per 3x3-led chain of n (2 or 3) convs in one launch:
+// one line per 3x3-led chain of n (2 or 3) convs in one launch:
 //   chain arch n (N C H W K R S sh sw ph pw) x n residual us
+// and one line per stem conv with its max pooling in one launch:
+//   convpool arch N C H W K R S sh sw ph pw xb act (max N C H W R S sh sw ph pw xb)
+//            fk fp waves ty tx us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -359,8 +411,15 @@ int neo_tune_db_save(const char* path) {
         for (int x : kv.first.second) f << ' ' << x;
         f << ' ' << kv.second << '\n';
     }
+    for (const auto& kv : g_convpool_db) {
+        f << "convpool " << kv.first.first;
+        for (int x : kv.first.second) f << ' ' << x;
+        const ConvPoolConfig& c = kv.second.cfg;
+        f << ' ' << c.fk << ' ' << c.fp << ' ' << c.waves << ' ' << c.ty << ' ' << c.tx << ' '
+          << kv.second.us << '\n';
+    }
     return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                     g_chain_db.size())
+                     g_chain_db.size() + g_convpool_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -373,6 +432,7 @@ int neo_tune_db_load(const char* path) {
     std::map<Key, Entry> add;
     std::map<GroupKey, Entry> add_group;
     std::map<GroupKey, float> add_pool, add_pair, add_chain;
+    std::map<GroupKey, PoolEntry> add_convpool;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -425,6 +485,33 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 9, "convpool ") == 0) {
+            std::string tag;
+            GroupKey ck;
+            PoolEntry pe;
+            bool ok = (bool)(is >> tag >> ck.first) && read_ints(is, kConvPoolInts, ck.second) &&
+                      (bool)(is >> pe.cfg.fk >> pe.cfg.fp >> pe.cfg.waves >> pe.cfg.ty >> pe.cfg.tx >>
+                             pe.us);
+            if (ok) {  // the entry must name a configuration the kernel takes for its shapes
+                const std::vector<int>& v = ck.second;
+                ConvShape cs{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7], v[8], v[9], v[10],
+                             (v[2] + 2 * v[9] - v[5]) / v[7] + 1, (v[3] + 2 * v[10] - v[6]) / v[8] + 1,
+                             0, 0, v[12]};
+                cs.xb = v[11];
+                cs.yb = 16;
+                PoolShape ps{v[14], v[15], v[16], v[17], v[18], v[19], v[20], v[21], v[22], v[23],
+                             0, 0, 0, 0};
+                ps.OH = (ps.H + 2 * ps.ph - ps.R) / ps.sh + 1;
+                ps.OW = (ps.W + 2 * ps.pw - ps.S) / ps.sw + 1;
+                ps.xb = v[24];
+                ok = v[7] > 0 && v[8] > 0 && ps.sh > 0 && ps.sw > 0 &&
+                     conv_pool_config_valid(cs, ps, pe.cfg);
+            }
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_convpool[ck] = pe;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -451,6 +538,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add_pool) g_pool_db[kv.first] = kv.second;
     for (const auto& kv : add_pair) g_pair_db[kv.first] = kv.second;
     for (const auto& kv : add_chain) g_chain_db[kv.first] = kv.second;
+    for (const auto& kv : add_convpool) g_convpool_db[kv.first] = kv.second;
     return n;
 }
 
@@ -461,12 +549,13 @@ void neo_tune_db_clear(void) {
     g_pool_db.clear();
     g_pair_db.clear();
     g_chain_db.clear();
+    g_convpool_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                 g_chain_db.size());
+                 g_chain_db.size() + g_convpool_db.size());
 }
 
 }  // extern "C"

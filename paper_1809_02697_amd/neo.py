@@ -32,6 +32,7 @@ PLAN_GROUP = 32
 PLAN_FUSE_GAP = 64
 PLAN_FUSE_PAIRS = 128
 PLAN_FUSE_CHAINS = 256
+PLAN_FUSE_POOL = 512
 BLOCK = 16
 SEARCH_BLOCKS = (0, 4, 8, 16, 32, 64)   # layout index space of neo_layout_search
 

@@ -45,7 +45,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(HERE, "csrc", f)
-               for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip")]
+               for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip",
+                         "conv_pool.hip")]
 PEAK = 157.3
 SIMDS = 1024         # 256 CUs x 4
 CLOCK_MHZ = 2400.0   # engine clock under load (bench.py's engine_clock)
@@ -87,7 +88,8 @@ def _rows(path):
 
 
 def is_conv(name):
-    return "conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name
+    return ("conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name or
+            "conv_pool_small" in name)
 
 
 def is_neo(name):

@@ -431,6 +431,19 @@ def tiny_graph(seed=7, N=2, C=5, H=13, W=11):
     return b.finish(_normal_input((N, C, H, W)))
 
 
+def stem_graph(seed=9, N=1, C=3, H=224, W=224, K=64, R=7, S=None, stride=2, pad=3,
+               pool=(3, 2, 1), input_dist="normal"):
+    """A network stem alone: conv (batch norm, ReLU) and the max pooling that
+    reads it, as the network output.  pool = (window, stride, pad)."""
+    b = _Builder("stem", (N, C, H, W), np.random.Generator(np.random.PCG64(seed)))
+    x = b.conv(0, K, R, S, stride=stride, pad=pad, name="stem")
+    x = b.pool("maxpool", x, pool[0], pool[1], pool[2], name="pool")
+    b.output(x)
+    if input_dist == "uniform":
+        return b.finish(lambda rng: _f32(rng.uniform(-1.0, 1.0, size=(N, C, H, W))))
+    return b.finish(_normal_input((N, C, H, W)))
+
+
 def vgg_like_tiny(seed=8, N=2):
     """A small plain network whose flatten follows a real spatial map (so the
     exit transform is a real permutation), with two dense layers."""
