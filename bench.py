@@ -303,10 +303,12 @@ def engine_clock(torch=None, plan=None, x=None, out=None, busy_runs=4000):
             torch.cuda.synchronize()
 
 
-def layer_table(torch, plan, x, out, reps, cold=True):
+def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False):
     """Each conv step of the plan timed alone (its kernel(s) as the plan
     launches them), grouped by distinct shapes, residuals and launch
-    configuration."""
+    configuration.  cold: also time every step with the caches flushed
+    (cold_hbm_only: only the steps whose algorithmic intensity is below the
+    ridge, the HBM-bound ones)."""
     d = plan.describe()
     plan.run(x, out)      # intermediate buffers hold real activations
     torch.cuda.synchronize()
@@ -316,7 +318,10 @@ def layer_table(torch, plan, x, out, reps, cold=True):
                      c["W"], c["N"], c["ic_bn"], c["oc_bn"], res) for c, res in members)
         key += (json.dumps(cfg, sort_keys=True),)
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
-        cold_us = time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4)) if cold else 0.0
+        f_, b_ = launch_costs(members)
+        hbm = f_ / b_ * PEAK_HBM_GBS / 1e3 < PEAK_FP32_TFLOPS
+        cold_us = (time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4))
+                   if cold and (hbm or not cold_hbm_only) else 0.0)
         if key in rows:
             rows[key]["uses"] += 1
             rows[key]["_t"].append(us)
@@ -339,7 +344,7 @@ def layer_table(torch, plan, x, out, reps, cold=True):
                  bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_FP32_TFLOPS else "hbm",
                  pct_mfma=round(100 * tf / PEAK_FP32_TFLOPS, 1),
                  pct_hbm=round(100 * gbs / PEAK_HBM_GBS, 1), pct_roof=round(100 * tf / roof, 1))
-        if cold:
+        if cold and cold_us > 0:
             r.update(cold_us=round(cold_us, 2),
                      cold_hbm_gbs=round(r["bytes"] / (cold_us * 1e-6) / 1e9, 1))
         out_rows.append(r)
@@ -564,7 +569,7 @@ def main():
         p32 = neo.Plan(g32, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
         x32 = torch.from_numpy(g32.x).cuda()
         o32 = p32.run(x32)
-        layers_b32 = layer_table(torch, p32, x32, o32, 10, cold=False)
+        layers_b32 = layer_table(torch, p32, x32, o32, 10, cold_hbm_only=True)
         tf32 = sum(r["flops"] * r["uses"] for r in layers_b32) / \
             sum(r["us"] * 1e-6 * r["uses"] for r in layers_b32) / 1e12
         for r in layers_b32:

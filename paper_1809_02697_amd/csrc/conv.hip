@@ -150,6 +150,10 @@ ConvArgs make_args(const ConvShape& s, const ConvConfig& c, int G, const float* 
 hipError_t launch_conv2d(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
                          bool wmfma, const float* bias, const float* res, float* y, float* ws,
                          hipStream_t st) {
+    if (c.fp == 0) {  // the streaming pointwise kernel (filter in kernel order)
+        if (!wmfma || !conv_stream_config_valid(s, c)) return hipErrorInvalidValue;
+        return launch_conv_stream(s, c, x, w, bias, res, y, st);
+    }
     if (!conv_config_valid(c) || !conv_blocks_valid(s)) return hipErrorInvalidValue;
     if (s.gap && s.N != 1) return hipErrorInvalidValue;
     const int G = conv_group(s, c);

@@ -48,8 +48,12 @@ struct ConvPoolArgs {
     int slots;         // conv outputs the workgroup can hold (WAVES * FP * 16)
 };
 
-template <int FK, int FP, int WAVES>
+// KR, KU: the filter rows and column groups when known at compile time (7 and
+// 2 for a 7x7 filter), so the step loop unrolls; 0: from P at run time.
+template <int FK, int FP, int WAVES, int KR, int KU>
 __global__ __launch_bounds__(WAVES * 64) void conv_pool_small(ConvPoolArgs P) {
+    constexpr bool kFixedT = KR > 0;
+    const int T = kFixedT ? KR * KU : P.T;
     extern __shared__ v4f lds[];
     v4f* patch = lds;                                 // [prows][pcols] pixels, channels 0..3
     v4f* filt = patch + P.prows * P.pcols;            // [FK][T][64 lanes]
@@ -122,25 +126,33 @@ __global__ __launch_bounds__(WAVES * 64) void conv_pool_small(ConvPoolArgs P) {
     for (int f = 0; f < FK; ++f)
 #pragma unroll
         for (int p = 0; p < FP; ++p) acc[f][p] = v4f{0.f, 0.f, 0.f, 0.f};
+    auto step = [&](int st, int off) {
+        v4f a[FK], b[FP];
+#pragma unroll
+        for (int f = 0; f < FK; ++f) a[f] = filt[(f * T + st) * 64 + lane];
+#pragma unroll
+        for (int p = 0; p < FP; ++p) b[p] = patch[bq[p] + off];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p)
+                    acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[f][t], b[p][t], acc[f][p], 0, 0, 0);
+    };
     if (wave * FP * 16 < NQ) {
-        int r = 0, u = 0;
-        for (int st = 0; st < P.T; ++st) {
-            const int off = r * P.pcols + 4 * u;
-            v4f a[FK], b[FP];
+        if constexpr (kFixedT) {
+            // steps (r, u) row by row
 #pragma unroll
-            for (int f = 0; f < FK; ++f) a[f] = filt[(f * P.T + st) * 64 + lane];
-#pragma unroll
-            for (int p = 0; p < FP; ++p) b[p] = patch[bq[p] + off];
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int f = 0; f < FK; ++f)
-#pragma unroll
-                    for (int p = 0; p < FP; ++p)
-                        acc[f][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[f][t], b[p][t], acc[f][p], 0, 0, 0);
-            if (++u == P.U) {
-                u = 0;
-                ++r;
+            for (int st = 0; st < KR * KU; ++st) step(st, (st / KU) * P.pcols + 4 * (st % KU));
+        } else {
+            int r = 0, u = 0;
+            for (int st = 0; st < T; ++st) {
+                step(st, r * P.pcols + 4 * u);
+                if (++u == P.U) {
+                    u = 0;
+                    ++r;
+                }
             }
         }
     }
@@ -215,7 +227,10 @@ constexpr size_t kMaxLds = 64 * 1024;
 
 template <int FK, int FP, int WAVES>
 hipError_t launch_t(const ConvPoolArgs& a, size_t lds, int wgs, hipStream_t st) {
-    hipLaunchKernelGGL((conv_pool_small<FK, FP, WAVES>), dim3(wgs), dim3(WAVES * 64), lds, st, a);
+    if (a.R == 7 && a.U == 2)  // a 7x7 filter: the step loop unrolled
+        hipLaunchKernelGGL((conv_pool_small<FK, FP, WAVES, 7, 2>), dim3(wgs), dim3(WAVES * 64), lds, st, a);
+    else
+        hipLaunchKernelGGL((conv_pool_small<FK, FP, WAVES, 0, 0>), dim3(wgs), dim3(WAVES * 64), lds, st, a);
     return hipGetLastError();
 }
 

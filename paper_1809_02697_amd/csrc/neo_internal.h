@@ -82,6 +82,23 @@ int conv_prepare(const char* fn, const float* x, int x_block, int N, int C, int 
                  int y_block, int y_blk_offset, int y_blk_total, ConvShape* shape,
                  ConvConfig* config, const float** residual);
 
+// Pointwise convolutions as a stream (conv_stream.hip): a launch
+// configuration with fp = 0 names the streaming kernel, whose waves keep fk
+// output blocks' filter in registers and walk 16-pixel groups, `waves` waves
+// per SIMD of the chip.  1x1, stride 1, no padding, NCHW16c in and out, at
+// most 8 input blocks, fk x input blocks <= 16; filter in kernel order.  The
+// results are bit-identical to the tile kernel with one wave and no split.
+bool conv_stream_eligible(const ConvShape& s);
+bool conv_stream_config_valid(const ConvShape& s, const ConvConfig& c);
+hipError_t launch_conv_stream(const ConvShape& s, const ConvConfig& c, const float* x, const float* w,
+                              const float* bias, const float* res, float* y, hipStream_t st);
+// A configuration of either kernel, independent of the shape (results files).
+inline bool conv_any_config_valid(const ConvConfig& c) {
+    const bool stream = c.fp == 0 && c.split == 1 && (c.fk == 1 || c.fk == 2 || c.fk == 4) &&
+                        (c.waves == 1 || c.waves == 2 || c.waves == 4 || c.waves == 8);
+    return stream || conv_config_valid(c);
+}
+
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
 // or null; res: NCHW[yb]c [N][ceil(K/yb)][OH][OW][yb] or null; y: NCHW[yb]c

@@ -788,6 +788,9 @@ void fuse_gap(neo_plan* P) {
         for (size_t v = 0; v < P->vals.size(); ++v) ok = ok && !(P->vals[v].view && is_pooled((int)v));
         if (!ok || dense.empty()) continue;
         S[pi].cs.gap = 1;
+        // the streaming pointwise kernel has no folded pool: the tile kernel's
+        // configuration for this shape instead
+        if (S[pi].cc.fp == 0) S[pi].cc = choose_conv_config(S[pi].cs);
         const int hw = iv.H * iv.W;
         for (size_t k : dense) {
             S[k].in = in;  // reads the conv's sums (and so runs after it)
@@ -1725,6 +1728,7 @@ static int tune_plan(neo_plan* P) {
                            s.b_off >= 0 ? prm + s.b_off : nullptr,
                            s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
                            val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
+            if (s.cs.gap && s.cc.fp == 0) s.cc = choose_conv_config(s.cs);
             s.tuned = rc == NEO_OK;
         }
         next.push_back(s);

@@ -82,6 +82,17 @@ std::vector<ConvConfig> candidates(const ConvShape& s) {
     return out;
 }
 
+// The streaming pointwise kernel's configurations for a shape it takes.
+std::vector<ConvConfig> stream_candidates(const ConvShape& s) {
+    std::vector<ConvConfig> out;
+    for (int fk : {1, 2, 4})
+        for (int wv : {1, 2, 4, 8}) {
+            const ConvConfig c{fk, 0, 1, wv};
+            if (conv_stream_config_valid(s, c)) out.push_back(c);
+        }
+    return out;
+}
+
 }  // namespace
 
 bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out) {
@@ -89,6 +100,8 @@ bool tuned_config(const ConvShape& s, bool wmfma, ConvConfig* out) {
     std::lock_guard<std::mutex> lk(g_mu);
     auto it = g_db.find(key_of(s, wmfma, arch));
     if (it == g_db.end()) return false;
+    // a stored streaming configuration the shape cannot take is ignored
+    if (it->second.cfg.fp == 0 && !conv_stream_config_valid(s, it->second.cfg)) return false;
     *out = it->second.cfg;
     return true;
 }
@@ -134,7 +147,9 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
             return NEO_OK;
         }
     }
-    const std::vector<ConvConfig> cands = candidates(s);
+    std::vector<ConvConfig> cands = candidates(s);
+    if (wmfma)
+        for (const ConvConfig& c : stream_candidates(s)) cands.push_back(c);
     size_t ws_bytes = 0;
     for (const ConvConfig& c : cands) ws_bytes = std::max(ws_bytes, conv_workspace_bytes(s, c));
     float* ws = nullptr;
@@ -526,7 +541,7 @@ int neo_tune_db_load(const char* path) {
         if (!(is >> k.arch >> k.N >> k.C >> k.H >> k.W >> k.K >> k.R >> k.S >> k.sh >> k.sw >> k.ph >>
               k.pw >> k.wmfma >> k.xb >> k.yb >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >>
               v.us) ||
-            !conv_config_valid(v.cfg) || !key_blocks_valid(k))
+            !conv_any_config_valid(v.cfg) || !key_blocks_valid(k) || (v.cfg.fp == 0 && !k.wmfma))
             return fail(NEO_ERR_INVALID_ARG,
                         "neo_tune_db_load: malformed line " + std::to_string(lineno));
         add[k] = v;

@@ -444,6 +444,17 @@ def stem_graph(seed=9, N=1, C=3, H=224, W=224, K=64, R=7, S=None, stride=2, pad=
     return b.finish(_normal_input((N, C, H, W)))
 
 
+def pointwise_graph(seed=10, N=2, C=64, H=56, W=56, K=64, residual=False):
+    """One 1x1 conv (batch norm, ReLU) over the input, with, when `residual`,
+    another 1x1 conv of the input (batch norm, no activation) added to it
+    before the ReLU."""
+    b = _Builder("pointwise", (N, C, H, W), np.random.Generator(np.random.PCG64(seed)))
+    sc = b.conv(0, K, 1, act="none", name="shortcut") if residual else -1
+    x = b.conv(0, K, 1, residual=sc, name="pointwise")
+    b.output(x)
+    return b.finish(lambda rng: _f32(rng.uniform(-1.0, 1.0, size=(N, C, H, W))))
+
+
 def vgg_like_tiny(seed=8, N=2):
     """A small plain network whose flatten follows a real spatial map (so the
     exit transform is a real permutation), with two dense layers."""
