@@ -24,8 +24,9 @@ Printed JSON line:
                the 256 MB MALL between runs)
   layers       per distinct conv shape: us, TFLOP/s, algorithmic GB/s, % of
                the binding roofline, and the launch configuration (warm);
-               cold_us / cold_hbm_gbs: the same launch after a 512 MB write
-               has flushed the caches, so its operands come from HBM
+               cold_us / cold_hbm_gbs: the same launch after a 512 MB read
+               has flushed the caches, so its operands come from HBM;
+               cold_copy_gbs: a plain copy under the same protocol
   models       end-to-end latency of ResNet-50 / VGG-16 / Inception-v3 at
                batch 1 and ResNet-50 at batch 32 for the ablation of Table 3:
                "naive" (transforms around every blocked operation), "eliminated"
@@ -200,24 +201,39 @@ def time_graph(torch, fn, reps, rounds=3):
 _FLUSH = None
 
 
-def time_cold(torch, fn, reps):
-    """Average time of fn() with caches cold: before each launch a 512 MB
-    buffer (twice the 256 MB MALL, far above the L2s) is overwritten, so the
-    launch's operands come from HBM.  HIP events bracket the launch alone."""
+def _flush_read(torch):
+    """Read a 512 MB buffer (twice the 256 MB MALL, far above the L2s) with the
+    library's global average pool, which writes only 512 KB: the caches then
+    hold its clean lines, so a following launch reads its operands from HBM
+    and evicts nothing dirty.  (Overwriting the buffer instead leaves 256 MB
+    of dirty lines whose write-back competes with the launch's reads: a plain
+    231 MB copy measured 4.3 TB/s after such a write and 5.7 TB/s after the
+    read.)"""
     global _FLUSH
+    from paper_1809_02697_amd import neo
     if _FLUSH is None:
-        _FLUSH = torch.empty(128 * 2 ** 20, device="cuda")
-    stream = torch.cuda.current_stream()
-    tot = 0.0
-    for _ in range(reps):
-        _FLUSH.fill_(1.0)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        tot += e0.elapsed_time(e1) * 1e3
-    return tot / reps
+        _FLUSH = (torch.ones((1, 8192, 32, 32, 16), device="cuda"),
+                  torch.empty((1, 8192, 1, 1, 16), device="cuda"))
+    neo.global_avgpool_blocked(_FLUSH[0], 8192 * 16, out=_FLUSH[1])
+
+
+def time_cold(torch, fn, reps):
+    """Average time of fn() with caches cold (_flush_read before every launch):
+    `reps` (flush, launch) pairs captured in one graph, minus the same number
+    of flushes alone, HIP events on the replay stream (us)."""
+    both = time_graph(torch, lambda: (_flush_read(torch), fn()), reps, rounds=2)
+    flush = time_graph(torch, lambda: _flush_read(torch), reps, rounds=2)
+    return max(both - flush, 0.0)
+
+
+def cold_copy_gbs(torch, mb=256, reps=8):
+    """HBM rate of a plain device-to-device copy of `mb` MB under the cold
+    protocol of time_cold (bytes read + written per second): what a kernel
+    with no arithmetic reaches."""
+    a = torch.ones(mb * 2 ** 18, device="cuda")
+    b = torch.empty_like(a)
+    us = time_cold(torch, lambda: b.copy_(a), reps)
+    return round(2 * mb * 2 ** 20 / (us * 1e-6) / 1e9, 1)
 
 
 def e2e_ms(torch, plan, x, out, steps, warmup):
@@ -320,7 +336,7 @@ def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False):
         us = time_graph(torch, lambda: plan.run_step(i, x, out), reps)
         f_, b_ = launch_costs(members)
         hbm = f_ / b_ * PEAK_HBM_GBS / 1e3 < PEAK_FP32_TFLOPS
-        cold_us = (time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 4))
+        cold_us = (time_cold(torch, lambda: plan.run_step(i, x, out), max(4, reps // 2))
                    if cold and (hbm or not cold_hbm_only) else 0.0)
         if key in rows:
             rows[key]["uses"] += 1
@@ -577,6 +593,7 @@ def main():
         p32.destroy()
         del g32, x32
         print(f"[bench] batch-32 conv layers: {tf32:.2f} TFLOP/s", file=sys.stderr, flush=True)
+    copy_gbs = None if args.no_layers else cold_copy_gbs(torch)
 
     cpu = None
     if not args.no_cpu:
@@ -612,6 +629,7 @@ def main():
         "cpu_baseline": cpu,
         "layers": layers,
         "layers_b32": layers_b32,
+        "cold_copy_gbs": copy_gbs,
         "models": models,
     }
     print(json.dumps(rec))
