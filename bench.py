@@ -70,7 +70,7 @@ def plan_schemes(desc):
     """{conv node: (ic_bn, oc_bn)} of a plan description."""
     out = {}
     for s in desc["steps"]:
-        for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair", "conv_chain")
+        for m in (s["members"] if s["kind"] in ("conv_group", "conv_pair", "conv_chain", "conv_pool")
                   else [s] if s["kind"] == "conv" else []):
             out[m["node"]] = (m["conv"]["ic_bn"], m["conv"]["oc_bn"])
     return out

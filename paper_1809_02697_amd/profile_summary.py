@@ -46,7 +46,7 @@ ROOT = os.path.dirname(HERE)
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SRCS = [os.path.join(HERE, "csrc", f)
                for f in ("conv_kernel.h", "conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip",
-                         "conv_pool.hip")]
+                         "conv_pool.hip", "conv_stream.hip")]
 PEAK = 157.3
 SIMDS = 1024         # 256 CUs x 4
 CLOCK_MHZ = 2400.0   # engine clock under load (bench.py's engine_clock)
@@ -89,7 +89,7 @@ def _rows(path):
 
 def is_conv(name):
     return ("conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name or
-            "conv_pool_small" in name)
+            "conv_pool_small" in name or "conv1x1_stream" in name)
 
 
 def is_neo(name):
