@@ -163,7 +163,7 @@ def stepwise_forward_durations(trace_path, n_steps):
 
 
 def graph_forward_durations(trace_path, n_steps):
-    """Sum of conv durations per graph-replayed forward before the spin kernel
+    """Sum of conv durations per back-to-back forward before the spin kernel
     (the profiled e2e and latency runs), and the forward spans.  A forward
     starts at a dispatch of the kernel that starts the step-by-step ones."""
     rows = sorted(_rows(trace_path), key=lambda r: int(r["Start_Timestamp"]))
@@ -210,6 +210,8 @@ def main(run_dir):
     tr_sum = _median([sum(f) for f in fwds])
     per_step = [_median([f[i] for f in fwds]) for i in range(n)]
     g_sums, g_spans = graph_forward_durations(trace, n_steps)
+    launch = bench["config"]["plan_choice"].get("launch", "graph")
+    mode = "one hipGraph replay" if launch == "graph" else "steps launched on the stream"
     tr_tf = sum(flops) / (tr_avg * n * 1e-6) / 1e12
 
     # -- traffic, warm and cold -------------------------------------------------------------
@@ -262,12 +264,12 @@ def main(run_dir):
           f"- roofline.frac from the trace: {tr_tf:.2f} TFLOP/s / {PEAK} = "
           f"**{tr_tf / PEAK:.4f}**; bench.py: {bench['roofline']['achieved']} TFLOP/s, frac "
           f"**{bench['roofline']['frac']}**.",
-          f"- bench.py e2e ResNet-50 batch 1 (graph replay): {bench['ms_per_step']} ms per forward "
+          f"- bench.py e2e ResNet-50 batch 1 ({mode}): {bench['ms_per_step']} ms per forward "
           f"(step by step between events: {bench.get('stepwise_forward_ms', 'n/a')} ms).  The "
-          f"traced forward's conv launches ({tr_sum:.1f} us) fit in the graph forward.",
-          f"- Under the profiler, graph replays run slower: the {len(g_sums)} profiled graph forwards "
-          f"span {_median(g_spans):.1f} us with {_median(g_sums):.1f} us of conv dispatches "
-          f"({_median(g_sums) / n:.2f} us per launch); these are not used.", "",
+          f"traced forward's conv launches ({tr_sum:.1f} us) fit in the e2e forward.",
+          f"- Under the profiler, back-to-back forwards run slower: the {len(g_sums)} profiled e2e "
+          f"forwards ({mode}) span {_median(g_spans):.1f} us with {_median(g_sums):.1f} us of conv "
+          f"dispatches ({_median(g_sums) / n:.2f} us per launch); these are not used.", "",
           "rocprofv3 --stats (the profiled bench run; all dispatches of the run):", "",
           "| kernel | calls | avg us | total % |", "|---|---:|---:|---:|"]
     stats = _rows(os.path.join(run_dir, "prof_bench", "bench_kernel_stats.csv"))

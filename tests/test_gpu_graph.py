@@ -213,8 +213,9 @@ def test_tuned_resnet50_end_to_end(neo):
 
 def test_bench_headline_plan_matches_oracle(neo):
     """The plan bench.py times for ResNet-50 batch 1 -- global search, horizontal
-    fusion, tuned, graph replay, the faster of the searched and one-block
-    plans -- against the oracle, replayed several times."""
+    fusion, tuned, the faster of the searched and one-block plans and of graph
+    replay and stream launches -- against the oracle, run several times; the
+    same plan in the other launch mode gives the same bits."""
     import os
     import sys
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
@@ -222,6 +223,8 @@ def test_bench_headline_plan_matches_oracle(neo):
     torch = torch_cuda()
     g = wl.resnet50(1)
     p, info = bench.headline_plan(neo, g, None, torch)
+    assert info["launch"] in ("graph", "stream")
+    d = p.describe()
     x = dev(g.x)
     out = torch.empty((1, 1000), device="cuda")
     ref = oracle_output(g)
@@ -232,4 +235,13 @@ def test_bench_headline_plan_matches_oracle(neo):
         first = y if first is None else first
         np.testing.assert_array_equal(y, first)
     p.destroy()
-    _gate_network(first, ref, g, f"bench headline plan ({info['kept']})")
+    base = (neo.PLAN_TUNE | neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS |
+            neo.PLAN_FUSE_CHAINS | neo.PLAN_FUSE_POOL)
+    other = neo.Plan(g, flags=base | (0 if d["hipgraph"] else neo.PLAN_HIPGRAPH),
+                     schemes=bench.plan_schemes(d))
+    assert bench.same_steps(other.describe(), d)
+    out.fill_(0.0)
+    other.run(x, out)
+    np.testing.assert_array_equal(host(out), first)
+    other.destroy()
+    _gate_network(first, ref, g, f"bench headline plan ({info['kept']}, {info['launch']})")
