@@ -166,6 +166,38 @@ int neo_pack_filter(const float* w_kcrs, int K, int C, int R, int S, int ic_bn, 
                     float* w_packed, neo_stream_t stream);
 
 /*
+ * Winograd convolution F(2x2, 3x3) -- the fast algorithm the paper leaves as
+ * future work beside its direct convolution (Sections 1 and 5); the nested
+ * minimal filtering algorithm of Lavin and Gray (2016).  The same result as
+ * neo_conv2d_blocked with R = S = 3 and stride 1, computed per 2x2 output
+ * tile as A^T [ sum_c (G g G^T) .* (B^T d B) ] A over the tile's 4x4 input
+ * patch d, with
+ *   B^T = [1 0 -1 0; 0 1 1 0; 0 -1 1 0; 0 1 0 -1],
+ *   G   = [1 0 0; 1/2 1/2 1/2; 1/2 -1/2 1/2; 0 0 1],
+ *   A^T = [1 1 1 0; 0 1 -1 -1]:
+ * 4 multiplications per output and input channel instead of 9.  The rounding
+ * differs from the direct sum's (results agree within float32 tolerance, not
+ * bit for bit).
+ *
+ * neo_winograd_filter: the transformed filter U = G g G^T of a KCRS
+ * [K][C][3][3] filter, computed in double and rounded once, zero padded:
+ * ceil(K/16) * ceil(C/16) * 16 * 256 floats, block (kb, cb, e) for element
+ * e = 4i + j of the 4x4 tile holding U[k][c] at ((c%16)/4 * 16 + k%16) * 4 +
+ * c%4.  w_kcrs and u are device buffers.
+ *
+ * neo_conv2d_winograd: x, bias, ep, y and the output view as for
+ * neo_conv2d_blocked (NCHW16c), u from neo_winograd_filter; pads >= 0 with
+ * OH = H + 2 pad_h - 2 >= 1 (and OW).  C must exceed 4 (smaller inputs are
+ * network stems: NEO_ERR_UNSUPPORTED).  Like neo_conv2d_blocked it may split
+ * the reduction over workgroups, with the same per-stream workspace (grown
+ * outside stream capture only).
+ */
+int neo_winograd_filter(const float* w_kcrs, int K, int C, float* u, neo_stream_t stream);
+int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float* u, int K,
+                        const float* bias, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
+                        int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+
+/*
  * Batch-norm folding (inference simplification inherited by the paper,
  * Section 3): with scale[k] = gamma[k] / sqrt(var[k] + eps),
  *   w_out[k][c][r][s] = w[k][c][r][s] * scale[k]
@@ -339,7 +371,15 @@ enum neo_plan_flags {
      * pooling, bit for bit.  With NEO_PLAN_TUNE the fused launch is kept only
      * where it measures faster than the two launches.  Not in the paper: a
      * batch-1 GPU design choice. */
-    NEO_PLAN_FUSE_POOL = 512
+    NEO_PLAN_FUSE_POOL = 512,
+    /* Run the 3x3 stride-1 convs that are launched alone (NCHW16c, more than
+     * 4 input channels) by Winograd F(2x2, 3x3) (neo_conv2d_winograd: the
+     * paper's future work): the plan also prepares each such conv's
+     * transformed filter.  With NEO_PLAN_TUNE the local search times the
+     * Winograd kernel's configurations beside the direct kernel's and keeps
+     * the faster algorithm per conv.  Results match the oracle within the
+     * float32 tolerance, not bit for bit. */
+    NEO_PLAN_WINOGRAD = 1024
 };
 
 /*
@@ -401,7 +441,10 @@ void neo_plan_destroy(neo_plan* plan);
  * launch's configuration and time; (GPU architecture, a pooling step's shape) -> its
  * time alone; (GPU architecture, the shapes of a pair of pointwise convs, residual) ->
  * the pair's time in one launch; (GPU architecture, the shapes of a 3x3-led chain of two
- * or three convs, residual) -> the chain's time in one launch.  Text file, one entry per line.  save returns the number of entries
+ * or three convs, residual) -> the chain's time in one launch; (GPU architecture, a stem
+ * conv's and its max pooling's shapes) -> the fused launch's configuration and time;
+ * (GPU architecture, a 3x3 stride-1 conv's shape) -> its Winograd configuration and time.
+ * Text file, one entry per line.  save returns the number of entries
  * written, load the number read, size the number held (entries are merged; a malformed
  * line fails the whole load with NEO_ERR_INVALID_ARG). */
 int neo_tune_db_save(const char* path);

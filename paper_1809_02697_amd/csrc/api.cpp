@@ -212,6 +212,18 @@ bool env_config(ConvConfig* c) {
     return true;
 }
 
+// Optional override of the Winograd launch configuration, "fk,fp,split,waves".
+bool env_wino_config(const ConvShape& s, ConvConfig* c) {
+    const char* v = std::getenv("NEO_WINO_CONFIG");
+    if (!v || !*v) return false;
+    ConvConfig t{1, 1, 1, 1};
+    if (std::sscanf(v, "%d,%d,%d,%d", &t.fk, &t.fp, &t.split, &t.waves) != 4 ||
+        !wino_config_valid(s, t))
+        return false;
+    *c = t;
+    return true;
+}
+
 }  // namespace
 
 namespace neo {
@@ -335,6 +347,40 @@ int neo_pack_filter(const float* w_kcrs, int K, int C, int R, int S, int ic_bn, 
     CHECK_SIZE((long)cdiv(K, oc_bn) * oc_bn * cdiv(C, ic_bn) * ic_bn * R * S);
     hipError_t e = launch_pack_filter(w_kcrs, K, C, R, S, ic_bn, oc_bn, w_packed, (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_pack_filter launch");
+}
+
+int neo_winograd_filter(const float* w_kcrs, int K, int C, float* u, neo_stream_t stream) {
+    if (!w_kcrs || !u) return fail(NEO_ERR_INVALID_ARG, "neo_winograd_filter: NULL buffer");
+    CHECK_POS(K); CHECK_POS(C);
+    if ((long)cdiv(K, 16) * cdiv(C, 16) * 16 * 256 >= (1L << 29))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_winograd_filter: transformed filter of 2 GiB or more");
+    hipError_t e = launch_wino_filter(w_kcrs, K, C, u, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_winograd_filter launch");
+}
+
+int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float* u, int K,
+                        const float* bias, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
+                        int y_cblk_offset, int y_cblk_total, neo_stream_t stream) {
+    ConvShape s;
+    ConvConfig cfg;
+    const float* res = nullptr;
+    int rc = conv_prepare("neo_conv2d_winograd", x, 16, N, C, H, W, u, K, 3, 3, bias, 1, 1, pad_h,
+                          pad_w, ep, y, 16, y_cblk_offset, y_cblk_total, &s, &cfg, &res);
+    if (rc != NEO_OK) return rc;
+    if (conv_small_c(s))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_winograd: needs more than 4 input channels "
+                                         "(use neo_conv2d_blocked)");
+    if (wino_filter_floats(s) >= (1UL << 29))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_conv2d_winograd: transformed filter of 2 GiB or more");
+    cfg = choose_wino_config(s);
+    env_wino_config(s, &cfg);
+    float* ws = nullptr;
+    if (cfg.split > 1) {
+        rc = stream_workspace((hipStream_t)stream, conv_workspace_bytes(s, cfg), &ws);
+        if (rc != NEO_OK) return rc;
+    }
+    hipError_t e = launch_wino(s, cfg, x, u, bias, res, y, ws, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_winograd launch");
 }
 
 int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,

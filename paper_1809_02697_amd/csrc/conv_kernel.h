@@ -716,6 +716,17 @@ __global__ __launch_bounds__(256) void split_reduce(ConvArgs a) {
     }
 }
 
+// The second pass alone, NCHW16c -> NCHW16c (also for the Winograd kernel,
+// whose split partials are raw outputs in the same layout).  Reads a.N, KB,
+// OH, OW, ws, split, bias, res, act, y, y_off, y_tot.
+inline hipError_t launch_split_reduce(const ConvArgs& a, hipStream_t st) {
+    const long total = (long)a.N * a.KB * a.OH * a.OW * 4;
+    long blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(split_reduce<false>, dim3((unsigned)blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 template <int FK, int FP, int G, bool SMALLC, bool WMFMA, int WAVES, bool XY>
 hipError_t launch_t(const ConvArgs& a, hipStream_t st) {
     const int wgs = cdiv(a.M, 16 * FP) * cdiv(a.KBk, FK) * a.split;

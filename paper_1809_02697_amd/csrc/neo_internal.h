@@ -99,6 +99,26 @@ inline bool conv_any_config_valid(const ConvConfig& c) {
     return stream || conv_config_valid(c);
 }
 
+// Winograd F(2x2, 3x3) convolution (winograd.hip): 3x3, stride 1, NCHW16c in
+// and out, more than 4 input channels.  Launch configuration: fk output
+// blocks and fp groups of 16 output tiles (2x2 each) per wave, the channel
+// blocks split over `split` workgroups (partials, then the direct kernel's
+// split reduction) and `waves` waves per workgroup.  u: the transformed filter
+// (winograd.h's order, wino_filter_floats floats).
+bool wino_eligible(const ConvShape& s);
+bool wino_config_valid(const ConvShape& s, const ConvConfig& c);
+ConvConfig choose_wino_config(const ConvShape& s);
+size_t wino_filter_floats(const ConvShape& s);
+void wino_filter_host(const float* w, int K, int C, float* u);
+hipError_t launch_wino_filter(const float* w, int K, int C, float* u, hipStream_t st);
+hipError_t launch_wino(const ConvShape& s, const ConvConfig& c, const float* x, const float* u,
+                       const float* bias, const float* res, float* y, float* ws, hipStream_t st);
+// Local search over the Winograd configurations (results database, "wino"
+// entries), and the database's configuration for a shape, if any.
+int tune_wino(const ConvShape& s, const float* x, const float* u, const float* bias,
+              const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
+bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
+
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
 // or null; res: NCHW[yb]c [N][ceil(K/yb)][OH][OW][yb] or null; y: NCHW[yb]c

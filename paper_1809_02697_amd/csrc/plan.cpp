@@ -79,6 +79,11 @@ struct Step {
     std::vector<Step> pools;    // ST_CONV_GROUP: a pooling step run by the same launch (0 or 1);
                                 // ST_CONV_POOL: the max pooling of members[0]'s output
     ConvPoolConfig cpc{1, 2, 5, 4, 8};  // ST_CONV_POOL
+    // ST_CONV with NEO_PLAN_WINOGRAD: the transformed filter (when the shape
+    // takes the Winograd kernel), whether the step runs it, its configuration
+    long u_off = -1;
+    bool wino = false;
+    ConvConfig wc{1, 1, 1, 1};
 };
 
 struct Xform {
@@ -445,6 +450,13 @@ int build_steps(neo_plan* P) {
                 pack_filter_host(w.data(), d.K, C, d.R, d.S, 16, 16, wp.data());
                 to_kernel_order(wp.data(), st.cs, wm.data());  // one float4 per lane and k-quad
                 st.w_off = add_params(P, wm);
+                if ((P->flags & NEO_PLAN_WINOGRAD) && wino_eligible(st.cs)) {
+                    std::vector<float> u(wino_filter_floats(st.cs));
+                    if ((long)u.size() >= (1L << 29))
+                        return fail(NEO_ERR_UNSUPPORTED, where + "Winograd filter of 2 GiB or more");
+                    wino_filter_host(w.data(), d.K, C, u.data());
+                    st.u_off = add_params(P, u);
+                }
                 if (has_b) st.b_off = add_params(P, b);
                 st.cc = choose_conv_config(st.cs);
                 if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
@@ -994,14 +1006,16 @@ std::string describe(const neo_plan* P) {
           << ",\"in\":" << s.in << ",\"out\":" << s.out << ",\"res\":" << s.res;
         auto conv_json = [&](const Step& s) {
             const ConvShape& c = s.cs;
+            const ConvConfig& cfg = s.wino ? s.wc : s.cc;  // the configuration that runs
             o << "{\"N\":" << c.N << ",\"C\":" << c.C << ",\"H\":" << c.H << ",\"W\":" << c.W
               << ",\"K\":" << c.K << ",\"R\":" << c.R << ",\"S\":" << c.S << ",\"stride\":[" << c.sh
               << "," << c.sw << "],\"pad\":[" << c.ph << "," << c.pw << "],\"OH\":" << c.OH
               << ",\"OW\":" << c.OW << ",\"y_off\":" << c.y_off << ",\"y_tot\":" << c.y_tot
               << ",\"act\":" << c.act << ",\"bias\":" << (s.b_off >= 0 ? "true" : "false")
               << ",\"ic_bn\":" << c.xb << ",\"oc_bn\":" << c.yb
-              << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"split\":" << s.cc.split
-              << ",\"waves\":" << s.cc.waves << ",\"tuned\":" << (s.tuned ? "true" : "false");
+              << ",\"tile\":[" << cfg.fk << "," << cfg.fp << "],\"split\":" << cfg.split
+              << ",\"waves\":" << cfg.waves << ",\"tuned\":" << (s.tuned ? "true" : "false")
+              << ",\"algo\":\"" << (s.wino ? "winograd" : "direct") << "\"";
             if (c.gap) o << ",\"gap_sums\":true";
             o << "}";
         };
@@ -1274,7 +1288,8 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         return fail(NEO_ERR_UNSUPPORTED, "neo_plan_create: block must be 16, 32 or 64");
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
                             NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP |
-                            NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS | NEO_PLAN_FUSE_POOL))
+                            NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS | NEO_PLAN_FUSE_POOL |
+                            NEO_PLAN_WINOGRAD))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
@@ -1295,6 +1310,16 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_POOL)) fuse_conv_pool(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_WINOGRAD)) {
+            // the convs still launched alone run the Winograd kernel (with
+            // NEO_PLAN_TUNE the local search then keeps it only where faster)
+            for (Step& st : P->steps)
+                if (st.kind == ST_CONV && st.u_off >= 0) {
+                    st.wino = true;
+                    st.wc = choose_wino_config(st.cs);
+                    if (!(flags & NEO_PLAN_HOST_ONLY)) (void)tuned_wino_config(st.cs, &st.wc);
+                }
+        }
     } catch (const std::bad_alloc&) {
         rc = fail(NEO_ERR_OOM, "neo_plan_create: host allocation failed");
     } catch (const std::exception& e) {
@@ -1337,7 +1362,8 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
             }
         }
         for (const Step& st : P->steps)
-            if (st.kind == ST_CONV) P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.cc));
+            if (st.kind == ST_CONV)
+                P->ws_bytes = std::max(P->ws_bytes, conv_workspace_bytes(st.cs, st.wino ? st.wc : st.cc));
         if (P->ws_bytes) e = hipMalloc(&P->d_ws, P->ws_bytes);
         if (e != hipSuccess) {
             (void)hipFree(P->d_params);
@@ -1412,6 +1438,13 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 break;
             }
             case ST_CONV:
+                if (s.wino) {
+                    e = launch_wino(s.cs, s.wc, val_ptr(P, s.in, x_nchw, y_out), prm + s.u_off,
+                                    s.b_off >= 0 ? prm + s.b_off : nullptr,
+                                    s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
+                                    val_ptr(P, s.out, x_nchw, y_out), P->d_ws, st);
+                    break;
+                }
                 e = launch_conv2d(s.cs, s.cc, val_ptr(P, s.in, x_nchw, y_out), prm + s.w_off, true,
                                   s.b_off >= 0 ? prm + s.b_off : nullptr,
                                   s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
@@ -1724,11 +1757,21 @@ static int tune_plan(neo_plan* P) {
             // (its launch then runs the configuration without a split)
             ConvShape ts = s.cs;
             ts.gap = 0;
+            float direct_us = 0.f;
             rc = tune_conv(ts, true, val_ptr(P, s.in, xin, yout), prm + s.w_off,
                            s.b_off >= 0 ? prm + s.b_off : nullptr,
                            s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
-                           val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, nullptr);
+                           val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, &direct_us);
             if (s.cs.gap && s.cc.fp == 0) s.cc = choose_conv_config(s.cs);
+            if (rc == NEO_OK && s.u_off >= 0) {
+                // the Winograd kernel runs the step only where it measures faster
+                float wino_us = 0.f;
+                rc = tune_wino(s.cs, val_ptr(P, s.in, xin, yout), prm + s.u_off,
+                               s.b_off >= 0 ? prm + s.b_off : nullptr,
+                               s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
+                               val_ptr(P, s.out, xin, yout), P->cap_stream, &s.wc, &wino_us);
+                s.wino = rc == NEO_OK && wino_us < direct_us;
+            }
             s.tuned = rc == NEO_OK;
         }
         next.push_back(s);

@@ -120,6 +120,8 @@ struct PoolEntry {
     float us;
 };
 std::map<GroupKey, PoolEntry> g_convpool_db;  // a stem conv and its max pool in one launch
+std::map<GroupKey, Entry> g_wino_db;          // a 3x3 conv by Winograd F(2x2, 3x3)
+constexpr int kWinoInts = 7;                  // N C H W K ph pw
 constexpr int kConvPoolInts = 13 + 12;        // conv N C H W K R S sh sw ph pw xb act, pool ints
 constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
@@ -177,6 +179,75 @@ int tune_conv(const ConvShape& s, bool wmfma, const float* x, const float* w, co
     {
         std::lock_guard<std::mutex> lk(g_mu);
         g_db[key_of(s, wmfma, arch)] = Entry{best, best_us};
+    }
+    *best_out = best;
+    if (us_out) *us_out = best_us;
+    return NEO_OK;
+}
+
+namespace {
+GroupKey wino_key(const ConvShape& s) { return {device_arch(), {s.N, s.C, s.H, s.W, s.K, s.ph, s.pw}}; }
+}  // namespace
+
+bool tuned_wino_config(const ConvShape& s, ConvConfig* out) {
+    const GroupKey key = wino_key(s);
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_wino_db.find(key);
+    if (it == g_wino_db.end() || !wino_config_valid(s, it->second.cfg)) return false;
+    *out = it->second.cfg;
+    return true;
+}
+
+// Every valid Winograd configuration with a partials workspace below 64 MB,
+// timed with the caller's buffers; keeps the fastest with its time.
+int tune_wino(const ConvShape& s, const float* x, const float* u, const float* bias,
+              const float* res, float* y, hipStream_t st, ConvConfig* best_out, float* us_out) {
+    const GroupKey key = wino_key(s);
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_wino_db.find(key);
+        if (it != g_wino_db.end() && wino_config_valid(s, it->second.cfg)) {
+            *best_out = it->second.cfg;
+            if (us_out) *us_out = it->second.us;
+            return NEO_OK;
+        }
+    }
+    std::vector<ConvConfig> cands;
+    for (int fk : {1, 2})
+        for (int fp : {1, 2})
+            for (int wv : {1, 2, 4, 8})
+                for (int sp : {1, 2, 4, 8}) {
+                    const ConvConfig c{fk, fp, sp, wv};
+                    if (wino_config_valid(s, c) && conv_workspace_bytes(s, c) <= (64u << 20))
+                        cands.push_back(c);
+                }
+    size_t ws_bytes = 0;
+    for (const ConvConfig& c : cands) ws_bytes = std::max(ws_bytes, conv_workspace_bytes(s, c));
+    float* ws = nullptr;
+    hipError_t e = hipSuccess;
+    if (ws_bytes) e = hipMalloc(&ws, ws_bytes);
+    if (e != hipSuccess) return fail(NEO_ERR_OOM, "Winograd tuning workspace allocation");
+    ConvConfig best = choose_wino_config(s);
+    float best_us = 1e30f;
+    {
+        Events ev;
+        for (const ConvConfig& c : cands) {
+            float us = 0.f;
+            e = time_launch([&] { return launch_wino(s, c, x, u, bias, res, y, ws, st); }, st, ev.e0,
+                            ev.e1, &us);
+            if (e != hipSuccess) break;
+            if (us < best_us) {
+                best_us = us;
+                best = c;
+            }
+        }
+        (void)hipStreamSynchronize(st);
+    }
+    if (ws) (void)hipFree(ws);
+    if (e != hipSuccess) return hip_fail(e, "Winograd tuning");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_wino_db[key] = Entry{best, best_us};
     }
     *best_out = best;
     if (us_out) *us_out = best_us;
@@ -386,9 +457,11 @@ extern "C" {
 //   pair arch (N C H W K R S sh sw ph pw) x 2 residual us
 // one line per 3x3-led chain of n (2 or 3) convs in one launch:
 //   chain arch n (N C H W K R S sh sw ph pw) x n residual us
-// and one line per stem conv with its max pooling in one launch:
+// one line per stem conv with its max pooling in one launch:
 //   convpool arch N C H W K R S sh sw ph pw xb act (max N C H W R S sh sw ph pw xb)
 //            fk fp waves ty tx us
+// and one line per 3x3 stride-1 conv by Winograd F(2x2, 3x3):
+//   wino arch N C H W K ph pw fk fp split waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -433,8 +506,14 @@ int neo_tune_db_save(const char* path) {
         f << ' ' << c.fk << ' ' << c.fp << ' ' << c.waves << ' ' << c.ty << ' ' << c.tx << ' '
           << kv.second.us << '\n';
     }
+    for (const auto& kv : g_wino_db) {
+        f << "wino " << kv.first.first;
+        for (int x : kv.first.second) f << ' ' << x;
+        const ConvConfig& c = kv.second.cfg;
+        f << ' ' << c.fk << ' ' << c.fp << ' ' << c.split << ' ' << c.waves << ' ' << kv.second.us << '\n';
+    }
     return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                     g_chain_db.size() + g_convpool_db.size())
+                     g_chain_db.size() + g_convpool_db.size() + g_wino_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -448,6 +527,7 @@ int neo_tune_db_load(const char* path) {
     std::map<GroupKey, Entry> add_group;
     std::map<GroupKey, float> add_pool, add_pair, add_chain;
     std::map<GroupKey, PoolEntry> add_convpool;
+    std::map<GroupKey, Entry> add_wino;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -527,6 +607,23 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 5, "wino ") == 0) {
+            std::string tag;
+            GroupKey wk;
+            bool ok = (bool)(is >> tag >> wk.first) && read_ints(is, kWinoInts, wk.second) &&
+                      (bool)(is >> v.cfg.fk >> v.cfg.fp >> v.cfg.split >> v.cfg.waves >> v.us);
+            if (ok) {  // the entry must name a configuration the kernel takes for its shape
+                const std::vector<int>& q = wk.second;
+                ConvShape cs{q[0], q[1], q[2], q[3], q[4], 3, 3, 1, 1, q[5], q[6],
+                             q[2] + 2 * q[5] - 2, q[3] + 2 * q[6] - 2, 0, 0, 0};
+                ok = q[0] > 0 && q[1] > 0 && q[2] > 0 && q[3] > 0 && q[4] > 0 && q[5] >= 0 &&
+                     q[6] >= 0 && wino_config_valid(cs, v.cfg);
+            }
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_wino[wk] = v;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -554,6 +651,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add_pair) g_pair_db[kv.first] = kv.second;
     for (const auto& kv : add_chain) g_chain_db[kv.first] = kv.second;
     for (const auto& kv : add_convpool) g_convpool_db[kv.first] = kv.second;
+    for (const auto& kv : add_wino) g_wino_db[kv.first] = kv.second;
     return n;
 }
 
@@ -565,12 +663,13 @@ void neo_tune_db_clear(void) {
     g_pair_db.clear();
     g_chain_db.clear();
     g_convpool_db.clear();
+    g_wino_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                 g_chain_db.size() + g_convpool_db.size());
+                 g_chain_db.size() + g_convpool_db.size() + g_wino_db.size());
 }
 
 }  // extern "C"

@@ -33,6 +33,7 @@ PLAN_FUSE_GAP = 64
 PLAN_FUSE_PAIRS = 128
 PLAN_FUSE_CHAINS = 256
 PLAN_FUSE_POOL = 512
+PLAN_WINOGRAD = 1024
 BLOCK = 16
 SEARCH_BLOCKS = (0, 4, 8, 16, 32, 64)   # layout index space of neo_layout_search
 
@@ -91,6 +92,9 @@ def lib():
         "neo_layout_search": [ctypes.POINTER(Node), I, I, I, I, I, I, P, P, P, P, P],
         "neo_layout_transform": [P, I, P, I, I, I, I, I, P],
         "neo_pack_filter": [P, I, I, I, I, I, I, P, P],
+        "neo_winograd_filter": [P, I, I, P, P],
+        "neo_conv2d_winograd": [P, I, I, I, I, P, I, P, I, I, ctypes.POINTER(Epilogue), P, I, I,
+                                P],
         "neo_fold_bn": [P, P, P, P, P, P, F, I, I, I, I, P, P],
         "neo_maxpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
         "neo_avgpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
@@ -263,6 +267,53 @@ def pack_filter(w, ic_bn=BLOCK, oc_bn=BLOCK, out=None, stream=None):
                           device=w.device, dtype=torch.float32)
     _check(lib().neo_pack_filter(_dptr(w, "w"), K, C, R, S, ic_bn, oc_bn, _dptr(out, "out"),
                                  _stream(stream)))
+    return out
+
+
+def winograd_filter_floats(K, C):
+    return cblocks(K) * cblocks(C) * 16 * 256
+
+
+def winograd_filter(w, out=None, stream=None):
+    """w: device KCRS [K][C][3][3] -> the Winograd F(2x2, 3x3) transformed
+    filter G w G^T, [ceil(K/16)][ceil(C/16)][16][256]."""
+    import torch
+    K, C, R, S = w.shape
+    if (R, S) != (3, 3):
+        raise ValueError("the Winograd filter transform takes 3x3 filters")
+    if out is None:
+        out = torch.empty((cblocks(K), cblocks(C), 16, 256), device=w.device, dtype=torch.float32)
+    _need(out, winograd_filter_floats(K, C), "out")
+    _check(lib().neo_winograd_filter(_dptr(w, "w"), K, C, _dptr(out, "out"), _stream(stream)))
+    return out
+
+
+def conv2d_winograd(x, C, u, K, bias=None, pad=1, act="none", residual=None, out=None,
+                    y_cblk_offset=0, y_cblk_total=None, stream=None):
+    """3x3 stride-1 convolution by Winograd F(2x2, 3x3): x NCHW16c of C
+    channels, u from winograd_filter; the rest as conv2d_blocked."""
+    import torch
+    ph, pw = _pair(pad)
+    N, XB, H, W, blk = x.shape
+    if blk != BLOCK or XB != cblocks(C):
+        raise ValueError(f"x shape {tuple(x.shape)} is not NCHW16c of {C} channels")
+    OH, OW = out_size(H, 3, 1, ph), out_size(W, 3, 1, pw)
+    tot = cblocks(K) if y_cblk_total is None else y_cblk_total
+    if out is None:
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=x.device,
+                          dtype=torch.float32)
+    if OH > 0 and OW > 0:
+        _need(out, N * tot * OH * OW * BLOCK, "out")
+        _need(residual, N * cblocks(K) * OH * OW * BLOCK, "residual")
+    _need(bias, cblocks(K) * BLOCK, "bias")
+    _need(u, winograd_filter_floats(K, C), "u")
+    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
+                  residual.data_ptr() if residual is not None else None)
+    if residual is not None:
+        _dptr(residual, "residual")
+    _check(lib().neo_conv2d_winograd(_dptr(x, "x"), N, C, H, W, _dptr(u, "u"), K,
+                                     _dptr(bias, "bias"), ph, pw, ctypes.byref(ep),
+                                     _dptr(out, "out"), y_cblk_offset, tot, _stream(stream)))
     return out
 
 
