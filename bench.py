@@ -145,9 +145,11 @@ def conv_launches(desc):
     for i, s in enumerate(desc["steps"]):
         if s["kind"] == "conv":
             c = s["conv"]
-            out.append((i, [(c, s["res"] >= 0)],
-                        dict(tile=c["tile"], split=c["split"], waves=c["waves"], ic_bn=c["ic_bn"],
-                             oc_bn=c["oc_bn"])))
+            cfg = dict(tile=c["tile"], split=c["split"], waves=c["waves"], ic_bn=c["ic_bn"],
+                       oc_bn=c["oc_bn"])
+            if c.get("algo") == "winograd":
+                cfg["algo"] = "winograd"
+            out.append((i, [(c, s["res"] >= 0)], cfg))
         elif s["kind"] == "conv_group":
             out.append((i, [(m["conv"], m["res"] >= 0) for m in s["members"]],
                         dict(tile=s["tile"], split=1, waves=s["waves"], ic_bn=16, oc_bn=16,
@@ -346,17 +348,28 @@ def engine_clock(torch=None, plan=None, x=None, out=None, busy_runs=4000):
             torch.cuda.synchronize()
 
 
-def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False):
+def wino_mfma_flops(c):
+    """MFMA work of a conv by Winograd F(2x2, 3x3): 16 products over the input
+    channels per 2x2 output tile (2 * 16 * K * C per tile)."""
+    tiles = c["N"] * -(-c["OH"] // 2) * -(-c["OW"] // 2)
+    return 2 * 16 * c["K"] * c["C"] * tiles
+
+
+def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False, select=None):
     """Each conv step of the plan timed alone (its kernel(s) as the plan
     launches them), grouped by distinct shapes, residuals and launch
     configuration.  cold: also time every step with the caches flushed
     (cold_hbm_only: only the steps whose algorithmic intensity is below the
-    ridge, the HBM-bound ones)."""
+    ridge, the HBM-bound ones).  select(cfg): the launches to time (default
+    all).  FLOPs are the direct convolution's (the metric's definition); a
+    Winograd launch also reports the rate of its own MFMA work."""
     d = plan.describe()
     plan.run(x, out)      # intermediate buffers hold real activations
     torch.cuda.synchronize()
     rows = {}
     for i, members, cfg in conv_launches(d):
+        if select is not None and not select(cfg):
+            continue
         key = tuple((c["C"], c["K"], c["R"], c["S"], tuple(c["stride"]), tuple(c["pad"]), c["H"],
                      c["W"], c["N"], c["ic_bn"], c["oc_bn"], res) for c, res in members)
         key += (json.dumps(cfg, sort_keys=True),)
@@ -373,7 +386,8 @@ def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False):
         flops, nbytes = launch_costs(members)
         rows[key] = dict(shape=" + ".join(conv_label(c) + (" +res" if res else "") for c, res in members),
                          uses=1, flops=flops,
-                         bytes=nbytes, config=cfg, _t=[us], _c=[cold_us])
+                         bytes=nbytes, config=cfg, _t=[us], _c=[cold_us],
+                         _wflops=sum(wino_mfma_flops(c) for c, _ in members))
     out_rows = []
     for r in rows.values():
         us = float(np.mean(r.pop("_t")))
@@ -390,6 +404,11 @@ def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False):
         if cold and cold_us > 0:
             r.update(cold_us=round(cold_us, 2),
                      cold_hbm_gbs=round(r["bytes"] / (cold_us * 1e-6) / 1e9, 1))
+        if r["config"].get("algo") == "winograd":
+            wtf = r.pop("_wflops") / (us * 1e-6) / 1e12
+            r.update(wino_mfma_tflops=round(wtf, 2), wino_pct_mfma=round(100 * wtf / PEAK_FP32_TFLOPS, 1))
+        else:
+            r.pop("_wflops", None)
         out_rows.append(r)
     return out_rows
 
@@ -404,20 +423,27 @@ def scheme_summary(d):
 
 def model_latencies(neo, torch, wl, steps):
     """End-to-end latency of each model (tuned, graph replay) for the three
-    plans of the Table 3 ablation; ResNet-50 also at fixed blocks 32 and 64."""
+    plans of the Table 3 ablation; ResNet-50 also at fixed blocks 32 and 64;
+    and with the 3x3 stride-1 convs free to run by Winograd F(2x2, 3x3) (the
+    paper's future work; the local search keeps it per conv where faster),
+    with and without the fusions."""
     res = {}
     for name, builder, batch in [("resnet50", wl.resnet50, 1), ("vgg16", wl.vgg16, 1),
-                                 ("inception_v3", wl.inception_v3, 1), ("resnet50", wl.resnet50, 32)]:
+                                 ("inception_v3", wl.inception_v3, 1), ("resnet50", wl.resnet50, 32),
+                                 ("vgg16", wl.vgg16, 32)]:
         g = builder(batch)
         x = torch.from_numpy(g.x).cuda()
         entry = {}
         fused = (neo.PLAN_GROUP | neo.PLAN_FUSE_GAP | neo.PLAN_FUSE_PAIRS | neo.PLAN_FUSE_CHAINS |
                  neo.PLAN_FUSE_POOL)
-        plans = [("eliminated", 0, 16), ("grouped", fused, 16)]
+        plans = [("eliminated", 0, 16), ("grouped", fused, 16), ("winograd", neo.PLAN_WINOGRAD, 16),
+                 ("winograd_grouped", fused | neo.PLAN_WINOGRAD, 16)]
         if batch == 1:   # (the batch-32 search measures ~190 schemes at ~0.6 s each)
             plans += [("searched", neo.PLAN_GLOBAL_SEARCH, 16), ("naive", neo.PLAN_NAIVE, 16)]
         if name == "resnet50":
             plans += [("eliminated_x32", 0, 32), ("eliminated_x64", 0, 64)]
+        if name == "vgg16" and batch == 32:   # (nothing to fuse in a chain of convs)
+            plans = [("eliminated", 0, 16), ("winograd", neo.PLAN_WINOGRAD, 16)]
         for label, flags, block in plans:
             t0 = time.perf_counter()
             p = neo.Plan(g, flags=flags | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH, block=block)
@@ -427,6 +453,9 @@ def model_latencies(neo, torch, wl, steps):
             d = p.describe()
             entry[label] = dict(ms=round(ms, 4), n_transforms=d["n_transforms"],
                                 launches=len(d["steps"]), plan_s=round(t_plan, 1))
+            if flags & neo.PLAN_WINOGRAD:
+                entry[label]["winograd_convs"] = sum(
+                    1 for st in d["steps"] if st["kind"] == "conv" and st["conv"]["algo"] == "winograd")
             if label == "searched":
                 entry[label]["schemes"] = scheme_summary(d)
                 entry[label]["predicted_us"] = round(d["search"]["cost_us"], 1)
@@ -441,7 +470,11 @@ def model_latencies(neo, torch, wl, steps):
             entry["elimination_speedup"] = round(entry["naive"]["ms"] / entry["eliminated"]["ms"], 3)
         if "searched" in entry:
             entry["search_speedup"] = round(entry["eliminated"]["ms"] / entry["searched"]["ms"], 3)
-        entry["group_speedup"] = round(entry["eliminated"]["ms"] / entry["grouped"]["ms"], 3)
+        if "grouped" in entry:
+            entry["group_speedup"] = round(entry["eliminated"]["ms"] / entry["grouped"]["ms"], 3)
+        direct = min(entry[k]["ms"] for k in ("eliminated", "grouped") if k in entry)
+        wino = min(entry[k]["ms"] for k in ("winograd", "winograd_grouped") if k in entry)
+        entry["winograd_speedup"] = round(direct / wino, 3)
         res[f"{name}_b{batch}"] = entry
         del g, x
         print(f"[bench] {name} b{batch}: {entry}", file=sys.stderr, flush=True)
@@ -608,7 +641,7 @@ def main():
 
     models = None if args.no_models else model_latencies(neo, torch, wl, 20)
 
-    layers_b32 = None
+    layers_b32 = layers_b32_winograd = None
     if not args.no_layers and not args.no_models:
         # the same kernels with the per-launch floor amortized over 32 images
         g32 = wl.resnet50(32)
@@ -621,6 +654,13 @@ def main():
         for r in layers_b32:
             del r["flops"], r["bytes"]
         p32.destroy()
+        # the 3x3 stride-1 layers again where the local search keeps Winograd
+        p32w = neo.Plan(g32, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH | neo.PLAN_WINOGRAD)
+        layers_b32_winograd = layer_table(torch, p32w, x32, o32, 10, cold=False,
+                                          select=lambda cfg: cfg.get("algo") == "winograd")
+        for r in layers_b32_winograd:
+            del r["flops"], r["bytes"]
+        p32w.destroy()
         del g32, x32
         print(f"[bench] batch-32 conv layers: {tf32:.2f} TFLOP/s", file=sys.stderr, flush=True)
     copy_gbs = None if args.no_layers else cold_copy_gbs(torch)
@@ -660,6 +700,7 @@ def main():
         "cpu_baseline": cpu,
         "layers": layers,
         "layers_b32": layers_b32,
+        "layers_b32_winograd": layers_b32_winograd,
         "cold_copy_gbs": copy_gbs,
         "models": models,
     }

@@ -1310,9 +1310,9 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_POOL)) fuse_conv_pool(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
-        if (rc == NEO_OK && (flags & NEO_PLAN_WINOGRAD)) {
-            // the convs still launched alone run the Winograd kernel (with
-            // NEO_PLAN_TUNE the local search then keeps it only where faster)
+        if (rc == NEO_OK && (flags & NEO_PLAN_WINOGRAD) && !(flags & NEO_PLAN_TUNE)) {
+            // untuned, the convs still launched alone run the Winograd kernel
+            // (with NEO_PLAN_TUNE the local search decides, conv by conv)
             for (Step& st : P->steps)
                 if (st.kind == ST_CONV && st.u_off >= 0) {
                     st.wino = true;
@@ -1751,7 +1751,9 @@ static int tune_plan(neo_plan* P) {
             }
             continue;
         }
-        if (s.kind == ST_CONV && !s.tuned) {
+        // (a conv the Winograd kernel could run is compared even when its
+        // direct configuration came from the results database)
+        if (s.kind == ST_CONV && (!s.tuned || s.u_off >= 0)) {
             const float* prm = P->d_params;
             // a conv with the global pool folded in is timed as a plain conv
             // (its launch then runs the configuration without a split)

@@ -306,3 +306,34 @@ def test_plan_tuned_batch32(gpu, model, N):
     assert_close_network(y, ref, f"{model} b{N} winograd tuned", graph=g)
     for i in range(N):
         assert_close_network(y[i:i + 1], ref[i:i + 1], f"{model} b{N} winograd image {i}")
+
+
+@pytest.mark.gpu
+def test_tuned_plan_compares_even_with_stored_direct_configs(gpu, tmp_path):
+    """A tuned plan times the Winograd kernel for every 3x3 stride-1 conv also
+    when the results database already holds the direct configurations (from
+    an earlier plan), and runs it only where it measured faster."""
+    from gpu_util import dev, host, oracle_output, assert_close_network
+    g = wl.resnet50(1)
+    gpu.tune_db_clear()
+    gpu.Plan(g, flags=gpu.PLAN_TUNE).destroy()          # direct configurations stored
+    p = gpu.Plan(g, flags=gpu.PLAN_TUNE | gpu.PLAN_WINOGRAD)
+    path = tmp_path / "db.txt"
+    gpu.tune_db_save(path)
+    wino = {tuple(int(v) for v in l.split()[2:9]): float(l.split()[-1])
+            for l in open(path) if l.startswith("wino ")}
+    assert len(wino) == 4                                 # R03, R11, R17, R23
+    direct = {}
+    for l in open(path):
+        f = l.split()
+        if f[0] == "gfx950" and f[6:12] == ["3", "3", "1", "1", "1", "1"] and f[12] == "1":
+            direct[(int(f[1]), int(f[2]), int(f[3]), int(f[4]), int(f[5]), 1, 1)] = float(f[-1])
+    for s in p.describe()["steps"]:
+        if s["kind"] == "conv" and (s["conv"]["R"], s["conv"]["stride"][0]) == (3, 1):
+            c = s["conv"]
+            key = (c["N"], c["C"], c["H"], c["W"], c["K"], 1, 1)
+            assert (c["algo"] == "winograd") == (wino[key] < direct[key]), (key, wino[key], direct[key])
+    y = host(p.run(dev(g.x)))
+    p.destroy()
+    assert_close_network(y, oracle_output(g), "resnet50 b1 tuned winograd", graph=g)
+    gpu.tune_db_clear()
