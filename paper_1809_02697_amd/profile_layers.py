@@ -4,6 +4,7 @@
         python -m paper_1809_02697_amd.profile_layers TUNE_DB [--cold] [--batch 32]
     rocprofv3 --pmc WRITE_SIZE ...                       (the same workload)
     rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 ... (the same workload)
+    ... profile_layers TUNE_DB --batch 32 --winograd [--reps 20]   (Winograd plan)
 
 Builds the plan bench.py times (batch 1: the headline plan; batch 32: the
 tuned one-block plan of the batch-32 layer table).  TUNE_DB is a local-search
@@ -25,13 +26,17 @@ COPY_MB = 64
 FLUSH_MB = 512
 
 
-def build_plan(neo, torch, wl, db, batch):
-    """(plan, graph) of the run whose results file is `db`."""
+def build_plan(neo, torch, wl, db, batch, winograd=False):
+    """(plan, graph) of the run whose results file is `db`; with `winograd`
+    the tuned one-block plan whose 3x3 stride-1 convs may run by Winograd
+    F(2x2, 3x3) (bench.py's ``winograd`` plan)."""
     from bench import headline_plan
     if db:
         neo.tune_db_load(db)
     g = wl.resnet50(batch)
-    if batch == 1:
+    if winograd:
+        plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH | neo.PLAN_WINOGRAD)
+    elif batch == 1:
         plan, _ = headline_plan(neo, g, db, torch)
     else:
         plan = neo.Plan(g, flags=neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
@@ -49,8 +54,12 @@ def main():
     ap.add_argument("--cold", action="store_true")
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--describe", help="write the plan's description (JSON) here")
+    ap.add_argument("--winograd", action="store_true",
+                    help="the plan with NEO_PLAN_WINOGRAD (3x3 stride-1 convs by Winograd where faster)")
+    ap.add_argument("--reps", type=int, default=1,
+                    help="run the step list this many times (for kernel-trace durations)")
     args = ap.parse_args()
-    plan, g = build_plan(neo, torch, wl, args.db, args.batch)
+    plan, g = build_plan(neo, torch, wl, args.db, args.batch, args.winograd)
     if args.describe:
         with open(args.describe, "w") as f:
             json.dump(plan.describe(), f)
@@ -64,10 +73,11 @@ def main():
     b.copy_(a)
     torch.cuda.synchronize()
     n = len(plan.describe()["steps"])
-    for i in range(n):
-        if flush is not None:
-            flush.fill_(1.0)
-        plan.run_step(i, x, out)
+    for _ in range(args.reps):
+        for i in range(n):
+            if flush is not None:
+                flush.fill_(1.0)
+            plan.run_step(i, x, out)
     torch.cuda.synchronize()
     print(f"profiled {n} steps after a {COPY_MB} MB copy (batch {args.batch}"
           f"{', cold' if args.cold else ''})", file=sys.stderr)

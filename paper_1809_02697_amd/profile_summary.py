@@ -16,6 +16,8 @@ Writes
   profiles/conv2d_blocked_resnet50_b1.md  launch durations, per-layer traffic
       (warm and cold) and MFMA utilisation at batch 1
   profiles/conv2d_blocked_resnet50_b32_mfma.md  MFMA utilisation at batch 32
+  profiles/wino_f2x3_resnet50_b32.md  the Winograd kernel's launches in the
+      batch-32 plan with NEO_PLAN_WINOGRAD: durations and MFMA utilisation
   profiles/conv2d_blocked_resnet50_b1_traffic.json  bytes per launch, tied to
       the hash of the kernel source it was measured with (bench.py reports it
       only while the source is unchanged)
@@ -70,6 +72,11 @@ COMMANDS = [
     "rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
     "--output-format csv -d RUN_DIR/pmc -o mfma32 -- python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --batch 32 "
     "--describe RUN_DIR/plan_b32.json",
+    "rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+    "--output-format csv -d RUN_DIR/pmc -o mfma32w -- python -m paper_1809_02697_amd.profile_layers "
+    "RUN_DIR/tune_db.txt --batch 32 --winograd --describe RUN_DIR/plan_b32w.json",
+    "rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_wino -o wino -- "
+    "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --batch 32 --winograd --reps 20",
     "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
 ]
 
@@ -89,7 +96,7 @@ def _rows(path):
 
 def is_conv(name):
     return ("conv2d_mfma" in name or "conv1x1_pair" in name or "conv3x3_chain" in name or
-            "conv_pool_small" in name or "conv1x1_stream" in name)
+            "conv_pool_small" in name or "conv1x1_stream" in name or "wino_f2x3" in name)
 
 
 def is_neo(name):
@@ -331,9 +338,69 @@ def main(run_dir):
                       f"{busy[i] / SIMDS / CLOCK_MHZ:.2f} | {mops[i] * 512 / f32:.3f} |")
         with open(os.path.join(PROFILES, "conv2d_blocked_resnet50_b32_mfma.md"), "w") as f:
             f.write("\n".join(md) + "\n")
+    # -- Winograd, batch 32 ------------------------------------------------------------------
+    pw = os.path.join(pmc, "mfma32w_counter_collection.csv")
+    tw = os.path.join(run_dir, "prof_wino", "wino_kernel_trace.csv")
+    if os.path.exists(pw) and os.path.exists(tw) and os.path.exists(os.path.join(run_dir, "plan_b32w.json")):
+        write_winograd(run_dir, pw, tw)
     print(json.dumps(dict(traffic_json, trace_avg_launch_us=round(tr_avg, 3),
                           bench_avg_launch_us=ev_avg, trace_frac=round(tr_tf / PEAK, 4),
                           bench_frac=bench["roofline"]["frac"])))
+
+
+def write_winograd(run_dir, pmc_path, trace_path):
+    """profiles/wino_f2x3_resnet50_b32.md: the Winograd launches of the tuned
+    batch-32 plan -- trace durations, MFMA utilisation and executed MFMA work
+    over the algorithmic Winograd work and over the direct convolution's."""
+    from bench import conv_label, conv_launches, launch_costs, wino_mfma_flops
+    d = json.load(open(os.path.join(run_dir, "plan_b32w.json")))
+    launches = conv_launches(d)
+    wi = [k for k, (_, _, cfg) in enumerate(launches) if cfg.get("algo") == "winograd"]
+    _, util = forward_dispatches(pmc_path, "MfmaUtil")
+    _, mops = forward_dispatches(pmc_path, "SQ_INSTS_VALU_MFMA_MOPS_F32")
+    _, busy = forward_dispatches(pmc_path, "SQ_VALU_MFMA_BUSY_CYCLES")
+    util, mops, busy = per_conv_max(util), per_conv(mops), per_conv(busy)
+    assert len(util) == len(launches), (len(util), len(launches))
+    # trace: the Winograd dispatches (and a split_reduce right after one), in plan order, repeated
+    rows = sorted(_rows(trace_path), key=lambda r: int(r["Start_Timestamp"]))
+    durs = []
+    prev_wino = False
+    for r in rows:
+        n = r["Kernel_Name"]
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        if "wino_f2x3" in n:
+            durs.append(us)
+            prev_wino = True
+        elif "split_reduce" in n and prev_wino:
+            durs[-1] += us
+        elif is_neo(n):
+            prev_wino = False
+    nw = len(wi)
+    reps = len(durs) // nw
+    assert reps >= 2 and len(durs) % nw == 0, (len(durs), nw)
+    per = [_median([durs[r * nw + j] for r in range(1, reps)]) for j in range(nw)]
+    md = ["# wino_f2x3 (Winograd F(2x2, 3x3)), ResNet-50 batch 32: duration and MFMA utilisation",
+          "", "Commands (from the repository root; RUN_DIR = gpurun_out; the results file of the "
+          "bench run above, whose `winograd` plan this is):", "", "```", COMMANDS[-3], COMMANDS[-2],
+          COMMANDS[-1], "```", "",
+          "The tuned one-block plan with NEO_PLAN_WINOGRAD: the local search keeps the Winograd "
+          "kernel for the 3x3 stride-1 convs listed.  Duration: median over the profiled repetitions "
+          "(the first dropped) of the kernel-trace timestamps.  TFLOP/s counts the direct "
+          "convolution's FLOPs (the metric's definition); MFMA work is the executed "
+          "SQ_INSTS_VALU_MFMA_MOPS_F32 x 512, against the Winograd algorithm's 2 x 16 x K x C per 2x2 "
+          "tile and against the direct FLOPs.", "",
+          "| # | layer | config (tile, split, waves) | us | TFLOP/s (direct count) | MfmaUtil % | "
+          "MFMA work / Winograd work | MFMA work / direct FLOPs |",
+          "|---:|---|---|---:|---:|---:|---:|---:|"]
+    for j, k in enumerate(wi):
+        _, members, cfg = launches[k]
+        c = members[0][0]
+        f_direct = launch_costs(members)[0]
+        md.append(f"| {k} | {conv_label(c)} | {cfg['tile']}, {cfg['split']}, {cfg['waves']} | "
+                  f"{per[j]:.2f} | {f_direct / (per[j] * 1e-6) / 1e12:.1f} | {util[k]:.1f} | "
+                  f"{mops[k] * 512 / wino_mfma_flops(c):.3f} | {mops[k] * 512 / f_direct:.3f} |")
+    with open(os.path.join(PROFILES, "wino_f2x3_resnet50_b32.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
 
 
 if __name__ == "__main__":
