@@ -58,7 +58,6 @@ struct WinoArgs {
     float* ws;          // split partials [split][N][KB][OH][OW][16]
     int N, CB, H, W, KB, OH, OW, ph, pw, TH, TW, NT, y_off, y_tot, act, split;
     int ntg, nkt;       // tile units of WAVES * FT * 16 tiles; channel tiles of FK blocks
-    int tfirst;         // 1: tile units fastest in the logical order, 0: channel tiles fastest
     int x_bytes, u_bytes;
     FastDiv div_tt, div_tw;  // tiles per image, tiles per row
 };
@@ -91,19 +90,14 @@ __global__ __launch_bounds__(WAVES * 64) void wino_f2x3(WinoArgs a) {
     const int li = lane & 15, g = lane >> 4;
     // logical workgroup: channel tiles fastest, so the workgroups that read
     // one input tile group are neighbours in the XCD's contiguous run
+    // (measured on ResNet-50's and VGG-16's 3x3 layers at batch 1 and 32, the
+    // other order -- one channel tile's filter slice per XCD, every tile unit
+    // -- is within 1 %)
     const int u = __builtin_amdgcn_readfirstlane(xcd_order());
-    int kt, tg, z;
-    if (a.tfirst) {
-        tg = u % a.ntg;
-        const int rest = u / a.ntg;
-        kt = rest % a.nkt;
-        z = rest / a.nkt;
-    } else {
-        kt = u % a.nkt;
-        const int rest = u / a.nkt;
-        tg = rest % a.ntg;
-        z = rest / a.ntg;
-    }
+    const int kt = u % a.nkt;
+    const int rest = u / a.nkt;
+    const int tg = rest % a.ntg;
+    const int z = rest / a.ntg;
 
     const __amdgpu_buffer_rsrc_t xr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
@@ -430,11 +424,6 @@ hipError_t launch_wino(const ConvShape& s, const ConvConfig& c, const float* x, 
     a.u_bytes = (int)(wino_filter_floats(s) * 4);
     a.div_tt = make_fastdiv((unsigned)(a.TH * a.TW));
     a.div_tw = make_fastdiv((unsigned)a.TW);
-    // channel tiles fastest: each XCD then reads a contiguous range of tile
-    // units (and every channel tile's filter).  Measured on ResNet-50's and
-    // VGG-16's 3x3 layers at batch 1 and 32, the other order (a channel tile's
-    // filter slice per XCD, every tile unit) is within 1 %.
-    a.tfirst = 0;
     hipError_t e = hipErrorInvalidValue;
     if (c.fk == 1 && c.fp == 1) e = by_waves<1, 1>(c.waves, a, st);
     if (c.fk == 2 && c.fp == 1) e = by_waves<2, 1>(c.waves, a, st);
