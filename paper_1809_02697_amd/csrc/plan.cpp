@@ -1313,8 +1313,10 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_WINOGRAD) && !(flags & NEO_PLAN_TUNE)) {
             // untuned, the convs still launched alone run the Winograd kernel
             // (with NEO_PLAN_TUNE the local search decides, conv by conv)
+            // (eligibility again: a fusion pass may have changed the step, as
+            // the global-pool fold does)
             for (Step& st : P->steps)
-                if (st.kind == ST_CONV && st.u_off >= 0) {
+                if (st.kind == ST_CONV && st.u_off >= 0 && wino_eligible(st.cs)) {
                     st.wino = true;
                     st.wc = choose_wino_config(st.cs);
                     if (!(flags & NEO_PLAN_HOST_ONLY)) (void)tuned_wino_config(st.cs, &st.wc);
@@ -1765,7 +1767,7 @@ static int tune_plan(neo_plan* P) {
                            s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
                            val_ptr(P, s.out, xin, yout), P->cap_stream, &s.cc, &direct_us);
             if (s.cs.gap && s.cc.fp == 0) s.cc = choose_conv_config(s.cs);
-            if (rc == NEO_OK && s.u_off >= 0) {
+            if (rc == NEO_OK && s.u_off >= 0 && wino_eligible(s.cs)) {
                 // the Winograd kernel runs the step only where it measures faster
                 float wino_us = 0.f;
                 rc = tune_wino(s.cs, val_ptr(P, s.in, xin, yout), prm + s.u_off,

@@ -337,3 +337,37 @@ def test_tuned_plan_compares_even_with_stored_direct_configs(gpu, tmp_path):
     p.destroy()
     assert_close_network(y, oracle_output(g), "resnet50 b1 tuned winograd", graph=g)
     gpu.tune_db_clear()
+
+
+def _gap_graph():
+    b = wl._Builder("gap3x3", (1, 32, 9, 9), np.random.Generator(np.random.PCG64(5)))
+    c1 = b.conv(0, 48, 3, pad=1, name="c1")
+    c2 = b.conv(c1, 64, 3, pad=1, name="c2")
+    gp = b.gap(c2)
+    fl = b.flatten(gp, 64)
+    b.output(b.dense(fl, 10, name="fc"))
+    return b.finish(lambda rng: wl._f32(rng.uniform(-1.0, 1.0, size=(1, 32, 9, 9))))
+
+
+def test_planner_keeps_a_pool_folded_conv_direct():
+    """A 3x3 stride-1 conv whose output the global pool reads, folded into it
+    (NEO_PLAN_FUSE_GAP), writes channel sums, which only the direct kernel
+    does: it stays direct under NEO_PLAN_WINOGRAD."""
+    g = _gap_graph()
+    d = _host_desc(g, neo.PLAN_WINOGRAD | neo.PLAN_FUSE_GAP)
+    convs = [s["conv"] for s in d["steps"] if s["kind"] == "conv"]
+    assert [c.get("gap_sums", False) for c in convs] == [False, True]
+    assert [c["algo"] for c in convs] == ["winograd", "direct"]
+
+
+@pytest.mark.gpu
+def test_plan_winograd_with_pool_fold(gpu):
+    """The plan above on the GPU, untuned and tuned, against the oracle."""
+    from gpu_util import assert_close, dev, host
+    g = _gap_graph()
+    ref = orc.run_graph(g)
+    for fl in (gpu.PLAN_WINOGRAD | gpu.PLAN_FUSE_GAP, gpu.PLAN_WINOGRAD | gpu.PLAN_FUSE_GAP | gpu.PLAN_TUNE):
+        p = gpu.Plan(g, flags=fl)
+        y = host(p.run(dev(g.x)))
+        p.destroy()
+        assert_close(y.reshape(ref.shape), ref, f"gap-folded plan, flags {fl}")
