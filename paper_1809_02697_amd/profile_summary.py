@@ -259,7 +259,7 @@ def main(run_dir):
         json.dump(traffic_json, f, indent=1)
 
     md = [f"# conv2d_blocked, ResNet-50 batch 1 (53 convs in {n} launches per forward)", "",
-          "Commands (run from the repository root on one MI355X; RUN_DIR = gpurun_out):", "",
+          "Commands (run from the repository root on one MI355X; RUN_DIR = the directory they write to):", "",
           "```"] + COMMANDS + ["```", "",
           f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
           "## Launch duration", "",
@@ -322,7 +322,7 @@ def main(run_dir):
         util, mops, busy = per_conv_max(util), per_conv(mops), per_conv(busy)
         assert len(util) == len(s32), (len(util), len(s32))
         md = ["# conv2d_blocked, ResNet-50 batch 32: MFMA utilisation per launch", "",
-              "Command (from the repository root; RUN_DIR = gpurun_out; the plan and results file "
+              "Command (from the repository root, RUN_DIR as above; the plan and results file "
               "of the bench run above):", "", "```", COMMANDS[7], COMMANDS[-1], "```", "",
               f"Kernel source sha256[:16]: `{kernel_hash()}`", "",
               "MfmaUtil = busy MFMA cycles summed over the 1024 SIMDs / (GPU active cycles x "
@@ -380,7 +380,7 @@ def write_winograd(run_dir, pmc_path, trace_path):
     assert reps >= 2 and len(durs) % nw == 0, (len(durs), nw)
     per = [_median([durs[r * nw + j] for r in range(1, reps)]) for j in range(nw)]
     md = ["# wino_f2x3 (Winograd F(2x2, 3x3)), ResNet-50 batch 32: duration and MFMA utilisation",
-          "", "Commands (from the repository root; RUN_DIR = gpurun_out; the results file of the "
+          "", "Commands (from the repository root, RUN_DIR as in the batch-1 summary; the results file of the "
           "bench run above, whose `winograd` plan this is):", "", "```", COMMANDS[-3], COMMANDS[-2],
           COMMANDS[-1], "```", "",
           "The tuned one-block plan with NEO_PLAN_WINOGRAD: the local search keeps the Winograd "
@@ -404,4 +404,6 @@ def write_winograd(run_dir, pmc_path, trace_path):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1] if len(sys.argv) > 1 else "gpurun_out")
+    if len(sys.argv) != 2:
+        sys.exit("usage: python -m paper_1809_02697_amd.profile_summary RUN_DIR")
+    main(sys.argv[1])
