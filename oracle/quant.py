@@ -1,0 +1,83 @@
+"""Integer (INT8) convolution, the paper's other future work -- TEST INFRASTRUCTURE ONLY.
+
+The paper names integer (8-bit) inference as future work and gives no
+scheme, so this module fixes one, the usual symmetric linear quantization:
+
+* activations: one scale s_x per tensor (given by the caller);
+  q = clamp(round_half_even(x / s_x), -127, 127) with the division in float32;
+* filters: one scale per output channel, s_w[k] = max |w[k, :, :, :]| / 127
+  (float32; 1 for an all-zero channel), q = clamp(round_half_even(w / s_w[k]));
+* the convolution of the quantized values accumulates exact integers
+  (|sum| <= 127^2 * C * R * S, below 2^31 for every layer here);
+* the output is dequantized with the per-channel multiplier m[k] = s_x * s_w[k]
+  (a float32 product, the value the library receives):
+  y = act(acc * m[k] + bias[k] + residual), in float64, rounded once.
+
+Only ``tests/`` use this module.  It shares no code with the HIP library.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+QMAX = 127
+
+
+def quantize(x, scale):
+    """float32 tensor -> int8 with one scale (float32 division, ties to even)."""
+    q = np.rint(np.asarray(x, np.float32) / np.float32(scale))
+    return np.clip(q, -QMAX, QMAX).astype(np.int8)
+
+
+def filter_scales(w):
+    """Per-output-channel scales max |w[k]| / 127 in float32 (1 for a zero channel)."""
+    w = np.asarray(w, np.float32)
+    m = np.abs(w).reshape(w.shape[0], -1).max(axis=1)
+    s = (m / np.float32(QMAX)).astype(np.float32)
+    s[m == 0] = np.float32(1.0)
+    return s
+
+
+def quantize_filter(w):
+    """KCRS float32 -> (KCRS int8, per-channel float32 scales)."""
+    s = filter_scales(w)
+    q = np.rint(np.asarray(w, np.float32) / s[:, None, None, None])
+    return np.clip(q, -QMAX, QMAX).astype(np.int8), s
+
+
+def conv2d_int(xq, wq, stride=1, pad=0):
+    """Cross-correlation of integer tensors with zero padding (NCHW x KCRS),
+    exact: the windows are unrolled and multiplied with a float64 matrix
+    product, whose every partial sum is an integer below 2^53.  int64 out."""
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    x = np.asarray(xq, np.float64)
+    w = np.asarray(wq, np.float64)
+    N, C, H, W = x.shape
+    K, _, R, S = w.shape
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    xp = np.zeros((N, C, H + 2 * ph, W + 2 * pw))
+    xp[:, :, ph:ph + H, pw:pw + W] = x
+    cols = np.empty((N, OH, OW, C, R, S))
+    for r in range(R):
+        for s in range(S):
+            cols[:, :, :, :, r, s] = xp[:, :, r:r + sh * (OH - 1) + 1:sh,
+                                        s:s + sw * (OW - 1) + 1:sw].transpose(0, 2, 3, 1)
+    y = cols.reshape(N * OH * OW, C * R * S) @ w.reshape(K, C * R * S).T
+    return np.rint(y).astype(np.int64).reshape(N, OH, OW, K).transpose(0, 3, 1, 2).copy()
+
+
+def multipliers(x_scale, w_scales):
+    """The per-channel dequantization multipliers s_x * s_w[k] (float32)."""
+    return (np.float32(x_scale) * np.asarray(w_scales, np.float32)).astype(np.float32)
+
+
+def dequantize(acc, mult, bias=None, residual=None, act="none"):
+    """act(acc * mult[k] + bias[k] + residual) in float64, rounded once."""
+    y = np.asarray(acc, np.float64) * np.asarray(mult, np.float64)[None, :, None, None]
+    if bias is not None:
+        y = y + np.asarray(bias, np.float64)[None, :, None, None]
+    if residual is not None:
+        y = y + np.asarray(residual, np.float64)
+    if act == "relu":
+        y = np.maximum(y, 0.0)
+    return y.astype(np.float32)

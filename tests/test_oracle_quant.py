@@ -1,0 +1,96 @@
+"""Pins of the oracle's integer (INT8) functions against hand values, closed
+forms and brute force (no GPU)."""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import quant as oq
+
+
+def test_quantize_rounds_half_to_even_and_clamps():
+    s = np.float32(0.25)          # a power of two: x / s is exact
+    x = s * np.array([0.0, 0.5, 1.5, 2.5, -0.5, -2.5, 3.49, 126.5, 127.5, 300.0, -300.0],
+                     np.float32)
+    np.testing.assert_array_equal(oq.quantize(x, s), [0, 0, 2, 2, 0, -2, 3, 126, 127, 127, -127])
+    # symmetric, and exact multiples of the scale map to their integers
+    k = np.arange(-127, 128, dtype=np.float32)
+    np.testing.assert_array_equal(oq.quantize(k * s, s), k.astype(np.int8))
+    r = np.random.default_rng(0).normal(0, 3, 1000).astype(np.float32)
+    np.testing.assert_array_equal(oq.quantize(-r, 0.1), -oq.quantize(r, 0.1))
+
+
+def test_filter_scales_map_each_channels_extreme_to_127():
+    w = np.zeros((3, 2, 1, 2), np.float32)
+    w[0] = [[[0.5, -1.0]], [[0.25, 0.0]]]     # max |w| 1.0
+    w[1] = [[[-6.35, 2.0]], [[1.0, 3.175]]]   # max |w| 6.35
+    q, s = oq.quantize_filter(w)               # channel 2 is all zero
+    np.testing.assert_array_equal(s, np.float32([1.0 / 127, 6.35 / 127, 1.0]))
+    assert q[0, 0, 0, 1] == -127 and q[1, 0, 0, 0] == -127
+    np.testing.assert_array_equal(q[0].ravel(), [64, -127, 32, 0])     # 63.5 -> 64 (ties to even)
+    np.testing.assert_array_equal(q[1].ravel(), [-127, 40, 20, 64])    # 63.5 -> 64
+    assert (q[2] == 0).all()
+
+
+def _brute(xq, wq, st, pd):
+    N, C, H, W = xq.shape
+    K, _, R, S = wq.shape
+    OH, OW = (H + 2 * pd[0] - R) // st[0] + 1, (W + 2 * pd[1] - S) // st[1] + 1
+    y = np.zeros((N, K, OH, OW), np.int64)
+    for n, k, oh, ow in itertools.product(range(N), range(K), range(OH), range(OW)):
+        acc = 0
+        for c, r, s in itertools.product(range(C), range(R), range(S)):
+            ih, iw = oh * st[0] - pd[0] + r, ow * st[1] - pd[1] + s
+            if 0 <= ih < H and 0 <= iw < W:
+                acc += int(xq[n, c, ih, iw]) * int(wq[k, c, r, s])
+        y[n, k, oh, ow] = acc
+    return y
+
+
+@pytest.mark.parametrize("N,C,H,W,K,R,S,st,pd", [
+    (1, 3, 5, 4, 2, 3, 3, (1, 1), (1, 1)),
+    (2, 2, 6, 7, 3, 1, 3, (2, 1), (0, 1)),
+    (1, 4, 7, 5, 2, 3, 1, (1, 2), (2, 0)),
+    (1, 1, 4, 4, 1, 2, 2, (2, 2), (0, 0)),
+])
+def test_integer_conv_equals_brute_force(N, C, H, W, K, R, S, st, pd):
+    rng = np.random.default_rng([N, C, H, W, K, R, S])
+    xq = rng.integers(-127, 128, (N, C, H, W)).astype(np.int8)
+    wq = rng.integers(-127, 128, (K, C, R, S)).astype(np.int8)
+    np.testing.assert_array_equal(oq.conv2d_int(xq, wq, st, pd), _brute(xq, wq, st, pd))
+
+
+def test_integer_conv_closed_forms():
+    rng = np.random.default_rng(3)
+    # 1x1 stride 1 is a matrix product of integers
+    xq = rng.integers(-127, 128, (2, 5, 3, 4)).astype(np.int8)
+    wq = rng.integers(-127, 128, (6, 5, 1, 1)).astype(np.int8)
+    want = np.einsum("kc,nchw->nkhw", wq[:, :, 0, 0].astype(np.int64), xq.astype(np.int64))
+    np.testing.assert_array_equal(oq.conv2d_int(xq, wq), want)
+    # a delta filter shifts the input (zero padding)
+    x = rng.integers(-127, 128, (1, 2, 5, 6)).astype(np.int8)
+    d = np.zeros((2, 2, 3, 3), np.int8)
+    d[0, 1, 2, 0] = 1
+    d[1, 0, 0, 2] = -1
+    y = oq.conv2d_int(x, d, 1, 1)
+    xp = np.pad(x.astype(np.int64), ((0, 0), (0, 0), (1, 1), (1, 1)))
+    np.testing.assert_array_equal(y[0, 0], xp[0, 1, 2:2 + 5, 0:0 + 6])
+    np.testing.assert_array_equal(y[0, 1], -xp[0, 0, 0:5, 2:2 + 6])
+    # sums beyond float32's exact range stay exact: all-127 inputs and filters,
+    # 512 channels x 3 x 3: 127^2 times the in-bounds taps (up to 74,317,824)
+    x = np.full((1, 512, 4, 4), 127, np.int8)
+    w = np.full((1, 512, 3, 3), 127, np.int8)
+    taps = np.array([[4, 6, 6, 4], [6, 9, 9, 6], [6, 9, 9, 6], [4, 6, 6, 4]])
+    np.testing.assert_array_equal(oq.conv2d_int(x, w, 1, 1)[0, 0], 127 * 127 * 512 * taps)
+
+
+def test_dequantize_by_hand():
+    acc = np.array([[[[100]], [[-3]]]], np.int64)          # N=1, K=2, 1x1
+    mult = oq.multipliers(0.5, np.float32([0.25, 2.0]))
+    np.testing.assert_array_equal(mult, np.float32([0.125, 1.0]))
+    bias = np.float32([1.0, 0.5])
+    res = np.array([[[[-20.0]], [[1.0]]]], np.float32)
+    # 100 * 0.125 + 1 - 20 = -6.5 -> ReLU 0; -3 * 1 + 0.5 + 1 = -1.5 -> 0
+    np.testing.assert_array_equal(oq.dequantize(acc, mult, bias, res, "relu").ravel(), [0.0, 0.0])
+    np.testing.assert_array_equal(oq.dequantize(acc, mult, bias, res).ravel(), [-6.5, -1.5])
+    np.testing.assert_array_equal(oq.dequantize(acc, mult).ravel(), [12.5, -3.0])
