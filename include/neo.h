@@ -38,6 +38,7 @@
 #define NEO_H
 
 #include <stddef.h>
+#include <stdint.h>
 
 #ifdef __cplusplus
 extern "C" {
@@ -196,6 +197,47 @@ int neo_winograd_filter(const float* w_kcrs, int K, int C, float* u, neo_stream_
 int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float* u, int K,
                         const float* bias, int pad_h, int pad_w, const neo_epilogue* ep, float* y,
                         int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+
+/*
+ * Integer (INT8) convolution -- the paper's other future work (Sections 1 and
+ * 5, integer inference), with the usual symmetric linear quantization (the
+ * paper gives no scheme):
+ *   activations  q_x = clamp(round_half_even(x / x_scale), -127, 127), one
+ *                scale per tensor, the division in float32;
+ *   filters      w_scale[k] = max |w[k][:][:][:]| / 127 (1 for an all-zero
+ *                output channel), q_w = clamp(round_half_even(w / w_scale[k]));
+ *   convolution  acc[n][k][oh][ow] = sum_{c,r,s} q_x * q_w, exact in int32
+ *                (the same windows, strides and zero padding as
+ *                neo_conv2d_blocked; |acc| <= 127^2 * C * R * S must stay below
+ *                2^31, i.e. C * R * S <= 133,000);
+ *   output       y = act(acc * (x_scale * w_scale[k]) + bias[k] + residual) in
+ *                float32 (the product x_scale * w_scale[k] rounded to float32).
+ *
+ * neo_quantize_int8: x device fp32 NCHW16c [N][ceil(C/16)][H][W][16] -> xq
+ *   device int8 NCHW16c of the same shape (padding lanes 0); x_scale > 0.
+ * neo_pack_filter_int8: w_kcrs device fp32 [K][C][R][S] -> w_packed device
+ *   int8, int8_filter_bytes = ceil(K/16) * ceil(C/64) * R * S * 1024 bytes,
+ *   block (kb, r, s, cg) holding for lane (k, g) the 16 bytes
+ *   q_w[16 kb + k][64 cg + 16 g + b][r][s], b = 0..15 (zero padded); and
+ *   w_scale device [ceil(K/16)*16] (padding channels 1).
+ * neo_conv2d_int8: xq, w_packed and w_scale as written above; bias device
+ *   [ceil(K/16)*16] or NULL; ep, y and the output view as for
+ *   neo_conv2d_blocked (float32 NCHW16c).
+ * neo_conv2d_int8_acc: the same convolution, writing the raw int32 sums to acc
+ *   device [N][ceil(K/16)][OH][OW][16] (padding channels 0): the exact part.
+ * Dilation and groups are 1.  Errors as for neo_conv2d_blocked.
+ */
+int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int8_t* xq,
+                      neo_stream_t stream);
+int neo_pack_filter_int8(const float* w_kcrs, int K, int C, int R, int S, int8_t* w_packed,
+                         float* w_scale, neo_stream_t stream);
+int neo_conv2d_int8(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed,
+                    const float* w_scale, int K, int R, int S, float x_scale, const float* bias,
+                    int stride_h, int stride_w, int pad_h, int pad_w, const neo_epilogue* ep,
+                    float* y, int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed, int K,
+                        int R, int S, int stride_h, int stride_w, int pad_h, int pad_w, int32_t* acc,
+                        neo_stream_t stream);
 
 /*
  * Batch-norm folding (inference simplification inherited by the paper,

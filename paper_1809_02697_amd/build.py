@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libneo.so")
 ARCH = "gfx950"
 SOURCES = ["conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip", "layout.hip", "pool.hip", "dense.hip", "api.cpp", "plan.cpp", "tune.cpp",
-           "search.cpp", "noalloc.hip", "conv_pool.hip", "conv_stream.hip", "winograd.hip"]
+           "search.cpp", "noalloc.hip", "conv_pool.hip", "conv_stream.hip", "winograd.hip", "conv_int8.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument"]

@@ -224,6 +224,21 @@ bool env_wino_config(const ConvShape& s, ConvConfig* c) {
     return true;
 }
 
+// Optional override of the INT8 launch configuration, "fk,fp,waves".
+bool env_i8_config(const ConvShape& s, ConvConfig* c) {
+    const char* v = std::getenv("NEO_I8_CONFIG");
+    if (!v || !*v) return false;
+    ConvConfig t{1, 1, 1, 1};
+    if (std::sscanf(v, "%d,%d,%d", &t.fk, &t.fp, &t.waves) != 3 || !int8_config_valid(s, t))
+        return false;
+    *c = t;
+    return true;
+}
+
+// Largest C * R * S whose exact int32 sum of products of values in
+// [-127, 127] cannot overflow: 127^2 * 133,000 < 2^31.
+constexpr long kMaxI8Reduction = 133000;
+
 }  // namespace
 
 namespace neo {
@@ -284,6 +299,45 @@ int conv_prepare(const char* fn, const float* x, int x_block, int N, int C, int 
 }
 
 }  // namespace neo
+
+namespace {
+
+int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int W,
+                     const int8_t* w_packed, const float* w_scale, int K, int R, int S,
+                     float x_scale, const float* bias, int stride_h, int stride_w, int pad_h,
+                     int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
+                     int y_cblk_total, int* acc, neo_stream_t stream) {
+    const std::string f(fn);
+    float* out = acc ? reinterpret_cast<float*>(acc) : y;
+    ConvShape s;
+    ConvConfig cfg;
+    const float* res = nullptr;
+    // the shape, view and pointer checks of the fp32 convolution (an int8
+    // tensor is a quarter of the fp32 one's bytes, so its limits hold too)
+    int rc = conv_prepare(fn, reinterpret_cast<const float*>(xq), 16, N, C, H, W,
+                          reinterpret_cast<const float*>(w_packed), K, R, S, bias, stride_h,
+                          stride_w, pad_h, pad_w, ep, out, 16, y_cblk_offset, y_cblk_total, &s,
+                          &cfg, &res);
+    if (rc != NEO_OK) return rc;
+    if (!acc) {
+        if (!w_scale) return fail(NEO_ERR_INVALID_ARG, f + ": w_scale is NULL");
+        if (!aligned16(w_scale)) return fail(NEO_ERR_ALIGN, f + ": w_scale not 16-byte aligned");
+        if (!(x_scale > 0.f) || !std::isfinite(x_scale))
+            return fail(NEO_ERR_INVALID_ARG, f + ": x_scale must be finite and > 0");
+    }
+    if ((long)C * R * S > kMaxI8Reduction)
+        return fail(NEO_ERR_UNSUPPORTED, f + ": C * R * S above 133,000 could overflow the "
+                                             "int32 accumulator");
+    if (int8_filter_bytes(K, C, R, S) > (size_t)kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, f + ": packed filter of 2 GiB or more");
+    cfg = choose_int8_config(s);
+    env_i8_config(s, &cfg);
+    hipError_t e = launch_conv_int8(s, cfg, xq, w_packed, w_scale, x_scale, bias, res, y, acc,
+                                    (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, (f + " launch").c_str());
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -381,6 +435,50 @@ int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float*
     }
     hipError_t e = launch_wino(s, cfg, x, u, bias, res, y, ws, (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_winograd launch");
+}
+
+int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int8_t* xq,
+                      neo_stream_t stream) {
+    if (!x || !xq) return fail(NEO_ERR_INVALID_ARG, "neo_quantize_int8: NULL buffer");
+    if (!aligned16(x) || !aligned16(xq))
+        return fail(NEO_ERR_ALIGN, "neo_quantize_int8: buffers not 16-byte aligned");
+    CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    if (!(x_scale > 0.f) || !std::isfinite(x_scale))
+        return fail(NEO_ERR_INVALID_ARG, "neo_quantize_int8: x_scale must be finite and > 0");
+    CHECK_SIZE(blocked_elems(N, C, H, W, 16));
+    hipError_t e = launch_quantize_int8(x, blocked_elems(N, C, H, W, 16) / 16, x_scale, xq,
+                                        (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_quantize_int8 launch");
+}
+
+int neo_pack_filter_int8(const float* w_kcrs, int K, int C, int R, int S, int8_t* w_packed,
+                         float* w_scale, neo_stream_t stream) {
+    if (!w_kcrs || !w_packed || !w_scale)
+        return fail(NEO_ERR_INVALID_ARG, "neo_pack_filter_int8: NULL buffer");
+    CHECK_POS(K); CHECK_POS(C); CHECK_POS(R); CHECK_POS(S);
+    CHECK_SIZE((long)K * C * R * S);
+    if (int8_filter_bytes(K, C, R, S) > (size_t)kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_pack_filter_int8: packed filter of 2 GiB or more");
+    hipError_t e = launch_pack_filter_int8(w_kcrs, K, C, R, S, w_packed, w_scale, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_pack_filter_int8 launch");
+}
+
+int neo_conv2d_int8(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed,
+                    const float* w_scale, int K, int R, int S, float x_scale, const float* bias,
+                    int stride_h, int stride_w, int pad_h, int pad_w, const neo_epilogue* ep,
+                    float* y, int y_cblk_offset, int y_cblk_total, neo_stream_t stream) {
+    return conv_int8_common("neo_conv2d_int8", xq, N, C, H, W, w_packed, w_scale, K, R, S, x_scale,
+                            bias, stride_h, stride_w, pad_h, pad_w, ep, y, y_cblk_offset,
+                            y_cblk_total, nullptr, stream);
+}
+
+int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed, int K,
+                        int R, int S, int stride_h, int stride_w, int pad_h, int pad_w, int32_t* acc,
+                        neo_stream_t stream) {
+    if (!acc) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_int8_acc: acc is NULL");
+    return conv_int8_common("neo_conv2d_int8_acc", xq, N, C, H, W, w_packed, nullptr, K, R, S, 1.f,
+                            nullptr, stride_h, stride_w, pad_h, pad_w, nullptr, nullptr, 0,
+                            cdiv(K, 16), acc, stream);
 }
 
 int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,

@@ -1,0 +1,388 @@
+// Integer (INT8) convolution on MFMA (gfx950) -- the paper's other future
+// work beside fast convolution algorithms (Sections 1 and 5): symmetric linear
+// quantization with exact integer accumulation.
+//
+//   - Activations stay in the blocked layout with int8 elements: NCHW16c,
+//     16 bytes per pixel block.  A reduction step is one kernel entry (r, s)
+//     and one group of 64 input channels (four 16-channel blocks): lane
+//     (i, g) loads the 16 bytes of block 4 cg + g of its pixel i with one
+//     buffer load (blocks past the last read as 0 through the range check).
+//   - v_mfma_i32_16x16x64_i8 takes 16 int8 per lane for A (filter, output
+//     channel i) and B (input, pixel i); lane group g and byte b of both name
+//     the same input channel 64 cg + 16 g + b, so the instruction sums over
+//     all 64 whatever its internal order.  Filters are packed so that the A
+//     operand is one 16-byte load too, in step order: block (kb, r, s, cg)
+//     holds, for lane (k, g), w[16 kb + k][64 cg + 16 g + b][r][s], b = 0..15.
+//   - The int32 accumulator is exact (|sum| <= 127^2 * C * R * S), and the
+//     waves of a workgroup add their partial tiles through LDS (integer sums:
+//     any order gives the same bits).  The MFMA result layout is the fp32
+//     kernel's: lane (i, g) holds output channels 4 g .. 4 g + 3 of pixel i.
+//   - Epilogue: y = act(acc * (s_x * s_w[k]) + bias[k] + residual) in float32,
+//     one float4 store into the NCHW16c output view; or (the _acc entry point)
+//     the raw int32 accumulators.
+#include <cstdint>
+
+#include "conv_kernel.h"
+
+namespace neo {
+
+using conv_detail::FastDiv;
+using conv_detail::fdiv;
+using conv_detail::kOutOfRange;
+using conv_detail::kRsrcWord3;
+using conv_detail::make_fastdiv;
+using conv_detail::v4f;
+using conv_detail::xcd_order;
+
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+constexpr int kQMax = 127;
+
+struct I8Args {
+    const int8_t* x;      // NCHW16c int8 [N][CB][H][W][16]
+    const int8_t* w;      // packed [KB][R][S][CG][64 lanes][16 bytes]
+    const float* wscale;  // [KB * 16] per-output-channel filter scales
+    float xscale;         // the activations' scale
+    const float* bias;    // [KB * 16] or null
+    const float* res;     // fp32 NCHW16c [N][KB][OH][OW][16] or null
+    float* y;             // fp32 NCHW16c view: blocks [y_off, y_off + KB) of y_tot
+    int* acc;             // raw mode: int32 NCHW16c [N][KB][OH][OW][16]
+    int N, CB, CG, H, W, KB, R, S, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act;
+    int T;                // reduction steps: R * S * CG
+    int npx, nkt;         // pixel tiles (16 * FP pixels), channel tiles (FK blocks)
+    int x_bytes, w_bytes;
+    FastDiv div_ohw, div_ow, div_npx;
+};
+
+__device__ inline v4i ld16(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
+    return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+template <int FK, int FP, int WAVES, bool RAW>
+__global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int li = lane & 15, g = lane >> 4;
+    // pixel tiles fastest in each XCD's contiguous run (as the fp32 kernel
+    // below its large-launch threshold)
+    const int u = __builtin_amdgcn_readfirstlane(xcd_order());
+    const int kt = fdiv(u, a.div_npx);
+    const int pxt = u - kt * a.npx;
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t wr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
+
+    const int hw16 = a.H * a.W * 16;  // bytes per channel block plane
+    bool pv[FP];
+    int pn[FP], poh[FP], pow_[FP], pih[FP], piw[FP], pbase[FP];
+#pragma unroll
+    for (int p = 0; p < FP; ++p) {
+        const int m = (pxt * FP + p) * 16 + li;
+        pv[p] = m < a.M;  // lanes past the last pixel compute pixel 0 and never store
+        const int mm = pv[p] ? m : 0;
+        const int n = fdiv(mm, a.div_ohw);
+        const int rem = mm - n * a.OH * a.OW;
+        const int oh = fdiv(rem, a.div_ow);
+        const int ow = rem - oh * a.OW;
+        pn[p] = n;
+        poh[p] = oh;
+        pow_[p] = ow;
+        pih[p] = oh * a.sh - a.ph;
+        piw[p] = ow * a.sw - a.pw;
+        // byte offset of the pixel's (r, s) = (0, 0) element, channel block g
+        pbase[p] = ((n * a.CB + g) * a.H + pih[p]) * a.W * 16 + piw[p] * 16;
+    }
+    unsigned woff[FK];
+#pragma unroll
+    for (int f = 0; f < FK; ++f)
+        woff[f] = (unsigned)((kt * FK + f) * a.T * 1024 + (g * 16 + li) * 16);
+
+    // this wave's contiguous run of steps st = (r * S + s) * CG + cg
+    const int w_lo = __builtin_amdgcn_readfirstlane((int)(((long)a.T * wave) / WAVES));
+    const int w_hi = __builtin_amdgcn_readfirstlane((int)(((long)a.T * (wave + 1)) / WAVES));
+
+    v4i acc[FK][FP];
+#pragma unroll
+    for (int f = 0; f < FK; ++f)
+#pragma unroll
+        for (int p = 0; p < FP; ++p) acc[f][p] = v4i{0, 0, 0, 0};
+
+    auto load = [&](int st, v4i (&A)[FK], v4i (&B)[FP]) {
+        const int cg = st % a.CG, rs = st / a.CG;
+        const int r = rs / a.S, s = rs - r * a.S;
+        const bool cok = 4 * cg + g < a.CB;
+#pragma unroll
+        for (int p = 0; p < FP; ++p) {
+            const bool ok = cok && (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
+            const unsigned off = ok ? (unsigned)(pbase[p] + 4 * cg * hw16 + (r * a.W + s) * 16) : kOutOfRange;
+            B[p] = ld16(xr, off, 0);
+        }
+        const int sw_ = __builtin_amdgcn_readfirstlane(st * 1024);
+#pragma unroll
+        for (int f = 0; f < FK; ++f) A[f] = ld16(wr, woff[f], sw_);
+    };
+
+    if (w_lo < w_hi) {
+        v4i A0[FK], B0[FP], A1[FK], B1[FP];
+        load(w_lo, A0, B0);
+        int st = w_lo;
+        // two steps per iteration, so the two operand sets stay in registers
+        for (; st + 1 < w_hi; st += 2) {
+            load(st + 1, A1, B1);
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p)
+                    acc[f][p] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[f], B0[p], acc[f][p], 0, 0, 0);
+            if (st + 2 < w_hi) load(st + 2, A0, B0);
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p)
+                    acc[f][p] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[f], B1[p], acc[f][p], 0, 0, 0);
+        }
+        if (st < w_hi) {
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p)
+                    acc[f][p] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[f], B0[p], acc[f][p], 0, 0, 0);
+        }
+    }
+
+    if constexpr (WAVES > 1) {
+        __shared__ v4i red[WAVES - 1][FK * FP][64];
+        if (wave > 0) {
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p) red[wave - 1][f * FP + p][lane] = acc[f][p];
+        }
+        __syncthreads();
+        if (wave != 0) return;
+#pragma unroll
+        for (int w = 0; w < WAVES - 1; ++w)
+#pragma unroll
+            for (int f = 0; f < FK; ++f)
+#pragma unroll
+                for (int p = 0; p < FP; ++p) acc[f][p] += red[w][f * FP + p][lane];
+    }
+
+    const int ohw = a.OH * a.OW;
+#pragma unroll
+    for (int f = 0; f < FK; ++f) {
+        const int kb = kt * FK + f;
+        v4f mult = v4f{0.f, 0.f, 0.f, 0.f}, bb = v4f{0.f, 0.f, 0.f, 0.f};
+        if constexpr (!RAW) {
+            const v4f ws = *reinterpret_cast<const v4f*>(a.wscale + kb * 16 + 4 * g);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) mult[v] = a.xscale * ws[v];
+            if (a.bias) bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
+        }
+#pragma unroll
+        for (int p = 0; p < FP; ++p) {
+            if (!pv[p]) continue;
+            const int pix = poh[p] * a.OW + pow_[p];
+            if constexpr (RAW) {
+                *reinterpret_cast<v4i*>(a.acc + ((pn[p] * a.KB + kb) * ohw + pix) * 16 + 4 * g) = acc[f][p];
+                continue;
+            }
+            v4f o;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[v] = (float)acc[f][p][v] * mult[v] + bb[v];
+            if (a.res) o += *reinterpret_cast<const v4f*>(a.res + ((pn[p] * a.KB + kb) * ohw + pix) * 16 + 4 * g);
+            if (a.act == NEO_ACT_RELU) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
+            }
+            *reinterpret_cast<v4f*>(a.y + ((pn[p] * a.y_tot + a.y_off + kb) * ohw + pix) * 16 + 4 * g) = o;
+        }
+    }
+}
+
+// fp32 NCHW16c -> int8 NCHW16c: clamp(round_half_even(x / scale), -127, 127),
+// one pixel block (16 values) per thread.  Padding lanes (+0.0) give 0.
+__global__ __launch_bounds__(256) void quantize_kernel(const float* x, long blocks, float scale, int8_t* q) {
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= blocks) return;
+    const v4f* src = reinterpret_cast<const v4f*>(x + t * 16);
+    union {
+        int8_t b[16];
+        v4i v;
+    } out;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const v4f v = src[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float r = rintf(v[j] / scale);
+            r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
+            out.b[4 * i + j] = (int8_t)(int)r;
+        }
+    }
+    *reinterpret_cast<v4i*>(q + t * 16) = out.v;
+}
+
+// KCRS fp32 -> per-output-channel scales and the packed int8 filter, one
+// workgroup per (padded) output channel: max |w[k]| by a tree in LDS, then
+// every element quantized and written to its packed position.
+__global__ __launch_bounds__(256) void pack_filter_i8_kernel(const float* w, int K, int C, int R, int S,
+                                                             int8_t* wq, float* wscale) {
+    const int k = blockIdx.x;
+    const int CG = (C + 63) / 64;
+    const long per = (long)C * R * S;
+    __shared__ float red[256];
+    float m = 0.f;
+    if (k < K)
+        for (long i = threadIdx.x; i < per; i += 256) m = fmaxf(m, fabsf(w[k * per + i]));
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + h]);
+        __syncthreads();
+    }
+    const float mx = red[0];
+    const float s = mx > 0.f ? mx / (float)kQMax : 1.f;
+    if (threadIdx.x == 0) wscale[k] = s;
+    // every (c, r, s) of this output channel's packed blocks, padding channels 0
+    const long total = (long)CG * 64 * R * S;
+    const int kb = k >> 4, kk = k & 15;
+    for (long i = threadIdx.x; i < total; i += 256) {
+        const int c = (int)(i / (R * S));
+        const int rs = (int)(i - (long)c * R * S);
+        const int r = rs / S, sx = rs - r * S;
+        int8_t q = 0;
+        if (k < K && c < C) {
+            float v = rintf(w[(k * (long)C + c) * R * S + rs] / s);
+            v = v > (float)kQMax ? (float)kQMax : (v < -(float)kQMax ? -(float)kQMax : v);
+            q = (int8_t)(int)v;
+        }
+        const int cg = c >> 6, gg = (c >> 4) & 3, b = c & 15;
+        wq[((((long)kb * R + r) * S + sx) * CG + cg) * 1024 + (gg * 16 + kk) * 16 + b] = q;
+    }
+}
+
+template <int FK, int FP, int WAVES, bool RAW>
+hipError_t launch_t(const I8Args& a, hipStream_t st) {
+    const long wgs = (long)a.npx * a.nkt;
+    hipLaunchKernelGGL((conv_i8<FK, FP, WAVES, RAW>), dim3((unsigned)wgs), dim3(WAVES * 64), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int FK, int FP, bool RAW>
+hipError_t by_waves(int waves, const I8Args& a, hipStream_t st) {
+    switch (waves) {
+        case 1: return launch_t<FK, FP, 1, RAW>(a, st);
+        case 2: return launch_t<FK, FP, 2, RAW>(a, st);
+        case 4: return launch_t<FK, FP, 4, RAW>(a, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <bool RAW>
+hipError_t by_tile(const ConvConfig& c, const I8Args& a, hipStream_t st) {
+    if (c.fk == 1 && c.fp == 1) return by_waves<1, 1, RAW>(c.waves, a, st);
+    if (c.fk == 1 && c.fp == 2) return by_waves<1, 2, RAW>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 1) return by_waves<2, 1, RAW>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 2) return by_waves<2, 2, RAW>(c.waves, a, st);
+    if (c.fk == 4 && c.fp == 2) return by_waves<4, 2, RAW>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 4) return by_waves<2, 4, RAW>(c.waves, a, st);
+    if (c.fk == 4 && c.fp == 4) return by_waves<4, 4, RAW>(c.waves, a, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+size_t int8_filter_bytes(int K, int C, int R, int S) {
+    return (size_t)cdiv(K, 16) * cdiv(C, 64) * R * S * 1024;
+}
+
+bool int8_config_valid(const ConvShape& s, const ConvConfig& c) {
+    const int KB = cdiv(s.K, 16);
+    const bool tile = (c.fk == 1 && (c.fp == 1 || c.fp == 2)) || (c.fk == 2 && c.fp <= 4 && c.fp != 3) ||
+                      (c.fk == 4 && (c.fp == 2 || c.fp == 4));
+    return tile && KB % c.fk == 0 && c.split == 1 && (c.waves == 1 || c.waves == 2 || c.waves == 4) &&
+           s.R * s.S * cdiv(s.C, 64) >= c.waves;
+}
+
+// The register tile and waves with the most tiles that still give every SIMD
+// work: larger tiles load fewer bytes per MFMA, more waves split short grids.
+ConvConfig choose_int8_config(const ConvShape& s) {
+    const int KB = cdiv(s.K, 16), MP = cdiv(s.N * s.OH * s.OW, 16);
+    static const ConvConfig order[] = {{4, 4, 1, 1}, {2, 4, 1, 1}, {4, 2, 1, 1}, {2, 2, 1, 1},
+                                       {2, 1, 1, 1}, {1, 2, 1, 1}, {1, 1, 1, 1}};
+    for (const ConvConfig& c0 : order) {
+        if (KB % c0.fk) continue;
+        const long tiles = (long)cdiv(MP, c0.fp) * (KB / c0.fk);
+        for (int wv : {1, 2, 4}) {
+            const ConvConfig c{c0.fk, c0.fp, 1, wv};
+            if (int8_config_valid(s, c) && tiles * wv >= 1024) return c;
+        }
+    }
+    for (int wv : {4, 2, 1}) {
+        const ConvConfig c{1, 1, 1, wv};
+        if (int8_config_valid(s, c)) return c;
+    }
+    return ConvConfig{1, 1, 1, 1};
+}
+
+hipError_t launch_quantize_int8(const float* x, long blocks, float scale, int8_t* q, hipStream_t st) {
+    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)((blocks + 255) / 256)), dim3(256), 0, st, x, blocks,
+                       scale, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, int8_t* wq, float* wscale,
+                                   hipStream_t st) {
+    hipLaunchKernelGGL(pack_filter_i8_kernel, dim3((unsigned)(cdiv(K, 16) * 16)), dim3(256), 0, st, w, K, C,
+                       R, S, wq, wscale);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
+                            const float* wscale, float xscale, const float* bias, const float* res,
+                            float* y, int* acc, hipStream_t st) {
+    if (!int8_config_valid(s, c)) return hipErrorInvalidValue;
+    I8Args a;
+    a.x = x;
+    a.w = w;
+    a.wscale = wscale;
+    a.xscale = xscale;
+    a.bias = bias;
+    a.res = res;
+    a.y = y;
+    a.acc = acc;
+    a.N = s.N;
+    a.CB = cdiv(s.C, 16);
+    a.CG = cdiv(s.C, 64);
+    a.H = s.H;
+    a.W = s.W;
+    a.KB = cdiv(s.K, 16);
+    a.R = s.R;
+    a.S = s.S;
+    a.sh = s.sh;
+    a.sw = s.sw;
+    a.ph = s.ph;
+    a.pw = s.pw;
+    a.OH = s.OH;
+    a.OW = s.OW;
+    a.M = s.N * s.OH * s.OW;
+    a.y_off = s.y_off;
+    a.y_tot = s.y_tot;
+    a.act = s.act;
+    a.T = s.R * s.S * a.CG;
+    a.npx = cdiv(a.M, 16 * c.fp);
+    a.nkt = a.KB / c.fk;
+    a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 16);
+    a.w_bytes = (int)int8_filter_bytes(s.K, s.C, s.R, s.S);
+    a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
+    a.div_ow = make_fastdiv((unsigned)s.OW);
+    a.div_npx = make_fastdiv((unsigned)a.npx);
+    return acc ? by_tile<true>(c, a, st) : by_tile<false>(c, a, st);
+}
+
+}  // namespace neo

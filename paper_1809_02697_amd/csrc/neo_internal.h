@@ -119,6 +119,22 @@ int tune_wino(const ConvShape& s, const float* x, const float* u, const float* b
               const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
 bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 
+// Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations, a
+// packed int8 filter with per-output-channel scales, int32 accumulation on
+// v_mfma_i32_16x16x64_i8.  Configuration: fk output blocks x fp pixel groups
+// per wave, `waves` waves splitting the reduction (split must be 1).
+// launch_conv_int8 writes the dequantized float32 output y (with the epilogue
+// of s: act, y_off, y_tot), or with `acc` non-null the raw int32 sums.
+size_t int8_filter_bytes(int K, int C, int R, int S);
+bool int8_config_valid(const ConvShape& s, const ConvConfig& c);
+ConvConfig choose_int8_config(const ConvShape& s);
+hipError_t launch_quantize_int8(const float* x, long blocks, float scale, int8_t* q, hipStream_t st);
+hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, int8_t* wq, float* wscale,
+                                   hipStream_t st);
+hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
+                            const float* wscale, float xscale, const float* bias, const float* res,
+                            float* y, int* acc, hipStream_t st);
+
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
 // or null; res: NCHW[yb]c [N][ceil(K/yb)][OH][OW][yb] or null; y: NCHW[yb]c

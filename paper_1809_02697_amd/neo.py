@@ -95,6 +95,11 @@ def lib():
         "neo_winograd_filter": [P, I, I, P, P],
         "neo_conv2d_winograd": [P, I, I, I, I, P, I, P, I, I, ctypes.POINTER(Epilogue), P, I, I,
                                 P],
+        "neo_quantize_int8": [P, I, I, I, I, F, P, P],
+        "neo_pack_filter_int8": [P, I, I, I, I, P, P, P],
+        "neo_conv2d_int8": [P, I, I, I, I, P, P, I, I, I, F, P, I, I, I, I,
+                            ctypes.POINTER(Epilogue), P, I, I, P],
+        "neo_conv2d_int8_acc": [P, I, I, I, I, P, I, I, I, I, I, I, I, P, P],
         "neo_fold_bn": [P, P, P, P, P, P, F, I, I, I, I, P, P],
         "neo_maxpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
         "neo_avgpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
@@ -156,6 +161,18 @@ def _dptr(t, name="tensor"):
         raise TypeError(f"{name} must be a device (cuda) tensor")
     if t.dtype != torch.float32:
         raise TypeError(f"{name} must be float32")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dptr_typed(t, dtype, name="tensor"):
+    """_dptr for a device tensor of another element type (int8, int32)."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device (cuda) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return ctypes.c_void_p(t.data_ptr())
@@ -314,6 +331,107 @@ def conv2d_winograd(x, C, u, K, bias=None, pad=1, act="none", residual=None, out
     _check(lib().neo_conv2d_winograd(_dptr(x, "x"), N, C, H, W, _dptr(u, "u"), K,
                                      _dptr(bias, "bias"), ph, pw, ctypes.byref(ep),
                                      _dptr(out, "out"), y_cblk_offset, tot, _stream(stream)))
+    return out
+
+
+def int8_filter_bytes(K, C, R, S):
+    return cblocks(K) * cblocks(C, 64) * R * S * 1024
+
+
+def quantize_int8(x, C, x_scale, out=None, stream=None):
+    """x: fp32 NCHW16c of C channels -> int8 NCHW16c,
+    clamp(round_half_even(x / x_scale), -127, 127)."""
+    import torch
+    N, XB, H, W, blk = x.shape
+    if blk != BLOCK or XB != cblocks(C):
+        raise ValueError(f"x shape {tuple(x.shape)} is not NCHW16c of {C} channels")
+    if out is None:
+        out = torch.empty(x.shape, device=x.device, dtype=torch.int8)
+    if out.numel() < x.numel():
+        raise ValueError(f"out holds {out.numel()} bytes, the call needs {x.numel()}")
+    _check(lib().neo_quantize_int8(_dptr(x, "x"), N, C, H, W, float(x_scale),
+                                   _dptr_typed(out, torch.int8, "out"), _stream(stream)))
+    return out
+
+
+def pack_filter_int8(w, out=None, scale=None, stream=None):
+    """w: device KCRS fp32 -> (packed int8 filter, per-output-channel scales
+    [ceil(K/16)*16] fp32), the scales max |w[k]| / 127."""
+    import torch
+    K, C, R, S = w.shape
+    nb = int8_filter_bytes(K, C, R, S)
+    if out is None:
+        out = torch.empty(nb, device=w.device, dtype=torch.int8)
+    if scale is None:
+        scale = torch.empty(cblocks(K) * BLOCK, device=w.device, dtype=torch.float32)
+    if out.numel() < nb:
+        raise ValueError(f"out holds {out.numel()} bytes, the call needs {nb}")
+    _need(scale, cblocks(K) * BLOCK, "scale")
+    _check(lib().neo_pack_filter_int8(_dptr(w, "w"), K, C, R, S,
+                                      _dptr_typed(out, torch.int8, "out"), _dptr(scale, "scale"),
+                                      _stream(stream)))
+    return out, scale
+
+
+def _int8_args(xq, C, w_packed, K, R, S, stride, pad):
+    (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
+    N, XB, H, W, blk = xq.shape
+    if blk != BLOCK or XB != cblocks(C):
+        raise ValueError(f"xq shape {tuple(xq.shape)} is not NCHW16c of {C} channels")
+    if w_packed.numel() < int8_filter_bytes(K, C, R, S):
+        raise ValueError(f"w_packed holds {w_packed.numel()} bytes, the call needs "
+                         f"{int8_filter_bytes(K, C, R, S)}")
+    return N, H, W, sh, sw, ph, pw, out_size(H, R, sh, ph), out_size(W, S, sw, pw)
+
+
+def _int8_ptrs(xq, w_packed):
+    import torch
+    return _dptr_typed(xq, torch.int8, "xq"), _dptr_typed(w_packed, torch.int8, "w_packed")
+
+
+def conv2d_int8(xq, C, w_packed, w_scale, K, R, S, x_scale, bias=None, stride=1, pad=0,
+                act="none", residual=None, out=None, y_cblk_offset=0, y_cblk_total=None,
+                stream=None):
+    """Integer convolution: xq int8 NCHW16c (quantize_int8), w_packed and
+    w_scale from pack_filter_int8; fp32 NCHW16c output
+    act(acc * x_scale * w_scale[k] + bias + residual), the view as conv2d_blocked."""
+    import torch
+    N, H, W, sh, sw, ph, pw, OH, OW = _int8_args(xq, C, w_packed, K, R, S, stride, pad)
+    tot = cblocks(K) if y_cblk_total is None else y_cblk_total
+    if out is None:
+        out = torch.empty((N, tot, max(OH, 0), max(OW, 0), BLOCK), device=xq.device,
+                          dtype=torch.float32)
+    if OH > 0 and OW > 0:
+        _need(out, N * tot * OH * OW * BLOCK, "out")
+        _need(residual, N * cblocks(K) * OH * OW * BLOCK, "residual")
+    _need(bias, cblocks(K) * BLOCK, "bias")
+    _need(w_scale, cblocks(K) * BLOCK, "w_scale")
+    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
+                  residual.data_ptr() if residual is not None else None)
+    if residual is not None:
+        _dptr(residual, "residual")
+    xp, wp = _int8_ptrs(xq, w_packed)
+    _check(lib().neo_conv2d_int8(xp, N, C, H, W, wp, _dptr(w_scale, "w_scale"), K, R, S,
+                                 float(x_scale), _dptr(bias, "bias"), sh, sw, ph, pw,
+                                 ctypes.byref(ep), _dptr(out, "out"), y_cblk_offset, tot,
+                                 _stream(stream)))
+    return out
+
+
+def conv2d_int8_acc(xq, C, w_packed, K, R, S, stride=1, pad=0, out=None, stream=None):
+    """The exact int32 sums of the integer convolution, int32 NCHW16c
+    [N][ceil(K/16)][OH][OW][16] (padding channels 0)."""
+    import torch
+    N, H, W, sh, sw, ph, pw, OH, OW = _int8_args(xq, C, w_packed, K, R, S, stride, pad)
+    if out is None:
+        out = torch.empty((N, cblocks(K), max(OH, 0), max(OW, 0), BLOCK), device=xq.device,
+                          dtype=torch.int32)
+    if OH > 0 and OW > 0 and out.numel() < N * cblocks(K) * OH * OW * BLOCK:
+        raise ValueError(f"out holds {out.numel()} values, the call needs "
+                         f"{N * cblocks(K) * OH * OW * BLOCK}")
+    xp, wp = _int8_ptrs(xq, w_packed)
+    _check(lib().neo_conv2d_int8_acc(xp, N, C, H, W, wp, K, R, S, sh, sw, ph, pw,
+                                     _dptr_typed(out, torch.int32, "out"), _stream(stream)))
     return out
 
 
