@@ -214,21 +214,25 @@ int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float*
  *                float32 (the product x_scale * w_scale[k] rounded to float32).
  *
  * neo_quantize_int8: x device fp32 NCHW16c [N][ceil(C/16)][H][W][16] -> xq
- *   device int8 NCHW16c of the same shape (padding lanes 0); x_scale > 0.
+ *   device int8 NCHW16c with the zero padding of the convolution that reads
+ *   it stored as a halo: [N][ceil(C/16)][H + 2 pad_h][W + 2 pad_w][16], the
+ *   pixel (h, w) at (h + pad_h, w + pad_w), halo and padding lanes 0;
+ *   x_scale > 0.
  * neo_pack_filter_int8: w_kcrs device fp32 [K][C][R][S] -> w_packed device
  *   int8, int8_filter_bytes = ceil(K/16) * ceil(C/64) * R * S * 1024 bytes,
  *   block (kb, r, s, cg) holding for lane (k, g) the 16 bytes
  *   q_w[16 kb + k][64 cg + 16 g + b][r][s], b = 0..15 (zero padded); and
  *   w_scale device [ceil(K/16)*16] (padding channels 1).
- * neo_conv2d_int8: xq, w_packed and w_scale as written above; bias device
+ * neo_conv2d_int8: xq, w_packed and w_scale as written above, xq quantized
+ *   with this call's pad_h and pad_w (H and W name the unpadded size); bias device
  *   [ceil(K/16)*16] or NULL; ep, y and the output view as for
  *   neo_conv2d_blocked (float32 NCHW16c).
  * neo_conv2d_int8_acc: the same convolution, writing the raw int32 sums to acc
  *   device [N][ceil(K/16)][OH][OW][16] (padding channels 0): the exact part.
  * Dilation and groups are 1.  Errors as for neo_conv2d_blocked.
  */
-int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int8_t* xq,
-                      neo_stream_t stream);
+int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int pad_h,
+                      int pad_w, int8_t* xq, neo_stream_t stream);
 int neo_pack_filter_int8(const float* w_kcrs, int K, int C, int R, int S, int8_t* w_packed,
                          float* w_scale, neo_stream_t stream);
 int neo_conv2d_int8(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed,

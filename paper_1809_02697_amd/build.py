@@ -19,11 +19,16 @@ SOURCES = ["conv.hip", "conv_xy.hip", "conv_group.hip", "conv_pair.hip", "layout
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument"]
+# Per-source additions.  The integer kernels keep their MFMA accumulators in
+# ordinary VGPRs: with the default AGPR form the compiler rotated them through
+# accumulator-register copies inside the reduction loop (v_accvgpr_mov).
+SOURCE_FLAGS = {"conv_int8.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _compile(src, objdir):
     obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
-    cmd = ["hipcc", "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + FLAGS
+    cmd = ["hipcc", "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + FLAGS + \
+        SOURCE_FLAGS.get(src, [])
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -330,6 +330,10 @@ int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int 
                                              "int32 accumulator");
     if (int8_filter_bytes(K, C, R, S) > (size_t)kMaxElems)
         return fail(NEO_ERR_UNSUPPORTED, f + ": packed filter of 2 GiB or more");
+    // (four channel-block planes of slack: the loads of blocks past the last
+    // stay below 2^31 as byte offsets and read 0 through the range check)
+    if (((long)N * cdiv(C, 16) + 4) * (H + 2L * pad_h) * (W + 2L * pad_w) * 16 > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, f + ": padded int8 input of 2 GiB or more");
     cfg = choose_int8_config(s);
     env_i8_config(s, &cfg);
     hipError_t e = launch_conv_int8(s, cfg, xq, w_packed, w_scale, x_scale, bias, res, y, acc,
@@ -437,17 +441,19 @@ int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float*
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_conv2d_winograd launch");
 }
 
-int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int8_t* xq,
-                      neo_stream_t stream) {
+int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int pad_h,
+                      int pad_w, int8_t* xq, neo_stream_t stream) {
     if (!x || !xq) return fail(NEO_ERR_INVALID_ARG, "neo_quantize_int8: NULL buffer");
     if (!aligned16(x) || !aligned16(xq))
         return fail(NEO_ERR_ALIGN, "neo_quantize_int8: buffers not 16-byte aligned");
     CHECK_POS(N); CHECK_POS(C); CHECK_POS(H); CHECK_POS(W);
+    if (pad_h < 0 || pad_w < 0) return fail(NEO_ERR_INVALID_ARG, "neo_quantize_int8: negative pad");
     if (!(x_scale > 0.f) || !std::isfinite(x_scale))
         return fail(NEO_ERR_INVALID_ARG, "neo_quantize_int8: x_scale must be finite and > 0");
     CHECK_SIZE(blocked_elems(N, C, H, W, 16));
-    hipError_t e = launch_quantize_int8(x, blocked_elems(N, C, H, W, 16) / 16, x_scale, xq,
-                                        (hipStream_t)stream);
+    if ((long)N * cdiv(C, 16) * (H + 2L * pad_h) * (W + 2L * pad_w) * 16 > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_quantize_int8: padded int8 tensor of 2 GiB or more");
+    hipError_t e = launch_quantize_int8(x, N, C, H, W, pad_h, pad_w, x_scale, xq, (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_quantize_int8 launch");
 }
 

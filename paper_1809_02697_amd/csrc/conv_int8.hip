@@ -2,17 +2,28 @@
 // work beside fast convolution algorithms (Sections 1 and 5): symmetric linear
 // quantization with exact integer accumulation.
 //
-//   - Activations stay in the blocked layout with int8 elements: NCHW16c,
-//     16 bytes per pixel block.  A reduction step is one kernel entry (r, s)
-//     and one group of 64 input channels (four 16-channel blocks): lane
-//     (i, g) loads the 16 bytes of block 4 cg + g of its pixel i with one
-//     buffer load (blocks past the last read as 0 through the range check).
+//   - Activations are int8 in the blocked layout, NCHW16c (16 bytes per
+//     pixel block), stored with the convolution's zero padding as an explicit
+//     halo: [N][CB][H + 2 ph][W + 2 pw][16].  The quantization pass writes the
+//     halo, so every tap of every output pixel is an in-bounds read and the
+//     reduction loop has no bounds tests.  A reduction step is one kernel
+//     entry (r, s) and one group of 64 input channels (four 16-channel
+//     blocks): lane (i, g) loads the 16 bytes of block 4 cg + g of its pixel i
+//     with one buffer load; a lane whose block does not exist (C not a
+//     multiple of 64) loads from an out-of-range offset, which reads 0
+//     without memory traffic.
 //   - v_mfma_i32_16x16x64_i8 takes 16 int8 per lane for A (filter, output
 //     channel i) and B (input, pixel i); lane group g and byte b of both name
 //     the same input channel 64 cg + 16 g + b, so the instruction sums over
 //     all 64 whatever its internal order.  Filters are packed so that the A
 //     operand is one 16-byte load too, in step order: block (kb, r, s, cg)
 //     holds, for lane (k, g), w[16 kb + k][64 cg + 16 g + b][r][s], b = 0..15.
+//   - A wave's instruction stream, not the matrix unit, bounds this kernel at
+//     the one or two waves per SIMD these layers give (a single wave issues
+//     about one instruction per eight cycles; one MFMA here is sixteen): the
+//     step decode is scalar and incremental, the loop issues per step only the
+//     loads, one address add per input load and the MFMAs, and the epilogue
+//     addresses are precomputed per pixel.
 //   - The int32 accumulator is exact (|sum| <= 127^2 * C * R * S), and the
 //     waves of a workgroup add their partial tiles through LDS (integer sums:
 //     any order gives the same bits).  The MFMA result layout is the fp32
@@ -20,6 +31,7 @@
 //   - Epilogue: y = act(acc * (s_x * s_w[k]) + bias[k] + residual) in float32,
 //     one float4 store into the NCHW16c output view; or (the _acc entry point)
 //     the raw int32 accumulators.
+#include <algorithm>
 #include <cstdint>
 
 #include "conv_kernel.h"
@@ -41,7 +53,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 constexpr int kQMax = 127;
 
 struct I8Args {
-    const int8_t* x;      // NCHW16c int8 [N][CB][H][W][16]
+    const int8_t* x;      // int8 NCHW16c with halo [N][CB][Hp][Wp][16]
     const int8_t* w;      // packed [KB][R][S][CG][64 lanes][16 bytes]
     const float* wscale;  // [KB * 16] per-output-channel filter scales
     float xscale;         // the activations' scale
@@ -49,9 +61,10 @@ struct I8Args {
     const float* res;     // fp32 NCHW16c [N][KB][OH][OW][16] or null
     float* y;             // fp32 NCHW16c view: blocks [y_off, y_off + KB) of y_tot
     int* acc;             // raw mode: int32 NCHW16c [N][KB][OH][OW][16]
-    int N, CB, CG, H, W, KB, R, S, sh, sw, ph, pw, OH, OW, M, y_off, y_tot, act;
+    int N, CB, CG, Hp, Wp, KB, S, sh, sw, OH, OW, M, y_off, y_tot, act;
     int T;                // reduction steps: R * S * CG
     int npx, nkt;         // pixel tiles (16 * FP pixels), channel tiles (FK blocks)
+    int ntiles;           // npx * nkt
     int x_bytes, w_bytes;
     FastDiv div_ohw, div_ow, div_npx;
 };
@@ -60,41 +73,79 @@ __device__ inline v4i ld16(__amdgpu_buffer_rsrc_t r, unsigned voff, int soff) {
     return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
+// A wave's position in its run of reduction steps st = (r * S + s) * CG + cg:
+// the step, its channel group and kernel column, and the input bytes the
+// channel group and tap add to a window's first byte.
+struct StepCursor {
+    int st, cg, s, uoff;
+};
+// The run's constants: the last step and the uoff increments to the next
+// channel group, the next tap of a kernel row and the next kernel row.
+struct StepGeometry {
+    int CG, S, hi, d_cg, d_s, d_r;
+};
+
+// Issue the loads of the cursor's step (input pixel blocks, filter blocks)
+// and advance the cursor, unless it is at the run's last step.
+template <int FK, int FP>
+__device__ __forceinline__ void load_step(const __amdgpu_buffer_rsrc_t xr, const __amdgpu_buffer_rsrc_t wr,
+                                          const int (&xbase)[FP], const unsigned (&woff)[FK], const int glim,
+                                          const StepGeometry geo, StepCursor& c, v4i (&A)[FK], v4i (&B)[FP]) {
+    // a lane whose channel block 4 cg + g does not exist (C <= 48, or the last
+    // group of a C that is not a multiple of 64) reads nothing: its filter
+    // bytes are zero, and the out-of-range offset costs no memory traffic
+    const bool gok = 4 * c.cg < glim;
+#pragma unroll
+    for (int p = 0; p < FP; ++p) B[p] = ld16(xr, gok ? (unsigned)(xbase[p] + c.uoff) : kOutOfRange, 0);
+#pragma unroll
+    for (int f = 0; f < FK; ++f) A[f] = ld16(wr, woff[f], c.st * 1024);
+    // scalar selects, not a branch tree: the compiler turned the branches
+    // into a load of the increment from a stack copy of geo, which waited
+    // for every outstanding load
+    const bool more = c.st + 1 < geo.hi;
+    const bool cg_wrap = c.cg + 1 == geo.CG;
+    const bool s_wrap = c.s + 1 == geo.S;
+    const int inc = cg_wrap ? (s_wrap ? geo.d_r : geo.d_s) : geo.d_cg;
+    const int cg_next = cg_wrap ? 0 : c.cg + 1;
+    const int s_next = cg_wrap ? (s_wrap ? 0 : c.s + 1) : c.s;
+    c.uoff = more ? c.uoff + inc : c.uoff;
+    c.cg = more ? cg_next : c.cg;
+    c.s = more ? s_next : c.s;
+    c.st = more ? c.st + 1 : c.st;
+}
+
 template <int FK, int FP, int WAVES, bool RAW>
 __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int li = lane & 15, g = lane >> 4;
-    // pixel tiles fastest in each XCD's contiguous run (as the fp32 kernel
-    // below its large-launch threshold)
-    const int u = __builtin_amdgcn_readfirstlane(xcd_order());
+    const int ohw = a.OH * a.OW;
+    const int plane = a.Hp * a.Wp * 16;  // bytes per channel-block plane
+    // Output tiles u = first, first + grid, ...: a workgroup runs several in
+    // turn, so the stores of one drain while the next one loads and
+    // multiplies.  Pixel tiles fastest in each XCD's contiguous run (as the
+    // fp32 kernel below its large-launch threshold).
+    for (int u = __builtin_amdgcn_readfirstlane(xcd_order()); u < a.ntiles; u += gridDim.x) {
     const int kt = fdiv(u, a.div_npx);
     const int pxt = u - kt * a.npx;
 
-    const __amdgpu_buffer_rsrc_t xr =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t wr =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
-
-    const int hw16 = a.H * a.W * 16;  // bytes per channel block plane
     bool pv[FP];
-    int pn[FP], poh[FP], pow_[FP], pih[FP], piw[FP], pbase[FP];
+    int xbase[FP], obase[FP], ybase[FP];
 #pragma unroll
     for (int p = 0; p < FP; ++p) {
         const int m = (pxt * FP + p) * 16 + li;
         pv[p] = m < a.M;  // lanes past the last pixel compute pixel 0 and never store
         const int mm = pv[p] ? m : 0;
         const int n = fdiv(mm, a.div_ohw);
-        const int rem = mm - n * a.OH * a.OW;
-        const int oh = fdiv(rem, a.div_ow);
-        const int ow = rem - oh * a.OW;
-        pn[p] = n;
-        poh[p] = oh;
-        pow_[p] = ow;
-        pih[p] = oh * a.sh - a.ph;
-        piw[p] = ow * a.sw - a.pw;
-        // byte offset of the pixel's (r, s) = (0, 0) element, channel block g
-        pbase[p] = ((n * a.CB + g) * a.H + pih[p]) * a.W * 16 + piw[p] * 16;
+        const int pix = mm - n * ohw;
+        const int oh = fdiv(pix, a.div_ow);
+        const int ow = pix - oh * a.OW;
+        // the (r, s) = (0, 0) byte of the pixel's window in channel block g
+        xbase[p] = ((n * a.CB + g) * a.Hp + oh * a.sh) * a.Wp * 16 + ow * a.sw * 16;
+        // its output element in channel block 0 of [N][KB][OH][OW][16]
+        // (residual, accumulators) and of the view's [N][y_tot][OH][OW][16]
+        obase[p] = (n * a.KB * ohw + pix) * 16 + 4 * g;
+        ybase[p] = (n * a.y_tot * ohw + pix) * 16 + 4 * g;
     }
     unsigned woff[FK];
 #pragma unroll
@@ -111,34 +162,42 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
 #pragma unroll
         for (int p = 0; p < FP; ++p) acc[f][p] = v4i{0, 0, 0, 0};
 
-    auto load = [&](int st, v4i (&A)[FK], v4i (&B)[FP]) {
-        const int cg = st % a.CG, rs = st / a.CG;
-        const int r = rs / a.S, s = rs - r * a.S;
-        const bool cok = 4 * cg + g < a.CB;
-#pragma unroll
-        for (int p = 0; p < FP; ++p) {
-            const bool ok = cok && (unsigned)(pih[p] + r) < (unsigned)a.H && (unsigned)(piw[p] + s) < (unsigned)a.W;
-            const unsigned off = ok ? (unsigned)(pbase[p] + 4 * cg * hw16 + (r * a.W + s) * 16) : kOutOfRange;
-            B[p] = ld16(xr, off, 0);
-        }
-        const int sw_ = __builtin_amdgcn_readfirstlane(st * 1024);
-#pragma unroll
-        for (int f = 0; f < FK; ++f) A[f] = ld16(wr, woff[f], sw_);
-    };
+    // The step the next load reads, kept in scalar registers and advanced by
+    // one per load (no divisions in the loop).  It stops at the run's last
+    // step: loads past the run read that step again (never used), so every
+    // load is unconditional and the waits count outstanding loads exactly.
+    StepCursor cur;
+    cur.st = w_lo;
+    {
+        const int rs = w_lo / a.CG;
+        cur.cg = w_lo - rs * a.CG;
+        const int r = rs / a.S;
+        cur.s = rs - r * a.S;
+        cur.uoff = cur.cg * 4 * plane + (r * a.Wp + cur.s) * 16;
+    }
+    const StepGeometry geo{a.CG, a.S, w_hi, 4 * plane, 16 - (a.CG - 1) * 4 * plane,
+                           (a.Wp - a.S + 1) * 16 - (a.CG - 1) * 4 * plane};
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.x), (short)0, a.x_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t wr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.w), (short)0, a.w_bytes, kRsrcWord3);
+    const int glim = a.CB - g;  // lane group g holds a real block while 4 cg < CB - g
+#define NEO_I8_LOAD(A, B) load_step<FK, FP>(xr, wr, xbase, woff, glim, geo, cur, A, B)
 
+    // two operand sets: the loads of step q + 1 are in flight during the
+    // MFMAs of step q
     if (w_lo < w_hi) {
         v4i A0[FK], B0[FP], A1[FK], B1[FP];
-        load(w_lo, A0, B0);
+        NEO_I8_LOAD(A0, B0);
         int st = w_lo;
-        // two steps per iteration, so the two operand sets stay in registers
-        for (; st + 1 < w_hi; st += 2) {
-            load(st + 1, A1, B1);
+        for (; st + 2 <= w_hi; st += 2) {
+            NEO_I8_LOAD(A1, B1);
 #pragma unroll
             for (int f = 0; f < FK; ++f)
 #pragma unroll
                 for (int p = 0; p < FP; ++p)
                     acc[f][p] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[f], B0[p], acc[f][p], 0, 0, 0);
-            if (st + 2 < w_hi) load(st + 2, A0, B0);
+            NEO_I8_LOAD(A0, B0);
 #pragma unroll
             for (int f = 0; f < FK; ++f)
 #pragma unroll
@@ -154,6 +213,8 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         }
     }
 
+#undef NEO_I8_LOAD
+
     if constexpr (WAVES > 1) {
         __shared__ v4i red[WAVES - 1][FK * FP][64];
         if (wave > 0) {
@@ -163,65 +224,87 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
                 for (int p = 0; p < FP; ++p) red[wave - 1][f * FP + p][lane] = acc[f][p];
         }
         __syncthreads();
-        if (wave != 0) return;
+        if (wave == 0) {
+            // one partner wave at a time: all LDS reads hoisted at once would
+            // need a register tile per partner
+#pragma unroll 1
+            for (int w = 0; w < WAVES - 1; ++w)
 #pragma unroll
-        for (int w = 0; w < WAVES - 1; ++w)
+                for (int f = 0; f < FK; ++f)
 #pragma unroll
-            for (int f = 0; f < FK; ++f)
-#pragma unroll
-                for (int p = 0; p < FP; ++p) acc[f][p] += red[w][f * FP + p][lane];
+                    for (int p = 0; p < FP; ++p) acc[f][p] += red[w][f * FP + p][lane];
+        }
+        // the partners may overwrite red for the next tile once wave 0 has it
+        __syncthreads();
+        if (wave != 0) continue;
     }
 
-    const int ohw = a.OH * a.OW;
+    if constexpr (RAW) {
+#pragma unroll
+        for (int f = 0; f < FK; ++f) {
+            const int kofs = (kt * FK + f) * ohw * 16;
+#pragma unroll
+            for (int p = 0; p < FP; ++p)
+                if (pv[p]) *reinterpret_cast<v4i*>(a.acc + obase[p] + kofs) = acc[f][p];
+        }
+        continue;
+    }
+    const bool relu = a.act == NEO_ACT_RELU;
+    const int yofs = a.y_off * ohw * 16;
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kt * FK + f;
-        v4f mult = v4f{0.f, 0.f, 0.f, 0.f}, bb = v4f{0.f, 0.f, 0.f, 0.f};
-        if constexpr (!RAW) {
-            const v4f ws = *reinterpret_cast<const v4f*>(a.wscale + kb * 16 + 4 * g);
+        const v4f ws = *reinterpret_cast<const v4f*>(a.wscale + kb * 16 + 4 * g);
+        const v4f bb = a.bias ? *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g) : v4f{0.f, 0.f, 0.f, 0.f};
+        v4f mult;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) mult[v] = a.xscale * ws[v];
-            if (a.bias) bb = *reinterpret_cast<const v4f*>(a.bias + kb * 16 + 4 * g);
-        }
+        for (int v = 0; v < 4; ++v) mult[v] = a.xscale * ws[v];
+        const int kofs = kb * ohw * 16;
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
             if (!pv[p]) continue;
-            const int pix = poh[p] * a.OW + pow_[p];
-            if constexpr (RAW) {
-                *reinterpret_cast<v4i*>(a.acc + ((pn[p] * a.KB + kb) * ohw + pix) * 16 + 4 * g) = acc[f][p];
-                continue;
-            }
             v4f o;
 #pragma unroll
             for (int v = 0; v < 4; ++v) o[v] = (float)acc[f][p][v] * mult[v] + bb[v];
-            if (a.res) o += *reinterpret_cast<const v4f*>(a.res + ((pn[p] * a.KB + kb) * ohw + pix) * 16 + 4 * g);
-            if (a.act == NEO_ACT_RELU) {
+            if (a.res) o += *reinterpret_cast<const v4f*>(a.res + obase[p] + kofs);
+            if (relu) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
             }
-            *reinterpret_cast<v4f*>(a.y + ((pn[p] * a.y_tot + a.y_off + kb) * ohw + pix) * 16 + 4 * g) = o;
+            *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
         }
+    }
     }
 }
 
-// fp32 NCHW16c -> int8 NCHW16c: clamp(round_half_even(x / scale), -127, 127),
-// one pixel block (16 values) per thread.  Padding lanes (+0.0) give 0.
-__global__ __launch_bounds__(256) void quantize_kernel(const float* x, long blocks, float scale, int8_t* q) {
+// fp32 NCHW16c [N][CB][H][W][16] -> int8 NCHW16c with a zero halo
+// [N][CB][H + 2 ph][W + 2 pw][16]: clamp(round_half_even(x / scale), -127,
+// 127), one pixel block (16 values) per thread.  Padding lanes (+0.0) give 0.
+__global__ __launch_bounds__(256) void quantize_kernel(const float* x, int H, int W, int ph, int pw, long blocks,
+                                                       float scale, int8_t* q) {
     const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= blocks) return;
-    const v4f* src = reinterpret_cast<const v4f*>(x + t * 16);
+    const int Wp = W + 2 * pw, Hp = H + 2 * ph;
+    const long rowp = t / Wp;
+    const int iw = (int)(t - rowp * Wp) - pw;
+    const long plane = rowp / Hp;  // n * CB + cb
+    const int ih = (int)(rowp - plane * Hp) - ph;
     union {
         int8_t b[16];
         v4i v;
     } out;
+    out.v = v4i{0, 0, 0, 0};
+    if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W) {
+        const v4f* src = reinterpret_cast<const v4f*>(x + ((plane * H + ih) * W + iw) * 16);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const v4f v = src[i];
+        for (int i = 0; i < 4; ++i) {
+            const v4f v = src[i];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            float r = rintf(v[j] / scale);
-            r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
-            out.b[4 * i + j] = (int8_t)(int)r;
+            for (int j = 0; j < 4; ++j) {
+                float r = rintf(v[j] / scale);
+                r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
+                out.b[4 * i + j] = (int8_t)(int)r;
+            }
         }
     }
     *reinterpret_cast<v4i*>(q + t * 16) = out.v;
@@ -268,7 +351,10 @@ __global__ __launch_bounds__(256) void pack_filter_i8_kernel(const float* w, int
 
 template <int FK, int FP, int WAVES, bool RAW>
 hipError_t launch_t(const I8Args& a, hipStream_t st) {
-    const long wgs = (long)a.npx * a.nkt;
+    // one workgroup per tile up to two rounds of the chip's SIMDs, then each
+    // workgroup takes several tiles in turn
+    const long cap = 2L * 1024 / WAVES;
+    const long wgs = a.ntiles <= cap ? a.ntiles : std::max(cap, (long)(a.ntiles + 3) / 4);
     hipLaunchKernelGGL((conv_i8<FK, FP, WAVES, RAW>), dim3((unsigned)wgs), dim3(WAVES * 64), 0, st, a);
     return hipGetLastError();
 }
@@ -330,9 +416,15 @@ ConvConfig choose_int8_config(const ConvShape& s) {
     return ConvConfig{1, 1, 1, 1};
 }
 
-hipError_t launch_quantize_int8(const float* x, long blocks, float scale, int8_t* q, hipStream_t st) {
-    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)((blocks + 255) / 256)), dim3(256), 0, st, x, blocks,
-                       scale, q);
+size_t int8_act_bytes(int N, int C, int H, int W, int ph, int pw) {
+    return (size_t)N * cdiv(C, 16) * (H + 2 * ph) * (W + 2 * pw) * 16;
+}
+
+hipError_t launch_quantize_int8(const float* x, int N, int C, int H, int W, int ph, int pw, float scale,
+                                int8_t* q, hipStream_t st) {
+    const long blocks = (long)(int8_act_bytes(N, C, H, W, ph, pw) / 16);
+    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)((blocks + 255) / 256)), dim3(256), 0, st, x, H, W, ph, pw,
+                       blocks, scale, q);
     return hipGetLastError();
 }
 
@@ -359,15 +451,12 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.CG = cdiv(s.C, 64);
-    a.H = s.H;
-    a.W = s.W;
+    a.Hp = s.H + 2 * s.ph;
+    a.Wp = s.W + 2 * s.pw;
     a.KB = cdiv(s.K, 16);
-    a.R = s.R;
     a.S = s.S;
     a.sh = s.sh;
     a.sw = s.sw;
-    a.ph = s.ph;
-    a.pw = s.pw;
     a.OH = s.OH;
     a.OW = s.OW;
     a.M = s.N * s.OH * s.OW;
@@ -377,7 +466,8 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.T = s.R * s.S * a.CG;
     a.npx = cdiv(a.M, 16 * c.fp);
     a.nkt = a.KB / c.fk;
-    a.x_bytes = (int)((long)s.N * a.CB * s.H * s.W * 16);
+    a.ntiles = a.npx * a.nkt;
+    a.x_bytes = (int)int8_act_bytes(s.N, s.C, s.H, s.W, s.ph, s.pw);
     a.w_bytes = (int)int8_filter_bytes(s.K, s.C, s.R, s.S);
     a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
     a.div_ow = make_fastdiv((unsigned)s.OW);

@@ -119,16 +119,21 @@ int tune_wino(const ConvShape& s, const float* x, const float* u, const float* b
               const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
 bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 
-// Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations, a
+// Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations with
+// the convolution's zero padding stored as a halo, a
 // packed int8 filter with per-output-channel scales, int32 accumulation on
 // v_mfma_i32_16x16x64_i8.  Configuration: fk output blocks x fp pixel groups
 // per wave, `waves` waves splitting the reduction (split must be 1).
 // launch_conv_int8 writes the dequantized float32 output y (with the epilogue
 // of s: act, y_off, y_tot), or with `acc` non-null the raw int32 sums.
 size_t int8_filter_bytes(int K, int C, int R, int S);
+// Bytes of the int8 activations with their zero halo: N * ceil(C/16) *
+// (H + 2 ph) * (W + 2 pw) * 16.
+size_t int8_act_bytes(int N, int C, int H, int W, int ph, int pw);
 bool int8_config_valid(const ConvShape& s, const ConvConfig& c);
 ConvConfig choose_int8_config(const ConvShape& s);
-hipError_t launch_quantize_int8(const float* x, long blocks, float scale, int8_t* q, hipStream_t st);
+hipError_t launch_quantize_int8(const float* x, int N, int C, int H, int W, int ph, int pw, float scale,
+                                int8_t* q, hipStream_t st);
 hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, int8_t* wq, float* wscale,
                                    hipStream_t st);
 hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,

@@ -95,7 +95,7 @@ def lib():
         "neo_winograd_filter": [P, I, I, P, P],
         "neo_conv2d_winograd": [P, I, I, I, I, P, I, P, I, I, ctypes.POINTER(Epilogue), P, I, I,
                                 P],
-        "neo_quantize_int8": [P, I, I, I, I, F, P, P],
+        "neo_quantize_int8": [P, I, I, I, I, F, I, I, P, P],
         "neo_pack_filter_int8": [P, I, I, I, I, P, P, P],
         "neo_conv2d_int8": [P, I, I, I, I, P, P, I, I, I, F, P, I, I, I, I,
                             ctypes.POINTER(Epilogue), P, I, I, P],
@@ -338,18 +338,21 @@ def int8_filter_bytes(K, C, R, S):
     return cblocks(K) * cblocks(C, 64) * R * S * 1024
 
 
-def quantize_int8(x, C, x_scale, out=None, stream=None):
-    """x: fp32 NCHW16c of C channels -> int8 NCHW16c,
-    clamp(round_half_even(x / x_scale), -127, 127)."""
+def quantize_int8(x, C, x_scale, pad=0, out=None, stream=None):
+    """x: fp32 NCHW16c of C channels -> int8 NCHW16c with the zero padding
+    `pad` of the convolution that reads it stored as a halo,
+    [N][CB][H + 2 ph][W + 2 pw][16], clamp(round_half_even(x / x_scale), -127, 127)."""
     import torch
+    ph, pw = _pair(pad)
     N, XB, H, W, blk = x.shape
     if blk != BLOCK or XB != cblocks(C):
         raise ValueError(f"x shape {tuple(x.shape)} is not NCHW16c of {C} channels")
+    shape = (N, XB, H + 2 * ph, W + 2 * pw, BLOCK)
     if out is None:
-        out = torch.empty(x.shape, device=x.device, dtype=torch.int8)
-    if out.numel() < x.numel():
-        raise ValueError(f"out holds {out.numel()} bytes, the call needs {x.numel()}")
-    _check(lib().neo_quantize_int8(_dptr(x, "x"), N, C, H, W, float(x_scale),
+        out = torch.empty(shape, device=x.device, dtype=torch.int8)
+    if out.numel() < int(np.prod(shape)):
+        raise ValueError(f"out holds {out.numel()} bytes, the call needs {int(np.prod(shape))}")
+    _check(lib().neo_quantize_int8(_dptr(x, "x"), N, C, H, W, float(x_scale), ph, pw,
                                    _dptr_typed(out, torch.int8, "out"), _stream(stream)))
     return out
 
@@ -375,9 +378,13 @@ def pack_filter_int8(w, out=None, scale=None, stream=None):
 
 def _int8_args(xq, C, w_packed, K, R, S, stride, pad):
     (sh, sw), (ph, pw) = _pair(stride), _pair(pad)
-    N, XB, H, W, blk = xq.shape
+    N, XB, Hp, Wp, blk = xq.shape
     if blk != BLOCK or XB != cblocks(C):
         raise ValueError(f"xq shape {tuple(xq.shape)} is not NCHW16c of {C} channels")
+    # xq carries the convolution's padding as its halo
+    H, W = Hp - 2 * ph, Wp - 2 * pw
+    if H < 1 or W < 1:
+        raise ValueError(f"xq shape {tuple(xq.shape)} is smaller than its halo of {(ph, pw)}")
     if w_packed.numel() < int8_filter_bytes(K, C, R, S):
         raise ValueError(f"w_packed holds {w_packed.numel()} bytes, the call needs "
                          f"{int8_filter_bytes(K, C, R, S)}")
@@ -392,7 +399,8 @@ def _int8_ptrs(xq, w_packed):
 def conv2d_int8(xq, C, w_packed, w_scale, K, R, S, x_scale, bias=None, stride=1, pad=0,
                 act="none", residual=None, out=None, y_cblk_offset=0, y_cblk_total=None,
                 stream=None):
-    """Integer convolution: xq int8 NCHW16c (quantize_int8), w_packed and
+    """Integer convolution: xq int8 NCHW16c with the halo `pad`
+    (quantize_int8 with the same pad), w_packed and
     w_scale from pack_filter_int8; fp32 NCHW16c output
     act(acc * x_scale * w_scale[k] + bias + residual), the view as conv2d_blocked."""
     import torch

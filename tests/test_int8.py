@@ -37,10 +37,11 @@ def test_argument_errors():
     assert _conv(C=14778) == -4 and "133,000" in neo.last_error()
     assert L.neo_conv2d_int8_acc(FAKE, 1, 16, 8, 8, FAKE, 16, 3, 3, 1, 1, 1, 1, None, None) == -1
     assert L.neo_conv2d_int8_acc(FAKE, 1, 16, 8, 8, FAKE, 16, 3, 3, 1, 1, 1, 1, MIS, None) == -3
-    assert L.neo_quantize_int8(None, 1, 16, 8, 8, 1.0, FAKE, None) == -1
-    assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 0.0, FAKE, None) == -1
-    assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 1.0, MIS, None) == -3
-    assert L.neo_quantize_int8(FAKE, 0, 16, 8, 8, 1.0, FAKE, None) == -1
+    assert L.neo_quantize_int8(None, 1, 16, 8, 8, 1.0, 1, 1, FAKE, None) == -1
+    assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 0.0, 1, 1, FAKE, None) == -1
+    assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 1.0, 1, 1, MIS, None) == -3
+    assert L.neo_quantize_int8(FAKE, 0, 16, 8, 8, 1.0, 1, 1, FAKE, None) == -1
+    assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 1.0, -1, 1, FAKE, None) == -1
     assert L.neo_pack_filter_int8(None, 16, 16, 3, 3, FAKE, FAKE, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 16, 16, 3, 3, FAKE, None, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 0, 16, 3, 3, FAKE, FAKE, None) == -1
@@ -55,13 +56,16 @@ def test_packed_filter_size():
 
 def test_binding_refuses_short_buffers():
     import torch
-    xq = torch.zeros((1, 1, 8, 8, 16), dtype=torch.int8)
+    xq = torch.zeros((1, 1, 10, 10, 16), dtype=torch.int8)     # 8 x 8 with a halo of 1
     wq = torch.zeros(neo.int8_filter_bytes(32, 16, 3, 3), dtype=torch.int8)
     with pytest.raises(ValueError, match="w_packed holds"):
         neo.conv2d_int8(xq, 16, wq[:-1], torch.ones(32), 32, 3, 3, 0.1, pad=1)
     with pytest.raises(ValueError, match="NCHW16c"):
         neo.conv2d_int8(torch.zeros((1, 2, 8, 8, 16), dtype=torch.int8), 16, wq, torch.ones(32),
                         32, 3, 3, 0.1)
+    with pytest.raises(ValueError, match="halo"):
+        neo.conv2d_int8(torch.zeros((1, 1, 2, 2, 16), dtype=torch.int8), 16, wq, torch.ones(32),
+                        32, 3, 3, 0.1, pad=1)
     with pytest.raises(ValueError, match="out"):
         neo.conv2d_int8(xq, 16, wq, torch.ones(32), 32, 3, 3, 0.1, pad=1,
                         out=torch.zeros(2 * 8 * 8 * 16 - 1))
@@ -76,6 +80,9 @@ def test_binding_refuses_short_buffers():
                              out=torch.zeros(100, dtype=torch.int8))
     with pytest.raises(ValueError, match="NCHW16c"):
         neo.quantize_int8(torch.zeros((1, 1, 8, 8, 16)), 17, 0.1)
+    with pytest.raises(ValueError, match="out holds"):
+        neo.quantize_int8(torch.zeros((1, 1, 8, 8, 16)), 16, 0.1, pad=1,
+                          out=torch.zeros((1, 1, 8, 8, 16), dtype=torch.int8))
 
 
 # ---- GPU -------------------------------------------------------------------------------------
@@ -115,7 +122,7 @@ def run_int8(gpu, c, xs, raw=False, bias=True, out=None, y_off=0, y_tot=None):
     """One LayerCase (no batch norm) through the device chain: layout
     transform, activation quantization, filter packing, convolution."""
     from gpu_util import dev
-    xq = gpu.quantize_int8(gpu.to_blocked(dev(c.x)), c.C, xs)
+    xq = gpu.quantize_int8(gpu.to_blocked(dev(c.x)), c.C, xs, pad=c.pad)
     wq, ws = gpu.pack_filter_int8(dev(c.w))
     if raw:
         return gpu.conv2d_int8_acc(xq, c.C, wq, c.K, c.R, c.S, stride=c.stride, pad=c.pad)
@@ -165,17 +172,21 @@ def assert_acc_equal(acc_b, want, K, what=""):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("C", [1, 16, 37])
-def test_quantize_bit_exact(gpu, C):
+@pytest.mark.parametrize("C,pad", [(1, (0, 0)), (16, (1, 1)), (37, (2, 1)), (64, (3, 0))])
+def test_quantize_bit_exact(gpu, C, pad):
     """Round half to even on exact ties, clamping, and random values: the
-    device's int8 NCHW16c equals the oracle's quantization, padding lanes 0."""
+    device's int8 NCHW16c equals the oracle's quantization inside the halo,
+    padding lanes and the halo 0."""
     from gpu_util import dev, host
     rng = np.random.default_rng([C, 8])
     s = np.float32(0.25)
     x = rng.normal(0, 12, (2, C, 5, 7)).astype(np.float32)
     x.flat[::3] = s * (rng.integers(-140, 140, x.size)[::3] + 0.5)   # exact ties, some clamped
-    q = host(gpu.quantize_int8(gpu.to_blocked(dev(x)), C, s))
-    np.testing.assert_array_equal(q, orc.to_blocked(oq.quantize(x, s)))
+    q = host(gpu.quantize_int8(gpu.to_blocked(dev(x)), C, s, pad=pad))
+    ph, pw = pad
+    want = np.zeros((2, C, 5 + 2 * ph, 7 + 2 * pw), np.int8)
+    want[:, :, ph:ph + 5, pw:pw + 7] = oq.quantize(x, s)
+    np.testing.assert_array_equal(q, orc.to_blocked(want))
 
 
 @pytest.mark.gpu
@@ -312,3 +323,19 @@ def test_resnet50_layers_batch32_sampled(gpu, lid):
     acc, want, mag = oracle_int8(c, xs, images=[0, 31])
     assert_acc_equal(acc_b, acc, c.K, lid)
     assert_dequant_close(orc.from_blocked(y_b, c.K), want, mag, lid)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("cfg,N", [("1,1,4", 6), ("1,1,2", 12)])
+def test_workgroups_taking_several_tiles(gpu, cfg, N, monkeypatch):
+    """A grid above two rounds of the chip's SIMDs: the workgroups take
+    several output tiles in turn (600 tiles for 512 workgroups of 4 waves,
+    1200 for 1024 of 2), accumulators and output against the oracle."""
+    from gpu_util import host
+    monkeypatch.setenv("NEO_I8_CONFIG", cfg)
+    c = wl.conv_case(64, 16, 3, 3, 1, 1, 40, 40, N=N, epilogue="res", with_bn=False,
+                     out_hw=(40, 40))
+    xs = act_scale(c.x)
+    acc, want, mag = oracle_int8(c, xs)
+    assert_acc_equal(host(run_int8(gpu, c, xs, raw=True)), acc, 16, cfg)
+    assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 16), want, mag, cfg)
