@@ -413,6 +413,89 @@ def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False, selec
     return out_rows
 
 
+PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 matrix peak (5.0 POP/s)
+
+
+def int8_layer(neo, torch, wl, i, N):
+    """ResNet-50 conv shape i at batch N set up for the integer path: seeded
+    float32 input in NCHW16c, its quantization (with the conv's halo), the
+    packed int8 filter and scales, zero bias, a residual where the layer has
+    one.  Returns the shape's figures and the conv and quantize launches."""
+    lid, C, K, R, st, pd, H, epi, uses = wl.RESNET50_LAYERS[i]
+    rng = np.random.default_rng([11, i])
+    OH = (H + 2 * pd - R) // st + 1
+    KB = -(-K // 16)
+    x = torch.from_numpy(rng.uniform(-1, 1, (N, C, H, H)).astype(np.float32)).cuda()
+    w = torch.from_numpy(rng.normal(0, np.sqrt(2 / (C * R * R)), (K, C, R, R)).astype(np.float32)).cuda()
+    xb = neo.to_blocked(x)
+    del x
+    xs = float(xb.abs().max().item() / 127)
+    xq = neo.quantize_int8(xb, C, xs, pad=pd)
+    wq, ws = neo.pack_filter_int8(w)
+    bias = torch.zeros(KB * 16, device="cuda")
+    res = torch.zeros((N, KB, OH, OH, 16), device="cuda") if epi == "res" else None
+    out = torch.empty((N, KB, OH, OH, 16), device="cuda")
+    act = "relu" if epi in ("relu", "res") else "none"
+
+    def conv():
+        neo.conv2d_int8(xq, C, wq, ws, K, R, R, xs, bias=bias, stride=st, pad=pd, act=act,
+                        residual=res, out=out)
+
+    def quant():
+        neo.quantize_int8(xb, C, xs, pad=pd, out=xq)
+    ops = 2 * N * K * C * R * R * OH * OH
+    nbytes = N * C * H * H + K * C * R * R + 4 * N * K * OH * OH * (2 if res is not None else 1) + 8 * K
+    label = f"{C}->{K} {R}x{R}/s{st} {H}->{OH}" + (" +res" if res is not None else "")
+    return dict(id=lid, shape=label, uses=uses, ops=ops, bytes=nbytes, conv=conv, quant=quant)
+
+
+def int8_layer_table(neo, torch, wl, N=32, reps=10, fp32_us=None):
+    """The 23 distinct ResNet-50 conv shapes at batch N through the integer
+    path (quantized activations with their halo, packed int8 filter, int32
+    MFMA accumulation, float32 epilogue with the layer's residual and ReLU),
+    each timed alone like layer_table (warm, back-to-back graph replays),
+    beside the activation quantization pass the layer needs and, from
+    fp32_us ({shape label: us} of the tuned fp32 plan), the fp32 conv of the
+    same shape.  Ops are the direct convolution's; bytes are algorithmic:
+    int8 input and filter, float32 output and residual."""
+    rows = []
+    for i in range(len(wl.RESNET50_LAYERS)):
+        L = int8_layer(neo, torch, wl, i, N)
+        us = time_graph(torch, L["conv"], reps)
+        q_us = time_graph(torch, L["quant"], reps)
+        ops, nbytes = L["ops"], L["bytes"]
+        ai = ops / nbytes
+        roof = min(PEAK_INT8_TOPS, ai * PEAK_HBM_GBS / 1e3)
+        tops = ops / (us * 1e-6) / 1e12
+        f32 = (fp32_us or {}).get(L["shape"])
+        rows.append(dict(id=L["id"], shape=L["shape"], uses=L["uses"],
+                         us=round(us, 2), quant_us=round(q_us, 2), tops=round(tops, 1),
+                         pct_int8_mfma=round(100 * tops / PEAK_INT8_TOPS, 1),
+                         alg_gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
+                         bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_INT8_TOPS else "hbm",
+                         pct_roof=round(100 * tops / roof, 1),
+                         fp32_us=f32, speedup_vs_fp32=round(f32 / us, 2) if f32 else None,
+                         _ops=ops))
+        del L
+    t = sum(r["us"] * r["uses"] for r in rows)
+    tq = sum((r["us"] + r["quant_us"]) * r["uses"] for r in rows)
+    ops = sum(r.pop("_ops") * r["uses"] for r in rows)
+    summary = dict(batch=N, convs=sum(r["uses"] for r in rows), sum_us=round(t, 1),
+                   sum_with_quant_us=round(tq, 1), tops=round(ops / (t * 1e-6) / 1e12, 1),
+                   pct_int8_mfma=round(100 * ops / (t * 1e-6) / 1e12 / PEAK_INT8_TOPS, 2))
+    m = [r for r in rows if r["fp32_us"]]
+    if m:
+        # over the shapes the fp32 plan launches alone (the stem runs fused
+        # with its max pool there)
+        t32 = sum(r["fp32_us"] * r["uses"] for r in m)
+        t8 = sum(r["us"] * r["uses"] for r in m)
+        t8q = sum((r["us"] + r["quant_us"]) * r["uses"] for r in m)
+        summary.update(fp32_matched_convs=sum(r["uses"] for r in m), fp32_sum_us=round(t32, 1),
+                       int8_matched_sum_us=round(t8, 1), speedup_vs_fp32=round(t32 / t8, 2),
+                       speedup_with_quant=round(t32 / t8q, 2))
+    return rows, summary
+
+
 def scheme_summary(d):
     """Histogram of the convs' (ic_bn, oc_bn) in a plan description."""
     h = {}
@@ -577,6 +660,8 @@ def main():
     ap.add_argument("--no-models", action="store_true", help="skip the other models and ablation")
     ap.add_argument("--tune-db", help="load this local-search results file before planning")
     ap.add_argument("--save-tune-db", help="write the local-search results here at the end")
+    ap.add_argument("--int8-only", action="store_true",
+                    help="only the batch-32 integer conv table (no fp32 comparison); one JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the batch-1 path has no cross-GPU work "
@@ -588,6 +673,10 @@ def main():
     from paper_1809_02697_amd import workloads as wl
     neo.lib()
     assert torch.cuda.is_available(), "no GPU"
+    if args.int8_only:
+        rows, summary = int8_layer_table(neo, torch, wl, 32, args.layer_reps, None)
+        print(json.dumps({"layers_b32_int8": rows, "int8_b32": summary}))
+        return
 
     if args.tune_db:
         neo.tune_db_load(args.tune_db)
@@ -641,7 +730,7 @@ def main():
 
     models = None if args.no_models else model_latencies(neo, torch, wl, 20)
 
-    layers_b32 = layers_b32_winograd = None
+    layers_b32 = layers_b32_winograd = layers_b32_int8 = int8_b32 = None
     if not args.no_layers and not args.no_models:
         # the same kernels with the per-launch floor amortized over 32 images
         g32 = wl.resnet50(32)
@@ -649,6 +738,7 @@ def main():
         x32 = torch.from_numpy(g32.x).cuda()
         o32 = p32.run(x32)
         layers_b32 = layer_table(torch, p32, x32, o32, 10, cold_hbm_only=True)
+        fp32_b32 = {r["shape"]: r["us"] for r in layers_b32 if "+ maxpool" not in r["shape"]}
         tf32 = sum(r["flops"] * r["uses"] for r in layers_b32) / \
             sum(r["us"] * 1e-6 * r["uses"] for r in layers_b32) / 1e12
         for r in layers_b32:
@@ -661,7 +751,11 @@ def main():
         for r in layers_b32_winograd:
             del r["flops"], r["bytes"]
         p32w.destroy()
-        del g32, x32
+        del g32, x32, o32
+        torch.cuda.empty_cache()
+        # the same shapes through the integer path
+        layers_b32_int8, int8_b32 = int8_layer_table(neo, torch, wl, 32, 10, fp32_b32)
+        print(f"[bench] batch-32 int8 conv layers: {int8_b32}", file=sys.stderr, flush=True)
         print(f"[bench] batch-32 conv layers: {tf32:.2f} TFLOP/s", file=sys.stderr, flush=True)
     copy_gbs = None if args.no_layers else cold_copy_gbs(torch)
 
@@ -701,6 +795,8 @@ def main():
         "layers": layers,
         "layers_b32": layers_b32,
         "layers_b32_winograd": layers_b32_winograd,
+        "layers_b32_int8": layers_b32_int8,
+        "int8_b32": int8_b32,
         "cold_copy_gbs": copy_gbs,
         "models": models,
     }

@@ -5,6 +5,7 @@
     rocprofv3 --pmc WRITE_SIZE ...                       (the same workload)
     rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 ... (the same workload)
     ... profile_layers TUNE_DB --batch 32 --winograd [--reps 20]   (Winograd plan)
+    ... profile_layers --int8 --batch 32 [--reps 20]    (the integer convs, no plan)
 
 Builds the plan bench.py times (batch 1: the headline plan; batch 32: the
 tuned one-block plan of the batch-32 layer table).  TUNE_DB is a local-search
@@ -43,6 +44,28 @@ def build_plan(neo, torch, wl, db, batch, winograd=False):
     return plan, g
 
 
+def int8_main(neo, torch, wl, batch, reps):
+    """The integer conv of every ResNet-50 shape (set up by bench.int8_layer:
+    quantized input with its halo, packed filter), then the calibration copy,
+    then the 23 convs in layer order, `reps` times: the conv_i8 dispatches
+    after the copy are those rounds."""
+    from bench import int8_layer
+    layers = [int8_layer(neo, torch, wl, i, batch) for i in range(len(wl.RESNET50_LAYERS))]
+    for L in layers:
+        L["conv"]()
+    torch.cuda.synchronize()
+    a = torch.ones(COPY_MB * 2 ** 18, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        for L in layers:
+            L["conv"]()
+    torch.cuda.synchronize()
+    print(f"profiled {len(layers)} int8 convs x {reps} after a {COPY_MB} MB copy (batch {batch})",
+          file=sys.stderr)
+
+
 def main():
     import torch
 
@@ -58,7 +81,12 @@ def main():
                     help="the plan with NEO_PLAN_WINOGRAD (3x3 stride-1 convs by Winograd where faster)")
     ap.add_argument("--reps", type=int, default=1,
                     help="run the step list this many times (for kernel-trace durations)")
+    ap.add_argument("--int8", action="store_true",
+                    help="instead of a plan: the 23 ResNet-50 conv shapes through the integer "
+                         "path (bench.py's int8 layer table), after the copy, --reps times")
     args = ap.parse_args()
+    if args.int8:
+        return int8_main(neo, torch, wl, args.batch, args.reps)
     plan, g = build_plan(neo, torch, wl, args.db, args.batch, args.winograd)
     if args.describe:
         with open(args.describe, "w") as f:

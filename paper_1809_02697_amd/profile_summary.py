@@ -18,6 +18,8 @@ Writes
   profiles/conv2d_blocked_resnet50_b32_mfma.md  MFMA utilisation at batch 32
   profiles/wino_f2x3_resnet50_b32.md  the Winograd kernel's launches in the
       batch-32 plan with NEO_PLAN_WINOGRAD: durations and MFMA utilisation
+  profiles/conv_i8_resnet50_b32.md  the integer conv of each ResNet-50 shape at
+      batch 32 (INT8_COMMANDS): durations, traffic, MFMA utilisation
   profiles/conv2d_blocked_resnet50_b1_traffic.json  bytes per launch, tied to
       the hash of the kernel source it was measured with (bench.py reports it
       only while the source is unchanged)
@@ -79,6 +81,19 @@ COMMANDS = [
     "python -m paper_1809_02697_amd.profile_layers RUN_DIR/tune_db.txt --batch 32 --winograd --reps 20",
     "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
 ]
+# the integer convs (no plan, no results file), summarized by write_int8
+INT8_COMMANDS = [
+    "rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_i8 -o i8 -- "
+    "python -m paper_1809_02697_amd.profile_layers --int8 --batch 32 --reps 20",
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d RUN_DIR/pmc -o i8fetch -- "
+    "python -m paper_1809_02697_amd.profile_layers --int8 --batch 32",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d RUN_DIR/pmc -o i8write -- "
+    "python -m paper_1809_02697_amd.profile_layers --int8 --batch 32",
+    "rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_I8 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE "
+    "--output-format csv -d RUN_DIR/pmc -o i8mfma -- "
+    "python -m paper_1809_02697_amd.profile_layers --int8 --batch 32",
+    "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
+]
 
 
 def kernel_hash():
@@ -92,6 +107,10 @@ def kernel_hash():
 def _rows(path):
     with open(path) as f:
         return list(csv.DictReader(f))
+
+
+def is_conv_i8(name):
+    return "conv_i8" in name
 
 
 def is_conv(name):
@@ -403,7 +422,78 @@ def write_winograd(run_dir, pmc_path, trace_path):
         f.write("\n".join(md) + "\n")
 
 
+def write_int8(run_dir):
+    """profiles/conv_i8_resnet50_b32.md: the integer conv of each ResNet-50
+    shape at batch 32 -- kernel-trace durations, HBM traffic against the
+    algorithmic bytes, MFMA utilisation."""
+    sys.path.insert(0, ROOT)
+    from paper_1809_02697_amd import workloads as wl
+    from paper_1809_02697_amd.profile_layers import COPY_MB
+    copy_bytes = COPY_MB * 2 ** 20
+    layers = wl.RESNET50_LAYERS
+    n = len(layers)
+    # durations: the conv_i8 dispatches after the last copy, n per round
+    rows = sorted(_rows(os.path.join(run_dir, "prof_i8", "i8_kernel_trace.csv")),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    last_copy = max(i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"])
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            for r in rows[last_copy + 1:] if is_conv_i8(r["Kernel_Name"])]
+    reps = len(durs) // n
+    assert reps >= 2 and len(durs) == reps * n, (len(durs), n)
+    per = [_median([durs[r * n + j] for r in range(1, reps)]) for j in range(n)]
+    pmc = os.path.join(run_dir, "pmc")
+
+    def after_copy(tag, counter=None):
+        copy, fwd = forward_dispatches(os.path.join(pmc, f"{tag}_counter_collection.csv"), counter)
+        vals = [v for name, v in fwd if is_conv_i8(name)]
+        assert len(vals) == n, (tag, len(vals))
+        return copy, vals
+    f_copy, fetch = after_copy("i8fetch")
+    w_copy, write = after_copy("i8write")
+    ff, fw = copy_bytes / (f_copy * 1024.0), copy_bytes / (w_copy * 1024.0)
+    _, mops = after_copy("i8mfma", "SQ_INSTS_VALU_MFMA_MOPS_I8")
+    _, busy = after_copy("i8mfma", "SQ_VALU_MFMA_BUSY_CYCLES")
+    _, gui = after_copy("i8mfma", "GRBM_GUI_ACTIVE")
+    N = 32
+    md = ["# conv_i8 (INT8 convolution, v_mfma_i32_16x16x64_i8), ResNet-50 shapes at batch 32", "",
+          "Commands (from the repository root on one MI355X; RUN_DIR = the directory they write to):",
+          "", "```"] + INT8_COMMANDS + ["```", "",
+          "Each of the 23 distinct ResNet-50 conv shapes at batch 32 through the integer path "
+          "(int8 input with its halo, packed int8 filter, float32 output with the layer's residual "
+          "and ReLU), in the launch configuration the library chooses.  Duration: median over the "
+          "profiled rounds (the first dropped) of the kernel-trace timestamps.  Traffic: FETCH_SIZE "
+          "and WRITE_SIZE (KiB per dispatch) scaled by the same counters on a plain copy of "
+          f"{COPY_MB} MB (factors {ff:.3f} and {fw:.3f}), warm caches, against the algorithmic "
+          "bytes (int8 input and filter once, float32 output and residual).  MFMA utilisation: "
+          "SQ_VALU_MFMA_BUSY_CYCLES over (GRBM_GUI_ACTIVE x 1024 SIMDs / 8 XCDs); executed MFMA "
+          "work is SQ_INSTS_VALU_MFMA_MOPS_I8 x 512 over the direct convolution's 2 N K C R S OH OW "
+          "(above 1 where padded channels are multiplied).", "",
+          "| layer | shape | us | TOPS | % of 5.0 POP/s | traffic MB | algorithmic MB | "
+          "traffic / alg | MFMA util % | MFMA work / alg ops |",
+          "|---|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    tot_t = tot_ops = 0.0
+    for j, (lid, C, K, R, st, pd, H, epi, uses) in enumerate(layers):
+        OH = (H + 2 * pd - R) // st + 1
+        ops = 2 * N * K * C * R * R * OH * OH
+        alg = N * C * H * H + K * C * R * R + 4 * N * K * OH * OH * (2 if epi == "res" else 1) + 8 * K
+        traffic = fetch[j] * 1024 * ff + write[j] * 1024 * fw
+        util = 100 * busy[j] / (gui[j] / 8 * SIMDS) if gui[j] else 0.0
+        tops = ops / (per[j] * 1e-6) / 1e12
+        tot_t += per[j] * uses
+        tot_ops += ops * uses
+        md.append(f"| {lid} | {C}->{K} {R}x{R}/s{st} {H}->{OH}{' +res' if epi == 'res' else ''} | "
+                  f"{per[j]:.2f} | {tops:.0f} | {100 * tops / 5000:.1f} | {traffic / 1e6:.2f} | "
+                  f"{alg / 1e6:.2f} | {traffic / alg:.2f} | {util:.1f} | {mops[j] * 512 / ops:.3f} |")
+    md += ["", f"Whole network (each shape times its uses, 53 convs): {tot_t:.1f} us of conv_i8, "
+               f"{tot_ops / (tot_t * 1e-6) / 1e12:.0f} TOPS."]
+    with open(os.path.join(PROFILES, "conv_i8_resnet50_b32.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+
+
 if __name__ == "__main__":
     if len(sys.argv) != 2:
         sys.exit("usage: python -m paper_1809_02697_amd.profile_summary RUN_DIR")
-    main(sys.argv[1])
+    if os.path.exists(os.path.join(sys.argv[1], "prof_i8", "i8_kernel_trace.csv")):
+        write_int8(sys.argv[1])
+    if os.path.exists(os.path.join(sys.argv[1], "bench.log")):
+        main(sys.argv[1])
