@@ -11,7 +11,14 @@ scheme, so this module fixes one, the usual symmetric linear quantization:
   (|sum| <= 127^2 * C * R * S, below 2^31 for every layer here);
 * the output is dequantized with the per-channel multiplier m[k] = s_x * s_w[k]
   (a float32 product, the value the library receives):
-  y = act(acc * m[k] + bias[k] + residual), in float64, rounded once.
+  y = act(acc * m[k] + bias[k] + residual), in float64, rounded once
+  (``dequantize``, the ideal value); ``epilogue_f32`` is the same expression
+  evaluated the way the library's interface fixes it, each operation rounded
+  to float32 in that order, no fused multiply-add;
+* an int8 output (the next layer's input) requantizes that float32 value with
+  the next layer's scale s_y: q = clamp(round_half_even(y * r), -127, 127),
+  r = 1 / s_y rounded to float32 and the product in float32 (one multiply per
+  value; it can differ from x / s_y by one step at an exact tie).
 
 Only ``tests/`` use this module.  It shares no code with the HIP library.
 """
@@ -81,3 +88,25 @@ def dequantize(acc, mult, bias=None, residual=None, act="none"):
     if act == "relu":
         y = np.maximum(y, 0.0)
     return y.astype(np.float32)
+
+
+def epilogue_f32(acc, mult, bias=None, residual=None, act="none"):
+    """act(((float32(acc) * m[k]) + bias[k]) + residual), every operation
+    rounded to float32 in this order (the int32 -> float32 conversion to
+    nearest, ties to even); ReLU maps every value not above 0 to +0."""
+    y = np.asarray(acc).astype(np.float32) * np.asarray(mult, np.float32)[None, :, None, None]
+    if bias is not None:
+        y = y + np.asarray(bias, np.float32)[None, :, None, None]
+    if residual is not None:
+        y = y + np.asarray(residual, np.float32)
+    if act == "relu":
+        y = np.where(y > 0, y, np.float32(0)).astype(np.float32)
+    return y.astype(np.float32)
+
+
+def requantize(y, scale):
+    """float32 -> int8 by the float32 reciprocal of the scale:
+    clamp(round_half_even(y * float32(1 / scale)), -127, 127)."""
+    r = np.float32(1) / np.float32(scale)
+    q = np.rint(np.asarray(y, np.float32) * r)
+    return np.clip(q, -QMAX, QMAX).astype(np.int8)

@@ -94,3 +94,43 @@ def test_dequantize_by_hand():
     np.testing.assert_array_equal(oq.dequantize(acc, mult, bias, res, "relu").ravel(), [0.0, 0.0])
     np.testing.assert_array_equal(oq.dequantize(acc, mult, bias, res).ravel(), [-6.5, -1.5])
     np.testing.assert_array_equal(oq.dequantize(acc, mult).ravel(), [12.5, -3.0])
+
+
+def test_epilogue_rounds_each_operation_to_float32():
+    # 2^24 + 1 converts to 2^24; adding 1 then ties back to 2^24 (even).  In
+    # float64 (or with the sum formed before rounding) the result would be
+    # 2^24 + 2, which float32 holds exactly.
+    acc = np.array([[[[2 ** 24 + 1]]]], np.int64)
+    one = np.float32([1.0])
+    assert oq.epilogue_f32(acc, one, one).item() == 2.0 ** 24
+    assert oq.dequantize(acc, one, one).item() == 2.0 ** 24 + 2
+    # hand values: (100 * 0.125 + 1) - 20 = -6.5 -> ReLU +0; (-3 * 1 + 0.5) + 1 = -1.5
+    acc = np.array([[[[100]], [[-3]]]], np.int64)
+    mult = oq.multipliers(0.5, np.float32([0.25, 2.0]))
+    bias = np.float32([1.0, 0.5])
+    res = np.array([[[[-20.0]], [[1.0]]]], np.float32)
+    np.testing.assert_array_equal(oq.epilogue_f32(acc, mult, bias, res).ravel(), [-6.5, -1.5])
+    y = oq.epilogue_f32(acc, mult, bias, res, "relu").ravel()
+    assert (y == 0).all() and not np.signbit(y).any()
+    # on random sums it stays within 6 u of the ideal value
+    rng = np.random.default_rng(5)
+    acc = rng.integers(-2 ** 26, 2 ** 26, (2, 3, 4, 5))
+    mult = rng.uniform(1e-5, 1e-3, 3).astype(np.float32)
+    b = rng.normal(0, 1, 3).astype(np.float32)
+    r = rng.normal(0, 1, acc.shape).astype(np.float32)
+    y32 = oq.epilogue_f32(acc, mult, b, r).astype(np.float64)
+    y64 = oq.dequantize(acc, mult, b, r).astype(np.float64)
+    mag = np.abs(acc * mult.astype(np.float64)[None, :, None, None]) + \
+        np.abs(b.astype(np.float64))[None, :, None, None] + np.abs(r)
+    assert (np.abs(y32 - y64) <= 6 * 2.0 ** -24 * mag).all()
+
+
+def test_requantize_multiplies_by_the_float32_reciprocal():
+    s = np.float32(0.25)                       # reciprocal 4, exact
+    y = np.float32([0.125, 0.375, -0.375, 1.0, 40.0, -40.0])
+    np.testing.assert_array_equal(oq.requantize(y, s), [0, 2, -2, 4, 127, -127])
+    # 45.5 / 7 is an exact tie (6.5 -> 6), but 45.5 * float32(1/7) rounds to
+    # just above 6.5 in float32 (-> 7)
+    assert oq.quantize(np.float32([45.5]), 7.0)[0] == 6
+    assert oq.requantize(np.float32([45.5]), 7.0)[0] == 7
+
