@@ -229,6 +229,16 @@ int neo_conv2d_winograd(const float* x, int N, int C, int H, int W, const float*
  *   neo_conv2d_blocked (float32 NCHW16c).
  * neo_conv2d_int8_acc: the same convolution, writing the raw int32 sums to acc
  *   device [N][ceil(K/16)][OH][OW][16] (padding channels 0): the exact part.
+ * neo_conv2d_int8_q: the same float32 value requantized for the next layer,
+ *   q = clamp(round_half_even(y * r), -127, 127) with r = 1 / y_scale rounded
+ *   to float32 and the product in float32, into yq: device int8 NCHW16c with a
+ *   halo, blocks [y_cblk_offset, y_cblk_offset + ceil(K/16)) of
+ *   [N][y_cblk_total][OH + 2 y_pad_h][OW + 2 y_pad_w][16] (the next conv's
+ *   input, y_pad its padding).  The halo is never written: the caller zeroes
+ *   yq once.
+ * The float32 output is evaluated with one rounding per operation in this
+ *   order: float32(acc) * m[k] (m[k] = x_scale * w_scale[k] in float32),
+ *   + bias[k], + residual, then the activation (no fused multiply-add).
  * Dilation and groups are 1.  Errors as for neo_conv2d_blocked.
  */
 int neo_quantize_int8(const float* x, int N, int C, int H, int W, float x_scale, int pad_h,
@@ -239,6 +249,11 @@ int neo_conv2d_int8(const int8_t* xq, int N, int C, int H, int W, const int8_t* 
                     const float* w_scale, int K, int R, int S, float x_scale, const float* bias,
                     int stride_h, int stride_w, int pad_h, int pad_w, const neo_epilogue* ep,
                     float* y, int y_cblk_offset, int y_cblk_total, neo_stream_t stream);
+int neo_conv2d_int8_q(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed,
+                      const float* w_scale, int K, int R, int S, float x_scale, const float* bias,
+                      int stride_h, int stride_w, int pad_h, int pad_w, const neo_epilogue* ep,
+                      float y_scale, int y_pad_h, int y_pad_w, int8_t* yq, int y_cblk_offset,
+                      int y_cblk_total, neo_stream_t stream);
 int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed, int K,
                         int R, int S, int stride_h, int stride_w, int pad_h, int pad_w, int32_t* acc,
                         neo_stream_t stream);

@@ -306,9 +306,10 @@ int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int 
                      const int8_t* w_packed, const float* w_scale, int K, int R, int S,
                      float x_scale, const float* bias, int stride_h, int stride_w, int pad_h,
                      int pad_w, const neo_epilogue* ep, float* y, int y_cblk_offset,
-                     int y_cblk_total, int* acc, neo_stream_t stream) {
+                     int y_cblk_total, int* acc, int8_t* yq, float y_scale, int y_pad_h,
+                     int y_pad_w, neo_stream_t stream) {
     const std::string f(fn);
-    float* out = acc ? reinterpret_cast<float*>(acc) : y;
+    float* out = acc ? reinterpret_cast<float*>(acc) : yq ? reinterpret_cast<float*>(yq) : y;
     ConvShape s;
     ConvConfig cfg;
     const float* res = nullptr;
@@ -325,6 +326,14 @@ int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int 
         if (!(x_scale > 0.f) || !std::isfinite(x_scale))
             return fail(NEO_ERR_INVALID_ARG, f + ": x_scale must be finite and > 0");
     }
+    if (yq) {
+        if (!(y_scale > 0.f) || !std::isfinite(y_scale) || !std::isfinite(1.0f / y_scale))
+            return fail(NEO_ERR_INVALID_ARG, f + ": y_scale must be finite, > 0 and have a "
+                                                 "finite reciprocal");
+        if (y_pad_h < 0 || y_pad_w < 0) return fail(NEO_ERR_INVALID_ARG, f + ": negative y pad");
+        if ((long)N * y_cblk_total * (s.OH + 2L * y_pad_h) * (s.OW + 2L * y_pad_w) * 16 > kMaxElems)
+            return fail(NEO_ERR_UNSUPPORTED, f + ": padded int8 output of 2 GiB or more");
+    }
     if ((long)C * R * S > kMaxI8Reduction)
         return fail(NEO_ERR_UNSUPPORTED, f + ": C * R * S above 133,000 could overflow the "
                                              "int32 accumulator");
@@ -336,8 +345,8 @@ int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int 
         return fail(NEO_ERR_UNSUPPORTED, f + ": padded int8 input of 2 GiB or more");
     cfg = choose_int8_config(s);
     env_i8_config(s, &cfg);
-    hipError_t e = launch_conv_int8(s, cfg, xq, w_packed, w_scale, x_scale, bias, res, y, acc,
-                                    (hipStream_t)stream);
+    hipError_t e = launch_conv_int8(s, cfg, xq, w_packed, w_scale, x_scale, bias, res, y, acc, yq,
+                                    y_scale, y_pad_h, y_pad_w, (hipStream_t)stream);
     return e == hipSuccess ? NEO_OK : hip_fail(e, (f + " launch").c_str());
 }
 
@@ -475,7 +484,19 @@ int neo_conv2d_int8(const int8_t* xq, int N, int C, int H, int W, const int8_t* 
                     float* y, int y_cblk_offset, int y_cblk_total, neo_stream_t stream) {
     return conv_int8_common("neo_conv2d_int8", xq, N, C, H, W, w_packed, w_scale, K, R, S, x_scale,
                             bias, stride_h, stride_w, pad_h, pad_w, ep, y, y_cblk_offset,
-                            y_cblk_total, nullptr, stream);
+                            y_cblk_total, nullptr, nullptr, 0.f, 0, 0, stream);
+}
+
+int neo_conv2d_int8_q(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed,
+                      const float* w_scale, int K, int R, int S, float x_scale, const float* bias,
+                      int stride_h, int stride_w, int pad_h, int pad_w, const neo_epilogue* ep,
+                      float y_scale, int y_pad_h, int y_pad_w, int8_t* yq, int y_cblk_offset,
+                      int y_cblk_total, neo_stream_t stream) {
+    if (!yq) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_int8_q: yq is NULL");
+    return conv_int8_common("neo_conv2d_int8_q", xq, N, C, H, W, w_packed, w_scale, K, R, S,
+                            x_scale, bias, stride_h, stride_w, pad_h, pad_w, ep, nullptr,
+                            y_cblk_offset, y_cblk_total, nullptr, yq, y_scale, y_pad_h, y_pad_w,
+                            stream);
 }
 
 int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8_t* w_packed, int K,
@@ -484,7 +505,7 @@ int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8
     if (!acc) return fail(NEO_ERR_INVALID_ARG, "neo_conv2d_int8_acc: acc is NULL");
     return conv_int8_common("neo_conv2d_int8_acc", xq, N, C, H, W, w_packed, nullptr, K, R, S, 1.f,
                             nullptr, stride_h, stride_w, pad_h, pad_w, nullptr, nullptr, 0,
-                            cdiv(K, 16), acc, stream);
+                            cdiv(K, 16), acc, nullptr, 0.f, 0, 0, stream);
 }
 
 int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,

@@ -61,6 +61,9 @@ struct I8Args {
     const float* res;     // fp32 NCHW16c [N][KB][OH][OW][16] or null
     float* y;             // fp32 NCHW16c view: blocks [y_off, y_off + KB) of y_tot
     int* acc;             // raw mode: int32 NCHW16c [N][KB][OH][OW][16]
+    int8_t* yq;           // int8 mode: NCHW16c view with a halo [N][y_tot][OH + 2 qph][OW + 2 qpw][16]
+    float yrcp;           // int8 mode: 1 / (the output's scale), rounded to float32
+    int qph, qpw;         // int8 mode: the output's halo
     int N, CB, CG, Hp, Wp, KB, S, sh, sw, OH, OW, M, y_off, y_tot, act;
     int T;                // reduction steps: R * S * CG
     int npx, nkt;         // pixel tiles (16 * FP pixels), channel tiles (FK blocks)
@@ -114,7 +117,11 @@ __device__ __forceinline__ void load_step(const __amdgpu_buffer_rsrc_t xr, const
     c.st = more ? c.st + 1 : c.st;
 }
 
-template <int FK, int FP, int WAVES, bool RAW>
+// Output modes: the float32 epilogue, the raw int32 sums, or the float32
+// epilogue requantized to int8 into the next layer's halo'd input.
+constexpr int kOutF32 = 0, kOutAcc = 1, kOutI8 = 2;
+
+template <int FK, int FP, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -143,9 +150,15 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         // the (r, s) = (0, 0) byte of the pixel's window in channel block g
         xbase[p] = ((n * a.CB + g) * a.Hp + oh * a.sh) * a.Wp * 16 + ow * a.sw * 16;
         // its output element in channel block 0 of [N][KB][OH][OW][16]
-        // (residual, accumulators) and of the view's [N][y_tot][OH][OW][16]
+        // (residual, accumulators) and of the view: [N][y_tot][OH][OW][16]
+        // float32, or in int8 mode [N][y_tot][OH + 2 qph][OW + 2 qpw][16]
         obase[p] = (n * a.KB * ohw + pix) * 16 + 4 * g;
-        ybase[p] = (n * a.y_tot * ohw + pix) * 16 + 4 * g;
+        if constexpr (MODE == kOutI8) {
+            const int owq = a.OW + 2 * a.qpw;
+            ybase[p] = ((n * a.y_tot * (a.OH + 2 * a.qph) + oh + a.qph) * owq + ow + a.qpw) * 16 + 4 * g;
+        } else {
+            ybase[p] = (n * a.y_tot * ohw + pix) * 16 + 4 * g;
+        }
     }
     unsigned woff[FK];
 #pragma unroll
@@ -239,7 +252,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         if (wave != 0) continue;
     }
 
-    if constexpr (RAW) {
+    if constexpr (MODE == kOutAcc) {
 #pragma unroll
         for (int f = 0; f < FK; ++f) {
             const int kofs = (kt * FK + f) * ohw * 16;
@@ -250,7 +263,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         continue;
     }
     const bool relu = a.act == NEO_ACT_RELU;
-    const int yofs = a.y_off * ohw * 16;
+    // one block of the output view: ohw float32 pixels, or the int8 halo'd plane
+    const int yplane = MODE == kOutI8 ? (a.OH + 2 * a.qph) * (a.OW + 2 * a.qpw) : ohw;
+    const int yofs = a.y_off * yplane * 16;
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kt * FK + f;
@@ -263,15 +278,38 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
 #pragma unroll
         for (int p = 0; p < FP; ++p) {
             if (!pv[p]) continue;
+            // ((acc * m) + b) + r, each operation rounded to float32 in this
+            // order (no fused multiply-add): the value the interface defines
             v4f o;
+            {
+#pragma clang fp contract(off)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) o[v] = (float)acc[f][p][v] * mult[v] + bb[v];
-            if (a.res) o += *reinterpret_cast<const v4f*>(a.res + obase[p] + kofs);
+                for (int v = 0; v < 4; ++v) o[v] = (float)acc[f][p][v] * mult[v];
+                if (a.bias) o = o + bb;
+                if (a.res) o = o + *reinterpret_cast<const v4f*>(a.res + obase[p] + kofs);
+            }
             if (relu) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
             }
-            *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
+            if constexpr (MODE == kOutI8) {
+                // clamp(round_half_even(y * (1 / s_y)), -127, 127), four
+                // channels packed into one 4-byte store
+                unsigned packed = 0;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float q;
+                    {
+#pragma clang fp contract(off)
+                        q = rintf(o[v] * a.yrcp);
+                    }
+                    q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
+                    packed |= ((unsigned)(int)q & 0xffu) << (8 * v);
+                }
+                *reinterpret_cast<unsigned*>(a.yq + ybase[p] + yofs + kb * yplane * 16) = packed;
+            } else {
+                *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
+            }
         }
     }
     }
@@ -349,35 +387,35 @@ __global__ __launch_bounds__(256) void pack_filter_i8_kernel(const float* w, int
     }
 }
 
-template <int FK, int FP, int WAVES, bool RAW>
+template <int FK, int FP, int WAVES, int MODE>
 hipError_t launch_t(const I8Args& a, hipStream_t st) {
     // one workgroup per tile up to two rounds of the chip's SIMDs, then each
     // workgroup takes several tiles in turn
     const long cap = 2L * 1024 / WAVES;
     const long wgs = a.ntiles <= cap ? a.ntiles : std::max(cap, (long)(a.ntiles + 3) / 4);
-    hipLaunchKernelGGL((conv_i8<FK, FP, WAVES, RAW>), dim3((unsigned)wgs), dim3(WAVES * 64), 0, st, a);
+    hipLaunchKernelGGL((conv_i8<FK, FP, WAVES, MODE>), dim3((unsigned)wgs), dim3(WAVES * 64), 0, st, a);
     return hipGetLastError();
 }
 
-template <int FK, int FP, bool RAW>
+template <int FK, int FP, int MODE>
 hipError_t by_waves(int waves, const I8Args& a, hipStream_t st) {
     switch (waves) {
-        case 1: return launch_t<FK, FP, 1, RAW>(a, st);
-        case 2: return launch_t<FK, FP, 2, RAW>(a, st);
-        case 4: return launch_t<FK, FP, 4, RAW>(a, st);
+        case 1: return launch_t<FK, FP, 1, MODE>(a, st);
+        case 2: return launch_t<FK, FP, 2, MODE>(a, st);
+        case 4: return launch_t<FK, FP, 4, MODE>(a, st);
         default: return hipErrorInvalidValue;
     }
 }
 
-template <bool RAW>
+template <int MODE>
 hipError_t by_tile(const ConvConfig& c, const I8Args& a, hipStream_t st) {
-    if (c.fk == 1 && c.fp == 1) return by_waves<1, 1, RAW>(c.waves, a, st);
-    if (c.fk == 1 && c.fp == 2) return by_waves<1, 2, RAW>(c.waves, a, st);
-    if (c.fk == 2 && c.fp == 1) return by_waves<2, 1, RAW>(c.waves, a, st);
-    if (c.fk == 2 && c.fp == 2) return by_waves<2, 2, RAW>(c.waves, a, st);
-    if (c.fk == 4 && c.fp == 2) return by_waves<4, 2, RAW>(c.waves, a, st);
-    if (c.fk == 2 && c.fp == 4) return by_waves<2, 4, RAW>(c.waves, a, st);
-    if (c.fk == 4 && c.fp == 4) return by_waves<4, 4, RAW>(c.waves, a, st);
+    if (c.fk == 1 && c.fp == 1) return by_waves<1, 1, MODE>(c.waves, a, st);
+    if (c.fk == 1 && c.fp == 2) return by_waves<1, 2, MODE>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 1) return by_waves<2, 1, MODE>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 2) return by_waves<2, 2, MODE>(c.waves, a, st);
+    if (c.fk == 4 && c.fp == 2) return by_waves<4, 2, MODE>(c.waves, a, st);
+    if (c.fk == 2 && c.fp == 4) return by_waves<2, 4, MODE>(c.waves, a, st);
+    if (c.fk == 4 && c.fp == 4) return by_waves<4, 4, MODE>(c.waves, a, st);
     return hipErrorInvalidValue;
 }
 
@@ -437,7 +475,8 @@ hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, i
 
 hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                             const float* wscale, float xscale, const float* bias, const float* res,
-                            float* y, int* acc, hipStream_t st) {
+                            float* y, int* acc, int8_t* yq, float yscale, int qph, int qpw,
+                            hipStream_t st) {
     if (!int8_config_valid(s, c)) return hipErrorInvalidValue;
     I8Args a;
     a.x = x;
@@ -448,6 +487,10 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.res = res;
     a.y = y;
     a.acc = acc;
+    a.yq = yq;
+    a.yrcp = yq ? 1.0f / yscale : 0.f;
+    a.qph = qph;
+    a.qpw = qpw;
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.CG = cdiv(s.C, 64);
@@ -472,7 +515,8 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)a.npx);
-    return acc ? by_tile<true>(c, a, st) : by_tile<false>(c, a, st);
+    if (acc) return by_tile<kOutAcc>(c, a, st);
+    return yq ? by_tile<kOutI8>(c, a, st) : by_tile<kOutF32>(c, a, st);
 }
 
 }  // namespace neo

@@ -125,7 +125,9 @@ bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 // v_mfma_i32_16x16x64_i8.  Configuration: fk output blocks x fp pixel groups
 // per wave, `waves` waves splitting the reduction (split must be 1).
 // launch_conv_int8 writes the dequantized float32 output y (with the epilogue
-// of s: act, y_off, y_tot), or with `acc` non-null the raw int32 sums.
+// of s: act, y_off, y_tot), or with `acc` non-null the raw int32 sums, or
+// with `yq` non-null that output requantized by 1 / yscale into an int8
+// NCHW16c view with a (qph, qpw) halo.
 size_t int8_filter_bytes(int K, int C, int R, int S);
 // Bytes of the int8 activations with their zero halo: N * ceil(C/16) *
 // (H + 2 ph) * (W + 2 pw) * 16.
@@ -138,7 +140,8 @@ hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, i
                                    hipStream_t st);
 hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                             const float* wscale, float xscale, const float* bias, const float* res,
-                            float* y, int* acc, hipStream_t st);
+                            float* y, int* acc, int8_t* yq, float yscale, int qph, int qpw,
+                            hipStream_t st);
 
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]

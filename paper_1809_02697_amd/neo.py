@@ -100,6 +100,8 @@ def lib():
         "neo_conv2d_int8": [P, I, I, I, I, P, P, I, I, I, F, P, I, I, I, I,
                             ctypes.POINTER(Epilogue), P, I, I, P],
         "neo_conv2d_int8_acc": [P, I, I, I, I, P, I, I, I, I, I, I, I, P, P],
+        "neo_conv2d_int8_q": [P, I, I, I, I, P, P, I, I, I, F, P, I, I, I, I,
+                              ctypes.POINTER(Epilogue), F, I, I, P, I, I, P],
         "neo_fold_bn": [P, P, P, P, P, P, F, I, I, I, I, P, P],
         "neo_maxpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
         "neo_avgpool2d_blocked": [P, I, I, I, I, I, I, I, I, I, I, P, I, I, P],
@@ -423,6 +425,39 @@ def conv2d_int8(xq, C, w_packed, w_scale, K, R, S, x_scale, bias=None, stride=1,
                                  float(x_scale), _dptr(bias, "bias"), sh, sw, ph, pw,
                                  ctypes.byref(ep), _dptr(out, "out"), y_cblk_offset, tot,
                                  _stream(stream)))
+    return out
+
+
+def conv2d_int8_q(xq, C, w_packed, w_scale, K, R, S, x_scale, y_scale, bias=None, stride=1,
+                  pad=0, act="none", residual=None, out_pad=0, out=None, y_cblk_offset=0,
+                  y_cblk_total=None, stream=None):
+    """conv2d_int8 with its float32 output requantized for the next layer:
+    int8 NCHW16c [N][y_cblk_total][OH + 2 ph'][OW + 2 pw'][16] with the halo
+    `out_pad` (the next conv's padding) left as the caller made it (zeros when
+    `out` is allocated here), clamp(round_half_even(y * float32(1 / y_scale)))."""
+    import torch
+    N, H, W, sh, sw, ph, pw, OH, OW = _int8_args(xq, C, w_packed, K, R, S, stride, pad)
+    qph, qpw = _pair(out_pad)
+    tot = cblocks(K) if y_cblk_total is None else y_cblk_total
+    shape = (N, tot, max(OH, 0) + 2 * qph, max(OW, 0) + 2 * qpw, BLOCK)
+    if out is None:
+        out = torch.zeros(shape, device=xq.device, dtype=torch.int8)
+    if OH > 0 and OW > 0:
+        if out.numel() < int(np.prod(shape)):
+            raise ValueError(f"out holds {out.numel()} bytes, the call needs {int(np.prod(shape))}")
+        _need(residual, N * cblocks(K) * OH * OW * BLOCK, "residual")
+    _need(bias, cblocks(K) * BLOCK, "bias")
+    _need(w_scale, cblocks(K) * BLOCK, "w_scale")
+    ep = Epilogue(ACT[act] if isinstance(act, str) else int(act),
+                  residual.data_ptr() if residual is not None else None)
+    if residual is not None:
+        _dptr(residual, "residual")
+    xp, wp = _int8_ptrs(xq, w_packed)
+    _check(lib().neo_conv2d_int8_q(xp, N, C, H, W, wp, _dptr(w_scale, "w_scale"), K, R, S,
+                                   float(x_scale), _dptr(bias, "bias"), sh, sw, ph, pw,
+                                   ctypes.byref(ep), float(y_scale), qph, qpw,
+                                   _dptr_typed(out, torch.int8, "out"), y_cblk_offset, tot,
+                                   _stream(stream)))
     return out
 
 

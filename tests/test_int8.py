@@ -42,6 +42,14 @@ def test_argument_errors():
     assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 1.0, 1, 1, MIS, None) == -3
     assert L.neo_quantize_int8(FAKE, 0, 16, 8, 8, 1.0, 1, 1, FAKE, None) == -1
     assert L.neo_quantize_int8(FAKE, 1, 16, 8, 8, 1.0, -1, 1, FAKE, None) == -1
+    def q(ys=0.5, yq=FAKE, qp=1):
+        return L.neo_conv2d_int8_q(FAKE, 1, 16, 8, 8, FAKE, FAKE, 16, 3, 3, 1.0, None, 1, 1, 1, 1,
+                                   None, ys, qp, qp, yq, 0, 1, None)
+    assert q(yq=None) == -1 and "yq" in neo.last_error()
+    assert q(yq=MIS) == -3
+    for bad in (0.0, -2.0, float("inf"), float("nan"), 1e-45):
+        assert q(ys=bad) == -1 and "y_scale" in neo.last_error()
+    assert q(qp=-1) == -1
     assert L.neo_pack_filter_int8(None, 16, 16, 3, 3, FAKE, FAKE, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 16, 16, 3, 3, FAKE, None, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 0, 16, 3, 3, FAKE, FAKE, None) == -1
@@ -135,8 +143,9 @@ def run_int8(gpu, c, xs, raw=False, bias=True, out=None, y_off=0, y_tot=None):
 
 
 def oracle_int8(c, xs, bias=True, images=None):
-    """The oracle's integer chain: (exact accumulators, dequantized output,
-    the magnitude |acc m| + |bias| + |residual| of the epilogue's terms)."""
+    """The oracle's integer chain: (exact accumulators, the ideal dequantized
+    output, the magnitude |acc m| + |bias| + |residual| of the epilogue's
+    terms, the float32 epilogue as the interface evaluates it)."""
     sel = slice(None) if images is None else images
     acc = oq.conv2d_int(oq.quantize(c.x[sel], xs), oq.quantize_filter(c.w)[0], c.stride, c.pad)
     m = oq.multipliers(xs, oq.filter_scales(c.w))
@@ -149,14 +158,16 @@ def oracle_int8(c, xs, bias=True, images=None):
         mag = mag + np.abs(b.astype(np.float64))[None, :, None, None]
     if res is not None:
         mag = mag + np.abs(res.astype(np.float64))
-    return acc, y, mag
+    return acc, y, mag, oq.epilogue_f32(acc, m, b, res, act)
 
 
-def assert_dequant_close(got, want, mag, what=""):
-    """float32 epilogue: the int32 -> float32 conversion, the product with the
-    multiplier, the bias and residual adds each round once (the ReLU is
-    1-Lipschitz), and the oracle rounds once: |error| <= 6 u (|acc m| + |b| + |r|),
-    u = 2^-24."""
+def assert_dequant_close(got, want, mag, what="", exact=None):
+    """float32 epilogue: equal to the oracle's step-by-step float32 evaluation
+    (`exact`), and within 6 u (|acc m| + |b| + |r|), u = 2^-24, of the ideal
+    value (the int32 -> float32 conversion, the product, the bias and residual
+    adds each round once, the ReLU is 1-Lipschitz, the ideal rounds once)."""
+    if exact is not None:
+        np.testing.assert_array_equal(got, exact, err_msg=what)
     got = np.asarray(got, np.float64)
     bound = 6 * 2.0 ** -24 * mag + 1e-30
     bad = np.abs(got - want) > bound
@@ -231,7 +242,7 @@ def test_accumulators_bit_exact(gpu, e):
     c = wl.conv_case(C, K, R, S, st, pd, H, W, N=N, epilogue="none", with_bn=False)
     xs = act_scale(c.x)
     print(f"\n[int8] acc {e}", flush=True)
-    acc, _, _ = oracle_int8(c, xs)
+    acc, _, _, _ = oracle_int8(c, xs)
     assert_acc_equal(host(run_int8(gpu, c, xs, raw=True)), acc, K, str(e))
 
 
@@ -246,7 +257,7 @@ def test_accumulators_at_the_extremes(gpu, C, H, sign):
     c.w = np.ones_like(c.w)
     c.w[5] = -1.0
     xs = act_scale(c.x)
-    acc, _, _ = oracle_int8(c, xs)
+    acc, _, _, _ = oracle_int8(c, xs)
     assert np.abs(acc).max() == 127 * 127 * 9 * C
     assert_acc_equal(host(run_int8(gpu, c, xs, raw=True)), acc, 16, f"extreme C={C}")
 
@@ -261,9 +272,9 @@ def test_dequantized_output(gpu, epi):
     c = wl.conv_case(64, 80, 3, 3, 1, 1, 10, 9, N=2, epilogue=e, with_bn=False,
                      out_hw=(10, 9))
     xs = act_scale(c.x)
-    _, want, mag = oracle_int8(c, xs, bias=epi != "nobias")
+    _, want, mag, y32 = oracle_int8(c, xs, bias=epi != "nobias")
     got = orc.from_blocked(host(run_int8(gpu, c, xs, bias=epi != "nobias")), 80)
-    assert_dequant_close(got, want, mag, epi)
+    assert_dequant_close(got, want, mag, epi, y32)
 
 
 @pytest.mark.gpu
@@ -277,8 +288,8 @@ def test_concat_view(gpu):
     buf = torch.full((2, 6, 9, 9, 16), 7.0, device="cuda")
     run_int8(gpu, c, xs, out=buf, y_off=2, y_tot=6)
     b = host(buf)
-    _, want, mag = oracle_int8(c, xs)
-    assert_dequant_close(orc.from_blocked(np.ascontiguousarray(b[:, 2:5]), 40), want, mag, "view")
+    _, want, mag, y32 = oracle_int8(c, xs)
+    assert_dequant_close(orc.from_blocked(np.ascontiguousarray(b[:, 2:5]), 40), want, mag, "view", y32)
     assert (b[:, :2] == 7).all() and (b[:, 5:] == 7).all()
 
 
@@ -300,11 +311,11 @@ def test_every_configuration(gpu, cfg, monkeypatch):
                          out_hw=(H, W))
         xs = act_scale(c.x)
         print(f"\n[int8] forced {cfg} C={C}", flush=True)
-        acc, want, mag = oracle_int8(c, xs)
+        acc, want, mag, y32 = oracle_int8(c, xs)
         a1 = host(run_int8(gpu, c, xs, raw=True))
         assert_acc_equal(a1, acc, 64, cfg)
         np.testing.assert_array_equal(a1, host(run_int8(gpu, c, xs, raw=True)))
-        assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 64), want, mag, cfg)
+        assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 64), want, mag, cfg, y32)
 
 
 @pytest.mark.gpu
@@ -320,9 +331,9 @@ def test_resnet50_layers_batch32_sampled(gpu, lid):
     print(f"\n[int8] {lid} batch 32", flush=True)
     acc_b = host(run_int8(gpu, c, xs, raw=True))[[0, 31]]
     y_b = host(run_int8(gpu, c, xs))[[0, 31]]
-    acc, want, mag = oracle_int8(c, xs, images=[0, 31])
+    acc, want, mag, y32 = oracle_int8(c, xs, images=[0, 31])
     assert_acc_equal(acc_b, acc, c.K, lid)
-    assert_dequant_close(orc.from_blocked(y_b, c.K), want, mag, lid)
+    assert_dequant_close(orc.from_blocked(y_b, c.K), want, mag, lid, y32)
 
 
 @pytest.mark.gpu
@@ -336,6 +347,112 @@ def test_workgroups_taking_several_tiles(gpu, cfg, N, monkeypatch):
     c = wl.conv_case(64, 16, 3, 3, 1, 1, 40, 40, N=N, epilogue="res", with_bn=False,
                      out_hw=(40, 40))
     xs = act_scale(c.x)
-    acc, want, mag = oracle_int8(c, xs)
+    acc, want, mag, y32 = oracle_int8(c, xs)
     assert_acc_equal(host(run_int8(gpu, c, xs, raw=True)), acc, 16, cfg)
-    assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 16), want, mag, cfg)
+    assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 16), want, mag, cfg, y32)
+
+
+# ---- int8 output: the float32 epilogue requantized into the next layer's input ----------------
+def run_int8_q(gpu, c, xs, ys, out_pad, out=None, y_off=0, y_tot=None):
+    from gpu_util import dev
+    xq = gpu.quantize_int8(gpu.to_blocked(dev(c.x)), c.C, xs, pad=c.pad)
+    wq, ws = gpu.pack_filter_int8(dev(c.w))
+    res = gpu.to_blocked(dev(c.residual)) if c.epilogue == "res" else None
+    act = "relu" if c.epilogue in ("relu", "res", "bias_relu") else "none"
+    b = dev(_pad16(c.bias, c.K)) if c.bias is not None else None
+    return gpu.conv2d_int8_q(xq, c.C, wq, ws, c.K, c.R, c.S, xs, ys, bias=b, stride=c.stride,
+                             pad=c.pad, act=act, residual=res, out_pad=out_pad, out=out,
+                             y_cblk_offset=y_off, y_cblk_total=y_tot)
+
+
+def requant_ref(y32, ys, K, out_pad, blocks=None):
+    """The oracle's requantized output in the blocked layout with its halo
+    (zeros), padding channels 0."""
+    q = oq.requantize(y32, ys)
+    N, _, OH, OW = q.shape
+    ph, pw = out_pad
+    full = np.zeros((N, q.shape[1], OH + 2 * ph, OW + 2 * pw), np.int8)
+    full[:, :, ph:ph + OH, pw:pw + OW] = q
+    return orc.to_blocked(full)
+
+
+Q_CASES = [
+    # C, K, R, stride, pad, H, N, epilogue, out_pad
+    (64, 64, 3, 1, 1, 14, 2, "relu", (1, 1)),       # a 3x3 feeding a 3x3
+    (48, 40, 1, 1, 0, 9, 1, "none", (0, 0)),        # ragged K, signed output, no halo
+    (32, 80, 3, 2, 1, 15, 3, "relu", (2, 1)),       # stride 2, uneven halo
+    (64, 48, 1, 1, 0, 7, 2, "res", (1, 1)),         # residual + ReLU
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("e", Q_CASES, ids=[f"C{e[0]}K{e[1]}r{e[2]}s{e[3]}{e[7]}q{e[8][0]}{e[8][1]}"
+                                            for e in Q_CASES])
+def test_requantized_output_bit_exact(gpu, e):
+    """int8 output against the oracle's float32 epilogue requantized by the
+    float32 reciprocal of the output scale, the halo zero; the output scale is
+    the float output's max |y| / 127 (the next layer's calibration)."""
+    from gpu_util import host
+    C, K, R, st, pd, H, N, epi, qpad = e
+    OH = (H + 2 * pd - R) // st + 1
+    c = wl.conv_case(C, K, R, R, st, pd, H, H, N=N, epilogue=epi, with_bn=False, out_hw=(OH, OH))
+    xs = act_scale(c.x)
+    _, _, _, y32 = oracle_int8(c, xs)
+    ys = act_scale(y32) if np.abs(y32).max() > 0 else np.float32(1)
+    got = host(run_int8_q(gpu, c, xs, ys, qpad))
+    np.testing.assert_array_equal(got, requant_ref(y32, ys, K, qpad), err_msg=str(e))
+
+
+@pytest.mark.gpu
+def test_requantized_view_keeps_the_rest(gpu):
+    """Written into blocks [1, 4) of a 5-block int8 buffer prefilled with 7: the
+    other blocks and the halo keep their bytes."""
+    import torch
+    from gpu_util import host
+    c = wl.conv_case(24, 40, 3, 3, 1, 1, 9, 9, N=2, epilogue="relu", with_bn=False)
+    xs = act_scale(c.x)
+    _, _, _, y32 = oracle_int8(c, xs)
+    ys = act_scale(y32)
+    buf = torch.full((2, 5, 11, 11, 16), 7, dtype=torch.int8, device="cuda")
+    run_int8_q(gpu, c, xs, ys, (1, 1), out=buf, y_off=1, y_tot=5)
+    b = host(buf)
+    want = requant_ref(y32, ys, 40, (1, 1))
+    np.testing.assert_array_equal(b[:, 1:4, 1:10, 1:10], want[:, :, 1:10, 1:10])
+    assert (b[:, 0] == 7).all() and (b[:, 4] == 7).all()
+    inner = np.zeros(b.shape, bool)
+    inner[:, :, 1:10, 1:10] = True
+    assert (b[~inner] == 7).all()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("cfg", ["1,1,1", "2,2,2", "4,2,4", "4,4,1", "2,4,2"])
+def test_requantized_every_tile(gpu, cfg, monkeypatch):
+    from gpu_util import host
+    monkeypatch.setenv("NEO_I8_CONFIG", cfg)
+    c = wl.conv_case(80, 64, 3, 3, 1, 1, 13, 11, N=2, epilogue="res", with_bn=False,
+                     out_hw=(13, 11))
+    xs = act_scale(c.x)
+    _, _, _, y32 = oracle_int8(c, xs)
+    ys = act_scale(y32)
+    np.testing.assert_array_equal(host(run_int8_q(gpu, c, xs, ys, (1, 2))),
+                                  requant_ref(y32, ys, 64, (1, 2)), err_msg=cfg)
+
+
+@pytest.mark.gpu
+def test_two_layer_int8_chain(gpu):
+    """conv 1 (3x3, int8 output with conv 2's halo) -> conv 2 (3x3) reading it
+    directly: conv 2's sums against the oracle's chain, bit for bit."""
+    from gpu_util import dev, host
+    c1 = wl.conv_case(32, 48, 3, 3, 1, 1, 12, 10, N=2, epilogue="bias_relu", with_bn=False)
+    rng = np.random.default_rng(44)
+    w2 = rng.normal(0, np.sqrt(2 / (48 * 9)), (64, 48, 3, 3)).astype(np.float32)
+    xs = act_scale(c1.x)
+    _, _, _, y32 = oracle_int8(c1, xs)
+    ys = act_scale(y32)
+    # oracle chain: requantize, then the integer conv of layer 2
+    want = oq.conv2d_int(oq.requantize(y32, ys), oq.quantize_filter(w2)[0], 1, 1)
+    # device chain
+    q1 = run_int8_q(gpu, c1, xs, ys, (1, 1))
+    wq2, _ = gpu.pack_filter_int8(dev(w2))
+    acc2 = gpu.conv2d_int8_acc(q1, 48, wq2, 64, 3, 3, stride=1, pad=1)
+    assert_acc_equal(host(acc2), want, 64, "chain")
