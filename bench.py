@@ -414,6 +414,9 @@ def layer_table(torch, plan, x, out, reps, cold=True, cold_hbm_only=False, selec
 
 
 PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 matrix peak (5.0 POP/s)
+# ResNet-50 layers whose output a 3x3 conv reads (its padding 1 becomes the
+# int8 output's halo); every other output feeds a 1x1
+INT8_NEXT_PAD = {"R02": 1, "R05": 1, "R06": 1, "R10": 1, "R12": 1, "R16": 1, "R18": 1, "R22": 1}
 
 
 def int8_layer(neo, torch, wl, i, N):
@@ -443,10 +446,22 @@ def int8_layer(neo, torch, wl, i, N):
 
     def quant():
         neo.quantize_int8(xb, C, xs, pad=pd, out=xq)
+    # int8 output for the next layer: its halo is the padding of the conv that
+    # reads it in ResNet-50 (1 before a 3x3, 0 before a 1x1); output scale of
+    # the order of the float output's (its value does not change the time)
+    qpad = INT8_NEXT_PAD.get(lid, 0)
+    yq = torch.zeros((N, KB, OH + 2 * qpad, OH + 2 * qpad, 16), device="cuda", dtype=torch.int8)
+
+    def conv_q():
+        neo.conv2d_int8_q(xq, C, wq, ws, K, R, R, xs, 0.05, bias=bias, stride=st, pad=pd, act=act,
+                          residual=res, out_pad=qpad, out=yq)
     ops = 2 * N * K * C * R * R * OH * OH
-    nbytes = N * C * H * H + K * C * R * R + 4 * N * K * OH * OH * (2 if res is not None else 1) + 8 * K
+    rbytes = 4 * N * K * OH * OH if res is not None else 0
+    nbytes = N * C * H * H + K * C * R * R + 4 * N * K * OH * OH + rbytes + 8 * K
+    nbytes_q = N * C * H * H + K * C * R * R + N * K * OH * OH + rbytes + 8 * K
     label = f"{C}->{K} {R}x{R}/s{st} {H}->{OH}" + (" +res" if res is not None else "")
-    return dict(id=lid, shape=label, uses=uses, ops=ops, bytes=nbytes, conv=conv, quant=quant)
+    return dict(id=lid, shape=label, uses=uses, ops=ops, bytes=nbytes, bytes_q=nbytes_q, conv=conv,
+                quant=quant, conv_q=conv_q)
 
 
 def int8_layer_table(neo, torch, wl, N=32, reps=10, fp32_us=None):
@@ -456,13 +471,16 @@ def int8_layer_table(neo, torch, wl, N=32, reps=10, fp32_us=None):
     each timed alone like layer_table (warm, back-to-back graph replays),
     beside the activation quantization pass the layer needs and, from
     fp32_us ({shape label: us} of the tuned fp32 plan), the fp32 conv of the
-    same shape.  Ops are the direct convolution's; bytes are algorithmic:
-    int8 input and filter, float32 output and residual."""
+    same shape; int8_out_*: the same conv writing its output requantized to
+    int8 (the next layer's input, no quantization pass between int8 layers).
+    Ops are the direct convolution's; bytes are algorithmic: int8 input and
+    filter, float32 (or int8) output, float32 residual."""
     rows = []
     for i in range(len(wl.RESNET50_LAYERS)):
         L = int8_layer(neo, torch, wl, i, N)
         us = time_graph(torch, L["conv"], reps)
         q_us = time_graph(torch, L["quant"], reps)
+        us_q = time_graph(torch, L["conv_q"], reps)
         ops, nbytes = L["ops"], L["bytes"]
         ai = ops / nbytes
         roof = min(PEAK_INT8_TOPS, ai * PEAK_HBM_GBS / 1e3)
@@ -475,14 +493,20 @@ def int8_layer_table(neo, torch, wl, N=32, reps=10, fp32_us=None):
                          bound="mfma" if ai * PEAK_HBM_GBS / 1e3 >= PEAK_INT8_TOPS else "hbm",
                          pct_roof=round(100 * tops / roof, 1),
                          fp32_us=f32, speedup_vs_fp32=round(f32 / us, 2) if f32 else None,
+                         int8_out_us=round(us_q, 2),
+                         int8_out_tops=round(ops / (us_q * 1e-6) / 1e12, 1),
+                         int8_out_alg_gbs=round(L["bytes_q"] / (us_q * 1e-6) / 1e9, 1),
                          _ops=ops))
         del L
     t = sum(r["us"] * r["uses"] for r in rows)
     tq = sum((r["us"] + r["quant_us"]) * r["uses"] for r in rows)
     ops = sum(r.pop("_ops") * r["uses"] for r in rows)
+    tqo = sum(r["int8_out_us"] * r["uses"] for r in rows)
     summary = dict(batch=N, convs=sum(r["uses"] for r in rows), sum_us=round(t, 1),
                    sum_with_quant_us=round(tq, 1), tops=round(ops / (t * 1e-6) / 1e12, 1),
-                   pct_int8_mfma=round(100 * ops / (t * 1e-6) / 1e12 / PEAK_INT8_TOPS, 2))
+                   pct_int8_mfma=round(100 * ops / (t * 1e-6) / 1e12 / PEAK_INT8_TOPS, 2),
+                   int8_out_sum_us=round(tqo, 1),
+                   int8_out_tops=round(ops / (tqo * 1e-6) / 1e12, 1))
     m = [r for r in rows if r["fp32_us"]]
     if m:
         # over the shapes the fp32 plan launches alone (the stem runs fused
@@ -490,9 +514,11 @@ def int8_layer_table(neo, torch, wl, N=32, reps=10, fp32_us=None):
         t32 = sum(r["fp32_us"] * r["uses"] for r in m)
         t8 = sum(r["us"] * r["uses"] for r in m)
         t8q = sum((r["us"] + r["quant_us"]) * r["uses"] for r in m)
+        t8o = sum(r["int8_out_us"] * r["uses"] for r in m)
         summary.update(fp32_matched_convs=sum(r["uses"] for r in m), fp32_sum_us=round(t32, 1),
                        int8_matched_sum_us=round(t8, 1), speedup_vs_fp32=round(t32 / t8, 2),
-                       speedup_with_quant=round(t32 / t8q, 2))
+                       speedup_with_quant=round(t32 / t8q, 2),
+                       int8_out_speedup_vs_fp32=round(t32 / t8o, 2))
     return rows, summary
 
 
