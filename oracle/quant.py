@@ -20,6 +20,13 @@ scheme, so this module fixes one, the usual symmetric linear quantization:
   r = 1 / s_y rounded to float32 and the product in float32 (one multiply per
   value; it can differ from x / s_y by one step at an exact tie).
 
+Integer inference of a whole network (``run_graph_int8``): every conv's
+input is quantized with the scale max |x| / 127 of the tensor it reads
+(calibrated on the run itself), the filter is the batch-norm-folded one
+(``fold_bn``) quantized per output channel, and the conv's output is the
+float32 epilogue above; pools, concatenation, flatten and dense are the
+float32 oracle's own.
+
 Only ``tests/`` use this module.  It shares no code with the HIP library.
 """
 from __future__ import annotations
@@ -110,3 +117,72 @@ def requantize(y, scale):
     r = np.float32(1) / np.float32(scale)
     q = np.rint(np.asarray(y, np.float32) * r)
     return np.clip(q, -QMAX, QMAX).astype(np.int8)
+
+
+def fold_bn(w, bias, bn):
+    """Batch norm folded into the preceding conv (the inference
+    simplification of Section 2.2): s = gamma / sqrt(var + eps),
+    w' = w s, b' = (b - mean) s + beta, in float64, each rounded once to
+    float32 (eps as the float32 the network description holds)."""
+    g = np.asarray(bn["gamma"], np.float64)
+    v = np.asarray(bn["var"], np.float64)
+    s = g / np.sqrt(v + np.float64(np.float32(bn["eps"])))
+    w2 = (np.asarray(w, np.float64) * s[:, None, None, None]).astype(np.float32)
+    b = np.zeros(len(g)) if bias is None else np.asarray(bias, np.float64)
+    b2 = ((b - np.asarray(bn["mean"], np.float64)) * s + np.asarray(bn["beta"], np.float64))
+    return w2, b2.astype(np.float32)
+
+
+def act_scale(x):
+    """A tensor's scale: max |x| / 127 in float32 (1 for an all-zero tensor)."""
+    m = np.float32(np.abs(np.asarray(x, np.float32)).max())
+    return np.float32(m / np.float32(QMAX)) if m > 0 else np.float32(1.0)
+
+
+def conv_node_int8(n, x, residual=None):
+    """One conv node through the integer path: (output, the input's scale)."""
+    if n.bn is not None:
+        w, b = fold_bn(n.w, n.bias, n.bn)
+    else:
+        w = np.asarray(n.w, np.float32)
+        b = None if n.bias is None else np.asarray(n.bias, np.float32)
+    xs = act_scale(x)
+    wq, ws = quantize_filter(w)
+    acc = conv2d_int(quantize(x, xs), wq, n.stride, n.pad)
+    return epilogue_f32(acc, multipliers(xs, ws), b, residual, n.act), xs
+
+
+def run_graph_int8(graph, x=None):
+    """A network description with every conv through the integer path, node
+    by node; returns (output, the convs' input scales in node order)."""
+    import oracle as fo
+    x = graph.x if x is None else x
+    vals = [None] * len(graph.nodes)
+    scales = []
+    for i, n in enumerate(graph.nodes):
+        ins = [vals[j] for j in n.inputs]
+        if n.op == "input":
+            v = np.asarray(x, np.float32)
+        elif n.op == "conv":
+            v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None)
+            scales.append(xs)
+        elif n.op == "maxpool":
+            v = fo.maxpool2d(ins[0], n.R, n.S, n.stride, n.pad)
+        elif n.op == "avgpool":
+            v = fo.avgpool2d(ins[0], n.R, n.S, n.stride, n.pad)
+        elif n.op == "gap":
+            v = fo.global_avgpool(ins[0])
+        elif n.op == "concat":
+            v = fo.concat(ins)
+        elif n.op == "flatten":
+            v = fo.flatten(ins[0])
+        elif n.op == "dense":
+            v = fo.dense(ins[0], n.w, n.bias)
+            if n.act == "relu":
+                v = fo.relu(v)
+        elif n.op == "output":
+            v = ins[0]
+        else:
+            raise ValueError("unknown op " + n.op)
+        vals[i] = v
+    return vals[-1], np.array(scales, np.float32)

@@ -134,3 +134,71 @@ def test_requantize_multiplies_by_the_float32_reciprocal():
     assert oq.quantize(np.float32([45.5]), 7.0)[0] == 6
     assert oq.requantize(np.float32([45.5]), 7.0)[0] == 7
 
+
+
+def test_fold_bn_by_hand_and_against_the_unfolded_conv():
+    import oracle as fo
+    # var + eps = 4: s = gamma / 2; b' = (b - mean) s + beta
+    bn = dict(gamma=np.float32([2.0, 1.0]), beta=np.float32([0.5, -1.0]), mean=np.float32([1.0, 0.0]),
+              var=np.float32([4.0 - 2.0 ** -10, 4.0 - 2.0 ** -10]), eps=2.0 ** -10)
+    w = np.float32([3.0, -6.0]).reshape(2, 1, 1, 1)
+    w2, b2 = oq.fold_bn(w, np.float32([5.0, 2.0]), bn)
+    np.testing.assert_array_equal(w2.ravel(), [3.0, -3.0])
+    np.testing.assert_array_equal(b2, [(5 - 1) * 1 + 0.5, (2 - 0) * 0.5 - 1.0])
+    assert oq.fold_bn(w, None, bn)[1][0] == (0 - 1) * 1 + 0.5
+    # a folded conv equals the conv followed by batch norm (pinned primitives)
+    rng = np.random.default_rng(8)
+    x = rng.normal(0, 1, (1, 4, 6, 6)).astype(np.float32)
+    w = rng.normal(0, 0.3, (5, 4, 3, 3)).astype(np.float32)
+    bn = dict(gamma=rng.uniform(0.5, 1.5, 5).astype(np.float32), beta=rng.normal(0, 0.1, 5).astype(np.float32),
+              mean=rng.normal(0, 0.1, 5).astype(np.float32), var=rng.uniform(0.5, 1.5, 5).astype(np.float32),
+              eps=1e-5)
+    w2, b2 = oq.fold_bn(w, None, bn)
+    got = fo.bias_add(fo.conv2d(x, w2, 1, 1), b2)
+    want = fo.batchnorm(fo.conv2d(x, w, 1, 1), bn["gamma"], bn["beta"], bn["mean"], bn["var"], bn["eps"])
+    np.testing.assert_allclose(got, want, rtol=1e-5, atol=1e-6)
+
+
+def test_act_scale():
+    assert oq.act_scale(np.float32([[-254.0, 3.0]])) == np.float32(2.0)
+    assert oq.act_scale(np.zeros(5, np.float32)) == np.float32(1.0)
+    assert oq.act_scale(np.float32([0.5])) == np.float32(0.5) / np.float32(127)
+
+
+def _integer_graph():
+    """A network on which every quantization is exact: an integer input of
+    max 127, convs whose filters are 127 times a 0/1 pattern (per-channel
+    scale 1), so each conv's output is 127 times an integer tensor of max 127
+    (the next scale is 127) as long as every output channel keeps that max."""
+    from paper_1809_02697_amd.workloads import Graph, Node
+    rng = np.random.default_rng(12)
+    x = rng.integers(-127, 128, (2, 3, 6, 5)).astype(np.float32)
+    x[0, 0, 0, 0] = 127.0
+    eye = lambda K, C: (127.0 * np.eye(K, C)).reshape(K, C, 1, 1).astype(np.float32)
+    shift = np.zeros((3, 3, 3, 3), np.float32)
+    for k in range(3):
+        shift[k, k, 1, 1] = 127.0        # a centred delta: the identity with padding
+    nodes = [
+        Node("input"),
+        Node("conv", (0,), K=3, R=1, S=1, w=eye(3, 3)),                       # 127 x
+        Node("conv", (1,), K=3, R=3, S=3, pad=(1, 1), w=shift),               # 127 x again
+        Node("maxpool", (2,), R=2, S=2, stride=(2, 2)),                      # 3 x 3 x 2
+        Node("conv", (1,), K=3, R=1, S=1, w=eye(3, 3), residual=2, act="relu"),
+        Node("maxpool", (4,), R=2, S=2, stride=(2, 2)),
+        Node("concat", (3, 5)),
+        Node("flatten", (6,)),
+        Node("dense", (7,), K=4, w=rng.integers(-2, 3, (4, 6 * 3 * 2)).astype(np.float32)),
+        Node("output", (8,)),
+    ]
+    return Graph("integer", nodes, x.shape, x)
+
+
+def test_integer_network_equals_the_float_network():
+    """Every scale is a power of 127 and every value an integer below 2^24,
+    so the integer path reproduces the float oracle's network exactly, and
+    the scales are fixed by hand: 1 for the input, 127 after each conv."""
+    import oracle as fo
+    g = _integer_graph()
+    y8, scales = oq.run_graph_int8(g)
+    np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 127.0]))
+    np.testing.assert_array_equal(y8, fo.run_graph(g))
