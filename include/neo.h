@@ -440,7 +440,18 @@ enum neo_plan_flags {
      * Winograd kernel's configurations beside the direct kernel's and keeps
      * the faster algorithm per conv.  Results match the oracle within the
      * float32 tolerance, not bit for bit. */
-    NEO_PLAN_WINOGRAD = 1024
+    NEO_PLAN_WINOGRAD = 1024,
+    /* Integer inference (the paper's future work, Sections 1 and 5): every
+     * conv runs as its float32 input quantized with one scale per tensor
+     * (neo_quantize_int8, the conv's padding as the halo) followed by the
+     * integer convolution with its float32 epilogue (neo_conv2d_int8: bias,
+     * residual, activation); filters are the batch-norm-folded ones
+     * quantized per output channel on the device at plan creation.  Pools,
+     * concatenation, flatten and dense stay float32.  The input scales come
+     * from neo_plan_calibrate_int8, which must run before the plan does.
+     * Every conv is its own step in NCHW16c: block 16, and no NAIVE, TUNE,
+     * GLOBAL_SEARCH, fusion or WINOGRAD flag. */
+    NEO_PLAN_INT8 = 2048
 };
 
 /*
@@ -487,6 +498,20 @@ int neo_run_graph(neo_plan* plan, const float* x_nchw, float* y_out, neo_stream_
  * before it must have run for its input to be meaningful.  For timing single
  * layers as the plan launches them. */
 int neo_run_step(neo_plan* plan, int step, const float* x_nchw, float* y_out, neo_stream_t stream);
+
+/*
+ * Calibrate a NEO_PLAN_INT8 plan on the input x_nchw (device, NCHW; the
+ * output goes to y_out as for neo_run_graph): run the plan step by step on
+ * `stream` and, just before each conv, set that conv's input scale to
+ * max|x| / 127 in float32 over its float32 input as this run produced it
+ * (1 for an all-zero input).  Synchronizes the stream once per conv (the
+ * maximum is read back); drops a captured graph, which the next
+ * neo_run_graph captures again with the new scales.  neo_plan_describe then
+ * lists each conv's "x_scale".  Errors: NEO_ERR_STATE for a plan without
+ * NEO_PLAN_INT8 or host-only, NEO_ERR_INVALID_ARG / _ALIGN for the buffers,
+ * NEO_ERR_INVALID_ARG for a non-finite activation.
+ */
+int neo_plan_calibrate_int8(neo_plan* plan, const float* x_nchw, float* y_out, neo_stream_t stream);
 
 /* Free the plan and its device memory (synchronizes the device first).
  * NULL is ignored.  Later use of the handle returns NEO_ERR_STATE. */

@@ -348,6 +348,25 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* x, int H, in
     *reinterpret_cast<v4i*>(q + t * 16) = out.v;
 }
 
+// max |x| over n floats (n a multiple of 4, 16-byte aligned) into *out as
+// the float's bits (non-negative floats order like their bit patterns): a
+// grid-stride float4 pass, a wave maximum, one vector atomic per wave.
+// *out must hold 0 before (absmax_clear).
+__global__ __launch_bounds__(256) void absmax_kernel(const float* x, long n4, unsigned* out) {
+    float m = 0.f;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
+        const v4f v = reinterpret_cast<const v4f*>(x)[i];
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+    }
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+    if ((threadIdx.x & 63) == 0) atomicMax(out, __float_as_uint(m));
+}
+
+__global__ void absmax_clear(unsigned* out) {
+    if (threadIdx.x == 0) *out = 0u;
+}
+
 // KCRS fp32 -> per-output-channel scales and the packed int8 filter, one
 // workgroup per (padded) output channel: max |w[k]| by a tree in LDS, then
 // every element quantized and written to its packed position.
@@ -452,6 +471,14 @@ ConvConfig choose_int8_config(const ConvShape& s) {
         if (int8_config_valid(s, c)) return c;
     }
     return ConvConfig{1, 1, 1, 1};
+}
+
+hipError_t launch_absmax(const float* x, long n, unsigned* out, hipStream_t st) {
+    hipLaunchKernelGGL(absmax_clear, dim3(1), dim3(64), 0, st, out);
+    const long n4 = n / 4;
+    const long blocks = std::min<long>(2048, std::max<long>(1, (n4 + 255) / 256));
+    hipLaunchKernelGGL(absmax_kernel, dim3((unsigned)blocks), dim3(256), 0, st, x, n4, out);
+    return hipGetLastError();
 }
 
 size_t int8_act_bytes(int N, int C, int H, int W, int ph, int pw) {

@@ -134,6 +134,9 @@ size_t int8_filter_bytes(int K, int C, int R, int S);
 size_t int8_act_bytes(int N, int C, int H, int W, int ph, int pw);
 bool int8_config_valid(const ConvShape& s, const ConvConfig& c);
 ConvConfig choose_int8_config(const ConvShape& s);
+// max |x| over n floats (n a multiple of 4, x 16-byte aligned), written to
+// *out as the float's bit pattern.
+hipError_t launch_absmax(const float* x, long n, unsigned* out, hipStream_t st);
 hipError_t launch_quantize_int8(const float* x, int N, int C, int H, int W, int ph, int pw, float scale,
                                 int8_t* q, hipStream_t st);
 hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, int8_t* wq, float* wscale,

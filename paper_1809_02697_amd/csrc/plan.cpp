@@ -84,6 +84,14 @@ struct Step {
     long u_off = -1;
     bool wino = false;
     ConvConfig wc{1, 1, 1, 1};
+    // ST_CONV with NEO_PLAN_INT8: the folded KCRS filter (float offset), the
+    // per-channel scales the device packing writes (float offset), the packed
+    // int8 filter and the quantized input with its halo (byte offsets in the
+    // int8 arena), the input's scale (set by calibration), the configuration
+    bool i8 = false;
+    long kcrs_off = -1, ws8_off = -1, w8_off = -1, xq_off = -1;
+    float xscale = 1.f;
+    ConvConfig c8{1, 1, 1, 1};
 };
 
 struct Xform {
@@ -121,6 +129,12 @@ struct neo_plan {
     std::vector<float> params;  // host copy of prepared parameters
     float* d_params = nullptr;
     char* d_act = nullptr;
+    // NEO_PLAN_INT8: int8 arena (packed filters, quantized inputs), whether
+    // the input scales have been calibrated, the calibration's maximum word
+    long i8_bytes = 0;
+    int8_t* d_i8 = nullptr;
+    bool i8_ready = false;
+    unsigned* d_absmax = nullptr;
     // split-reduction workspace shared by the conv steps (they run in order)
     size_t ws_bytes = 0;
     float* d_ws = nullptr;
@@ -458,6 +472,26 @@ int build_steps(neo_plan* P) {
                     st.u_off = add_params(P, u);
                 }
                 if (has_b) st.b_off = add_params(P, b);
+                if (P->flags & NEO_PLAN_INT8) {
+                    if ((long)C * d.R * d.S > 133000)
+                        return fail(NEO_ERR_UNSUPPORTED, where + "C * R * S above 133,000 could overflow "
+                                                                 "the int32 accumulator");
+                    const long xq = (long)int8_act_bytes(ni.N, C, a->H, a->W, d.pad_h, d.pad_w);
+                    if ((long)int8_filter_bytes(d.K, C, d.R, d.S) >= (1L << 31) ||
+                        xq + 4L * (a->H + 2 * d.pad_h) * (a->W + 2 * d.pad_w) * 16 >= (1L << 31))
+                        return fail(NEO_ERR_UNSUPPORTED, where + "int8 input or filter of 2 GiB or more");
+                    st.i8 = true;
+                    st.kcrs_off = add_params(P, w);
+                    st.ws8_off = add_params(P, std::vector<float>((size_t)cdiv(d.K, 16) * 16, 1.f));
+                    auto take = [&](long bytes) {
+                        const long off = P->i8_bytes;
+                        P->i8_bytes += (bytes + 255) / 256 * 256;
+                        return off;
+                    };
+                    st.w8_off = take((long)int8_filter_bytes(d.K, C, d.R, d.S));
+                    st.xq_off = take(xq);
+                    st.c8 = choose_int8_config(st.cs);
+                }
                 st.cc = choose_conv_config(st.cs);
                 if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
                 const int v = B.new_val(id, ni.N, ni.C, ni.H, ni.W, ni.oc);
@@ -1015,7 +1049,14 @@ std::string describe(const neo_plan* P) {
               << ",\"ic_bn\":" << c.xb << ",\"oc_bn\":" << c.yb
               << ",\"tile\":[" << cfg.fk << "," << cfg.fp << "],\"split\":" << cfg.split
               << ",\"waves\":" << cfg.waves << ",\"tuned\":" << (s.tuned ? "true" : "false")
-              << ",\"algo\":\"" << (s.wino ? "winograd" : "direct") << "\"";
+              << ",\"algo\":\"" << (s.i8 ? "int8" : s.wino ? "winograd" : "direct") << "\"";
+            if (s.i8) {
+                char xs[32];
+                std::snprintf(xs, sizeof xs, "%.9g", (double)s.xscale);
+                o << ",\"int8\":{\"tile\":[" << s.c8.fk << "," << s.c8.fp << "],\"waves\":" << s.c8.waves
+                  << ",\"x_scale\":" << xs << ",\"calibrated\":" << (P->i8_ready ? "true" : "false")
+                  << "}";
+            }
             if (c.gap) o << ",\"gap_sums\":true";
             o << "}";
         };
@@ -1289,8 +1330,16 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
     if (flags & ~(unsigned)(NEO_PLAN_HOST_ONLY | NEO_PLAN_NAIVE | NEO_PLAN_HIPGRAPH | NEO_PLAN_TUNE |
                             NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP | NEO_PLAN_FUSE_GAP |
                             NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS | NEO_PLAN_FUSE_POOL |
-                            NEO_PLAN_WINOGRAD))
+                            NEO_PLAN_WINOGRAD | NEO_PLAN_INT8))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
+    if ((flags & NEO_PLAN_INT8) &&
+        ((flags & (NEO_PLAN_NAIVE | NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP |
+                   NEO_PLAN_FUSE_GAP | NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS |
+                   NEO_PLAN_FUSE_POOL | NEO_PLAN_WINOGRAD)) ||
+         block != 16))
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: NEO_PLAN_INT8 plans every conv alone in "
+                                         "NCHW16c (block 16; no naive transforms, tuning, search, "
+                                         "fusion or Winograd)");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
     if ((flags & NEO_PLAN_GLOBAL_SEARCH) && (flags & NEO_PLAN_NAIVE))
@@ -1352,6 +1401,26 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
             (void)hipFree(P->d_act);
             delete P;
             return hip_fail(e, "neo_plan_create: parameter upload");
+        }
+        if (flags & NEO_PLAN_INT8) {
+            // the packed int8 filters and their scales, from the folded filters
+            e = hipMalloc(&P->d_i8, std::max<long>(P->i8_bytes, 256));
+            if (e == hipSuccess) e = hipMalloc(&P->d_absmax, 256);
+            for (const Step& st : P->steps)
+                if (e == hipSuccess && st.kind == ST_CONV && st.i8)
+                    e = launch_pack_filter_int8(P->d_params + st.kcrs_off, st.cs.K, st.cs.C, st.cs.R,
+                                                st.cs.S, P->d_i8 + st.w8_off, P->d_params + st.ws8_off,
+                                                nullptr);
+            if (e == hipSuccess) e = hipDeviceSynchronize();
+            if (e != hipSuccess) {
+                if (P->d_i8) (void)hipFree(P->d_i8);
+                if (P->d_absmax) (void)hipFree(P->d_absmax);
+                (void)hipFree(P->d_params);
+                (void)hipFree(P->d_act);
+                delete P;
+                return e == hipErrorOutOfMemory ? fail(NEO_ERR_OOM, "neo_plan_create: int8 arena")
+                                                : hip_fail(e, "neo_plan_create: int8 filter packing");
+            }
         }
         if (flags & NEO_PLAN_TUNE) {
             const int trc = tune_plan(P);
@@ -1440,6 +1509,20 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 break;
             }
             case ST_CONV:
+                if (s.i8) {
+                    // the fp32 input quantized with its halo, then the integer conv
+                    const Val& in = P->vals[s.in];
+                    int8_t* xq = P->d_i8 + s.xq_off;
+                    e = launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                                             s.cs.ph, s.cs.pw, s.xscale, xq, st);
+                    if (e == hipSuccess)
+                        e = launch_conv_int8(s.cs, s.c8, xq, P->d_i8 + s.w8_off, prm + s.ws8_off, s.xscale,
+                                             s.b_off >= 0 ? prm + s.b_off : nullptr,
+                                             s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
+                                             val_ptr(P, s.out, x_nchw, y_out), nullptr, nullptr, 1.f, 0, 0,
+                                             st);
+                    break;
+                }
                 if (s.wino) {
                     e = launch_wino(s.cs, s.wc, val_ptr(P, s.in, x_nchw, y_out), prm + s.u_off,
                                     s.b_off >= 0 ? prm + s.b_off : nullptr,
@@ -1828,6 +1911,8 @@ int neo_run_graph(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t s
     if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_graph: NULL buffer");
     if (!aligned16(x_nchw) || !aligned16(y_out))
         return fail(NEO_ERR_ALIGN, "neo_run_graph: buffers must be 16-byte aligned");
+    if ((P->flags & NEO_PLAN_INT8) && !P->i8_ready)
+        return fail(NEO_ERR_STATE, "neo_run_graph: an int8 plan runs after neo_plan_calibrate_int8");
     hipStream_t st = (hipStream_t)stream;
     if (!(P->flags & NEO_PLAN_HIPGRAPH)) return enqueue_steps(P, x_nchw, y_out, st);
     if (!P->graph_exec || P->graph_x != x_nchw || P->graph_y != y_out) {
@@ -1846,7 +1931,45 @@ int neo_run_step(neo_plan* P, int step, const float* x_nchw, float* y_out, neo_s
     if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_run_step: NULL buffer");
     if (!aligned16(x_nchw) || !aligned16(y_out))
         return fail(NEO_ERR_ALIGN, "neo_run_step: buffers must be 16-byte aligned");
+    if ((P->flags & NEO_PLAN_INT8) && !P->i8_ready)
+        return fail(NEO_ERR_STATE, "neo_run_step: an int8 plan runs after neo_plan_calibrate_int8");
     return enqueue_step(P, P->steps[step], x_nchw, y_out, (hipStream_t)stream);
+}
+
+int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_stream_t stream) {
+    if (!live(P)) return fail(NEO_ERR_STATE, "neo_plan_calibrate_int8: not a live plan");
+    if (!(P->flags & NEO_PLAN_INT8) || (P->flags & NEO_PLAN_HOST_ONLY))
+        return fail(NEO_ERR_STATE, "neo_plan_calibrate_int8: not a device plan with NEO_PLAN_INT8");
+    if (!x_nchw || !y_out) return fail(NEO_ERR_INVALID_ARG, "neo_plan_calibrate_int8: NULL buffer");
+    if (!aligned16(x_nchw) || !aligned16(y_out))
+        return fail(NEO_ERR_ALIGN, "neo_plan_calibrate_int8: buffers must be 16-byte aligned");
+    hipStream_t st = (hipStream_t)stream;
+    drop_graph(P);
+    P->i8_ready = false;
+    for (Step& s : P->steps) {
+        if (s.kind == ST_CONV && s.i8) {
+            // the input's scale: max |x| / 127 over the conv's float32 input
+            // as this run produced it (1 for an all-zero input)
+            const Val& in = P->vals[s.in];
+            const long n = (long)in.N * cdiv(in.C, 16) * 16 * in.H * in.W;
+            unsigned bits = 0;
+            hipError_t e = launch_absmax(val_ptr(P, s.in, x_nchw, y_out), n, P->d_absmax, st);
+            if (e == hipSuccess) e = hipMemcpyAsync(&bits, P->d_absmax, 4, hipMemcpyDeviceToHost, st);
+            if (e == hipSuccess) e = hipStreamSynchronize(st);
+            if (e != hipSuccess) return hip_fail(e, "neo_plan_calibrate_int8: input maximum");
+            float m;
+            std::memcpy(&m, &bits, 4);
+            if (!std::isfinite(m))
+                return fail(NEO_ERR_INVALID_ARG, "neo_plan_calibrate_int8: non-finite activation");
+            s.xscale = m > 0.f ? m / 127.0f : 1.0f;
+        }
+        const int rc = enqueue_step(P, s, x_nchw, y_out, st);
+        if (rc != NEO_OK) return rc;
+    }
+    hipError_t e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "neo_plan_calibrate_int8: run");
+    P->i8_ready = true;
+    return NEO_OK;
 }
 
 void neo_plan_destroy(neo_plan* plan) {
@@ -1862,6 +1985,8 @@ void neo_plan_destroy(neo_plan* plan) {
         (void)hipFree(plan->d_params);
         (void)hipFree(plan->d_act);
         if (plan->d_ws) (void)hipFree(plan->d_ws);
+        if (plan->d_i8) (void)hipFree(plan->d_i8);
+        if (plan->d_absmax) (void)hipFree(plan->d_absmax);
     }
     delete plan;
 }

@@ -34,6 +34,7 @@ PLAN_FUSE_PAIRS = 128
 PLAN_FUSE_CHAINS = 256
 PLAN_FUSE_POOL = 512
 PLAN_WINOGRAD = 1024
+PLAN_INT8 = 2048
 BLOCK = 16
 SEARCH_BLOCKS = (0, 4, 8, 16, 32, 64)   # layout index space of neo_layout_search
 
@@ -114,6 +115,7 @@ def lib():
         "neo_plan_conv_params": [P, I, P, P],
         "neo_run_graph": [P, P, P, P],
         "neo_run_step": [P, I, P, P, P],
+        "neo_plan_calibrate_int8": [P, P, P, P],
         "neo_tune_db_save": [ctypes.c_char_p],
         "neo_tune_db_load": [ctypes.c_char_p],
         "neo_tune_db_clear": [],
@@ -703,6 +705,21 @@ class Plan:
         _need(out, int(np.prod(self.output_shape)), "out")
         _check(lib().neo_run_graph(self.handle, _dptr(x, "x"), _dptr(out, "out"),
                                    _stream(stream)))
+        return out
+
+    def calibrate_int8(self, x, out=None, stream=None):
+        """NEO_PLAN_INT8: set every conv's input scale from a run on x (device
+        NCHW); returns that run's output."""
+        import torch
+        if tuple(x.shape) != self.input_shape:
+            raise ValueError(f"input shape {tuple(x.shape)} != plan input {self.input_shape}")
+        if out is None:
+            N, C, H, W = self.output_shape
+            shape = (N, C) if (H, W) == (1, 1) else (N, C, H, W)
+            out = torch.empty(shape, device=x.device, dtype=torch.float32)
+        _need(out, int(np.prod(self.output_shape)), "out")
+        _check(lib().neo_plan_calibrate_int8(self.handle, _dptr(x, "x"), _dptr(out, "out"),
+                                             _stream(stream)))
         return out
 
     def run_step(self, step, x, out, stream=None):
