@@ -21,11 +21,13 @@ scheme, so this module fixes one, the usual symmetric linear quantization:
   value; it can differ from x / s_y by one step at an exact tie).
 
 Integer inference of a whole network (``run_graph_int8``): every conv's
-input is quantized with the scale max |x| / 127 of the tensor it reads
-(calibrated on the run itself), the filter is the batch-norm-folded one
-(``fold_bn``) quantized per output channel, and the conv's output is the
-float32 epilogue above; pools, concatenation, flatten and dense are the
-float32 oracle's own.
+input has the scale max |x| / 127 of the float32 tensor it reads
+(calibrated on the run itself) and is quantized by division, except an
+input that is the output of a conv read by nothing else: that conv writes
+it requantized (by the reciprocal, as above).  The filter is the
+batch-norm-folded one (``fold_bn``) quantized per output channel, and the
+conv's output is the float32 epilogue above; pools, concatenation, flatten
+and dense are the float32 oracle's own.
 
 Only ``tests/`` use this module.  It shares no code with the HIP library.
 """
@@ -139,8 +141,10 @@ def act_scale(x):
     return np.float32(m / np.float32(QMAX)) if m > 0 else np.float32(1.0)
 
 
-def conv_node_int8(n, x, residual=None):
-    """One conv node through the integer path: (output, the input's scale)."""
+def conv_node_int8(n, x, residual=None, chained=False):
+    """One conv node through the integer path: (output, the input's scale);
+    `chained`: x is the float32 output of the conv that writes this conv's
+    input requantized."""
     if n.bn is not None:
         w, b = fold_bn(n.w, n.bias, n.bn)
     else:
@@ -148,7 +152,7 @@ def conv_node_int8(n, x, residual=None):
         b = None if n.bias is None else np.asarray(n.bias, np.float32)
     xs = act_scale(x)
     wq, ws = quantize_filter(w)
-    acc = conv2d_int(quantize(x, xs), wq, n.stride, n.pad)
+    acc = conv2d_int((requantize if chained else quantize)(x, xs), wq, n.stride, n.pad)
     return epilogue_f32(acc, multipliers(xs, ws), b, residual, n.act), xs
 
 
@@ -159,12 +163,20 @@ def run_graph_int8(graph, x=None):
     x = graph.x if x is None else x
     vals = [None] * len(graph.nodes)
     scales = []
+    uses = [[] for _ in graph.nodes]     # (consumer, as input or as residual)
+    for i, n in enumerate(graph.nodes):
+        for j in n.inputs:
+            uses[j].append((i, "in"))
+        if n.residual >= 0:
+            uses[n.residual].append((i, "res"))
     for i, n in enumerate(graph.nodes):
         ins = [vals[j] for j in n.inputs]
         if n.op == "input":
             v = np.asarray(x, np.float32)
         elif n.op == "conv":
-            v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None)
+            j = n.inputs[0]
+            chained = graph.nodes[j].op == "conv" and uses[j] == [(i, "in")]
+            v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None, chained)
             scales.append(xs)
         elif n.op == "maxpool":
             v = fo.maxpool2d(ins[0], n.R, n.S, n.stride, n.pad)

@@ -168,8 +168,9 @@ def test_act_scale():
 def _integer_graph():
     """A network on which every quantization is exact: an integer input of
     max 127, convs whose filters are 127 times a 0/1 pattern (per-channel
-    scale 1), so each conv's output is 127 times an integer tensor of max 127
-    (the next scale is 127) as long as every output channel keeps that max."""
+    scale 1), so each conv's output is 127 times its input's integers and
+    the next scale a power of 127.  Conv 1's output is read by conv 2 alone
+    (a chained, requantized input); the rest take their own quantization."""
     from paper_1809_02697_amd.workloads import Graph, Node
     rng = np.random.default_rng(12)
     x = rng.integers(-127, 128, (2, 3, 6, 5)).astype(np.float32)
@@ -181,24 +182,24 @@ def _integer_graph():
     nodes = [
         Node("input"),
         Node("conv", (0,), K=3, R=1, S=1, w=eye(3, 3)),                       # 127 x
-        Node("conv", (1,), K=3, R=3, S=3, pad=(1, 1), w=shift),               # 127 x again
+        Node("conv", (1,), K=3, R=3, S=3, pad=(1, 1), w=shift),               # 127^2 x
         Node("maxpool", (2,), R=2, S=2, stride=(2, 2)),                      # 3 x 3 x 2
-        Node("conv", (1,), K=3, R=1, S=1, w=eye(3, 3), residual=2, act="relu"),
-        Node("maxpool", (4,), R=2, S=2, stride=(2, 2)),
-        Node("concat", (3, 5)),
-        Node("flatten", (6,)),
-        Node("dense", (7,), K=4, w=rng.integers(-2, 3, (4, 6 * 3 * 2)).astype(np.float32)),
-        Node("output", (8,)),
+        Node("conv", (3,), K=3, R=1, S=1, w=eye(3, 3), residual=3, act="relu"),
+        Node("concat", (3, 4)),
+        Node("flatten", (5,)),
+        Node("dense", (6,), K=4, w=rng.integers(-2, 3, (4, 6 * 3 * 2)).astype(np.float32)),
+        Node("output", (7,)),
     ]
     return Graph("integer", nodes, x.shape, x)
 
 
 def test_integer_network_equals_the_float_network():
-    """Every scale is a power of 127 and every value an integer below 2^24,
-    so the integer path reproduces the float oracle's network exactly, and
-    the scales are fixed by hand: 1 for the input, 127 after each conv."""
+    """Every scale is a power of 127 and every quantization exact (the last
+    conv's products round once, on both sides alike), so the integer path
+    reproduces the float oracle's network exactly, with the scales fixed by
+    hand: 1 for the input, 127 for conv 1's output, 127^2 for the pool's."""
     import oracle as fo
     g = _integer_graph()
     y8, scales = oq.run_graph_int8(g)
-    np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 127.0]))
+    np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 16129.0]))
     np.testing.assert_array_equal(y8, fo.run_graph(g))
