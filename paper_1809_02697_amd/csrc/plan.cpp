@@ -92,6 +92,11 @@ struct Step {
     long kcrs_off = -1, ws8_off = -1, w8_off = -1, xq_off = -1;
     float xscale = 1.f;
     ConvConfig c8{1, 1, 1, 1};
+    // int8 chain: this conv's output is the only input of step q_next, an
+    // int8 conv, and is written requantized straight into its halo'd input
+    // (q_next >= 0); this conv's input is written so by its producer (q_by_prev)
+    int q_next = -1;
+    bool q_by_prev = false;
 };
 
 struct Xform {
@@ -135,6 +140,7 @@ struct neo_plan {
     int8_t* d_i8 = nullptr;
     bool i8_ready = false;
     unsigned* d_absmax = nullptr;
+    bool i8_f32_out = false;  // calibration: a chained conv's first run writes float32
     // split-reduction workspace shared by the conv steps (they run in order)
     size_t ws_bytes = 0;
     float* d_ws = nullptr;
@@ -996,6 +1002,39 @@ bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_ou
     return true;
 }
 
+// NEO_PLAN_INT8: a conv whose output value is read by nothing but one other
+// conv's input writes that output requantized into the consumer's int8 input
+// (with the consumer's scale and padding halo), and the consumer's
+// quantization pass is dropped.
+void chain_int8(neo_plan* P) {
+    const int ns = (int)P->steps.size();
+    for (int i = 0; i < ns; ++i) {
+        Step& s = P->steps[i];
+        if (s.kind != ST_CONV || !s.i8) continue;
+        const int v = s.out;
+        if (P->vals[v].view || v == P->out_val || P->vals[v].buf < 0) continue;
+        bool other = false;
+        for (const Val& w : P->vals)
+            if (w.alias_of == v) other = true;
+        int reader = -1, uses = 0;
+        for (int j = 0; j < ns; ++j) {
+            const Step& t = P->steps[j];
+            if (t.in == v) {
+                ++uses;
+                reader = j;
+            }
+            if (t.res == v || t.out2 == v) other = true;
+            for (const Step& m : t.members)
+                if (m.in == v || m.res == v) other = true;
+        }
+        if (other || uses != 1 || reader <= i) continue;
+        Step& t = P->steps[reader];
+        if (t.kind != ST_CONV || !t.i8) continue;
+        s.q_next = reader;
+        t.q_by_prev = true;
+    }
+}
+
 std::string describe(const neo_plan* P) {
     std::ostringstream o;
     auto lay = [](int l) { return l ? "NCHW" + std::to_string(l) + "c" : std::string("NCHW"); };
@@ -1055,7 +1094,8 @@ std::string describe(const neo_plan* P) {
                 std::snprintf(xs, sizeof xs, "%.9g", (double)s.xscale);
                 o << ",\"int8\":{\"tile\":[" << s.c8.fk << "," << s.c8.fp << "],\"waves\":" << s.c8.waves
                   << ",\"x_scale\":" << xs << ",\"calibrated\":" << (P->i8_ready ? "true" : "false")
-                  << "}";
+                  << ",\"writes_next_input\":" << (s.q_next >= 0 ? "true" : "false")
+                  << ",\"input_from_producer\":" << (s.q_by_prev ? "true" : "false") << "}";
             }
             if (c.gap) o << ",\"gap_sums\":true";
             o << "}";
@@ -1354,6 +1394,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) chain_int8(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
@@ -1405,6 +1446,9 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (flags & NEO_PLAN_INT8) {
             // the packed int8 filters and their scales, from the folded filters
             e = hipMalloc(&P->d_i8, std::max<long>(P->i8_bytes, 256));
+            // zero once: the halos of the inputs a producer writes directly
+            // are never written again
+            if (e == hipSuccess) e = hipMemset(P->d_i8, 0, std::max<long>(P->i8_bytes, 256));
             if (e == hipSuccess) e = hipMalloc(&P->d_absmax, 256);
             for (const Step& st : P->steps)
                 if (e == hipSuccess && st.kind == ST_CONV && st.i8)
@@ -1510,17 +1554,22 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
             }
             case ST_CONV:
                 if (s.i8) {
-                    // the fp32 input quantized with its halo, then the integer conv
+                    // the fp32 input quantized with its halo (unless the
+                    // producer wrote it), then the integer conv, whose output
+                    // is either float32 or the next conv's int8 input
                     const Val& in = P->vals[s.in];
                     int8_t* xq = P->d_i8 + s.xq_off;
-                    e = launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
-                                             s.cs.ph, s.cs.pw, s.xscale, xq, st);
+                    if (!s.q_by_prev)
+                        e = launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                                                 s.cs.ph, s.cs.pw, s.xscale, xq, st);
+                    const Step* nx = (s.q_next >= 0 && !P->i8_f32_out) ? &P->steps[s.q_next] : nullptr;
                     if (e == hipSuccess)
                         e = launch_conv_int8(s.cs, s.c8, xq, P->d_i8 + s.w8_off, prm + s.ws8_off, s.xscale,
                                              s.b_off >= 0 ? prm + s.b_off : nullptr,
                                              s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
-                                             val_ptr(P, s.out, x_nchw, y_out), nullptr, nullptr, 1.f, 0, 0,
-                                             st);
+                                             nx ? nullptr : val_ptr(P, s.out, x_nchw, y_out), nullptr,
+                                             nx ? P->d_i8 + nx->xq_off : nullptr, nx ? nx->xscale : 1.f,
+                                             nx ? nx->cs.ph : 0, nx ? nx->cs.pw : 0, st);
                     break;
                 }
                 if (s.wino) {
@@ -1946,24 +1995,42 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
     hipStream_t st = (hipStream_t)stream;
     drop_graph(P);
     P->i8_ready = false;
-    for (Step& s : P->steps) {
-        if (s.kind == ST_CONV && s.i8) {
-            // the input's scale: max |x| / 127 over the conv's float32 input
-            // as this run produced it (1 for an all-zero input)
-            const Val& in = P->vals[s.in];
-            const long n = (long)in.N * cdiv(in.C, 16) * 16 * in.H * in.W;
-            unsigned bits = 0;
-            hipError_t e = launch_absmax(val_ptr(P, s.in, x_nchw, y_out), n, P->d_absmax, st);
-            if (e == hipSuccess) e = hipMemcpyAsync(&bits, P->d_absmax, 4, hipMemcpyDeviceToHost, st);
-            if (e == hipSuccess) e = hipStreamSynchronize(st);
-            if (e != hipSuccess) return hip_fail(e, "neo_plan_calibrate_int8: input maximum");
-            float m;
-            std::memcpy(&m, &bits, 4);
-            if (!std::isfinite(m))
-                return fail(NEO_ERR_INVALID_ARG, "neo_plan_calibrate_int8: non-finite activation");
-            s.xscale = m > 0.f ? m / 127.0f : 1.0f;
+    // max |x| / 127 in float32 over n floats of the device tensor x (1 for zeros)
+    auto scale_of = [&](const float* x, long n, float* out) {
+        unsigned bits = 0;
+        hipError_t e = launch_absmax(x, n, P->d_absmax, st);
+        if (e == hipSuccess) e = hipMemcpyAsync(&bits, P->d_absmax, 4, hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "neo_plan_calibrate_int8: input maximum");
+        float m;
+        std::memcpy(&m, &bits, 4);
+        if (!std::isfinite(m)) return fail(NEO_ERR_INVALID_ARG, "neo_plan_calibrate_int8: non-finite activation");
+        *out = m > 0.f ? m / 127.0f : 1.0f;
+        return (int)NEO_OK;
+    };
+    auto elems = [&](int v) {
+        const Val& a = P->vals[v];
+        return (long)a.N * cdiv(a.C, 16) * 16 * a.H * a.W;
+    };
+    for (size_t i = 0; i < P->steps.size(); ++i) {
+        Step& s = P->steps[i];
+        int rc;
+        // the scale of an input quantized by its own pass: from that input
+        if (s.kind == ST_CONV && s.i8 && !s.q_by_prev &&
+            (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in), &s.xscale)) != NEO_OK)
+            return rc;
+        if (s.kind == ST_CONV && s.i8 && s.q_next >= 0) {
+            // a chained producer: run it once with its float32 output, take
+            // the consumer's scale from that, then run it as the plan does
+            P->i8_f32_out = true;
+            rc = enqueue_step(P, s, x_nchw, y_out, st);
+            P->i8_f32_out = false;
+            if (rc != NEO_OK) return rc;
+            if ((rc = scale_of(val_ptr(P, s.out, x_nchw, y_out), elems(s.out),
+                               &P->steps[s.q_next].xscale)) != NEO_OK)
+                return rc;
         }
-        const int rc = enqueue_step(P, s, x_nchw, y_out, st);
+        rc = enqueue_step(P, s, x_nchw, y_out, st);
         if (rc != NEO_OK) return rc;
     }
     hipError_t e = hipStreamSynchronize(st);

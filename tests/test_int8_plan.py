@@ -3,8 +3,9 @@ neo_plan_calibrate_int8) against the oracle's integer network executor
 (oracle.quant.run_graph_int8).
 
 Every int8 layer's arithmetic is fixed exactly (quantization by float32
-division, exact integer sums, the float32 epilogue one rounding per
-operation, max pools exact), so on networks without average pooling the
+division, or by the float32 reciprocal where the producing conv writes the
+input itself; exact integer sums; the float32 epilogue one rounding per
+operation; max pools exact), so on networks without average pooling the
 calibrated input scales of all convs must equal the oracle's bit for bit:
 each is the maximum of a tensor that both sides computed identically.  Only
 the global average pool and the dense layers that follow the last conv sum
@@ -27,6 +28,10 @@ def test_host_plan_and_flags():
     assert len(convs) == 53 and len(d["steps"]) == 57
     assert all(s["conv"]["algo"] == "int8" and not s["conv"]["int8"]["calibrated"] for s in convs)
     assert not any(s["kind"].startswith("conv_") for s in d["steps"])     # no fused steps
+    # the convs whose output only the next conv reads write its int8 input:
+    # the 1x1 reduce -> 3x3 -> 1x1 expand links of the 16 bottlenecks
+    assert sum(s["conv"]["int8"]["writes_next_input"] for s in convs) == 32
+    assert sum(s["conv"]["int8"]["input_from_producer"] for s in convs) == 32
     L = neo.lib()
     FAKE = ctypes.c_void_p(1 << 20)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
