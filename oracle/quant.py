@@ -23,8 +23,8 @@ scheme, so this module fixes one, the usual symmetric linear quantization:
 Integer inference of a whole network (``run_graph_int8``): every conv's
 input has the scale max |x| / 127 of the float32 tensor it reads
 (calibrated on the run itself) and is quantized by division, except an
-input that is the output of a conv read by nothing else: that conv writes
-it requantized (by the reciprocal, as above).  The filter is the
+input that is the output of a conv whose conv readers all have the same
+padding: that conv writes it requantized (by the reciprocal, as above).  The filter is the
 batch-norm-folded one (``fold_bn``) quantized per output channel, and the
 conv's output is the float32 epilogue above; pools, concatenation, flatten
 and dense are the float32 oracle's own.
@@ -175,7 +175,9 @@ def run_graph_int8(graph, x=None):
             v = np.asarray(x, np.float32)
         elif n.op == "conv":
             j = n.inputs[0]
-            chained = graph.nodes[j].op == "conv" and uses[j] == [(i, "in")]
+            pads = {tuple(graph.nodes[c].pad) for c, how in uses[j]
+                    if how == "in" and graph.nodes[c].op == "conv"}
+            chained = graph.nodes[j].op == "conv" and len(pads) == 1
             v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None, chained)
             scales.append(xs)
         elif n.op == "maxpool":
