@@ -535,7 +535,8 @@ def model_latencies(neo, torch, wl, steps):
     plans of the Table 3 ablation; ResNet-50 also at fixed blocks 32 and 64;
     and with the 3x3 stride-1 convs free to run by Winograd F(2x2, 3x3) (the
     paper's future work; the local search keeps it per conv where faster),
-    with and without the fusions."""
+    with and without the fusions; and integer inference (NEO_PLAN_INT8, its
+    speedup over the fastest float32 plan of the entry)."""
     res = {}
     for name, builder, batch in [("resnet50", wl.resnet50, 1), ("vgg16", wl.vgg16, 1),
                                  ("inception_v3", wl.inception_v3, 1), ("resnet50", wl.resnet50, 32),
@@ -575,6 +576,24 @@ def model_latencies(neo, torch, wl, steps):
                 entry["conv_tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
                 entry["images_per_s"] = round(batch / (ms * 1e-3), 1)
             p.destroy()
+        if name != "inception_v3":
+            # integer inference (every conv quantized + int8; calibrated on
+            # this input, untimed), graph replay; ResNet-50 and VGG-16 only,
+            # the networks whose int8 parity is exact (no average pooling)
+            t0 = time.perf_counter()
+            p = neo.Plan(g, flags=neo.PLAN_INT8 | neo.PLAN_HIPGRAPH)
+            out = p.calibrate_int8(x)
+            t_plan = time.perf_counter() - t0
+            ms = e2e_ms(torch, p, x, out, steps, 3)
+            d = p.describe()
+            q = [st["conv"]["int8"] for st in d["steps"] if st["kind"] == "conv"]
+            entry["int8"] = dict(ms=round(ms, 4), launches=len(d["steps"]) +
+                                 sum(x["quantizes_input"] for x in q),
+                                 quantization_passes=sum(x["quantizes_input"] for x in q),
+                                 plan_s=round(t_plan, 1))
+            p.destroy()
+            entry["int8_speedup"] = round(min(v["ms"] for k, v in entry.items()
+                                              if isinstance(v, dict) and k != "int8") / ms, 3)
         if "naive" in entry:
             entry["elimination_speedup"] = round(entry["naive"]["ms"] / entry["eliminated"]["ms"], 3)
         if "searched" in entry:

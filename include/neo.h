@@ -446,8 +446,14 @@ enum neo_plan_flags {
      * (neo_quantize_int8, the conv's padding as the halo) followed by the
      * integer convolution with its float32 epilogue (neo_conv2d_int8: bias,
      * residual, activation); filters are the batch-norm-folded ones
-     * quantized per output channel on the device at plan creation.  Pools,
-     * concatenation, flatten and dense stay float32.  The input scales come
+     * quantized per output channel on the device at plan creation.  A value
+     * that int8 convs read has one int8 copy per padding among them (shared
+     * by those convs, one scale: max|value| / 127); when all of them pad
+     * alike and a conv produces the value, that conv's epilogue writes the
+     * copy (requantized by the float32 reciprocal of the scale, beside its
+     * float32 output when anything else reads that), otherwise the first
+     * reader runs the quantization pass.  Pools, concatenation, flatten and
+     * dense stay float32.  The input scales come
      * from neo_plan_calibrate_int8, which must run before the plan does.
      * Every conv is its own step in NCHW16c: block 16, and no NAIVE, TUNE,
      * GLOBAL_SEARCH, fusion or WINOGRAD flag. */

@@ -61,9 +61,10 @@ struct I8Args {
     const float* res;     // fp32 NCHW16c [N][KB][OH][OW][16] or null
     float* y;             // fp32 NCHW16c view: blocks [y_off, y_off + KB) of y_tot
     int* acc;             // raw mode: int32 NCHW16c [N][KB][OH][OW][16]
-    int8_t* yq;           // int8 mode: NCHW16c view with a halo [N][y_tot][OH + 2 qph][OW + 2 qpw][16]
+    int8_t* yq;           // int8 modes: NCHW16c with a halo [N][KB][OH + 2 qph][OW + 2 qpw][16]
     float yrcp;           // int8 mode: 1 / (the output's scale), rounded to float32
-    int qph, qpw;         // int8 mode: the output's halo
+    int qph, qpw;         // int8 modes: the output's halo
+    int q_off, q_tot;     // int8 modes: blocks [q_off, q_off + KB) of q_tot
     int N, CB, CG, Hp, Wp, KB, S, sh, sw, OH, OW, M, y_off, y_tot, act;
     int T;                // reduction steps: R * S * CG
     int npx, nkt;         // pixel tiles (16 * FP pixels), channel tiles (FK blocks)
@@ -117,9 +118,10 @@ __device__ __forceinline__ void load_step(const __amdgpu_buffer_rsrc_t xr, const
     c.st = more ? c.st + 1 : c.st;
 }
 
-// Output modes: the float32 epilogue, the raw int32 sums, or the float32
-// epilogue requantized to int8 into the next layer's halo'd input.
-constexpr int kOutF32 = 0, kOutAcc = 1, kOutI8 = 2;
+// Output modes: the float32 epilogue, the raw int32 sums, the float32
+// epilogue requantized to int8 into the next layer's halo'd input, or both
+// the float32 output and its requantized copy.
+constexpr int kOutF32 = 0, kOutAcc = 1, kOutI8 = 2, kOutBoth = 3;
 
 template <int FK, int FP, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
     const int pxt = u - kt * a.npx;
 
     bool pv[FP];
-    int xbase[FP], obase[FP], ybase[FP];
+    int xbase[FP], obase[FP], ybase[FP], qbase[FP];
 #pragma unroll
     for (int p = 0; p < FP; ++p) {
         const int m = (pxt * FP + p) * 16 + li;
@@ -153,12 +155,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         // (residual, accumulators) and of the view: [N][y_tot][OH][OW][16]
         // float32, or in int8 mode [N][y_tot][OH + 2 qph][OW + 2 qpw][16]
         obase[p] = (n * a.KB * ohw + pix) * 16 + 4 * g;
-        if constexpr (MODE == kOutI8) {
-            const int owq = a.OW + 2 * a.qpw;
-            ybase[p] = ((n * a.y_tot * (a.OH + 2 * a.qph) + oh + a.qph) * owq + ow + a.qpw) * 16 + 4 * g;
-        } else {
-            ybase[p] = (n * a.y_tot * ohw + pix) * 16 + 4 * g;
-        }
+        ybase[p] = (n * a.y_tot * ohw + pix) * 16 + 4 * g;
+        const int owq = a.OW + 2 * a.qpw;
+        qbase[p] = ((n * a.q_tot * (a.OH + 2 * a.qph) + oh + a.qph) * owq + ow + a.qpw) * 16 + 4 * g;
     }
     unsigned woff[FK];
 #pragma unroll
@@ -263,9 +262,8 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         continue;
     }
     const bool relu = a.act == NEO_ACT_RELU;
-    // one block of the output view: ohw float32 pixels, or the int8 halo'd plane
-    const int yplane = MODE == kOutI8 ? (a.OH + 2 * a.qph) * (a.OW + 2 * a.qpw) : ohw;
-    const int yofs = a.y_off * yplane * 16;
+    const int yofs = a.y_off * ohw * 16;
+    const int qplane = (a.OH + 2 * a.qph) * (a.OW + 2 * a.qpw);  // one block of the int8 copy
 #pragma unroll
     for (int f = 0; f < FK; ++f) {
         const int kb = kt * FK + f;
@@ -292,7 +290,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
             }
-            if constexpr (MODE == kOutI8) {
+            if constexpr (MODE == kOutF32 || MODE == kOutBoth)
+                *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
+            if constexpr (MODE == kOutI8 || MODE == kOutBoth) {
                 // clamp(round_half_even(y * (1 / s_y)), -127, 127), four
                 // channels packed into one 4-byte store
                 unsigned packed = 0;
@@ -306,9 +306,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
                     q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
                     packed |= ((unsigned)(int)q & 0xffu) << (8 * v);
                 }
-                *reinterpret_cast<unsigned*>(a.yq + ybase[p] + yofs + kb * yplane * 16) = packed;
-            } else {
-                *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
+                *reinterpret_cast<unsigned*>(a.yq + qbase[p] + (a.q_off + kb) * qplane * 16) = packed;
             }
         }
     }
@@ -518,6 +516,10 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.yrcp = yq ? 1.0f / yscale : 0.f;
     a.qph = qph;
     a.qpw = qpw;
+    // the int8 output takes the view of s when it is the only output; beside
+    // the float32 output it is a whole tensor of its own
+    a.q_off = y ? 0 : s.y_off;
+    a.q_tot = y ? cdiv(s.K, 16) : s.y_tot;
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.CG = cdiv(s.C, 64);
@@ -543,7 +545,8 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     a.div_ow = make_fastdiv((unsigned)s.OW);
     a.div_npx = make_fastdiv((unsigned)a.npx);
     if (acc) return by_tile<kOutAcc>(c, a, st);
-    return yq ? by_tile<kOutI8>(c, a, st) : by_tile<kOutF32>(c, a, st);
+    if (yq) return y ? by_tile<kOutBoth>(c, a, st) : by_tile<kOutI8>(c, a, st);
+    return by_tile<kOutF32>(c, a, st);
 }
 
 }  // namespace neo

@@ -127,7 +127,8 @@ bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 // launch_conv_int8 writes the dequantized float32 output y (with the epilogue
 // of s: act, y_off, y_tot), or with `acc` non-null the raw int32 sums, or
 // with `yq` non-null that output requantized by 1 / yscale into an int8
-// NCHW16c view with a (qph, qpw) halo.
+// NCHW16c view with a (qph, qpw) halo (with `y` null: the view of s;
+// with `y` too: both outputs, the int8 one a whole [N][KB] tensor).
 size_t int8_filter_bytes(int K, int C, int R, int S);
 // Bytes of the int8 activations with their zero halo: N * ceil(C/16) *
 // (H + 2 ph) * (W + 2 pw) * 16.

@@ -86,17 +86,26 @@ struct Step {
     ConvConfig wc{1, 1, 1, 1};
     // ST_CONV with NEO_PLAN_INT8: the folded KCRS filter (float offset), the
     // per-channel scales the device packing writes (float offset), the packed
-    // int8 filter and the quantized input with its halo (byte offsets in the
-    // int8 arena), the input's scale (set by calibration), the configuration
+    // int8 filter (byte offset in the int8 arena), the configuration; the
+    // int8 copy of the input it reads (qc), whether this step runs that
+    // copy's quantization pass, the copy its own epilogue writes (q_out; -1:
+    // none) and whether it also writes its float32 output
     bool i8 = false;
-    long kcrs_off = -1, ws8_off = -1, w8_off = -1, xq_off = -1;
-    float xscale = 1.f;
+    long kcrs_off = -1, ws8_off = -1, w8_off = -1;
     ConvConfig c8{1, 1, 1, 1};
-    // int8 chain: this conv's output is the only input of step q_next, an
-    // int8 conv, and is written requantized straight into its halo'd input
-    // (q_next >= 0); this conv's input is written so by its producer (q_by_prev)
-    int q_next = -1;
-    bool q_by_prev = false;
+    int qc = -1, q_out = -1;
+    bool quant_here = false, f32_needed = true;
+};
+
+// NEO_PLAN_INT8: the int8 copy of a value with one halo (the padding of the
+// convs that read it), in the int8 arena, with its scale; written by the
+// epilogue of the conv producing the value (writer) or by one quantization
+// pass (run by the first conv that reads it)
+struct I8Copy {
+    int val, ph, pw;
+    long xq_off;
+    float xscale = 1.f;
+    int writer = -1;
 };
 
 struct Xform {
@@ -140,7 +149,8 @@ struct neo_plan {
     int8_t* d_i8 = nullptr;
     bool i8_ready = false;
     unsigned* d_absmax = nullptr;
-    bool i8_f32_out = false;  // calibration: a chained conv's first run writes float32
+    bool i8_f32_out = false;  // calibration: a writer's first run writes float32 only
+    std::vector<I8Copy> i8_copies;
     // split-reduction workspace shared by the conv steps (they run in order)
     size_t ws_bytes = 0;
     float* d_ws = nullptr;
@@ -495,7 +505,6 @@ int build_steps(neo_plan* P) {
                         return off;
                     };
                     st.w8_off = take((long)int8_filter_bytes(d.K, C, d.R, d.S));
-                    st.xq_off = take(xq);
                     st.c8 = choose_int8_config(st.cs);
                 }
                 st.cc = choose_conv_config(st.cs);
@@ -1002,36 +1011,56 @@ bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_ou
     return true;
 }
 
-// NEO_PLAN_INT8: a conv whose output value is read by nothing but one other
-// conv's input writes that output requantized into the consumer's int8 input
-// (with the consumer's scale and padding halo), and the consumer's
-// quantization pass is dropped.
-void chain_int8(neo_plan* P) {
+// NEO_PLAN_INT8: one int8 copy per (value, halo) that int8 convs read,
+// shared by all of them (one scale: the value's).  The conv producing the
+// value writes the copy from its epilogue when the value has one copy only
+// (every conv reading it has the same padding), beside its float32 output if
+// anything else reads that; otherwise the first conv to read the copy runs
+// its quantization pass.
+void plan_int8_copies(neo_plan* P) {
     const int ns = (int)P->steps.size();
     for (int i = 0; i < ns; ++i) {
-        Step& s = P->steps[i];
-        if (s.kind != ST_CONV || !s.i8) continue;
-        const int v = s.out;
-        if (P->vals[v].view || v == P->out_val || P->vals[v].buf < 0) continue;
-        bool other = false;
-        for (const Val& w : P->vals)
-            if (w.alias_of == v) other = true;
-        int reader = -1, uses = 0;
-        for (int j = 0; j < ns; ++j) {
-            const Step& t = P->steps[j];
-            if (t.in == v) {
-                ++uses;
-                reader = j;
-            }
-            if (t.res == v || t.out2 == v) other = true;
-            for (const Step& m : t.members)
-                if (m.in == v || m.res == v) other = true;
-        }
-        if (other || uses != 1 || reader <= i) continue;
-        Step& t = P->steps[reader];
+        Step& t = P->steps[i];
         if (t.kind != ST_CONV || !t.i8) continue;
-        s.q_next = reader;
-        t.q_by_prev = true;
+        int c = -1;
+        for (int k = 0; k < (int)P->i8_copies.size(); ++k) {
+            const I8Copy& q = P->i8_copies[k];
+            if (q.val == t.in && q.ph == t.cs.ph && q.pw == t.cs.pw) c = k;
+        }
+        if (c < 0) {
+            const Val& v = P->vals[t.in];
+            I8Copy q{t.in, t.cs.ph, t.cs.pw, P->i8_bytes};
+            P->i8_bytes += ((long)int8_act_bytes(v.N, v.C, v.H, v.W, t.cs.ph, t.cs.pw) + 255) / 256 * 256;
+            c = (int)P->i8_copies.size();
+            P->i8_copies.push_back(q);
+            t.quant_here = true;  // the first reader, unless a writer takes it over
+        }
+        t.qc = c;
+    }
+    for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
+        I8Copy& q = P->i8_copies[c];
+        int copies_of_val = 0;
+        for (const I8Copy& o : P->i8_copies) copies_of_val += o.val == q.val;
+        int w = -1;
+        for (int i = 0; i < ns; ++i)
+            if (P->steps[i].out == q.val && P->steps[i].kind == ST_CONV && P->steps[i].i8) w = i;
+        if (copies_of_val != 1 || w < 0) continue;
+        // the writer: does anything read its float32 output?
+        bool f32 = q.val == P->out_val || P->vals[q.val].view;
+        for (const Val& o : P->vals)
+            if (o.alias_of == q.val) f32 = true;
+        for (int i = 0; i < ns; ++i) {
+            const Step& t = P->steps[i];
+            if ((t.in == q.val && !(t.kind == ST_CONV && t.i8)) || t.res == q.val || t.out2 == q.val)
+                f32 = true;
+            for (const Step& m : t.members)
+                if (m.in == q.val || m.res == q.val) f32 = true;
+        }
+        q.writer = w;
+        P->steps[w].q_out = c;
+        P->steps[w].f32_needed = f32;
+        for (Step& t : P->steps)
+            if (t.qc == c) t.quant_here = false;
     }
 }
 
@@ -1091,11 +1120,12 @@ std::string describe(const neo_plan* P) {
               << ",\"algo\":\"" << (s.i8 ? "int8" : s.wino ? "winograd" : "direct") << "\"";
             if (s.i8) {
                 char xs[32];
-                std::snprintf(xs, sizeof xs, "%.9g", (double)s.xscale);
+                std::snprintf(xs, sizeof xs, "%.9g", (double)P->i8_copies[s.qc].xscale);
                 o << ",\"int8\":{\"tile\":[" << s.c8.fk << "," << s.c8.fp << "],\"waves\":" << s.c8.waves
                   << ",\"x_scale\":" << xs << ",\"calibrated\":" << (P->i8_ready ? "true" : "false")
-                  << ",\"writes_next_input\":" << (s.q_next >= 0 ? "true" : "false")
-                  << ",\"input_from_producer\":" << (s.q_by_prev ? "true" : "false") << "}";
+                  << ",\"input_copy\":" << s.qc << ",\"quantizes_input\":"
+                  << (s.quant_here ? "true" : "false") << ",\"writes_copy\":" << s.q_out
+                  << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false") << "}";
             }
             if (c.gap) o << ",\"gap_sums\":true";
             o << "}";
@@ -1394,7 +1424,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
-        if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) chain_int8(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) plan_int8_copies(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
@@ -1554,22 +1584,23 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
             }
             case ST_CONV:
                 if (s.i8) {
-                    // the fp32 input quantized with its halo (unless the
-                    // producer wrote it), then the integer conv, whose output
-                    // is either float32 or the next conv's int8 input
+                    // the input's int8 copy (quantized here by the first
+                    // reader, unless its producer wrote it), the integer conv,
+                    // its float32 output and/or the int8 copy it writes
                     const Val& in = P->vals[s.in];
-                    int8_t* xq = P->d_i8 + s.xq_off;
-                    if (!s.q_by_prev)
+                    const I8Copy& qc = P->i8_copies[s.qc];
+                    int8_t* xq = P->d_i8 + qc.xq_off;
+                    if (s.quant_here)
                         e = launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
-                                                 s.cs.ph, s.cs.pw, s.xscale, xq, st);
-                    const Step* nx = (s.q_next >= 0 && !P->i8_f32_out) ? &P->steps[s.q_next] : nullptr;
+                                                 qc.ph, qc.pw, qc.xscale, xq, st);
+                    const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
+                    float* y = (!qo || s.f32_needed) ? val_ptr(P, s.out, x_nchw, y_out) : nullptr;
                     if (e == hipSuccess)
-                        e = launch_conv_int8(s.cs, s.c8, xq, P->d_i8 + s.w8_off, prm + s.ws8_off, s.xscale,
+                        e = launch_conv_int8(s.cs, s.c8, xq, P->d_i8 + s.w8_off, prm + s.ws8_off, qc.xscale,
                                              s.b_off >= 0 ? prm + s.b_off : nullptr,
-                                             s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr,
-                                             nx ? nullptr : val_ptr(P, s.out, x_nchw, y_out), nullptr,
-                                             nx ? P->d_i8 + nx->xq_off : nullptr, nx ? nx->xscale : 1.f,
-                                             nx ? nx->cs.ph : 0, nx ? nx->cs.pw : 0, st);
+                                             s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr, y,
+                                             nullptr, qo ? P->d_i8 + qo->xq_off : nullptr,
+                                             qo ? qo->xscale : 1.f, qo ? qo->ph : 0, qo ? qo->pw : 0, st);
                     break;
                 }
                 if (s.wino) {
@@ -2015,19 +2046,20 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
     for (size_t i = 0; i < P->steps.size(); ++i) {
         Step& s = P->steps[i];
         int rc;
-        // the scale of an input quantized by its own pass: from that input
-        if (s.kind == ST_CONV && s.i8 && !s.q_by_prev &&
-            (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in), &s.xscale)) != NEO_OK)
+        // a copy quantized by its own pass: the scale of the value it reads
+        if (s.kind == ST_CONV && s.i8 && s.quant_here &&
+            (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in),
+                           &P->i8_copies[s.qc].xscale)) != NEO_OK)
             return rc;
-        if (s.kind == ST_CONV && s.i8 && s.q_next >= 0) {
-            // a chained producer: run it once with its float32 output, take
-            // the consumer's scale from that, then run it as the plan does
+        if (s.kind == ST_CONV && s.i8 && s.q_out >= 0) {
+            // a copy's writer: run it once with its float32 output only, take
+            // the copy's scale from that, then run it as the plan does
             P->i8_f32_out = true;
             rc = enqueue_step(P, s, x_nchw, y_out, st);
             P->i8_f32_out = false;
             if (rc != NEO_OK) return rc;
             if ((rc = scale_of(val_ptr(P, s.out, x_nchw, y_out), elems(s.out),
-                               &P->steps[s.q_next].xscale)) != NEO_OK)
+                               &P->i8_copies[s.q_out].xscale)) != NEO_OK)
                 return rc;
         }
         rc = enqueue_step(P, s, x_nchw, y_out, st);

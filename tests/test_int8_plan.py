@@ -4,7 +4,7 @@ neo_plan_calibrate_int8) against the oracle's integer network executor
 
 Every int8 layer's arithmetic is fixed exactly (quantization by float32
 division, or by the float32 reciprocal where the producing conv writes the
-input itself; exact integer sums; the float32 epilogue one rounding per
+input's int8 copy itself; exact integer sums; the float32 epilogue one rounding per
 operation; max pools exact), so on networks without average pooling the
 calibrated input scales of all convs must equal the oracle's bit for bit:
 each is the maximum of a tensor that both sides computed identically.  Only
@@ -28,10 +28,17 @@ def test_host_plan_and_flags():
     assert len(convs) == 53 and len(d["steps"]) == 57
     assert all(s["conv"]["algo"] == "int8" and not s["conv"]["int8"]["calibrated"] for s in convs)
     assert not any(s["kind"].startswith("conv_") for s in d["steps"])     # no fused steps
-    # the convs whose output only the next conv reads write its int8 input:
-    # the 1x1 reduce -> 3x3 -> 1x1 expand links of the 16 bottlenecks
-    assert sum(s["conv"]["int8"]["writes_next_input"] for s in convs) == 32
-    assert sum(s["conv"]["int8"]["input_from_producer"] for s in convs) == 32
+    # one int8 copy per (value, padding): 49 for 53 convs (each stage's input
+    # is shared by its reduce and projection convs); every conv output that
+    # convs read is written as a copy by its producer (47; 12 of them, the
+    # outputs of identity-shortcut blocks, also in float32 for the residual),
+    # so only the network input and the max pool's output are quantized by a
+    # pass of their own
+    q = [s["conv"]["int8"] for s in convs]
+    assert len({x["input_copy"] for x in q}) == 49
+    assert sum(x["quantizes_input"] for x in q) == 2
+    assert sum(x["writes_copy"] >= 0 for x in q) == 47
+    assert sum(x["writes_copy"] >= 0 and x["writes_f32"] for x in q) == 12
     L = neo.lib()
     FAKE = ctypes.c_void_p(1 << 20)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
