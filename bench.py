@@ -581,7 +581,7 @@ def model_latencies(neo, torch, wl, steps):
             # this input, untimed), graph replay; ResNet-50 and VGG-16 only,
             # the networks whose int8 parity is exact (no average pooling)
             t0 = time.perf_counter()
-            p = neo.Plan(g, flags=neo.PLAN_INT8 | neo.PLAN_HIPGRAPH)
+            p = neo.Plan(g, flags=neo.PLAN_INT8 | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
             out = p.calibrate_int8(x)
             t_plan = time.perf_counter() - t0
             ms = e2e_ms(torch, p, x, out, steps, 3)

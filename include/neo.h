@@ -455,8 +455,10 @@ enum neo_plan_flags {
      * reader runs the quantization pass.  Pools, concatenation, flatten and
      * dense stay float32.  The input scales come
      * from neo_plan_calibrate_int8, which must run before the plan does.
-     * Every conv is its own step in NCHW16c: block 16, and no NAIVE, TUNE,
-     * GLOBAL_SEARCH, fusion or WINOGRAD flag. */
+     * Every conv is its own step in NCHW16c: block 16, and no NAIVE,
+     * GLOBAL_SEARCH, fusion or WINOGRAD flag.  With NEO_PLAN_TUNE the local
+     * search times every int8 configuration of each conv (an "int8" line in
+     * the results file). */
     NEO_PLAN_INT8 = 2048
 };
 

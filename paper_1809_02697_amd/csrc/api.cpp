@@ -344,6 +344,7 @@ int conv_int8_common(const char* fn, const int8_t* xq, int N, int C, int H, int 
     if (((long)N * cdiv(C, 16) + 4) * (H + 2L * pad_h) * (W + 2L * pad_w) * 16 > kMaxElems)
         return fail(NEO_ERR_UNSUPPORTED, f + ": padded int8 input of 2 GiB or more");
     cfg = choose_int8_config(s);
+    if (!acc) (void)tuned_int8_config(s, yq ? 2 : 0, &cfg);
     env_i8_config(s, &cfg);
     hipError_t e = launch_conv_int8(s, cfg, xq, w_packed, w_scale, x_scale, bias, res, y, acc, yq,
                                     y_scale, y_pad_h, y_pad_w, (hipStream_t)stream);

@@ -118,6 +118,12 @@ hipError_t launch_wino(const ConvShape& s, const ConvConfig& c, const float* x, 
 int tune_wino(const ConvShape& s, const float* x, const float* u, const float* bias,
               const float* res, float* y, hipStream_t st, ConvConfig* best, float* us);
 bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
+// The same for the integer conv (configurations of int8_config_valid), keyed
+// also by its output mode `out` (0 float32, 2 int8, 3 both).
+int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
+              const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
+              hipStream_t st, ConvConfig* best, float* us);
+bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg);
 
 // Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations with
 // the convolution's zero padding stored as a halo, a

@@ -1403,13 +1403,13 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                             NEO_PLAN_WINOGRAD | NEO_PLAN_INT8))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & NEO_PLAN_INT8) &&
-        ((flags & (NEO_PLAN_NAIVE | NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP |
+        ((flags & (NEO_PLAN_NAIVE | NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP |
                    NEO_PLAN_FUSE_GAP | NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS |
                    NEO_PLAN_FUSE_POOL | NEO_PLAN_WINOGRAD)) ||
          block != 16))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: NEO_PLAN_INT8 plans every conv alone in "
-                                         "NCHW16c (block 16; no naive transforms, tuning, search, "
-                                         "fusion or Winograd)");
+                                         "NCHW16c (block 16; no naive transforms, search, fusion "
+                                         "or Winograd)");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
     if ((flags & NEO_PLAN_GLOBAL_SEARCH) && (flags & NEO_PLAN_NAIVE))
@@ -1424,7 +1424,15 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         rc = parse(P, nodes, n_nodes, true);
         if (rc == NEO_OK && (flags & NEO_PLAN_GLOBAL_SEARCH)) rc = search_schemes(P);
         if (rc == NEO_OK) rc = build_steps(P);
-        if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) plan_int8_copies(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) {
+            plan_int8_copies(P);
+            if (!(flags & NEO_PLAN_HOST_ONLY))
+                for (Step& st : P->steps)
+                    if (st.kind == ST_CONV && st.i8) {
+                        const int mode = st.q_out < 0 ? 0 : st.f32_needed ? 3 : 2;
+                        st.tuned = tuned_int8_config(st.cs, mode, &st.c8);
+                    }
+        }
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_PAIRS)) fuse_pairs(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
@@ -1914,6 +1922,19 @@ static int tune_plan(neo_plan* P) {
                 next.push_back(c);
                 next.push_back(pl);
             }
+            continue;
+        }
+        if (s.kind == ST_CONV && s.i8) {
+            // an integer conv: its configurations timed with its own output mode
+            const I8Copy* qo = s.q_out >= 0 ? &P->i8_copies[s.q_out] : nullptr;
+            rc = tune_int8(s.cs, P->d_i8 + P->i8_copies[s.qc].xq_off, P->d_i8 + s.w8_off,
+                           P->d_params + s.ws8_off, s.b_off >= 0 ? P->d_params + s.b_off : nullptr,
+                           s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
+                           (!qo || s.f32_needed) ? val_ptr(P, s.out, xin, yout) : nullptr,
+                           qo ? P->d_i8 + qo->xq_off : nullptr, qo ? qo->ph : 0, qo ? qo->pw : 0,
+                           P->cap_stream, &s.c8, nullptr);
+            s.tuned = rc == NEO_OK;
+            next.push_back(s);
             continue;
         }
         // (a conv the Winograd kernel could run is compared even when its

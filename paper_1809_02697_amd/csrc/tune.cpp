@@ -122,6 +122,8 @@ struct PoolEntry {
 std::map<GroupKey, PoolEntry> g_convpool_db;  // a stem conv and its max pool in one launch
 std::map<GroupKey, Entry> g_wino_db;          // a 3x3 conv by Winograd F(2x2, 3x3)
 constexpr int kWinoInts = 7;                  // N C H W K ph pw
+std::map<GroupKey, Entry> g_i8_db;            // an integer conv, by output mode
+constexpr int kI8Ints = 12;                   // N C H W K R S sh sw ph pw out
 constexpr int kConvPoolInts = 13 + 12;        // conv N C H W K R S sh sw ph pw xb act, pool ints
 constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
@@ -248,6 +250,69 @@ int tune_wino(const ConvShape& s, const float* x, const float* u, const float* b
     {
         std::lock_guard<std::mutex> lk(g_mu);
         g_wino_db[key] = Entry{best, best_us};
+    }
+    *best_out = best;
+    if (us_out) *us_out = best_us;
+    return NEO_OK;
+}
+
+namespace {
+GroupKey i8_key(const ConvShape& s, int out) {
+    return {device_arch(), {s.N, s.C, s.H, s.W, s.K, s.R, s.S, s.sh, s.sw, s.ph, s.pw, out}};
+}
+}  // namespace
+
+bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg) {
+    const GroupKey key = i8_key(s, out);
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_i8_db.find(key);
+    if (it == g_i8_db.end() || !int8_config_valid(s, it->second.cfg)) return false;
+    *cfg = it->second.cfg;
+    return true;
+}
+
+// Every valid integer-conv configuration, timed with the caller's buffers
+// (their contents do not change the time); keeps the fastest with its time.
+int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
+              const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
+              hipStream_t st, ConvConfig* best_out, float* us_out) {
+    const int out = yq ? (y ? 3 : 2) : 0;
+    const GroupKey key = i8_key(s, out);
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_i8_db.find(key);
+        if (it != g_i8_db.end() && int8_config_valid(s, it->second.cfg)) {
+            *best_out = it->second.cfg;
+            if (us_out) *us_out = it->second.us;
+            return NEO_OK;
+        }
+    }
+    ConvConfig best = choose_int8_config(s);
+    float best_us = 1e30f;
+    hipError_t e = hipSuccess;
+    {
+        Events ev;
+        for (int fk : {1, 2, 4})
+            for (int fp : {1, 2, 4})
+                for (int wv : {1, 2, 4}) {
+                    const ConvConfig c{fk, fp, 1, wv};
+                    if (!int8_config_valid(s, c)) continue;
+                    float us = 0.f;
+                    e = time_launch([&] { return launch_conv_int8(s, c, x, w, wscale, 1.f, bias, res, y,
+                                                                  nullptr, yq, 1.f, qph, qpw, st); },
+                                    st, ev.e0, ev.e1, &us);
+                    if (e != hipSuccess) break;
+                    if (us < best_us) {
+                        best_us = us;
+                        best = c;
+                    }
+                }
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "int8 tuning");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_i8_db[key] = Entry{best, best_us};
     }
     *best_out = best;
     if (us_out) *us_out = best_us;
@@ -460,8 +525,10 @@ extern "C" {
 // one line per stem conv with its max pooling in one launch:
 //   convpool arch N C H W K R S sh sw ph pw xb act (max N C H W R S sh sw ph pw xb)
 //            fk fp waves ty tx us
-// and one line per 3x3 stride-1 conv by Winograd F(2x2, 3x3):
+// one line per 3x3 stride-1 conv by Winograd F(2x2, 3x3):
 //   wino arch N C H W K ph pw fk fp split waves us
+// and one line per integer conv (out: 0 float32, 2 int8, 3 both outputs):
+//   int8 arch N C H W K R S sh sw ph pw out fk fp waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -512,8 +579,14 @@ int neo_tune_db_save(const char* path) {
         const ConvConfig& c = kv.second.cfg;
         f << ' ' << c.fk << ' ' << c.fp << ' ' << c.split << ' ' << c.waves << ' ' << kv.second.us << '\n';
     }
+    for (const auto& kv : g_i8_db) {
+        f << "int8 " << kv.first.first;
+        for (int x : kv.first.second) f << ' ' << x;
+        const ConvConfig& c = kv.second.cfg;
+        f << ' ' << c.fk << ' ' << c.fp << ' ' << c.waves << ' ' << kv.second.us << '\n';
+    }
     return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                     g_chain_db.size() + g_convpool_db.size() + g_wino_db.size())
+                     g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -527,7 +600,7 @@ int neo_tune_db_load(const char* path) {
     std::map<GroupKey, Entry> add_group;
     std::map<GroupKey, float> add_pool, add_pair, add_chain;
     std::map<GroupKey, PoolEntry> add_convpool;
-    std::map<GroupKey, Entry> add_wino;
+    std::map<GroupKey, Entry> add_wino, add_i8;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -624,6 +697,29 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 5, "int8 ") == 0) {
+            std::string tag;
+            GroupKey ik;
+            v.cfg.split = 1;
+            bool ok = (bool)(is >> tag >> ik.first) && read_ints(is, kI8Ints, ik.second) &&
+                      (bool)(is >> v.cfg.fk >> v.cfg.fp >> v.cfg.waves >> v.us);
+            if (ok) {  // the entry must name a configuration the kernel takes for its shape
+                const std::vector<int>& q = ik.second;
+                ok = q[0] > 0 && q[1] > 0 && q[2] > 0 && q[3] > 0 && q[4] > 0 && q[5] > 0 && q[6] > 0 &&
+                     q[7] > 0 && q[8] > 0 && q[9] >= 0 && q[10] >= 0 &&
+                     (q[11] == 0 || q[11] == 2 || q[11] == 3);
+                if (ok) {
+                    const int OH = (q[2] + 2 * q[9] - q[5]) / q[7] + 1, OW = (q[3] + 2 * q[10] - q[6]) / q[8] + 1;
+                    ConvShape cs{q[0], q[1], q[2], q[3], q[4], q[5], q[6], q[7], q[8], q[9], q[10],
+                                 OH, OW, 0, 0, 0};
+                    ok = OH > 0 && OW > 0 && int8_config_valid(cs, v.cfg);
+                }
+            }
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_i8[ik] = v;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -652,6 +748,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add_chain) g_chain_db[kv.first] = kv.second;
     for (const auto& kv : add_convpool) g_convpool_db[kv.first] = kv.second;
     for (const auto& kv : add_wino) g_wino_db[kv.first] = kv.second;
+    for (const auto& kv : add_i8) g_i8_db[kv.first] = kv.second;
     return n;
 }
 
@@ -664,12 +761,13 @@ void neo_tune_db_clear(void) {
     g_chain_db.clear();
     g_convpool_db.clear();
     g_wino_db.clear();
+    g_i8_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                 g_chain_db.size() + g_convpool_db.size() + g_wino_db.size());
+                 g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size());
 }
 
 }  // extern "C"

@@ -44,7 +44,7 @@ def test_host_plan_and_flags():
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
     p.destroy()
     for extra in (neo.PLAN_GROUP, neo.PLAN_FUSE_PAIRS, neo.PLAN_WINOGRAD, neo.PLAN_NAIVE,
-                  neo.PLAN_GLOBAL_SEARCH, neo.PLAN_TUNE):
+                  neo.PLAN_GLOBAL_SEARCH):
         with pytest.raises(RuntimeError, match="NEO_PLAN_INT8"):
             neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8 | extra)
     with pytest.raises(RuntimeError, match="NEO_PLAN_INT8"):
@@ -121,6 +121,27 @@ def test_int8_network_against_the_oracle(gpu, name, N):
 
 
 @pytest.mark.gpu
+def test_tuned_int8_plan_gives_the_same_bits(gpu):
+    """The local search picks other tiles and wave splits; the integer sums
+    are exact and the epilogue the same, so the output is bit-identical."""
+    from gpu_util import dev, host
+    g = wl.resnet50(1)
+    _, y, _, p = run_int8_plan(gpu, g)
+    p.destroy()
+    pt = gpu.Plan(g, flags=gpu.PLAN_INT8 | gpu.PLAN_TUNE | gpu.PLAN_HIPGRAPH)
+    d = pt.describe()
+    assert all(s["conv"]["tuned"] for s in d["steps"] if s["kind"] == "conv")
+    tiles = {tuple(s["conv"]["int8"]["tile"]) + (s["conv"]["int8"]["waves"],)
+             for s in d["steps"] if s["kind"] == "conv"}
+    x = dev(g.x)
+    pt.calibrate_int8(x)
+    yt = host(pt.run(x))
+    pt.destroy()
+    print(f"\n[int8 plan] tuned: {len(tiles)} distinct configurations")
+    np.testing.assert_array_equal(yt, y)
+
+
+@pytest.mark.gpu
 def test_int8_plan_runs_only_after_calibration(gpu):
     from gpu_util import dev
     g = wl.vgg_like_tiny()
@@ -149,3 +170,27 @@ def test_recalibration_on_another_input(gpu):
     assert not np.array_equal(y_a, y_b)
     from gpu_util import assert_close_network
     assert_close_network(y_b, ref_b.reshape(y_b.shape), "recalibrated")
+
+
+def test_results_file_int8_lines(tmp_path):
+    """An "int8" line of the results file loads (and is saved back) when it
+    names a configuration the kernel takes for its shape; others are refused."""
+    neo.tune_db_clear()
+    arch = "gfx950"
+    good = tmp_path / "good.txt"
+    good.write_text(f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 0 4 2 1 12.5\n"
+                    f"int8 {arch} 32 256 14 14 256 3 3 1 1 1 1 3 2 4 2 11.25\n")
+    assert neo.tune_db_load(str(good)) == 2 and neo.tune_db_size() == 2
+    out = tmp_path / "saved.txt"
+    neo.tune_db_save(str(out))
+    assert sorted(l for l in out.read_text().splitlines() if l.startswith("int8 ")) == \
+        sorted(good.read_text().splitlines())
+    for bad in (f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 0 3 2 1 12.5",     # no 3-block tile
+                f"int8 {arch} 1 64 56 56 48 3 3 1 1 1 1 0 4 2 1 12.5",     # 3 blocks: fk 4 does not divide
+                f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 1 4 2 1 12.5",     # output mode 1
+                f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 0 4 2 8 12.5"):    # 8 waves
+        f = tmp_path / "bad.txt"
+        f.write_text(bad + "\n")
+        with pytest.raises(RuntimeError, match="malformed"):
+            neo.tune_db_load(str(f))
+    neo.tune_db_clear()
