@@ -16,6 +16,9 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // Thread index t = (((n * CB + cb) * OH + oh) * OW + ow) * (x / 4) + quad, for
 // t < (N * CB * OH * OW) << lq (lq = log2(x / 4)).  Taps outside the input are
 // skipped (max: as if padded with -inf; average: divided by the taps inside).
+// The average sums in double, row by row, and rounds once to float32 after
+// the division: the result is the exact mean rounded, whatever the hardware
+// (the float32 sum of the same taps could differ in its last bit).
 // With a compile-time KR x KS window every tap's load is issued before any is
 // used: a tap outside the input loads pixel (0, 0) of the block and is
 // discarded by a select, so the loads of one output are in flight together;
@@ -40,6 +43,7 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
         acc = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
     else
         acc = v4f{0.f, 0.f, 0.f, 0.f};
+    double dacc[4] = {0.0, 0.0, 0.0, 0.0};
     int cnt = 0;
     if constexpr (KR > 0) {
         v4f v[KR][KS];
@@ -61,7 +65,8 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
 #pragma unroll
                     for (int i = 0; i < 4; ++i) acc[i] = v[r][c][i] > acc[i] ? v[r][c][i] : acc[i];
                 } else {
-                    acc += v[r][c];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) dacc[i] += (double)v[r][c][i];
                 }
                 ++cnt;
             }
@@ -77,16 +82,17 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
 #pragma unroll
                     for (int i = 0; i < 4; ++i) acc[i] = v[i] > acc[i] ? v[i] : acc[i];
                 } else {
-                    acc += v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) dacc[i] += (double)v[i];
                 }
                 ++cnt;
             }
         }
     }
     if (!MAX) {
-        const float d = (float)cnt;
+        const double d = (double)cnt;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
+        for (int i = 0; i < 4; ++i) acc[i] = (float)(dacc[i] / d);
     }
     *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X + 4 * q) = acc;
 }

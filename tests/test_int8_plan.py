@@ -5,11 +5,12 @@ neo_plan_calibrate_int8) against the oracle's integer network executor
 Every int8 layer's arithmetic is fixed exactly (quantization by float32
 division, or by the float32 reciprocal where the producing conv writes the
 input's int8 copy itself; exact integer sums; the float32 epilogue one rounding per
-operation; max pools exact), so on networks without average pooling the
-calibrated input scales of all convs must equal the oracle's bit for bit:
-each is the maximum of a tensor that both sides computed identically.  Only
-the global average pool and the dense layers that follow the last conv sum
-floats in different orders, so the logits are held to the network tolerance."""
+operation; max pools exact; average pools the exact mean rounded once), so
+the calibrated input scales of all convs must equal the oracle's bit for
+bit: each is the maximum of a tensor that both sides computed identically.
+Only the global average pool and the dense layers that follow the last conv
+sum floats in different orders, so the logits are held to the network
+tolerance."""
 import ctypes
 
 import numpy as np
@@ -84,7 +85,8 @@ def run_int8_plan(gpu, g, flags=0):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("name,N", [("vgg_tiny", 2), ("resnet50", 1), ("resnet50", 2), ("vgg16", 1)])
+@pytest.mark.parametrize("name,N", [("vgg_tiny", 2), ("resnet50", 1), ("resnet50", 2), ("vgg16", 1),
+                                    ("inception_v3", 1)])
 def test_int8_network_against_the_oracle(gpu, name, N):
     """All conv input scales bit-exact against the oracle's integer network;
     the logits within the network tolerance of the oracle's (top-1 equal);
