@@ -433,6 +433,8 @@ hipError_t by_tile(const ConvConfig& c, const I8Args& a, hipStream_t st) {
     if (c.fk == 4 && c.fp == 2) return by_waves<4, 2, MODE>(c.waves, a, st);
     if (c.fk == 2 && c.fp == 4) return by_waves<2, 4, MODE>(c.waves, a, st);
     if (c.fk == 4 && c.fp == 4) return by_waves<4, 4, MODE>(c.waves, a, st);
+    if (c.fk == 8 && c.fp == 2) return by_waves<8, 2, MODE>(c.waves, a, st);
+    if (c.fk == 8 && c.fp == 4) return by_waves<8, 4, MODE>(c.waves, a, st);
     return hipErrorInvalidValue;
 }
 
@@ -445,7 +447,7 @@ size_t int8_filter_bytes(int K, int C, int R, int S) {
 bool int8_config_valid(const ConvShape& s, const ConvConfig& c) {
     const int KB = cdiv(s.K, 16);
     const bool tile = (c.fk == 1 && (c.fp == 1 || c.fp == 2)) || (c.fk == 2 && c.fp <= 4 && c.fp != 3) ||
-                      (c.fk == 4 && (c.fp == 2 || c.fp == 4));
+                      ((c.fk == 4 || c.fk == 8) && (c.fp == 2 || c.fp == 4));
     return tile && KB % c.fk == 0 && c.split == 1 && (c.waves == 1 || c.waves == 2 || c.waves == 4) &&
            s.R * s.S * cdiv(s.C, 64) >= c.waves;
 }

@@ -292,7 +292,7 @@ int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float*
     hipError_t e = hipSuccess;
     {
         Events ev;
-        for (int fk : {1, 2, 4})
+        for (int fk : {1, 2, 4, 8})
             for (int fp : {1, 2, 4})
                 for (int wv : {1, 2, 4}) {
                     const ConvConfig c{fk, fp, 1, wv};

@@ -319,6 +319,29 @@ def test_every_configuration(gpu, cfg, monkeypatch):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("cfg", ["8,2,1", "8,2,4", "8,4,1", "8,4,2"])
+def test_eight_block_tiles(gpu, cfg, monkeypatch):
+    """The 8-output-block tiles (K a multiple of 128): a 1x1 over four channel
+    groups and a 3x3 with a ragged pixel tile and residual + ReLU, the sums
+    and both outputs against the oracle (the configuration is checked to be
+    one the kernel takes, so the override is not silently ignored)."""
+    from gpu_util import host
+    fk, fp, wv = map(int, cfg.split(","))
+    monkeypatch.setenv("NEO_I8_CONFIG", cfg)
+    for C, R, H, N in [(200, 1, 9, 2), (80, 3, 13, 1)]:
+        c = wl.conv_case(C, 128, R, R, 1, R // 2, H, H, N=N, epilogue="res", with_bn=False,
+                         out_hw=(H, H))
+        assert R * R * -(-C // 64) >= wv and 8 % fk == 0
+        xs = act_scale(c.x)
+        acc, want, mag, y32 = oracle_int8(c, xs)
+        assert_acc_equal(host(run_int8(gpu, c, xs, raw=True)), acc, 128, cfg)
+        assert_dequant_close(orc.from_blocked(host(run_int8(gpu, c, xs)), 128), want, mag, cfg, y32)
+        ys = act_scale(y32)
+        np.testing.assert_array_equal(host(run_int8_q(gpu, c, xs, ys, (1, 1))),
+                                      requant_ref(y32, ys, 128, (1, 1)), err_msg=cfg)
+
+
+@pytest.mark.gpu
 @pytest.mark.parametrize("lid", ["R01", "R03", "R08", "R11", "R19", "R23"])
 def test_resnet50_layers_batch32_sampled(gpu, lid):
     """ResNet-50 layers at batch 32 in the launch configuration the library
