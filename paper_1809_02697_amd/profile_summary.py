@@ -461,7 +461,10 @@ def write_int8(run_dir):
           "Each of the 23 distinct ResNet-50 conv shapes at batch 32 through the integer path "
           "(int8 input with its halo, packed int8 filter, float32 output with the layer's residual "
           "and ReLU), in the launch configuration the library chooses.  Duration: median over the "
-          "profiled rounds (the first dropped) of the kernel-trace timestamps.  Traffic: FETCH_SIZE "
+          "profiled rounds (the first dropped) of the kernel-trace timestamps; the layers run "
+          "round-robin, so each one's operands have left the 256 MB MALL by its turn (the bench "
+          "line's layer table replays one layer back to back, warm, and measures less on the "
+          "layers with large outputs).  Traffic: FETCH_SIZE "
           "and WRITE_SIZE (KiB per dispatch) scaled by the same counters on a plain copy of "
           f"{COPY_MB} MB (factors {ff:.3f} and {fw:.3f}), warm caches, against the algorithmic "
           "bytes (int8 input and filter once, float32 output and residual).  MFMA utilisation: "
