@@ -455,10 +455,16 @@ enum neo_plan_flags {
      * reader runs the quantization pass.  Pools, concatenation, flatten and
      * dense stay float32.  The input scales come
      * from neo_plan_calibrate_int8, which must run before the plan does.
-     * Every conv is its own step in NCHW16c: block 16, and no NAIVE,
-     * GLOBAL_SEARCH, fusion or WINOGRAD flag.  With NEO_PLAN_TUNE the local
-     * search times every int8 configuration of each conv (an "int8" line in
-     * the results file). */
+     * Convs run in NCHW16c: block 16, and no NAIVE, GLOBAL_SEARCH, WINOGRAD
+     * or fusion flag other than NEO_PLAN_GROUP, which puts independent int8
+     * convs (and a pooling step) in one launch, as for float32 (one int8
+     * configuration for all members; their quantization passes run before
+     * the launch, each copy's at its first reader in the grouped order; the
+     * results are those of the convs alone, bit for bit).  With
+     * NEO_PLAN_TUNE the local search times every int8 configuration of each
+     * conv ("int8" lines in the results file) and of each group ("i8group"
+     * lines), keeping a group, its convs in one launch with the pool alone,
+     * or every conv alone, whichever measures fastest. */
     NEO_PLAN_INT8 = 2048
 };
 
@@ -537,7 +543,10 @@ void neo_plan_destroy(neo_plan* plan);
  * the pair's time in one launch; (GPU architecture, the shapes of a 3x3-led chain of two
  * or three convs, residual) -> the chain's time in one launch; (GPU architecture, a stem
  * conv's and its max pooling's shapes) -> the fused launch's configuration and time;
- * (GPU architecture, a 3x3 stride-1 conv's shape) -> its Winograd configuration and time.
+ * (GPU architecture, a 3x3 stride-1 conv's shape) -> its Winograd configuration and time;
+ * (GPU architecture, an integer conv's shape and output mode) -> its int8 configuration and
+ * time; (GPU architecture, the shapes and output modes of a launch's integer convs and its
+ * pooling step) -> the launch's int8 configuration and time.
  * Text file, one entry per line.  save returns the number of entries
  * written, load the number read, size the number held (entries are merged; a malformed
  * line fails the whole load with NEO_ERR_INVALID_ARG). */

@@ -120,21 +120,18 @@ __device__ __forceinline__ void load_step(const __amdgpu_buffer_rsrc_t xr, const
 
 // Output modes: the float32 epilogue, the raw int32 sums, the float32
 // epilogue requantized to int8 into the next layer's halo'd input, or both
-// the float32 output and its requantized copy.
-constexpr int kOutF32 = 0, kOutAcc = 1, kOutI8 = 2, kOutBoth = 3;
+// the float32 output and its requantized copy; kOutDyn (group launches,
+// whose members differ) writes whichever of y and yq is not null.
+constexpr int kOutF32 = 0, kOutAcc = 1, kOutI8 = 2, kOutBoth = 3, kOutDyn = 4;
 
+// One output tile u (channel tile kt, pixel tile pxt, pixel tiles fastest)
+// of the convolution a, by all WAVES waves of the workgroup (wave: this
+// wave's index, uniform; lane: its lane).
 template <int FK, int FP, int WAVES, int MODE>
-__global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+__device__ __forceinline__ void i8_tile(const I8Args& a, const int u, const int wave, const int lane) {
     const int li = lane & 15, g = lane >> 4;
     const int ohw = a.OH * a.OW;
     const int plane = a.Hp * a.Wp * 16;  // bytes per channel-block plane
-    // Output tiles u = first, first + grid, ...: a workgroup runs several in
-    // turn, so the stores of one drain while the next one loads and
-    // multiplies.  Pixel tiles fastest in each XCD's contiguous run (as the
-    // fp32 kernel below its large-launch threshold).
-    for (int u = __builtin_amdgcn_readfirstlane(xcd_order()); u < a.ntiles; u += gridDim.x) {
     const int kt = fdiv(u, a.div_npx);
     const int pxt = u - kt * a.npx;
 
@@ -248,7 +245,7 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
         }
         // the partners may overwrite red for the next tile once wave 0 has it
         __syncthreads();
-        if (wave != 0) continue;
+        if (wave != 0) return;
     }
 
     if constexpr (MODE == kOutAcc) {
@@ -259,8 +256,10 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
             for (int p = 0; p < FP; ++p)
                 if (pv[p]) *reinterpret_cast<v4i*>(a.acc + obase[p] + kofs) = acc[f][p];
         }
-        continue;
+        return;
     }
+    const bool out_f32 = MODE == kOutF32 || MODE == kOutBoth || (MODE == kOutDyn && a.y);
+    const bool out_i8 = MODE == kOutI8 || MODE == kOutBoth || (MODE == kOutDyn && a.yq);
     const bool relu = a.act == NEO_ACT_RELU;
     const int yofs = a.y_off * ohw * 16;
     const int qplane = (a.OH + 2 * a.qph) * (a.OW + 2 * a.qpw);  // one block of the int8 copy
@@ -290,9 +289,8 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) o[v] = o[v] > 0.f ? o[v] : 0.f;
             }
-            if constexpr (MODE == kOutF32 || MODE == kOutBoth)
-                *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
-            if constexpr (MODE == kOutI8 || MODE == kOutBoth) {
+            if (out_f32) *reinterpret_cast<v4f*>(a.y + ybase[p] + yofs + kofs) = o;
+            if (out_i8) {
                 // clamp(round_half_even(y * (1 / s_y)), -127, 127), four
                 // channels packed into one 4-byte store
                 unsigned packed = 0;
@@ -310,7 +308,55 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
             }
         }
     }
+}
+
+// Output tiles u = first, first + grid, ...: a workgroup runs several in
+// turn, so the stores of one drain while the next one loads and multiplies.
+// Pixel tiles fastest in each XCD's contiguous run (as the fp32 kernel below
+// its large-launch threshold).
+template <int FK, int FP, int WAVES, int MODE>
+__global__ __launch_bounds__(WAVES * 64) void conv_i8(I8Args a) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int u = __builtin_amdgcn_readfirstlane(xcd_order()); u < a.ntiles; u += gridDim.x)
+        i8_tile<FK, FP, WAVES, MODE>(a, u, wave, lane);
+}
+
+// Several independent integer convolutions in one launch (the float32 group
+// launch's scheme, for batch 1, where each alone is too small to fill the
+// chip): member m owns workgroups [start[m], start[m + 1]), a whole number of
+// rounds over the XCDs, one tile per workgroup (cnt[m] real, the rest exit),
+// its tiles in a launch of its own's per-XCD order.  Members share the tile
+// and wave count and may differ in their outputs.  A pooling step may ride
+// along in the workgroups past the convs' (the pooling kernel's arithmetic).
+constexpr int kMaxI8Group = 4;
+struct I8GroupArgs {
+    I8Args a[kMaxI8Group];
+    int start[kMaxI8Group + 1];
+    int cnt[kMaxI8Group];
+    int n;
+    conv_detail::PoolPart pool;
+};
+
+template <int FK, int FP, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void conv_i8_group(I8GroupArgs ga) {
+    const int nconv = ga.start[ga.n];
+    if ((int)blockIdx.x >= nconv) {
+        using conv_detail::pool_part_run;
+        const int wg = blockIdx.x - nconv;
+        if (ga.pool.max)
+            ga.pool.k33 ? pool_part_run<true, 3>(ga.pool, wg) : pool_part_run<true, 0>(ga.pool, wg);
+        else
+            ga.pool.k33 ? pool_part_run<false, 3>(ga.pool, wg) : pool_part_run<false, 0>(ga.pool, wg);
+        return;
     }
+    int m = 0;
+    while (m + 1 < ga.n && (int)blockIdx.x >= ga.start[m + 1]) ++m;
+    m = __builtin_amdgcn_readfirstlane(m);
+    const int b = blockIdx.x - ga.start[m];
+    if (b >= ga.cnt[m]) return;
+    i8_tile<FK, FP, WAVES, kOutDyn>(ga.a[m], xcd_order(b, ga.cnt[m]),
+                                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), threadIdx.x & 63);
 }
 
 // fp32 NCHW16c [N][CB][H][W][16] -> int8 NCHW16c with a zero halo
@@ -438,6 +484,79 @@ hipError_t by_tile(const ConvConfig& c, const I8Args& a, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
+template <int FK, int FP>
+hipError_t group_by_waves(int waves, const I8GroupArgs& ga, int wgs, hipStream_t st) {
+    switch (waves) {
+        case 1: hipLaunchKernelGGL((conv_i8_group<FK, FP, 1>), dim3(wgs), dim3(64), 0, st, ga); break;
+        case 2: hipLaunchKernelGGL((conv_i8_group<FK, FP, 2>), dim3(wgs), dim3(128), 0, st, ga); break;
+        case 4: hipLaunchKernelGGL((conv_i8_group<FK, FP, 4>), dim3(wgs), dim3(256), 0, st, ga); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t group_by_tile(const ConvConfig& c, const I8GroupArgs& ga, int wgs, hipStream_t st) {
+    if (c.fk == 1 && c.fp == 1) return group_by_waves<1, 1>(c.waves, ga, wgs, st);
+    if (c.fk == 1 && c.fp == 2) return group_by_waves<1, 2>(c.waves, ga, wgs, st);
+    if (c.fk == 2 && c.fp == 1) return group_by_waves<2, 1>(c.waves, ga, wgs, st);
+    if (c.fk == 2 && c.fp == 2) return group_by_waves<2, 2>(c.waves, ga, wgs, st);
+    if (c.fk == 4 && c.fp == 2) return group_by_waves<4, 2>(c.waves, ga, wgs, st);
+    if (c.fk == 2 && c.fp == 4) return group_by_waves<2, 4>(c.waves, ga, wgs, st);
+    if (c.fk == 4 && c.fp == 4) return group_by_waves<4, 4>(c.waves, ga, wgs, st);
+    if (c.fk == 8 && c.fp == 2) return group_by_waves<8, 2>(c.waves, ga, wgs, st);
+    if (c.fk == 8 && c.fp == 4) return group_by_waves<8, 4>(c.waves, ga, wgs, st);
+    return hipErrorInvalidValue;
+}
+
+// The kernel arguments of one integer conv (its shape, launch
+// configuration, operands and outputs).
+I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
+                    const float* wscale, float xscale, const float* bias, const float* res, float* y,
+                    int* acc, int8_t* yq, float yscale, int qph, int qpw) {
+    I8Args a;
+    a.x = x;
+    a.w = w;
+    a.wscale = wscale;
+    a.xscale = xscale;
+    a.bias = bias;
+    a.res = res;
+    a.y = y;
+    a.acc = acc;
+    a.yq = yq;
+    a.yrcp = yq ? 1.0f / yscale : 0.f;
+    a.qph = qph;
+    a.qpw = qpw;
+    // the int8 output takes the view of s when it is the only output; beside
+    // the float32 output it is a whole tensor of its own
+    a.q_off = y ? 0 : s.y_off;
+    a.q_tot = y ? cdiv(s.K, 16) : s.y_tot;
+    a.N = s.N;
+    a.CB = cdiv(s.C, 16);
+    a.CG = cdiv(s.C, 64);
+    a.Hp = s.H + 2 * s.ph;
+    a.Wp = s.W + 2 * s.pw;
+    a.KB = cdiv(s.K, 16);
+    a.S = s.S;
+    a.sh = s.sh;
+    a.sw = s.sw;
+    a.OH = s.OH;
+    a.OW = s.OW;
+    a.M = s.N * s.OH * s.OW;
+    a.y_off = s.y_off;
+    a.y_tot = s.y_tot;
+    a.act = s.act;
+    a.T = s.R * s.S * a.CG;
+    a.npx = cdiv(a.M, 16 * c.fp);
+    a.nkt = a.KB / c.fk;
+    a.ntiles = a.npx * a.nkt;
+    a.x_bytes = (int)int8_act_bytes(s.N, s.C, s.H, s.W, s.ph, s.pw);
+    a.w_bytes = (int)int8_filter_bytes(s.K, s.C, s.R, s.S);
+    a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
+    a.div_ow = make_fastdiv((unsigned)s.OW);
+    a.div_npx = make_fastdiv((unsigned)a.npx);
+    return a;
+}
+
 }  // namespace
 
 size_t int8_filter_bytes(int K, int C, int R, int S) {
@@ -505,50 +624,92 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
                             float* y, int* acc, int8_t* yq, float yscale, int qph, int qpw,
                             hipStream_t st) {
     if (!int8_config_valid(s, c)) return hipErrorInvalidValue;
-    I8Args a;
-    a.x = x;
-    a.w = w;
-    a.wscale = wscale;
-    a.xscale = xscale;
-    a.bias = bias;
-    a.res = res;
-    a.y = y;
-    a.acc = acc;
-    a.yq = yq;
-    a.yrcp = yq ? 1.0f / yscale : 0.f;
-    a.qph = qph;
-    a.qpw = qpw;
-    // the int8 output takes the view of s when it is the only output; beside
-    // the float32 output it is a whole tensor of its own
-    a.q_off = y ? 0 : s.y_off;
-    a.q_tot = y ? cdiv(s.K, 16) : s.y_tot;
-    a.N = s.N;
-    a.CB = cdiv(s.C, 16);
-    a.CG = cdiv(s.C, 64);
-    a.Hp = s.H + 2 * s.ph;
-    a.Wp = s.W + 2 * s.pw;
-    a.KB = cdiv(s.K, 16);
-    a.S = s.S;
-    a.sh = s.sh;
-    a.sw = s.sw;
-    a.OH = s.OH;
-    a.OW = s.OW;
-    a.M = s.N * s.OH * s.OW;
-    a.y_off = s.y_off;
-    a.y_tot = s.y_tot;
-    a.act = s.act;
-    a.T = s.R * s.S * a.CG;
-    a.npx = cdiv(a.M, 16 * c.fp);
-    a.nkt = a.KB / c.fk;
-    a.ntiles = a.npx * a.nkt;
-    a.x_bytes = (int)int8_act_bytes(s.N, s.C, s.H, s.W, s.ph, s.pw);
-    a.w_bytes = (int)int8_filter_bytes(s.K, s.C, s.R, s.S);
-    a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
-    a.div_ow = make_fastdiv((unsigned)s.OW);
-    a.div_npx = make_fastdiv((unsigned)a.npx);
+    const I8Args a = make_i8_args(s, c, x, w, wscale, xscale, bias, res, y, acc, yq, yscale, qph, qpw);
     if (acc) return by_tile<kOutAcc>(c, a, st);
     if (yq) return y ? by_tile<kOutBoth>(c, a, st) : by_tile<kOutI8>(c, a, st);
     return by_tile<kOutF32>(c, a, st);
+}
+
+static_assert(kMaxI8Group == kMaxGroupConvs, "group size");
+
+bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c) {
+    if (n < 1 || n > kMaxGroupConvs) return false;
+    for (int i = 0; i < n; ++i)
+        if (!int8_config_valid(s[i], c)) return false;
+    return true;
+}
+
+// The largest register tile (then the most waves) for which the members'
+// tiles together still give every SIMD work, as for a single conv.
+ConvConfig choose_int8_group_config(const ConvShape* s, int n) {
+    static const ConvConfig order[] = {{4, 4, 1, 1}, {2, 4, 1, 1}, {4, 2, 1, 1}, {2, 2, 1, 1},
+                                       {2, 1, 1, 1}, {1, 2, 1, 1}, {1, 1, 1, 1}};
+    for (const ConvConfig& c0 : order) {
+        long tiles = 0;
+        for (int i = 0; i < n; ++i)
+            tiles += (long)cdiv(cdiv(s[i].N * s[i].OH * s[i].OW, 16), c0.fp) * (cdiv(s[i].K, 16) / c0.fk);
+        for (int wv : {1, 2, 4}) {
+            const ConvConfig c{c0.fk, c0.fp, 1, wv};
+            if (int8_group_config_valid(s, n, c) && tiles * wv >= 1024) return c;
+        }
+    }
+    for (int wv : {4, 2, 1}) {
+        const ConvConfig c{1, 1, 1, wv};
+        if (int8_group_config_valid(s, n, c)) return c;
+    }
+    return ConvConfig{1, 1, 1, 1};
+}
+
+hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& c, const GroupPool* pool,
+                                  hipStream_t st) {
+    ConvShape shp[kMaxGroupConvs];
+    for (int i = 0; i < n && i < kMaxGroupConvs; ++i) shp[i] = mem[i].s;
+    if (!int8_group_config_valid(shp, n, c)) return hipErrorInvalidValue;
+    if (pool && pool->s.xb != 16) return hipErrorInvalidValue;
+    I8GroupArgs ga;
+    ga.n = n;
+    ga.start[0] = 0;
+    // dispatch order: the members with the most reduction steps first (they
+    // finish last), ties in the given order
+    int order[kMaxI8Group];
+    for (int i = 0; i < n; ++i) order[i] = i;
+    auto steps = [&](int i) { return shp[i].R * shp[i].S * cdiv(shp[i].C, 64); };
+    std::stable_sort(order, order + n, [&](int p, int q) { return steps(p) > steps(q); });
+    long total_wgs = 0;
+    for (int j = 0; j < n; ++j) {
+        const I8Member& m = mem[order[j]];
+        if (!m.y && !m.yq) return hipErrorInvalidValue;
+        ga.a[j] = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
+                               m.yscale, m.qph, m.qpw);
+        ga.cnt[j] = ga.a[j].ntiles;
+        total_wgs += (long)cdiv(ga.cnt[j], conv_detail::kXcds) * conv_detail::kXcds;
+        if (total_wgs >= (1L << 30)) return hipErrorInvalidValue;
+        ga.start[j + 1] = ga.start[j] + cdiv(ga.cnt[j], conv_detail::kXcds) * conv_detail::kXcds;
+    }
+    for (int i = n; i < kMaxI8Group; ++i) {
+        ga.a[i] = ga.a[n - 1];
+        ga.cnt[i] = 0;
+        ga.start[i + 1] = ga.start[n];
+    }
+    conv_detail::PoolPart& pp = ga.pool;
+    pp = conv_detail::PoolPart{};
+    if (pool) {
+        const PoolShape& ps = pool->s;
+        pp.x = pool->x;
+        pp.y = pool->y;
+        pp.s = ps;
+        pp.CB = cdiv(ps.C, ps.xb);
+        pp.lq = 2;  // log2(16 / 4): four channel quads per 16-channel block
+        const long total = ((long)ps.N * pp.CB * ps.OH * ps.OW) << pp.lq;
+        if (total >= (1L << 31)) return hipErrorInvalidValue;
+        pp.total = (int)total;
+        pp.max = pool->max ? 1 : 0;
+        pp.k33 = ps.R == 3 && ps.S == 3;
+        // one output quad per thread, at most 1024 workgroups (then grid-stride)
+        const long per = 64L * c.waves;
+        pp.wgs = (int)std::min<long>(1024, std::max<long>(1, (total + per - 1) / per));
+    }
+    return group_by_tile(c, ga, ga.start[n] + pp.wgs, st);
 }
 
 }  // namespace neo

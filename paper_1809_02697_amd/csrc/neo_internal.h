@@ -190,6 +190,32 @@ hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, con
                              const float* const* w, const float* const* bias,
                              const float* const* res, float* const* y, const GroupPool* pool,
                              hipStream_t st);
+// Several independent integer convolutions in one launch: each member's
+// operands and outputs as for launch_conv_int8 (y and/or yq; no raw sums),
+// one configuration valid for every member; pool (may be null, block 16)
+// runs in extra workgroups of the launch.
+struct I8Member {
+    ConvShape s;
+    const int8_t* x;
+    const int8_t* w;
+    const float* wscale;
+    float xscale;
+    const float* bias;
+    const float* res;
+    float* y;
+    int8_t* yq;
+    float yscale;
+    int qph, qpw;
+};
+bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);
+ConvConfig choose_int8_group_config(const ConvShape* s, int n);
+hipError_t launch_conv_int8_group(const I8Member* m, int n, const ConvConfig& c, const GroupPool* pool,
+                                  hipStream_t st);
+// Local search over the configurations valid for every member of an integer
+// group (with its pool, if any), keyed by the members' shapes and output
+// modes (0 float32, 2 int8, 3 both) and the pool.
+int tune_int8_group(const I8Member* m, int n, const GroupPool* pool, hipStream_t st, ConvConfig* best,
+                    float* us);
 // Local search over the configurations valid for every member of a group
 // (with its pool, if any); results are kept per group of workloads.
 int tune_conv_group(const ConvShape* s, int n, const float* const* x, const float* const* w,

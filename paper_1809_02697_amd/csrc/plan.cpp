@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <mutex>
 #include <queue>
@@ -757,7 +758,7 @@ void group_ready_convs(neo_plan* P) {
             if (ok) ready.push_back(j);
         }
         for (int j : ready) {
-            if (S[j].kind == ST_CONV && conv_group_eligible(S[j].cs))
+            if (S[j].kind == ST_CONV && (S[j].i8 || conv_group_eligible(S[j].cs)))
                 convs.push_back(j);
             else if (pools_ride && (S[j].kind == ST_MAXPOOL || S[j].kind == ST_AVGPOOL))
                 pools.push_back(j);
@@ -780,6 +781,18 @@ void group_ready_convs(neo_plan* P) {
             for (size_t m = k; m < e; ++m) grp.members.push_back(S[convs[m]]);
             std::vector<ConvShape> shp;
             for (const Step& m : grp.members) shp.push_back(m.cs);
+            if (grp.members[0].i8) {
+                // integer convs (an int8 plan has no others): one int8
+                // configuration for all members
+                grp.i8 = true;
+                grp.c8 = choose_int8_group_config(shp.data(), (int)shp.size());
+                for (Step& m : grp.members) {
+                    m.c8 = grp.c8;
+                    m.tuned = false;
+                }
+                out.push_back(grp);
+                continue;
+            }
             grp.cc = choose_group_config(shp.data(), (int)shp.size());
             // launch-configuration sweeps: "fk,fp,waves" for every group it suits
             if (const char* ev = std::getenv("NEO_GROUP_CONFIG")) {
@@ -1064,6 +1077,24 @@ void plan_int8_copies(neo_plan* P) {
     }
 }
 
+// NEO_PLAN_INT8 with NEO_PLAN_GROUP: grouping reorders the steps, so the
+// quantization pass of a copy that no conv writes moves to the copy's first
+// reader in the new order (a group runs its members' passes before its
+// launch, so readers in the same launch see the copy complete).
+void place_int8_quant_passes(neo_plan* P) {
+    std::vector<char> seen(P->i8_copies.size(), 0);
+    auto visit = [&](Step& t) {
+        if (t.kind != ST_CONV || !t.i8) return;
+        const bool first = P->i8_copies[t.qc].writer < 0 && !seen[t.qc];
+        t.quant_here = first;
+        seen[t.qc] = 1;
+    };
+    for (Step& t : P->steps) {
+        visit(t);
+        for (Step& m : t.members) visit(m);
+    }
+}
+
 std::string describe(const neo_plan* P) {
     std::ostringstream o;
     auto lay = [](int l) { return l ? "NCHW" + std::to_string(l) + "c" : std::string("NCHW"); };
@@ -1135,8 +1166,10 @@ std::string describe(const neo_plan* P) {
             conv_json(s);
         }
         if (s.kind == ST_CONV_GROUP) {
-            o << ",\"tile\":[" << s.cc.fk << "," << s.cc.fp << "],\"waves\":" << s.cc.waves
-              << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"members\":[";
+            const ConvConfig& gc = s.i8 ? s.c8 : s.cc;
+            o << ",\"tile\":[" << gc.fk << "," << gc.fp << "],\"waves\":" << gc.waves
+              << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"algo\":\""
+              << (s.i8 ? "int8" : "direct") << "\",\"members\":[";
             for (size_t m = 0; m < s.members.size(); ++m) {
                 const Step& ms = s.members[m];
                 o << (m ? "," : "") << "{\"node\":" << ms.node << ",\"in\":" << ms.in
@@ -1403,13 +1436,13 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                             NEO_PLAN_WINOGRAD | NEO_PLAN_INT8))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: unknown flags");
     if ((flags & NEO_PLAN_INT8) &&
-        ((flags & (NEO_PLAN_NAIVE | NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_GROUP |
-                   NEO_PLAN_FUSE_GAP | NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS |
-                   NEO_PLAN_FUSE_POOL | NEO_PLAN_WINOGRAD)) ||
+        ((flags & (NEO_PLAN_NAIVE | NEO_PLAN_GLOBAL_SEARCH | NEO_PLAN_FUSE_GAP |
+                   NEO_PLAN_FUSE_PAIRS | NEO_PLAN_FUSE_CHAINS | NEO_PLAN_FUSE_POOL |
+                   NEO_PLAN_WINOGRAD)) ||
          block != 16))
-        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: NEO_PLAN_INT8 plans every conv alone in "
-                                         "NCHW16c (block 16; no naive transforms, search, fusion "
-                                         "or Winograd)");
+        return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: NEO_PLAN_INT8 plans its convs in NCHW16c "
+                                         "(block 16; no naive transforms, search, fusion other "
+                                         "than NEO_PLAN_GROUP, or Winograd)");
     if ((flags & (NEO_PLAN_TUNE | NEO_PLAN_GLOBAL_SEARCH)) && (flags & NEO_PLAN_HOST_ONLY))
         return fail(NEO_ERR_INVALID_ARG, "neo_plan_create: tuning and search need a device plan");
     if ((flags & NEO_PLAN_GLOBAL_SEARCH) && (flags & NEO_PLAN_NAIVE))
@@ -1438,6 +1471,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_CHAINS)) fuse_chains(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_POOL)) fuse_conv_pool(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_GROUP)) group_ready_convs(P);
+        if (rc == NEO_OK && (flags & NEO_PLAN_GROUP) && (flags & NEO_PLAN_INT8)) place_int8_quant_passes(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_WINOGRAD) && !(flags & NEO_PLAN_TUNE)) {
             // untuned, the convs still launched alone run the Winograd kernel
             // (with NEO_PLAN_TUNE the local search decides, conv by conv)
@@ -1488,11 +1522,17 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
             // are never written again
             if (e == hipSuccess) e = hipMemset(P->d_i8, 0, std::max<long>(P->i8_bytes, 256));
             if (e == hipSuccess) e = hipMalloc(&P->d_absmax, 256);
-            for (const Step& st : P->steps)
+            // (every integer conv: the steps' and the group launches' members)
+            auto pack = [&](const Step& st) {
                 if (e == hipSuccess && st.kind == ST_CONV && st.i8)
                     e = launch_pack_filter_int8(P->d_params + st.kcrs_off, st.cs.K, st.cs.C, st.cs.R,
                                                 st.cs.S, P->d_i8 + st.w8_off, P->d_params + st.ws8_off,
                                                 nullptr);
+            };
+            for (const Step& st : P->steps) {
+                pack(st);
+                for (const Step& m : st.members) pack(m);
+            }
             if (e == hipSuccess) e = hipDeviceSynchronize();
             if (e != hipSuccess) {
                 if (P->d_i8) (void)hipFree(P->d_i8);
@@ -1575,6 +1615,37 @@ int neo_plan_conv_params(const neo_plan* plan, int node_id, float* w_packed, flo
     return fail(NEO_ERR_INVALID_ARG, "neo_plan_conv_params: node is not a conv of this plan");
 }
 
+// An integer conv step's operands and outputs (its input's int8 copy, the
+// packed filter and scales, the float32 output and/or the copy it writes).
+static I8Member i8_member(const neo_plan* P, const Step& s, const float* x_nchw, float* y_out) {
+    const I8Copy& qc = P->i8_copies[s.qc];
+    const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
+    I8Member m;
+    m.s = s.cs;
+    m.x = P->d_i8 + qc.xq_off;
+    m.w = P->d_i8 + s.w8_off;
+    m.wscale = P->d_params + s.ws8_off;
+    m.xscale = qc.xscale;
+    m.bias = s.b_off >= 0 ? P->d_params + s.b_off : nullptr;
+    m.res = s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr;
+    m.y = (!qo || s.f32_needed) ? val_ptr(P, s.out, x_nchw, y_out) : nullptr;
+    m.yq = qo ? P->d_i8 + qo->xq_off : nullptr;
+    m.yscale = qo ? qo->xscale : 1.f;
+    m.qph = qo ? qo->ph : 0;
+    m.qpw = qo ? qo->pw : 0;
+    return m;
+}
+
+// The quantization pass of an integer conv step's input copy, if it runs it.
+static hipError_t i8_quant_pass(const neo_plan* P, const Step& s, const float* x_nchw, float* y_out,
+                                hipStream_t st) {
+    if (!s.quant_here) return hipSuccess;
+    const Val& in = P->vals[s.in];
+    const I8Copy& qc = P->i8_copies[s.qc];
+    return launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W, qc.ph, qc.pw,
+                                qc.xscale, P->d_i8 + qc.xq_off, st);
+}
+
 static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* y_out,
                         hipStream_t st) {
     {
@@ -1624,10 +1695,22 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                                   val_ptr(P, s.out, x_nchw, y_out), P->d_ws, st);
                 break;
             case ST_CONV_GROUP: {
+                const int n = (int)s.members.size();
+                GroupPool gp;
+                const bool has_pool = group_pool(P, s, x_nchw, y_out, &gp);
+                if (s.i8) {
+                    // the members' quantization passes, then one launch
+                    I8Member mem[kMaxGroupConvs];
+                    for (int m = 0; m < n && e == hipSuccess; ++m) {
+                        e = i8_quant_pass(P, s.members[m], x_nchw, y_out, st);
+                        mem[m] = i8_member(P, s.members[m], x_nchw, y_out);
+                    }
+                    if (e == hipSuccess) e = launch_conv_int8_group(mem, n, s.c8, has_pool ? &gp : nullptr, st);
+                    break;
+                }
                 ConvShape shp[kMaxGroupConvs];
                 const float *xs[kMaxGroupConvs], *ws[kMaxGroupConvs], *bs[kMaxGroupConvs], *rs[kMaxGroupConvs];
                 float* ys[kMaxGroupConvs];
-                const int n = (int)s.members.size();
                 for (int m = 0; m < n; ++m) {
                     const Step& ms = s.members[m];
                     shp[m] = ms.cs;
@@ -1637,8 +1720,6 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     rs[m] = ms.res >= 0 ? val_ptr(P, ms.res, x_nchw, y_out) : nullptr;
                     ys[m] = val_ptr(P, ms.out, x_nchw, y_out);
                 }
-                GroupPool gp;
-                const bool has_pool = group_pool(P, s, x_nchw, y_out, &gp);
                 e = launch_conv_group(shp, n, s.cc, xs, ws, bs, rs, ys, has_pool ? &gp : nullptr, st);
                 break;
             }
@@ -1772,6 +1853,57 @@ static int tune_plan(neo_plan* P) {
     std::vector<Step> next;
     for (Step& s : P->steps) {
         if (rc != NEO_OK) break;
+        if (s.kind == ST_CONV_GROUP && s.i8 && !s.tuned) {
+            // integer convs: the group (with its pool), the group with the
+            // pool alone, or every conv alone (each in its own output mode)
+            const int n = (int)s.members.size();
+            I8Member mem[kMaxGroupConvs];
+            for (int m = 0; m < n; ++m) mem[m] = i8_member(P, s.members[m], xin, yout);
+            GroupPool gp;
+            const bool has_pool = group_pool(P, s, xin, yout, &gp);
+            float fused_us = 0.f, split_us = 0.f, alone_us = 0.f, pool_us = 0.f;
+            ConvConfig fused_cc = s.c8, split_cc = s.c8;
+            rc = tune_int8_group(mem, n, has_pool ? &gp : nullptr, P->cap_stream, &fused_cc, &fused_us);
+            if (rc == NEO_OK && has_pool) rc = tune_pool(gp, P->cap_stream, &pool_us);
+            if (rc == NEO_OK && has_pool && n > 1)
+                rc = tune_int8_group(mem, n, nullptr, P->cap_stream, &split_cc, &split_us);
+            ConvConfig own[kMaxGroupConvs];
+            for (int m = 0; m < n && rc == NEO_OK; ++m) {
+                float us = 0.f;
+                const I8Member& q = mem[m];
+                rc = tune_int8(q.s, q.x, q.w, q.wscale, q.bias, q.res, q.y, q.yq, q.qph, q.qpw, P->cap_stream,
+                               &own[m], &us);
+                alone_us += us;
+            }
+            if (rc != NEO_OK) break;
+            alone_us += pool_us;
+            split_us += pool_us;
+            const bool split_ok = has_pool && n > 1;
+            Step keep = s;
+            keep.tuned = true;
+            if (fused_us < alone_us && (!split_ok || fused_us <= split_us)) {
+                keep.c8 = fused_cc;
+            } else if (split_ok && split_us < alone_us) {
+                next.push_back(s.pools[0]);
+                keep.pools.clear();
+                keep.c8 = split_cc;
+            } else {
+                if (has_pool) next.push_back(s.pools[0]);
+                for (int m = 0; m < n; ++m) {
+                    Step ms = s.members[m];
+                    ms.c8 = own[m];
+                    ms.tuned = true;
+                    next.push_back(ms);
+                }
+                continue;
+            }
+            for (Step& ms : keep.members) {
+                ms.c8 = keep.c8;
+                ms.tuned = true;
+            }
+            next.push_back(keep);
+            continue;
+        }
         if (s.kind == ST_CONV_GROUP && !s.tuned) {
             ConvShape shp[kMaxGroupConvs];
             const float *xs[kMaxGroupConvs], *ws[kMaxGroupConvs], *bs[kMaxGroupConvs], *rs[kMaxGroupConvs];
@@ -1965,6 +2097,9 @@ static int tune_plan(neo_plan* P) {
         next.push_back(s);
     }
     if (rc == NEO_OK) P->steps.swap(next);
+    // groups the search split up: their convs' quantization passes again at
+    // each copy's first reader
+    if (rc == NEO_OK && (P->flags & NEO_PLAN_INT8)) place_int8_quant_passes(P);
     if (xin) (void)hipFree(xin);
     if (yout) (void)hipFree(yout);
     return rc;
@@ -2064,8 +2199,22 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
         const Val& a = P->vals[v];
         return (long)a.N * cdiv(a.C, 16) * 16 * a.H * a.W;
     };
-    for (size_t i = 0; i < P->steps.size(); ++i) {
-        Step& s = P->steps[i];
+    // one step as the calibration runs it: a group's members (and its pool)
+    // one by one, which computes what the group launch does
+    std::function<int(const Step&)> calibrate_step = [&](const Step& s) -> int {
+        if (s.kind == ST_CONV_GROUP && s.i8) {
+            for (const Step& m : s.members) {
+                Step one = m;
+                one.c8 = s.c8;
+                const int rc = calibrate_step(one);
+                if (rc != NEO_OK) return rc;
+            }
+            for (const Step& pl : s.pools) {
+                const int rc = enqueue_step(P, pl, x_nchw, y_out, st);
+                if (rc != NEO_OK) return rc;
+            }
+            return NEO_OK;
+        }
         int rc;
         // a copy quantized by its own pass: the scale of the value it reads
         if (s.kind == ST_CONV && s.i8 && s.quant_here &&
@@ -2083,7 +2232,10 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
                                &P->i8_copies[s.q_out].xscale)) != NEO_OK)
                 return rc;
         }
-        rc = enqueue_step(P, s, x_nchw, y_out, st);
+        return enqueue_step(P, s, x_nchw, y_out, st);
+    };
+    for (const Step& s : P->steps) {
+        const int rc = calibrate_step(s);
         if (rc != NEO_OK) return rc;
     }
     hipError_t e = hipStreamSynchronize(st);

@@ -124,6 +124,7 @@ std::map<GroupKey, Entry> g_wino_db;          // a 3x3 conv by Winograd F(2x2, 3
 constexpr int kWinoInts = 7;                  // N C H W K ph pw
 std::map<GroupKey, Entry> g_i8_db;            // an integer conv, by output mode
 constexpr int kI8Ints = 12;                   // N C H W K R S sh sw ph pw out
+std::map<GroupKey, Entry> g_i8group_db;       // integer convs (and a pool) in one launch
 constexpr int kConvPoolInts = 13 + 12;        // conv N C H W K R S sh sw ph pw xb act, pool ints
 constexpr int kPairInts = 23;         // both convs' N C H W K R S sh sw ph pw, residual
 constexpr int kGroupShapeInts = 11;  // N C H W K R S sh sw ph pw per member
@@ -313,6 +314,76 @@ int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float*
     {
         std::lock_guard<std::mutex> lk(g_mu);
         g_i8_db[key] = Entry{best, best_us};
+    }
+    *best_out = best;
+    if (us_out) *us_out = best_us;
+    return NEO_OK;
+}
+
+namespace {
+// the shape of an integer conv from its key ints (N C H W K R S sh sw ph pw
+// ...), or false when they name no convolution
+bool i8_shape(const int* q, ConvShape* cs) {
+    if (!(q[0] > 0 && q[1] > 0 && q[2] > 0 && q[3] > 0 && q[4] > 0 && q[5] > 0 && q[6] > 0 && q[7] > 0 &&
+          q[8] > 0 && q[9] >= 0 && q[10] >= 0))
+        return false;
+    const int OH = (q[2] + 2 * q[9] - q[5]) / q[7] + 1, OW = (q[3] + 2 * q[10] - q[6]) / q[8] + 1;
+    *cs = ConvShape{q[0], q[1], q[2], q[3], q[4], q[5], q[6], q[7], q[8], q[9], q[10], OH, OW, 0, 0, 0};
+    return OH > 0 && OW > 0;
+}
+}  // namespace
+
+// Every configuration valid for all members of an integer group, timed with
+// the caller's buffers; keeps the fastest with its time.
+int tune_int8_group(const I8Member* m, int n, const GroupPool* pool, hipStream_t st, ConvConfig* best_out,
+                    float* us_out) {
+    // key: n, m (0 or 1 pools), the members' shapes and output modes, the pool's
+    if (n < 1 || n > kMaxGroupConvs) return fail(NEO_ERR_INVALID_ARG, "int8 group tuning: 1 to 4 members");
+    GroupKey key{device_arch(), {n, pool ? 1 : 0}};
+    ConvShape shp[kMaxGroupConvs];
+    for (int i = 0; i < n; ++i) {
+        const ConvShape& c = m[i].s;
+        shp[i] = c;
+        const int out = m[i].yq ? (m[i].y ? 3 : 2) : 0;
+        key.second.insert(key.second.end(), {c.N, c.C, c.H, c.W, c.K, c.R, c.S, c.sh, c.sw, c.ph, c.pw, out});
+    }
+    if (pool) {
+        const std::vector<int> pi = pool_ints(*pool);
+        key.second.insert(key.second.end(), pi.begin(), pi.end());
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_i8group_db.find(key);
+        if (it != g_i8group_db.end() && int8_group_config_valid(shp, n, it->second.cfg)) {
+            *best_out = it->second.cfg;
+            if (us_out) *us_out = it->second.us;
+            return NEO_OK;
+        }
+    }
+    ConvConfig best = choose_int8_group_config(shp, n);
+    float best_us = 1e30f;
+    hipError_t e = hipSuccess;
+    {
+        Events ev;
+        for (int fk : {1, 2, 4, 8})
+            for (int fp : {1, 2, 4})
+                for (int wv : {1, 2, 4}) {
+                    const ConvConfig c{fk, fp, 1, wv};
+                    if (e != hipSuccess || !int8_group_config_valid(shp, n, c)) continue;
+                    float us = 0.f;
+                    e = time_launch([&] { return launch_conv_int8_group(m, n, c, pool, st); }, st, ev.e0,
+                                    ev.e1, &us);
+                    if (e == hipSuccess && us < best_us) {
+                        best_us = us;
+                        best = c;
+                    }
+                }
+        (void)hipStreamSynchronize(st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "int8 group tuning");
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_i8group_db[key] = Entry{best, best_us};
     }
     *best_out = best;
     if (us_out) *us_out = best_us;
@@ -527,8 +598,11 @@ extern "C" {
 //            fk fp waves ty tx us
 // one line per 3x3 stride-1 conv by Winograd F(2x2, 3x3):
 //   wino arch N C H W K ph pw fk fp split waves us
-// and one line per integer conv (out: 0 float32, 2 int8, 3 both outputs):
+// one line per integer conv (out: 0 float32, 2 int8, 3 both outputs):
 //   int8 arch N C H W K R S sh sw ph pw out fk fp waves us
+// and one line per launch of n integer convs and m (0 or 1) pooling steps:
+//   i8group arch n m (N C H W K R S sh sw ph pw out) x n (max N C H W R S sh sw ph pw xb) x m
+//           fk fp waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
     std::ofstream f(path);
@@ -585,8 +659,15 @@ int neo_tune_db_save(const char* path) {
         const ConvConfig& c = kv.second.cfg;
         f << ' ' << c.fk << ' ' << c.fp << ' ' << c.waves << ' ' << kv.second.us << '\n';
     }
+    for (const auto& kv : g_i8group_db) {
+        f << "i8group " << kv.first.first;  // the key's ints start with n and m
+        for (int x : kv.first.second) f << ' ' << x;
+        const ConvConfig& c = kv.second.cfg;
+        f << ' ' << c.fk << ' ' << c.fp << ' ' << c.waves << ' ' << kv.second.us << '\n';
+    }
     return f ? (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                     g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size())
+                     g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size() +
+                     g_i8group_db.size())
              : fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: write failed");
 }
 
@@ -600,7 +681,7 @@ int neo_tune_db_load(const char* path) {
     std::map<GroupKey, Entry> add_group;
     std::map<GroupKey, float> add_pool, add_pair, add_chain;
     std::map<GroupKey, PoolEntry> add_convpool;
-    std::map<GroupKey, Entry> add_wino, add_i8;
+    std::map<GroupKey, Entry> add_wino, add_i8, add_i8group;
     auto read_ints = [](std::istringstream& is, int count, std::vector<int>& out) {
         for (int i = 0; i < count; ++i) {
             int x = 0;
@@ -720,6 +801,30 @@ int neo_tune_db_load(const char* path) {
             ++n;
             continue;
         }
+        if (line.compare(0, 8, "i8group ") == 0) {
+            std::string tag;
+            GroupKey gk;
+            int members = 0, pools = -1;
+            v.cfg.split = 1;
+            bool ok = (bool)(is >> tag >> gk.first >> members >> pools) && members >= 1 &&
+                      members <= kMaxGroupConvs && (pools == 0 || pools == 1);
+            if (ok) {
+                gk.second = {members, pools};
+                ok = read_ints(is, members * kI8Ints + pools * kPoolShapeInts, gk.second) &&
+                     (bool)(is >> v.cfg.fk >> v.cfg.fp >> v.cfg.waves >> v.us);
+            }
+            ConvShape shp[kMaxGroupConvs];
+            for (int i = 0; ok && i < members; ++i) {
+                const int* q = gk.second.data() + 2 + i * kI8Ints;
+                ok = i8_shape(q, &shp[i]) && (q[11] == 0 || q[11] == 2 || q[11] == 3);
+            }
+            // the pool rides in blocks of 16 only
+            ok = ok && (pools == 0 || gk.second.back() == 16) && int8_group_config_valid(shp, members, v.cfg);
+            if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
+            add_i8group[gk] = v;
+            ++n;
+            continue;
+        }
         if (line.compare(0, 5, "pool ") == 0) {
             std::string tag;
             GroupKey pk;
@@ -749,6 +854,7 @@ int neo_tune_db_load(const char* path) {
     for (const auto& kv : add_convpool) g_convpool_db[kv.first] = kv.second;
     for (const auto& kv : add_wino) g_wino_db[kv.first] = kv.second;
     for (const auto& kv : add_i8) g_i8_db[kv.first] = kv.second;
+    for (const auto& kv : add_i8group) g_i8group_db[kv.first] = kv.second;
     return n;
 }
 
@@ -762,12 +868,14 @@ void neo_tune_db_clear(void) {
     g_convpool_db.clear();
     g_wino_db.clear();
     g_i8_db.clear();
+    g_i8group_db.clear();
 }
 
 int neo_tune_db_size(void) {
     std::lock_guard<std::mutex> lk(g_mu);
     return (int)(g_db.size() + g_group_db.size() + g_pool_db.size() + g_pair_db.size() +
-                 g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size());
+                 g_chain_db.size() + g_convpool_db.size() + g_wino_db.size() + g_i8_db.size() +
+                 g_i8group_db.size());
 }
 
 }  // extern "C"

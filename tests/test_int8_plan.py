@@ -44,8 +44,7 @@ def test_host_plan_and_flags():
     FAKE = ctypes.c_void_p(1 << 20)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
     p.destroy()
-    for extra in (neo.PLAN_GROUP, neo.PLAN_FUSE_PAIRS, neo.PLAN_WINOGRAD, neo.PLAN_NAIVE,
-                  neo.PLAN_GLOBAL_SEARCH):
+    for extra in (neo.PLAN_FUSE_PAIRS, neo.PLAN_WINOGRAD, neo.PLAN_NAIVE, neo.PLAN_GLOBAL_SEARCH):
         with pytest.raises(RuntimeError, match="NEO_PLAN_INT8"):
             neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8 | extra)
     with pytest.raises(RuntimeError, match="NEO_PLAN_INT8"):
@@ -54,6 +53,60 @@ def test_host_plan_and_flags():
     p = neo.Plan(wl.tiny_graph(), flags=neo.PLAN_HOST_ONLY)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7
     p.destroy()
+
+
+def conv_steps(d):
+    """(step index, conv description) of every conv, group members included."""
+    out = []
+    for i, s in enumerate(d["steps"]):
+        if s["kind"] == "conv":
+            out.append((i, s["conv"]))
+        elif s["kind"] == "conv_group":
+            out.extend((i, m["conv"]) for m in s["members"])
+    return out
+
+
+@pytest.mark.parametrize("name", ["resnet50", "inception_v3"])
+def test_host_grouped_int8_plan(name):
+    """NEO_PLAN_INT8 | NEO_PLAN_GROUP: independent integer convs share
+    launches (pools ride along), every conv is still planned once, and each
+    copy that no conv writes is quantized once, by its first reader in the
+    grouped order (members of one launch count as one position: the launch
+    runs its members' passes first)."""
+    g = wl.MODELS[name](1)
+    p0 = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)
+    d0 = p0.describe()
+    p0.destroy()
+    p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8 | neo.PLAN_GROUP)
+    d = p.describe()
+    p.destroy()
+    cs = conv_steps(d)
+    assert sorted(c["int8"]["input_copy"] for _, c in cs) == sorted(s["conv"]["int8"]["input_copy"]
+                                                                  for s in d0["steps"] if s["kind"] == "conv")
+    groups = [s for s in d["steps"] if s["kind"] == "conv_group"]
+    assert groups and all(s["algo"] == "int8" and 2 <= len(s["members"]) + ("pool" in s) for s in groups)
+    for s in groups:
+        assert all(m["conv"]["int8"]["tile"] == s["tile"] and m["conv"]["int8"]["waves"] == s["waves"]
+                   for m in s["members"])
+    # the same copies are written by the same convs; passes only where no conv writes
+    writers = {c["int8"]["writes_copy"] for _, c in cs if c["int8"]["writes_copy"] >= 0}
+    first = {}
+    for i, c in cs:
+        first.setdefault(c["int8"]["input_copy"], i)
+    for i, c in cs:
+        q = c["int8"]["input_copy"]
+        want = q not in writers and i == first[q]
+        if c["int8"]["quantizes_input"]:
+            assert want
+    passes = [c["int8"]["input_copy"] for _, c in cs if c["int8"]["quantizes_input"]]
+    assert len(passes) == len(set(passes)) == len({c["int8"]["input_copy"] for _, c in cs} - writers)
+    n_launch = len(d["steps"]) + len(passes)
+    n_launch0 = len(d0["steps"]) + sum(s["conv"]["int8"]["quantizes_input"] for s in d0["steps"]
+                                       if s["kind"] == "conv")
+    print(f"\n[int8 group] {name}: {n_launch0} -> {n_launch} launches, {len(groups)} groups")
+    assert n_launch < n_launch0
+    if name == "inception_v3":
+        assert len(groups) == 27 and sum("pool" in s for s in groups) == 11 and len(passes) == 30
 
 
 # ---- GPU -------------------------------------------------------------------------------------
@@ -66,9 +119,13 @@ def gpu():
 
 
 def plan_scales(d):
-    """{conv node id: its calibrated input scale} from a plan description."""
-    return {s["node"]: np.float32(s["conv"]["int8"]["x_scale"]) for s in d["steps"]
-            if s["kind"] == "conv"}
+    """{conv node id: its calibrated input scale} from a plan description
+    (group members included)."""
+    out = {}
+    for s in d["steps"]:
+        for m in [s] if s["kind"] == "conv" else s.get("members", []) if s["kind"] == "conv_group" else []:
+            out[m["node"]] = np.float32(m["conv"]["int8"]["x_scale"])
+    return out
 
 
 def run_int8_plan(gpu, g, flags=0):
@@ -79,7 +136,7 @@ def run_int8_plan(gpu, g, flags=0):
     x = dev(g.x)
     y_cal = host(p.calibrate_int8(x))
     d = p.describe()
-    assert all(s["conv"]["int8"]["calibrated"] for s in d["steps"] if s["kind"] == "conv")
+    assert all(c["int8"]["calibrated"] for _, c in conv_steps(d))
     y = host(p.run(x))
     return y_cal, y, plan_scales(d), p
 
@@ -144,6 +201,37 @@ def test_tuned_int8_plan_gives_the_same_bits(gpu):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("name,N", [("vgg_tiny", 2), ("resnet50", 1), ("inception_v3", 1),
+                                    ("inception_v3", 2)])
+def test_grouped_int8_plan_gives_the_same_bits(gpu, name, N):
+    """Convs in one launch compute what they compute alone (exact sums, the
+    same epilogue, the pools' own arithmetic), so the grouped plan's scales
+    equal the oracle's and its outputs the ungrouped plan's, bit for bit;
+    graph replays too; the tuned grouped plan (groups kept, split or
+    dissolved by the local search) as well."""
+    from gpu_util import dev, host
+    g = wl.vgg_like_tiny(N=N) if name == "vgg_tiny" else wl.MODELS[name](N)
+    print(f"\n[int8 group] {name} N={N}", flush=True)
+    _, y, scales, p = run_int8_plan(gpu, g)
+    p.destroy()
+    for flags in (gpu.PLAN_GROUP | gpu.PLAN_HIPGRAPH, gpu.PLAN_GROUP | gpu.PLAN_TUNE | gpu.PLAN_HIPGRAPH):
+        y_cal, yg, sg, pg = run_int8_plan(gpu, g, flags)
+        d = pg.describe()
+        yr = host(pg.run(dev(g.x)))
+        pg.destroy()
+        n_groups = sum(s["kind"] == "conv_group" for s in d["steps"])
+        print(f"[int8 group] flags {flags}: {n_groups} groups, {len(d['steps'])} steps", flush=True)
+        assert sg == scales
+        np.testing.assert_array_equal(yg, y)
+        np.testing.assert_array_equal(y_cal, y)
+        np.testing.assert_array_equal(yr, y)
+    if name != "vgg_tiny":
+        _, ref_scales = oq.run_graph_int8(g)
+        np.testing.assert_array_equal(np.array([scales[i] for i in g.node_ids("conv")], np.float32),
+                                      ref_scales)
+
+
+@pytest.mark.gpu
 def test_int8_plan_runs_only_after_calibration(gpu):
     from gpu_util import dev
     g = wl.vgg_like_tiny()
@@ -191,6 +279,36 @@ def test_results_file_int8_lines(tmp_path):
                 f"int8 {arch} 1 64 56 56 48 3 3 1 1 1 1 0 4 2 1 12.5",     # 3 blocks: fk 4 does not divide
                 f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 1 4 2 1 12.5",     # output mode 1
                 f"int8 {arch} 1 64 56 56 64 3 3 1 1 1 1 0 4 2 8 12.5"):    # 8 waves
+        f = tmp_path / "bad.txt"
+        f.write_text(bad + "\n")
+        with pytest.raises(RuntimeError, match="malformed"):
+            neo.tune_db_load(str(f))
+    neo.tune_db_clear()
+
+
+def test_results_file_int8_group_lines(tmp_path):
+    """An "i8group" line (n members with their output modes, m pools, the
+    configuration) loads and saves back when the configuration suits every
+    member; others are refused."""
+    neo.tune_db_clear()
+    arch = "gfx950"
+    a = "1 64 35 35 64 1 1 1 1 0 0 0"      # 1x1, float32 output
+    b = "1 64 35 35 48 1 1 1 1 0 0 2"      # 1x1 to 48 channels, int8 copy (3 blocks: fk 1)
+    pool = "0 1 64 35 35 3 3 1 1 1 1 16"   # 3x3 average pool, block 16
+    good = tmp_path / "good.txt"
+    good.write_text(f"i8group {arch} 2 1 {a} {b} {pool} 1 2 1 7.5\n"
+                    f"i8group {arch} 2 0 {a} {b} 1 1 1 6.25\n")
+    assert neo.tune_db_load(str(good)) == 2 and neo.tune_db_size() == 2
+    out = tmp_path / "saved.txt"
+    neo.tune_db_save(str(out))
+    assert sorted(l for l in out.read_text().splitlines() if l.startswith("i8group ")) == \
+        sorted(good.read_text().splitlines())
+    for bad in (f"i8group {arch} 2 1 {a} {b} {pool} 2 2 1 7.5",             # fk 2: 48 channels
+                f"i8group {arch} 2 1 {a} {b} 0 1 64 35 35 3 3 1 1 1 1 8 1 1 1 7.5",  # block 8
+                f"i8group {arch} 2 2 {a} {b} {pool} {pool} 1 1 1 7.5",     # two pools
+                f"i8group {arch} 5 0 {a} {a} {a} {a} {a} 1 1 1 7.5",       # five members
+                f"i8group {arch} 1 0 1 64 35 35 64 1 1 1 1 0 0 1 1 1 1 7.5",  # output mode 1
+                f"i8group {arch} 2 0 {a} {b} 1 1 2"):                       # no time
         f = tmp_path / "bad.txt"
         f.write_text(bad + "\n")
         with pytest.raises(RuntimeError, match="malformed"):
