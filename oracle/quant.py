@@ -23,8 +23,9 @@ scheme, so this module fixes one, the usual symmetric linear quantization:
 Integer inference of a whole network (``run_graph_int8``): every conv's
 input has the scale max |x| / 127 of the float32 tensor it reads
 (calibrated on the run itself) and is quantized by division, except an
-input that is the output of a conv whose conv readers all have the same
-padding: that conv writes it requantized (by the reciprocal, as above).  The filter is the
+input that is the output of a conv: that conv writes it requantized (by the
+reciprocal, as above), one int8 tensor shared by every conv that reads it,
+whatever their paddings (the padding is storage, not arithmetic).  The filter is the
 batch-norm-folded one (``fold_bn``) quantized per output channel, and the
 conv's output is the float32 epilogue above; pools, concatenation, flatten
 and dense are the float32 oracle's own.
@@ -163,21 +164,15 @@ def run_graph_int8(graph, x=None):
     x = graph.x if x is None else x
     vals = [None] * len(graph.nodes)
     scales = []
-    uses = [[] for _ in graph.nodes]     # (consumer, as input or as residual)
-    for i, n in enumerate(graph.nodes):
-        for j in n.inputs:
-            uses[j].append((i, "in"))
-        if n.residual >= 0:
-            uses[n.residual].append((i, "res"))
     for i, n in enumerate(graph.nodes):
         ins = [vals[j] for j in n.inputs]
         if n.op == "input":
             v = np.asarray(x, np.float32)
         elif n.op == "conv":
-            j = n.inputs[0]
-            pads = {tuple(graph.nodes[c].pad) for c, how in uses[j]
-                    if how == "in" and graph.nodes[c].op == "conv"}
-            chained = graph.nodes[j].op == "conv" and len(pads) == 1
+            # a conv's output is the one int8 tensor all convs reading it
+            # share (whatever their paddings), requantized by that conv;
+            # any other value is quantized by its own pass
+            chained = graph.nodes[n.inputs[0]].op == "conv"
             v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None, chained)
             scales.append(xs)
         elif n.op == "maxpool":

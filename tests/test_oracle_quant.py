@@ -203,3 +203,39 @@ def test_integer_network_equals_the_float_network():
     y8, scales = oq.run_graph_int8(g)
     np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 16129.0]))
     np.testing.assert_array_equal(y8, fo.run_graph(g))
+
+
+def test_conv_output_read_with_two_paddings_is_requantized():
+    """A conv's output read by a 1x3 conv (padding (0, 1)) and a 3x1 conv
+    (padding (1, 0)) is requantized by the reciprocal for both.  The value
+    45.5 at scale 7 is the exact tie 6.5: division rounds it to 6 (half to
+    even), 45.5 * float32(1/7) to 7.  By hand: the input's scale is 1 (its
+    maximum 127 sits in a channel no filter reads); the first conv gives
+    127 * x0 (at most 889 = 7 * 127, so scale 7) and the constant 45.5 from
+    its bias; the delta filters (127 at the centre tap of channel 1) then
+    give 127 * 7 * 7 = 6223 at every pixel (5334 with the division)."""
+    from paper_1809_02697_amd.workloads import Graph, Node
+    rng = np.random.default_rng(3)
+    x = np.zeros((1, 3, 4, 5), np.float32)
+    x[0, 0] = rng.integers(-7, 8, (4, 5))
+    x[0, 0, 2, 3] = 7.0
+    x[0, 2, 1, 1] = 127.0
+    wa = np.zeros((2, 3, 1, 1), np.float32)
+    wa[0, 0] = 127.0
+    wa[1, 1] = 127.0
+    wb = np.zeros((1, 2, 1, 3), np.float32)
+    wb[0, 1, 0, 1] = 127.0
+    wc = np.zeros((1, 2, 3, 1), np.float32)
+    wc[0, 1, 1, 0] = 127.0
+    nodes = [
+        Node("input"),
+        Node("conv", (0,), K=2, R=1, S=1, w=wa, bias=np.float32([0.0, 45.5])),
+        Node("conv", (1,), K=1, R=1, S=3, pad=(0, 1), w=wb),
+        Node("conv", (1,), K=1, R=3, S=1, pad=(1, 0), w=wc),
+        Node("concat", (2, 3)),
+        Node("output", (4,)),
+    ]
+    g = Graph("two paddings", nodes, x.shape, x)
+    y, scales = oq.run_graph_int8(g)
+    np.testing.assert_array_equal(scales, np.float32([1.0, 7.0, 7.0]))
+    np.testing.assert_array_equal(y, np.full((1, 2, 4, 5), 6223.0, np.float32))
