@@ -213,7 +213,8 @@ hipError_t launch_conv_group(const ConvShape* s, int n, const ConvConfig& c, con
                              const float* const* res, float* const* y, const GroupPool* pool,
                              hipStream_t st) {
     if (!conv_group_config_valid(s, n, c)) return hipErrorInvalidValue;
-    if (pool && !pow2_block(pool->s.xb)) return hipErrorInvalidValue;
+    // (a pool with an int8 copy runs in integer group launches only)
+    if (pool && (!pow2_block(pool->s.xb) || !pool->x || !pool->y || pool->q.yq)) return hipErrorInvalidValue;
     int G = 4;
     for (int i = 0; i < n; ++i) G = std::min(G, conv_group(s[i], c));
     ConvGroupArgs ga;

@@ -66,6 +66,7 @@ struct I8Args {
     int qph, qpw;         // int8 modes: the output's halo
     int q_off, q_tot;     // int8 modes: blocks [q_off, q_off + KB) of q_tot
     int N, CB, CG, Hp, Wp, KB, S, sh, sw, OH, OW, M, y_off, y_tot, act;
+    int hoff, woff;       // x's halo beyond the conv's padding (rows, columns)
     int T;                // reduction steps: R * S * CG
     int npx, nkt;         // pixel tiles (16 * FP pixels), channel tiles (FK blocks)
     int ntiles;           // npx * nkt
@@ -147,7 +148,7 @@ __device__ __forceinline__ void i8_tile(const I8Args& a, const int u, const int 
         const int oh = fdiv(pix, a.div_ow);
         const int ow = pix - oh * a.OW;
         // the (r, s) = (0, 0) byte of the pixel's window in channel block g
-        xbase[p] = ((n * a.CB + g) * a.Hp + oh * a.sh) * a.Wp * 16 + ow * a.sw * 16;
+        xbase[p] = ((n * a.CB + g) * a.Hp + oh * a.sh + a.hoff) * a.Wp * 16 + (ow * a.sw + a.woff) * 16;
         // its output element in channel block 0 of [N][KB][OH][OW][16]
         // (residual, accumulators) and of the view: [N][y_tot][OH][OW][16]
         // float32, or in int8 mode [N][y_tot][OH + 2 qph][OW + 2 qpw][16]
@@ -345,9 +346,9 @@ __global__ __launch_bounds__(WAVES * 64) void conv_i8_group(I8GroupArgs ga) {
         using conv_detail::pool_part_run;
         const int wg = blockIdx.x - nconv;
         if (ga.pool.max)
-            ga.pool.k33 ? pool_part_run<true, 3>(ga.pool, wg) : pool_part_run<true, 0>(ga.pool, wg);
+            ga.pool.k33 ? pool_part_run<true, 3, true>(ga.pool, wg) : pool_part_run<true, 0, true>(ga.pool, wg);
         else
-            ga.pool.k33 ? pool_part_run<false, 3>(ga.pool, wg) : pool_part_run<false, 0>(ga.pool, wg);
+            ga.pool.k33 ? pool_part_run<false, 3, true>(ga.pool, wg) : pool_part_run<false, 0, true>(ga.pool, wg);
         return;
     }
     int m = 0;
@@ -512,7 +513,7 @@ hipError_t group_by_tile(const ConvConfig& c, const I8GroupArgs& ga, int wgs, hi
 // configuration, operands and outputs).
 I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                     const float* wscale, float xscale, const float* bias, const float* res, float* y,
-                    int* acc, int8_t* yq, float yscale, int qph, int qpw) {
+                    int* acc, int8_t* yq, float yscale, int qph, int qpw, int xph, int xpw) {
     I8Args a;
     a.x = x;
     a.w = w;
@@ -533,8 +534,12 @@ I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, co
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.CG = cdiv(s.C, 64);
-    a.Hp = s.H + 2 * s.ph;
-    a.Wp = s.W + 2 * s.pw;
+    // x's halo (xph, xpw) >= the padding: the window of output (oh, ow)
+    // starts hoff = xph - ph rows and woff = xpw - pw columns into it
+    a.Hp = s.H + 2 * xph;
+    a.Wp = s.W + 2 * xpw;
+    a.hoff = xph - s.ph;
+    a.woff = xpw - s.pw;
     a.KB = cdiv(s.K, 16);
     a.S = s.S;
     a.sh = s.sh;
@@ -549,7 +554,7 @@ I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, co
     a.npx = cdiv(a.M, 16 * c.fp);
     a.nkt = a.KB / c.fk;
     a.ntiles = a.npx * a.nkt;
-    a.x_bytes = (int)int8_act_bytes(s.N, s.C, s.H, s.W, s.ph, s.pw);
+    a.x_bytes = (int)int8_act_bytes(s.N, s.C, s.H, s.W, xph, xpw);
     a.w_bytes = (int)int8_filter_bytes(s.K, s.C, s.R, s.S);
     a.div_ohw = make_fastdiv((unsigned)(s.OH * s.OW));
     a.div_ow = make_fastdiv((unsigned)s.OW);
@@ -622,9 +627,11 @@ hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, i
 hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                             const float* wscale, float xscale, const float* bias, const float* res,
                             float* y, int* acc, int8_t* yq, float yscale, int qph, int qpw,
-                            hipStream_t st) {
-    if (!int8_config_valid(s, c)) return hipErrorInvalidValue;
-    const I8Args a = make_i8_args(s, c, x, w, wscale, xscale, bias, res, y, acc, yq, yscale, qph, qpw);
+                            hipStream_t st, int xph, int xpw) {
+    if (xph < 0) xph = s.ph;
+    if (xpw < 0) xpw = s.pw;
+    if (!int8_config_valid(s, c) || xph < s.ph || xpw < s.pw) return hipErrorInvalidValue;
+    const I8Args a = make_i8_args(s, c, x, w, wscale, xscale, bias, res, y, acc, yq, yscale, qph, qpw, xph, xpw);
     if (acc) return by_tile<kOutAcc>(c, a, st);
     if (yq) return y ? by_tile<kOutBoth>(c, a, st) : by_tile<kOutI8>(c, a, st);
     return by_tile<kOutF32>(c, a, st);
@@ -678,9 +685,9 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
     long total_wgs = 0;
     for (int j = 0; j < n; ++j) {
         const I8Member& m = mem[order[j]];
-        if (!m.y && !m.yq) return hipErrorInvalidValue;
+        if ((!m.y && !m.yq) || m.xph < m.s.ph || m.xpw < m.s.pw) return hipErrorInvalidValue;
         ga.a[j] = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
-                               m.yscale, m.qph, m.qpw);
+                               m.yscale, m.qph, m.qpw, m.xph, m.xpw);
         ga.cnt[j] = ga.a[j].ntiles;
         total_wgs += (long)cdiv(ga.cnt[j], conv_detail::kXcds) * conv_detail::kXcds;
         if (total_wgs >= (1L << 30)) return hipErrorInvalidValue;
@@ -705,6 +712,8 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
         pp.total = (int)total;
         pp.max = pool->max ? 1 : 0;
         pp.k33 = ps.R == 3 && ps.S == 3;
+        pp.q = pool->q;
+        if ((!pp.y && !pp.q.yq) || (pp.q.yq && !(pp.q.scale > 0.f))) return hipErrorInvalidValue;
         // one output quad per thread, at most 1024 workgroups (then grid-stride)
         const long per = 64L * c.waves;
         pp.wgs = (int)std::min<long>(1024, std::max<long>(1, (total + per - 1) / per));

@@ -650,6 +650,7 @@ struct PoolPart {
     float* y;
     PoolShape s;
     int CB, lq, total, max, k33, wgs;  // wgs = 0: no pooling step
+    PoolQ q;                           // its int8 copy (integer group launches only)
 };
 struct ConvGroupArgs {
     ConvArgs a[kMaxGroup];
@@ -659,10 +660,10 @@ struct ConvGroupArgs {
     PoolPart pool;
 };
 
-template <bool MAX, int K>
+template <bool MAX, int K, bool Q = false>
 __device__ inline void pool_part_run(const PoolPart& p, int wg) {
     for (int t = wg * blockDim.x + threadIdx.x; t < p.total; t += p.wgs * blockDim.x)
-        pool_detail::pool_elem<MAX, K, K>(p.x, p.y, p.s, p.CB, p.lq, t);
+        pool_detail::pool_elem<MAX, K, K, Q>(p.x, p.y, p.s, p.CB, p.lq, t, p.q);
 }
 
 template <int FK, int FP, int G, int WAVES>

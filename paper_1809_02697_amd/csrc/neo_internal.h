@@ -122,7 +122,7 @@ bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 // also by its output mode `out` (0 float32, 2 int8, 3 both).
 int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
               const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
-              hipStream_t st, ConvConfig* best, float* us);
+              hipStream_t st, ConvConfig* best, float* us, int xph = -1, int xpw = -1);
 bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg);
 
 // Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations with
@@ -148,10 +148,12 @@ hipError_t launch_quantize_int8(const float* x, int N, int C, int H, int W, int 
                                 int8_t* q, hipStream_t st);
 hipError_t launch_pack_filter_int8(const float* w, int K, int C, int R, int S, int8_t* wq, float* wscale,
                                    hipStream_t st);
+// x carries a zero halo of (xph, xpw), at least the conv's padding (-1: the
+// padding itself), so one int8 copy serves convs of different paddings.
 hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                             const float* wscale, float xscale, const float* bias, const float* res,
                             float* y, int* acc, int8_t* yq, float yscale, int qph, int qpw,
-                            hipStream_t st);
+                            hipStream_t st, int xph = -1, int xpw = -1);
 
 // Launch the blocked convolution.  x: NCHW[xb]c; w: KCRS[16]c[16]k, or with
 // wmfma the kernel's own filter order (to_kernel_order); bias: [ceil(K/16)*16]
@@ -169,13 +171,25 @@ struct PoolShape {
     int xb = 16;
 };
 
+// An int8 copy of a pooling step's output (block 16 only): int8 NCHW16c
+// with a (qph, qpw) zero halo, [N][ceil(C/16)][OH + 2 qph][OW + 2 qpw][16],
+// each value clamp(round_half_even(y / scale), -127, 127) with the division
+// in float32 (the quantization pass's arithmetic); yq null: none.
+struct PoolQ {
+    int8_t* yq = nullptr;
+    float scale = 1.f;
+    int qph = 0, qpw = 0;
+};
+
 // A pooling step run by the last workgroups of a fused conv launch (it is
-// independent of the launch's convs).
+// independent of the launch's convs); q: its int8 copy (integer group
+// launches only), y may then be null.
 struct GroupPool {
     PoolShape s;
     bool max;
     const float* x;
     float* y;
+    PoolQ q{};
 };
 
 // Several independent convolutions in one launch (horizontal fusion): NCHW16c
@@ -206,6 +220,7 @@ struct I8Member {
     int8_t* yq;
     float yscale;
     int qph, qpw;
+    int xph, xpw;  // the halo of x, at least the conv's padding
 };
 bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);
 ConvConfig choose_int8_group_config(const ConvShape* s, int n);
@@ -339,6 +354,10 @@ hipError_t launch_pack_filter(const float* w, int K, int C, int R, int S, int ib
 // ---- pools ----------------------------------------------------------------------------
 hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
 hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st);
+// Pooling on NCHW16c writing the float32 output y (may be null) and/or its
+// int8 copy q (the same float32 values quantized).
+hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y, const PoolQ& q,
+                         hipStream_t st);
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st);
 
 // ---- global layout search (search.cpp) -----------------------------------------------------

@@ -98,9 +98,9 @@ struct Step {
     bool quant_here = false, f32_needed = true;
 };
 
-// NEO_PLAN_INT8: the int8 copy of a value with one halo (the padding of the
-// convs that read it), in the int8 arena, with its scale; written by the
-// epilogue of the conv producing the value (writer) or by one quantization
+// NEO_PLAN_INT8: the int8 copy of a value, its halo the largest padding of
+// the convs that read it, in the int8 arena, with its scale; written by the
+// conv or pooling step producing the value (writer) or by one quantization
 // pass (run by the first conv that reads it)
 struct I8Copy {
     int val, ph, pw;
@@ -1021,43 +1021,58 @@ bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_ou
     gp->max = ps.kind == ST_MAXPOOL;
     gp->x = val_ptr(P, ps.in, x_in, y_out);
     gp->y = val_ptr(P, ps.out, x_in, y_out);
+    gp->q = PoolQ{};
+    if (ps.q_out >= 0 && !P->i8_f32_out) {
+        // NEO_PLAN_INT8: the int8 copy its conv readers share
+        const I8Copy& qo = P->i8_copies[ps.q_out];
+        gp->q.yq = P->d_i8 + qo.xq_off;
+        gp->q.scale = qo.xscale;
+        gp->q.qph = qo.ph;
+        gp->q.qpw = qo.pw;
+        if (!ps.f32_needed) gp->y = nullptr;
+    }
     return true;
 }
 
-// NEO_PLAN_INT8: one int8 copy per (value, halo) that int8 convs read,
-// shared by all of them (one scale: the value's).  The conv producing the
-// value writes the copy from its epilogue when the value has one copy only
-// (every conv reading it has the same padding), beside its float32 output if
-// anything else reads that; otherwise the first conv to read the copy runs
-// its quantization pass.
+// NEO_PLAN_INT8: one int8 copy per value that int8 convs read, shared by
+// all of them (one scale: the value's), its halo the largest padding among
+// them (each conv starts its windows that much further in).  The step
+// producing the value writes the copy when it is a conv (requantizing its
+// epilogue's value) or a pooling step (quantizing its output), beside its
+// float32 output if anything else reads that; otherwise the first conv to
+// read the copy runs its quantization pass.
 void plan_int8_copies(neo_plan* P) {
     const int ns = (int)P->steps.size();
     for (int i = 0; i < ns; ++i) {
         Step& t = P->steps[i];
         if (t.kind != ST_CONV || !t.i8) continue;
         int c = -1;
-        for (int k = 0; k < (int)P->i8_copies.size(); ++k) {
-            const I8Copy& q = P->i8_copies[k];
-            if (q.val == t.in && q.ph == t.cs.ph && q.pw == t.cs.pw) c = k;
-        }
+        for (int k = 0; k < (int)P->i8_copies.size(); ++k)
+            if (P->i8_copies[k].val == t.in) c = k;
         if (c < 0) {
-            const Val& v = P->vals[t.in];
-            I8Copy q{t.in, t.cs.ph, t.cs.pw, P->i8_bytes};
-            P->i8_bytes += ((long)int8_act_bytes(v.N, v.C, v.H, v.W, t.cs.ph, t.cs.pw) + 255) / 256 * 256;
             c = (int)P->i8_copies.size();
-            P->i8_copies.push_back(q);
+            P->i8_copies.push_back(I8Copy{t.in, t.cs.ph, t.cs.pw, -1});
             t.quant_here = true;  // the first reader, unless a writer takes it over
         }
+        I8Copy& q = P->i8_copies[c];
+        q.ph = std::max(q.ph, t.cs.ph);
+        q.pw = std::max(q.pw, t.cs.pw);
         t.qc = c;
+    }
+    for (I8Copy& q : P->i8_copies) {
+        const Val& v = P->vals[q.val];
+        q.xq_off = P->i8_bytes;
+        P->i8_bytes += ((long)int8_act_bytes(v.N, v.C, v.H, v.W, q.ph, q.pw) + 255) / 256 * 256;
     }
     for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
         I8Copy& q = P->i8_copies[c];
-        int copies_of_val = 0;
-        for (const I8Copy& o : P->i8_copies) copies_of_val += o.val == q.val;
         int w = -1;
-        for (int i = 0; i < ns; ++i)
-            if (P->steps[i].out == q.val && P->steps[i].kind == ST_CONV && P->steps[i].i8) w = i;
-        if (copies_of_val != 1 || w < 0) continue;
+        for (int i = 0; i < ns; ++i) {
+            const Step& t = P->steps[i];
+            if (t.out == q.val && ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL))
+                w = i;
+        }
+        if (w < 0) continue;
         // the writer: does anything read its float32 output?
         bool f32 = q.val == P->out_val || P->vals[q.val].view;
         for (const Val& o : P->vals)
@@ -1178,9 +1193,14 @@ std::string describe(const neo_plan* P) {
                 o << "}";
             }
             o << "]";
-            for (const Step& ps : s.pools)
+            for (const Step& ps : s.pools) {
                 o << ",\"pool\":{\"kind\":\"" << kinds[ps.kind] << "\",\"node\":" << ps.node
-                  << ",\"in\":" << ps.in << ",\"out\":" << ps.out << "}";
+                  << ",\"in\":" << ps.in << ",\"out\":" << ps.out;
+                if (ps.q_out >= 0)
+                    o << ",\"int8\":{\"writes_copy\":" << ps.q_out << ",\"writes_f32\":"
+                      << (ps.f32_needed ? "true" : "false") << "}";
+                o << "}";
+            }
         }
         if (s.kind == ST_CONV_PAIR || s.kind == ST_CONV_CHAIN) {
             o << ",\"out2\":" << s.out2 << ",\"tuned\":" << (s.tuned ? "true" : "false") << ",\"members\":[";
@@ -1207,6 +1227,9 @@ std::string describe(const neo_plan* P) {
               << "],\"pad\":[" << ps.ph << "," << ps.pw << "],\"OH\":" << ps.OH << ",\"OW\":" << ps.OW
               << "}";
         }
+        if ((s.kind == ST_MAXPOOL || s.kind == ST_AVGPOOL) && s.q_out >= 0)
+            o << ",\"int8\":{\"writes_copy\":" << s.q_out << ",\"writes_f32\":"
+              << (s.f32_needed ? "true" : "false") << "}";
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) {
             o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out;
@@ -1633,6 +1656,8 @@ static I8Member i8_member(const neo_plan* P, const Step& s, const float* x_nchw,
     m.yscale = qo ? qo->xscale : 1.f;
     m.qph = qo ? qo->ph : 0;
     m.qpw = qo ? qo->pw : 0;
+    m.xph = qc.ph;
+    m.xpw = qc.pw;
     return m;
 }
 
@@ -1679,7 +1704,8 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                                              s.b_off >= 0 ? prm + s.b_off : nullptr,
                                              s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr, y,
                                              nullptr, qo ? P->d_i8 + qo->xq_off : nullptr,
-                                             qo ? qo->xscale : 1.f, qo ? qo->ph : 0, qo ? qo->pw : 0, st);
+                                             qo ? qo->xscale : 1.f, qo ? qo->ph : 0, qo ? qo->pw : 0, st,
+                                             qc.ph, qc.pw);
                     break;
                 }
                 if (s.wino) {
@@ -1755,10 +1781,22 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 break;
             }
             case ST_MAXPOOL:
-                e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
-                break;
             case ST_AVGPOOL:
-                e = launch_avgpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
+                if (s.q_out >= 0 && !P->i8_f32_out) {
+                    // NEO_PLAN_INT8: the pool writes the int8 copy its conv readers share
+                    const I8Copy& qo = P->i8_copies[s.q_out];
+                    PoolQ q;
+                    q.yq = P->d_i8 + qo.xq_off;
+                    q.scale = qo.xscale;
+                    q.qph = qo.ph;
+                    q.qpw = qo.pw;
+                    e = launch_pool_q(s.ps, s.kind == ST_MAXPOOL, val_ptr(P, s.in, x_nchw, y_out),
+                                      s.f32_needed ? val_ptr(P, s.out, x_nchw, y_out) : nullptr, q, st);
+                } else if (s.kind == ST_MAXPOOL) {
+                    e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
+                } else {
+                    e = launch_avgpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
+                }
                 break;
             case ST_GAP: {
                 const Val& in = P->vals[s.in];
@@ -1872,7 +1910,7 @@ static int tune_plan(neo_plan* P) {
                 float us = 0.f;
                 const I8Member& q = mem[m];
                 rc = tune_int8(q.s, q.x, q.w, q.wscale, q.bias, q.res, q.y, q.yq, q.qph, q.qpw, P->cap_stream,
-                               &own[m], &us);
+                               &own[m], &us, q.xph, q.xpw);
                 alone_us += us;
             }
             if (rc != NEO_OK) break;
@@ -2059,12 +2097,13 @@ static int tune_plan(neo_plan* P) {
         if (s.kind == ST_CONV && s.i8) {
             // an integer conv: its configurations timed with its own output mode
             const I8Copy* qo = s.q_out >= 0 ? &P->i8_copies[s.q_out] : nullptr;
-            rc = tune_int8(s.cs, P->d_i8 + P->i8_copies[s.qc].xq_off, P->d_i8 + s.w8_off,
+            const I8Copy& qc = P->i8_copies[s.qc];
+            rc = tune_int8(s.cs, P->d_i8 + qc.xq_off, P->d_i8 + s.w8_off,
                            P->d_params + s.ws8_off, s.b_off >= 0 ? P->d_params + s.b_off : nullptr,
                            s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
                            (!qo || s.f32_needed) ? val_ptr(P, s.out, xin, yout) : nullptr,
                            qo ? P->d_i8 + qo->xq_off : nullptr, qo ? qo->ph : 0, qo ? qo->pw : 0,
-                           P->cap_stream, &s.c8, nullptr);
+                           P->cap_stream, &s.c8, nullptr, qc.ph, qc.pw);
             s.tuned = rc == NEO_OK;
             next.push_back(s);
             continue;
@@ -2210,7 +2249,7 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
                 if (rc != NEO_OK) return rc;
             }
             for (const Step& pl : s.pools) {
-                const int rc = enqueue_step(P, pl, x_nchw, y_out, st);
+                const int rc = calibrate_step(pl);
                 if (rc != NEO_OK) return rc;
             }
             return NEO_OK;
@@ -2221,9 +2260,10 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
             (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in),
                            &P->i8_copies[s.qc].xscale)) != NEO_OK)
             return rc;
-        if (s.kind == ST_CONV && s.i8 && s.q_out >= 0) {
-            // a copy's writer: run it once with its float32 output only, take
-            // the copy's scale from that, then run it as the plan does
+        if (s.q_out >= 0) {
+            // a copy's writer (conv or pool): run it once with its float32
+            // output only, take the copy's scale from that, then run it as
+            // the plan does
             P->i8_f32_out = true;
             rc = enqueue_step(P, s, x_nchw, y_out, st);
             P->i8_f32_out = false;

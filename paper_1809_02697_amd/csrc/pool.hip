@@ -21,6 +21,15 @@ __global__ __launch_bounds__(256) void pool_blk(const float* __restrict__ x, flo
         pool_detail::pool_elem<MAX, KR, KS>(x, y, s, CB, lq, t);
 }
 
+// The same, on NCHW16c, with the int8 copy of the output (pool_elem's Q).
+template <bool MAX, int KR, int KS>
+__global__ __launch_bounds__(256) void pool_blk_q(const float* __restrict__ x, float* __restrict__ y,
+                                                  PoolShape s, int CB, PoolQ q) {
+    const int total = (s.N * CB * s.OH * s.OW) << 2;
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x)
+        pool_detail::pool_elem<MAX, KR, KS, true>(x, y, s, CB, 2, t, q);
+}
+
 // One wave per (n, 16-channel group j) whatever the block x: lane = 4 *
 // pixel_slot + quad; each lane sums the pixels p = slot, slot + 16, ... of its
 // quad's channels, then the 16 slots are summed with cross-lane shuffles in a
@@ -75,7 +84,7 @@ inline dim3 grid_for(long total) {
 
 template <bool MAX>
 hipError_t launch_pool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
-    if (!pow2_block(s.xb)) return hipErrorInvalidValue;
+    if (!pow2_block(s.xb) || !x || !y) return hipErrorInvalidValue;
     const int CB = cdiv(s.C, s.xb), lq = ilog2(s.xb / 4);
     const dim3 g = grid_for(((long)s.N * CB * s.OH * s.OW) << lq), b(256);
     if (s.R == 3 && s.S == 3)
@@ -93,6 +102,25 @@ hipError_t launch_maxpool(const PoolShape& s, const float* x, float* y, hipStrea
 
 hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStream_t st) {
     return launch_pool<false>(s, x, y, st);
+}
+
+template <bool MAX>
+hipError_t launch_pool_q_t(const PoolShape& s, const float* x, float* y, const PoolQ& q, hipStream_t st) {
+    const int CB = cdiv(s.C, 16);
+    const dim3 g = grid_for(((long)s.N * CB * s.OH * s.OW) << 2), b(256);
+    if (s.R == 3 && s.S == 3)
+        hipLaunchKernelGGL((pool_blk_q<MAX, 3, 3>), g, b, 0, st, x, y, s, CB, q);
+    else if (s.R == 2 && s.S == 2)
+        hipLaunchKernelGGL((pool_blk_q<MAX, 2, 2>), g, b, 0, st, x, y, s, CB, q);
+    else
+        hipLaunchKernelGGL((pool_blk_q<MAX, 0, 0>), g, b, 0, st, x, y, s, CB, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y, const PoolQ& q,
+                         hipStream_t st) {
+    if (s.xb != 16 || !x || (!y && !q.yq) || (q.yq && !(q.scale > 0.f))) return hipErrorInvalidValue;
+    return max ? launch_pool_q_t<true>(s, x, y, q, st) : launch_pool_q_t<false>(s, x, y, q, st);
 }
 
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st) {

@@ -24,11 +24,14 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // discarded by a select, so the loads of one output are in flight together;
 // KR = 0 walks the window from the shape.  Both walk the taps row by row, so
 // the sums are the same.
-template <bool MAX, int KR, int KS>
+// Q: the output may also (or only: y null) be written as its int8 copy q
+// (block 16, one quad of four channels = four bytes of the pixel's 16).
+template <bool MAX, int KR, int KS, bool Q = false>
 __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __restrict__ y,
-                                          const PoolShape& s, int CB, int lq, int t) {
+                                          const PoolShape& s, int CB, int lq, int t,
+                                          const PoolQ& q = PoolQ{}) {
     const int X = s.xb;
-    const int q = t & ((1 << lq) - 1);
+    const int qd = t & ((1 << lq) - 1);
     int r_ = t >> lq;
     const int ow = r_ % s.OW;
     r_ /= s.OW;
@@ -36,7 +39,7 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
     r_ /= s.OH;
     const int cb = r_ % CB;
     const int n = r_ / CB;
-    const float* xb = x + (n * CB + cb) * s.H * s.W * X + 4 * q;
+    const float* xb = x + (n * CB + cb) * s.H * s.W * X + 4 * qd;
     const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
     v4f acc;
     if (MAX)
@@ -94,7 +97,22 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] = (float)(dacc[i] / d);
     }
-    *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X + 4 * q) = acc;
+    if (!Q || y) *reinterpret_cast<v4f*>(y + (((n * s.y_tot + s.y_off + cb) * s.OH + oh) * s.OW + ow) * X + 4 * qd) = acc;
+    if constexpr (Q) {
+        if (q.yq) {
+            // clamp(round_half_even(v / scale), -127, 127), the division in float32
+            unsigned packed = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float r = rintf(acc[i] / q.scale);
+                r = r > 127.f ? 127.f : (r < -127.f ? -127.f : r);
+                packed |= ((unsigned)(int)r & 0xffu) << (8 * i);
+            }
+            const int owq = s.OW + 2 * q.qpw;
+            const long at = (((long)(n * CB + cb) * (s.OH + 2 * q.qph) + oh + q.qph) * owq + ow + q.qpw) * 16 + 4 * qd;
+            *reinterpret_cast<unsigned*>(q.yq + at) = packed;
+        }
+    }
 }
 
 }  // namespace pool_detail

@@ -276,7 +276,7 @@ bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg) {
 // (their contents do not change the time); keeps the fastest with its time.
 int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
               const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
-              hipStream_t st, ConvConfig* best_out, float* us_out) {
+              hipStream_t st, ConvConfig* best_out, float* us_out, int xph, int xpw) {
     const int out = yq ? (y ? 3 : 2) : 0;
     const GroupKey key = i8_key(s, out);
     {
@@ -300,7 +300,7 @@ int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float*
                     if (!int8_config_valid(s, c)) continue;
                     float us = 0.f;
                     e = time_launch([&] { return launch_conv_int8(s, c, x, w, wscale, 1.f, bias, res, y,
-                                                                  nullptr, yq, 1.f, qph, qpw, st); },
+                                                                  nullptr, yq, 1.f, qph, qpw, st, xph, xpw); },
                                     st, ev.e0, ev.e1, &us);
                     if (e != hipSuccess) break;
                     if (us < best_us) {
@@ -347,9 +347,10 @@ int tune_int8_group(const I8Member* m, int n, const GroupPool* pool, hipStream_t
         const int out = m[i].yq ? (m[i].y ? 3 : 2) : 0;
         key.second.insert(key.second.end(), {c.N, c.C, c.H, c.W, c.K, c.R, c.S, c.sh, c.sw, c.ph, c.pw, out});
     }
-    if (pool) {
+    if (pool) {  // the pool's shape and its output mode (0 float32, 2 int8, 3 both)
         const std::vector<int> pi = pool_ints(*pool);
         key.second.insert(key.second.end(), pi.begin(), pi.end());
+        key.second.push_back(pool->q.yq ? (pool->y ? 3 : 2) : 0);
     }
     {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -550,6 +551,21 @@ int tune_conv_pool(const ConvShape& c, const PoolShape& p, const float* x, const
 }
 
 int tune_pool(const GroupPool& p, hipStream_t st, float* us_out) {
+    if (p.q.yq) {
+        // a pool writing an int8 copy (its float32 output may be absent):
+        // timed as it runs, not kept (the results file keys pools by shape)
+        float us = 0.f;
+        hipError_t e;
+        {
+            Events ev;
+            e = time_launch([&] { return launch_pool_q(p.s, p.max, p.x, p.y, p.q, st); }, st, ev.e0, ev.e1,
+                            &us);
+            (void)hipStreamSynchronize(st);
+        }
+        if (e != hipSuccess) return hip_fail(e, "pool timing");
+        *us_out = us;
+        return NEO_OK;
+    }
     const GroupKey key{device_arch(), pool_ints(p)};
     {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -601,7 +617,7 @@ extern "C" {
 // one line per integer conv (out: 0 float32, 2 int8, 3 both outputs):
 //   int8 arch N C H W K R S sh sw ph pw out fk fp waves us
 // and one line per launch of n integer convs and m (0 or 1) pooling steps:
-//   i8group arch n m (N C H W K R S sh sw ph pw out) x n (max N C H W R S sh sw ph pw xb) x m
+//   i8group arch n m (N C H W K R S sh sw ph pw out) x n (max N C H W R S sh sw ph pw xb out) x m
 //           fk fp waves us
 int neo_tune_db_save(const char* path) {
     if (!path) return fail(NEO_ERR_INVALID_ARG, "neo_tune_db_save: path is NULL");
@@ -810,7 +826,7 @@ int neo_tune_db_load(const char* path) {
                       members <= kMaxGroupConvs && (pools == 0 || pools == 1);
             if (ok) {
                 gk.second = {members, pools};
-                ok = read_ints(is, members * kI8Ints + pools * kPoolShapeInts, gk.second) &&
+                ok = read_ints(is, members * kI8Ints + pools * (kPoolShapeInts + 1), gk.second) &&
                      (bool)(is >> v.cfg.fk >> v.cfg.fp >> v.cfg.waves >> v.us);
             }
             ConvShape shp[kMaxGroupConvs];
@@ -818,8 +834,10 @@ int neo_tune_db_load(const char* path) {
                 const int* q = gk.second.data() + 2 + i * kI8Ints;
                 ok = i8_shape(q, &shp[i]) && (q[11] == 0 || q[11] == 2 || q[11] == 3);
             }
-            // the pool rides in blocks of 16 only
-            ok = ok && (pools == 0 || gk.second.back() == 16) && int8_group_config_valid(shp, members, v.cfg);
+            // the pool rides in blocks of 16 only; its output mode 0, 2 or 3
+            const int pm = gk.second.back();
+            ok = ok && (pools == 0 || (gk.second[gk.second.size() - 2] == 16 && (pm == 0 || pm == 2 || pm == 3))) &&
+                 int8_group_config_valid(shp, members, v.cfg);
             if (!ok) return fail(NEO_ERR_INVALID_ARG, bad + std::to_string(lineno));
             add_i8group[gk] = v;
             ++n;

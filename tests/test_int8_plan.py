@@ -29,17 +29,19 @@ def test_host_plan_and_flags():
     assert len(convs) == 53 and len(d["steps"]) == 57
     assert all(s["conv"]["algo"] == "int8" and not s["conv"]["int8"]["calibrated"] for s in convs)
     assert not any(s["kind"].startswith("conv_") for s in d["steps"])     # no fused steps
-    # one int8 copy per (value, padding): 49 for 53 convs (each stage's input
-    # is shared by its reduce and projection convs); every conv output that
-    # convs read is written as a copy by its producer (47; 12 of them, the
-    # outputs of identity-shortcut blocks, also in float32 for the residual),
-    # so only the network input and the max pool's output are quantized by a
-    # pass of their own
+    # one int8 copy per value: 49 for 53 convs (each stage's input is shared
+    # by its reduce and projection convs); every conv output that convs read
+    # is written as a copy by its producer (47; 12 of them, the outputs of
+    # identity-shortcut blocks, also in float32 for the residual), and the
+    # max pool writes its output's copy (int8 only), so only the network
+    # input is quantized by a pass of its own
     q = [s["conv"]["int8"] for s in convs]
     assert len({x["input_copy"] for x in q}) == 49
-    assert sum(x["quantizes_input"] for x in q) == 2
+    assert sum(x["quantizes_input"] for x in q) == 1 and q[0]["quantizes_input"]
     assert sum(x["writes_copy"] >= 0 for x in q) == 47
     assert sum(x["writes_copy"] >= 0 and x["writes_f32"] for x in q) == 12
+    pool = [s for s in d["steps"] if s["kind"] == "maxpool"][0]
+    assert pool["int8"]["writes_copy"] >= 0 and not pool["int8"]["writes_f32"]
     L = neo.lib()
     FAKE = ctypes.c_void_p(1 << 20)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
@@ -88,8 +90,13 @@ def test_host_grouped_int8_plan(name):
     for s in groups:
         assert all(m["conv"]["int8"]["tile"] == s["tile"] and m["conv"]["int8"]["waves"] == s["waves"]
                    for m in s["members"])
-    # the same copies are written by the same convs; passes only where no conv writes
+    # the same copies are written by the same convs and pools; passes only
+    # where no conv or pool writes
     writers = {c["int8"]["writes_copy"] for _, c in cs if c["int8"]["writes_copy"] >= 0}
+    for s in d["steps"]:
+        for p_ in [s] + ([s["pool"]] if "pool" in s else []):
+            if "int8" in p_ and "writes_copy" in p_["int8"] and "input_copy" not in p_["int8"]:
+                writers.add(p_["int8"]["writes_copy"])
     first = {}
     for i, c in cs:
         first.setdefault(c["int8"]["input_copy"], i)
@@ -106,7 +113,11 @@ def test_host_grouped_int8_plan(name):
     print(f"\n[int8 group] {name}: {n_launch0} -> {n_launch} launches, {len(groups)} groups")
     assert n_launch < n_launch0
     if name == "inception_v3":
-        assert len(groups) == 27 and sum("pool" in s for s in groups) == 11 and len(passes) == 30
+        # passes: the input and the 10 concatenations convs read; the 4 values
+        # read by a 1x3 and a 3x1 conv have one copy, halo (1, 1), written
+        # by their producer; the pools write their own outputs' copies
+        assert len(groups) == 27 and sum("pool" in s for s in groups) == 11 and len(passes) == 11
+        assert sum(1 for _, c in cs if c["int8"]["quantizes_input"]) == 11
 
 
 # ---- GPU -------------------------------------------------------------------------------------
@@ -294,7 +305,7 @@ def test_results_file_int8_group_lines(tmp_path):
     arch = "gfx950"
     a = "1 64 35 35 64 1 1 1 1 0 0 0"      # 1x1, float32 output
     b = "1 64 35 35 48 1 1 1 1 0 0 2"      # 1x1 to 48 channels, int8 copy (3 blocks: fk 1)
-    pool = "0 1 64 35 35 3 3 1 1 1 1 16"   # 3x3 average pool, block 16
+    pool = "0 1 64 35 35 3 3 1 1 1 1 16 2" # 3x3 average pool, block 16, int8 output
     good = tmp_path / "good.txt"
     good.write_text(f"i8group {arch} 2 1 {a} {b} {pool} 1 2 1 7.5\n"
                     f"i8group {arch} 2 0 {a} {b} 1 1 1 6.25\n")
@@ -304,7 +315,8 @@ def test_results_file_int8_group_lines(tmp_path):
     assert sorted(l for l in out.read_text().splitlines() if l.startswith("i8group ")) == \
         sorted(good.read_text().splitlines())
     for bad in (f"i8group {arch} 2 1 {a} {b} {pool} 2 2 1 7.5",             # fk 2: 48 channels
-                f"i8group {arch} 2 1 {a} {b} 0 1 64 35 35 3 3 1 1 1 1 8 1 1 1 7.5",  # block 8
+                f"i8group {arch} 2 1 {a} {b} 0 1 64 35 35 3 3 1 1 1 1 8 2 1 1 1 7.5",  # block 8
+                f"i8group {arch} 2 1 {a} {b} 0 1 64 35 35 3 3 1 1 1 1 16 1 1 1 1 7.5",  # pool mode 1
                 f"i8group {arch} 2 2 {a} {b} {pool} {pool} 1 1 1 7.5",     # two pools
                 f"i8group {arch} 5 0 {a} {a} {a} {a} {a} 1 1 1 7.5",       # five members
                 f"i8group {arch} 1 0 1 64 35 35 64 1 1 1 1 0 0 1 1 1 1 7.5",  # output mode 1
