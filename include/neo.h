@@ -447,13 +447,15 @@ enum neo_plan_flags {
      * integer convolution with its float32 epilogue (neo_conv2d_int8: bias,
      * residual, activation); filters are the batch-norm-folded ones
      * quantized per output channel on the device at plan creation.  A value
-     * that int8 convs read has one int8 copy per padding among them (shared
-     * by those convs, one scale: max|value| / 127); when all of them pad
-     * alike and a conv produces the value, that conv's epilogue writes the
-     * copy (requantized by the float32 reciprocal of the scale, beside its
-     * float32 output when anything else reads that), otherwise the first
+     * that int8 convs read has one int8 copy (shared by those convs, one
+     * scale: max|value| / 127), its zero halo the largest padding among
+     * them.  When a conv produces the value, that conv's epilogue writes the
+     * copy (requantized by the float32 reciprocal of the scale); when a
+     * pooling step does, the pool writes it (quantized by division, as the
+     * pass would); either beside its float32 output when anything else
+     * reads that.  Otherwise (the network input, a concatenation) the first
      * reader runs the quantization pass.  Pools, concatenation, flatten and
-     * dense stay float32.  The input scales come
+     * dense compute in float32.  The input scales come
      * from neo_plan_calibrate_int8, which must run before the plan does.
      * Convs run in NCHW16c: block 16, and no NAIVE, GLOBAL_SEARCH, WINOGRAD
      * or fusion flag other than NEO_PLAN_GROUP, which puts independent int8
@@ -518,8 +520,11 @@ int neo_run_step(neo_plan* plan, int step, const float* x_nchw, float* y_out, ne
  * output goes to y_out as for neo_run_graph): run the plan step by step on
  * `stream` and, just before each conv, set that conv's input scale to
  * max|x| / 127 in float32 over its float32 input as this run produced it
- * (1 for an all-zero input).  Synchronizes the stream once per conv (the
- * maximum is read back); drops a captured graph, which the next
+ * (1 for an all-zero input; a copy's writer, conv or pool, runs once with
+ * its float32 output only for that, then as the plan does; the members of a
+ * group launch run one by one, which computes the same values).
+ * Synchronizes the stream once per conv (the maximum is read back); drops
+ * a captured graph, which the next
  * neo_run_graph captures again with the new scales.  neo_plan_describe then
  * lists each conv's "x_scale".  Errors: NEO_ERR_STATE for a plan without
  * NEO_PLAN_INT8 or host-only, NEO_ERR_INVALID_ARG / _ALIGN for the buffers,
