@@ -25,7 +25,10 @@ input has the scale max |x| / 127 of the float32 tensor it reads
 (calibrated on the run itself) and is quantized by division, except an
 input that is the output of a conv: that conv writes it requantized (by the
 reciprocal, as above), one int8 tensor shared by every conv that reads it,
-whatever their paddings (the padding is storage, not arithmetic).  The filter is the
+whatever their paddings (the padding is storage, not arithmetic); and a
+concatenation whose parts are conv or pool outputs that nothing else reads:
+each part's producer writes its slice with the concatenation's scale (a
+conv part requantized, a pool part by division).  The filter is the
 batch-norm-folded one (``fold_bn``) quantized per output channel, and the
 conv's output is the float32 epilogue above; pools, concatenation, flatten
 and dense are the float32 oracle's own.
@@ -143,9 +146,12 @@ def act_scale(x):
 
 
 def conv_node_int8(n, x, residual=None, chained=False):
-    """One conv node through the integer path: (output, the input's scale);
-    `chained`: x is the float32 output of the conv that writes this conv's
-    input requantized."""
+    """One conv node through the integer path: (output, the input's scale).
+    How x becomes int8: `chained` True: x is the float32 output of the conv
+    that writes this conv's input requantized; False: quantized by division;
+    or a list of (channel count, chained) parts in channel order (a
+    concatenation whose parts' producers write their slices, each by its
+    own rule, with the concatenation's scale)."""
     if n.bn is not None:
         w, b = fold_bn(n.w, n.bias, n.bn)
     else:
@@ -153,7 +159,16 @@ def conv_node_int8(n, x, residual=None, chained=False):
         b = None if n.bias is None else np.asarray(n.bias, np.float32)
     xs = act_scale(x)
     wq, ws = quantize_filter(w)
-    acc = conv2d_int((requantize if chained else quantize)(x, xs), wq, n.stride, n.pad)
+    if isinstance(chained, list):
+        xq, c0 = [], 0
+        for cnt, ch in chained:
+            xq.append((requantize if ch else quantize)(x[:, c0:c0 + cnt], xs))
+            c0 += cnt
+        assert c0 == x.shape[1]
+        xq = np.concatenate(xq, axis=1)
+    else:
+        xq = (requantize if chained else quantize)(x, xs)
+    acc = conv2d_int(xq, wq, n.stride, n.pad)
     return epilogue_f32(acc, multipliers(xs, ws), b, residual, n.act), xs
 
 
@@ -164,16 +179,37 @@ def run_graph_int8(graph, x=None):
     x = graph.x if x is None else x
     vals = [None] * len(graph.nodes)
     scales = []
+    uses = [[] for _ in graph.nodes]
+    for i, n in enumerate(graph.nodes):
+        for j in n.inputs:
+            uses[j].append(i)
+        if n.residual >= 0:
+            uses[n.residual].append(i)
+
+    def rule(j):
+        """How a conv's input value j becomes int8 (conv_node_int8's chained)."""
+        src = graph.nodes[j]
+        if src.op == "conv":
+            return True
+        if src.op == "concat":
+            if all(graph.nodes[p].op in ("conv", "maxpool", "avgpool") and uses[p] == [j]
+                   for p in src.inputs):
+                return [(vals[p].shape[1], graph.nodes[p].op == "conv") for p in src.inputs]
+        return False
+
     for i, n in enumerate(graph.nodes):
         ins = [vals[j] for j in n.inputs]
         if n.op == "input":
             v = np.asarray(x, np.float32)
         elif n.op == "conv":
             # a conv's output is the one int8 tensor all convs reading it
-            # share (whatever their paddings), requantized by that conv;
-            # any other value is quantized by its own pass
-            chained = graph.nodes[n.inputs[0]].op == "conv"
-            v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None, chained)
+            # share (whatever their paddings), requantized by that conv; a
+            # concatenation of conv and pool outputs read by nothing else is
+            # assembled by its parts' producers, each with its own rule and
+            # the concatenation's scale; any other value is quantized by its
+            # own pass (a pool's output: by the pool, the same division)
+            v, xs = conv_node_int8(n, ins[0], vals[n.residual] if n.residual >= 0 else None,
+                                   rule(n.inputs[0]))
             scales.append(xs)
         elif n.op == "maxpool":
             v = fo.maxpool2d(ins[0], n.R, n.S, n.stride, n.pad)

@@ -239,3 +239,42 @@ def test_conv_output_read_with_two_paddings_is_requantized():
     y, scales = oq.run_graph_int8(g)
     np.testing.assert_array_equal(scales, np.float32([1.0, 7.0, 7.0]))
     np.testing.assert_array_equal(y, np.full((1, 2, 4, 5), 6223.0, np.float32))
+
+
+def test_concatenation_is_assembled_by_its_parts_producers():
+    """A concatenation of a conv's output and a pool's output (each read by
+    nothing else), read by a conv: its int8 tensor has the concatenation's
+    scale, the conv part requantized by the reciprocal and the pool part
+    quantized by division.  Both parts hold 45.5 at scale 7 (the exact tie
+    6.5): the conv part gives 7, the pool part 6, so the reading conv (delta
+    filters on one channel of each part) gives 127 * 7 * 7 = 6223 and
+    127 * 6 * 7 = 5334 at every pixel; quantizing the whole concatenation
+    one way would give one of them twice.  Scales by hand: 1 for the
+    input (its 127 sits in a channel no filter reads), 1 for it again, 7
+    for the concatenation (maximum 127 * 7 = 889 in the conv part)."""
+    from paper_1809_02697_amd.workloads import Graph, Node
+    rng = np.random.default_rng(5)
+    x = np.zeros((1, 3, 4, 5), np.float32)
+    x[0, 0] = rng.integers(-7, 8, (4, 5))
+    x[0, 0, 3, 4] = 7.0
+    x[0, 2, 0, 2] = 127.0
+    wa = np.zeros((2, 3, 1, 1), np.float32)
+    wa[0, 0] = 127.0
+    wa[1, 1] = 127.0
+    wb = np.zeros((2, 3, 1, 1), np.float32)
+    wb[0, 1] = 127.0     # the conv part's constant channel
+    wb[1, 2] = 127.0     # the pool part
+    nodes = [
+        Node("input"),
+        Node("conv", (0,), K=2, R=1, S=1, w=wa, bias=np.float32([0.0, 45.5])),
+        Node("conv", (0,), K=1, R=1, S=1, w=np.zeros((1, 3, 1, 1), np.float32), bias=np.float32([45.5])),
+        Node("maxpool", (2,), R=1, S=1, stride=(1, 1)),
+        Node("concat", (1, 3)),
+        Node("conv", (4,), K=2, R=1, S=1, w=wb),
+        Node("output", (5,)),
+    ]
+    g = Graph("assembled concatenation", nodes, x.shape, x)
+    y, scales = oq.run_graph_int8(g)
+    np.testing.assert_array_equal(scales, np.float32([1.0, 1.0, 7.0]))
+    want = np.stack([np.full((4, 5), 6223.0), np.full((4, 5), 5334.0)])[None].astype(np.float32)
+    np.testing.assert_array_equal(y, want)
