@@ -513,7 +513,8 @@ hipError_t group_by_tile(const ConvConfig& c, const I8GroupArgs& ga, int wgs, hi
 // configuration, operands and outputs).
 I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                     const float* wscale, float xscale, const float* bias, const float* res, float* y,
-                    int* acc, int8_t* yq, float yscale, int qph, int qpw, int xph, int xpw) {
+                    int* acc, int8_t* yq, float yscale, int qph, int qpw, int xph, int xpw,
+                    int q_off = -1, int q_tot = -1) {
     I8Args a;
     a.x = x;
     a.w = w;
@@ -528,9 +529,9 @@ I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, co
     a.qph = qph;
     a.qpw = qpw;
     // the int8 output takes the view of s when it is the only output; beside
-    // the float32 output it is a whole tensor of its own
-    a.q_off = y ? 0 : s.y_off;
-    a.q_tot = y ? cdiv(s.K, 16) : s.y_tot;
+    // the float32 output it is a whole tensor of its own; or the view given
+    a.q_off = q_off >= 0 ? q_off : y ? 0 : s.y_off;
+    a.q_tot = q_tot >= 0 ? q_tot : y ? cdiv(s.K, 16) : s.y_tot;
     a.N = s.N;
     a.CB = cdiv(s.C, 16);
     a.CG = cdiv(s.C, 64);
@@ -637,6 +638,15 @@ hipError_t launch_conv_int8(const ConvShape& s, const ConvConfig& c, const int8_
     return by_tile<kOutF32>(c, a, st);
 }
 
+hipError_t launch_conv_int8_m(const I8Member& m, const ConvConfig& c, hipStream_t st) {
+    if (!int8_config_valid(m.s, c) || m.xph < m.s.ph || m.xpw < m.s.pw || (!m.y && !m.yq))
+        return hipErrorInvalidValue;
+    const I8Args a = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
+                                  m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot);
+    if (m.yq) return m.y ? by_tile<kOutBoth>(c, a, st) : by_tile<kOutI8>(c, a, st);
+    return by_tile<kOutF32>(c, a, st);
+}
+
 static_assert(kMaxI8Group == kMaxGroupConvs, "group size");
 
 bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c) {
@@ -687,7 +697,7 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
         const I8Member& m = mem[order[j]];
         if ((!m.y && !m.yq) || m.xph < m.s.ph || m.xpw < m.s.pw) return hipErrorInvalidValue;
         ga.a[j] = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
-                               m.yscale, m.qph, m.qpw, m.xph, m.xpw);
+                               m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot);
         ga.cnt[j] = ga.a[j].ntiles;
         total_wgs += (long)cdiv(ga.cnt[j], conv_detail::kXcds) * conv_detail::kXcds;
         if (total_wgs >= (1L << 30)) return hipErrorInvalidValue;

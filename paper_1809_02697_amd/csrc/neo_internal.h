@@ -120,9 +120,8 @@ int tune_wino(const ConvShape& s, const float* x, const float* u, const float* b
 bool tuned_wino_config(const ConvShape& s, ConvConfig* out);
 // The same for the integer conv (configurations of int8_config_valid), keyed
 // also by its output mode `out` (0 float32, 2 int8, 3 both).
-int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
-              const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
-              hipStream_t st, ConvConfig* best, float* us, int xph = -1, int xpw = -1);
+struct I8Member;
+int tune_int8(const I8Member& m, hipStream_t st, ConvConfig* best, float* us);
 bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg);
 
 // Integer (INT8) convolution (conv_int8.hip): int8 NCHW16c activations with
@@ -179,6 +178,7 @@ struct PoolQ {
     int8_t* yq = nullptr;
     float scale = 1.f;
     int qph = 0, qpw = 0;
+    int q_off = 0, q_tot = 0;  // the output's blocks [q_off, q_off + CB) of q_tot (0: CB)
 };
 
 // A pooling step run by the last workgroups of a fused conv launch (it is
@@ -221,7 +221,12 @@ struct I8Member {
     float yscale;
     int qph, qpw;
     int xph, xpw;  // the halo of x, at least the conv's padding
+    // yq's view in blocks: [q_off, q_off + KB) of q_tot (-1: the view of s
+    // when y is null, else the whole [N][KB] tensor)
+    int q_off, q_tot;
 };
+// One integer conv from a member's operands (float32 and/or int8 outputs).
+hipError_t launch_conv_int8_m(const I8Member& m, const ConvConfig& c, hipStream_t st);
 bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);
 ConvConfig choose_int8_group_config(const ConvShape* s, int n);
 hipError_t launch_conv_int8_group(const I8Member* m, int n, const ConvConfig& c, const GroupPool* pool,

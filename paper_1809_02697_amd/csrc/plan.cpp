@@ -96,6 +96,9 @@ struct Step {
     ConvConfig c8{1, 1, 1, 1};
     int qc = -1, q_out = -1;
     bool quant_here = false, f32_needed = true;
+    // the slice of copy q_out this step writes, in blocks ([q_off8, q_off8 +
+    // its blocks) of q_tot8), when it is one part of a concatenation's copy
+    int q_off8 = -1, q_tot8 = -1;
 };
 
 // NEO_PLAN_INT8: the int8 copy of a value, its halo the largest padding of
@@ -107,6 +110,9 @@ struct I8Copy {
     long xq_off;
     float xscale = 1.f;
     int writer = -1;
+    // a concatenation's copy assembled by its parts' producers, each writing
+    // its slice (their steps carry q_out = this copy)
+    bool assembled = false;
 };
 
 struct Xform {
@@ -1029,6 +1035,8 @@ bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_ou
         gp->q.scale = qo.xscale;
         gp->q.qph = qo.ph;
         gp->q.qpw = qo.pw;
+        gp->q.q_off = ps.q_off8 >= 0 ? ps.q_off8 : 0;
+        gp->q.q_tot = ps.q_tot8 > 0 ? ps.q_tot8 : 0;
         if (!ps.f32_needed) gp->y = nullptr;
     }
     return true;
@@ -1090,6 +1098,54 @@ void plan_int8_copies(neo_plan* P) {
         for (Step& t : P->steps)
             if (t.qc == c) t.quant_here = false;
     }
+    // a concatenation (nothing produces it as a whole) whose parts are all
+    // produced by int8 convs or pooling steps: each part's producer writes
+    // its slice of the copy, with the concatenation's scale
+    for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
+        I8Copy& q = P->i8_copies[c];
+        const Val& cv = P->vals[q.val];
+        if (q.writer >= 0 || cv.node < 0 || P->nodes[cv.node].nd.op != NEO_OP_CONCAT || cv.layout != 16 ||
+            cv.view)
+            continue;
+        std::vector<std::pair<int, int>> parts;  // (producer step, block offset in the concatenation)
+        bool ok = true;
+        for (int j : P->nodes[cv.node].inputs) {
+            int u = -1;
+            for (int k = 0; k < (int)P->vals.size(); ++k)
+                if (P->vals[k].node == j && P->vals[k].view && P->vals[k].layout == cv.layout &&
+                    P->vals[k].alias_of < 0)
+                    u = k;
+            int w = -1;
+            for (int i = 0; ok && u >= 0 && i < ns; ++i) {
+                const Step& t = P->steps[i];
+                if (t.out == u && ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL))
+                    w = i;
+            }
+            if (u < 0 || w < 0 || P->steps[w].q_out >= 0) {
+                ok = false;
+                break;
+            }
+            parts.emplace_back(w, P->vals[u].c_off - cv.c_off);
+        }
+        if (!ok || parts.empty()) continue;
+        bool f32 = q.val == P->out_val || cv.view;
+        for (const Val& o : P->vals)
+            if (o.alias_of == q.val) f32 = true;
+        for (int i = 0; i < ns; ++i) {
+            const Step& t = P->steps[i];
+            if ((t.in == q.val && !(t.kind == ST_CONV && t.i8)) || t.res == q.val) f32 = true;
+        }
+        q.assembled = true;
+        for (const auto& pw : parts) {
+            Step& t = P->steps[pw.first];
+            t.q_out = c;
+            t.f32_needed = f32;
+            t.q_off8 = pw.second;
+            t.q_tot8 = cdiv(cv.C, 16);
+        }
+        for (Step& t : P->steps)
+            if (t.qc == c) t.quant_here = false;
+    }
 }
 
 // NEO_PLAN_INT8 with NEO_PLAN_GROUP: grouping reorders the steps, so the
@@ -1100,7 +1156,8 @@ void place_int8_quant_passes(neo_plan* P) {
     std::vector<char> seen(P->i8_copies.size(), 0);
     auto visit = [&](Step& t) {
         if (t.kind != ST_CONV || !t.i8) return;
-        const bool first = P->i8_copies[t.qc].writer < 0 && !seen[t.qc];
+        const I8Copy& q = P->i8_copies[t.qc];
+        const bool first = q.writer < 0 && !q.assembled && !seen[t.qc];
         t.quant_here = first;
         seen[t.qc] = 1;
     };
@@ -1171,7 +1228,9 @@ std::string describe(const neo_plan* P) {
                   << ",\"x_scale\":" << xs << ",\"calibrated\":" << (P->i8_ready ? "true" : "false")
                   << ",\"input_copy\":" << s.qc << ",\"quantizes_input\":"
                   << (s.quant_here ? "true" : "false") << ",\"writes_copy\":" << s.q_out
-                  << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false") << "}";
+                  << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false");
+                if (s.q_off8 >= 0) o << ",\"writes_slice\":[" << s.q_off8 << "," << s.q_tot8 << "]";
+                o << "}";
             }
             if (c.gap) o << ",\"gap_sums\":true";
             o << "}";
@@ -1196,9 +1255,12 @@ std::string describe(const neo_plan* P) {
             for (const Step& ps : s.pools) {
                 o << ",\"pool\":{\"kind\":\"" << kinds[ps.kind] << "\",\"node\":" << ps.node
                   << ",\"in\":" << ps.in << ",\"out\":" << ps.out;
-                if (ps.q_out >= 0)
+                if (ps.q_out >= 0) {
                     o << ",\"int8\":{\"writes_copy\":" << ps.q_out << ",\"writes_f32\":"
-                      << (ps.f32_needed ? "true" : "false") << "}";
+                      << (ps.f32_needed ? "true" : "false");
+                    if (ps.q_off8 >= 0) o << ",\"writes_slice\":[" << ps.q_off8 << "," << ps.q_tot8 << "]";
+                    o << "}";
+                }
                 o << "}";
             }
         }
@@ -1227,9 +1289,12 @@ std::string describe(const neo_plan* P) {
               << "],\"pad\":[" << ps.ph << "," << ps.pw << "],\"OH\":" << ps.OH << ",\"OW\":" << ps.OW
               << "}";
         }
-        if ((s.kind == ST_MAXPOOL || s.kind == ST_AVGPOOL) && s.q_out >= 0)
+        if ((s.kind == ST_MAXPOOL || s.kind == ST_AVGPOOL) && s.q_out >= 0) {
             o << ",\"int8\":{\"writes_copy\":" << s.q_out << ",\"writes_f32\":"
-              << (s.f32_needed ? "true" : "false") << "}";
+              << (s.f32_needed ? "true" : "false");
+            if (s.q_off8 >= 0) o << ",\"writes_slice\":[" << s.q_off8 << "," << s.q_tot8 << "]";
+            o << "}";
+        }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
         if (s.kind == ST_DENSE) {
             o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out;
@@ -1658,6 +1723,8 @@ static I8Member i8_member(const neo_plan* P, const Step& s, const float* x_nchw,
     m.qpw = qo ? qo->pw : 0;
     m.xph = qc.ph;
     m.xpw = qc.pw;
+    m.q_off = qo ? s.q_off8 : -1;
+    m.q_tot = qo ? s.q_tot8 : -1;
     return m;
 }
 
@@ -1691,21 +1758,8 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     // the input's int8 copy (quantized here by the first
                     // reader, unless its producer wrote it), the integer conv,
                     // its float32 output and/or the int8 copy it writes
-                    const Val& in = P->vals[s.in];
-                    const I8Copy& qc = P->i8_copies[s.qc];
-                    int8_t* xq = P->d_i8 + qc.xq_off;
-                    if (s.quant_here)
-                        e = launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
-                                                 qc.ph, qc.pw, qc.xscale, xq, st);
-                    const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
-                    float* y = (!qo || s.f32_needed) ? val_ptr(P, s.out, x_nchw, y_out) : nullptr;
-                    if (e == hipSuccess)
-                        e = launch_conv_int8(s.cs, s.c8, xq, P->d_i8 + s.w8_off, prm + s.ws8_off, qc.xscale,
-                                             s.b_off >= 0 ? prm + s.b_off : nullptr,
-                                             s.res >= 0 ? val_ptr(P, s.res, x_nchw, y_out) : nullptr, y,
-                                             nullptr, qo ? P->d_i8 + qo->xq_off : nullptr,
-                                             qo ? qo->xscale : 1.f, qo ? qo->ph : 0, qo ? qo->pw : 0, st,
-                                             qc.ph, qc.pw);
+                    e = i8_quant_pass(P, s, x_nchw, y_out, st);
+                    if (e == hipSuccess) e = launch_conv_int8_m(i8_member(P, s, x_nchw, y_out), s.c8, st);
                     break;
                 }
                 if (s.wino) {
@@ -1790,6 +1844,8 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     q.scale = qo.xscale;
                     q.qph = qo.ph;
                     q.qpw = qo.pw;
+                    q.q_off = s.q_off8 >= 0 ? s.q_off8 : 0;
+                    q.q_tot = s.q_tot8 > 0 ? s.q_tot8 : 0;
                     e = launch_pool_q(s.ps, s.kind == ST_MAXPOOL, val_ptr(P, s.in, x_nchw, y_out),
                                       s.f32_needed ? val_ptr(P, s.out, x_nchw, y_out) : nullptr, q, st);
                 } else if (s.kind == ST_MAXPOOL) {
@@ -1909,8 +1965,7 @@ static int tune_plan(neo_plan* P) {
             for (int m = 0; m < n && rc == NEO_OK; ++m) {
                 float us = 0.f;
                 const I8Member& q = mem[m];
-                rc = tune_int8(q.s, q.x, q.w, q.wscale, q.bias, q.res, q.y, q.yq, q.qph, q.qpw, P->cap_stream,
-                               &own[m], &us, q.xph, q.xpw);
+                rc = tune_int8(q, P->cap_stream, &own[m], &us);
                 alone_us += us;
             }
             if (rc != NEO_OK) break;
@@ -2096,14 +2151,7 @@ static int tune_plan(neo_plan* P) {
         }
         if (s.kind == ST_CONV && s.i8) {
             // an integer conv: its configurations timed with its own output mode
-            const I8Copy* qo = s.q_out >= 0 ? &P->i8_copies[s.q_out] : nullptr;
-            const I8Copy& qc = P->i8_copies[s.qc];
-            rc = tune_int8(s.cs, P->d_i8 + qc.xq_off, P->d_i8 + s.w8_off,
-                           P->d_params + s.ws8_off, s.b_off >= 0 ? P->d_params + s.b_off : nullptr,
-                           s.res >= 0 ? val_ptr(P, s.res, xin, yout) : nullptr,
-                           (!qo || s.f32_needed) ? val_ptr(P, s.out, xin, yout) : nullptr,
-                           qo ? P->d_i8 + qo->xq_off : nullptr, qo ? qo->ph : 0, qo ? qo->pw : 0,
-                           P->cap_stream, &s.c8, nullptr, qc.ph, qc.pw);
+            rc = tune_int8(i8_member(P, s, xin, yout), P->cap_stream, &s.c8, nullptr);
             s.tuned = rc == NEO_OK;
             next.push_back(s);
             continue;
@@ -2238,6 +2286,21 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
         const Val& a = P->vals[v];
         return (long)a.N * cdiv(a.C, 16) * 16 * a.H * a.W;
     };
+    // an assembled copy's parts (the steps writing its slices; group members
+    // with their group's configuration), and whether its scale is set
+    std::vector<std::vector<Step>> parts(P->i8_copies.size());
+    for (const Step& t : P->steps) {
+        auto add = [&](const Step& x, const ConvConfig* c8) {
+            if (x.q_out < 0 || !P->i8_copies[x.q_out].assembled) return;
+            Step one = x;
+            if (c8) one.c8 = *c8;
+            parts[x.q_out].push_back(one);
+        };
+        add(t, nullptr);
+        for (const Step& m : t.members) add(m, t.i8 ? &t.c8 : nullptr);
+        for (const Step& pl : t.pools) add(pl, nullptr);
+    }
+    std::vector<char> assembled(P->i8_copies.size(), 0);
     // one step as the calibration runs it: a group's members (and its pool)
     // one by one, which computes what the group launch does
     std::function<int(const Step&)> calibrate_step = [&](const Step& s) -> int {
@@ -2255,11 +2318,28 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
             return NEO_OK;
         }
         int rc;
+        if (s.kind == ST_CONV && s.i8 && P->i8_copies[s.qc].assembled && !assembled[s.qc]) {
+            // the first reader of an assembled copy: every part has run in
+            // float32; the scale of the whole concatenation, then the parts
+            // again, now writing their slices
+            I8Copy& q = P->i8_copies[s.qc];
+            if ((rc = scale_of(val_ptr(P, q.val, x_nchw, y_out), elems(q.val), &q.xscale)) != NEO_OK) return rc;
+            for (const Step& part : parts[s.qc])
+                if ((rc = enqueue_step(P, part, x_nchw, y_out, st)) != NEO_OK) return rc;
+            assembled[s.qc] = 1;
+        }
         // a copy quantized by its own pass: the scale of the value it reads
         if (s.kind == ST_CONV && s.i8 && s.quant_here &&
             (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in),
                            &P->i8_copies[s.qc].xscale)) != NEO_OK)
             return rc;
+        if (s.q_out >= 0 && P->i8_copies[s.q_out].assembled) {
+            // a part of an assembled copy: float32 only until the copy's scale is known
+            P->i8_f32_out = true;
+            rc = enqueue_step(P, s, x_nchw, y_out, st);
+            P->i8_f32_out = false;
+            return rc;
+        }
         if (s.q_out >= 0) {
             // a copy's writer (conv or pool): run it once with its float32
             // output only, take the copy's scale from that, then run it as

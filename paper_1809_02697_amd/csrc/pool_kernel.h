@@ -109,7 +109,9 @@ __device__ __forceinline__ void pool_elem(const float* __restrict__ x, float* __
                 packed |= ((unsigned)(int)r & 0xffu) << (8 * i);
             }
             const int owq = s.OW + 2 * q.qpw;
-            const long at = (((long)(n * CB + cb) * (s.OH + 2 * q.qph) + oh + q.qph) * owq + ow + q.qpw) * 16 + 4 * qd;
+            const int qtot = q.q_tot > 0 ? q.q_tot : CB;
+            const long at =
+                (((long)(n * qtot + q.q_off + cb) * (s.OH + 2 * q.qph) + oh + q.qph) * owq + ow + q.qpw) * 16 + 4 * qd;
             *reinterpret_cast<unsigned*>(q.yq + at) = packed;
         }
     }

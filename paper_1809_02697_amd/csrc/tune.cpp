@@ -274,10 +274,9 @@ bool tuned_int8_config(const ConvShape& s, int out, ConvConfig* cfg) {
 
 // Every valid integer-conv configuration, timed with the caller's buffers
 // (their contents do not change the time); keeps the fastest with its time.
-int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float* wscale,
-              const float* bias, const float* res, float* y, int8_t* yq, int qph, int qpw,
-              hipStream_t st, ConvConfig* best_out, float* us_out, int xph, int xpw) {
-    const int out = yq ? (y ? 3 : 2) : 0;
+int tune_int8(const I8Member& m, hipStream_t st, ConvConfig* best_out, float* us_out) {
+    const ConvShape& s = m.s;
+    const int out = m.yq ? (m.y ? 3 : 2) : 0;
     const GroupKey key = i8_key(s, out);
     {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -299,8 +298,7 @@ int tune_int8(const ConvShape& s, const int8_t* x, const int8_t* w, const float*
                     const ConvConfig c{fk, fp, 1, wv};
                     if (!int8_config_valid(s, c)) continue;
                     float us = 0.f;
-                    e = time_launch([&] { return launch_conv_int8(s, c, x, w, wscale, 1.f, bias, res, y,
-                                                                  nullptr, yq, 1.f, qph, qpw, st, xph, xpw); },
+                    e = time_launch([&] { return launch_conv_int8_m(m, c, st); },
                                     st, ev.e0, ev.e1, &us);
                     if (e != hipSuccess) break;
                     if (us < best_us) {
