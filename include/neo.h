@@ -453,8 +453,11 @@ enum neo_plan_flags {
      * copy (requantized by the float32 reciprocal of the scale); when a
      * pooling step does, the pool writes it (quantized by division, as the
      * pass would); either beside its float32 output when anything else
-     * reads that.  Otherwise (the network input, a concatenation) the first
-     * reader runs the quantization pass.  Pools, concatenation, flatten and
+     * reads that.  A concatenation whose parts are all conv or pool outputs
+     * is assembled by its parts' producers, each writing its slice of the
+     * copy with the concatenation's scale.  Otherwise (the network input, a
+     * concatenation of concatenations) the first reader runs the
+     * quantization pass.  Pools, concatenation, flatten and
      * dense compute in float32.  The input scales come
      * from neo_plan_calibrate_int8, which must run before the plan does.
      * Convs run in NCHW16c: block 16, and no NAIVE, GLOBAL_SEARCH, WINOGRAD
@@ -521,7 +524,9 @@ int neo_run_step(neo_plan* plan, int step, const float* x_nchw, float* y_out, ne
  * `stream` and, just before each conv, set that conv's input scale to
  * max|x| / 127 in float32 over its float32 input as this run produced it
  * (1 for an all-zero input; a copy's writer, conv or pool, runs once with
- * its float32 output only for that, then as the plan does; the members of a
+ * its float32 output only for that, then as the plan does; the parts of an
+ * assembled concatenation run in float32 only, and again with their slices
+ * once the first reader has set the concatenation's scale; the members of a
  * group launch run one by one, which computes the same values).
  * Synchronizes the stream once per conv (the maximum is read back); drops
  * a captured graph, which the next
