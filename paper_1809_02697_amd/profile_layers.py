@@ -6,6 +6,7 @@
     rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 ... (the same workload)
     ... profile_layers TUNE_DB --batch 32 --winograd [--reps 20]   (Winograd plan)
     ... profile_layers --int8 --batch 32 [--reps 20]    (the integer convs, no plan)
+    ... profile_layers --int8-plan MODEL --batch 1 --reps 20   (a whole int8 network)
 
 Builds the plan bench.py times (batch 1: the headline plan; batch 32: the
 tuned one-block plan of the batch-32 layer table).  TUNE_DB is a local-search
@@ -66,6 +67,33 @@ def int8_main(neo, torch, wl, batch, reps):
           file=sys.stderr)
 
 
+def int8_plan_main(neo, torch, wl, model, batch, reps):
+    """The integer network bench.py times as its int8_grouped entry
+    (NEO_PLAN_INT8 | GROUP | TUNE | HIPGRAPH, calibrated on the network's
+    input): one forward, the calibration copy, then `reps` forwards step by
+    step, each step alone on the GPU (a synchronize after it: under the
+    profiler, back-to-back launches run slower than they do unprofiled) --
+    the dispatches after the copy, in equal runs."""
+    g = wl.MODELS[model](batch)
+    x = torch.from_numpy(g.x).cuda()
+    plan = neo.Plan(g, flags=neo.PLAN_INT8 | neo.PLAN_GROUP | neo.PLAN_TUNE | neo.PLAN_HIPGRAPH)
+    out = plan.calibrate_int8(x)
+    plan.run(x, out)
+    torch.cuda.synchronize()
+    a = torch.ones(COPY_MB * 2 ** 18, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    d = plan.describe()
+    for _ in range(reps):
+        for i in range(len(d["steps"])):
+            plan.run_step(i, x, out)
+            torch.cuda.synchronize()
+    print(f"profiled {reps} int8 forwards of {model} batch {batch} ({len(d['steps'])} steps) "
+          f"after a {COPY_MB} MB copy", file=sys.stderr)
+    plan.destroy()
+
+
 def main():
     import torch
 
@@ -84,9 +112,14 @@ def main():
     ap.add_argument("--int8", action="store_true",
                     help="instead of a plan: the 23 ResNet-50 conv shapes through the integer "
                          "path (bench.py's int8 layer table), after the copy, --reps times")
+    ap.add_argument("--int8-plan", metavar="MODEL",
+                    help="instead: the tuned, grouped int8 plan of MODEL (resnet50, vgg16, "
+                         "inception_v3), --reps graph replays after the copy")
     args = ap.parse_args()
     if args.int8:
         return int8_main(neo, torch, wl, args.batch, args.reps)
+    if args.int8_plan:
+        return int8_plan_main(neo, torch, wl, args.int8_plan, args.batch, args.reps)
     plan, g = build_plan(neo, torch, wl, args.db, args.batch, args.winograd)
     if args.describe:
         with open(args.describe, "w") as f:

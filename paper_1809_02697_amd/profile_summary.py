@@ -95,6 +95,20 @@ INT8_COMMANDS = [
     "python -m paper_1809_02697_amd.profile_summary RUN_DIR",
 ]
 
+# whole integer networks at batch 1 (the bench line's int8_grouped plans),
+# summarized by write_int8_plans
+INT8_PLAN_MODELS = ("resnet50", "inception_v3", "vgg16")
+INT8_PLAN_REPS = 20
+INT8_PLAN_COMMANDS = [
+    f"rocprofv3 --kernel-trace --stats --output-format csv -d RUN_DIR/prof_i8plan -o {m} -- "
+    f"python -m paper_1809_02697_amd.profile_layers --int8-plan {m} --batch 1 --reps {INT8_PLAN_REPS}"
+    for m in INT8_PLAN_MODELS] + ["python -m paper_1809_02697_amd.profile_summary RUN_DIR"]
+# kernel name -> the part of an integer forward it does (first match)
+INT8_PLAN_KINDS = [("conv_i8_group", "int8 conv group launches"), ("conv_i8", "int8 convs alone"),
+                   ("quantize_kernel", "quantization passes"), ("pool_blk_q", "pools writing an int8 copy"),
+                   ("pool_blk", "float32 pools"), ("gap_blk", "global average pool"),
+                   ("dense_", "dense layers"), ("_to_", "layout transforms")]
+
 
 def kernel_hash():
     """sha256[:16] of the conv kernel's sources (templates and instantiations)."""
@@ -493,9 +507,75 @@ def write_int8(run_dir):
         f.write("\n".join(md) + "\n")
 
 
+def write_int8_plans(run_dir):
+    """profiles/int8_plans_b1.md: where the time of one integer forward at
+    batch 1 goes (the tuned, grouped plans the bench line's int8 entries
+    time), from the kernel-trace timestamps of graph-replayed forwards."""
+    md = ["# Integer networks at batch 1 (NEO_PLAN_INT8 | GROUP | TUNE)", "",
+          "Commands (from the repository root on one MI355X; RUN_DIR = the directory they write to):",
+          "", "```"] + INT8_PLAN_COMMANDS + ["```", "",
+          f"Each workload calibrates the plan on the network's input, runs one forward, a plain copy "
+          f"(the marker), then {INT8_PLAN_REPS} forwards step by step, each step alone on the GPU "
+          "(under the profiler, back-to-back launches run slower than unprofiled; launched alone "
+          "their durations match HIP-event timings).  Per forward: the dispatches after the copy "
+          "in equal runs, each kernel's kernel-trace duration summed by what it does (median over "
+          "the forwards, the first dropped).  Launched alone, each of these small kernels pays "
+          "its whole start-up (wave launch, instruction and argument fetch), which the "
+          "unprofiled graph replays of the bench line (models.*.int8_grouped) overlap with the "
+          "previous kernel's tail: the sums below exceed that end-to-end latency, so read the "
+          "shares, not the absolute times.", ""]
+    e2e = {}
+    try:
+        line = open(os.path.join(run_dir, "bench.log")).read().strip().splitlines()[-1]
+        for k, v in (json.loads(line).get("models") or {}).items():
+            if isinstance(v.get("int8_grouped"), dict):
+                e2e[k] = v["int8_grouped"]["ms"]
+    except (OSError, ValueError, IndexError):
+        pass
+    for m in INT8_PLAN_MODELS:
+        path = os.path.join(run_dir, "prof_i8plan", f"{m}_kernel_trace.csv")
+        if not os.path.exists(path):
+            continue
+        rows = sorted(_rows(path), key=lambda r: int(r["Start_Timestamp"]))
+        last_copy = max(i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"])
+        fwd = rows[last_copy + 1:]
+        n = len(fwd) // INT8_PLAN_REPS
+        assert n > 0 and len(fwd) == n * INT8_PLAN_REPS, (m, len(fwd))
+        kinds = {}
+        spans, totals = [], []
+        for r in range(1, INT8_PLAN_REPS):
+            part = fwd[r * n:(r + 1) * n]
+            spans.append((int(part[-1]["End_Timestamp"]) - int(part[0]["Start_Timestamp"])) / 1e3)
+            per = {}
+            for row in part:
+                name = row["Kernel_Name"]
+                kind = next((k for pat, k in INT8_PLAN_KINDS if pat in name), "other")
+                t = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3
+                c, u = per.get(kind, (0, 0.0))
+                per[kind] = (c + 1, u + t)
+            for kind, (c, u) in per.items():
+                kinds.setdefault(kind, []).append((c, u))
+            totals.append(sum(u for _, u in per.values()))
+        ref = (f"; the bench run of this directory replays the forward in {e2e[m + '_b1'] * 1e3:.1f} us"
+               if m + "_b1" in e2e else "")
+        md += [f"## {m}", "",
+               f"{n} dispatches per forward; kernel time, each launched alone, {_median(totals):.1f} us{ref}.",
+               "",
+               "| part | dispatches | us per forward | share of kernel time |", "|---|---:|---:|---:|"]
+        tot = _median(totals)
+        for kind, vals in sorted(kinds.items(), key=lambda kv: -_median([u for _, u in kv[1]])):
+            u = _median([u for _, u in vals])
+            md.append(f"| {kind} | {vals[0][0]} | {u:.1f} | {100 * u / tot:.0f} % |")
+        md.append("")
+    with open(os.path.join(PROFILES, "int8_plans_b1.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+
+
 if __name__ == "__main__":
     if len(sys.argv) != 2:
         sys.exit("usage: python -m paper_1809_02697_amd.profile_summary RUN_DIR")
+    if os.path.isdir(os.path.join(sys.argv[1], "prof_i8plan")):
+        write_int8_plans(sys.argv[1])
     if os.path.exists(os.path.join(sys.argv[1], "prof_i8", "i8_kernel_trace.csv")):
         write_int8(sys.argv[1])
     if os.path.exists(os.path.join(sys.argv[1], "bench.log")):
