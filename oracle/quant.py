@@ -30,8 +30,11 @@ concatenation whose parts are conv or pool outputs that nothing else reads:
 each part's producer writes its slice with the concatenation's scale (a
 conv part requantized, a pool part by division).  The filter is the
 batch-norm-folded one (``fold_bn``) quantized per output channel, and the
-conv's output is the float32 epilogue above; pools, concatenation, flatten
-and dense are the float32 oracle's own.
+conv's output is the float32 epilogue above.  Dense layers take the same
+path: weights quantized per output row, the flattened input with one scale
+(requantized by the producing dense layer, else quantized by division),
+exact integer dot products, the same float32 epilogue.  Pools,
+concatenation and flatten are the float32 oracle's own.
 
 Only ``tests/`` use this module.  It shares no code with the HIP library.
 """
@@ -172,9 +175,33 @@ def conv_node_int8(n, x, residual=None, chained=False):
     return epilogue_f32(acc, multipliers(xs, ws), b, residual, n.act), xs
 
 
+def dense_int(xq, wq):
+    """Exact integer dot products acc[n, k] = sum_i xq[n, i] * wq[k, i]
+    (int64: |acc| <= 127^2 * IN)."""
+    return np.asarray(xq, np.int64) @ np.asarray(wq, np.int64).T
+
+
+def dense_node_int8(n, x, chained=False):
+    """One dense node through the integer path: (output, the input's scale).
+    The weights [out][in] are quantized per output row (quantize_filter on
+    [out][in][1][1]), the input (flattened) with one scale; `chained`: x is
+    the float32 output of the dense layer that writes this one's input
+    requantized, else it is quantized by division.  The output is the conv's
+    float32 epilogue on the exact sums (bias, activation)."""
+    x2 = np.asarray(x, np.float32).reshape(x.shape[0], -1)
+    w = np.asarray(n.w, np.float32)
+    b = None if n.bias is None else np.asarray(n.bias, np.float32)
+    xs = act_scale(x2)
+    wq, ws = quantize_filter(w.reshape(w.shape[0], w.shape[1], 1, 1))
+    acc = dense_int((requantize if chained else quantize)(x2, xs), wq.reshape(w.shape))
+    y = epilogue_f32(acc[:, :, None, None], multipliers(xs, ws), b, None, n.act)
+    return y[:, :, 0, 0], xs
+
+
 def run_graph_int8(graph, x=None):
-    """A network description with every conv through the integer path, node
-    by node; returns (output, the convs' input scales in node order)."""
+    """A network description with every conv and dense layer through the
+    integer path, node by node; returns (output, their input scales in node
+    order)."""
     import oracle as fo
     x = graph.x if x is None else x
     vals = [None] * len(graph.nodes)
@@ -222,9 +249,14 @@ def run_graph_int8(graph, x=None):
         elif n.op == "flatten":
             v = fo.flatten(ins[0])
         elif n.op == "dense":
-            v = fo.dense(ins[0], n.w, n.bias)
-            if n.act == "relu":
-                v = fo.relu(v)
+            # a dense layer's output read by the next dense layer (through a
+            # flatten, if any) is requantized by it; any other input is
+            # quantized by division
+            src = n.inputs[0]
+            while graph.nodes[src].op == "flatten":
+                src = graph.nodes[src].inputs[0]
+            v, xs = dense_node_int8(n, ins[0], graph.nodes[src].op == "dense")
+            scales.append(xs)
         elif n.op == "output":
             v = ins[0]
         else:

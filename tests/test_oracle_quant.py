@@ -170,7 +170,11 @@ def _integer_graph():
     max 127, convs whose filters are 127 times a 0/1 pattern (per-channel
     scale 1), so each conv's output is 127 times its input's integers and
     the next scale a power of 127.  Conv 1's output is read by conv 2 alone
-    (a chained, requantized input); the rest take their own quantization."""
+    (a chained, requantized input); the rest take their own quantization.
+    The dense layer reads the concatenation [P, 128 P] (P the pool's output,
+    128 P the residual block's) at scale 128 * 127^2: the 128 P half
+    quantizes exactly, and the dense weights (127 times a -1/0/1 pattern,
+    row scale 1) are zero on the P half, whose quantization is not exact."""
     from paper_1809_02697_amd.workloads import Graph, Node
     rng = np.random.default_rng(12)
     x = rng.integers(-127, 128, (2, 3, 6, 5)).astype(np.float32)
@@ -179,6 +183,9 @@ def _integer_graph():
     shift = np.zeros((3, 3, 3, 3), np.float32)
     for k in range(3):
         shift[k, k, 1, 1] = 127.0        # a centred delta: the identity with padding
+    wd = np.zeros((4, 6 * 3 * 2), np.float32)
+    wd[:, 18:] = 127.0 * rng.integers(-1, 2, (4, 18))
+    wd[:, 18] = 127.0                    # every row nonzero: row scale 1
     nodes = [
         Node("input"),
         Node("conv", (0,), K=3, R=1, S=1, w=eye(3, 3)),                       # 127 x
@@ -187,7 +194,7 @@ def _integer_graph():
         Node("conv", (3,), K=3, R=1, S=1, w=eye(3, 3), residual=3, act="relu"),
         Node("concat", (3, 4)),
         Node("flatten", (5,)),
-        Node("dense", (6,), K=4, w=rng.integers(-2, 3, (4, 6 * 3 * 2)).astype(np.float32)),
+        Node("dense", (6,), K=4, w=wd),
         Node("output", (7,)),
     ]
     return Graph("integer", nodes, x.shape, x)
@@ -197,12 +204,51 @@ def test_integer_network_equals_the_float_network():
     """Every scale is a power of 127 and every quantization exact (the last
     conv's products round once, on both sides alike), so the integer path
     reproduces the float oracle's network exactly, with the scales fixed by
-    hand: 1 for the input, 127 for conv 1's output, 127^2 for the pool's."""
+    hand: 1 for the input, 127 for conv 1's output, 127^2 for the pool's,
+    128 * 127^2 for the dense layer's input (the dense sums stay below 2^24
+    and round once on both sides)."""
     import oracle as fo
     g = _integer_graph()
     y8, scales = oq.run_graph_int8(g)
-    np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 16129.0]))
+    np.testing.assert_array_equal(scales, np.float32([1.0, 127.0, 16129.0, 128.0 * 16129.0]))
     np.testing.assert_array_equal(y8, fo.run_graph(g))
+
+
+def test_dense_layers_chain_by_requantization():
+    """A dense layer's output read by the next dense layer is requantized
+    (the reciprocal), the network input of the first quantized by division.
+    By hand: the input [7, 0, 127] has scale 1; dense 1 (rows 127 e0 and
+    127 e1, row scale 1, bias [0, 45.5]) gives [889, 45.5], scale 7; 45.5 / 7
+    is the exact tie 6.5, requantized to 7 (division: 6), 889 to 127; dense 2
+    (rows 127 e1 and 127 e0) then gives 127 * 7 * 7 = 6223 and
+    127 * 127 * 7 = 112903."""
+    from paper_1809_02697_amd.workloads import Graph, Node
+    x = np.float32([7.0, 0.0, 127.0]).reshape(1, 3, 1, 1)
+    wa = np.float32([[127, 0, 0], [0, 127, 0]])
+    wb = np.float32([[0, 127], [127, 0]])
+    nodes = [
+        Node("input"),
+        Node("flatten", (0,)),
+        Node("dense", (1,), K=2, w=wa, bias=np.float32([0.0, 45.5])),
+        Node("dense", (2,), K=2, w=wb),
+        Node("output", (3,)),
+    ]
+    y, scales = oq.run_graph_int8(Graph("dense chain", nodes, x.shape, x))
+    np.testing.assert_array_equal(scales, np.float32([1.0, 7.0]))
+    np.testing.assert_array_equal(y, np.float32([[6223.0, 112903.0]]))
+
+
+def test_integer_dense_sums_exactly():
+    """dense_int is the exact integer matrix product: brute force on a small
+    case, and the extreme 127^2 * 25088 (VGG-16's first dense layer)."""
+    rng = np.random.default_rng(9)
+    xq = rng.integers(-127, 128, (3, 37)).astype(np.int8)
+    wq = rng.integers(-127, 128, (5, 37)).astype(np.int8)
+    want = np.array([[sum(int(xq[n, i]) * int(wq[k, i]) for i in range(37)) for k in range(5)]
+                     for n in range(3)])
+    np.testing.assert_array_equal(oq.dense_int(xq, wq), want)
+    big = oq.dense_int(np.full((1, 25088), 127, np.int8), np.full((2, 25088), -127, np.int8))
+    assert big.dtype == np.int64 and (big == -127 * 127 * 25088).all()
 
 
 def test_conv_output_read_with_two_paddings_is_requantized():
