@@ -395,14 +395,18 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* x, int H, in
 
 // max |x| over n floats (n a multiple of 4, 16-byte aligned) into *out as
 // the float's bits (non-negative floats order like their bit patterns): a
-// grid-stride float4 pass, a wave maximum, one vector atomic per wave.
-// *out must hold 0 before (absmax_clear).
-__global__ __launch_bounds__(256) void absmax_kernel(const float* x, long n4, unsigned* out) {
+// grid-stride float4 pass (the last n % 4 floats by the first threads), a
+// wave maximum, one vector atomic per wave.  *out must hold 0 before
+// (absmax_clear).
+__global__ __launch_bounds__(256) void absmax_kernel(const float* x, long n, unsigned* out) {
     float m = 0.f;
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
+    const long n4 = n / 4;
+    const long t0 = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    for (long i = t0; i < n4; i += (long)gridDim.x * blockDim.x) {
         const v4f v = reinterpret_cast<const v4f*>(x)[i];
         m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
     }
+    if (t0 < n - 4 * n4) m = fmaxf(m, fabsf(x[4 * n4 + t0]));
 #pragma unroll
     for (int d = 32; d > 0; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
     if ((threadIdx.x & 63) == 0) atomicMax(out, __float_as_uint(m));
@@ -448,6 +452,118 @@ __global__ __launch_bounds__(256) void pack_filter_i8_kernel(const float* w, int
         }
         const int cg = c >> 6, gg = (c >> 4) & 3, b = c & 15;
         wq[((((long)kb * R + r) * S + sx) * CG + cg) * 1024 + (gg * 16 + kk) * 16 + b] = q;
+    }
+}
+
+// Integer dense layer (the fully connected layers of integer inference):
+// acc[n][k] = sum_i xq[n][i] * wq[k][i], exact in int32 (|acc| <= 127^2 * IN),
+// then the conv's float32 epilogue.  Rows of xq and wq are padded with zeros
+// to INp = 16 * in16 bytes.  One wave per output row k: its lanes take the
+// row's 16-byte chunks in turn (one load, four 4-byte dot products per chunk
+// and image), keep one sum per image, and add them across the wave; lane n
+// then finishes image n0 + n.  Images n0 .. n0 + NB - 1 per launch.
+struct DenseI8Args {
+    const int8_t* x;      // [N][INp]
+    const int8_t* w;      // [OUT][INp]
+    const float* wscale;  // [OUT]
+    float xscale;
+    const float* bias;    // [OUT] or null
+    float* y;             // [N][OUT] or null
+    int8_t* yq;           // [N][OUTq] or null: y requantized by yrcp
+    float yrcp;
+    int N, in16, OUT, OUTq, act, n0;
+};
+
+template <int NB>
+__global__ __launch_bounds__(256) void dense_i8(DenseI8Args a) {
+    const int lane = threadIdx.x & 63;
+    const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (k >= a.OUT) return;
+    const long inp = 16L * a.in16;
+    int acc[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) acc[n] = 0;
+    const int nb = min(NB, a.N - a.n0);
+    const v4i* wr = reinterpret_cast<const v4i*>(a.w + k * inp);
+    for (int c = lane; c < a.in16; c += 64) {
+        const v4i wv = wr[c];
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+            if (n < nb) {
+                const v4i xv = reinterpret_cast<const v4i*>(a.x + (a.n0 + n) * inp)[c];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[n] = __builtin_amdgcn_sdot4(wv[j], xv[j], acc[n], false);
+            }
+        }
+    }
+#pragma unroll
+    for (int n = 0; n < NB; ++n)
+#pragma unroll
+        for (int d = 32; d > 0; d >>= 1) acc[n] += __shfl_xor(acc[n], d, 64);
+    // lane n keeps image n's sum (a select chain, not a dynamic register index)
+    int mine = acc[0];
+#pragma unroll
+    for (int n = 1; n < NB; ++n) mine = lane == n ? acc[n] : mine;
+    if (lane >= nb) return;
+    const int img = a.n0 + lane;
+    float o;
+    {
+#pragma clang fp contract(off)
+        const float m = a.xscale * a.wscale[k];
+        o = (float)mine * m;
+        if (a.bias) o = o + a.bias[k];
+    }
+    if (a.act == NEO_ACT_RELU) o = o > 0.f ? o : 0.f;
+    if (a.y) a.y[(long)img * a.OUT + k] = o;
+    if (a.yq) {
+        float q;
+        {
+#pragma clang fp contract(off)
+            q = rintf(o * a.yrcp);
+        }
+        q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
+        a.yq[(long)img * a.OUTq + k] = (int8_t)(int)q;
+    }
+}
+
+// float32 [N][IN] -> int8 [N][INp] (the padding bytes are not written):
+// clamp(round_half_even(x / scale), -127, 127), the division in float32.
+__global__ __launch_bounds__(256) void quantize_rows_kernel(const float* x, long total, int IN, long inp,
+                                                            float scale, int8_t* q) {
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= total) return;
+    const long n = t / IN;
+    const int i = (int)(t - n * IN);
+    float r = rintf(x[t] / scale);
+    r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
+    q[n * inp + i] = (int8_t)(int)r;
+}
+
+// A dense layer's weights [OUT][IN] float32 -> per-row scales max|w[k]| / 127
+// (1 for a zero row) and int8 rows [OUT][INp] (padding 0), one workgroup per row.
+__global__ __launch_bounds__(256) void pack_dense_i8_kernel(const float* w, int IN, long inp, int8_t* wq,
+                                                            float* wscale) {
+    const int k = blockIdx.x;
+    __shared__ float red[256];
+    float m = 0.f;
+    for (long i = threadIdx.x; i < IN; i += 256) m = fmaxf(m, fabsf(w[(long)k * IN + i]));
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + h]);
+        __syncthreads();
+    }
+    const float mx = red[0];
+    const float s = mx > 0.f ? mx / (float)kQMax : 1.f;
+    if (threadIdx.x == 0) wscale[k] = s;
+    for (long i = threadIdx.x; i < inp; i += 256) {
+        int8_t q = 0;
+        if (i < IN) {
+            float v = rintf(w[(long)k * IN + i] / s);
+            v = v > (float)kQMax ? (float)kQMax : (v < -(float)kQMax ? -(float)kQMax : v);
+            q = (int8_t)(int)v;
+        }
+        wq[(long)k * inp + i] = q;
     }
 }
 
@@ -602,7 +718,7 @@ hipError_t launch_absmax(const float* x, long n, unsigned* out, hipStream_t st) 
     hipLaunchKernelGGL(absmax_clear, dim3(1), dim3(64), 0, st, out);
     const long n4 = n / 4;
     const long blocks = std::min<long>(2048, std::max<long>(1, (n4 + 255) / 256));
-    hipLaunchKernelGGL(absmax_kernel, dim3((unsigned)blocks), dim3(256), 0, st, x, n4, out);
+    hipLaunchKernelGGL(absmax_kernel, dim3((unsigned)blocks), dim3(256), 0, st, x, n, out);
     return hipGetLastError();
 }
 
@@ -729,6 +845,58 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
         pp.wgs = (int)std::min<long>(1024, std::max<long>(1, (total + per - 1) / per));
     }
     return group_by_tile(c, ga, ga.start[n] + pp.wgs, st);
+}
+
+size_t dense_i8_row_bytes(int IN) { return (size_t)cdiv(IN, 16) * 16; }
+
+hipError_t launch_pack_dense_int8(const float* w, int OUT, int IN, int8_t* wq, float* wscale, hipStream_t st) {
+    if (OUT <= 0 || IN <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(pack_dense_i8_kernel, dim3((unsigned)OUT), dim3(256), 0, st, w, IN,
+                       (long)dense_i8_row_bytes(IN), wq, wscale);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_rows_int8(const float* x, int N, int IN, float scale, int8_t* q, hipStream_t st) {
+    const long total = (long)N * IN;
+    if (total <= 0 || !(scale > 0.f)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, total, IN,
+                       (long)dense_i8_row_bytes(IN), scale, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_dense_int8(const int8_t* xq, const int8_t* wq, const float* wscale, float xscale,
+                             const float* bias, int N, int IN, int OUT, int act, float* y, int8_t* yq,
+                             float yscale, hipStream_t st) {
+    if (N <= 0 || IN <= 0 || OUT <= 0 || (!y && !yq) || (long)IN * 127 * 127 >= (1L << 31))
+        return hipErrorInvalidValue;
+    DenseI8Args a;
+    a.x = xq;
+    a.w = wq;
+    a.wscale = wscale;
+    a.xscale = xscale;
+    a.bias = bias;
+    a.y = y;
+    a.yq = yq;
+    a.yrcp = yq ? 1.0f / yscale : 0.f;
+    a.N = N;
+    a.in16 = cdiv(IN, 16);
+    a.OUT = OUT;
+    a.OUTq = (int)dense_i8_row_bytes(OUT);
+    a.act = act;
+    const dim3 grid((unsigned)cdiv(OUT, 4)), block(256);
+    for (int n0 = 0; n0 < N; n0 += 32) {
+        a.n0 = n0;
+        const int nb = std::min(32, N - n0);
+        if (nb == 1) hipLaunchKernelGGL(dense_i8<1>, grid, block, 0, st, a);
+        else if (nb == 2) hipLaunchKernelGGL(dense_i8<2>, grid, block, 0, st, a);
+        else if (nb <= 4) hipLaunchKernelGGL(dense_i8<4>, grid, block, 0, st, a);
+        else if (nb <= 8) hipLaunchKernelGGL(dense_i8<8>, grid, block, 0, st, a);
+        else if (nb <= 16) hipLaunchKernelGGL(dense_i8<16>, grid, block, 0, st, a);
+        else hipLaunchKernelGGL(dense_i8<32>, grid, block, 0, st, a);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace neo

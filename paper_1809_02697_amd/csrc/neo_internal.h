@@ -140,8 +140,8 @@ size_t int8_filter_bytes(int K, int C, int R, int S);
 size_t int8_act_bytes(int N, int C, int H, int W, int ph, int pw);
 bool int8_config_valid(const ConvShape& s, const ConvConfig& c);
 ConvConfig choose_int8_config(const ConvShape& s);
-// max |x| over n floats (n a multiple of 4, x 16-byte aligned), written to
-// *out as the float's bit pattern.
+// max |x| over n floats (x 16-byte aligned), written to *out as the float's
+// bit pattern.
 hipError_t launch_absmax(const float* x, long n, unsigned* out, hipStream_t st);
 hipError_t launch_quantize_int8(const float* x, int N, int C, int H, int W, int ph, int pw, float scale,
                                 int8_t* q, hipStream_t st);
@@ -225,6 +225,16 @@ struct I8Member {
     // when y is null, else the whole [N][KB] tensor)
     int q_off, q_tot;
 };
+// Integer dense layer: xq int8 [N][INp] (INp = dense_i8_row_bytes(IN), rows
+// zero-padded), wq int8 [OUT][INp] with per-row scales, exact int32 dot
+// products, the conv's float32 epilogue (bias, act) into y [N][OUT] and/or
+// requantized by 1 / yscale into yq int8 [N][dense_i8_row_bytes(OUT)].
+size_t dense_i8_row_bytes(int IN);
+hipError_t launch_pack_dense_int8(const float* w, int OUT, int IN, int8_t* wq, float* wscale, hipStream_t st);
+hipError_t launch_quantize_rows_int8(const float* x, int N, int IN, float scale, int8_t* q, hipStream_t st);
+hipError_t launch_dense_int8(const int8_t* xq, const int8_t* wq, const float* wscale, float xscale,
+                             const float* bias, int N, int IN, int OUT, int act, float* y, int8_t* yq,
+                             float yscale, hipStream_t st);
 // One integer conv from a member's operands (float32 and/or int8 outputs).
 hipError_t launch_conv_int8_m(const I8Member& m, const ConvConfig& c, hipStream_t st);
 bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);

@@ -113,6 +113,8 @@ struct I8Copy {
     // a concatenation's copy assembled by its parts' producers, each writing
     // its slice (their steps carry q_out = this copy)
     bool assembled = false;
+    // a dense layer's input: int8 rows [N][dense_i8_row_bytes(C)], no halo
+    bool rows = false;
 };
 
 struct Xform {
@@ -588,6 +590,17 @@ int build_steps(neo_plan* P) {
                 std::vector<float> w(d.w, d.w + (long)d.K * a->C);
                 st.w_off = add_params(P, w);
                 if (d.bias) st.b_off = add_params(P, std::vector<float>(d.bias, d.bias + d.K));
+                if (P->flags & NEO_PLAN_INT8) {
+                    // integer dense layer: int8 rows and their scales (packed on the device)
+                    if ((long)a->C * 127 * 127 >= (1L << 31) ||
+                        (long)d.K * (long)dense_i8_row_bytes(a->C) >= (1L << 31))
+                        return fail(NEO_ERR_UNSUPPORTED, where + "int8 dense layer too wide for int32 sums "
+                                                                 "or 2 GiB of weights");
+                    st.i8 = true;
+                    st.ws8_off = add_params(P, std::vector<float>((size_t)d.K, 1.f));
+                    st.w8_off = P->i8_bytes;
+                    P->i8_bytes += ((long)d.K * (long)dense_i8_row_bytes(a->C) + 255) / 256 * 256;
+                }
                 const int v = B.new_val(id, ni.N, ni.C, 1, 1, 0);
                 st.out = v;
                 P->steps.push_back(st);
@@ -1051,46 +1064,65 @@ bool group_pool(const neo_plan* P, const Step& s, const float* x_in, float* y_ou
 // read the copy runs its quantization pass.
 void plan_int8_copies(neo_plan* P) {
     const int ns = (int)P->steps.size();
+    // the value itself, through aliases (a flatten reads its source's storage)
+    auto root = [&](int v) {
+        while (P->vals[v].alias_of >= 0) v = P->vals[v].alias_of;
+        return v;
+    };
     for (int i = 0; i < ns; ++i) {
         Step& t = P->steps[i];
-        if (t.kind != ST_CONV || !t.i8) continue;
+        if (!((t.kind == ST_CONV || t.kind == ST_DENSE) && t.i8)) continue;
+        const bool rows = t.kind == ST_DENSE;
         int c = -1;
         for (int k = 0; k < (int)P->i8_copies.size(); ++k)
-            if (P->i8_copies[k].val == t.in) c = k;
+            if (P->i8_copies[k].val == t.in && P->i8_copies[k].rows == rows) c = k;
         if (c < 0) {
             c = (int)P->i8_copies.size();
-            P->i8_copies.push_back(I8Copy{t.in, t.cs.ph, t.cs.pw, -1});
+            I8Copy q{t.in, rows ? 0 : t.cs.ph, rows ? 0 : t.cs.pw, -1};
+            q.rows = rows;
+            P->i8_copies.push_back(q);
             t.quant_here = true;  // the first reader, unless a writer takes it over
         }
         I8Copy& q = P->i8_copies[c];
-        q.ph = std::max(q.ph, t.cs.ph);
-        q.pw = std::max(q.pw, t.cs.pw);
+        if (!rows) {
+            q.ph = std::max(q.ph, t.cs.ph);
+            q.pw = std::max(q.pw, t.cs.pw);
+        }
         t.qc = c;
     }
     for (I8Copy& q : P->i8_copies) {
         const Val& v = P->vals[q.val];
         q.xq_off = P->i8_bytes;
-        P->i8_bytes += ((long)int8_act_bytes(v.N, v.C, v.H, v.W, q.ph, q.pw) + 255) / 256 * 256;
+        const long bytes = q.rows ? (long)v.N * (long)dense_i8_row_bytes(v.C * v.H * v.W)
+                                  : (long)int8_act_bytes(v.N, v.C, v.H, v.W, q.ph, q.pw);
+        P->i8_bytes += (bytes + 255) / 256 * 256;
     }
     for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
         I8Copy& q = P->i8_copies[c];
         int w = -1;
         for (int i = 0; i < ns; ++i) {
             const Step& t = P->steps[i];
-            if (t.out == q.val && ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL))
-                w = i;
+            // a conv or pool writes a conv input's copy; a dense layer the next dense layer's
+            const bool kind_ok = q.rows ? (t.kind == ST_DENSE && t.i8)
+                                        : ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL ||
+                                           t.kind == ST_AVGPOOL);
+            if (t.out >= 0 && root(t.out) == root(q.val) && kind_ok) w = i;
         }
         if (w < 0) continue;
-        // the writer: does anything read its float32 output?
-        bool f32 = q.val == P->out_val || P->vals[q.val].view;
-        for (const Val& o : P->vals)
-            if (o.alias_of == q.val) f32 = true;
+        // the writer: does anything other than this copy's int8 readers read
+        // its float32 output (itself or an alias of it: a flatten), or is
+        // it the network's output or a concatenation's slice?
+        const int rv = root(q.val);
+        auto same = [&](int v) { return v >= 0 && root(v) == rv; };
+        bool f32 = false;
+        for (int o = 0; o < (int)P->vals.size(); ++o)
+            if (same(o) && (o == P->out_val || P->vals[o].view)) f32 = true;
         for (int i = 0; i < ns; ++i) {
             const Step& t = P->steps[i];
-            if ((t.in == q.val && !(t.kind == ST_CONV && t.i8)) || t.res == q.val || t.out2 == q.val)
-                f32 = true;
+            const bool int8_reader = (t.kind == ST_CONV || t.kind == ST_DENSE) && t.i8 && t.qc == c;
+            if ((same(t.in) && !int8_reader) || same(t.res) || (t.out2 >= 0 && same(t.out2))) f32 = true;
             for (const Step& m : t.members)
-                if (m.in == q.val || m.res == q.val) f32 = true;
+                if (same(m.in) || same(m.res)) f32 = true;
         }
         q.writer = w;
         P->steps[w].q_out = c;
@@ -1155,7 +1187,7 @@ void plan_int8_copies(neo_plan* P) {
 void place_int8_quant_passes(neo_plan* P) {
     std::vector<char> seen(P->i8_copies.size(), 0);
     auto visit = [&](Step& t) {
-        if (t.kind != ST_CONV || !t.i8) return;
+        if (!((t.kind == ST_CONV || t.kind == ST_DENSE) && t.i8)) return;
         const I8Copy& q = P->i8_copies[t.qc];
         const bool first = q.writer < 0 && !q.assembled && !seen[t.qc];
         t.quant_here = first;
@@ -1299,6 +1331,14 @@ std::string describe(const neo_plan* P) {
         if (s.kind == ST_DENSE) {
             o << ",\"dense\":{\"in\":" << s.dense_in << ",\"out\":" << s.dense_out;
             if (s.gap_parts) o << ",\"gap_parts\":" << s.gap_parts;
+            if (s.i8) {
+                char xs[32];
+                std::snprintf(xs, sizeof xs, "%.9g", (double)P->i8_copies[s.qc].xscale);
+                o << ",\"algo\":\"int8\",\"int8\":{\"x_scale\":" << xs << ",\"calibrated\":"
+                  << (P->i8_ready ? "true" : "false") << ",\"input_copy\":" << s.qc
+                  << ",\"quantizes_input\":" << (s.quant_here ? "true" : "false") << ",\"writes_copy\":"
+                  << s.q_out << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false") << "}";
+            }
             o << "}";
         }
         o << "}";
@@ -1616,6 +1656,9 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                     e = launch_pack_filter_int8(P->d_params + st.kcrs_off, st.cs.K, st.cs.C, st.cs.R,
                                                 st.cs.S, P->d_i8 + st.w8_off, P->d_params + st.ws8_off,
                                                 nullptr);
+                if (e == hipSuccess && st.kind == ST_DENSE && st.i8)
+                    e = launch_pack_dense_int8(P->d_params + st.w_off, st.dense_out, st.dense_in,
+                                               P->d_i8 + st.w8_off, P->d_params + st.ws8_off, nullptr);
             };
             for (const Step& st : P->steps) {
                 pack(st);
@@ -1734,6 +1777,9 @@ static hipError_t i8_quant_pass(const neo_plan* P, const Step& s, const float* x
     if (!s.quant_here) return hipSuccess;
     const Val& in = P->vals[s.in];
     const I8Copy& qc = P->i8_copies[s.qc];
+    if (qc.rows)
+        return launch_quantize_rows_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C * in.H * in.W, qc.xscale,
+                                         P->d_i8 + qc.xq_off, st);
     return launch_quantize_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W, qc.ph, qc.pw,
                                 qc.xscale, P->d_i8 + qc.xq_off, st);
 }
@@ -1862,6 +1908,22 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
             }
             case ST_DENSE: {
                 const Val& in = P->vals[s.in];
+                if (s.i8) {
+                    // the input's int8 rows (quantized here by the first
+                    // reader, unless the producing dense layer wrote them),
+                    // the integer dense layer, its float32 output and/or the
+                    // next dense layer's int8 rows
+                    const I8Copy& qc = P->i8_copies[s.qc];
+                    const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
+                    e = i8_quant_pass(P, s, x_nchw, y_out, st);
+                    if (e == hipSuccess)
+                        e = launch_dense_int8(P->d_i8 + qc.xq_off, P->d_i8 + s.w8_off, prm + s.ws8_off, qc.xscale,
+                                              s.b_off >= 0 ? prm + s.b_off : nullptr, in.N, s.dense_in,
+                                              s.dense_out, s.act,
+                                              (!qo || s.f32_needed) ? val_ptr(P, s.out, x_nchw, y_out) : nullptr,
+                                              qo ? P->d_i8 + qo->xq_off : nullptr, qo ? qo->xscale : 1.f, st);
+                    break;
+                }
                 if (s.gap_parts)
                     e = launch_dense_parts(val_ptr(P, s.in, x_nchw, y_out), s.gap_parts, s.gap_stride,
                                            s.gap_scale, s.dense_in, prm + s.w_off, s.dense_out,
@@ -2282,9 +2344,9 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
         *out = m > 0.f ? m / 127.0f : 1.0f;
         return (int)NEO_OK;
     };
-    auto elems = [&](int v) {
+    auto elems = [&](int v) {  // the floats of a value (blocked: with its padding lanes)
         const Val& a = P->vals[v];
-        return (long)a.N * cdiv(a.C, 16) * 16 * a.H * a.W;
+        return a.layout ? (long)a.N * cdiv(a.C, a.layout) * a.layout * a.H * a.W : (long)a.N * a.C * a.H * a.W;
     };
     // an assembled copy's parts (the steps writing its slices; group members
     // with their group's configuration), and whether its scale is set
@@ -2329,7 +2391,7 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
             assembled[s.qc] = 1;
         }
         // a copy quantized by its own pass: the scale of the value it reads
-        if (s.kind == ST_CONV && s.i8 && s.quant_here &&
+        if ((s.kind == ST_CONV || s.kind == ST_DENSE) && s.i8 && s.quant_here &&
             (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in),
                            &P->i8_copies[s.qc].xscale)) != NEO_OK)
             return rc;

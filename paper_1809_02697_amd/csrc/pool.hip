@@ -34,8 +34,12 @@ __global__ __launch_bounds__(256) void pool_blk_q(const float* __restrict__ x, f
 // pixel_slot + quad; each lane sums the pixels p = slot, slot + 16, ... of its
 // quad's channels, then the 16 slots are summed with cross-lane shuffles in a
 // fixed tree order -- the same order for every block, so the result does not
-// depend on the layout.  Channel c = 16 j + 4 q sits in block c / x at lane
-// c % x (lx = log2 x); quads past the last block (x < 16) are idle.
+// depend on the layout.  The sums are in double and the mean is rounded once
+// to float32: n float32 values whose exponents span e bits sum exactly in a
+// double while n * 2^(e + 24) <= 2^53 (for a 7x7 or 8x8 map: nonzero values
+// within a factor 2^23 of each other), and then the result is the exact mean
+// rounded, whatever the order.  Channel c = 16 j + 4 q sits in block c / x at
+// lane c % x (lx = log2 x); quads past the last block (x < 16) are idle.
 __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, float* __restrict__ y,
                                                int N, int G16, int XB, int lx, int HW) {
     const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -48,7 +52,7 @@ __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, floa
     const bool ok = c < (XB << lx);
     const int blk = n * XB + (c >> lx), sub = c & (X - 1);
     const float* xb = x + (long)blk * HW * X + sub;
-    v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
     if (ok) {
         int p = slot;
         for (; p + 48 < HW; p += 64) {  // four pixels of the slot in flight
@@ -56,9 +60,15 @@ __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, floa
 #pragma unroll
             for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const v4f*>(xb + (p + 16 * u) * X);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) acc += v[u];
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += (double)v[u][i];
         }
-        for (; p < HW; p += 16) acc += *reinterpret_cast<const v4f*>(xb + p * X);
+        for (; p < HW; p += 16) {
+            const v4f v = *reinterpret_cast<const v4f*>(xb + p * X);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] += (double)v[i];
+        }
     }
 #pragma unroll
     for (int off = 4; off < 64; off <<= 1) {
@@ -66,10 +76,11 @@ __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, floa
         for (int i = 0; i < 4; ++i) acc[i] += __shfl_xor(acc[i], off, 64);
     }
     if (slot == 0 && ok) {
-        const float d = (float)HW;
+        const double d = (double)HW;
+        v4f o;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = acc[i] / d;
-        *reinterpret_cast<v4f*>(y + blk * X + sub) = acc;
+        for (int i = 0; i < 4; ++i) o[i] = (float)(acc[i] / d);
+        *reinterpret_cast<v4f*>(y + blk * X + sub) = o;
     }
 }
 
