@@ -457,9 +457,14 @@ enum neo_plan_flags {
      * is assembled by its parts' producers, each writing its slice of the
      * copy with the concatenation's scale.  Otherwise (the network input, a
      * concatenation of concatenations) the first reader runs the
-     * quantization pass.  Pools, concatenation, flatten and
-     * dense compute in float32.  The input scales come
-     * from neo_plan_calibrate_int8, which must run before the plan does.
+     * quantization pass.  Dense layers run in int8 too: weights quantized
+     * per output row, the flattened input one int8 row per image (written by
+     * the producing dense layer, requantized, or quantized by a pass),
+     * exact int32 dot products, the same float32 epilogue.  Pools,
+     * concatenation and flatten compute in float32 (the average pools and
+     * the global average pool sum in double and round the mean once).  The
+     * input scales come from neo_plan_calibrate_int8, which must run before
+     * the plan does.
      * Convs run in NCHW16c: block 16, and no NAIVE, GLOBAL_SEARCH, WINOGRAD
      * or fusion flag other than NEO_PLAN_GROUP, which puts independent int8
      * convs (and a pooling step) in one launch, as for float32 (one int8
@@ -521,17 +526,16 @@ int neo_run_step(neo_plan* plan, int step, const float* x_nchw, float* y_out, ne
 /*
  * Calibrate a NEO_PLAN_INT8 plan on the input x_nchw (device, NCHW; the
  * output goes to y_out as for neo_run_graph): run the plan step by step on
- * `stream` and, just before each conv, set that conv's input scale to
+ * `stream` and, just before each conv or dense layer, set its input scale to
  * max|x| / 127 in float32 over its float32 input as this run produced it
  * (1 for an all-zero input; a copy's writer, conv or pool, runs once with
  * its float32 output only for that, then as the plan does; the parts of an
  * assembled concatenation run in float32 only, and again with their slices
  * once the first reader has set the concatenation's scale; the members of a
  * group launch run one by one, which computes the same values).
- * Synchronizes the stream once per conv (the maximum is read back); drops
- * a captured graph, which the next
- * neo_run_graph captures again with the new scales.  neo_plan_describe then
- * lists each conv's "x_scale".  Errors: NEO_ERR_STATE for a plan without
+ * Synchronizes the stream once per int8 layer (the maximum is read back);
+ * drops a captured graph, which the next neo_run_graph captures again with
+ * the new scales.  neo_plan_describe then lists each int8 layer's "x_scale".  Errors: NEO_ERR_STATE for a plan without
  * NEO_PLAN_INT8 or host-only, NEO_ERR_INVALID_ARG / _ALIGN for the buffers,
  * NEO_ERR_INVALID_ARG for a non-finite activation.
  */
