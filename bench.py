@@ -589,7 +589,8 @@ def model_latencies(neo, torch, wl, steps):
             d = p.describe()
             q = [c["int8"] for st in d["steps"]
                  for c in ([st["conv"]] if st["kind"] == "conv" else
-                           [m["conv"] for m in st.get("members", [])] if st["kind"] == "conv_group" else [])]
+                           [m["conv"] for m in st.get("members", [])] if st["kind"] == "conv_group" else
+                           [st["dense"]] if st["kind"] == "dense" and "int8" in st["dense"] else [])]
             passes = sum(c["quantizes_input"] for c in q)
             int8_runs[label] = dict(ms=round(ms, 4), launches=len(d["steps"]) + passes,
                                     quantization_passes=passes, plan_s=round(t_plan, 1),
