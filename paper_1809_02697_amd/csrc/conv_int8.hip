@@ -458,10 +458,13 @@ __global__ __launch_bounds__(256) void pack_filter_i8_kernel(const float* w, int
 // Integer dense layer (the fully connected layers of integer inference):
 // acc[n][k] = sum_i xq[n][i] * wq[k][i], exact in int32 (|acc| <= 127^2 * IN),
 // then the conv's float32 epilogue.  Rows of xq and wq are padded with zeros
-// to INp = 16 * in16 bytes.  One wave per output row k: its lanes take the
-// row's 16-byte chunks in turn (one load, four 4-byte dot products per chunk
-// and image), keep one sum per image, and add them across the wave; lane n
-// then finishes image n0 + n.  Images n0 .. n0 + NB - 1 per launch.
+// to INp = 16 * in16 bytes.  One wave per R output rows k0 .. k0 + R - 1:
+// its lanes take the rows' 16-byte chunks in turn (one load per row and
+// image, four 4-byte dot products per row and image), keep one sum per row
+// and image, and add them across the wave; lane n then finishes image
+// n0 + n of each row.  Images n0 .. n0 + NB - 1 per launch.  (R > 1 would
+// reuse each input chunk for R rows; measured slower at 32 images than the
+// 1x1 integer conv a plan runs there, so the launcher uses R = 1.)
 struct DenseI8Args {
     const int8_t* x;      // [N][INp]
     const int8_t* w;      // [OUT][INp]
@@ -474,55 +477,71 @@ struct DenseI8Args {
     int N, in16, OUT, OUTq, act, n0;
 };
 
-template <int NB>
+template <int NB, int R>
 __global__ __launch_bounds__(256) void dense_i8(DenseI8Args a) {
     const int lane = threadIdx.x & 63;
-    const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (k >= a.OUT) return;
+    const int k0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
+    if (k0 >= a.OUT) return;
     const long inp = 16L * a.in16;
-    int acc[NB];
+    int acc[R][NB];
 #pragma unroll
-    for (int n = 0; n < NB; ++n) acc[n] = 0;
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int n = 0; n < NB; ++n) acc[r][n] = 0;
     const int nb = min(NB, a.N - a.n0);
-    const v4i* wr = reinterpret_cast<const v4i*>(a.w + k * inp);
+    // rows past OUT (the last wave of a ragged OUT) read row k0 again and are never stored
+    const v4i* wr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) wr[r] = reinterpret_cast<const v4i*>(a.w + (k0 + r < a.OUT ? k0 + r : k0) * inp);
     for (int c = lane; c < a.in16; c += 64) {
-        const v4i wv = wr[c];
+        v4i wv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) wv[r] = wr[r][c];
 #pragma unroll
         for (int n = 0; n < NB; ++n) {
             if (n < nb) {
                 const v4i xv = reinterpret_cast<const v4i*>(a.x + (a.n0 + n) * inp)[c];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[n] = __builtin_amdgcn_sdot4(wv[j], xv[j], acc[n], false);
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[r][n] = __builtin_amdgcn_sdot4(wv[r][j], xv[j], acc[r][n], false);
             }
         }
     }
 #pragma unroll
-    for (int n = 0; n < NB; ++n)
+    for (int r = 0; r < R; ++r)
 #pragma unroll
-        for (int d = 32; d > 0; d >>= 1) acc[n] += __shfl_xor(acc[n], d, 64);
-    // lane n keeps image n's sum (a select chain, not a dynamic register index)
-    int mine = acc[0];
+        for (int n = 0; n < NB; ++n)
 #pragma unroll
-    for (int n = 1; n < NB; ++n) mine = lane == n ? acc[n] : mine;
+            for (int d = 32; d > 0; d >>= 1) acc[r][n] += __shfl_xor(acc[r][n], d, 64);
     if (lane >= nb) return;
     const int img = a.n0 + lane;
-    float o;
-    {
-#pragma clang fp contract(off)
-        const float m = a.xscale * a.wscale[k];
-        o = (float)mine * m;
-        if (a.bias) o = o + a.bias[k];
-    }
-    if (a.act == NEO_ACT_RELU) o = o > 0.f ? o : 0.f;
-    if (a.y) a.y[(long)img * a.OUT + k] = o;
-    if (a.yq) {
-        float q;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int k = k0 + r;
+        if (k >= a.OUT) break;
+        // lane n keeps image n's sum (a select chain, not a dynamic register index)
+        int mine = acc[r][0];
+#pragma unroll
+        for (int n = 1; n < NB; ++n) mine = lane == n ? acc[r][n] : mine;
+        float o;
         {
 #pragma clang fp contract(off)
-            q = rintf(o * a.yrcp);
+            const float m = a.xscale * a.wscale[k];
+            o = (float)mine * m;
+            if (a.bias) o = o + a.bias[k];
         }
-        q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
-        a.yq[(long)img * a.OUTq + k] = (int8_t)(int)q;
+        if (a.act == NEO_ACT_RELU) o = o > 0.f ? o : 0.f;
+        if (a.y) a.y[(long)img * a.OUT + k] = o;
+        if (a.yq) {
+            float q;
+            {
+#pragma clang fp contract(off)
+                q = rintf(o * a.yrcp);
+            }
+            q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
+            a.yq[(long)img * a.OUTq + k] = (int8_t)(int)q;
+        }
     }
 }
 
@@ -883,16 +902,18 @@ hipError_t launch_dense_int8(const int8_t* xq, const int8_t* wq, const float* ws
     a.OUT = OUT;
     a.OUTq = (int)dense_i8_row_bytes(OUT);
     a.act = act;
-    const dim3 grid((unsigned)cdiv(OUT, 4)), block(256);
+    // one row per wave: the weight stream bounds the layer for a few images
+    // (a plan runs a dense layer over many images as a 1x1 integer conv)
+    const dim3 g1((unsigned)cdiv(OUT, 4)), block(256);
     for (int n0 = 0; n0 < N; n0 += 32) {
         a.n0 = n0;
         const int nb = std::min(32, N - n0);
-        if (nb == 1) hipLaunchKernelGGL(dense_i8<1>, grid, block, 0, st, a);
-        else if (nb == 2) hipLaunchKernelGGL(dense_i8<2>, grid, block, 0, st, a);
-        else if (nb <= 4) hipLaunchKernelGGL(dense_i8<4>, grid, block, 0, st, a);
-        else if (nb <= 8) hipLaunchKernelGGL(dense_i8<8>, grid, block, 0, st, a);
-        else if (nb <= 16) hipLaunchKernelGGL(dense_i8<16>, grid, block, 0, st, a);
-        else hipLaunchKernelGGL(dense_i8<32>, grid, block, 0, st, a);
+        if (nb == 1) hipLaunchKernelGGL((dense_i8<1, 1>), g1, block, 0, st, a);
+        else if (nb == 2) hipLaunchKernelGGL((dense_i8<2, 1>), g1, block, 0, st, a);
+        else if (nb <= 4) hipLaunchKernelGGL((dense_i8<4, 1>), g1, block, 0, st, a);
+        else if (nb <= 8) hipLaunchKernelGGL((dense_i8<8, 1>), g1, block, 0, st, a);
+        else if (nb <= 16) hipLaunchKernelGGL((dense_i8<16, 1>), g1, block, 0, st, a);
+        else hipLaunchKernelGGL((dense_i8<32, 1>), g1, block, 0, st, a);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -99,6 +99,9 @@ struct Step {
     // the slice of copy q_out this step writes, in blocks ([q_off8, q_off8 +
     // its blocks) of q_tot8), when it is one part of a concatenation's copy
     int q_off8 = -1, q_tot8 = -1;
+    // ST_DENSE with NEO_PLAN_INT8 over many images: run as the 1x1 integer
+    // conv cs (its filter packed in the conv's order, configuration c8)
+    bool d_conv = false;
 };
 
 // NEO_PLAN_INT8: the int8 copy of a value, its halo the largest padding of
@@ -597,9 +600,20 @@ int build_steps(neo_plan* P) {
                         return fail(NEO_ERR_UNSUPPORTED, where + "int8 dense layer too wide for int32 sums "
                                                                  "or 2 GiB of weights");
                     st.i8 = true;
-                    st.ws8_off = add_params(P, std::vector<float>((size_t)d.K, 1.f));
+                    // from 8 images on, a 1x1 conv over a 1x1 map: the conv
+                    // kernel's int8 input [N][ceil(IN/16)][1][1][16] is these
+                    // rows, and its float32 output [N][OUT/16][1][1][16] the
+                    // plain [N][OUT] when OUT is a multiple of 16
+                    st.d_conv = ni.N >= 8 && d.K % 16 == 0 && (long)a->C <= 133000;
+                    st.ws8_off = add_params(P, std::vector<float>((size_t)cdiv(d.K, 16) * 16, 1.f));
                     st.w8_off = P->i8_bytes;
-                    P->i8_bytes += ((long)d.K * (long)dense_i8_row_bytes(a->C) + 255) / 256 * 256;
+                    const long wbytes = st.d_conv ? (long)int8_filter_bytes(d.K, a->C, 1, 1)
+                                                  : (long)d.K * (long)dense_i8_row_bytes(a->C);
+                    P->i8_bytes += (wbytes + 255) / 256 * 256;
+                    if (st.d_conv) {
+                        st.cs = ConvShape{ni.N, a->C, 1, 1, d.K, 1, 1, 1, 1, 0, 0, 1, 1, 0, d.K / 16, d.act};
+                        st.c8 = choose_int8_config(st.cs);
+                    }
                 }
                 const int v = B.new_val(id, ni.N, ni.C, 1, 1, 0);
                 st.out = v;
@@ -1334,7 +1348,10 @@ std::string describe(const neo_plan* P) {
             if (s.i8) {
                 char xs[32];
                 std::snprintf(xs, sizeof xs, "%.9g", (double)P->i8_copies[s.qc].xscale);
-                o << ",\"algo\":\"int8\",\"int8\":{\"x_scale\":" << xs << ",\"calibrated\":"
+                o << ",\"algo\":\"int8\",\"int8\":{\"conv_mode\":" << (s.d_conv ? "true" : "false");
+                if (s.d_conv)
+                    o << ",\"tile\":[" << s.c8.fk << "," << s.c8.fp << "],\"waves\":" << s.c8.waves;
+                o << ",\"x_scale\":" << xs << ",\"calibrated\":"
                   << (P->i8_ready ? "true" : "false") << ",\"input_copy\":" << s.qc
                   << ",\"quantizes_input\":" << (s.quant_here ? "true" : "false") << ",\"writes_copy\":"
                   << s.q_out << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false") << "}";
@@ -1589,7 +1606,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
             plan_int8_copies(P);
             if (!(flags & NEO_PLAN_HOST_ONLY))
                 for (Step& st : P->steps)
-                    if (st.kind == ST_CONV && st.i8) {
+                    if ((st.kind == ST_CONV || (st.kind == ST_DENSE && st.d_conv)) && st.i8) {
                         const int mode = st.q_out < 0 ? 0 : st.f32_needed ? 3 : 2;
                         st.tuned = tuned_int8_config(st.cs, mode, &st.c8);
                     }
@@ -1657,8 +1674,11 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
                                                 st.cs.S, P->d_i8 + st.w8_off, P->d_params + st.ws8_off,
                                                 nullptr);
                 if (e == hipSuccess && st.kind == ST_DENSE && st.i8)
-                    e = launch_pack_dense_int8(P->d_params + st.w_off, st.dense_out, st.dense_in,
-                                               P->d_i8 + st.w8_off, P->d_params + st.ws8_off, nullptr);
+                    e = st.d_conv  // [OUT][IN] float32 is KCRS with R = S = 1
+                            ? launch_pack_filter_int8(P->d_params + st.w_off, st.dense_out, st.dense_in, 1, 1,
+                                                      P->d_i8 + st.w8_off, P->d_params + st.ws8_off, nullptr)
+                            : launch_pack_dense_int8(P->d_params + st.w_off, st.dense_out, st.dense_in,
+                                                     P->d_i8 + st.w8_off, P->d_params + st.ws8_off, nullptr);
             };
             for (const Step& st : P->steps) {
                 pack(st);
@@ -1916,7 +1936,9 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     const I8Copy& qc = P->i8_copies[s.qc];
                     const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
                     e = i8_quant_pass(P, s, x_nchw, y_out, st);
-                    if (e == hipSuccess)
+                    if (e == hipSuccess && s.d_conv)
+                        e = launch_conv_int8_m(i8_member(P, s, x_nchw, y_out), s.c8, st);
+                    else if (e == hipSuccess)
                         e = launch_dense_int8(P->d_i8 + qc.xq_off, P->d_i8 + s.w8_off, prm + s.ws8_off, qc.xscale,
                                               s.b_off >= 0 ? prm + s.b_off : nullptr, in.N, s.dense_in,
                                               s.dense_out, s.act,
@@ -2211,8 +2233,9 @@ static int tune_plan(neo_plan* P) {
             }
             continue;
         }
-        if (s.kind == ST_CONV && s.i8) {
-            // an integer conv: its configurations timed with its own output mode
+        if ((s.kind == ST_CONV || (s.kind == ST_DENSE && s.d_conv)) && s.i8) {
+            // an integer conv (or a dense layer run as one): its configurations
+            // timed with its own output mode
             rc = tune_int8(i8_member(P, s, xin, yout), P->cap_stream, &s.c8, nullptr);
             s.tuned = rc == NEO_OK;
             next.push_back(s);
