@@ -26,9 +26,10 @@ input has the scale max |x| / 127 of the float32 tensor it reads
 input that is the output of a conv: that conv writes it requantized (by the
 reciprocal, as above), one int8 tensor shared by every conv that reads it,
 whatever their paddings (the padding is storage, not arithmetic); and a
-concatenation whose parts are conv or pool outputs that nothing else reads:
-each part's producer writes its slice with the concatenation's scale (a
-conv part requantized, a pool part by division).  The filter is the
+concatenation whose parts are conv or pool outputs that nothing else reads
+(through nested concatenations): each part's producer writes its slice with
+the concatenation's scale (a conv part requantized, a pool part by
+division).  The filter is the
 batch-norm-folded one (``fold_bn``) quantized per output channel, and the
 conv's output is the float32 epilogue above.  Dense layers take the same
 path: weights quantized per output row, the flattened input with one scale
@@ -213,15 +214,35 @@ def run_graph_int8(graph, x=None):
         if n.residual >= 0:
             uses[n.residual].append(i)
 
+    def parts(j):
+        """A concatenation's parts in channel order as (channels, requantized),
+        through nested concatenations, when every part is a conv or pool
+        output read by nothing but its concatenation; else None."""
+        out = []
+        for p in graph.nodes[j].inputs:
+            op = graph.nodes[p].op
+            if uses[p] != [j]:
+                return None
+            if op in ("conv", "maxpool", "avgpool"):
+                out.append((vals[p].shape[1], op == "conv"))
+            elif op == "concat":
+                sub = parts(p)
+                if sub is None:
+                    return None
+                out += sub
+            else:
+                return None
+        return out
+
     def rule(j):
         """How a conv's input value j becomes int8 (conv_node_int8's chained)."""
         src = graph.nodes[j]
         if src.op == "conv":
             return True
         if src.op == "concat":
-            if all(graph.nodes[p].op in ("conv", "maxpool", "avgpool") and uses[p] == [j]
-                   for p in src.inputs):
-                return [(vals[p].shape[1], graph.nodes[p].op == "conv") for p in src.inputs]
+            p = parts(j)
+            if p is not None:
+                return p
         return False
 
     for i, n in enumerate(graph.nodes):

@@ -324,3 +324,35 @@ def test_concatenation_is_assembled_by_its_parts_producers():
     np.testing.assert_array_equal(scales, np.float32([1.0, 1.0, 7.0]))
     want = np.stack([np.full((4, 5), 6223.0), np.full((4, 5), 5334.0)])[None].astype(np.float32)
     np.testing.assert_array_equal(y, want)
+
+
+def test_nested_concatenation_is_assembled_by_its_parts_producers():
+    """The same assembly through a concatenation nested in another: the
+    outer concatenation [conv part, [pool part]] reads like the flat one
+    (6223 and 5334 by hand, scales 1, 1, 7)."""
+    from paper_1809_02697_amd.workloads import Graph, Node
+    rng = np.random.default_rng(5)
+    x = np.zeros((1, 3, 4, 5), np.float32)
+    x[0, 0] = rng.integers(-7, 8, (4, 5))
+    x[0, 0, 3, 4] = 7.0
+    x[0, 2, 0, 2] = 127.0
+    wa = np.zeros((2, 3, 1, 1), np.float32)
+    wa[0, 0] = 127.0
+    wa[1, 1] = 127.0
+    wb = np.zeros((2, 3, 1, 1), np.float32)
+    wb[0, 1] = 127.0
+    wb[1, 2] = 127.0
+    nodes = [
+        Node("input"),
+        Node("conv", (0,), K=2, R=1, S=1, w=wa, bias=np.float32([0.0, 45.5])),
+        Node("conv", (0,), K=1, R=1, S=1, w=np.zeros((1, 3, 1, 1), np.float32), bias=np.float32([45.5])),
+        Node("maxpool", (2,), R=1, S=1, stride=(1, 1)),
+        Node("concat", (3,)),
+        Node("concat", (1, 4)),
+        Node("conv", (5,), K=2, R=1, S=1, w=wb),
+        Node("output", (6,)),
+    ]
+    y, scales = oq.run_graph_int8(Graph("nested concatenation", nodes, x.shape, x))
+    np.testing.assert_array_equal(scales, np.float32([1.0, 1.0, 7.0]))
+    want = np.stack([np.full((4, 5), 6223.0), np.full((4, 5), 5334.0)])[None].astype(np.float32)
+    np.testing.assert_array_equal(y, want)
