@@ -1154,26 +1154,32 @@ void plan_int8_copies(neo_plan* P) {
             cv.view)
             continue;
         std::vector<std::pair<int, int>> parts;  // (producer step, block offset in the concatenation)
-        bool ok = true;
-        for (int j : P->nodes[cv.node].inputs) {
-            int u = -1;
-            for (int k = 0; k < (int)P->vals.size(); ++k)
-                if (P->vals[k].node == j && P->vals[k].view && P->vals[k].layout == cv.layout &&
-                    P->vals[k].alias_of < 0)
-                    u = k;
-            int w = -1;
-            for (int i = 0; ok && u >= 0 && i < ns; ++i) {
-                const Step& t = P->steps[i];
-                if (t.out == u && ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL))
-                    w = i;
+        // the parts of concatenation node `node`, through nested
+        // concatenations (views whose offsets are in the root buffer)
+        std::function<bool(int)> collect = [&](int node) {
+            for (int j : P->nodes[node].inputs) {
+                int u = -1;
+                for (int k = 0; k < (int)P->vals.size(); ++k)
+                    if (P->vals[k].node == j && P->vals[k].view && P->vals[k].layout == cv.layout &&
+                        P->vals[k].alias_of < 0)
+                        u = k;
+                if (u < 0) return false;
+                if (P->nodes[j].nd.op == NEO_OP_CONCAT) {
+                    if (!collect(j)) return false;
+                    continue;
+                }
+                int w = -1;
+                for (int i = 0; i < ns; ++i) {
+                    const Step& t = P->steps[i];
+                    if (t.out == u && ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL))
+                        w = i;
+                }
+                if (w < 0 || P->steps[w].q_out >= 0) return false;
+                parts.emplace_back(w, P->vals[u].c_off - cv.c_off);
             }
-            if (u < 0 || w < 0 || P->steps[w].q_out >= 0) {
-                ok = false;
-                break;
-            }
-            parts.emplace_back(w, P->vals[u].c_off - cv.c_off);
-        }
-        if (!ok || parts.empty()) continue;
+            return true;
+        };
+        if (!collect(cv.node) || parts.empty()) continue;
         bool f32 = q.val == P->out_val || cv.view;
         for (const Val& o : P->vals)
             if (o.alias_of == q.val) f32 = true;

@@ -112,11 +112,11 @@ def test_host_grouped_int8_plan(name):
     print(f"\n[int8 group] {name}: {n_launch0} -> {n_launch} launches, {len(groups)} groups")
     assert n_launch < n_launch0
     if name == "inception_v3":
-        # passes: the input and the one concatenation with concatenations
-        # among its parts; the 4 values read by a 1x3 and a 3x1 conv have one
-        # copy, halo (1, 1), written by their producer; the pools write their
-        # own outputs' copies; 9 concatenations are assembled by their parts
-        assert len(groups) == 27 and sum("pool" in s for s in groups) == 11 and len(passes) == 2
+        # one pass, the input's; the 4 values read by a 1x3 and a 3x1 conv
+        # have one copy, halo (1, 1), written by their producer; the pools
+        # write their own outputs' copies; the 10 concatenations convs read
+        # are assembled by their parts (one through two nested ones)
+        assert len(groups) == 27 and sum("pool" in s for s in groups) == 11 and len(passes) == 1
         slices = {}
         for s in d["steps"]:
             for w in ([s["conv"]["int8"]] if s["kind"] == "conv" else
@@ -125,7 +125,7 @@ def test_host_grouped_int8_plan(name):
                       ([s["int8"]] if s["kind"] in ("maxpool", "avgpool") and "int8" in s else [])):
                 if "writes_slice" in w:
                     slices.setdefault(w["writes_copy"], []).append(w["writes_slice"])
-        assert len(slices) == 9
+        assert len(slices) == 10
         for parts in slices.values():      # the parts tile the copy's blocks in order
             parts.sort()
             assert parts[0][0] == 0 and len({t for _, t in parts}) == 1
