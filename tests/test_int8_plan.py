@@ -172,8 +172,8 @@ def run_int8_plan(gpu, g, flags=0):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("name,N", [("vgg_tiny", 2), ("vgg_tiny", 20), ("resnet50", 1), ("resnet50", 2),
-                                    ("vgg16", 1), ("inception_v3", 1)])
+@pytest.mark.parametrize("name,N", [("tiny", 2), ("vgg_tiny", 2), ("vgg_tiny", 20), ("resnet50", 1),
+                                    ("resnet50", 2), ("vgg16", 1), ("inception_v3", 1)])
 def test_int8_network_against_the_oracle(gpu, name, N):
     """All conv and dense input scales and the logits bit-exact against the
     oracle's integer network; the calibration run and a later run
@@ -181,7 +181,8 @@ def test_int8_network_against_the_oracle(gpu, name, N):
     the dense kernel's four-rows-per-wave path, in a launch of 16 images
     and one of 4, with a ragged last row group of 10 outputs.)"""
     from gpu_util import dev, host
-    g = wl.vgg_like_tiny(N=N) if name == "vgg_tiny" else wl.MODELS[name](N)
+    g = (wl.vgg_like_tiny(N=N) if name == "vgg_tiny" else wl.tiny_graph() if name == "tiny" else
+         wl.MODELS[name](N))
     print(f"\n[int8 plan] {name} N={N}", flush=True)
     y_cal, y, scales, p = run_int8_plan(gpu, g)
     p.destroy()
