@@ -558,6 +558,25 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(const float* x, long
     q[n * inp + i] = (int8_t)(int)r;
 }
 
+// The exit of the blocked layout for an integer dense layer: NCHW16c float32
+// -> the flattened NCHW order, as float32 (y, may be null) and/or int8 rows
+// (yq [N][inp]) quantized by division.  One thread per output element.
+__global__ __launch_bounds__(256) void blk_to_rows_q(const float* x, int C, int H, int W, long total, long per,
+                                                     long inp, float* y, int8_t* yq, float scale) {
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= total) return;
+    const long n = t / per;
+    const int i = (int)(t - n * per);  // (c * H + h) * W + w
+    const int c = i / (H * W), hw = i - c * (H * W);
+    const float v = x[((n * ((C + 15) / 16) + c / 16) * (long)(H * W) + hw) * 16 + (c & 15)];
+    if (y) y[t] = v;
+    if (yq) {
+        float r = rintf(v / scale);
+        r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
+        yq[n * inp + i] = (int8_t)(int)r;
+    }
+}
+
 // A dense layer's weights [OUT][IN] float32 -> per-row scales max|w[k]| / 127
 // (1 for a zero row) and int8 rows [OUT][INp] (padding 0), one workgroup per row.
 __global__ __launch_bounds__(256) void pack_dense_i8_kernel(const float* w, int IN, long inp, int8_t* wq,
@@ -867,6 +886,15 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
 }
 
 size_t dense_i8_row_bytes(int IN) { return (size_t)cdiv(IN, 16) * 16; }
+
+hipError_t launch_blk_to_rows_int8(const float* x, int N, int C, int H, int W, float* y, int8_t* yq,
+                                   float scale, hipStream_t st) {
+    const long per = (long)C * H * W, total = (long)N * per;
+    if (total <= 0 || !x || (!y && !yq) || (yq && !(scale > 0.f))) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(blk_to_rows_q, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, C, H, W, total,
+                       per, (long)dense_i8_row_bytes((int)per), y, yq, scale);
+    return hipGetLastError();
+}
 
 hipError_t launch_pack_dense_int8(const float* w, int OUT, int IN, int8_t* wq, float* wscale, hipStream_t st) {
     if (OUT <= 0 || IN <= 0) return hipErrorInvalidValue;

@@ -374,6 +374,15 @@ hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStrea
 hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y, const PoolQ& q,
                          hipStream_t st);
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st);
+// The global average pool on NCHW16c (C a multiple of 16) writing the means
+// y (may be null) and/or their int8 rows yq [N][C], quantized by division.
+hipError_t launch_gap_q(const float* x, int N, int C, int H, int W, float* y, int8_t* yq, float scale,
+                        hipStream_t st);
+// NCHW16c float32 [N][ceil(C/16)][H][W][16] -> the flattened NCHW rows
+// (index (c * H + h) * W + w of image n): float32 y [N][C*H*W] (may be
+// null) and/or int8 yq [N][dense_i8_row_bytes(C*H*W)], quantized by division.
+hipError_t launch_blk_to_rows_int8(const float* x, int N, int C, int H, int W, float* y, int8_t* yq,
+                                   float scale, hipStream_t st);
 
 // ---- global layout search (search.cpp) -----------------------------------------------------
 struct SearchNode {

@@ -1117,9 +1117,16 @@ void plan_int8_copies(neo_plan* P) {
         for (int i = 0; i < ns; ++i) {
             const Step& t = P->steps[i];
             // a conv or pool writes a conv input's copy; a dense layer the next dense layer's
-            const bool kind_ok = q.rows ? (t.kind == ST_DENSE && t.i8)
-                                        : ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL ||
-                                           t.kind == ST_AVGPOOL);
+            // a dense layer's rows: the dense layer before it, the global pool
+            // (NCHW16c, whole blocks: its means are the rows) or the exit of
+            // the blocked layout (NCHW16c -> NCHW, not into a slice)
+            const Val* to = t.out >= 0 ? &P->vals[t.out] : nullptr;
+            const bool kind_ok =
+                q.rows ? ((t.kind == ST_DENSE && t.i8) ||
+                          (t.kind == ST_GAP && to->layout == 16 && to->C % 16 == 0) ||
+                          (t.kind == ST_TRANSFORM && t.src_block == 16 && t.dst_block == 0 && !to->view &&
+                           to->alias_of < 0 && !P->vals[t.in].view))
+                       : ((t.kind == ST_CONV && t.i8) || t.kind == ST_MAXPOOL || t.kind == ST_AVGPOOL);
             if (t.out >= 0 && root(t.out) == root(q.val) && kind_ok) w = i;
         }
         if (w < 0) continue;
@@ -1341,7 +1348,8 @@ std::string describe(const neo_plan* P) {
               << "],\"pad\":[" << ps.ph << "," << ps.pw << "],\"OH\":" << ps.OH << ",\"OW\":" << ps.OW
               << "}";
         }
-        if ((s.kind == ST_MAXPOOL || s.kind == ST_AVGPOOL) && s.q_out >= 0) {
+        if ((s.kind == ST_MAXPOOL || s.kind == ST_AVGPOOL || s.kind == ST_GAP || s.kind == ST_TRANSFORM) &&
+            s.q_out >= 0) {
             o << ",\"int8\":{\"writes_copy\":" << s.q_out << ",\"writes_f32\":"
               << (s.f32_needed ? "true" : "false");
             if (s.q_off8 >= 0) o << ",\"writes_slice\":[" << s.q_off8 << "," << s.q_tot8 << "]";
@@ -1820,6 +1828,13 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 const Val& in = P->vals[s.in];
                 const Val& out = P->vals[s.out];
                 float* dst = val_ptr(P, s.out, x_nchw, y_out);
+                if (s.q_out >= 0 && !P->i8_f32_out) {
+                    // NEO_PLAN_INT8: NCHW16c -> NCHW also as the dense layer's int8 rows
+                    const I8Copy& qo = P->i8_copies[s.q_out];
+                    e = launch_blk_to_rows_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                                                s.f32_needed ? dst : nullptr, P->d_i8 + qo.xq_off, qo.xscale, st);
+                    break;
+                }
                 e = launch_layout_transform(val_ptr(P, s.in, x_nchw, y_out), in.layout, dst,
                                             out.layout, in.N, in.C, in.H, in.W, out.c_off,
                                             out.c_tot, st);
@@ -1928,6 +1943,14 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                 break;
             case ST_GAP: {
                 const Val& in = P->vals[s.in];
+                if (s.q_out >= 0 && !P->i8_f32_out) {
+                    // NEO_PLAN_INT8: the means also as the dense layer's int8 rows
+                    const I8Copy& qo = P->i8_copies[s.q_out];
+                    e = launch_gap_q(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C, in.H, in.W,
+                                     s.f32_needed ? val_ptr(P, s.out, x_nchw, y_out) : nullptr,
+                                     P->d_i8 + qo.xq_off, qo.xscale, st);
+                    break;
+                }
                 e = launch_gap(val_ptr(P, s.in, x_nchw, y_out), in.layout, in.N, in.C, in.H, in.W,
                                val_ptr(P, s.out, x_nchw, y_out), st);
                 break;

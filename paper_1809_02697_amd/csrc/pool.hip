@@ -40,8 +40,13 @@ __global__ __launch_bounds__(256) void pool_blk_q(const float* __restrict__ x, f
 // within a factor 2^23 of each other), and then the result is the exact mean
 // rounded, whatever the order.  Channel c = 16 j + 4 q sits in block c / x at
 // lane c % x (lx = log2 x); quads past the last block (x < 16) are idle.
+// Q: the means also (or only: y null) written as int8 rows yq [N][inp]
+// (block 16: channel c of image n at n * inp + c), clamp(round_half_even(
+// mean / scale), -127, 127) with the division in float32.
+template <bool Q>
 __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, float* __restrict__ y,
-                                               int N, int G16, int XB, int lx, int HW) {
+                                               int N, int G16, int XB, int lx, int HW, int8_t* yq = nullptr,
+                                               float scale = 1.f, int inp = 0) {
     const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (wave_id >= N * G16) return;
     const int n = wave_id / G16, j = wave_id - n * G16;
@@ -80,7 +85,17 @@ __global__ __launch_bounds__(256) void gap_blk(const float* __restrict__ x, floa
         v4f o;
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[i] = (float)(acc[i] / d);
-        *reinterpret_cast<v4f*>(y + blk * X + sub) = o;
+        if (!Q || y) *reinterpret_cast<v4f*>(y + blk * X + sub) = o;
+        if constexpr (Q) {
+            unsigned packed = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float r = rintf(o[i] / scale);
+                r = r > 127.f ? 127.f : (r < -127.f ? -127.f : r);
+                packed |= ((unsigned)(int)r & 0xffu) << (8 * i);
+            }
+            *reinterpret_cast<unsigned*>(yq + (long)n * inp + c) = packed;
+        }
     }
 }
 
@@ -137,8 +152,18 @@ hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y,
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st) {
     if (!pow2_block(xb)) return hipErrorInvalidValue;
     const int XB = cdiv(C, xb), G16 = cdiv(XB * xb, 16);
-    hipLaunchKernelGGL(gap_blk, dim3(cdiv(N * G16, 4)), dim3(256), 0, st, x, y, N, G16, XB,
+    hipLaunchKernelGGL(gap_blk<false>, dim3(cdiv(N * G16, 4)), dim3(256), 0, st, x, y, N, G16, XB,
                        ilog2(xb), H * W);
+    return hipGetLastError();
+}
+
+hipError_t launch_gap_q(const float* x, int N, int C, int H, int W, float* y, int8_t* yq, float scale,
+                        hipStream_t st) {
+    // block 16, C a multiple of 16: the means of image n are the row n * C ...
+    if (C % 16 || !x || !yq || !(scale > 0.f)) return hipErrorInvalidValue;
+    const int XB = C / 16, G16 = XB;
+    hipLaunchKernelGGL(gap_blk<true>, dim3(cdiv(N * G16, 4)), dim3(256), 0, st, x, y, N, G16, XB, 4, H * W, yq,
+                       scale, C);
     return hipGetLastError();
 }
 
