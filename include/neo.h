@@ -459,7 +459,9 @@ enum neo_plan_flags {
      * concatenation of concatenations) the first reader runs the
      * quantization pass.  Dense layers run in int8 too: weights quantized
      * per output row, the flattened input one int8 row per image (written by
-     * the producing dense layer, requantized, or quantized by a pass),
+     * the producing dense layer, requantized, or by the global average pool
+     * or the exit of the blocked layout, quantized by division, or by a
+     * pass),
      * exact int32 dot products, the same float32 epilogue.  Pools,
      * concatenation and flatten compute in float32 (the average pools and
      * the global average pool sum in double and round the mean once).  The
