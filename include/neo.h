@@ -259,6 +259,38 @@ int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8
                         neo_stream_t stream);
 
 /*
+ * Integer dense (fully connected) layer, the same quantization scheme as the
+ * integer conv (integer inference is the paper's future work, Sections 1
+ * and 5): y[n][k] = act(float32(acc) * m[k] + bias[k]) with acc[n][k] =
+ * sum_i xq[n][i] * w_q[k][i] exact in int32 and m[k] = x_scale * w_scale[k],
+ * evaluated one rounding per operation as for neo_conv2d_int8.  Rows are
+ * padded with zero bytes to INp = ceil(in_features / 16) * 16.
+ * neo_pack_dense_int8: w device fp32 [out_features][in_features] -> w_rows
+ *   device int8 [out_features][INp] (clamp(round_half_even(w / w_scale[k]),
+ *   -127, 127), the padding 0), w_scale device [out_features] = max |w[k]| /
+ *   127 (1 for a zero row).
+ * neo_quantize_rows_int8: x device fp32 [N][in_features] -> xq device int8
+ *   [N][INp], clamp(round_half_even(x / x_scale), -127, 127) with the
+ *   division in float32, the padding bytes written 0; x_scale > 0.
+ * neo_dense_int8: xq and w_rows as written above; bias device [out_features]
+ *   or NULL; act NEO_ACT_NONE or NEO_ACT_RELU; y device fp32
+ *   [N][out_features] and/or (non-NULL) yq device int8
+ *   [N][ceil(out_features / 16) * 16]: y requantized for the next dense
+ *   layer, clamp(round_half_even(y * r), -127, 127) with r = 1 / y_scale in
+ *   float32 (yq's padding bytes are not written: the caller zeroes them
+ *   once).  in_features at most 133,144 (the int32 sum's bound).  xq and
+ *   w_rows 16-byte aligned (NEO_ERR_ALIGN); NULL or non-positive arguments
+ *   NEO_ERR_INVALID_ARG; other errors as for neo_conv2d_blocked.
+ */
+int neo_pack_dense_int8(const float* w, int out_features, int in_features, int8_t* w_rows, float* w_scale,
+                        neo_stream_t stream);
+int neo_quantize_rows_int8(const float* x, int N, int in_features, float x_scale, int8_t* xq,
+                           neo_stream_t stream);
+int neo_dense_int8(const int8_t* xq, int N, int in_features, const int8_t* w_rows, const float* w_scale,
+                   int out_features, float x_scale, const float* bias, int act, float* y, float y_scale,
+                   int8_t* yq, neo_stream_t stream);
+
+/*
  * Batch-norm folding (inference simplification inherited by the paper,
  * Section 3): with scale[k] = gamma[k] / sqrt(var[k] + eps),
  *   w_out[k][c][r][s] = w[k][c][r][s] * scale[k]

@@ -509,6 +509,55 @@ int neo_conv2d_int8_acc(const int8_t* xq, int N, int C, int H, int W, const int8
                             cdiv(K, 16), acc, nullptr, 0.f, 0, 0, stream);
 }
 
+int neo_pack_dense_int8(const float* w, int out_features, int in_features, int8_t* w_rows, float* w_scale,
+                        neo_stream_t stream) {
+    if (!w || !w_rows || !w_scale) return fail(NEO_ERR_INVALID_ARG, "neo_pack_dense_int8: NULL buffer");
+    if (!aligned16(w_rows)) return fail(NEO_ERR_ALIGN, "neo_pack_dense_int8: w_rows not 16-byte aligned");
+    CHECK_POS(out_features); CHECK_POS(in_features);
+    CHECK_SIZE((long)out_features * in_features);
+    if ((long)out_features * (long)dense_i8_row_bytes(in_features) > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_pack_dense_int8: int8 weights of 2 GiB or more");
+    hipError_t e = launch_pack_dense_int8(w, out_features, in_features, w_rows, w_scale, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_pack_dense_int8 launch");
+}
+
+int neo_quantize_rows_int8(const float* x, int N, int in_features, float x_scale, int8_t* xq,
+                           neo_stream_t stream) {
+    if (!x || !xq) return fail(NEO_ERR_INVALID_ARG, "neo_quantize_rows_int8: NULL buffer");
+    if (!aligned16(xq)) return fail(NEO_ERR_ALIGN, "neo_quantize_rows_int8: xq not 16-byte aligned");
+    CHECK_POS(N); CHECK_POS(in_features);
+    if (!(x_scale > 0.f) || !std::isfinite(x_scale))
+        return fail(NEO_ERR_INVALID_ARG, "neo_quantize_rows_int8: x_scale must be finite and > 0");
+    if ((long)N * (long)dense_i8_row_bytes(in_features) > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_quantize_rows_int8: rows of 2 GiB or more");
+    hipError_t e = launch_quantize_rows_int8(x, N, in_features, x_scale, xq, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_quantize_rows_int8 launch");
+}
+
+int neo_dense_int8(const int8_t* xq, int N, int in_features, const int8_t* w_rows, const float* w_scale,
+                   int out_features, float x_scale, const float* bias, int act, float* y, float y_scale,
+                   int8_t* yq, neo_stream_t stream) {
+    if (!xq || !w_rows || !w_scale) return fail(NEO_ERR_INVALID_ARG, "neo_dense_int8: NULL buffer");
+    if (!y && !yq) return fail(NEO_ERR_INVALID_ARG, "neo_dense_int8: neither y nor yq given");
+    if (!aligned16(xq) || !aligned16(w_rows))
+        return fail(NEO_ERR_ALIGN, "neo_dense_int8: xq and w_rows must be 16-byte aligned");
+    CHECK_POS(N); CHECK_POS(in_features); CHECK_POS(out_features);
+    if (act != NEO_ACT_NONE && act != NEO_ACT_RELU) return fail(NEO_ERR_INVALID_ARG, "neo_dense_int8: act");
+    if (!(x_scale > 0.f) || !std::isfinite(x_scale))
+        return fail(NEO_ERR_INVALID_ARG, "neo_dense_int8: x_scale must be finite and > 0");
+    if (yq && (!(y_scale > 0.f) || !std::isfinite(y_scale) || !std::isfinite(1.0f / y_scale)))
+        return fail(NEO_ERR_INVALID_ARG, "neo_dense_int8: y_scale must be finite, > 0, with a finite reciprocal");
+    if ((long)in_features * 127 * 127 >= (1L << 31))
+        return fail(NEO_ERR_UNSUPPORTED, "neo_dense_int8: in_features above 133,144 could overflow int32");
+    if ((long)N * (long)dense_i8_row_bytes(in_features) > kMaxElems ||
+        (long)out_features * (long)dense_i8_row_bytes(in_features) > kMaxElems ||
+        (long)N * out_features > kMaxElems)
+        return fail(NEO_ERR_UNSUPPORTED, "neo_dense_int8: a tensor of 2 GiB or more");
+    hipError_t e = launch_dense_int8(xq, w_rows, w_scale, x_scale, bias, N, in_features, out_features, act, y, yq,
+                                     y_scale, (hipStream_t)stream);
+    return e == hipSuccess ? NEO_OK : hip_fail(e, "neo_dense_int8 launch");
+}
+
 int neo_fold_bn(const float* w, const float* bias, const float* gamma, const float* beta,
                 const float* mean, const float* var, float eps, int K, int C, int R, int S,
                 float* w_out, float* bias_out) {

@@ -545,17 +545,21 @@ __global__ __launch_bounds__(256) void dense_i8(DenseI8Args a) {
     }
 }
 
-// float32 [N][IN] -> int8 [N][INp] (the padding bytes are not written):
+// float32 [N][IN] -> int8 [N][INp] (the padding bytes i >= IN written 0):
 // clamp(round_half_even(x / scale), -127, 127), the division in float32.
 __global__ __launch_bounds__(256) void quantize_rows_kernel(const float* x, long total, int IN, long inp,
                                                             float scale, int8_t* q) {
-    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;  // over N * INp
     if (t >= total) return;
-    const long n = t / IN;
-    const int i = (int)(t - n * IN);
-    float r = rintf(x[t] / scale);
-    r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
-    q[n * inp + i] = (int8_t)(int)r;
+    const long n = t / inp;
+    const int i = (int)(t - n * inp);
+    int8_t b = 0;
+    if (i < IN) {
+        float r = rintf(x[n * IN + i] / scale);
+        r = r > (float)kQMax ? (float)kQMax : (r < -(float)kQMax ? -(float)kQMax : r);
+        b = (int8_t)(int)r;
+    }
+    q[t] = b;
 }
 
 // The exit of the blocked layout for an integer dense layer: NCHW16c float32
@@ -904,10 +908,10 @@ hipError_t launch_pack_dense_int8(const float* w, int OUT, int IN, int8_t* wq, f
 }
 
 hipError_t launch_quantize_rows_int8(const float* x, int N, int IN, float scale, int8_t* q, hipStream_t st) {
-    const long total = (long)N * IN;
-    if (total <= 0 || !(scale > 0.f)) return hipErrorInvalidValue;
+    const long inp = (long)dense_i8_row_bytes(IN), total = (long)N * inp;
+    if (N <= 0 || IN <= 0 || !(scale > 0.f)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, total, IN,
-                       (long)dense_i8_row_bytes(IN), scale, q);
+                       inp, scale, q);
     return hipGetLastError();
 }
 

@@ -97,6 +97,9 @@ def lib():
         "neo_conv2d_winograd": [P, I, I, I, I, P, I, P, I, I, ctypes.POINTER(Epilogue), P, I, I,
                                 P],
         "neo_quantize_int8": [P, I, I, I, I, F, I, I, P, P],
+        "neo_pack_dense_int8": [P, I, I, P, P, P],
+        "neo_quantize_rows_int8": [P, I, I, F, P, P],
+        "neo_dense_int8": [P, I, I, P, P, I, F, P, I, P, F, P, P],
         "neo_pack_filter_int8": [P, I, I, I, I, P, P, P],
         "neo_conv2d_int8": [P, I, I, I, I, P, P, I, I, I, F, P, I, I, I, I,
                             ctypes.POINTER(Epilogue), P, I, I, P],
@@ -378,6 +381,74 @@ def pack_filter_int8(w, out=None, scale=None, stream=None):
                                       _dptr_typed(out, torch.int8, "out"), _dptr(scale, "scale"),
                                       _stream(stream)))
     return out, scale
+
+
+def dense_row_bytes(n):
+    """Bytes of one int8 row of n values, padded to 16."""
+    return -(-int(n) // BLOCK) * BLOCK
+
+
+def pack_dense_int8(w, out=None, scale=None, stream=None):
+    """w: device [out][in] fp32 -> (int8 rows [out][dense_row_bytes(in)],
+    per-row scales [out] fp32), the scales max |w[k]| / 127."""
+    import torch
+    OUT, IN = w.shape
+    shape = (OUT, dense_row_bytes(IN))
+    if out is None:
+        out = torch.empty(shape, device=w.device, dtype=torch.int8)
+    if scale is None:
+        scale = torch.empty(OUT, device=w.device, dtype=torch.float32)
+    if out.numel() < OUT * shape[1]:
+        raise ValueError(f"out holds {out.numel()} bytes, the call needs {OUT * shape[1]}")
+    _need(scale, OUT, "scale")
+    _check(lib().neo_pack_dense_int8(_dptr(w, "w"), OUT, IN, _dptr_typed(out, torch.int8, "out"),
+                                     _dptr(scale, "scale"), _stream(stream)))
+    return out, scale
+
+
+def quantize_rows_int8(x, x_scale, out=None, stream=None):
+    """x: device [N][in] fp32 -> int8 rows [N][dense_row_bytes(in)],
+    clamp(round_half_even(x / x_scale), -127, 127), the padding 0."""
+    import torch
+    N, IN = x.shape
+    shape = (N, dense_row_bytes(IN))
+    if out is None:
+        out = torch.empty(shape, device=x.device, dtype=torch.int8)
+    if out.numel() < N * shape[1]:
+        raise ValueError(f"out holds {out.numel()} bytes, the call needs {N * shape[1]}")
+    _check(lib().neo_quantize_rows_int8(_dptr(x, "x"), N, IN, float(x_scale),
+                                        _dptr_typed(out, torch.int8, "out"), _stream(stream)))
+    return out
+
+
+def dense_int8(xq, IN, w_rows, w_scale, OUT, x_scale, bias=None, act="none", out=None,
+               y_scale=None, out_q=None, stream=None):
+    """Integer dense layer: xq int8 rows [N][dense_row_bytes(IN)]
+    (quantize_rows_int8), w_rows and w_scale from pack_dense_int8; fp32 output
+    [N][OUT] act(acc * x_scale * w_scale[k] + bias) (out), and with y_scale
+    also its int8 rows for the next dense layer (out_q, [N][dense_row_bytes(OUT)])
+    -- out=False for the int8 rows only."""
+    import torch
+    N = xq.shape[0]
+    if xq.numel() < N * dense_row_bytes(IN) or w_rows.numel() < OUT * dense_row_bytes(IN):
+        raise ValueError("xq or w_rows smaller than the layer's rows")
+    _need(w_scale, OUT, "w_scale")
+    _need(bias, OUT, "bias")
+    if out is None:
+        out = torch.empty((N, OUT), device=xq.device, dtype=torch.float32)
+    if out is not False:
+        _need(out, N * OUT, "out")
+    if y_scale is not None and out_q is None:
+        out_q = torch.zeros((N, dense_row_bytes(OUT)), device=xq.device, dtype=torch.int8)
+    if out_q is not None and out_q.numel() < N * dense_row_bytes(OUT):
+        raise ValueError(f"out_q holds {out_q.numel()} bytes, the call needs {N * dense_row_bytes(OUT)}")
+    yp = None if out is False else _dptr(out, "out")
+    qp = None if out_q is None else _dptr_typed(out_q, torch.int8, "out_q")
+    _check(lib().neo_dense_int8(_dptr_typed(xq, torch.int8, "xq"), N, IN,
+                                _dptr_typed(w_rows, torch.int8, "w_rows"), _dptr(w_scale, "w_scale"), OUT,
+                                float(x_scale), _dptr(bias, "bias"), ACT[act] if isinstance(act, str) else int(act),
+                                yp, float(y_scale or 0.0), qp, _stream(stream)))
+    return (None if out is False else out), out_q
 
 
 def _int8_args(xq, C, w_packed, K, R, S, stride, pad):

@@ -1,8 +1,11 @@
 """Integer (INT8) convolution (neo_quantize_int8, neo_pack_filter_int8,
-neo_conv2d_int8, neo_conv2d_int8_acc): argument handling on the host; on the
-GPU the quantized activations, the packed filter and its scales, and the int32
-accumulators bit-exact against the oracle's integer path (oracle.quant), and
-the dequantized float32 output within the rounding bound of its epilogue."""
+neo_conv2d_int8, neo_conv2d_int8_acc) and dense layer (neo_pack_dense_int8,
+neo_quantize_rows_int8, neo_dense_int8): argument handling on the host; on
+the GPU the quantized activations, the packed filters and their scales, and
+the int32 accumulators bit-exact against the oracle's integer path
+(oracle.quant), and the dequantized float32 output within the rounding bound
+of its epilogue (and bit-exact against the oracle's step-by-step float32
+evaluation)."""
 import ctypes
 
 import numpy as np
@@ -53,6 +56,32 @@ def test_argument_errors():
     assert L.neo_pack_filter_int8(None, 16, 16, 3, 3, FAKE, FAKE, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 16, 16, 3, 3, FAKE, None, None) == -1
     assert L.neo_pack_filter_int8(FAKE, 0, 16, 3, 3, FAKE, FAKE, None) == -1
+
+
+def test_dense_argument_errors():
+    """The integer dense layer's calls validate before any device work."""
+    L = neo.lib()
+    def d(xq=FAKE, IN=64, w=FAKE, ws=FAKE, OUT=16, xs=1.0, act=0, y=FAKE, ys=0.0, yq=None):
+        return L.neo_dense_int8(xq, 1, IN, w, ws, OUT, xs, None, act, y, ys, yq, None)
+    assert d(xq=None) == -1 and "neo_dense_int8" in neo.last_error()
+    assert d(ws=None) == -1
+    assert d(y=None, yq=None) == -1 and "neither" in neo.last_error()
+    assert d(xq=MIS) == -3 and d(w=MIS) == -3
+    assert d(IN=0) == -1 and d(OUT=-1) == -1
+    assert d(act=7) == -1
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert d(xs=bad) == -1 and "x_scale" in neo.last_error()
+    for bad in (0.0, -2.0, float("inf"), 1e-45):
+        assert d(yq=FAKE, ys=bad) == -1 and "y_scale" in neo.last_error()
+    # 133,145 inputs: 127^2 times that exceeds int32 (133,144 do not)
+    assert d(IN=133145) == -4 and "133,144" in neo.last_error()
+    assert L.neo_pack_dense_int8(None, 16, 64, FAKE, FAKE, None) == -1
+    assert L.neo_pack_dense_int8(FAKE, 16, 64, MIS, FAKE, None) == -3
+    assert L.neo_pack_dense_int8(FAKE, 0, 64, FAKE, FAKE, None) == -1
+    assert L.neo_quantize_rows_int8(FAKE, 1, 64, 0.0, FAKE, None) == -1
+    assert L.neo_quantize_rows_int8(FAKE, 1, 64, 1.0, MIS, None) == -3
+    assert L.neo_quantize_rows_int8(None, 1, 64, 1.0, FAKE, None) == -1
+    assert neo.dense_row_bytes(1000) == 1008 and neo.dense_row_bytes(4096) == 4096
 
 
 def test_packed_filter_size():
@@ -479,3 +508,64 @@ def test_two_layer_int8_chain(gpu):
     wq2, _ = gpu.pack_filter_int8(dev(w2))
     acc2 = gpu.conv2d_int8_acc(q1, 48, wq2, 64, 3, 3, stride=1, pad=1)
     assert_acc_equal(host(acc2), want, 64, "chain")
+
+
+# ---- integer dense layer -----------------------------------------------------------------
+@pytest.mark.gpu
+@pytest.mark.parametrize("N,IN,OUT", [(1, 1000, 10), (3, 37, 1000), (20, 512, 64), (40, 4096, 17)])
+def test_dense_int8_against_the_oracle(gpu, N, IN, OUT):
+    """The packed rows and scales, the quantized input rows (padding 0), the
+    float32 output with and without ReLU and its requantized rows, bit-exact
+    against the oracle's integer dense layer (quantize_filter per row,
+    dense_int, epilogue_f32, requantize); 40 images take two launches."""
+    from gpu_util import dev, host
+    rng = np.random.default_rng(N * 7919 + IN + OUT)
+    x = rng.uniform(-1, 1, (N, IN)).astype(np.float32)
+    w = (rng.standard_normal((OUT, IN)) * np.sqrt(2.0 / IN)).astype(np.float32)
+    b = rng.normal(0, 0.1, OUT).astype(np.float32)
+    xs = oq.act_scale(x)
+    wq, ws = oq.quantize_filter(w.reshape(OUT, IN, 1, 1))
+    wq = wq.reshape(OUT, IN)
+    rows, scale = neo.pack_dense_int8(dev(w))
+    r = host(rows)
+    np.testing.assert_array_equal(r[:, :IN], wq)
+    assert (r[:, IN:] == 0).all()
+    np.testing.assert_array_equal(host(scale), ws)
+    xq = neo.quantize_rows_int8(dev(x), xs)
+    q = host(xq)
+    np.testing.assert_array_equal(q[:, :IN], oq.quantize(x, xs))
+    assert (q[:, IN:] == 0).all()
+    acc = oq.dense_int(oq.quantize(x, xs), wq)
+    for act in ("none", "relu"):
+        y, _ = neo.dense_int8(xq, IN, rows, scale, OUT, xs, bias=dev(b), act=act)
+        ref = oq.epilogue_f32(acc[:, :, None, None], oq.multipliers(xs, ws), b, None, act)[:, :, 0, 0]
+        np.testing.assert_array_equal(host(y), ref)
+    ys = oq.act_scale(ref)
+    y2, yq = neo.dense_int8(xq, IN, rows, scale, OUT, xs, bias=dev(b), act="relu", y_scale=ys)
+    np.testing.assert_array_equal(host(y2), ref)
+    got = host(yq)
+    np.testing.assert_array_equal(got[:, :OUT], oq.requantize(ref, ys))
+    assert (got[:, OUT:] == 0).all()
+    # the int8 rows alone
+    _, yq2 = neo.dense_int8(xq, IN, rows, scale, OUT, xs, bias=dev(b), act="relu", out=False, y_scale=ys)
+    np.testing.assert_array_equal(host(yq2), got)
+
+
+@pytest.mark.gpu
+def test_dense_int8_extreme_sums(gpu):
+    """Every value +-127 over 25,088 inputs (VGG-16's first dense layer): the
+    sums reach 127^2 * 25,088 = 404,654,592 and stay exact."""
+    from gpu_util import dev, host
+    IN, OUT, N = 25088, 32, 2
+    x = np.ones((N, IN), np.float32)
+    x[1] = -1.0
+    w = np.ones((OUT, IN), np.float32)
+    w[1::2] = -1.0
+    rows, scale = neo.pack_dense_int8(dev(w))
+    xq = neo.quantize_rows_int8(dev(x), 1.0 / 127)
+    y, _ = neo.dense_int8(xq, IN, rows, scale, OUT, np.float32(1.0 / 127))
+    acc = oq.dense_int(oq.quantize(x, np.float32(1.0 / 127)), oq.quantize_filter(w.reshape(OUT, IN, 1, 1))[0]
+                       .reshape(OUT, IN))
+    assert int(np.abs(acc).max()) == 127 * 127 * IN
+    ref = oq.epilogue_f32(acc[:, :, None, None], oq.multipliers(np.float32(1.0 / 127), host(scale)))[:, :, 0, 0]
+    np.testing.assert_array_equal(host(y), ref)
