@@ -37,7 +37,8 @@ path: weights quantized per output row, the flattened input with one scale
 exact integer dot products, the same float32 epilogue.  Pools,
 concatenation and flatten are the float32 oracle's own.
 
-Only ``tests/`` use this module.  It shares no code with the HIP library.
+Only ``tests/`` and ``__graft_entry__.smoke()`` use this module.  It shares no code with
+the HIP library.
 """
 from __future__ import annotations
 
