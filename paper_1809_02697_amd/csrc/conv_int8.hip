@@ -562,6 +562,103 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(const float* x, long
     q[t] = b;
 }
 
+// A conv over few input channels (a network's stem) as a 1x1 conv: the
+// float32 NCHW16c input [N][ceil(C/16)][H][W][16] quantized into its im2col
+// rows, int8 NCHW16c [N][ceil(R*S*C/16)][OH][OW][16] with channel
+// (r * S + s) * C + c holding input channel c at tap (r, s) of output pixel
+// (oh, ow) (0 outside the image and past R*S*C), clamp(round_half_even(x /
+// scale), -127, 127) with the division in float32.  The 1x1 conv over it
+// sums the same products as the conv.  NCHW: the input is plain NCHW
+// [N][C][H][W] instead (a network's input, read without its blocked copy).
+//
+// One workgroup per 64 output pixels of one row: the R input rows they
+// read, span = 63 sw + S pixels wide, quantized once into LDS as int8 rows
+// [C][R][span] plus one zero row (each input value is read by up to
+// R S / (sh sw) taps; one float32 division per value), and a table of each
+// im2col channel's offset in that tile (the zero row past R*S*C); then every
+// thread assembles 16-byte output blocks with 16 LDS byte reads at its
+// pixel's offset plus the table's (wave-uniform) entries.  64 consecutive
+// pixels of a block row are one contiguous 1 KiB store.  No integer
+// division per element: each thread steps its (row, column) by the
+// workgroup size.
+constexpr int kIm2colPix = 64;
+template <bool NCHW>
+__global__ __launch_bounds__(256) void im2col_q_kernel(const float* x, int C, int H, int W, int R, int S, int sh,
+                                                       int sw, int ph, int pw, int OH, int OW, int CBc,
+                                                       float scale, int8_t* q) {
+    extern __shared__ int lds_words[];
+    const int span = (kIm2colPix - 1) * sw + S;
+    const int rows = C * R;                     // + the zero row
+    int* table = lds_words;                     // [CBc * 16]
+    int8_t* tile = reinterpret_cast<int8_t*>(lds_words + CBc * 16);  // [rows + 1][span]
+    const int n = blockIdx.z, oh = blockIdx.y, ow0 = blockIdx.x * kIm2colPix;
+    const int ih0 = oh * sh - ph, iw0 = ow0 * sw - pw;
+    const int CBx = (C + 15) / 16;
+    const float* xn = x + (NCHW ? (long)n * C * H * W : (long)n * CBx * H * W * 16);
+    const int RSC = R * S * C;
+    for (int ch = threadIdx.x; ch < CBc * 16; ch += 256) {  // (256 threads)
+        int off = rows * span;                              // the zero row
+        if (ch < RSC) {
+            const int rs = ch / C, c = ch - rs * C, r = rs / S;
+            off = (c * R + r) * span + (rs - r * S);
+        }
+        table[ch] = off;
+    }
+    // element e = row * span + j of the tile, row = c * R + r; thread t takes
+    // e = t, t + 256, ...: (row, j) and (c, r) stepped, not divided
+    const int total = (rows + 1) * span;
+    const int drow = 256 / span, dj = 256 - drow * span;
+    int j = threadIdx.x % span, r = threadIdx.x / span, c = 0;
+    while (r >= R) {
+        r -= R;
+        ++c;
+    }
+    constexpr int kBatch = 8;  // loads in flight per thread before the first LDS store
+    for (int e0 = threadIdx.x; e0 < total; e0 += kBatch * 256) {
+        float v[kBatch];
+        int slot[kBatch];
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+            const int ih = ih0 + r, iw = iw0 + j;
+            v[k] = (c < C && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W)
+                       ? (NCHW ? xn[((long)c * H + ih) * W + iw]
+                               : xn[((long)((c >> 4) * H + ih) * W + iw) * 16 + (c & 15)])
+                       : 0.f;
+            slot[k] = (c * R + r) * span + j;  // = e0 + 256 k while inside the tile
+            j += dj;
+            r += drow;
+            if (j >= span) {
+                j -= span;
+                ++r;
+            }
+            while (r >= R) {
+                r -= R;
+                ++c;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+            float q8 = rintf(v[k] / scale);
+            q8 = q8 > (float)kQMax ? (float)kQMax : (q8 < -(float)kQMax ? -(float)kQMax : q8);
+            if (e0 + k * 256 < total) tile[slot[k]] = (int8_t)(int)q8;
+        }
+    }
+    __syncthreads();
+    const int owl = threadIdx.x % kIm2colPix, ow = ow0 + owl;
+    if (ow >= OW) return;
+    const int8_t* px = tile + owl * sw;
+    for (int cb = threadIdx.x / kIm2colPix; cb < CBc; cb += 256 / kIm2colPix) {
+        const int* t16 = table + cb * 16;
+        union {
+            int8_t b[16];
+            v4i v;
+        } out;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) out.b[i] = px[t16[i]];
+        *reinterpret_cast<v4i*>(q + ((((long)n * CBc + cb) * OH + oh) * OW + ow) * 16) = out.v;
+    }
+}
+
 // The exit of the blocked layout for an integer dense layer: NCHW16c float32
 // -> the flattened NCHW order, as float32 (y, may be null) and/or int8 rows
 // (yq [N][inp]) quantized by division.  One thread per output element.
@@ -890,6 +987,33 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
 }
 
 size_t dense_i8_row_bytes(int IN) { return (size_t)cdiv(IN, 16) * 16; }
+
+ConvShape im2col_shape(const ConvShape& s) {
+    ConvShape t = s;
+    t.C = s.C * s.R * s.S;
+    t.H = s.OH;
+    t.W = s.OW;
+    t.R = t.S = t.sh = t.sw = 1;
+    t.ph = t.pw = 0;
+    return t;
+}
+
+size_t im2col_lds_bytes(const ConvShape& s) {
+    return (size_t)cdiv(s.C * s.R * s.S, 16) * 64 + (size_t)(s.C * s.R + 1) * ((kIm2colPix - 1) * s.sw + s.S);
+}
+
+hipError_t launch_im2col_int8(const float* x, bool nchw, const ConvShape& s, float scale, int8_t* q,
+                              hipStream_t st) {
+    const int CBc = cdiv(s.C * s.R * s.S, 16);
+    const size_t lds = im2col_lds_bytes(s);
+    if (s.N <= 0 || s.N > 65535 || s.OH <= 0 || s.OH > 65535 || s.OW <= 0 || lds > kIm2colMaxLds ||
+        !(scale > 0.f))
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(nchw ? im2col_q_kernel<true> : im2col_q_kernel<false>, dim3(cdiv(s.OW, kIm2colPix), s.OH, s.N),
+                       dim3(256), lds, st, x, s.C, s.H, s.W, s.R, s.S, s.sh, s.sw, s.ph, s.pw, s.OH, s.OW, CBc,
+                       scale, q);
+    return hipGetLastError();
+}
 
 hipError_t launch_blk_to_rows_int8(const float* x, int N, int C, int H, int W, float* y, int8_t* yq,
                                    float scale, hipStream_t st) {

@@ -235,6 +235,18 @@ hipError_t launch_quantize_rows_int8(const float* x, int N, int IN, float scale,
 hipError_t launch_dense_int8(const int8_t* xq, const int8_t* wq, const float* wscale, float xscale,
                              const float* bias, int N, int IN, int OUT, int act, float* y, int8_t* yq,
                              float yscale, hipStream_t st);
+// A conv over few input channels as a 1x1 conv: the shape of that 1x1 conv
+// (R * S * C channels on the OH x OW map), and the quantization of the conv's
+// float32 input x (NCHW16c, or plain NCHW when nchw) into its im2col rows
+// (int8 NCHW16c, no halo) by division by scale.
+// (the pass stages each 64 output pixels' input rows in LDS: (C R + 1) *
+// (63 sw + S) bytes and a 4-byte offset per im2col channel, at most
+// kIm2colMaxLds; N and OH at most 65535)
+ConvShape im2col_shape(const ConvShape& s);
+constexpr size_t kIm2colMaxLds = 32768;
+size_t im2col_lds_bytes(const ConvShape& s);
+hipError_t launch_im2col_int8(const float* x, bool nchw, const ConvShape& s, float scale, int8_t* q,
+                              hipStream_t st);
 // One integer conv from a member's operands (float32 and/or int8 outputs).
 hipError_t launch_conv_int8_m(const I8Member& m, const ConvConfig& c, hipStream_t st);
 bool int8_group_config_valid(const ConvShape* s, int n, const ConvConfig& c);

@@ -102,7 +102,15 @@ struct Step {
     // ST_DENSE with NEO_PLAN_INT8 over many images: run as the 1x1 integer
     // conv cs (its filter packed in the conv's order, configuration c8)
     bool d_conv = false;
+    // ST_CONV with NEO_PLAN_INT8 over few input channels (a network stem):
+    // run as the 1x1 integer conv over the input's im2col rows (R * S * C
+    // channels, the filter in K(RS)C order), which sums the same products
+    // with far fewer 64-channel reduction steps
+    bool i2c = false;
 };
+
+// The shape an integer conv step runs.
+static ConvShape int8_conv_shape(const Step& s) { return s.i2c ? im2col_shape(s.cs) : s.cs; }
 
 // NEO_PLAN_INT8: the int8 copy of a value, its halo the largest padding of
 // the convs that read it, in the int8 arena, with its scale; written by the
@@ -118,6 +126,13 @@ struct I8Copy {
     bool assembled = false;
     // a dense layer's input: int8 rows [N][dense_i8_row_bytes(C)], no halo
     bool rows = false;
+    // the im2col rows of one conv's input (the conv's shape), no halo;
+    // quantized by that conv's own pass
+    bool im2col = false;
+    ConvShape ics{};
+    // im2col from the plain NCHW value src, whose blocked copy (val) nothing
+    // else reads: the layout transform producing val is dropped
+    int src = -1;
 };
 
 struct Xform {
@@ -509,6 +524,24 @@ int build_steps(neo_plan* P) {
                         xq + 4L * (a->H + 2 * d.pad_h) * (a->W + 2 * d.pad_w) * 16 >= (1L << 31))
                         return fail(NEO_ERR_UNSUPPORTED, where + "int8 input or filter of 2 GiB or more");
                     st.i8 = true;
+                    // im2col when it at least halves the reduction steps
+                    // (C = 3: 3 instead of 49 for 7x7, 1 instead of 9 for 3x3;
+                    // a conv's input is never a concatenation's slice)
+                    const long rsc = (long)C * d.R * d.S;
+                    st.i2c = d.R * d.S > 1 && P->vals[st.in].layout == 16 && P->vals[st.in].alias_of < 0 &&
+                             2 * cdiv(rsc, 64) <= (long)d.R * d.S * cdiv(C, 64) &&
+                             (long)int8_act_bytes(ni.N, (int)rsc, ni.H, ni.W, 0, 0) + 4L * ni.H * ni.W * 16 <
+                                 (1L << 31) &&
+                             im2col_lds_bytes(st.cs) <= kIm2colMaxLds && ni.N <= 65535 && ni.H <= 65535;
+                    if (st.i2c) {
+                        // KCRS -> K(RS)C: channel (r * S + s) * C + c of the 1x1 filter
+                        std::vector<float> wt(w.size());
+                        for (long k = 0; k < d.K; ++k)
+                            for (int c = 0; c < C; ++c)
+                                for (int rs = 0; rs < d.R * d.S; ++rs)
+                                    wt[(k * d.R * d.S + rs) * C + c] = w[(k * C + c) * d.R * d.S + rs];
+                        w.swap(wt);
+                    }
                     st.kcrs_off = add_params(P, w);
                     st.ws8_off = add_params(P, std::vector<float>((size_t)cdiv(d.K, 16) * 16, 1.f));
                     auto take = [&](long bytes) {
@@ -516,8 +549,9 @@ int build_steps(neo_plan* P) {
                         P->i8_bytes += (bytes + 255) / 256 * 256;
                         return off;
                     };
-                    st.w8_off = take((long)int8_filter_bytes(d.K, C, d.R, d.S));
-                    st.c8 = choose_int8_config(st.cs);
+                    const ConvShape s8 = int8_conv_shape(st);
+                    st.w8_off = take((long)int8_filter_bytes(s8.K, s8.C, s8.R, s8.S));
+                    st.c8 = choose_int8_config(s8);
                 }
                 st.cc = choose_conv_config(st.cs);
                 if (!(P->flags & NEO_PLAN_HOST_ONLY)) st.tuned = tuned_config(st.cs, true, &st.cc);
@@ -813,7 +847,7 @@ void group_ready_convs(neo_plan* P) {
             grp.in = S[convs[k]].in;
             for (size_t m = k; m < e; ++m) grp.members.push_back(S[convs[m]]);
             std::vector<ConvShape> shp;
-            for (const Step& m : grp.members) shp.push_back(m.cs);
+            for (const Step& m : grp.members) shp.push_back(m.i8 ? int8_conv_shape(m) : m.cs);
             if (grp.members[0].i8) {
                 // integer convs (an int8 plan has no others): one int8
                 // configuration for all members
@@ -1088,17 +1122,19 @@ void plan_int8_copies(neo_plan* P) {
         if (!((t.kind == ST_CONV || t.kind == ST_DENSE) && t.i8)) continue;
         const bool rows = t.kind == ST_DENSE;
         int c = -1;
-        for (int k = 0; k < (int)P->i8_copies.size(); ++k)
-            if (P->i8_copies[k].val == t.in && P->i8_copies[k].rows == rows) c = k;
+        for (int k = 0; k < (int)P->i8_copies.size() && !t.i2c; ++k)
+            if (P->i8_copies[k].val == t.in && P->i8_copies[k].rows == rows && !P->i8_copies[k].im2col) c = k;
         if (c < 0) {
             c = (int)P->i8_copies.size();
-            I8Copy q{t.in, rows ? 0 : t.cs.ph, rows ? 0 : t.cs.pw, -1};
+            I8Copy q{t.in, rows || t.i2c ? 0 : t.cs.ph, rows || t.i2c ? 0 : t.cs.pw, -1};
             q.rows = rows;
+            q.im2col = t.i2c;
+            q.ics = t.cs;
             P->i8_copies.push_back(q);
             t.quant_here = true;  // the first reader, unless a writer takes it over
         }
         I8Copy& q = P->i8_copies[c];
-        if (!rows) {
+        if (!rows && !t.i2c) {
             q.ph = std::max(q.ph, t.cs.ph);
             q.pw = std::max(q.pw, t.cs.pw);
         }
@@ -1107,12 +1143,15 @@ void plan_int8_copies(neo_plan* P) {
     for (I8Copy& q : P->i8_copies) {
         const Val& v = P->vals[q.val];
         q.xq_off = P->i8_bytes;
-        const long bytes = q.rows ? (long)v.N * (long)dense_i8_row_bytes(v.C * v.H * v.W)
-                                  : (long)int8_act_bytes(v.N, v.C, v.H, v.W, q.ph, q.pw);
+        const ConvShape is = im2col_shape(q.ics);
+        const long bytes = q.rows     ? (long)v.N * (long)dense_i8_row_bytes(v.C * v.H * v.W)
+                           : q.im2col ? (long)int8_act_bytes(is.N, is.C, is.H, is.W, 0, 0)
+                                      : (long)int8_act_bytes(v.N, v.C, v.H, v.W, q.ph, q.pw);
         P->i8_bytes += (bytes + 255) / 256 * 256;
     }
     for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
         I8Copy& q = P->i8_copies[c];
+        if (q.im2col) continue;  // its conv's own pass
         int w = -1;
         for (int i = 0; i < ns; ++i) {
             const Step& t = P->steps[i];
@@ -1157,8 +1196,8 @@ void plan_int8_copies(neo_plan* P) {
     for (int c = 0; c < (int)P->i8_copies.size(); ++c) {
         I8Copy& q = P->i8_copies[c];
         const Val& cv = P->vals[q.val];
-        if (q.writer >= 0 || cv.node < 0 || P->nodes[cv.node].nd.op != NEO_OP_CONCAT || cv.layout != 16 ||
-            cv.view)
+        if (q.writer >= 0 || q.im2col || cv.node < 0 || P->nodes[cv.node].nd.op != NEO_OP_CONCAT ||
+            cv.layout != 16 || cv.view)
             continue;
         std::vector<std::pair<int, int>> parts;  // (producer step, block offset in the concatenation)
         // the parts of concatenation node `node`, through nested
@@ -1192,7 +1231,7 @@ void plan_int8_copies(neo_plan* P) {
             if (o.alias_of == q.val) f32 = true;
         for (int i = 0; i < ns; ++i) {
             const Step& t = P->steps[i];
-            if ((t.in == q.val && !(t.kind == ST_CONV && t.i8)) || t.res == q.val) f32 = true;
+            if ((t.in == q.val && !(t.kind == ST_CONV && t.i8 && !t.i2c)) || t.res == q.val) f32 = true;
         }
         q.assembled = true;
         for (const auto& pw : parts) {
@@ -1204,6 +1243,34 @@ void plan_int8_copies(neo_plan* P) {
         }
         for (Step& t : P->steps)
             if (t.qc == c) t.quant_here = false;
+    }
+}
+
+// NEO_PLAN_INT8: an im2col copy whose value is only the NCHW -> NCHW16c
+// transform of a plain NCHW value (a network's input) read by nothing else:
+// the pass reads the NCHW value and the transform step goes (at batch 32 it
+// would write 16 float lanes per pixel for 3 channels).
+void drop_im2col_transforms(neo_plan* P) {
+    for (I8Copy& q : P->i8_copies) {
+        if (!q.im2col) continue;
+        int ti = -1, readers = 0;
+        for (int i = 0; i < (int)P->steps.size(); ++i) {
+            const Step& t = P->steps[i];
+            if (t.kind == ST_TRANSFORM && t.out == q.val && t.src_block == 0 && t.dst_block == 16) ti = i;
+            if (t.in == q.val || t.res == q.val || t.out2 == q.val) ++readers;
+            for (const Step& m : t.members)
+                if (m.in == q.val || m.res == q.val) ++readers;
+        }
+        bool plain = q.val != P->out_val && !P->vals[q.val].view;
+        for (const Val& v : P->vals)
+            if (v.alias_of == q.val) plain = false;
+        if (ti < 0 || readers != 1 || !plain) continue;
+        const Val& sv = P->vals[P->steps[ti].in];
+        if (sv.layout != 0 || sv.view || sv.alias_of >= 0) continue;
+        q.src = P->steps[ti].in;
+        P->steps.erase(P->steps.begin() + ti);
+        for (I8Copy& o : P->i8_copies)
+            if (o.writer > ti) --o.writer;
     }
 }
 
@@ -1288,6 +1355,8 @@ std::string describe(const neo_plan* P) {
                   << ",\"input_copy\":" << s.qc << ",\"quantizes_input\":"
                   << (s.quant_here ? "true" : "false") << ",\"writes_copy\":" << s.q_out
                   << ",\"writes_f32\":" << (s.f32_needed ? "true" : "false");
+                if (s.i2c)
+                    o << ",\"im2col\":" << (P->i8_copies[s.qc].src >= 0 ? "\"nchw\"" : "\"blocked\"");
                 if (s.q_off8 >= 0) o << ",\"writes_slice\":[" << s.q_off8 << "," << s.q_tot8 << "]";
                 o << "}";
             }
@@ -1618,11 +1687,12 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK) rc = build_steps(P);
         if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) {
             plan_int8_copies(P);
+            drop_im2col_transforms(P);
             if (!(flags & NEO_PLAN_HOST_ONLY))
                 for (Step& st : P->steps)
                     if ((st.kind == ST_CONV || (st.kind == ST_DENSE && st.d_conv)) && st.i8) {
                         const int mode = st.q_out < 0 ? 0 : st.f32_needed ? 3 : 2;
-                        st.tuned = tuned_int8_config(st.cs, mode, &st.c8);
+                        st.tuned = tuned_int8_config(int8_conv_shape(st), mode, &st.c8);
                     }
         }
         if (rc == NEO_OK && (flags & NEO_PLAN_FUSE_GAP)) fuse_gap(P);
@@ -1683,10 +1753,11 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
             if (e == hipSuccess) e = hipMalloc(&P->d_absmax, 256);
             // (every integer conv: the steps' and the group launches' members)
             auto pack = [&](const Step& st) {
-                if (e == hipSuccess && st.kind == ST_CONV && st.i8)
-                    e = launch_pack_filter_int8(P->d_params + st.kcrs_off, st.cs.K, st.cs.C, st.cs.R,
-                                                st.cs.S, P->d_i8 + st.w8_off, P->d_params + st.ws8_off,
-                                                nullptr);
+                if (e == hipSuccess && st.kind == ST_CONV && st.i8) {
+                    const ConvShape s8 = int8_conv_shape(st);  // (im2col: the K(RS)C filter as 1x1)
+                    e = launch_pack_filter_int8(P->d_params + st.kcrs_off, s8.K, s8.C, s8.R, s8.S,
+                                                P->d_i8 + st.w8_off, P->d_params + st.ws8_off, nullptr);
+                }
                 if (e == hipSuccess && st.kind == ST_DENSE && st.i8)
                     e = st.d_conv  // [OUT][IN] float32 is KCRS with R = S = 1
                             ? launch_pack_filter_int8(P->d_params + st.w_off, st.dense_out, st.dense_in, 1, 1,
@@ -1786,7 +1857,7 @@ static I8Member i8_member(const neo_plan* P, const Step& s, const float* x_nchw,
     const I8Copy& qc = P->i8_copies[s.qc];
     const I8Copy* qo = (s.q_out >= 0 && !P->i8_f32_out) ? &P->i8_copies[s.q_out] : nullptr;
     I8Member m;
-    m.s = s.cs;
+    m.s = int8_conv_shape(s);
     m.x = P->d_i8 + qc.xq_off;
     m.w = P->d_i8 + s.w8_off;
     m.wscale = P->d_params + s.ws8_off;
@@ -1811,6 +1882,9 @@ static hipError_t i8_quant_pass(const neo_plan* P, const Step& s, const float* x
     if (!s.quant_here) return hipSuccess;
     const Val& in = P->vals[s.in];
     const I8Copy& qc = P->i8_copies[s.qc];
+    if (qc.im2col)
+        return launch_im2col_int8(val_ptr(P, qc.src >= 0 ? qc.src : s.in, x_nchw, y_out), qc.src >= 0, qc.ics,
+                                  qc.xscale, P->d_i8 + qc.xq_off, st);
     if (qc.rows)
         return launch_quantize_rows_int8(val_ptr(P, s.in, x_nchw, y_out), in.N, in.C * in.H * in.W, qc.xscale,
                                          P->d_i8 + qc.xq_off, st);
@@ -2443,10 +2517,13 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
             assembled[s.qc] = 1;
         }
         // a copy quantized by its own pass: the scale of the value it reads
-        if ((s.kind == ST_CONV || s.kind == ST_DENSE) && s.i8 && s.quant_here &&
-            (rc = scale_of(val_ptr(P, s.in, x_nchw, y_out), elems(s.in),
-                           &P->i8_copies[s.qc].xscale)) != NEO_OK)
-            return rc;
+        // (an im2col pass from the NCHW value: that value's)
+        if ((s.kind == ST_CONV || s.kind == ST_DENSE) && s.i8 && s.quant_here) {
+            const int src = P->i8_copies[s.qc].src >= 0 ? P->i8_copies[s.qc].src : s.in;
+            if ((rc = scale_of(val_ptr(P, src, x_nchw, y_out), elems(src), &P->i8_copies[s.qc].xscale)) !=
+                NEO_OK)
+                return rc;
+        }
         if (s.q_out >= 0 && P->i8_copies[s.q_out].assembled) {
             // a part of an assembled copy: float32 only until the copy's scale is known
             P->i8_f32_out = true;

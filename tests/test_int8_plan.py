@@ -25,7 +25,8 @@ def test_host_plan_and_flags():
     p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)
     d = p.describe()
     convs = [s for s in d["steps"] if s["kind"] == "conv"]
-    assert len(convs) == 53 and len(d["steps"]) == 57
+    # (the stem reads the network input directly: no NCHW -> NCHW16c step)
+    assert len(convs) == 53 and len(d["steps"]) == 56
     assert all(s["conv"]["algo"] == "int8" and not s["conv"]["int8"]["calibrated"] for s in convs)
     assert not any(s["kind"].startswith("conv_") for s in d["steps"])     # no fused steps
     # one int8 copy per value: 49 for 53 convs (each stage's input is shared
@@ -37,6 +38,10 @@ def test_host_plan_and_flags():
     q = [s["conv"]["int8"] for s in convs]
     assert len({x["input_copy"] for x in q}) == 49
     assert sum(x["quantizes_input"] for x in q) == 1 and q[0]["quantizes_input"]
+    # the 7x7 stem over 3 channels runs as a 1x1 conv over its input's im2col
+    # rows (147 channels: 3 reduction steps of 64 instead of 49), quantized
+    # straight from the NCHW network input
+    assert [x.get("im2col", False) for x in q] == ["nchw"] + [False] * 52
     assert sum(x["writes_copy"] >= 0 for x in q) == 47
     assert sum(x["writes_copy"] >= 0 and x["writes_f32"] for x in q) == 12
     pool = [s for s in d["steps"] if s["kind"] == "maxpool"][0]
@@ -169,6 +174,50 @@ def run_int8_plan(gpu, g, flags=0):
     assert all(c["int8"]["calibrated"] for _, c in conv_steps(d))
     y = host(p.run(x))
     return y_cal, y, plan_scales(d), p
+
+
+STEMS = [  # (C, R, S, stride, pad, H, W, N, im2col)
+    (3, 7, 7, 2, 3, 37, 41, 2, True),     # ResNet's stem: 147 channels, ragged last block
+    (3, 3, 3, 2, 0, 29, 29, 1, True),     # Inception's: 27 channels
+    (17, 3, 3, 1, 1, 15, 13, 2, True),    # two input blocks: 153 channels
+    (5, 5, 3, 1, (2, 1), 19, 9, 3, True),
+    (40, 3, 3, 1, 1, 11, 11, 1, False),   # 360 channels: 6 steps against 9, not taken
+    (3, 1, 1, 1, 0, 9, 9, 1, False),      # a 1x1 conv: nothing to gain
+]
+
+
+@pytest.mark.parametrize("C,R,S,stride,pad,H,W,N,i2c", STEMS)
+def test_host_im2col_choice(C, R, S, stride, pad, H, W, N, i2c):
+    """An integer conv runs over its input's im2col rows exactly when that at
+    least halves its 64-channel reduction steps."""
+    g = wl.stem_graph(N=N, C=C, H=H, W=W, K=32, R=R, S=S, stride=stride, pad=pad)
+    p = neo.Plan(g, flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)
+    d = p.describe()
+    (_, c), = conv_steps(d)
+    p.destroy()
+    assert c["int8"].get("im2col", False) == ("nchw" if i2c else False) and c["int8"]["quantizes_input"]
+    # the network input's blocked copy only when the direct conv reads it
+    # (besides the exit of the pool's output to NCHW)
+    assert sum(s["kind"] == "transform" for s in d["steps"]) == (1 if i2c else 2)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("C,R,S,stride,pad,H,W,N,i2c", STEMS)
+def test_im2col_stem_against_the_oracle(gpu, C, R, S, stride, pad, H, W, N, i2c):
+    """The stem through the im2col rows (or the direct path) bit-exact
+    against the oracle's integer conv: the same int8 inputs, the same integer
+    sums, the same float32 epilogue."""
+    from gpu_util import dev, host
+    print(f"\n[int8 stem] C={C} R={R} S={S} stride={stride} pad={pad} {H}x{W} N={N}", flush=True)
+    g = wl.stem_graph(N=N, C=C, H=H, W=W, K=32, R=R, S=S, stride=stride, pad=pad)
+    y_cal, y, scales, p = run_int8_plan(gpu, g)
+    (_, c), = conv_steps(p.describe())
+    p.destroy()
+    assert bool(c["int8"].get("im2col", False)) == i2c
+    ref, ref_scales = oq.run_graph_int8(g)
+    assert np.array_equal(np.array([scales[i] for i in int8_ids(g)], np.float32), ref_scales)
+    np.testing.assert_array_equal(y, ref.reshape(y.shape))
+    np.testing.assert_array_equal(y_cal, y)
 
 
 @pytest.mark.gpu
