@@ -105,7 +105,9 @@ INT8_PLAN_COMMANDS = [
     for m in INT8_PLAN_MODELS] + ["python -m paper_1809_02697_amd.profile_summary RUN_DIR"]
 # kernel name -> the part of an integer forward it does (first match)
 INT8_PLAN_KINDS = [("conv_i8_group", "int8 conv group launches"), ("conv_i8", "int8 convs alone"),
-                   ("quantize_kernel", "quantization passes"), ("pool_blk_q", "pools writing an int8 copy"),
+                   ("quantize_kernel", "quantization passes"),
+                   ("im2col_q", "quantization passes (im2col rows of the stem)"),
+                   ("pool_blk_q", "pools writing an int8 copy"),
                    ("pool_blk", "float32 pools"), ("gap_blk", "global average pool"),
                    ("dense_", "dense layers"), ("_to_", "layout transforms")]
 
