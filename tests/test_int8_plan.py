@@ -220,6 +220,36 @@ def test_im2col_stem_against_the_oracle(gpu, C, R, S, stride, pad, H, W, N, i2c)
     np.testing.assert_array_equal(y_cal, y)
 
 
+def two_stems_graph(N=2, H=21, W=19):
+    """Two small-channel convs reading the network input (a 7x7 and a 3x3,
+    both im2col), concatenated: the input's blocked copy has two readers, so
+    both passes read it instead of the NCHW input."""
+    b = wl._Builder("two_stems", (N, 3, H, W), np.random.Generator(np.random.PCG64(11)))
+    a = b.conv(0, 32, 7, stride=2, pad=3, name="s7")
+    c = b.conv(0, 16, 3, stride=2, pad=1, name="s3")
+    b.output(b.concat([a, c], name="cat"))
+    return b.finish(wl._normal_input((N, 3, H, W)))
+
+
+def test_host_im2col_from_the_blocked_input():
+    p = neo.Plan(two_stems_graph(), flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)
+    d = p.describe()
+    p.destroy()
+    assert [c["int8"].get("im2col") for _, c in conv_steps(d)] == ["blocked", "blocked"]
+
+
+@pytest.mark.gpu
+def test_im2col_from_the_blocked_input_against_the_oracle(gpu):
+    print("\n[int8 stem] two stems from the blocked input", flush=True)
+    g = two_stems_graph()
+    y_cal, y, scales, p = run_int8_plan(gpu, g)
+    p.destroy()
+    ref, ref_scales = oq.run_graph_int8(g)
+    assert np.array_equal(np.array([scales[i] for i in int8_ids(g)], np.float32), ref_scales)
+    np.testing.assert_array_equal(y, ref.reshape(y.shape))
+    np.testing.assert_array_equal(y_cal, y)
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("name,N", [("tiny", 2), ("vgg_tiny", 2), ("vgg_tiny", 20), ("resnet50", 1),
                                     ("resnet50", 2), ("vgg16", 1), ("inception_v3", 1)])
