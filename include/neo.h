@@ -489,7 +489,12 @@ enum neo_plan_flags {
      * is assembled by its parts' producers, each writing its slice of the
      * copy with the concatenation's scale.  Otherwise (the network input, a
      * concatenation of concatenations) the first reader runs the
-     * quantization pass.  Dense layers run in int8 too: weights quantized
+     * quantization pass.  A conv over few input channels (a stem) whose
+     * 64-channel reduction steps at least halve that way runs as a 1x1
+     * integer conv over its input's im2col rows (channel (r*S + s)*C + c;
+     * the same integer sums): its pass writes those rows, from the NCHW
+     * network input directly when nothing else reads the input's blocked
+     * copy (that layout transform is then not run).  Dense layers run in int8 too: weights quantized
      * per output row, the flattened input one int8 row per image (written by
      * the producing dense layer, requantized, or by the global average pool
      * or the exit of the blocked layout, quantized by division, or by a
