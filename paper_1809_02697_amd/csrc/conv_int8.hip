@@ -63,6 +63,7 @@ struct I8Args {
     int* acc;             // raw mode: int32 NCHW16c [N][KB][OH][OW][16]
     int8_t* yq;           // int8 modes: NCHW16c with a halo [N][KB][OH + 2 qph][OW + 2 qpw][16]
     float yrcp;           // int8 mode: 1 / (the output's scale), rounded to float32
+    float ydiv;           // > 0: requantize by division by this scale instead
     int qph, qpw;         // int8 modes: the output's halo
     int q_off, q_tot;     // int8 modes: blocks [q_off, q_off + KB) of q_tot
     int N, CB, CG, Hp, Wp, KB, S, sh, sw, OH, OW, M, y_off, y_tot, act;
@@ -300,7 +301,7 @@ __device__ __forceinline__ void i8_tile(const I8Args& a, const int u, const int 
                     float q;
                     {
 #pragma clang fp contract(off)
-                        q = rintf(o[v] * a.yrcp);
+                        q = a.ydiv > 0.f ? rintf(o[v] / a.ydiv) : rintf(o[v] * a.yrcp);
                     }
                     q = q > (float)kQMax ? (float)kQMax : (q < -(float)kQMax ? -(float)kQMax : q);
                     packed |= ((unsigned)(int)q & 0xffu) << (8 * v);
@@ -769,7 +770,7 @@ hipError_t group_by_tile(const ConvConfig& c, const I8GroupArgs& ga, int wgs, hi
 I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, const int8_t* w,
                     const float* wscale, float xscale, const float* bias, const float* res, float* y,
                     int* acc, int8_t* yq, float yscale, int qph, int qpw, int xph, int xpw,
-                    int q_off = -1, int q_tot = -1) {
+                    int q_off = -1, int q_tot = -1, bool ydivide = false) {
     I8Args a;
     a.x = x;
     a.w = w;
@@ -781,6 +782,7 @@ I8Args make_i8_args(const ConvShape& s, const ConvConfig& c, const int8_t* x, co
     a.acc = acc;
     a.yq = yq;
     a.yrcp = yq ? 1.0f / yscale : 0.f;
+    a.ydiv = yq && ydivide ? yscale : 0.f;
     a.qph = qph;
     a.qpw = qpw;
     // the int8 output takes the view of s when it is the only output; beside
@@ -897,7 +899,7 @@ hipError_t launch_conv_int8_m(const I8Member& m, const ConvConfig& c, hipStream_
     if (!int8_config_valid(m.s, c) || m.xph < m.s.ph || m.xpw < m.s.pw || (!m.y && !m.yq))
         return hipErrorInvalidValue;
     const I8Args a = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
-                                  m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot);
+                                  m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot, m.ydivide);
     if (m.yq) return m.y ? by_tile<kOutBoth>(c, a, st) : by_tile<kOutI8>(c, a, st);
     return by_tile<kOutF32>(c, a, st);
 }
@@ -952,7 +954,7 @@ hipError_t launch_conv_int8_group(const I8Member* mem, int n, const ConvConfig& 
         const I8Member& m = mem[order[j]];
         if ((!m.y && !m.yq) || m.xph < m.s.ph || m.xpw < m.s.pw) return hipErrorInvalidValue;
         ga.a[j] = make_i8_args(m.s, c, m.x, m.w, m.wscale, m.xscale, m.bias, m.res, m.y, nullptr, m.yq,
-                               m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot);
+                               m.yscale, m.qph, m.qpw, m.xph, m.xpw, m.q_off, m.q_tot, m.ydivide);
         ga.cnt[j] = ga.a[j].ntiles;
         total_wgs += (long)cdiv(ga.cnt[j], conv_detail::kXcds) * conv_detail::kXcds;
         if (total_wgs >= (1L << 30)) return hipErrorInvalidValue;

@@ -224,6 +224,9 @@ struct I8Member {
     // yq's view in blocks: [q_off, q_off + KB) of q_tot (-1: the view of s
     // when y is null, else the whole [N][KB] tensor)
     int q_off, q_tot;
+    // requantize by division by yscale (the quantization pass's arithmetic)
+    // instead of by its float32 reciprocal
+    bool ydivide = false;
 };
 // Integer dense layer: xq int8 [N][INp] (INp = dense_i8_row_bytes(IN), rows
 // zero-padded), wq int8 [OUT][INp] with per-row scales, exact int32 dot
@@ -385,6 +388,10 @@ hipError_t launch_avgpool(const PoolShape& s, const float* x, float* y, hipStrea
 // int8 copy q (the same float32 values quantized).
 hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y, const PoolQ& q,
                          hipStream_t st);
+// Max pooling of int8 NCHW16c x8 [N][ceil(C/16)][H][W][16] (no halo) into the
+// int8 copy q (q.scale unused): quantization by division is monotone, so the
+// max of values quantized with the copy's scale is the quantized max.
+hipError_t launch_maxpool_i8(const PoolShape& s, const int8_t* x8, const PoolQ& q, hipStream_t st);
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st);
 // The global average pool on NCHW16c (C a multiple of 16) writing the means
 // y (may be null) and/or their int8 rows yq [N][C], quantized by division.

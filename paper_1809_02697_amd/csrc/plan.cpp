@@ -99,6 +99,8 @@ struct Step {
     // the slice of copy q_out this step writes, in blocks ([q_off8, q_off8 +
     // its blocks) of q_tot8), when it is one part of a concatenation's copy
     int q_off8 = -1, q_tot8 = -1;
+    // ST_MAXPOOL with NEO_PLAN_INT8: pools copy p8, its conv's int8 output
+    int p8 = -1;
     // ST_DENSE with NEO_PLAN_INT8 over many images: run as the 1x1 integer
     // conv cs (its filter packed in the conv's order, configuration c8)
     bool d_conv = false;
@@ -133,6 +135,11 @@ struct I8Copy {
     // im2col from the plain NCHW value src, whose blocked copy (val) nothing
     // else reads: the layout transform producing val is dropped
     int src = -1;
+    // a max pool's input written in int8 by its conv (no halo) for an int8
+    // max pool: requantized by division, with the pool's copy's scale
+    // (copy pool_copy); set at calibration
+    bool divide = false;
+    int pool_copy = -1;
 };
 
 struct Xform {
@@ -827,7 +834,7 @@ void group_ready_convs(neo_plan* P) {
         for (int j : ready) {
             if (S[j].kind == ST_CONV && (S[j].i8 || conv_group_eligible(S[j].cs)))
                 convs.push_back(j);
-            else if (pools_ride && (S[j].kind == ST_MAXPOOL || S[j].kind == ST_AVGPOOL))
+            else if (pools_ride && (S[j].kind == ST_MAXPOOL || S[j].kind == ST_AVGPOOL) && S[j].p8 < 0)
                 pools.push_back(j);
             else
                 out.push_back(S[j]);
@@ -1274,6 +1281,46 @@ void drop_im2col_transforms(neo_plan* P) {
     }
 }
 
+// NEO_PLAN_INT8: a max pool that writes its output's int8 copy (int8 only)
+// from a conv output nothing else reads pools that conv's output in int8
+// instead: the conv requantizes by division with the pool copy's scale (no
+// float32 output) and the pool takes byte maxima -- quantization by division
+// is monotone, so these are the quantized maxima, the same bits.  Taken
+// where the conv's float32 output is at least 16 MiB (measured: at batch 32
+// the pool reads a quarter of the bytes and the conv writes a quarter; on
+// batch-1 maps the dividing epilogue and the extra launch shape cost more
+// than the bytes saved).
+void int8_pool_inputs(neo_plan* P) {
+    const int ns = (int)P->steps.size();
+    for (int pi = 0; pi < ns; ++pi) {
+        Step& p = P->steps[pi];
+        if (p.kind != ST_MAXPOOL || p.q_out < 0 || p.f32_needed || p.q_off8 >= 0) continue;
+        const int v = p.in;
+        const Val& vv = P->vals[v];
+        if (v == P->out_val || vv.view || vv.alias_of >= 0 || vv.layout != 16 ||
+            (long)vv.N * cdiv(vv.C, 16) * 16 * vv.H * vv.W * 4 < (16L << 20))
+            continue;
+        int ci = -1, readers = 0;
+        for (int i = 0; i < ns; ++i) {
+            const Step& t = P->steps[i];
+            if (t.out == v && t.kind == ST_CONV && t.i8 && t.q_out < 0) ci = i;
+            if (t.in == v || t.res == v || t.out2 == v) ++readers;
+        }
+        for (const Val& o : P->vals)
+            if (o.alias_of == v) ++readers;
+        if (ci < 0 || readers != 1) continue;
+        I8Copy q{v, 0, 0, P->i8_bytes};
+        q.divide = true;
+        q.pool_copy = p.q_out;
+        q.writer = ci;
+        P->i8_bytes += ((long)int8_act_bytes(vv.N, vv.C, vv.H, vv.W, 0, 0) + 255) / 256 * 256;
+        P->i8_copies.push_back(q);
+        P->steps[ci].q_out = (int)P->i8_copies.size() - 1;
+        P->steps[ci].f32_needed = false;
+        p.p8 = P->steps[ci].q_out;
+    }
+}
+
 // NEO_PLAN_INT8 with NEO_PLAN_GROUP: grouping reorders the steps, so the
 // quantization pass of a copy that no conv writes moves to the copy's first
 // reader in the new order (a group runs its members' passes before its
@@ -1422,6 +1469,7 @@ std::string describe(const neo_plan* P) {
             o << ",\"int8\":{\"writes_copy\":" << s.q_out << ",\"writes_f32\":"
               << (s.f32_needed ? "true" : "false");
             if (s.q_off8 >= 0) o << ",\"writes_slice\":[" << s.q_off8 << "," << s.q_tot8 << "]";
+            if (s.p8 >= 0) o << ",\"reads_int8\":" << s.p8;
             o << "}";
         }
         if (s.kind == ST_TRANSFORM) o << ",\"src_block\":" << s.src_block << ",\"dst_block\":" << s.dst_block;
@@ -1688,6 +1736,7 @@ int neo_plan_create(const neo_node* nodes, int n_nodes, int N, int C, int H, int
         if (rc == NEO_OK && (flags & NEO_PLAN_INT8)) {
             plan_int8_copies(P);
             drop_im2col_transforms(P);
+            int8_pool_inputs(P);
             if (!(flags & NEO_PLAN_HOST_ONLY))
                 for (Step& st : P->steps)
                     if ((st.kind == ST_CONV || (st.kind == ST_DENSE && st.d_conv)) && st.i8) {
@@ -1873,6 +1922,7 @@ static I8Member i8_member(const neo_plan* P, const Step& s, const float* x_nchw,
     m.xpw = qc.pw;
     m.q_off = qo ? s.q_off8 : -1;
     m.q_tot = qo ? s.q_tot8 : -1;
+    m.ydivide = qo && qo->divide;
     return m;
 }
 
@@ -2007,8 +2057,11 @@ static int enqueue_step(neo_plan* P, const Step& s, const float* x_nchw, float* 
                     q.qpw = qo.pw;
                     q.q_off = s.q_off8 >= 0 ? s.q_off8 : 0;
                     q.q_tot = s.q_tot8 > 0 ? s.q_tot8 : 0;
-                    e = launch_pool_q(s.ps, s.kind == ST_MAXPOOL, val_ptr(P, s.in, x_nchw, y_out),
-                                      s.f32_needed ? val_ptr(P, s.out, x_nchw, y_out) : nullptr, q, st);
+                    if (s.p8 >= 0)  // from its conv's int8 output
+                        e = launch_maxpool_i8(s.ps, P->d_i8 + P->i8_copies[s.p8].xq_off, q, st);
+                    else
+                        e = launch_pool_q(s.ps, s.kind == ST_MAXPOOL, val_ptr(P, s.in, x_nchw, y_out),
+                                          s.f32_needed ? val_ptr(P, s.out, x_nchw, y_out) : nullptr, q, st);
                 } else if (s.kind == ST_MAXPOOL) {
                     e = launch_maxpool(s.ps, val_ptr(P, s.in, x_nchw, y_out), val_ptr(P, s.out, x_nchw, y_out), st);
                 } else {
@@ -2539,9 +2592,24 @@ int neo_plan_calibrate_int8(neo_plan* P, const float* x_nchw, float* y_out, neo_
             rc = enqueue_step(P, s, x_nchw, y_out, st);
             P->i8_f32_out = false;
             if (rc != NEO_OK) return rc;
-            if ((rc = scale_of(val_ptr(P, s.out, x_nchw, y_out), elems(s.out),
-                               &P->i8_copies[s.q_out].xscale)) != NEO_OK)
+            I8Copy& qo = P->i8_copies[s.q_out];
+            if (qo.pool_copy >= 0) {
+                // a max pool's int8 input: the pool's float32 output gives
+                // the scale of both copies
+                for (const Step& pl : P->steps)
+                    if (pl.p8 == s.q_out) {
+                        P->i8_f32_out = true;
+                        rc = enqueue_step(P, pl, x_nchw, y_out, st);
+                        P->i8_f32_out = false;
+                        if (rc != NEO_OK) return rc;
+                        if ((rc = scale_of(val_ptr(P, pl.out, x_nchw, y_out), elems(pl.out),
+                                           &P->i8_copies[qo.pool_copy].xscale)) != NEO_OK)
+                            return rc;
+                        qo.xscale = P->i8_copies[qo.pool_copy].xscale;
+                    }
+            } else if ((rc = scale_of(val_ptr(P, s.out, x_nchw, y_out), elems(s.out), &qo.xscale)) != NEO_OK) {
                 return rc;
+            }
         }
         return enqueue_step(P, s, x_nchw, y_out, st);
     };

@@ -149,6 +149,57 @@ hipError_t launch_pool_q(const PoolShape& s, bool max, const float* x, float* y,
     return max ? launch_pool_q_t<true>(s, x, y, q, st) : launch_pool_q_t<false>(s, x, y, q, st);
 }
 
+// One thread per output pixel block: the byte-wise max over the window's
+// in-image taps (a window always holds one), one 16-byte store.
+__global__ __launch_bounds__(256) void maxpool_i8_blk(const int8_t* __restrict__ x, PoolShape s, int CB, PoolQ q) {
+    const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (long)s.N * CB * s.OH * s.OW) return;
+    const int ow = (int)(t % s.OW);
+    long r_ = t / s.OW;
+    const int oh = (int)(r_ % s.OH);
+    r_ /= s.OH;
+    const int cb = (int)(r_ % CB);
+    const long n = r_ / CB;
+    const int8_t* xb = x + (n * CB + cb) * s.H * s.W * 16;
+    const int ih0 = oh * s.sh - s.ph, iw0 = ow * s.sw - s.pw;
+    int m[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) m[i] = -128;
+    for (int r = 0; r < s.R; ++r) {
+        const int ih = ih0 + r;
+        if ((unsigned)ih >= (unsigned)s.H) continue;
+        for (int c = 0; c < s.S; ++c) {
+            const int iw = iw0 + c;
+            if ((unsigned)iw >= (unsigned)s.W) continue;
+            union {
+                int4 v;
+                int8_t b[16];
+            } u;
+            u.v = *reinterpret_cast<const int4*>(xb + ((long)ih * s.W + iw) * 16);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) m[i] = u.b[i] > m[i] ? u.b[i] : m[i];
+        }
+    }
+    union {
+        int4 v;
+        int8_t b[16];
+    } o;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o.b[i] = (int8_t)m[i];
+    const int qtot = q.q_tot > 0 ? q.q_tot : CB;
+    const long at = (((n * qtot + q.q_off + cb) * (s.OH + 2 * q.qph) + oh + q.qph) * (long)(s.OW + 2 * q.qpw) + ow +
+                     q.qpw) * 16;
+    *reinterpret_cast<int4*>(q.yq + at) = o.v;
+}
+
+hipError_t launch_maxpool_i8(const PoolShape& s, const int8_t* x8, const PoolQ& q, hipStream_t st) {
+    const int CB = cdiv(s.C, 16);
+    const long total = (long)s.N * CB * s.OH * s.OW;
+    if (s.xb != 16 || !x8 || !q.yq || total <= 0 || s.ph >= s.R || s.pw >= s.S) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(maxpool_i8_blk, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x8, s, CB, q);
+    return hipGetLastError();
+}
+
 hipError_t launch_gap(const float* x, int xb, int N, int C, int H, int W, float* y, hipStream_t st) {
     if (!pow2_block(xb)) return hipErrorInvalidValue;
     const int XB = cdiv(C, xb), G16 = cdiv(XB * xb, 16);

@@ -46,6 +46,8 @@ def test_host_plan_and_flags():
     assert sum(x["writes_copy"] >= 0 and x["writes_f32"] for x in q) == 12
     pool = [s for s in d["steps"] if s["kind"] == "maxpool"][0]
     assert pool["int8"]["writes_copy"] >= 0 and not pool["int8"]["writes_f32"]
+    # (the stem's 3.2 MB output is pooled in float32: below 16 MiB)
+    assert "reads_int8" not in pool["int8"]
     L = neo.lib()
     FAKE = ctypes.c_void_p(1 << 20)
     assert L.neo_plan_calibrate_int8(p.handle, FAKE, FAKE, None) == -7   # host-only: NEO_ERR_STATE
@@ -214,6 +216,43 @@ def test_im2col_stem_against_the_oracle(gpu, C, R, S, stride, pad, H, W, N, i2c)
     (_, c), = conv_steps(p.describe())
     p.destroy()
     assert bool(c["int8"].get("im2col", False)) == i2c
+    ref, ref_scales = oq.run_graph_int8(g)
+    assert np.array_equal(np.array([scales[i] for i in int8_ids(g)], np.float32), ref_scales)
+    np.testing.assert_array_equal(y, ref.reshape(y.shape))
+    np.testing.assert_array_equal(y_cal, y)
+
+
+def pooled_stem_graph(N=8, H=128, W=128):
+    """A 3x3 stem (32 channels, 16.8 MB of float32 output at batch 8), a max
+    pool and a 1x1 conv reading the pool: the stem's output is pooled in
+    int8."""
+    b = wl._Builder("pooled_stem", (N, 3, H, W), np.random.Generator(np.random.PCG64(12)))
+    x = b.conv(0, 32, 3, pad=1, name="stem")
+    x = b.pool("maxpool", x, 3, 2, 1, name="pool")
+    b.output(b.conv(x, 16, 1, name="c1"))
+    return b.finish(wl._normal_input((N, 3, H, W)))
+
+
+def test_host_int8_pool_input():
+    p = neo.Plan(pooled_stem_graph(), flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)
+    d = p.describe()
+    p.destroy()
+    (_, stem), _ = conv_steps(d)
+    pool = [s for s in d["steps"] if s["kind"] == "maxpool"][0]
+    assert pool["int8"]["reads_int8"] == stem["int8"]["writes_copy"] >= 0 and not stem["int8"]["writes_f32"]
+    p = neo.Plan(pooled_stem_graph(N=7), flags=neo.PLAN_HOST_ONLY | neo.PLAN_INT8)   # 14.7 MB: float32
+    assert "reads_int8" not in [s for s in p.describe()["steps"] if s["kind"] == "maxpool"][0]["int8"]
+    p.destroy()
+
+
+@pytest.mark.gpu
+def test_int8_pool_input_against_the_oracle(gpu):
+    """The stem requantized by division with the pool's scale, the max pool
+    over bytes: the oracle's bits (its pool quantizes the float32 maxima)."""
+    print("\n[int8 pool] pooled stem N=8", flush=True)
+    g = pooled_stem_graph()
+    y_cal, y, scales, p = run_int8_plan(gpu, g)
+    p.destroy()
     ref, ref_scales = oq.run_graph_int8(g)
     assert np.array_equal(np.array([scales[i] for i in int8_ids(g)], np.float32), ref_scales)
     np.testing.assert_array_equal(y, ref.reshape(y.shape))
