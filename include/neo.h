@@ -494,7 +494,11 @@ enum neo_plan_flags {
      * integer conv over its input's im2col rows (channel (r*S + s)*C + c;
      * the same integer sums): its pass writes those rows, from the NCHW
      * network input directly when nothing else reads the input's blocked
-     * copy (that layout transform is then not run).  Dense layers run in int8 too: weights quantized
+     * copy (that layout transform is then not run).  A max pool writing
+     * its output's copy from a conv output of at least 16 MiB (float32)
+     * that nothing else reads pools in int8: the conv requantizes by
+     * division with the pool copy's scale, the pool takes byte maxima (the
+     * same bits: that quantization is monotone).  Dense layers run in int8 too: weights quantized
      * per output row, the flattened input one int8 row per image (written by
      * the producing dense layer, requantized, or by the global average pool
      * or the exit of the blocked layout, quantized by division, or by a
